@@ -1,0 +1,289 @@
+"""ctypes wrapper of the plain CPU oracle (``ocref.cpp``).
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, by the package smoke check
+and by the bench's CPU-baseline leg, never by the product path.  It shares
+no code with the HIP library.  Inputs are numpy arrays; floating-point inputs
+are widened to float64 and every result is float64 (integers stay exact).
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ocref.cpp")
+_LIB = os.path.join(_HERE, "libocref.so")
+
+OK, ERR_ARG, ERR_RANGE = 0, 1, 2
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with the host compiler (g++), never hipcc."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(
+            ["g++", "-O2", "-std=c++17", "-fopenmp", "-shared", "-fPIC", _SRC, "-o", tmp]
+        )
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build()
+        L = C.CDLL(_LIB)
+        p, i32, i64 = C.c_void_p, C.c_int32, C.c_int64
+        sig = {
+            "ocref_build": [p, p, p, i32, i32, i32, C.POINTER(p)],
+            "ocref_level_size": [p, i32, C.POINTER(i64), C.POINTER(i64)],
+            "ocref_level": [p, i32, p, p, p],
+            "ocref_signal": [p, p],
+            "ocref_neighbors": [p, i32, i32, i32, p],
+            "ocref_conv_fwd": [p, i64, i32, p, i64, i32, p, i32, p, i64, p],
+            "ocref_conv_bwd_data": [p, i64, i32, p, i32, p, i32, i64, p, p],
+            "ocref_conv_bwd_weight": [p, i64, i32, p, i64, i32, p, i32, p, i64, p],
+            "ocref_renew": [p, i64, p, i32, p],
+            "ocref_renew_bwd": [p, i64, p, i32, i64, p],
+            "ocref_pool_fwd": [p, i64, p, i64, i32, p, p],
+            "ocref_pool_bwd": [p, i64, p, p, i32, i64, p],
+            "ocref_unpool_fwd": [p, i64, p, p, i32, i64, p],
+            "ocref_unpool_bwd": [p, i64, p, p, i32, p],
+            "ocref_relu_fwd": [p, i64, p],
+            "ocref_relu_bwd": [p, p, i64, p],
+        }
+        for name, args in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = C.c_int
+        L.ocref_free.argtypes = [p]
+        L.ocref_free.restype = None
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code):
+        super().__init__(f"oracle status {code}")
+        self.code = code
+
+
+def _check(rc):
+    if rc != OK:
+        raise OracleError(rc)
+
+
+class Octree:
+    """Super-octree built by breadth-first subdivision (Sec. 3.1)."""
+
+    def __init__(self, points, normals, offsets, depth, full_depth=2):
+        points = np.ascontiguousarray(points, dtype=np.float32).reshape(-1, 3)
+        normals = np.ascontiguousarray(normals, dtype=np.float32).reshape(-1, 3)
+        offsets = _i32(offsets)
+        self.batch = len(offsets) - 1
+        self.depth = depth
+        self.full_depth = full_depth
+        h = C.c_void_p()
+        _check(lib().ocref_build(_ptr(points), _ptr(normals), _ptr(offsets), self.batch, depth,
+                                 full_depth, C.byref(h)))
+        self._h = h
+        self.levels = []
+        for l in range(depth + 1):
+            n, m = C.c_int64(), C.c_int64()
+            _check(lib().ocref_level_size(h, l, C.byref(n), C.byref(m)))
+            keys = np.zeros(n.value, np.uint32)
+            labels = np.zeros(n.value, np.int32)
+            rows = np.zeros(m.value, np.int32)
+            _check(lib().ocref_level(h, l, _ptr(keys), _ptr(labels), _ptr(rows)))
+            self.levels.append({"keys": keys, "labels": labels, "rows": rows})
+        sig = np.zeros((len(self.levels[depth]["keys"]), 3), np.float32)
+        _check(lib().ocref_signal(h, _ptr(sig)))
+        self.signal = sig
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.ocref_free(h)
+            self._h = None
+
+    def num(self, l):
+        return len(self.levels[l]["keys"])
+
+    def nonempty(self, l):
+        return len(self.levels[l]["rows"])
+
+    def keys(self, l):
+        return self.levels[l]["keys"]
+
+    def labels(self, l):
+        return self.levels[l]["labels"]
+
+    def rows(self, l):
+        return self.levels[l]["rows"]
+
+    def neighbors(self, l, K=3, stride=1):
+        n = self.num(l) if stride == 1 else self.nonempty(l - 1)
+        nb = np.zeros((n, K ** 3), np.int32)
+        _check(lib().ocref_neighbors(self._h, l, K, stride, _ptr(nb)))
+        return nb
+
+
+def conv_fwd(nb, x, w, rows=None):
+    """Y = im2col(X; nb) . W, w [K^3][cin][cout]; rows: optional subset of outputs."""
+    nb = _i32(nb)
+    x = _f64(x)
+    w = _f64(w)
+    K3, cin, cout = w.shape
+    assert nb.shape[1] == K3 and x.shape[1] == cin
+    n_out = nb.shape[0]
+    if rows is not None:
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        y = np.zeros((len(rows), cout))
+        _check(lib().ocref_conv_fwd(_ptr(nb), n_out, K3, _ptr(x), x.shape[0], cin, _ptr(w), cout,
+                                    _ptr(rows), len(rows), _ptr(y)))
+    else:
+        y = np.zeros((n_out, cout))
+        _check(lib().ocref_conv_fwd(_ptr(nb), n_out, K3, _ptr(x), x.shape[0], cin, _ptr(w), cout,
+                                    None, 0, _ptr(y)))
+    return y
+
+
+def conv_bwd_data(nb, dy, w, n_in, want=None):
+    """dX = col2im(dY . W^T; nb); want: optional bool mask of input rows to compute."""
+    nb = _i32(nb)
+    dy = _f64(dy)
+    w = _f64(w)
+    K3, cin, cout = w.shape
+    dx = np.zeros((n_in, cin))
+    wm = None if want is None else np.ascontiguousarray(want, dtype=np.uint8)
+    _check(lib().ocref_conv_bwd_data(_ptr(nb), nb.shape[0], K3, _ptr(dy), cout, _ptr(w), cin, n_in,
+                                     _ptr(wm), _ptr(dx)))
+    return dx
+
+
+def conv_bwd_weight(nb, x, dy, K3, entries=None):
+    """dW = col^T . dY, [K^3][cin][cout]; entries: optional flat indices to compute."""
+    nb = _i32(nb)
+    x = _f64(x)
+    dy = _f64(dy)
+    cin, cout = x.shape[1], dy.shape[1]
+    if entries is not None:
+        entries = np.ascontiguousarray(entries, dtype=np.int64)
+        dw = np.zeros(len(entries))
+        _check(lib().ocref_conv_bwd_weight(_ptr(nb), nb.shape[0], K3, _ptr(x), x.shape[0], cin,
+                                           _ptr(dy), cout, _ptr(entries), len(entries), _ptr(dw)))
+        return dw
+    dw = np.zeros((K3, cin, cout))
+    _check(lib().ocref_conv_bwd_weight(_ptr(nb), nb.shape[0], K3, _ptr(x), x.shape[0], cin,
+                                       _ptr(dy), cout, None, 0, _ptr(dw)))
+    return dw
+
+
+def renew(labels_lm1, yhat):
+    labels_lm1 = _i32(labels_lm1)
+    yhat = _f64(yhat)
+    y = np.zeros((len(labels_lm1), yhat.shape[1]))
+    _check(lib().ocref_renew(_ptr(labels_lm1), len(labels_lm1), _ptr(yhat), yhat.shape[1], _ptr(y)))
+    return y
+
+
+def renew_bwd(labels_lm1, dy, m):
+    labels_lm1 = _i32(labels_lm1)
+    dy = _f64(dy)
+    dyhat = np.zeros((m, dy.shape[1]))
+    _check(lib().ocref_renew_bwd(_ptr(labels_lm1), len(labels_lm1), _ptr(dy), dy.shape[1], m,
+                                 _ptr(dyhat)))
+    return dyhat
+
+
+def conv_s2_fwd(tree: Octree, l, x, w):
+    """Stride-2 conv (Sec. 3.2): conv at the first sibling of each group, renewed into T_{l-1}."""
+    K = round(w.shape[0] ** (1 / 3))
+    nb = tree.neighbors(l, K, stride=2)
+    return renew(tree.labels(l - 1), conv_fwd(nb, x, w))
+
+
+def conv_s2_bwd(tree: Octree, l, x, w, dy):
+    K = round(w.shape[0] ** (1 / 3))
+    nb = tree.neighbors(l, K, stride=2)
+    dyhat = renew_bwd(tree.labels(l - 1), dy, nb.shape[0])
+    dx = conv_bwd_data(nb, dyhat, w, x.shape[0])
+    dw = conv_bwd_weight(nb, x, dyhat, w.shape[0])
+    return dx, dw
+
+
+def pool_fwd(labels_lm1, x):
+    labels_lm1 = _i32(labels_lm1)
+    x = _f64(x)
+    c = x.shape[1]
+    y = np.zeros((len(labels_lm1), c))
+    sw = np.zeros((x.shape[0] // 8, c), np.uint8)
+    _check(lib().ocref_pool_fwd(_ptr(labels_lm1), len(labels_lm1), _ptr(x), x.shape[0], c, _ptr(y),
+                                _ptr(sw)))
+    return y, sw
+
+
+def pool_bwd(labels_lm1, dy, sw, n_l):
+    labels_lm1 = _i32(labels_lm1)
+    dy = _f64(dy)
+    sw = np.ascontiguousarray(sw, dtype=np.uint8)
+    c = dy.shape[1]
+    dx = np.zeros((n_l, c))
+    _check(lib().ocref_pool_bwd(_ptr(labels_lm1), len(labels_lm1), _ptr(dy), _ptr(sw), c, n_l,
+                                _ptr(dx)))
+    return dx
+
+
+def unpool_fwd(labels_lm1, x, sw, n_l):
+    labels_lm1 = _i32(labels_lm1)
+    x = _f64(x)
+    sw = np.ascontiguousarray(sw, dtype=np.uint8)
+    c = x.shape[1]
+    y = np.zeros((n_l, c))
+    _check(lib().ocref_unpool_fwd(_ptr(labels_lm1), len(labels_lm1), _ptr(x), _ptr(sw), c, n_l,
+                                  _ptr(y)))
+    return y
+
+
+def unpool_bwd(labels_lm1, dy, sw):
+    labels_lm1 = _i32(labels_lm1)
+    dy = _f64(dy)
+    sw = np.ascontiguousarray(sw, dtype=np.uint8)
+    c = dy.shape[1]
+    dx = np.zeros((len(labels_lm1), c))
+    _check(lib().ocref_unpool_bwd(_ptr(labels_lm1), len(labels_lm1), _ptr(dy), _ptr(sw), c,
+                                  _ptr(dx)))
+    return dx
+
+
+def relu_fwd(x):
+    x = _f64(x)
+    y = np.zeros_like(x)
+    _check(lib().ocref_relu_fwd(_ptr(x), x.size, _ptr(y)))
+    return y
+
+
+def relu_bwd(x, dy):
+    x = _f64(x)
+    dy = _f64(dy)
+    dx = np.zeros_like(x)
+    _check(lib().ocref_relu_bwd(_ptr(x), _ptr(dy), x.size, _ptr(dx)))
+    return dx
