@@ -1,0 +1,208 @@
+/*
+ * oc.h -- C ABI of the MI355X (gfx950) octree-CNN hot path.
+ *
+ * Implements the GPU side of O-CNN (Wang et al., "O-CNN: Octree-based
+ * Convolutional Neural Networks for 3D Shape Analysis", arXiv 1712.01537):
+ * building the per-depth packed super-octree of a batch of oriented point
+ * clouds (Sec. 3.1), and convolution, max-pooling and max-unpooling restricted
+ * to the octants of that octree (Sec. 3.2).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Depth l has N_l octants (every child of a non-empty depth-(l-1) octant,
+ *    empty or not; N_0 = batch) of which M_l are non-empty.  N_l = 8 M_{l-1}.
+ *  - Feature maps are row-major [N_l][C] (one row per octant, in key order,
+ *    channels contiguous), fp32 unless a dtype argument says otherwise.
+ *  - Convolution weights are [K^3][Cin][Cout], fp32 (or bf16 for OC_BF16),
+ *    tap index k = ((dx+r)K + (dy+r))K + (dz+r) with r = (K-1)/2 and
+ *    (dx,dy,dz) the neighbour's offset; x varies slowest, matching the bit
+ *    order of the shuffle key.  The operation is a cross-correlation with no
+ *    bias; a neighbour that is not in the octree reads as zero (Sec. 3.2,
+ *    unrolled convolution).
+ *  - Every pointer named "dev" is device memory of the current HIP device;
+ *    "host" pointers are host memory.  The caller owns every buffer it passes;
+ *    the library never frees them.  Buffers must not alias unless stated.
+ *  - Every call enqueues work on `stream` and returns without waiting, except
+ *    oc_build, which waits exactly once (to read the per-depth counts).
+ *  - Argument errors are detected before any work is enqueued and returned
+ *    as a status; nothing is written in that case.  Asynchronous device
+ *    faults surface as OC_ERR_DEVICE from a later call.  oc_last_error()
+ *    gives a message for the calling thread's last failure.  No C++
+ *    exception crosses this interface.
+ *  - An octree is immutable after oc_build; calls on different streams may
+ *    use it concurrently.
+ */
+#ifndef OC_H_
+#define OC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OC_OK = 0,
+  OC_ERR_ARG = 1,          /* invalid argument, null pointer, shape mismatch */
+  OC_ERR_RANGE = 2,        /* a point outside [0,1]^3 or NaN */
+  OC_ERR_NOMEM = 3,        /* the allocator returned NULL */
+  OC_ERR_DEVICE = 4,       /* a HIP runtime error */
+  OC_ERR_UNSUPPORTED = 5   /* valid but not implemented (e.g. kernel size) */
+} oc_status;
+
+typedef enum { OC_F32 = 0, OC_BF16 = 1 } oc_dtype;
+
+/* oc_conv_fwd / oc_conv_bwd flag: y = max(0, conv(x)); the backward then
+ * masks dy with [y > 0] (Sec. 4, ReLU after each convolution). */
+#define OC_FUSE_RELU 1
+
+/* Device memory provider for the octree's arrays and oc_build's temporaries.
+ * alloc returns device memory usable in stream order on `stream` (NULL on
+ * failure); free releases it in stream order.  Pass NULL to oc_build to use
+ * hipMalloc/hipFree. */
+typedef struct oc_allocator {
+  void* (*alloc)(void* ctx, size_t bytes, hipStream_t stream);
+  void (*free)(void* ctx, void* ptr, hipStream_t stream);
+  void* ctx;
+} oc_allocator;
+
+typedef struct oc_octree oc_octree; /* opaque, immutable after oc_build */
+
+/* Per-depth arrays of a built octree (Sec. 3.1), all dev, owned by the octree.
+ *   keys          [N_l]  shuffle key x1y1z1...xlylzl of each octant with the
+ *                        shape index in bits 24..31 (super-octree key,
+ *                        Sec. 3.1 "Mini-batch"); ascending.
+ *   labels        [N_l]  0 for an empty octant, p for the p-th non-empty one
+ *                        of the whole batch (1-based, Sec. 3.1 "Label").
+ *   rows_of_label [M_l]  inverse of labels: the row holding label p at p-1.
+ *   nbr           [M_{l-1}][27] (NULL at l = 0): for sibling group g (the
+ *                        children of the g-th non-empty octant of depth l-1),
+ *                        and parent offset o = (ox+1)*9 + (oy+1)*3 + (oz+1)
+ *                        with ox,oy,oz in {-1,0,1}, the first-child row
+ *                        8(label-1) at depth l of the depth-(l-1) octant at
+ *                        that offset from the group's parent, or -1 if that
+ *                        octant is outside the cube, empty or absent.  Every
+ *                        neighbour of every octant of the group within
+ *                        offset +-2 per axis is reachable from these 27
+ *                        entries (the shared neighbourhood of the eight
+ *                        siblings, Sec. 3.2 and Fig. 4). */
+typedef struct oc_level {
+  int32_t depth;
+  int64_t num_octants;  /* N_l */
+  int64_t num_nonempty; /* M_l */
+  const uint32_t* keys;
+  const int32_t* labels;
+  const int32_t* rows_of_label;
+  const int32_t* nbr;
+} oc_level;
+
+/* Build the super-octree of `batch` shapes (Sec. 3.1).
+ *   points       dev f32 [P][3], every coordinate in [0,1] (else
+ *                OC_ERR_RANGE); shape b owns points
+ *                shape_offsets[b] .. shape_offsets[b+1]-1.
+ *   normals      dev f32 [P][3], averaged per non-empty leaf into the input
+ *                signal (Sec. 3.1 "Input signal").
+ *   shape_offsets host i32 [batch+1], non-decreasing, shape_offsets[0] = 0.
+ *   batch        1..256 (8-bit shape index in the key).
+ *   depth        1..8 (3*depth key bits must fit below the shape byte).
+ *   full_depth   0..depth: octants shallower than full_depth are forced
+ *                non-empty, so every octant of depth full_depth exists
+ *                (Sec. 4 uses 2).
+ *   alloc        NULL for hipMalloc/hipFree.
+ * Quantisation: cell = min(floor(p * 2^depth), 2^depth - 1) per axis, in fp32.
+ * On success *out owns its arrays until oc_octree_free.  Waits once on
+ * `stream`. */
+oc_status oc_build(const float* points, const float* normals, const int32_t* shape_offsets,
+                   int32_t batch, int32_t depth, int32_t full_depth, const oc_allocator* alloc,
+                   hipStream_t stream, oc_octree** out);
+
+/* Sizes and device arrays of depth l (0..depth). */
+oc_status oc_octree_level(const oc_octree* tree, int32_t l, oc_level* out);
+
+/* Tree depth, full depth and batch size. */
+oc_status oc_octree_info(const oc_octree* tree, int32_t* depth, int32_t* full_depth,
+                         int32_t* batch);
+
+/* Input signal, dev f32 [N_depth][3]: mean normal of the points in each
+ * non-empty leaf, zero for empty leaves (Sec. 3.1 "Input signal"). */
+const float* oc_octree_signal(const oc_octree* tree);
+
+/* Release the octree's arrays (in stream order on the build stream). */
+void oc_octree_free(oc_octree* tree);
+
+/* Octree convolution forward (Sec. 3.2).
+ *   depth   input depth l (1..tree depth).
+ *   ksize   3 or 5 (stride 1); 3 (stride 2).
+ *   stride  1: output at all N_l octants of depth l.
+ *           2: output at depth l-1: the convolution is evaluated at the
+ *              first sibling of every group and written to the row of its
+ *              parent; rows of empty parents are zero (Sec. 3.2 stride-2
+ *              paragraphs, Fig. 2(d)).
+ *   dt      OC_F32: x, w fp32.  OC_BF16: x, w bf16 (round-to-nearest-even
+ *           values held as uint16); products accumulate in fp32.
+ *   x       dev [N_l][cin].      w  dev [K^3][cin][cout].
+ *   y       dev f32 [N_out][cout], N_out = N_l (stride 1) or N_{l-1}.
+ *   flags   0 or OC_FUSE_RELU.
+ * cin, cout in 1..1024. */
+oc_status oc_conv_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                      oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
+                      float* y, int32_t flags, hipStream_t stream);
+
+/* Bytes of device workspace oc_conv_bwd needs for these arguments. */
+size_t oc_conv_bwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                             oc_dtype dt, int32_t cin, int32_t cout);
+
+/* Octree convolution backward (Sec. 3.2; the transposed products of the
+ * forward).  Arguments as oc_conv_fwd, plus
+ *   y    dev f32 [N_out][cout], the forward output, read only when flags has
+ *        OC_FUSE_RELU (then dy is masked with [y > 0]); may be NULL otherwise.
+ *   dy   dev f32 [N_out][cout] upstream gradient.
+ *   dx   dev f32 [N_l][cin] or NULL: gradient w.r.t. x (overwritten).
+ *   dw   dev f32 [K^3][cin][cout] or NULL: gradient w.r.t. w (overwritten).
+ *   ws   dev workspace of at least oc_conv_bwd_workspace() bytes.
+ * Deterministic: no floating-point atomics; repeated calls give identical
+ * bits. */
+oc_status oc_conv_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                      oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
+                      const float* y, const float* dy, float* dx, float* dw, void* ws,
+                      size_t ws_bytes, int32_t flags, hipStream_t stream);
+
+/* 2x2x2 max-pooling from depth l to l-1 (Sec. 3.2 "Pooling", Fig. 5): for
+ * every row i of depth l-1 with label p > 0, y[i] = channel-wise max of the
+ * 8 rows 8(p-1)..8(p-1)+7 of depth l, sw[p-1][c] = the child index 0..7 of
+ * that maximum (the first one on ties); rows with label 0 get y = 0.
+ *   x  dev f32 [N_l][c];  y dev f32 [N_{l-1}][c];  sw dev u8 [M_{l-1}][c]. */
+oc_status oc_pool_fwd(const oc_octree* tree, int32_t depth, const float* x, int32_t c, float* y,
+                      uint8_t* sw, hipStream_t stream);
+
+/* Gradient of oc_pool_fwd: dx[8(p-1) + sw[p-1][c]][c] = dy[i][c] for the row
+ * i of label p at depth l-1; every other entry of dx is 0.
+ *   dy dev f32 [N_{l-1}][c];  sw as produced by oc_pool_fwd;
+ *   dx dev f32 [N_l][c]. */
+oc_status oc_pool_bwd(const oc_octree* tree, int32_t depth, const float* dy, const uint8_t* sw,
+                      int32_t c, float* dx, hipStream_t stream);
+
+/* 2x2x2 max-unpooling from depth l-1 to l (Sec. 3.2 "Unpooling", Fig. 5):
+ * y[8(p-1) + sw[p-1][c]][c] = x[i][c] for the row i of label p at depth
+ * l-1; every other entry of y is 0 (rows of empty parents have no children).
+ *   depth  target depth l.  x dev f32 [N_{l-1}][c];  y dev f32 [N_l][c]. */
+oc_status oc_unpool_fwd(const oc_octree* tree, int32_t depth, const float* x, const uint8_t* sw,
+                        int32_t c, float* y, hipStream_t stream);
+
+/* Gradient of oc_unpool_fwd: dx[i][c] = dy[8(p-1) + sw[p-1][c]][c] for the
+ * row i of label p > 0 at depth l-1, 0 for label 0.
+ *   dy dev f32 [N_l][c];  dx dev f32 [N_{l-1}][c]. */
+oc_status oc_unpool_bwd(const oc_octree* tree, int32_t depth, const float* dy, const uint8_t* sw,
+                        int32_t c, float* dx, hipStream_t stream);
+
+const char* oc_status_str(oc_status s);
+const char* oc_last_error(void); /* thread-local message of the last failure */
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OC_H_ */

@@ -1,0 +1,330 @@
+"""Python binding of liboc, the MI355X octree-CNN hot path (O-CNN, arXiv 1712.01537).
+
+Argument marshalling only: every step runs in the HIP kernels of ``liboc.so``
+(built from ``csrc/`` by ``build.py``).  torch provides device memory (the
+octree's arrays are carved from torch tensors through the allocator callback
+of ``oc_build``) and the stream every call is enqueued on (torch's current
+stream).  The functions carry the C ABI's names; see ``include/oc.h`` for the
+contract of each.
+
+If ``liboc.so`` is missing or cannot be loaded, every entry point raises
+:class:`OcError`; there is no other implementation to fall back to.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+__all__ = [
+    "OcError",
+    "Octree",
+    "lib_path",
+    "load",
+    "oc_build",
+    "oc_conv_fwd",
+    "oc_conv_bwd",
+    "oc_pool_fwd",
+    "oc_pool_bwd",
+    "oc_unpool_fwd",
+    "oc_unpool_bwd",
+    "OC_FUSE_RELU",
+    "EXPORTS",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+OC_FUSE_RELU = 1
+OC_F32, OC_BF16 = 0, 1
+STATUS = {0: "OC_OK", 1: "OC_ERR_ARG", 2: "OC_ERR_RANGE", 3: "OC_ERR_NOMEM", 4: "OC_ERR_DEVICE",
+          5: "OC_ERR_UNSUPPORTED"}
+
+# Every symbol include/oc.h declares.
+EXPORTS = (
+    "oc_build", "oc_octree_level", "oc_octree_info", "oc_octree_signal", "oc_octree_free",
+    "oc_conv_fwd", "oc_conv_bwd_workspace", "oc_conv_bwd", "oc_pool_fwd", "oc_pool_bwd",
+    "oc_unpool_fwd", "oc_unpool_bwd", "oc_status_str", "oc_last_error",
+)
+
+
+class OcError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+def lib_path() -> str:
+    return os.path.join(_HERE, "liboc.so")
+
+
+class _Level(C.Structure):
+    _fields_ = [
+        ("depth", C.c_int32),
+        ("num_octants", C.c_int64),
+        ("num_nonempty", C.c_int64),
+        ("keys", C.c_void_p),
+        ("labels", C.c_void_p),
+        ("rows_of_label", C.c_void_p),
+        ("nbr", C.c_void_p),
+    ]
+
+
+_ALLOC_FN = C.CFUNCTYPE(C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p)
+_FREE_FN = C.CFUNCTYPE(None, C.c_void_p, C.c_void_p, C.c_void_p)
+
+
+class _Allocator(C.Structure):
+    _fields_ = [("alloc", _ALLOC_FN), ("free", _FREE_FN), ("ctx", C.c_void_p)]
+
+
+# Live device allocations made for the library: data_ptr -> backing tensor.
+_live: dict[int, torch.Tensor] = {}
+
+
+def _torch_alloc(ctx, nbytes, stream):
+    try:
+        t = torch.empty(int(nbytes), dtype=torch.uint8, device="cuda")
+    except Exception:  # out of memory -> NULL -> OC_ERR_NOMEM
+        return None
+    _live[t.data_ptr()] = t
+    return t.data_ptr()
+
+
+def _torch_free(ctx, ptr, stream):
+    _live.pop(int(ptr), None)
+
+
+_alloc_cb = _ALLOC_FN(_torch_alloc)
+_free_cb = _FREE_FN(_torch_free)
+_allocator = _Allocator(_alloc_cb, _free_cb, None)
+
+_lib = None
+
+
+def load():
+    """Load liboc.so (built in-tree by build.py); raise OcError if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = lib_path()
+    if not os.path.exists(path):
+        raise OcError(-1, f"{path} is missing: run paper_1712_01537_amd/build.py (hipcc, gfx950)")
+    L = C.CDLL(path)
+    p, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+    sigs = {
+        "oc_build": ([p, p, p, i32, i32, i32, p, p, C.POINTER(p)], C.c_int),
+        "oc_octree_level": ([p, i32, C.POINTER(_Level)], C.c_int),
+        "oc_octree_info": ([p, p, p, p], C.c_int),
+        "oc_octree_signal": ([p], p),
+        "oc_octree_free": ([p], None),
+        "oc_conv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, i32, p], C.c_int),
+        "oc_conv_bwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
+        "oc_conv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, p, sz, i32, p],
+                        C.c_int),
+        "oc_pool_fwd": ([p, i32, p, i32, p, p, p], C.c_int),
+        "oc_pool_bwd": ([p, i32, p, p, i32, p, p], C.c_int),
+        "oc_unpool_fwd": ([p, i32, p, p, i32, p, p], C.c_int),
+        "oc_unpool_bwd": ([p, i32, p, p, i32, p, p], C.c_int),
+        "oc_status_str": ([C.c_int], C.c_char_p),
+        "oc_last_error": ([], C.c_char_p),
+    }
+    for name, (args, res) in sigs.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = L
+    return L
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise OcError(rc, load().oc_last_error().decode())
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None, shape=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise OcError(1, f"{name} must be a CUDA (HIP) tensor")
+    if not t.is_contiguous():
+        raise OcError(1, f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise OcError(1, f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise OcError(1, f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return C.c_void_p(t.data_ptr())
+
+
+class Octree:
+    """A built super-octree; its arrays live in torch-owned device memory."""
+
+    def __init__(self, handle: C.c_void_p):
+        self._h = handle
+        d, fd, b = C.c_int32(), C.c_int32(), C.c_int32()
+        _check(load().oc_octree_info(handle, C.byref(d), C.byref(fd), C.byref(b)))
+        self.depth, self.full_depth, self.batch = d.value, fd.value, b.value
+        self._lv = []
+        for l in range(self.depth + 1):
+            lv = _Level()
+            _check(load().oc_octree_level(handle, l, C.byref(lv)))
+            self._lv.append(lv)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def num(self, l: int) -> int:
+        return int(self._lv[l].num_octants)
+
+    def nonempty(self, l: int) -> int:
+        return int(self._lv[l].num_nonempty)
+
+    def _view(self, ptr, count, dtype, shape):
+        if count == 0 or not ptr:
+            return torch.empty(shape, dtype=dtype, device="cuda")
+        esz = torch.empty((), dtype=dtype).element_size()
+        for base, t in _live.items():
+            if base <= ptr < base + t.numel():
+                off = ptr - base
+                return t[off:off + count * esz].view(dtype).view(shape)
+        raise OcError(1, "octree array not found among live allocations")
+
+    def keys(self, l):
+        return self._view(self._lv[l].keys, self.num(l), torch.int32, (self.num(l),))
+
+    def labels(self, l):
+        return self._view(self._lv[l].labels, self.num(l), torch.int32, (self.num(l),))
+
+    def rows(self, l):
+        return self._view(self._lv[l].rows_of_label, self.nonempty(l), torch.int32, (self.nonempty(l),))
+
+    def nbr(self, l):
+        m = self.nonempty(l - 1)
+        return self._view(self._lv[l].nbr, 27 * m, torch.int32, (m, 27))
+
+    def signal(self):
+        n = self.num(self.depth)
+        return self._view(load().oc_octree_signal(self._h), 3 * n, torch.float32, (n, 3))
+
+    def free(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            load().oc_octree_free(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def oc_build(points: torch.Tensor, normals: torch.Tensor, shape_offsets, depth: int,
+             full_depth: int = 2) -> Octree:
+    """Build the super-octree of a batch of point clouds (dev f32 [P][3] each)."""
+    L = load()
+    offs = torch.as_tensor(shape_offsets, dtype=torch.int32).cpu().contiguous()
+    P = int(offs[-1])
+    if points.numel() != 3 * P or normals.numel() != 3 * P:
+        raise OcError(1, f"points/normals must hold {P} x 3 values")
+    pp = _dev(points, "points", torch.float32)
+    nn = _dev(normals, "normals", torch.float32)
+    h = C.c_void_p()
+    _check(L.oc_build(pp, nn, C.c_void_p(offs.data_ptr()), len(offs) - 1, depth, full_depth,
+                      C.byref(_allocator), _stream(), C.byref(h)))
+    return Octree(h)
+
+
+def _dtype_code(x: torch.Tensor):
+    if x.dtype == torch.float32:
+        return OC_F32
+    if x.dtype == torch.bfloat16:
+        return OC_BF16
+    raise OcError(1, f"unsupported dtype {x.dtype}")
+
+
+def _conv_dims(tree: Octree, depth: int, stride: int, x, w):
+    if not 1 <= depth <= tree.depth:
+        raise OcError(1, f"depth {depth} not in 1..{tree.depth}")
+    K3, cin, cout = w.shape
+    n_in = tree.num(depth)
+    n_out = n_in if stride == 1 else tree.num(depth - 1)
+    if x is not None and tuple(x.shape) != (n_in, cin):
+        raise OcError(1, f"x has shape {tuple(x.shape)}, expected {(n_in, cin)}")
+    return K3, cin, cout, n_in, n_out
+
+
+def oc_conv_fwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tensor,
+                w: torch.Tensor, relu: bool = False, y: torch.Tensor | None = None) -> torch.Tensor:
+    K3, cin, cout, n_in, n_out = _conv_dims(tree, depth, stride, x, w)
+    if K3 != ksize ** 3:
+        raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
+    dt = _dtype_code(x)
+    if w.dtype != x.dtype:
+        raise OcError(1, "x and w must share a dtype")
+    if y is None:
+        y = torch.empty((n_out, cout), dtype=torch.float32, device=x.device)
+    _check(load().oc_conv_fwd(tree.handle, depth, ksize, stride, dt, _dev(x, "x"), cin,
+                              _dev(w, "w"), cout, _dev(y, "y", torch.float32, (n_out, cout)),
+                              OC_FUSE_RELU if relu else 0, _stream()))
+    return y
+
+
+def oc_conv_bwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tensor,
+                w: torch.Tensor, dy: torch.Tensor, y: torch.Tensor | None = None,
+                relu: bool = False, need_dx: bool = True, need_dw: bool = True):
+    K3, cin, cout, n_in, n_out = _conv_dims(tree, depth, stride, x, w)
+    if K3 != ksize ** 3:
+        raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
+    dt = _dtype_code(w)
+    L = load()
+    dx = torch.empty((n_in, cin), dtype=torch.float32, device=w.device) if need_dx else None
+    dw = torch.empty((K3, cin, cout), dtype=torch.float32, device=w.device) if need_dw else None
+    ws_bytes = L.oc_conv_bwd_workspace(tree.handle, depth, ksize, stride, dt, cin, cout)
+    ws = torch.empty(max(int(ws_bytes), 1), dtype=torch.uint8, device=w.device)
+    yp = _dev(y, "y", torch.float32, (n_out, cout)) if relu else None
+    _check(L.oc_conv_bwd(tree.handle, depth, ksize, stride, dt, _dev(x, "x") if x is not None else None,
+                         cin, _dev(w, "w"), cout, yp,
+                         _dev(dy, "dy", torch.float32, (n_out, cout)),
+                         _dev(dx, "dx") if dx is not None else None,
+                         _dev(dw, "dw") if dw is not None else None,
+                         _dev(ws, "ws"), ws.numel(), OC_FUSE_RELU if relu else 0, _stream()))
+    return dx, dw
+
+
+def oc_pool_fwd(tree: Octree, depth: int, x: torch.Tensor):
+    c = x.shape[1]
+    n_in, n_out, m = tree.num(depth), tree.num(depth - 1), tree.nonempty(depth - 1)
+    y = torch.empty((n_out, c), dtype=torch.float32, device=x.device)
+    sw = torch.empty((m, c), dtype=torch.uint8, device=x.device)
+    _check(load().oc_pool_fwd(tree.handle, depth, _dev(x, "x", torch.float32, (n_in, c)), c,
+                              _dev(y, "y"), _dev(sw, "sw"), _stream()))
+    return y, sw
+
+
+def oc_pool_bwd(tree: Octree, depth: int, dy: torch.Tensor, sw: torch.Tensor) -> torch.Tensor:
+    c = dy.shape[1]
+    n_in, n_out, m = tree.num(depth), tree.num(depth - 1), tree.nonempty(depth - 1)
+    dx = torch.empty((n_in, c), dtype=torch.float32, device=dy.device)
+    _check(load().oc_pool_bwd(tree.handle, depth, _dev(dy, "dy", torch.float32, (n_out, c)),
+                              _dev(sw, "sw", torch.uint8, (m, c)), c, _dev(dx, "dx"), _stream()))
+    return dx
+
+
+def oc_unpool_fwd(tree: Octree, depth: int, x: torch.Tensor, sw: torch.Tensor) -> torch.Tensor:
+    c = x.shape[1]
+    n_l, n_p, m = tree.num(depth), tree.num(depth - 1), tree.nonempty(depth - 1)
+    y = torch.empty((n_l, c), dtype=torch.float32, device=x.device)
+    _check(load().oc_unpool_fwd(tree.handle, depth, _dev(x, "x", torch.float32, (n_p, c)),
+                                _dev(sw, "sw", torch.uint8, (m, c)), c, _dev(y, "y"), _stream()))
+    return y
+
+
+def oc_unpool_bwd(tree: Octree, depth: int, dy: torch.Tensor, sw: torch.Tensor) -> torch.Tensor:
+    c = dy.shape[1]
+    n_l, n_p, m = tree.num(depth), tree.num(depth - 1), tree.nonempty(depth - 1)
+    dx = torch.empty((n_p, c), dtype=torch.float32, device=dy.device)
+    _check(load().oc_unpool_bwd(tree.handle, depth, _dev(dy, "dy", torch.float32, (n_l, c)),
+                                _dev(sw, "sw", torch.uint8, (m, c)), c, _dev(dx, "dx"), _stream()))
+    return dx

@@ -1,0 +1,100 @@
+// Error reporting, allocation and octree accessors of the C ABI.
+#include <cstring>
+
+#include "common.h"
+
+namespace {
+thread_local char g_msg[512] = "";
+}
+
+namespace oc {
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_msg, sizeof(g_msg), fmt, ap);
+  va_end(ap);
+}
+
+oc_status fail(oc_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_msg, sizeof(g_msg), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+void* dev_alloc(const oc_allocator& a, size_t bytes, hipStream_t s) {
+  if (bytes == 0) bytes = 256;
+  if (a.alloc) return a.alloc(a.ctx, bytes, s);
+  void* p = nullptr;
+  if (hipMalloc(&p, bytes) != hipSuccess) return nullptr;
+  return p;
+}
+
+void dev_free(const oc_allocator& a, void* p, hipStream_t s) {
+  if (!p) return;
+  if (a.free) {
+    a.free(a.ctx, p, s);
+    return;
+  }
+  // hipFree waits for the device, so pending work on the buffer completes.
+  (void)hipFree(p);
+}
+
+oc_status check_tree_level(const oc_octree* t, int32_t l, int32_t min_l) {
+  if (!t) return fail(OC_ERR_ARG, "octree is NULL");
+  if (l < min_l || l > t->depth)
+    return fail(OC_ERR_ARG, "depth %d not in %d..%d", l, min_l, t->depth);
+  return OC_OK;
+}
+
+}  // namespace oc
+
+extern "C" {
+
+oc_status oc_octree_level(const oc_octree* t, int32_t l, oc_level* out) {
+  oc_status st = oc::check_tree_level(t, l, 0);
+  if (st != OC_OK) return st;
+  if (!out) return oc::fail(OC_ERR_ARG, "oc_octree_level: out is NULL");
+  out->depth = l;
+  out->num_octants = t->N[l];
+  out->num_nonempty = t->M[l];
+  out->keys = t->keys[l];
+  out->labels = t->labels[l];
+  out->rows_of_label = t->rows[l];
+  out->nbr = t->nbr[l];
+  return OC_OK;
+}
+
+oc_status oc_octree_info(const oc_octree* t, int32_t* depth, int32_t* full_depth, int32_t* batch) {
+  if (!t) return oc::fail(OC_ERR_ARG, "octree is NULL");
+  if (depth) *depth = t->depth;
+  if (full_depth) *full_depth = t->full_depth;
+  if (batch) *batch = t->batch;
+  return OC_OK;
+}
+
+const float* oc_octree_signal(const oc_octree* t) { return t ? t->signal : nullptr; }
+
+void oc_octree_free(oc_octree* t) {
+  if (!t) return;
+  oc::dev_free(t->alloc, t->block, t->stream);
+  delete t;
+}
+
+const char* oc_status_str(oc_status s) {
+  switch (s) {
+    case OC_OK: return "ok";
+    case OC_ERR_ARG: return "invalid argument";
+    case OC_ERR_RANGE: return "point outside the unit cube";
+    case OC_ERR_NOMEM: return "out of device memory";
+    case OC_ERR_DEVICE: return "device error";
+    case OC_ERR_UNSUPPORTED: return "unsupported";
+  }
+  return "unknown status";
+}
+
+const char* oc_last_error(void) { return g_msg; }
+
+}  // extern "C"

@@ -1,0 +1,55 @@
+"""The C-ABI library loads and exports every function include/oc.h declares;
+argument errors are reported before any device work (runs without a GPU)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import paper_1712_01537_amd as oc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "oc.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(oc_[a-z_]+)\s*\(", src)))
+
+
+def test_header_matches_binding():
+    names = _declared()
+    assert "oc_build" in names and "oc_conv_bwd" in names
+    assert sorted(oc.EXPORTS) == names
+
+
+def test_library_exports_every_symbol():
+    L = oc.load()
+    for name in _declared():
+        assert hasattr(L, name), name
+
+
+def test_argument_errors_without_device():
+    L = oc.load()
+    out = C.c_void_p()
+    offs = (C.c_int32 * 3)(0, 0, 0)
+    assert L.oc_build(None, None, offs, 0, 3, 2, None, None, C.byref(out)) == 1   # batch 0
+    assert L.oc_build(None, None, offs, 2, 9, 2, None, None, C.byref(out)) == 1   # depth 9
+    assert L.oc_build(None, None, offs, 2, 3, 4, None, None, C.byref(out)) == 1   # full > depth
+    assert L.oc_build(None, None, None, 2, 3, 2, None, None, C.byref(out)) == 1   # no offsets
+    bad = (C.c_int32 * 3)(0, 5, 2)
+    assert L.oc_build(None, None, bad, 2, 3, 2, None, None, C.byref(out)) == 1    # decreasing
+    assert b"decrease" in L.oc_last_error()
+    assert L.oc_build(None, None, (C.c_int32 * 2)(0, 4), 1, 3, 2, None, None, C.byref(out)) == 1
+    assert L.oc_conv_fwd(None, 1, 3, 1, 0, None, 3, None, 4, None, 0, None) == 1
+    assert L.oc_pool_fwd(None, 1, None, 3, None, None, None) == 1
+    assert L.oc_octree_signal(None) is None
+    assert L.oc_status_str(2) == b"point outside the unit cube"
+    L.oc_octree_free(None)
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(oc, "_lib", None)
+    monkeypatch.setattr(oc, "lib_path", lambda: str(tmp_path / "liboc.so"))
+    with pytest.raises(oc.OcError):
+        oc.load()

@@ -1,0 +1,110 @@
+"""GPU parity of the octree build: keys, labels, label->row maps and the
+sibling-group neighbour tables bit-exact against the CPU oracle; the input
+signal within fp32 tolerance."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import assert_f32_close, per_octant_neighbors
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu():
+    import paper_1712_01537_amd as oc
+    return oc
+
+
+def _build_both(pts, nrm, offs, depth, full):
+    oc = _gpu()
+    print(f"[build] P={len(pts)} B={len(offs) - 1} depth={depth} full={full}", flush=True)
+    ref = oracle.Octree(pts, nrm, offs, depth, full)
+    tree = oc.oc_build(torch.as_tensor(pts).cuda(), torch.as_tensor(nrm).cuda(), offs, depth, full)
+    torch.cuda.synchronize()
+    return ref, tree
+
+
+def _compare_tree(ref, tree, nb_depths=None, K=3):
+    assert tree.depth == ref.depth and tree.batch == ref.batch
+    for l in range(ref.depth + 1):
+        assert tree.num(l) == ref.num(l), l
+        assert tree.nonempty(l) == ref.nonempty(l), l
+        np.testing.assert_array_equal(tree.keys(l).cpu().numpy().view(np.uint32), ref.keys(l), err_msg=f"keys {l}")
+        np.testing.assert_array_equal(tree.labels(l).cpu().numpy(), ref.labels(l), err_msg=f"labels {l}")
+        np.testing.assert_array_equal(tree.rows(l).cpu().numpy(), ref.rows(l), err_msg=f"rows {l}")
+    for l in (nb_depths if nb_depths is not None else range(1, ref.depth + 1)):
+        if ref.num(l) == 0:
+            continue
+        got = per_octant_neighbors(tree.nbr(l).cpu().numpy(), K)
+        np.testing.assert_array_equal(got, ref.neighbors(l, K), err_msg=f"neighbours depth {l} K {K}")
+    assert_f32_close(tree.signal().cpu().numpy(), ref.signal, "signal", rtol=1e-6, atol=1e-7)
+
+
+SMALL = [  # seed, shapes, points per shape, depth, full depth, spread
+    (1, 1, 300, 3, 0, "uniform"),
+    (2, 3, [200, 0, 57], 4, 2, "union"),
+    (3, 2, 500, 5, 1, "union"),
+    (4, 4, [1, 2, 3, 0], 4, 4, "uniform"),
+    (5, 5, 2000, 6, 2, "union"),
+    (6, 2, 40000, 8, 2, "union"),
+    (7, 17, 300, 5, 2, "union"),
+]
+
+
+@pytest.mark.parametrize("seed,B,n,depth,full,spread", SMALL)
+def test_build_small(seed, B, n, depth, full, spread):
+    pts, nrm, offs = synth.random_cloud(seed, B, n, spread)
+    ref, tree = _build_both(pts, nrm, offs, depth, full)
+    _compare_tree(ref, tree)
+    # K = 5 neighbourhoods come from the same 27-entry tables
+    _compare_tree(ref, tree, nb_depths=[depth], K=5)
+
+
+def test_build_fig2_example():
+    pts = np.array([[.1, .1, .1], [.1, .1, .6], [.1, .6, .1], [.4, .9, .4], [.2, .2, .05]], np.float32)
+    nrm = np.array([[1, 0, 0], [0, 1, 0], [0, 0, 1], [0, 0, -1], [0, 1, 0]], np.float32)
+    ref, tree = _build_both(pts, nrm, [0, 5], 2, 1)
+    _compare_tree(ref, tree)
+    assert tree.labels(1).cpu().tolist() == [1, 2, 3, 0, 0, 0, 0, 0]
+
+
+def test_build_all_empty_and_errors():
+    oc = _gpu()
+    pts = np.zeros((0, 3), np.float32)
+    ref, tree = _build_both(pts, pts, [0, 0, 0], 4, 2)
+    _compare_tree(ref, tree)
+    ref0, tree0 = _build_both(pts, pts, [0, 0], 3, 0)
+    _compare_tree(ref0, tree0)
+    bad = torch.tensor([[0.5, 1.5, 0.2]], device="cuda")
+    with pytest.raises(oc.OcError) as e:
+        oc.oc_build(bad, bad, [0, 1], 3, 2)
+    assert e.value.code == 2
+    nan = torch.tensor([[0.5, float("nan"), 0.2]], device="cuda")
+    with pytest.raises(oc.OcError) as e:
+        oc.oc_build(nan, nan, [0, 1], 3, 2)
+    assert e.value.code == 2
+
+
+def test_build_deterministic():
+    pts, nrm, offs = synth.make_points("net_d5", batch=4)
+    oc = _gpu()
+    p, n = torch.as_tensor(pts).cuda(), torch.as_tensor(nrm).cuda()
+    a = oc.oc_build(p, n, offs, 5, 2)
+    b = oc.oc_build(p, n, offs, 5, 2)
+    for l in range(6):
+        assert torch.equal(a.keys(l), b.keys(l)) and torch.equal(a.labels(l), b.labels(l))
+        if l:
+            assert torch.equal(a.nbr(l), b.nbr(l))
+    assert torch.equal(a.signal().view(torch.int32), b.signal().view(torch.int32))
+
+
+@pytest.mark.parametrize("name", ["sphere_d5", "net_d5", "net_d6", "deep_d8", "wide_d7"])
+def test_build_workloads_full_size(name):
+    w = synth.WORKLOADS[name]
+    pts, nrm, offs = synth.make_points(w)
+    ref, tree = _build_both(pts, nrm, offs, w.depth, w.full_depth)
+    _compare_tree(ref, tree, nb_depths=[w.depth])
+    print(f"[build] {name}: N = {[tree.num(l) for l in range(w.depth + 1)]}, "
+          f"M = {[tree.nonempty(l) for l in range(w.depth + 1)]}", flush=True)

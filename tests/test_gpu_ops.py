@@ -1,0 +1,257 @@
+"""GPU parity of convolution, pooling and unpooling against the CPU oracle.
+
+Small cases compare every output element; the full-size workloads compare
+sampled output rows, sampled input-gradient rows and sampled weight-gradient
+entries, each computed one by one by the oracle, in the launch configuration
+the bench uses."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import (assert_bf16_close, assert_dw_close, assert_f32_close, bf16_round)
+
+pytestmark = pytest.mark.gpu
+
+
+def _oc():
+    import paper_1712_01537_amd as oc
+    return oc
+
+
+def _trees(pts, nrm, offs, depth, full=2):
+    oc = _oc()
+    ref = oracle.Octree(pts, nrm, offs, depth, full)
+    tree = oc.oc_build(torch.as_tensor(pts).cuda(), torch.as_tensor(nrm).cuda(), offs, depth, full)
+    assert [tree.num(l) for l in range(depth + 1)] == [ref.num(l) for l in range(depth + 1)]
+    return ref, tree
+
+
+def _cuda(a, dtype=torch.float32):
+    return torch.as_tensor(np.ascontiguousarray(a)).to(dtype).cuda()
+
+
+def _mask_ambiguous(dy, yref, relu):
+    """Zero the upstream gradient where the fp32 sign of the pre-activation is
+    not decided by the oracle's float64 value within the forward tolerance, so
+    both sides take the same ReLU decision (float64 decides, rounded to fp32)."""
+    if not relu:
+        return dy
+    dy = dy.copy()
+    dy[np.abs(yref) <= 1e-4] = 0.0
+    return dy
+
+
+SMALL = [  # seed, B, n, depth, K, stride, cin, cout, relu
+    (1, 2, 400, 4, 3, 1, 5, 7, False),
+    (2, 3, 300, 4, 3, 1, 16, 32, True),
+    (3, 1, 800, 5, 5, 1, 8, 8, False),
+    (4, 2, 500, 4, 3, 2, 6, 10, False),
+    (5, 2, 500, 5, 3, 2, 16, 16, True),
+    (6, 1, 300, 3, 3, 1, 3, 16, True),
+    (7, 4, 300, 4, 5, 1, 12, 20, True),
+    (8, 2, 900, 5, 3, 1, 64, 128, False),
+]
+
+
+@pytest.mark.parametrize("seed,B,n,depth,K,stride,cin,cout,relu", SMALL)
+def test_conv_small_fp32(seed, B, n, depth, K, stride, cin, cout, relu):
+    oc = _oc()
+    print(f"[conv] seed={seed} B={B} d={depth} K={K} s={stride} {cin}->{cout} relu={relu}", flush=True)
+    pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
+    ref, tree = _trees(pts, nrm, offs, depth)
+    l = depth
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((ref.num(l), cin)).astype(np.float32)
+    w = (rng.standard_normal((K ** 3, cin, cout)) / np.sqrt(K ** 3 * cin)).astype(np.float32)
+    n_out = ref.num(l) if stride == 1 else ref.num(l - 1)
+    if stride == 1:
+        nb = ref.neighbors(l, K)
+        yref = oracle.conv_fwd(nb, x, w)
+    else:
+        nb = ref.neighbors(l, K, stride=2)
+        yref = oracle.renew(ref.labels(l - 1), oracle.conv_fwd(nb, x, w))
+    dy = _mask_ambiguous(rng.standard_normal((n_out, cout)).astype(np.float32), yref, relu)
+    y = oc.oc_conv_fwd(tree, l, K, stride, _cuda(x), _cuda(w), relu=relu)
+    yr = oracle.relu_fwd(yref) if relu else yref
+    assert_f32_close(y.cpu().numpy(), yr, "y")
+    dx, dw = oc.oc_conv_bwd(tree, l, K, stride, _cuda(x), _cuda(w), _cuda(dy), y=y, relu=relu)
+    dye = oracle.relu_bwd(yref, dy) if relu else dy
+    if stride == 1:
+        dxr = oracle.conv_bwd_data(nb, dye, w, ref.num(l))
+        dwr = oracle.conv_bwd_weight(nb, x, dye, K ** 3)
+    else:
+        dxr, dwr = oracle.conv_s2_bwd(ref, l, x, w, dye)
+    assert_f32_close(dx.cpu().numpy(), dxr, "dx")
+    assert_dw_close(dw.cpu().numpy(), dwr, "dw")
+    # deterministic: identical bits on a second call
+    dx2, dw2 = oc.oc_conv_bwd(tree, l, K, stride, _cuda(x), _cuda(w), _cuda(dy), y=y, relu=relu)
+    assert torch.equal(dx.view(torch.int32), dx2.view(torch.int32))
+    assert torch.equal(dw.view(torch.int32), dw2.view(torch.int32))
+
+
+@pytest.mark.parametrize("K,stride", [(3, 1), (5, 1), (3, 2)])
+def test_conv_small_bf16(K, stride):
+    oc = _oc()
+    pts, nrm, offs = synth.random_cloud(20 + K, 2, 600, "union")
+    ref, tree = _trees(pts, nrm, offs, 5)
+    l, cin, cout = 5, 32, 48
+    rng = np.random.default_rng(K)
+    x32 = rng.standard_normal((ref.num(l), cin)).astype(np.float32)
+    w32 = (rng.standard_normal((K ** 3, cin, cout)) / np.sqrt(K ** 3 * cin)).astype(np.float32)
+    x, w = bf16_round(x32), bf16_round(w32)
+    nb = ref.neighbors(l, K, stride=stride)
+
+    def fwd(a, b):
+        r = oracle.conv_fwd(nb, a, b)
+        return oracle.renew(ref.labels(l - 1), r) if stride == 2 else r
+
+    yref = fwd(x, w)
+    y = oc.oc_conv_fwd(tree, l, K, stride, _cuda(x, torch.bfloat16), _cuda(w, torch.bfloat16))
+    # same bf16 values on both sides: only the fp32 accumulation differs
+    assert_f32_close(y.cpu().numpy(), yref, "y bf16 inputs")
+    # against the fp32-input oracle: the bf16 rounding of inputs and weights
+    assert_bf16_close(y.cpu().numpy(), fwd(x32, w32), "y vs fp32 oracle")
+    dy = rng.standard_normal(yref.shape).astype(np.float32)
+    dx, dw = oc.oc_conv_bwd(tree, l, K, stride, _cuda(x, torch.bfloat16), _cuda(w, torch.bfloat16), _cuda(dy))
+    if stride == 1:
+        dxr = oracle.conv_bwd_data(nb, dy, w, ref.num(l))
+        dwr = oracle.conv_bwd_weight(nb, x, dy, K ** 3)
+    else:
+        dxr, dwr = oracle.conv_s2_bwd(ref, l, x, w, dy)
+    assert_f32_close(dx.cpu().numpy(), dxr, "dx bf16 weights")
+    assert_dw_close(dw.cpu().numpy(), dwr, "dw bf16 inputs")
+
+
+@pytest.mark.parametrize("seed,B,n,depth,c", [(31, 2, 500, 4, 8), (32, 3, 300, 5, 3), (33, 1, 100, 3, 32)])
+def test_pool_unpool_small(seed, B, n, depth, c):
+    oc = _oc()
+    pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
+    ref, tree = _trees(pts, nrm, offs, depth)
+    l = depth
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((ref.num(l), c)).astype(np.float32)
+    x[::5] = np.round(x[::5])  # plenty of ties among siblings
+    y, sw = oc.oc_pool_fwd(tree, l, _cuda(x))
+    yr, swr = oracle.pool_fwd(ref.labels(l - 1), x)
+    np.testing.assert_array_equal(y.cpu().numpy(), yr)
+    np.testing.assert_array_equal(sw.cpu().numpy(), swr)
+    dy = rng.standard_normal((ref.num(l - 1), c)).astype(np.float32)
+    np.testing.assert_array_equal(oc.oc_pool_bwd(tree, l, _cuda(dy), sw).cpu().numpy(),
+                                  oracle.pool_bwd(ref.labels(l - 1), dy, swr, ref.num(l)))
+    np.testing.assert_array_equal(oc.oc_unpool_fwd(tree, l, _cuda(dy), sw).cpu().numpy(),
+                                  oracle.unpool_fwd(ref.labels(l - 1), dy, swr, ref.num(l)))
+    g = rng.standard_normal((ref.num(l), c)).astype(np.float32)
+    np.testing.assert_array_equal(oc.oc_unpool_bwd(tree, l, _cuda(g), sw).cpu().numpy(),
+                                  oracle.unpool_bwd(ref.labels(l - 1), g, swr))
+
+
+def test_conv_edge_cases():
+    oc = _oc()
+    # a single shape with one point, full depth 0: depth-1 has 8 octants, one group
+    pts = np.array([[0.3, 0.6, 0.9]], np.float32)
+    nrm = np.ones((1, 3), np.float32)
+    ref, tree = _trees(pts, nrm, [0, 1], 3, 0)
+    for l in (1, 2, 3):
+        x = np.arange(ref.num(l) * 2, dtype=np.float32).reshape(-1, 2) / 7
+        w = np.linspace(-1, 1, 27 * 2 * 3, dtype=np.float32).reshape(27, 2, 3)
+        y = oc.oc_conv_fwd(tree, l, 3, 1, _cuda(x), _cuda(w))
+        assert_f32_close(y.cpu().numpy(), oracle.conv_fwd(ref.neighbors(l, 3), x, w), f"y l={l}")
+    # argument errors are reported, nothing launched
+    with pytest.raises(oc.OcError):
+        oc.oc_conv_fwd(tree, 0, 3, 1, _cuda(np.zeros((1, 2))), _cuda(np.zeros((27, 2, 3))))
+    with pytest.raises(oc.OcError):
+        oc.oc_conv_fwd(tree, 3, 7, 1, _cuda(np.zeros((ref.num(3), 2))), _cuda(np.zeros((343, 2, 3))))
+
+
+# ----------------------------------------------------------------------------
+# full-size workloads, sampled
+
+
+def _sample(rng, n, k):
+    return np.sort(rng.choice(n, size=min(k, n), replace=False))
+
+
+def _check_conv_full(ref, tree, l, K, stride, x, w, relu, dy, tag, dtype=torch.float32):
+    oc = _oc()
+    rng = np.random.default_rng(0)
+    n_in = ref.num(l)
+    nb = ref.neighbors(l, K, stride=stride)
+    xq, wq = (x, w) if dtype == torch.float32 else (bf16_round(x), bf16_round(w))
+    print(f"[{tag}] conv d{l} K{K} s{stride} {x.shape[1]}->{w.shape[2]} rows {n_in}", flush=True)
+    y = oc.oc_conv_fwd(tree, l, K, stride, _cuda(xq, dtype), _cuda(wq, dtype), relu=relu)
+    yg = y.cpu().numpy()
+    if relu or stride == 2:
+        pre = oracle.conv_fwd(nb, xq, wq)
+        if stride == 2:
+            pre = oracle.renew(ref.labels(l - 1), pre)
+        dy = _mask_ambiguous(dy, pre, relu)
+        assert_f32_close(yg, oracle.relu_fwd(pre) if relu else pre, f"{tag} y")
+        dye = oracle.relu_bwd(pre, dy) if relu else dy
+    else:
+        rows = _sample(rng, yg.shape[0], 3000)
+        assert_f32_close(yg[rows], oracle.conv_fwd(nb, xq, wq, rows=rows), f"{tag} y")
+        dye = dy
+    dx, dw = oc.oc_conv_bwd(tree, l, K, stride, _cuda(xq, dtype), _cuda(wq, dtype), _cuda(dy),
+                            y=y, relu=relu)
+    want = np.zeros(n_in, bool)
+    want[_sample(rng, n_in, 3000)] = True
+    ent = _sample(rng, w.size, 300)
+    if stride == 1:
+        dxr = oracle.conv_bwd_data(nb, dye, wq, n_in, want=want)
+        dwr = oracle.conv_bwd_weight(nb, xq, dye, K ** 3, entries=ent)
+    else:
+        dyh = oracle.renew_bwd(ref.labels(l - 1), dye, nb.shape[0])
+        dxr = oracle.conv_bwd_data(nb, dyh, wq, n_in, want=want)
+        dwr = oracle.conv_bwd_weight(nb, xq, dyh, K ** 3, entries=ent)
+    assert_f32_close(dx.cpu().numpy()[want], dxr[want], f"{tag} dx")
+    rule = assert_dw_close(dw.cpu().numpy().ravel()[ent], dwr, f"{tag} dw")
+    print(f"[{tag}] dw rule: {rule}", flush=True)
+    return y
+
+
+@pytest.mark.parametrize("name", ["sphere_d5", "net_d5", "net_d6", "deep_d8", "wide_d7"])
+def test_workload_full_size(name):
+    oc = _oc()
+    w_ = synth.WORKLOADS[name]
+    pts, nrm, offs = synth.make_points(w_)
+    ref, tree = _trees(pts, nrm, offs, w_.depth, w_.full_depth)
+    first = True
+    for li, L in enumerate(w_.layers):
+        l = L.depth
+        if L.op == "conv":
+            if first and w_.signal_input:
+                x = ref.signal  # the oracle's averaged normals
+            else:
+                x = synth.make_features([w_.seed_id, 3000 + li], ref.num(l), L.cin)
+            first = False
+            K = L.ksize
+            w = synth.make_weights(w_, li, K, L.cin, L.cout)
+            n_out = ref.num(l) if L.stride == 1 else ref.num(l - 1)
+            dy = synth.make_upstream(w_, li, n_out, L.cout)
+            _check_conv_full(ref, tree, l, K, L.stride, x, w, L.relu, dy, f"{name}/{li}")
+            if L.dtype == "bf16":
+                _check_conv_full(ref, tree, l, K, L.stride, x, w, L.relu, dy, f"{name}/{li}/bf16",
+                                 dtype=torch.bfloat16)
+        elif L.op == "pool":
+            x = synth.make_features([w_.seed_id, 3000 + li], ref.num(l), L.cin)
+            print(f"[{name}/{li}] pool d{l} C{L.cin}", flush=True)
+            y, sw = oc.oc_pool_fwd(tree, l, _cuda(x))
+            yr, swr = oracle.pool_fwd(ref.labels(l - 1), x)
+            np.testing.assert_array_equal(y.cpu().numpy(), yr)
+            np.testing.assert_array_equal(sw.cpu().numpy(), swr)
+            dy = synth.make_upstream(w_, li, ref.num(l - 1), L.cin)
+            np.testing.assert_array_equal(oc.oc_pool_bwd(tree, l, _cuda(dy), sw).cpu().numpy(),
+                                          oracle.pool_bwd(ref.labels(l - 1), dy, swr, ref.num(l)))
+        elif L.op == "unpool":
+            x = synth.make_features([w_.seed_id, 3000 + li], ref.num(l), L.cin)
+            _, sw = oc.oc_pool_fwd(tree, l, _cuda(x))
+            _, swr = oracle.pool_fwd(ref.labels(l - 1), x)
+            xp = synth.make_features([w_.seed_id, 4000 + li], ref.num(l - 1), L.cin)
+            print(f"[{name}/{li}] unpool d{l} C{L.cin}", flush=True)
+            np.testing.assert_array_equal(oc.oc_unpool_fwd(tree, l, _cuda(xp), sw).cpu().numpy(),
+                                          oracle.unpool_fwd(ref.labels(l - 1), xp, swr, ref.num(l)))
+            g = synth.make_upstream(w_, li, ref.num(l), L.cin)
+            np.testing.assert_array_equal(oc.oc_unpool_bwd(tree, l, _cuda(g), sw).cpu().numpy(),
+                                          oracle.unpool_bwd(ref.labels(l - 1), g, swr))
