@@ -77,11 +77,11 @@ def test_build_all_empty_and_errors():
     _compare_tree(ref, tree)
     ref0, tree0 = _build_both(pts, pts, [0, 0], 3, 0)
     _compare_tree(ref0, tree0)
-    bad = torch.tensor([[0.5, 1.5, 0.2]], device="cuda")
+    bad = torch.tensor([[0.5, 1.5, 0.2]], dtype=torch.float32, device="cuda")
     with pytest.raises(oc.OcError) as e:
         oc.oc_build(bad, bad, [0, 1], 3, 2)
     assert e.value.code == 2
-    nan = torch.tensor([[0.5, float("nan"), 0.2]], device="cuda")
+    nan = torch.tensor([[0.5, float("nan"), 0.2]], dtype=torch.float32, device="cuda")
     with pytest.raises(oc.OcError) as e:
         oc.oc_build(nan, nan, [0, 1], 3, 2)
     assert e.value.code == 2

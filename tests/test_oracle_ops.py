@@ -14,7 +14,6 @@ import torch.nn.functional as F
 import oracle
 import synth
 
-torch.set_default_dtype(torch.float64)
 
 
 def _coords(tree, l):
@@ -34,7 +33,7 @@ def _scatter(tree, l, feat):
     """Dense grid [B][C][2^l]^3 holding feat at the existing octants, 0 elsewhere."""
     b, x, y, z = _coords(tree, l)
     s = 2 ** l
-    g = torch.zeros((tree.batch, feat.shape[1], s, s, s))
+    g = torch.zeros((tree.batch, feat.shape[1], s, s, s), dtype=torch.float64)
     g[b, :, x, y, z] = feat
     return g
 
