@@ -1,0 +1,368 @@
+#!/usr/bin/env python3
+"""Throughput of the octree-CNN hot path (O-CNN, arXiv 1712.01537) on one MI355X.
+
+One step is one pass of the whole path over one batch of synthetic shapes whose
+points and normals are already in HBM:
+  oc_build (keys, sort, labels, signal, hash + sibling-group neighbour tables),
+  then the workload's network forward (conv + fused ReLU, max-pool) and
+  backward (pool routing, conv input and weight gradients).
+The default workload is the 32-shape depth-6 network: conv3 3->16 @d6,
+16->32 @d5, 32->64 @d4, 64->128 @d3 (each + ReLU + 2x2x2 max-pool), then
+conv3 + ReLU 128->256 @d2, fp32.
+
+The printed JSON line reports:
+  value          nominal convolution fwd+bwd GFLOP/s of the whole step
+                 (6 N_out K^3 Cin Cout per conv layer, every tap counted as
+                 im2col does, divided by the wall time of the step);
+  octants_per_s  output octants of all conv layers per second;
+  roofline       the dominant kernel: its algorithmic flops (or bytes) per
+                 launch over its mean launch time, from HIP events on the
+                 stream it runs on, against the MI355X peak;
+  cpu_baseline   the plain CPU oracle on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK = {  # MI355X published peaks
+    "hbm_GBps": 8000.0,
+    "fp32_TFLOPs": 157.3,
+    "bf16_TFLOPs": 2500.0,
+}
+
+# Per-kernel-class accounting: "flops" (MFMA-bound) or "bytes" (HBM-bound).
+BOUND = {
+    "conv_fwd": "mfma",
+    "conv_bwd_data": "mfma",
+    "conv_bwd_weight": "mfma",
+    "pool_fwd": "hbm",
+    "pool_bwd": "hbm",
+    "unpool_fwd": "hbm",
+    "unpool_bwd": "hbm",
+    "build": "hbm",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="net_d6")
+    ap.add_argument("--cpu-shapes", type=int, default=32,
+                    help="shapes of the batch the CPU oracle runs (0: skip)")
+    ap.add_argument("--layers", action="store_true", help="also print per-layer timings to stderr")
+    return ap.parse_args()
+
+
+class Step:
+    """Enqueue one build + forward + backward of a workload's network."""
+
+    def __init__(self, oc, torch, synth, wl):
+        self.oc, self.torch, self.wl = oc, torch, wl
+        pts, nrm, offs = synth.make_points(wl)
+        dev = "cuda"
+        self.pts = torch.as_tensor(pts).to(dev)
+        self.nrm = torch.as_tensor(nrm).to(dev)
+        self.offs = offs
+        self.npoints = len(pts)
+        self.dtype = torch.float32
+        self.weights = {}
+        for li, L in enumerate(wl.layers):
+            if L.op == "conv":
+                w = synth.make_weights(wl, li, L.ksize, L.cin, L.cout)
+                t = torch.as_tensor(w).to(dev)
+                if L.dtype == "bf16":
+                    t = t.to(torch.bfloat16)
+                self.weights[li] = t
+        # sizes come from a first build; the upstream gradient of the last
+        # layer and the input features of layers that do not read the signal
+        # are drawn once and stay resident
+        tree = oc.oc_build(self.pts, self.nrm, offs, wl.depth, wl.full_depth)
+        self.N = [tree.num(l) for l in range(wl.depth + 1)]
+        self.M = [tree.nonempty(l) for l in range(wl.depth + 1)]
+        tree.free()
+        last = len(wl.layers) - 1
+        Ll = wl.layers[last]
+        n_last = self._n_out(Ll)
+        self.dy_last = torch.as_tensor(
+            synth.make_upstream(wl, last, n_last, Ll.cout)).to(dev)
+        self.x0 = None
+        if not wl.signal_input:
+            L0 = wl.layers[0]
+            self.x0 = torch.as_tensor(synth.make_features([wl.seed_id, 3000], self.N[L0.depth],
+                                                          L0.cin)).to(dev)
+            if L0.dtype == "bf16":
+                self.x0 = self.x0.to(torch.bfloat16)
+        self.events = None  # {tag: [(start, end), ...]} when recording
+        self.traced = set()
+
+    def _n_out(self, L):
+        if L.op == "conv":
+            return self.N[L.depth] if L.stride == 1 else self.N[L.depth - 1]
+        if L.op == "pool":
+            return self.N[L.depth - 1]
+        return self.N[L.depth]
+
+    # --- accounting -------------------------------------------------------
+    def conv_flops(self):
+        """Nominal fwd+bwd flops and output octants of every conv layer."""
+        f = o = 0
+        for L in self.wl.layers:
+            if L.op == "conv":
+                n = self._n_out(L)
+                f += 6 * n * L.ksize ** 3 * L.cin * L.cout
+                o += n
+        return f, o
+
+    def work(self, tag, L):
+        """Algorithmic flops (MFMA-bound classes) or HBM bytes of one launch."""
+        N, M = self.N, self.M
+        if tag == "build":
+            d = self.wl.depth
+            return (self.npoints * 24 + sum(8 * N[k] + 4 * M[k] for k in range(d + 1))
+                    + 16 * N[d] + sum(108 * M[k - 1] for k in range(1, d + 1)))
+        if tag.startswith("conv"):
+            n = self._n_out(L)
+            return 2 * n * L.ksize ** 3 * L.cin * L.cout
+        l, c = L.depth, L.cin
+        if tag == "pool_fwd":
+            return N[l] * c * 4 + N[l - 1] * 4 + N[l - 1] * c * 4 + M[l - 1] * c
+        if tag == "pool_bwd":
+            return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l] * c * 4
+        return 0
+
+    # --- one step ----------------------------------------------------------
+    def _run(self, tag, L, fn):
+        if self.events is not None and tag in self.traced:
+            torch = self.torch
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            r = fn()
+            b.record()
+            self.events.setdefault(tag, []).append((a, b, L))
+            return r
+        return fn()
+
+    def __call__(self):
+        oc, wl = self.oc, self.wl
+        tree = self._run("build", None, lambda: oc.oc_build(self.pts, self.nrm, self.offs,
+                                                            wl.depth, wl.full_depth))
+        x = tree.signal() if wl.signal_input else self.x0
+        saved = []
+        for li, L in enumerate(wl.layers):
+            if L.op == "conv":
+                w = self.weights[li]
+                y = self._run("conv_fwd", L, lambda: oc.oc_conv_fwd(
+                    tree, L.depth, L.ksize, L.stride, x, w, relu=L.relu))
+                saved.append((li, x, y, None))
+                x = y
+            elif L.op == "pool":
+                p, sw = self._run("pool_fwd", L, lambda: oc.oc_pool_fwd(tree, L.depth, x))
+                saved.append((li, x, p, sw))
+                x = p
+        g = self.dy_last
+        for li, xin, yout, sw in reversed(saved):
+            L = wl.layers[li]
+            if L.op == "conv":
+                w = self.weights[li]
+                dx, _ = self._run("conv_bwd_data", L, lambda: oc.oc_conv_bwd(
+                    tree, L.depth, L.ksize, L.stride, xin, w, g, y=yout, relu=L.relu,
+                    need_dx=True, need_dw=False))
+                _, dw = self._run("conv_bwd_weight", L, lambda: oc.oc_conv_bwd(
+                    tree, L.depth, L.ksize, L.stride, xin, w, g, y=yout, relu=L.relu,
+                    need_dx=False, need_dw=True))
+                g = dx
+            elif L.op == "pool":
+                g = self._run("pool_bwd", L, lambda: oc.oc_pool_bwd(tree, L.depth, g, sw))
+        tree.free()
+        return g
+
+    def collect(self):
+        """Per-class (total ms, launches, total work) of the recorded events."""
+        out = {}
+        for tag, lst in (self.events or {}).items():
+            ms = sum(a.elapsed_time(b) for a, b, _ in lst)
+            work = sum(self.work(tag, L) for _, _, L in lst)
+            out[tag] = {"ms": ms, "launches": len(lst), "work": work, "per_layer": [
+                (f"d{L.depth}" if L is not None else "-", a.elapsed_time(b)) for a, b, L in lst]}
+        return out
+
+
+def cpu_baseline(synth, wl, shapes):
+    """The oracle on the first `shapes` shapes of the batch: build, neighbour
+    search and the network's forward and backward, timed on the host."""
+    import numpy as np
+
+    import oracle
+
+    pts, nrm, offs = synth.make_points(wl, batch=shapes)
+    t0 = time.perf_counter()
+    ref = oracle.Octree(pts, nrm, offs, wl.depth, wl.full_depth)
+    x = ref.signal if wl.signal_input else synth.make_features(
+        [wl.seed_id, 3000], ref.num(wl.layers[0].depth), wl.layers[0].cin)
+    saved, flops = [], 0
+    for li, L in enumerate(wl.layers):
+        l = L.depth
+        if L.op == "conv":
+            nb = ref.neighbors(l, L.ksize, stride=L.stride)
+            w = synth.make_weights(wl, li, L.ksize, L.cin, L.cout)
+            pre = oracle.conv_fwd(nb, x, w)
+            if L.stride == 2:
+                pre = oracle.renew(ref.labels(l - 1), pre)
+            y = oracle.relu_fwd(pre) if L.relu else pre
+            saved.append((li, nb, x, w, pre))
+            flops += 6 * y.shape[0] * L.ksize ** 3 * L.cin * L.cout
+            x = y
+        elif L.op == "pool":
+            y, sw = oracle.pool_fwd(ref.labels(l - 1), x)
+            saved.append((li, None, x, sw, None))
+            x = y
+    g = synth.make_upstream(wl, len(wl.layers) - 1, x.shape[0], x.shape[1])
+    for li, nb, xin, w_or_sw, pre in reversed(saved):
+        L = wl.layers[li]
+        l = L.depth
+        if L.op == "conv":
+            ge = oracle.relu_bwd(pre, g) if L.relu else g
+            if L.stride == 2:
+                ge = oracle.renew_bwd(ref.labels(l - 1), ge, nb.shape[0])
+            oracle.conv_bwd_weight(nb, xin, ge, L.ksize ** 3)
+            g = oracle.conv_bwd_data(nb, ge, w_or_sw, xin.shape[0])
+        else:
+            g = oracle.pool_bwd(ref.labels(l - 1), g, w_or_sw, ref.num(l))
+    dt = time.perf_counter() - t0
+    return {"value": round(flops / dt / 1e9, 4), "unit": "GFLOP/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"first {shapes} of {wl.batch} shapes of the same workload, one step "
+                      f"(build, neighbour search, forward and backward; {flops / 1e9:.2f} GFLOP "
+                      f"in {dt:.2f} s, float64)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              f"(the path would shard by shape with one dW all-reduce per layer, not built)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_1712_01537_amd as oc
+    import synth
+
+    oc.load()  # raises if liboc.so is missing: there is no other implementation
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    wl = synth.WORKLOADS[args.workload]
+    print(f"[bench] workload {wl.name}: generating inputs", file=sys.stderr, flush=True)
+    step = Step(oc, torch, synth, wl)
+    flops, octants = step.conv_flops()
+    print(f"[bench] N_l = {step.N}, M_l = {step.M}", file=sys.stderr, flush=True)
+
+    # warmup, with every op class timed to find the dominant one
+    step.events, step.traced = {}, set(BOUND)
+    for _ in range(max(args.warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+    warm = step.collect()
+    dominant = max(warm, key=lambda k: warm[k]["ms"])
+    print(f"[bench] warmup done; dominant op class: {dominant}", file=sys.stderr, flush=True)
+
+    # timed region: K steps; events bracket only the dominant class
+    step.events, step.traced = {}, {dominant}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+    dom = step.collect()[dominant]
+    print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+
+    per_launch_ms = dom["ms"] / dom["launches"]
+    per_launch_work = dom["work"] / dom["launches"]
+    if BOUND[dominant] == "mfma":
+        achieved = per_launch_work / (per_launch_ms * 1e-3) / 1e12
+        peak, unit = PEAK["fp32_TFLOPs"], "TFLOP/s"
+    else:
+        achieved = per_launch_work / (per_launch_ms * 1e-3) / 1e9
+        peak, unit = PEAK["hbm_GBps"], "GB/s"
+    roofline = {"bound": BOUND[dominant], "kernel": dominant, "achieved": round(achieved, 3),
+                "peak": peak, "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                "launches_per_step": dom["launches"] // args.steps,
+                "mean_launch_us": round(per_launch_ms * 1e3, 2)}
+
+    if args.layers:
+        for tag, v in sorted(warm.items(), key=lambda kv: -kv[1]["ms"]):
+            per = {}
+            for name, t in v["per_layer"]:
+                per[name] = per.get(name, 0.0) + t / max(args.warmup, 1)
+            print(f"[bench] {tag:16s} {v['ms'] / max(args.warmup, 1):8.3f} ms/step  "
+                  + "  ".join(f"{k}:{t:.3f}" for k, t in per.items()), file=sys.stderr)
+
+    cpu = None
+    if args.cpu_shapes > 0:
+        print(f"[bench] cpu oracle on {args.cpu_shapes} shapes", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(synth, wl, min(args.cpu_shapes, wl.batch))
+
+    line = {
+        "metric": "octree-conv fwd+bwd GFLOP/s & octants/s per layer; % HBM/MFMA roofline",
+        "value": round(flops / (ms * 1e-3) / 1e9, 3),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if all(L.dtype == "f32" for L in wl.layers) else "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "description": WORKLOAD_TEXT.get(wl.name, ""),
+            "batch": wl.batch,
+            "depth": wl.depth,
+            "points": step.npoints,
+            "octants_per_depth": step.N,
+            "nonempty_per_depth": step.M,
+            "conv_gflop_per_step": round(flops / 1e9, 4),
+        },
+        "octants_per_s": round(octants / (ms * 1e-3), 1),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+WORKLOAD_TEXT = {
+    "net_d6": "32 shapes (unions of 1-4 spheres/boxes, 20k surface points each), depth-6 "
+              "octree built on the GPU each step; conv3+ReLU+maxpool 3->16 @d6, 16->32 @d5, "
+              "32->64 @d4, 64->128 @d3, conv3+ReLU 128->256 @d2; fp32 forward and backward",
+    "net_d5": "32 shapes, depth 5; conv3 3->32 @d5 + pool, 32->64 @d4 + pool, 64->128 @d3 + "
+              "pool, 128->256 @d2; fp32 forward and backward",
+    "sphere_d5": "one sphere, 20k points, depth 5; conv3 3->32 + pool; fp32 fwd+bwd",
+    "deep_d8": "8 shapes, 100k points each, depth 8; conv3 16->16 @d8, pool, unpool; fp32",
+    "wide_d7": "16 shapes, 100k points each, depth 7; conv5 64->64 and stride-2 conv3 "
+               "64->128, bf16 inputs with fp32 accumulation",
+}
+
+
+if __name__ == "__main__":
+    main()

@@ -62,10 +62,17 @@ def lib():
             f = getattr(L, name)
             f.argtypes = args
             f.restype = C.c_int
+        L.ocref_num_threads.argtypes = []
+        L.ocref_num_threads.restype = C.c_int
         L.ocref_free.argtypes = [p]
         L.ocref_free.restype = None
         _lib = L
     return _lib
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(lib().ocref_num_threads())
 
 
 def _ptr(a):

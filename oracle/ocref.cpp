@@ -28,6 +28,8 @@
 // torch conv3d / max_pool3d / max_unpool3d in float64, autograd, finite
 // differences and the adjoint identity.
 
+#include <omp.h>
+
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
@@ -443,6 +445,9 @@ int ocref_unpool_bwd(const int32_t* labels, int64_t n_lm1, const double* dy, con
     }
   return OK;
 }
+
+// Threads the OpenMP loops above use (reported beside CPU timings).
+int ocref_num_threads(void) { return omp_get_max_threads(); }
 
 // ReLU (Sec. 4): y = max(0, x); backward dx = dy * [x > 0].
 int ocref_relu_fwd(const double* x, int64_t n, double* y) {

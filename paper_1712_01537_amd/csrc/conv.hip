@@ -21,6 +21,7 @@
 #include <algorithm>
 
 #include "common.h"
+#include "conv_mfma.h"
 
 namespace {
 
@@ -238,6 +239,11 @@ oc_status oc_conv_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   if (!x || !w || !y) return oc::fail(OC_ERR_ARG, "oc_conv_fwd: NULL buffer");
   if (sh.n_out == 0) return OC_OK;
   const int relu = (flags & OC_FUSE_RELU) ? 1 : 0;
+  if (dt == OC_F32 && stride == 1) {
+    oc::conv_s1_fwd_f32(t, l, K, (const float*)x, cin, (const float*)w, cout, y, relu, s);
+    OC_LAUNCH_CHECK();
+    return OC_OK;
+  }
   const unsigned grid = grid_for(sh.n_out * cout);
   if (dt == OC_F32)
     hipLaunchKernelGGL(k_conv_fwd_simple<float>, dim3(grid), dim3(TB), 0, s,
@@ -257,6 +263,7 @@ size_t oc_conv_bwd_workspace(const oc_octree* t, int32_t l, int32_t K, int32_t s
   if (check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_bwd_workspace") != OC_OK) return 0;
   int nparts;
   dw_chunk(sh, cin, cout, &nparts);
+  if (dt == OC_F32 && stride == 1) nparts = (int)oc::conv_s1_dw_parts(t, l, K, cin, cout);
   return (size_t)nparts * sh.K3 * cin * cout * sizeof(float);
 }
 
@@ -273,6 +280,8 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   const float* ym = (flags & OC_FUSE_RELU) ? y : nullptr;
   int nparts = 0;
   const int64_t chunk = dw_chunk(sh, cin, cout, &nparts);
+  const bool mfma = dt == OC_F32 && stride == 1;
+  if (mfma) nparts = (int)oc::conv_s1_dw_parts(t, l, K, cin, cout);
   const int64_t entries = (int64_t)sh.K3 * cin * cout;
   if (dw && ws_bytes < (size_t)nparts * entries * sizeof(float))
     return oc::fail(OC_ERR_ARG, "oc_conv_bwd: workspace %zu bytes < %zu", ws_bytes,
@@ -280,7 +289,9 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   if (dw && !ws) return oc::fail(OC_ERR_ARG, "oc_conv_bwd: NULL workspace");
   const int32_t* nbr = t->nbr[l];
   const int32_t* rows_out = t->rows[l - 1];
-  if (dx && sh.n_in > 0) {
+  if (dx && sh.n_in > 0 && mfma) {
+    oc::conv_s1_bwd_data_f32(t, l, K, dy, ym, cout, (const float*)w, cin, dx, s);
+  } else if (dx && sh.n_in > 0) {
     const unsigned grid = grid_for(sh.n_in * cin);
     if (stride == 1) {
       if (dt == OC_F32)
@@ -301,6 +312,8 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   if (dw) {
     if (sh.units == 0) {
       oc::fill_u32(dw, 0u, entries, s);
+    } else if (mfma) {
+      oc::conv_s1_bwd_weight_f32(t, l, K, (const float*)x, cin, dy, ym, cout, dw, (float*)ws, s);
     } else {
       float* part = (float*)ws;
       dim3 grid(grid_for(entries), nparts);

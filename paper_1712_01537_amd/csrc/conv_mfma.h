@@ -1,0 +1,27 @@
+// Launchers of the fp32 matrix-core convolution kernels (conv_mfma.hip).
+#pragma once
+
+#include "common.h"
+
+namespace oc {
+
+// y [N_l][cout] = conv(x [N_l][cin], w [K^3][cin][cout]), stride 1; relu != 0
+// applies max(0, .) to the output.
+void conv_s1_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin, const float* w,
+                     int cout, float* y, int relu, hipStream_t s);
+
+// dx [N_l][cin] = input gradient of a stride-1 convolution for upstream
+// gradient dy [N_l][cout]; ymask (nullable) masks dy with [ymask > 0].
+void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, const float* ymask,
+                          int cout, const float* w, int cin, float* dx, hipStream_t s);
+
+// Number of [K^3][cin][cout] fp32 partial sums conv_s1_bwd_weight_f32 needs.
+size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout);
+
+// dw [K^3][cin][cout] = weight gradient of a stride-1 convolution; part holds
+// conv_s1_dw_parts() partial sums.
+void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, int cin,
+                            const float* dy, const float* ymask, int cout, float* dw, float* part,
+                            hipStream_t s);
+
+}  // namespace oc
