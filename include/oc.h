@@ -145,11 +145,18 @@ void oc_octree_free(oc_octree* tree);
  *           values held as uint16); products accumulate in fp32.
  *   x       dev [N_l][cin].      w  dev [K^3][cin][cout].
  *   y       dev f32 [N_out][cout], N_out = N_l (stride 1) or N_{l-1}.
+ *   ws      dev workspace of at least oc_conv_fwd_workspace() bytes (may be
+ *           NULL when that is 0): partial sums of a reduction split across
+ *           workgroups, added in a fixed order (results are reproducible).
  *   flags   0 or OC_FUSE_RELU.
  * cin, cout in 1..1024. */
 oc_status oc_conv_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
                       oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
-                      float* y, int32_t flags, hipStream_t stream);
+                      float* y, void* ws, size_t ws_bytes, int32_t flags, hipStream_t stream);
+
+/* Bytes of device workspace oc_conv_fwd needs for these arguments. */
+size_t oc_conv_fwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                             oc_dtype dt, int32_t cin, int32_t cout);
 
 /* Bytes of device workspace oc_conv_bwd needs for these arguments. */
 size_t oc_conv_bwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,

@@ -42,7 +42,7 @@ STATUS = {0: "OC_OK", 1: "OC_ERR_ARG", 2: "OC_ERR_RANGE", 3: "OC_ERR_NOMEM", 4: 
 # Every symbol include/oc.h declares.
 EXPORTS = (
     "oc_build", "oc_octree_level", "oc_octree_info", "oc_octree_signal", "oc_octree_free",
-    "oc_conv_fwd", "oc_conv_bwd_workspace", "oc_conv_bwd", "oc_pool_fwd", "oc_pool_bwd",
+    "oc_conv_fwd", "oc_conv_fwd_workspace", "oc_conv_bwd_workspace", "oc_conv_bwd", "oc_pool_fwd", "oc_pool_bwd",
     "oc_unpool_fwd", "oc_unpool_bwd", "oc_status_str", "oc_last_error",
 )
 
@@ -117,7 +117,8 @@ def load():
         "oc_octree_info": ([p, p, p, p], C.c_int),
         "oc_octree_signal": ([p], p),
         "oc_octree_free": ([p], None),
-        "oc_conv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, i32, p], C.c_int),
+        "oc_conv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, sz, i32, p], C.c_int),
+        "oc_conv_fwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
         "oc_conv_bwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
         "oc_conv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, p, sz, i32, p],
                         C.c_int),
@@ -265,9 +266,13 @@ def oc_conv_fwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tens
         raise OcError(1, "x and w must share a dtype")
     if y is None:
         y = torch.empty((n_out, cout), dtype=torch.float32, device=x.device)
-    _check(load().oc_conv_fwd(tree.handle, depth, ksize, stride, dt, _dev(x, "x"), cin,
-                              _dev(w, "w"), cout, _dev(y, "y", torch.float32, (n_out, cout)),
-                              OC_FUSE_RELU if relu else 0, _stream()))
+    L = load()
+    ws_bytes = int(L.oc_conv_fwd_workspace(tree.handle, depth, ksize, stride, dt, cin, cout))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device) if ws_bytes else None
+    _check(L.oc_conv_fwd(tree.handle, depth, ksize, stride, dt, _dev(x, "x"), cin,
+                         _dev(w, "w"), cout, _dev(y, "y", torch.float32, (n_out, cout)),
+                         _dev(ws, "ws") if ws is not None else None, ws_bytes,
+                         OC_FUSE_RELU if relu else 0, _stream()))
     return y
 
 

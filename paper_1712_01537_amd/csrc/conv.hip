@@ -226,21 +226,54 @@ int64_t dw_chunk(const ConvShape& sh, int cin, int cout, int* nparts) {
   return chunk;
 }
 
+// Workspace bytes of each part of a convolution call.
+size_t fwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,
+                    int cout) {
+  if (dt == OC_F32 && sh.stride == 1 && sh.n_in > 0) return oc::conv_s1_tile_ws(t, l, sh.K, cin, cout);
+  return 0;
+}
+
+size_t bwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,
+                    int cout) {
+  if (sh.units == 0) return 0;
+  const size_t entries = (size_t)sh.K3 * cin * cout;
+  if (dt == OC_F32 && sh.stride == 1) {
+    // input gradient, then weight gradient: the same bytes serve both in stream order
+    const size_t a = oc::conv_s1_tile_ws(t, l, sh.K, cout, cin);
+    const size_t b = oc::conv_s1_dw_parts(t, l, sh.K, cin, cout) * entries * sizeof(float);
+    return std::max(a, b);
+  }
+  int nparts;
+  dw_chunk(sh, cin, cout, &nparts);
+  return (size_t)nparts * entries * sizeof(float);
+}
+
 }  // namespace
 
 extern "C" {
 
+size_t oc_conv_fwd_workspace(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,
+                             int32_t cin, int32_t cout) {
+  ConvShape sh;
+  if (check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_fwd_workspace") != OC_OK) return 0;
+  return fwd_ws_bytes(t, l, sh, dt, cin, cout);
+}
+
 oc_status oc_conv_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,
                       const void* x, int32_t cin, const void* w, int32_t cout, float* y,
-                      int32_t flags, hipStream_t s) {
+                      void* ws, size_t ws_bytes, int32_t flags, hipStream_t s) {
   ConvShape sh;
   oc_status st = check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_fwd");
   if (st != OC_OK) return st;
   if (!x || !w || !y) return oc::fail(OC_ERR_ARG, "oc_conv_fwd: NULL buffer");
   if (sh.n_out == 0) return OC_OK;
+  const size_t need = fwd_ws_bytes(t, l, sh, dt, cin, cout);
+  if (need && (!ws || ws_bytes < need))
+    return oc::fail(OC_ERR_ARG, "oc_conv_fwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0, need);
   const int relu = (flags & OC_FUSE_RELU) ? 1 : 0;
   if (dt == OC_F32 && stride == 1) {
-    oc::conv_s1_fwd_f32(t, l, K, (const float*)x, cin, (const float*)w, cout, y, relu, s);
+    oc::conv_s1_fwd_f32(t, l, K, (const float*)x, cin, (const float*)w, cout, y, relu, (float*)ws,
+                        s);
     OC_LAUNCH_CHECK();
     return OC_OK;
   }
@@ -261,10 +294,7 @@ size_t oc_conv_bwd_workspace(const oc_octree* t, int32_t l, int32_t K, int32_t s
                              int32_t cin, int32_t cout) {
   ConvShape sh;
   if (check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_bwd_workspace") != OC_OK) return 0;
-  int nparts;
-  dw_chunk(sh, cin, cout, &nparts);
-  if (dt == OC_F32 && stride == 1) nparts = (int)oc::conv_s1_dw_parts(t, l, K, cin, cout);
-  return (size_t)nparts * sh.K3 * cin * cout * sizeof(float);
+  return bwd_ws_bytes(t, l, sh, dt, cin, cout);
 }
 
 oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,
@@ -277,20 +307,18 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   if (!w || !dy) return oc::fail(OC_ERR_ARG, "oc_conv_bwd: NULL w or dy");
   if ((flags & OC_FUSE_RELU) && !y) return oc::fail(OC_ERR_ARG, "oc_conv_bwd: OC_FUSE_RELU needs y");
   if (dw && !x) return oc::fail(OC_ERR_ARG, "oc_conv_bwd: dw needs x");
+  const size_t need = (dx || dw) ? bwd_ws_bytes(t, l, sh, dt, cin, cout) : 0;
+  if (need && (!ws || ws_bytes < need))
+    return oc::fail(OC_ERR_ARG, "oc_conv_bwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0, need);
   const float* ym = (flags & OC_FUSE_RELU) ? y : nullptr;
   int nparts = 0;
   const int64_t chunk = dw_chunk(sh, cin, cout, &nparts);
   const bool mfma = dt == OC_F32 && stride == 1;
-  if (mfma) nparts = (int)oc::conv_s1_dw_parts(t, l, K, cin, cout);
   const int64_t entries = (int64_t)sh.K3 * cin * cout;
-  if (dw && ws_bytes < (size_t)nparts * entries * sizeof(float))
-    return oc::fail(OC_ERR_ARG, "oc_conv_bwd: workspace %zu bytes < %zu", ws_bytes,
-                    (size_t)nparts * entries * sizeof(float));
-  if (dw && !ws) return oc::fail(OC_ERR_ARG, "oc_conv_bwd: NULL workspace");
   const int32_t* nbr = t->nbr[l];
   const int32_t* rows_out = t->rows[l - 1];
   if (dx && sh.n_in > 0 && mfma) {
-    oc::conv_s1_bwd_data_f32(t, l, K, dy, ym, cout, (const float*)w, cin, dx, s);
+    oc::conv_s1_bwd_data_f32(t, l, K, dy, ym, cout, (const float*)w, cin, dx, (float*)ws, s);
   } else if (dx && sh.n_in > 0) {
     const unsigned grid = grid_for(sh.n_in * cin);
     if (stride == 1) {

@@ -5,15 +5,21 @@
 
 namespace oc {
 
+// Bytes of split-reduction workspace the stride-1 group-tile kernel needs for
+// kk reduction channels and nn output channels at depth l (0: none).
+size_t conv_s1_tile_ws(const oc_octree* t, int l, int K, int kk, int nn);
+
 // y [N_l][cout] = conv(x [N_l][cin], w [K^3][cin][cout]), stride 1; relu != 0
-// applies max(0, .) to the output.
+// applies max(0, .) to the output.  ws: conv_s1_tile_ws(t, l, K, cin, cout)
+// bytes.
 void conv_s1_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin, const float* w,
-                     int cout, float* y, int relu, hipStream_t s);
+                     int cout, float* y, int relu, float* ws, hipStream_t s);
 
 // dx [N_l][cin] = input gradient of a stride-1 convolution for upstream
 // gradient dy [N_l][cout]; ymask (nullable) masks dy with [ymask > 0].
+// ws: conv_s1_tile_ws(t, l, K, cout, cin) bytes.
 void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, const float* ymask,
-                          int cout, const float* w, int cin, float* dx, hipStream_t s);
+                          int cout, const float* w, int cin, float* dx, float* ws, hipStream_t s);
 
 // Number of [K^3][cin][cout] fp32 partial sums conv_s1_bwd_weight_f32 needs.
 size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout);

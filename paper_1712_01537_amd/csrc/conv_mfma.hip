@@ -55,37 +55,56 @@ __device__ __forceinline__ int32_t tile_src(const int32_t* __restrict__ nb, int 
 // ---------------------------------------------------------------------------
 // Stride-1 implicit GEMM over group tiles.
 //   K   kernel size (3 or 5);  V  channels per lane per LDS read (1 or 4);
-//   MR  16-row blocks per wave (2 MR groups);  NR  16-column blocks per wave;
-//   FLIP  false: forward, W[k][c][n] at (k*kk + c)*nn + n;
-//         true : input gradient, W'[k][c][n] = W[K3-1-k][n][c].
-// Grid: x = ceil(groups / (WAVES*2*MR)), y = ceil(nn / (16*NR)).
-template <int K, int V, int MR, int NR, bool FLIP>
+//   MR, NR  16-row / 16-column MFMA blocks per wave;  WM  waves along rows
+//   (WAVES / WM along columns);  FLIP  false: forward, W[k][c][n] at
+//   (k*kk + c)*nn + n;  true: input gradient, W'[k][c][n] = W[K3-1-k][n][c].
+// A workgroup computes BM = 16 WM MR rows (BM / 8 sibling groups) by
+// BN = 16 (WAVES/WM) NR columns.  Per chunk of CC reduction channels it
+// gathers the groups' (K+1)^3 tiles into LDS, then walks the taps in slabs
+// of TSL taps, staging each slab's weights as Bt[tap][n][c] so that a lane
+// reads its V channels with one LDS load.  Group tiles are stored with two
+// padding rows per x-slab and rows of RS = CC + 4 floats, which puts the
+// eight children of a group (and 16 consecutive weight columns) on distinct
+// LDS banks.
+// Grid: x = ceil(groups / (BM/8)), y = ceil(nn / BN), z = splits of the
+// reduction channels, cps chunks each.  With one split the result (ReLU
+// applied if relu) goes to out; otherwise split z writes its partial sum to
+// part[z][row][n] and k_sum_split finishes.
+template <int K, int V, int MR, int NR, int WM, bool FLIP>
 __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nbr, int64_t ngroups,
                                                   const float* __restrict__ x,
                                                   const float* __restrict__ xmask, int kk,
                                                   const float* __restrict__ w, int nn,
-                                                  float* __restrict__ out, int relu) {
-  constexpr int R = (K - 1) / 2, S = K + 1, P3 = S * S * S, K3 = K * K * K;
-  constexpr int CC = 4 * V;                  // channels per LDS fill
-  constexpr int CCP = V == 4 ? CC + 4 : CC;  // padded tile row (floats)
-  constexpr int GPW = 2 * MR;                // groups per wave
-  constexpr int GPB = GPW * WAVES;           // groups per workgroup
-  __shared__ __attribute__((aligned(16))) float tile[GPB * P3 * CCP];
+                                                  float* __restrict__ out, int relu, int cps,
+                                                  float* __restrict__ part) {
+  constexpr int WN = WAVES / WM;
+  constexpr int R = (K - 1) / 2, S = K + 1, K2 = K * K, K3 = K2 * K, S3 = S * S * S;
+  constexpr int PX = S * S + 2;  // tile rows per x-slab (two padding rows)
+  constexpr int P3 = S * PX;     // tile rows per group
+  constexpr int CC = 4 * V;
+  constexpr int RS = V == 4 ? CC + 4 : CC;
+  constexpr int BM = WM * MR * 16, BN = WN * NR * 16, GPB = BM / 8;
+  constexpr int TSL = (V == 1 && K == 3) ? K3 : K2;  // taps per weight slab
+  __shared__ __attribute__((aligned(16))) float At[GPB * P3 * RS];
+  __shared__ __attribute__((aligned(16))) float Bt[TSL * BN * RS];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int li = lane & 15, q = lane >> 4;
+  const int wm = wave % WM, wn = wave / WM;
   const int64_t g0 = (int64_t)blockIdx.x * GPB;
-  const int n0 = blockIdx.y * (16 * NR);
+  const int n0 = blockIdx.y * BN;
+  const int cb = blockIdx.z * cps * CC;
+  const int ce = cb + cps * CC < kk ? cb + cps * CC : kk;
 
-  // this lane's output child (row of A) within each of its row blocks
   const int c = li & 7;
   const int cx = c >> 2, cy = (c >> 1) & 1, cz = c & 1;
-  int tbase[MR];  // tile row of this lane's child at tap offset -R (all axes)
+  int tbase[MR];  // tile row of this lane's child at tap offset -R on every axis
 #pragma unroll
-  for (int mr = 0; mr < MR; ++mr) {
-    const int gl = wave * GPW + 2 * mr + (li >> 3);
-    tbase[mr] = gl * P3 + (cx * S + cy) * S + cz;
-  }
+  for (int mr = 0; mr < MR; ++mr)
+    tbase[mr] = ((wm * MR + mr) * 2 + (li >> 3)) * P3 + cx * PX + cy * S + cz;
+  int bcol[NR];  // this lane's column within the workgroup's BN
+#pragma unroll
+  for (int nr = 0; nr < NR; ++nr) bcol[nr] = (wn * NR + nr) * 16 + li;
 
   v4f acc[MR][NR];
 #pragma unroll
@@ -93,17 +112,18 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
 #pragma unroll
     for (int nr = 0; nr < NR; ++nr) acc[mr][nr] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  for (int c0 = 0; c0 < kk; c0 += CC) {
+  for (int c0 = cb; c0 < ce; c0 += CC) {
     __syncthreads();
-    // gather the tiles of this channel chunk: one thread per (row, 4 channels)
+    // gather the group tiles of this channel chunk: one thread per (position, 4 channels)
     constexpr int F4 = CC / 4;
-    for (int e = tid; e < GPB * P3 * F4; e += TB) {
-      const int row = e / F4, f = e - row * F4;
-      const int gl = row / P3, p = row - gl * P3;
+    for (int e = tid; e < GPB * S3 * F4; e += TB) {
+      const int rp = e / F4, f = e - rp * F4;
+      const int gl = rp / S3, p = rp - gl * S3;
+      const int px = p / (S * S), py = (p / S) % S, pz = p % S;
       const int64_t g = g0 + gl;
       v4f v = {0.f, 0.f, 0.f, 0.f};
       if (g < ngroups) {
-        const int32_t src = tile_src<R>(nbr + 27 * g, p / (S * S), (p / S) % S, p % S);
+        const int32_t src = tile_src<R>(nbr + 27 * g, px, py, pz);
         if (src >= 0) {
           const int ch = c0 + 4 * f;
           const float* xr = x + (int64_t)src * kk;
@@ -125,77 +145,108 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
           }
         }
       }
-      *reinterpret_cast<v4f*>(&tile[row * CCP + 4 * f]) = v;
+      *reinterpret_cast<v4f*>(&At[(gl * P3 + px * PX + py * S + pz) * RS + 4 * f]) = v;
     }
-    __syncthreads();
 
-    // B operand of tap k: reduction channel c0 + V q + s, column n0 + 16 nr + li
-    auto load_b = [&](int k, float (&b)[NR][V]) {
+    for (int k0 = 0; k0 < K3; k0 += TSL) {
+      if (k0 > 0) __syncthreads();  // previous slab consumed
+      // stage the weights of taps k0 .. k0+TSL-1 as Bt[t][n][c]
+      if constexpr (FLIP) {
+        for (int e = tid; e < TSL * BN * F4; e += TB) {
+          const int f = e % F4, tn = e / F4, n = tn % BN, t = tn / BN;
+          const int gn = n0 + n, ch = c0 + 4 * f;
+          v4f v = {0.f, 0.f, 0.f, 0.f};
+          if (gn < nn) {
+            const float* wr = w + ((int64_t)(K3 - 1 - (k0 + t)) * nn + gn) * kk;
+            if (ch + 4 <= kk && (kk & 3) == 0) {
+              v = *reinterpret_cast<const v4f*>(wr + ch);
+            } else {
 #pragma unroll
-      for (int nr = 0; nr < NR; ++nr) {
-        const int n = n0 + 16 * nr + li;
-#pragma unroll
-        for (int s = 0; s < V; ++s) {
-          const int ch = c0 + V * q + s;
+              for (int j = 0; j < 4; ++j)
+                if (ch + j < kk) v[j] = wr[ch + j];
+            }
+          }
+          *reinterpret_cast<v4f*>(&Bt[(t * BN + n) * RS + 4 * f]) = v;
+        }
+      } else {
+        for (int e = tid; e < TSL * CC * BN; e += TB) {
+          const int n = e % BN, tc = e / BN, cc = tc % CC, t = tc / CC;
+          const int gn = n0 + n, ch = c0 + cc;
           float v = 0.f;
-          if (n < nn && ch < kk)
-            v = FLIP ? w[((int64_t)(K3 - 1 - k) * nn + n) * kk + ch]
-                     : w[((int64_t)k * kk + ch) * nn + n];
-          b[nr][s] = v;
+          if (gn < nn && ch < kk) v = w[((int64_t)(k0 + t) * kk + ch) * nn + gn];
+          Bt[(t * BN + n) * RS + cc] = v;
         }
       }
-    };
-    float bc[NR][V], bn[NR][V];
-    load_b(0, bc);
-#pragma unroll 1
-    for (int k = 0; k < K3; ++k) {
-      if (k + 1 < K3) load_b(k + 1, bn);
-      const int dx = k / (K * K), dy = (k / K) % K, dz = k % K;  // tap offset + R
-      const int toff = (dx * S + dy) * S + dz;
-      float a[MR][V];
+      __syncthreads();
+
+#pragma unroll 3
+      for (int t = 0; t < TSL; ++t) {
+        const int k = k0 + t;
+        const int toff = (k / K2) * PX + ((k / K) % K) * S + k % K;
+        float a[MR][V], b[NR][V];
 #pragma unroll
-      for (int mr = 0; mr < MR; ++mr) {
-        const float* tp = &tile[(tbase[mr] + toff) * CCP + V * q];
-        if constexpr (V == 4) {
-          const v4f t = *reinterpret_cast<const v4f*>(tp);
+        for (int mr = 0; mr < MR; ++mr) {
+          const float* tp = &At[(tbase[mr] + toff) * RS + V * q];
+          if constexpr (V == 4) {
+            const v4f u = *reinterpret_cast<const v4f*>(tp);
 #pragma unroll
-          for (int s = 0; s < 4; ++s) a[mr][s] = t[s];
-        } else {
-          a[mr][0] = tp[0];
+            for (int j = 0; j < 4; ++j) a[mr][j] = u[j];
+          } else {
+            a[mr][0] = tp[0];
+          }
         }
+#pragma unroll
+        for (int nr = 0; nr < NR; ++nr) {
+          const float* bp = &Bt[(t * BN + bcol[nr]) * RS + V * q];
+          if constexpr (V == 4) {
+            const v4f u = *reinterpret_cast<const v4f*>(bp);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) b[nr][j] = u[j];
+          } else {
+            b[nr][0] = bp[0];
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < V; ++j)
+#pragma unroll
+          for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+            for (int nr = 0; nr < NR; ++nr) acc[mr][nr] = mfma4(a[mr][j], b[nr][j], acc[mr][nr]);
       }
-#pragma unroll
-      for (int s = 0; s < V; ++s)
-#pragma unroll
-        for (int mr = 0; mr < MR; ++mr)
-#pragma unroll
-          for (int nr = 0; nr < NR; ++nr) acc[mr][nr] = mfma4(a[mr][s], bc[nr][s], acc[mr][nr]);
-#pragma unroll
-      for (int nr = 0; nr < NR; ++nr)
-#pragma unroll
-        for (int s = 0; s < V; ++s) bc[nr][s] = bn[nr][s];
     }
   }
 
   // epilogue: accumulator j of lane l is row 4(l/16)+j, column l%16
   const int64_t nrows = 8 * ngroups;
+  const bool split = gridDim.z > 1;
+  float* dst = split ? part + (int64_t)blockIdx.z * nrows * nn : out;
 #pragma unroll
   for (int mr = 0; mr < MR; ++mr) {
-    const int64_t rbase = 8 * (g0 + wave * GPW + 2 * mr) + 4 * q;
+    const int64_t rbase = 8 * g0 + (wm * MR + mr) * 16 + 4 * q;
 #pragma unroll
     for (int nr = 0; nr < NR; ++nr) {
-      const int n = n0 + 16 * nr + li;
+      const int n = n0 + bcol[nr];
       if (n >= nn) continue;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int64_t row = rbase + j;
         if (row < nrows) {
-          float v = acc[mr][nr][j];
-          out[row * nn + n] = relu ? fmaxf(v, 0.f) : v;
+          const float v = acc[mr][nr][j];
+          dst[row * nn + n] = (!split && relu) ? fmaxf(v, 0.f) : v;
         }
       }
     }
   }
+}
+
+// out[e] = sum over splits of part[z][e] (in split order), ReLU if relu.
+__global__ __launch_bounds__(TB) void k_sum_split(const float* __restrict__ part, int splits,
+                                                  int64_t n, float* __restrict__ out, int relu) {
+  const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (e >= n) return;
+  float s = 0.f;
+  for (int z = 0; z < splits; ++z) s += part[(int64_t)z * n + e];
+  out[e] = relu ? fmaxf(s, 0.f) : s;
 }
 
 // ---------------------------------------------------------------------------
@@ -322,39 +373,58 @@ __global__ __launch_bounds__(TB) void k_sum_parts(const float* __restrict__ part
 // Launch-shape selection.
 
 struct TileCfg {
-  int V, MR, NR;
+  int V, MR, NR, WM, splits, cps;
 };
 
-TileCfg pick_tile(int K, int kk, int nn) {
+// Workgroup tile and split of the reduction for a stride-1 layer of G groups.
+TileCfg pick_tile(int K, int64_t G, int kk, int nn) {
   TileCfg c;
   c.V = (K == 3 && kk >= 16) ? 4 : 1;
-  c.MR = 1;
-  c.NR = nn <= 16 ? 1 : nn <= 32 ? 2 : 4;
+  if (nn <= 16) {
+    c.WM = 4, c.MR = 1, c.NR = 1;  // 64 x 16
+  } else if (nn <= 32) {
+    c.WM = 2, c.MR = 2, c.NR = 1;  // 64 x 32
+  } else {
+    c.WM = 2, c.MR = 2, c.NR = 2;  // 64 x 64
+  }
+  const int BM = 16 * c.WM * c.MR, BN = 16 * (WAVES / c.WM) * c.NR;
+  const int64_t tiles = oc::cdiv(G, BM / 8) * oc::cdiv(nn, BN);
+  const int chunks = (int)oc::cdiv(kk, 4 * c.V);
+  int splits = 1;
+  while (tiles * splits < 512 && splits * 2 <= chunks) splits *= 2;
+  c.cps = (int)oc::cdiv(chunks, splits);
+  c.splits = (int)oc::cdiv(chunks, c.cps);
   return c;
 }
 
-template <int K, int V, int MR, int NR, bool FLIP>
-void launch_tile(const oc_octree* t, int l, const float* x, const float* xmask, int kk,
-                 const float* w, int nn, float* out, int relu, hipStream_t s) {
+template <int K, int V, int MR, int NR, int WM, bool FLIP>
+void launch_tile(const oc_octree* t, int l, const TileCfg& c, const float* x, const float* xmask,
+                 int kk, const float* w, int nn, float* out, int relu, float* part,
+                 hipStream_t s) {
   const int64_t G = t->M[l - 1];
-  constexpr int GPB = 2 * MR * WAVES;
-  dim3 grid((unsigned)oc::cdiv(G, GPB), (unsigned)oc::cdiv(nn, 16 * NR));
-  hipLaunchKernelGGL((k_conv_tile<K, V, MR, NR, FLIP>), grid, dim3(TB), 0, s,
-                     (const int32_t*)t->nbr[l], G, x, xmask, kk, w, nn, out, relu);
+  constexpr int BM = 16 * WM * MR, BN = 16 * (WAVES / WM) * NR;
+  dim3 grid((unsigned)oc::cdiv(G, BM / 8), (unsigned)oc::cdiv(nn, BN), (unsigned)c.splits);
+  hipLaunchKernelGGL((k_conv_tile<K, V, MR, NR, WM, FLIP>), grid, dim3(TB), 0, s,
+                     (const int32_t*)t->nbr[l], G, x, xmask, kk, w, nn, out, relu, c.cps, part);
+  if (c.splits > 1) {
+    const int64_t n = t->N[l] * (int64_t)nn;
+    hipLaunchKernelGGL(k_sum_split, dim3((unsigned)oc::cdiv(n, TB)), dim3(TB), 0, s,
+                       (const float*)part, c.splits, n, out, relu);
+  }
 }
 
 template <bool FLIP>
 void dispatch_tile(const oc_octree* t, int l, int K, const float* x, const float* xmask, int kk,
-                   const float* w, int nn, float* out, int relu, hipStream_t s) {
-  const TileCfg c = pick_tile(K, kk, nn);
-#define OC_TILE(K_, V_, NR_)                                                     \
-  if (K == K_ && c.V == V_ && c.NR == NR_) {                                     \
-    launch_tile<K_, V_, 1, NR_, FLIP>(t, l, x, xmask, kk, w, nn, out, relu, s); \
-    return;                                                                      \
+                   const float* w, int nn, float* out, int relu, float* part, hipStream_t s) {
+  const TileCfg c = pick_tile(K, t->M[l - 1], kk, nn);
+#define OC_TILE(K_, V_, MR_, NR_, WM_)                                                     \
+  if (K == K_ && c.V == V_ && c.MR == MR_ && c.NR == NR_ && c.WM == WM_) {                 \
+    launch_tile<K_, V_, MR_, NR_, WM_, FLIP>(t, l, c, x, xmask, kk, w, nn, out, relu, part, s); \
+    return;                                                                                \
   }
-  OC_TILE(3, 4, 1) OC_TILE(3, 4, 2) OC_TILE(3, 4, 4)
-  OC_TILE(3, 1, 1) OC_TILE(3, 1, 2) OC_TILE(3, 1, 4)
-  OC_TILE(5, 1, 1) OC_TILE(5, 1, 2) OC_TILE(5, 1, 4)
+  OC_TILE(3, 4, 1, 1, 4) OC_TILE(3, 4, 2, 1, 2) OC_TILE(3, 4, 2, 2, 2)
+  OC_TILE(3, 1, 1, 1, 4) OC_TILE(3, 1, 2, 1, 2) OC_TILE(3, 1, 2, 2, 2)
+  OC_TILE(5, 1, 1, 1, 4) OC_TILE(5, 1, 2, 1, 2) OC_TILE(5, 1, 2, 2, 2)
 #undef OC_TILE
 }
 
@@ -391,14 +461,19 @@ void launch_dw(const oc_octree* t, int l, const DwCfg& c, const float* x, int ci
 
 namespace oc {
 
+size_t conv_s1_tile_ws(const oc_octree* t, int l, int K, int kk, int nn) {
+  const TileCfg c = pick_tile(K, t->M[l - 1], kk, nn);
+  return c.splits > 1 ? (size_t)c.splits * t->N[l] * nn * sizeof(float) : 0;
+}
+
 void conv_s1_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin, const float* w,
-                     int cout, float* y, int relu, hipStream_t s) {
-  dispatch_tile<false>(t, l, K, x, nullptr, cin, w, cout, y, relu, s);
+                     int cout, float* y, int relu, float* ws, hipStream_t s) {
+  dispatch_tile<false>(t, l, K, x, nullptr, cin, w, cout, y, relu, ws, s);
 }
 
 void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, const float* ymask,
-                          int cout, const float* w, int cin, float* dx, hipStream_t s) {
-  dispatch_tile<true>(t, l, K, dy, ymask, cout, w, cin, dx, 0, s);
+                          int cout, const float* w, int cin, float* dx, float* ws, hipStream_t s) {
+  dispatch_tile<true>(t, l, K, dy, ymask, cout, w, cin, dx, 0, ws, s);
 }
 
 size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout) {

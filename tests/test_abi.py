@@ -41,7 +41,7 @@ def test_argument_errors_without_device():
     assert L.oc_build(None, None, bad, 2, 3, 2, None, None, C.byref(out)) == 1    # decreasing
     assert b"decrease" in L.oc_last_error()
     assert L.oc_build(None, None, (C.c_int32 * 2)(0, 4), 1, 3, 2, None, None, C.byref(out)) == 1
-    assert L.oc_conv_fwd(None, 1, 3, 1, 0, None, 3, None, 4, None, 0, None) == 1
+    assert L.oc_conv_fwd(None, 1, 3, 1, 0, None, 3, None, 4, None, None, 0, 0, None) == 1
     assert L.oc_pool_fwd(None, 1, None, 3, None, None, None) == 1
     assert L.oc_octree_signal(None) is None
     assert L.oc_status_str(2) == b"point outside the unit cube"
