@@ -82,11 +82,21 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
   constexpr int PX = S * S + 2;  // tile rows per x-slab (two padding rows)
   constexpr int P3 = S * PX;     // tile rows per group
   constexpr int CC = 4 * V;
+  constexpr int F4 = CC / 4;
   constexpr int RS = V == 4 ? CC + 4 : CC;
   constexpr int BM = WM * MR * 16, BN = WN * NR * 16, GPB = BM / 8;
   constexpr int TSL = (V == 1 && K == 3) ? K3 : K2;  // taps per weight slab
+  constexpr int NSL = K3 / TSL;                     // slabs per channel chunk
+  // Staging of the next step's global loads in registers.  Tile: each pass
+  // covers GPP groups, thread -> fixed (group of the pass, position, channel
+  // quad); NA passes.  Weight slab: (tap, column, channel quad) elements,
+  // float4 along the contiguous axis of W; NB passes.
+  constexpr int GPP = TB / (S3 * F4) > 0 ? TB / (S3 * F4) : 1;
+  constexpr int NA = GPB / GPP;
+  constexpr int NB = (TSL * BN * F4 + TB - 1) / TB;
   __shared__ __attribute__((aligned(16))) float At[GPB * P3 * RS];
   __shared__ __attribute__((aligned(16))) float Bt[TSL * BN * RS];
+  __shared__ int32_t Src[GPB * S3];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int li = lane & 15, q = lane >> 4;
@@ -95,6 +105,13 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
   const int n0 = blockIdx.y * BN;
   const int cb = blockIdx.z * cps * CC;
   const int ce = cb + cps * CC < kk ? cb + cps * CC : kk;
+
+  // source rows of every tile position of the workgroup's groups, once
+  for (int e = tid; e < GPB * S3; e += TB) {
+    const int gl = e / S3, p = e - gl * S3;
+    const int64_t g = g0 + gl;
+    Src[e] = g < ngroups ? tile_src<R>(nbr + 27 * g, p / (S * S), (p / S) % S, p % S) : -1;
+  }
 
   const int c = li & 7;
   const int cx = c >> 2, cy = (c >> 1) & 1, cz = c & 1;
@@ -112,73 +129,130 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
 #pragma unroll
     for (int nr = 0; nr < NR; ++nr) acc[mr][nr] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  for (int c0 = cb; c0 < ce; c0 += CC) {
-    __syncthreads();
-    // gather the group tiles of this channel chunk: one thread per (position, 4 channels)
-    constexpr int F4 = CC / 4;
-    for (int e = tid; e < GPB * S3 * F4; e += TB) {
-      const int rp = e / F4, f = e - rp * F4;
-      const int gl = rp / S3, p = rp - gl * S3;
-      const int px = p / (S * S), py = (p / S) % S, pz = p % S;
-      const int64_t g = g0 + gl;
-      v4f v = {0.f, 0.f, 0.f, 0.f};
-      if (g < ngroups) {
-        const int32_t src = tile_src<R>(nbr + 27 * g, px, py, pz);
-        if (src >= 0) {
-          const int ch = c0 + 4 * f;
-          const float* xr = x + (int64_t)src * kk;
-          if (ch + 4 <= kk && (kk & 3) == 0) {
-            v = *reinterpret_cast<const v4f*>(xr + ch);
-            if (xmask) {
-              const v4f m = *reinterpret_cast<const v4f*>(xmask + (int64_t)src * kk + ch);
+  // this thread's tile element: group a_g + GPP i, position a_p, channels 4 a_f..
+  const bool a_on = tid < GPP * S3 * F4;
+  const int a_g = tid / (S3 * F4), a_p = (tid / F4) % S3, a_f = tid % F4;
+  const int a_lds = (a_g * P3 + (a_p / (S * S)) * PX + ((a_p / S) % S) * S + a_p % S) * RS + 4 * a_f;
+  v4f ra[NA], rm[FLIP ? NA : 1];
+
+  // global -> registers: the tile of channel chunk c0 (mask values are kept
+  // apart so that no wait is needed before the compute that follows)
+  auto load_a = [&](int c0) {
+    const int ch = c0 + 4 * a_f;
 #pragma unroll
-              for (int j = 0; j < 4; ++j) v[j] = m[j] > 0.f ? v[j] : 0.f;
+    for (int i = 0; i < NA; ++i) {
+      const int32_t src = a_on ? Src[(a_g + GPP * i) * S3 + a_p] : -1;
+      v4f v = {0.f, 0.f, 0.f, 0.f}, m = {1.f, 1.f, 1.f, 1.f};
+      if (src >= 0 && ch < kk) {
+        const float* xr = x + (int64_t)src * kk + ch;
+        const float* xm = xmask ? xmask + (int64_t)src * kk + ch : nullptr;
+        if (ch + 4 <= kk && (kk & 3) == 0) {
+          v = *reinterpret_cast<const v4f*>(xr);
+          if (FLIP && xm) m = *reinterpret_cast<const v4f*>(xm);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (ch + j < kk) {
+              v[j] = xr[j];
+              if (FLIP && xm) m[j] = xm[j];
             }
-          } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-              if (ch + j < kk) {
-                float a = xr[ch + j];
-                if (xmask && !(xmask[(int64_t)src * kk + ch + j] > 0.f)) a = 0.f;
-                v[j] = a;
-              }
-          }
         }
       }
-      *reinterpret_cast<v4f*>(&At[(gl * P3 + px * PX + py * S + pz) * RS + 4 * f]) = v;
+      ra[i] = v;
+      if constexpr (FLIP) rm[i] = m;
     }
-
-    for (int k0 = 0; k0 < K3; k0 += TSL) {
-      if (k0 > 0) __syncthreads();  // previous slab consumed
-      // stage the weights of taps k0 .. k0+TSL-1 as Bt[t][n][c]
-      if constexpr (FLIP) {
-        for (int e = tid; e < TSL * BN * F4; e += TB) {
-          const int f = e % F4, tn = e / F4, n = tn % BN, t = tn / BN;
-          const int gn = n0 + n, ch = c0 + 4 * f;
-          v4f v = {0.f, 0.f, 0.f, 0.f};
-          if (gn < nn) {
-            const float* wr = w + ((int64_t)(K3 - 1 - (k0 + t)) * nn + gn) * kk;
-            if (ch + 4 <= kk && (kk & 3) == 0) {
-              v = *reinterpret_cast<const v4f*>(wr + ch);
-            } else {
+  };
+  auto store_a = [&]() {
+    if (!a_on) return;
 #pragma unroll
-              for (int j = 0; j < 4; ++j)
-                if (ch + j < kk) v[j] = wr[ch + j];
-            }
+    for (int i = 0; i < NA; ++i) {
+      v4f v = ra[i];
+      if constexpr (FLIP) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = rm[i][j] > 0.f ? v[j] : 0.f;
+      }
+      *reinterpret_cast<v4f*>(&At[a_lds + i * GPP * P3 * RS]) = v;
+    }
+  };
+
+  // weight slab element of this thread, pass i
+  float4 rb[NB];
+  auto load_b = [&](int c0, int k0) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int e = tid + i * TB;
+      float4 v = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (FLIP) {  // (t, n, f): 4 consecutive channels of W[K3-1-k][n]
+        const int f = e % F4, n = (e / F4) % BN, t = e / (F4 * BN);
+        const int gn = n0 + n, ch = c0 + 4 * f;
+        if (t < TSL && gn < nn && ch < kk) {
+          const float* wr = w + ((int64_t)(K3 - 1 - (k0 + t)) * nn + gn) * kk + ch;
+          if (ch + 4 <= kk && (kk & 3) == 0) {
+            v = *reinterpret_cast<const float4*>(wr);
+          } else {
+            v.x = wr[0];
+            if (ch + 1 < kk) v.y = wr[1];
+            if (ch + 2 < kk) v.z = wr[2];
+            if (ch + 3 < kk) v.w = wr[3];
           }
-          *reinterpret_cast<v4f*>(&Bt[(t * BN + n) * RS + 4 * f]) = v;
         }
-      } else {
-        for (int e = tid; e < TSL * CC * BN; e += TB) {
-          const int n = e % BN, tc = e / BN, cc = tc % CC, t = tc / CC;
-          const int gn = n0 + n, ch = c0 + cc;
-          float v = 0.f;
-          if (gn < nn && ch < kk) v = w[((int64_t)(k0 + t) * kk + ch) * nn + gn];
-          Bt[(t * BN + n) * RS + cc] = v;
+      } else {  // (t, cc, n4): 4 consecutive columns of W[k][ch]
+        const int n4 = e % (BN / 4), cc = (e / (BN / 4)) % CC, t = e / (BN / 4 * CC);
+        const int gn = n0 + 4 * n4, ch = c0 + cc;
+        if (t < TSL && ch < kk) {
+          const float* wr = w + ((int64_t)(k0 + t) * kk + ch) * nn + gn;
+          if (gn + 4 <= nn && (nn & 3) == 0) {
+            v = *reinterpret_cast<const float4*>(wr);
+          } else {
+            if (gn < nn) v.x = wr[0];
+            if (gn + 1 < nn) v.y = wr[1];
+            if (gn + 2 < nn) v.z = wr[2];
+            if (gn + 3 < nn) v.w = wr[3];
+          }
         }
       }
-      __syncthreads();
+      rb[i] = v;
+    }
+  };
+  auto store_b = [&]() {
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int e = tid + i * TB;
+      if constexpr (FLIP) {
+        const int f = e % F4, n = (e / F4) % BN, t = e / (F4 * BN);
+        if (t < TSL) *reinterpret_cast<float4*>(&Bt[(t * BN + n) * RS + 4 * f]) = rb[i];
+      } else {
+        const int n4 = e % (BN / 4), cc = (e / (BN / 4)) % CC, t = e / (BN / 4 * CC);
+        if (t < TSL) {
+          float* d = &Bt[(t * BN + 4 * n4) * RS + cc];
+          d[0] = rb[i].x;
+          d[RS] = rb[i].y;
+          d[2 * RS] = rb[i].z;
+          d[3 * RS] = rb[i].w;
+        }
+      }
+    }
+  };
 
+  __syncthreads();  // Src ready
+  if (cb < ce) {
+    load_a(cb);
+    load_b(cb, 0);
+  }
+  for (int c0 = cb; c0 < ce; c0 += CC) {
+    for (int sl = 0; sl < NSL; ++sl) {
+      const int k0 = sl * TSL;
+      __syncthreads();  // the previous step's LDS reads are done
+      if (sl == 0) store_a();
+      store_b();
+      __syncthreads();
+      // prefetch the next step while this one computes
+      if (sl + 1 < NSL) {
+        load_b(c0, k0 + TSL);
+      } else if (c0 + CC < ce) {
+        load_a(c0 + CC);
+        load_b(c0 + CC, 0);
+      }
 #pragma unroll 3
       for (int t = 0; t < TSL; ++t) {
         const int k = k0 + t;
@@ -250,123 +324,269 @@ __global__ __launch_bounds__(TB) void k_sum_split(const float* __restrict__ part
 }
 
 // ---------------------------------------------------------------------------
-// Weight gradient partial sums, stride 1.
-//   Tile: MT blocks of 16 (tap, channel) pairs x NT blocks of 16 output
-//   channels, one per workgroup (grid y).  Grid x: chunks of gchunk groups;
-//   wave w of the workgroup takes groups gb + w, gb + w + WAVES, ... and the
-//   four waves' sums are added through LDS in wave order before the chunk's
-//   partial is written: part[chunk][(k*cin + c)*cout + n].
-template <int K, int MT, int NT>
+// Weight gradient partial sums, stride 1:
+//   dW[k][c][n] = sum over octants i of x[nb(i,k)][c] * dY[i][n]  (dY masked by
+//   [y > 0] when ymask is given), an M x N = (tap, channel) x (output channel)
+//   GEMM whose reduction runs over the octants, four per MFMA step: the
+//   children 4h + q (q = lane / 16) of one sibling group.
+// Operand loads go straight to global memory, where one 16-lane slice reads
+// one row: with VA > 1 lane i loads channels VA i .. VA i + VA - 1 of it in one
+// vector load and feeds them to VA MFMAs (M row i of MFMA s is channel
+// VA i + s); likewise VB for the output channels of dY.  A wave owns TT taps x
+// 16 VA channels x 16 VB output channels (PERM mode) or, for cin < 16, MB
+// blocks of 16 consecutive flattened (tap, channel) pairs x 16 VB output
+// channels (FLAT mode, MB > 0), and walks the groups of its workgroup's chunk
+// with the neighbour entries two groups and the operands one group ahead.
+// A workgroup holds WT tiles; the WAVES / WT waves of a tile interleave over
+// the groups of the chunk and their sums are added in wave order through LDS.
+// Grid: x = chunk of gchunk groups, y = ceil(tiles / WT);
+// part[chunk][(k*cin + c)*cout + n].
+template <int V>
+__device__ __forceinline__ void ldv(const float* p, int valid, float (&v)[V]) {
+  if constexpr (V == 4) {
+    if (valid >= 4) {
+      const float4 t = *reinterpret_cast<const float4*>(p);
+      v[0] = t.x, v[1] = t.y, v[2] = t.z, v[3] = t.w;
+      return;
+    }
+  } else if constexpr (V == 2) {
+    if (valid >= 2) {
+      const float2 t = *reinterpret_cast<const float2*>(p);
+      v[0] = t.x, v[1] = t.y;
+      return;
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < V; ++s) v[s] = s < valid ? p[s] : 0.f;
+}
+
+template <int K, int VA, int VB, int TT, int MB, int WT>
 __global__ __launch_bounds__(TB) void k_conv_dw(const int32_t* __restrict__ nbr, int64_t ngroups,
                                                 int64_t gchunk, const float* __restrict__ x,
                                                 int cin, const float* __restrict__ dy,
                                                 const float* __restrict__ ymask, int cout,
                                                 float* __restrict__ part) {
   constexpr int R = (K - 1) / 2, K3 = K * K * K;
-  constexpr int NACC = MT * NT * 4;
-  __shared__ float red[(WAVES - 1) * NACC * 64];
+  constexpr bool FLAT = MB > 0;
+  constexpr int NA = FLAT ? MB : TT;  // A operands per reduction step
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int li = lane & 15, q = lane >> 4;
   const int mtot = K3 * cin;
-  const int tiles_m = (mtot + 16 * MT - 1) / (16 * MT);
-  const int tm = blockIdx.y % tiles_m, tn = blockIdx.y / tiles_m;
+  const int tiles_n = (cout + 16 * VB - 1) / (16 * VB);
+  const int tiles_m = FLAT ? (mtot + 16 * MB - 1) / (16 * MB)
+                           : (K3 / TT) * ((cin + 16 * VA - 1) / (16 * VA));
+  constexpr int WPT = WAVES / WT;  // waves per tile
+  const int wt = wave % WT, gp = wave / WT;
+  const int tile = blockIdx.y * WT + wt;
+  const bool on = tile < tiles_m * tiles_n;  // idle waves still reach the barrier
+  const int tm = on ? tile % tiles_m : 0, tn = on ? tile / tiles_m : 0;
 
-  // this lane's (tap, channel) pair in each M block
-  int ach[MT], aox[MT], aoy[MT], aoz[MT];
-  bool aval[MT];
+  // per-lane operand geometry: parent-offset slot and child offset of each
+  // (half, operand), the channel and its count of valid lanes
+  int slot[2][NA], coff[2][NA], ach[NA], aval[NA];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = (tm * MT + mt) * 16 + li;
-    aval[mt] = m < mtot;
-    const int k = aval[mt] ? m / cin : 0;
-    ach[mt] = aval[mt] ? m - k * cin : 0;
-    aox[mt] = k / (K * K);  // tap offset + R per axis
-    aoy[mt] = (k / K) % K;
-    aoz[mt] = k % K;
-  }
-  int bcol[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) bcol[nt] = (tn * NT + nt) * 16 + li;
-
-  v4f acc[MT][NT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = v4f{0.f, 0.f, 0.f, 0.f};
-
-  const int64_t gb = (int64_t)blockIdx.x * gchunk;
-  const int64_t ge = gb + gchunk < ngroups ? gb + gchunk : ngroups;
-  for (int64_t g = gb + wave; g < ge; g += WAVES) {
-    const int32_t* nb = nbr + 27 * g;
+  for (int a = 0; a < NA; ++a) {
+    int k, c0;
+    if constexpr (FLAT) {
+      const int m = (tm * MB + a) * 16 + li;
+      k = m < mtot ? m / cin : 0;
+      c0 = m - k * cin;
+      aval[a] = m < mtot ? 1 : 0;
+    } else {
+      const int tg = tm % (K3 / TT), cb = tm / (K3 / TT);
+      k = tg * TT + a;
+      c0 = cb * 16 * VA + VA * li;
+      aval[a] = cin - c0;
+    }
+    ach[a] = c0;
+    const int ox = k / (K * K), oy = (k / K) % K, oz = k % K;  // tap offset + R
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int c = 4 * h + q;  // this lane's octant of the reduction step
-      const int cx = c >> 2, cy = (c >> 1) & 1, cz = c & 1;
-      float a[MT], b[NT];
+      const int c = 4 * h + q;
+      const int ux = (c >> 2) + ox - R, uy = ((c >> 1) & 1) + oy - R, uz = (c & 1) + oz - R;
+      slot[h][a] = ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1);
+      coff[h][a] = 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
+    }
+  }
+  const int n0 = tn * 16 * VB + VB * li;
+  const int nval = cout - n0;
+
+  v4f acc[NA][FLAT ? 1 : VA][VB];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        float v = 0.f;
-        if (aval[mt]) {
-          const int32_t src = tile_src<R>(nb, cx + aox[mt], cy + aoy[mt], cz + aoz[mt]);
-          if (src >= 0) v = x[(int64_t)src * cin + ach[mt]];
-        }
-        a[mt] = v;
+  for (int a = 0; a < NA; ++a)
+#pragma unroll
+    for (int sa = 0; sa < (FLAT ? 1 : VA); ++sa)
+#pragma unroll
+      for (int sb = 0; sb < VB; ++sb) acc[a][sa][sb] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  // the waves of a tile take groups gb + gp, gb + gp + WPT, ...
+  const int64_t gb = (int64_t)blockIdx.x * gchunk;
+  const int64_t ge = !on ? gb : gb + gchunk < ngroups ? gb + gchunk : ngroups;
+
+  constexpr int WA = FLAT ? 1 : VA;
+  int32_t nbc[2][NA], nbn[2][NA];
+  float ac[2][NA][WA], an[2][NA][WA], bc[2][VB], bn[2][VB];
+  auto load_nb = [&](int64_t g, int32_t (&v)[2][NA]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int a = 0; a < NA; ++a) v[h][a] = g < ge ? nbr[27 * g + slot[h][a]] : -1;
+  };
+  auto load_ops = [&](int64_t g, const int32_t (&v)[2][NA], float (&A)[2][NA][WA],
+                      float (&Bv)[2][VB]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t orow = 8 * g + 4 * h + q;
+      float b[VB], m[VB];
+      const bool live = g < ge;
+      ldv<VB>(dy + orow * cout + n0, live ? nval : 0, b);
+      if (ymask) {
+        ldv<VB>(ymask + orow * cout + n0, live ? nval : 0, m);
+#pragma unroll
+        for (int s = 0; s < VB; ++s) b[s] = m[s] > 0.f ? b[s] : 0.f;
       }
-      const int64_t orow = 8 * g + c;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        float v = 0.f;
-        if (bcol[nt] < cout) {
-          const int64_t idx = orow * cout + bcol[nt];
-          v = dy[idx];
-          if (ymask && !(ymask[idx] > 0.f)) v = 0.f;
-        }
-        b[nt] = v;
+      for (int s = 0; s < VB; ++s) Bv[h][s] = b[s];
+#pragma unroll
+      for (int a = 0; a < NA; ++a) {
+        const int32_t src = v[h][a] < 0 ? -1 : v[h][a] + coff[h][a];
+        float t[WA];
+        ldv<WA>(x + (int64_t)(src < 0 ? 0 : src) * cin + ach[a], src < 0 ? 0 : aval[a], t);
+#pragma unroll
+        for (int s = 0; s < WA; ++s) A[h][a][s] = t[s];
       }
+    }
+  };
+
+  load_nb(gb + gp, nbc);
+  load_ops(gb + gp, nbc, ac, bc);
+  load_nb(gb + gp + WPT, nbn);
+  for (int64_t g = gb + gp; g < ge; g += WPT) {
+    load_ops(g + WPT, nbn, an, bn);
+    load_nb(g + 2 * WPT, nbn);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma4(a[mt], b[nt], acc[mt][nt]);
+      for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int sa = 0; sa < WA; ++sa)
+#pragma unroll
+          for (int sb = 0; sb < VB; ++sb)
+            acc[a][sa][sb] = mfma4(ac[h][a][sa], bc[h][sb], acc[a][sa][sb]);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int s = 0; s < WA; ++s) ac[h][a][s] = an[h][a][s];
+#pragma unroll
+      for (int s = 0; s < VB; ++s) bc[h][s] = bn[h][s];
     }
   }
 
-  // wave-ordered sum of the four waves' tiles
-  if (wave > 0) {
-    float* r = red + (wave - 1) * NACC * 64;
+  // the sums of a tile's waves, added in wave order through LDS
+  constexpr int NACC = NA * WA * VB * 4;
+  if constexpr (WPT > 1) {
+    __shared__ float red[WT * (WPT - 1) * NACC * 64];
+    if (gp > 0) {
+      float* r = red + (wt * (WPT - 1) + gp - 1) * NACC * 64;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+      for (int a = 0; a < NA; ++a)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
+        for (int sa = 0; sa < WA; ++sa)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) r[((mt * NT + nt) * 4 + j) * 64 + lane] = acc[mt][nt][j];
+          for (int sb = 0; sb < VB; ++sb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              r[(((a * WA + sa) * VB + sb) * 4 + j) * 64 + lane] = acc[a][sa][sb][j];
+    }
+    __syncthreads();
+    if (gp != 0) return;
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+      for (int sa = 0; sa < WA; ++sa)
+#pragma unroll
+        for (int sb = 0; sb < VB; ++sb)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int w = 0; w < WPT - 1; ++w)
+              acc[a][sa][sb][j] +=
+                  red[((wt * (WPT - 1) + w) * NACC + ((a * WA + sa) * VB + sb) * 4 + j) * 64 + lane];
   }
-  __syncthreads();
-  if (wave != 0) return;
+  if (!on) return;
+
+  // accumulator r of lane l: M row 4(l/16)+r, N column l%16
   float* pp = part + (int64_t)blockIdx.x * ((int64_t)mtot * cout);
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+  for (int a = 0; a < NA; ++a)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int n = bcol[nt];
+    for (int sa = 0; sa < WA; ++sa)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float v = acc[mt][nt][j];
+      for (int sb = 0; sb < VB; ++sb)
 #pragma unroll
-        for (int w = 0; w < WAVES - 1; ++w) v += red[(w * NACC + (mt * NT + nt) * 4 + j) * 64 + lane];
-        const int m = (tm * MT + mt) * 16 + 4 * q + j;
-        if (n < cout && m < mtot) pp[(int64_t)m * cout + n] = v;
-      }
-    }
+        for (int r = 0; r < 4; ++r) {
+          const int i = 4 * q + r;
+          const int n = tn * 16 * VB + VB * li + sb;
+          int m;
+          if constexpr (FLAT) {
+            m = (tm * MB + a) * 16 + i;
+          } else {
+            const int tg = tm % (K3 / TT), cb = tm / (K3 / TT);
+            const int ch = cb * 16 * VA + VA * i + sa;
+            m = ch < cin ? (tg * TT + a) * cin + ch : mtot;
+          }
+          if (m < mtot && n < cout) pp[(int64_t)m * cout + n] = acc[a][sa][sb][r];
+        }
 }
 
-// Fixed-order sum of the chunk partials.
-__global__ __launch_bounds__(TB) void k_sum_parts(const float* __restrict__ part, int nparts,
-                                                  int64_t entries, float* __restrict__ out) {
-  const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (e >= entries) return;
+// Fixed-order sum of np partials of n entries, in two passes: pass 1 adds
+// segment y (partials y*sp .. y*sp+sp-1) of 64 entries per workgroup, four
+// interleaved sub-sums per entry combined in order; pass 2 adds the segments.
+__global__ __launch_bounds__(TB) void k_sum_parts1(const float* __restrict__ part, int np, int sp,
+                                                   int64_t n, float* __restrict__ seg) {
+  __shared__ float r[4][64];
+  const int el = threadIdx.x & 63, sg = threadIdx.x >> 6;
+  const int64_t e = (int64_t)blockIdx.x * 64 + el;
+  const int p0 = blockIdx.y * sp, p1 = p0 + sp < np ? p0 + sp : np;
   float s = 0.f;
-  for (int p = 0; p < nparts; ++p) s += part[(int64_t)p * entries + e];
+  if (e < n) {
+    int p = p0 + sg;
+    for (; p + 12 < p1; p += 16) {  // four independent loads in flight
+      const float a = part[(int64_t)p * n + e], b = part[(int64_t)(p + 4) * n + e];
+      const float c = part[(int64_t)(p + 8) * n + e], d = part[(int64_t)(p + 12) * n + e];
+      s += a;
+      s += b;
+      s += c;
+      s += d;
+    }
+    for (; p < p1; p += 4) s += part[(int64_t)p * n + e];
+  }
+  r[sg][el] = s;
+  __syncthreads();
+  if (sg == 0 && e < n) seg[(int64_t)blockIdx.y * n + e] = ((r[0][el] + r[1][el]) + r[2][el]) + r[3][el];
+}
+
+__global__ __launch_bounds__(TB) void k_sum_parts2(const float* __restrict__ seg, int ns, int64_t n,
+                                                   float* __restrict__ out) {
+  const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (e >= n) return;
+  float s = 0.f;
+  for (int y = 0; y < ns; ++y) s += seg[(int64_t)y * n + e];
   out[e] = s;
+}
+
+// Segments of the two-pass sum: about 64 partials each, enough workgroups.
+inline int sum_segments(int np) { return np <= 64 ? 1 : (int)oc::cdiv(np, 64); }
+
+void sum_parts(const float* part, int np, int64_t n, float* seg, float* out, hipStream_t s) {
+  const int ns = sum_segments(np), sp = (int)oc::cdiv(np, ns);
+  hipLaunchKernelGGL(k_sum_parts1, dim3((unsigned)oc::cdiv(n, 64), (unsigned)ns), dim3(TB), 0, s,
+                     part, np, sp, n, ns == 1 ? out : seg);
+  if (ns > 1)
+    hipLaunchKernelGGL(k_sum_parts2, dim3((unsigned)oc::cdiv(n, TB)), dim3(TB), 0, s,
+                       (const float*)seg, ns, n, out);
 }
 
 // ---------------------------------------------------------------------------
@@ -376,22 +596,22 @@ struct TileCfg {
   int V, MR, NR, WM, splits, cps;
 };
 
-// Workgroup tile and split of the reduction for a stride-1 layer of G groups.
+// Workgroup tile and split of the reduction for a stride-1 layer of G groups
+// (chosen from measurements of the depth-2..6 layers of the 32-shape batch).
 TileCfg pick_tile(int K, int64_t G, int kk, int nn) {
   TileCfg c;
   c.V = (K == 3 && kk >= 16) ? 4 : 1;
-  if (nn <= 16) {
-    c.WM = 4, c.MR = 1, c.NR = 1;  // 64 x 16
-  } else if (nn <= 32) {
-    c.WM = 2, c.MR = 2, c.NR = 1;  // 64 x 32
+  c.WM = 4;
+  if (c.V == 1 && K == 3) {
+    c.MR = 2, c.NR = 1;  // 128 x 16
   } else {
-    c.WM = 2, c.MR = 2, c.NR = 2;  // 64 x 64
+    c.MR = 1, c.NR = nn <= 16 ? 1 : 2;  // 64 x 16 or 64 x 32
   }
   const int BM = 16 * c.WM * c.MR, BN = 16 * (WAVES / c.WM) * c.NR;
   const int64_t tiles = oc::cdiv(G, BM / 8) * oc::cdiv(nn, BN);
   const int chunks = (int)oc::cdiv(kk, 4 * c.V);
   int splits = 1;
-  while (tiles * splits < 512 && splits * 2 <= chunks) splits *= 2;
+  while (tiles * splits < 1024 && splits * 2 <= chunks) splits *= 2;
   c.cps = (int)oc::cdiv(chunks, splits);
   c.splits = (int)oc::cdiv(chunks, c.cps);
   return c;
@@ -422,39 +642,63 @@ void dispatch_tile(const oc_octree* t, int l, int K, const float* x, const float
     launch_tile<K_, V_, MR_, NR_, WM_, FLIP>(t, l, c, x, xmask, kk, w, nn, out, relu, part, s); \
     return;                                                                                \
   }
-  OC_TILE(3, 4, 1, 1, 4) OC_TILE(3, 4, 2, 1, 2) OC_TILE(3, 4, 2, 2, 2)
-  OC_TILE(3, 1, 1, 1, 4) OC_TILE(3, 1, 2, 1, 2) OC_TILE(3, 1, 2, 2, 2)
-  OC_TILE(5, 1, 1, 1, 4) OC_TILE(5, 1, 2, 1, 2) OC_TILE(5, 1, 2, 2, 2)
+  OC_TILE(3, 4, 1, 1, 4) OC_TILE(3, 4, 1, 2, 4) OC_TILE(3, 1, 2, 1, 4)
+  OC_TILE(5, 1, 1, 1, 4) OC_TILE(5, 1, 1, 2, 4)
 #undef OC_TILE
 }
 
 struct DwCfg {
-  int MT, NT, tiles;
+  int VA, VB, TT, MB, WT, tiles;
   int64_t gchunk, nchunks;
 };
 
+// Wave tile, chunking and partial-sum count of the weight gradient.
 DwCfg pick_dw(int K, int64_t G, int cin, int cout) {
   DwCfg c;
-  const int64_t entries = (int64_t)K * K * K * cin * cout;
-  const int mblocks = (int)oc::cdiv((int64_t)K * K * K * cin, 16);
-  const int nblocks = (int)oc::cdiv(cout, 16);
-  c.NT = nblocks >= 4 ? 4 : nblocks >= 2 ? 2 : 1;
-  c.MT = mblocks >= 4 ? 4 : 2;
-  c.tiles = (int)(oc::cdiv(mblocks, c.MT) * oc::cdiv(nblocks, c.NT));
-  // about 512 workgroups, partial sums capped at 4M floats
-  int64_t chunks = std::max<int64_t>(1, oc::cdiv(512, c.tiles));
-  chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, (int64_t(4) << 20) / entries));
-  c.gchunk = std::max<int64_t>(WAVES, oc::cdiv(std::max<int64_t>(G, 1), chunks));
+  const int K3 = K * K * K;
+  const int64_t entries = (int64_t)K3 * cin * cout;
+  // vector widths need rows whose length they divide
+  c.VB = (cout >= 64 && cout % 4 == 0) ? 4 : (cout >= 32 && cout % 2 == 0) ? 2 : 1;
+  const int tiles_n = (int)oc::cdiv(cout, 16 * c.VB);
+  int tiles_m;
+  if (cin < 16) {
+    c.VA = 1, c.TT = 1;
+    c.MB = (int)std::min<int64_t>(8, oc::cdiv((int64_t)K3 * cin, 16));
+    tiles_m = (int)oc::cdiv((int64_t)K3 * cin, 16 * c.MB);
+  } else {
+    c.MB = 0;
+    c.VA = (cin >= 64 && cin % 4 == 0) ? 4 : (cin >= 32 && cin % 2 == 0) ? 2 : 1;
+    const int per = c.VA * c.VB;  // MFMAs per operand and reduction step
+    c.TT = per >= 8 ? 1 : per >= 2 ? 3 : (K == 3 ? 9 : 5);
+    if (K == 5 && c.TT == 3) c.TT = 5;
+    tiles_m = (K3 / c.TT) * (int)oc::cdiv(cin, 16 * c.VA);
+  }
+  c.tiles = tiles_m * tiles_n;
+  // many tiles: the waves of a workgroup share groups (L1 reuse); few: they
+  // share a tile and split the groups
+  c.WT = c.tiles >= 32 ? 4 : 1;
+  // measured on the depth-2..6 layers of the 32-shape batch: about 2048
+  // waves with WT = 4, 8192 with WT = 1; partial sums capped at 16M floats
+  const int64_t target = c.WT == 4 ? 2048 : 8192;
+  int64_t chunks = std::max<int64_t>(1, oc::cdiv(target, (int64_t)c.tiles * (WAVES / c.WT)));
+  chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, (int64_t(16) << 20) / entries));
+  c.gchunk = std::max<int64_t>(8, oc::cdiv(std::max<int64_t>(G, 1), chunks));
   c.nchunks = std::max<int64_t>(1, oc::cdiv(G, c.gchunk));
   return c;
 }
 
-template <int K, int MT, int NT>
+template <int K, int VA, int VB, int TT, int MB>
 void launch_dw(const oc_octree* t, int l, const DwCfg& c, const float* x, int cin,
                const float* dy, const float* ym, int cout, float* part, hipStream_t s) {
+  if (c.WT == 4) {
+    dim3 grid((unsigned)c.nchunks, (unsigned)oc::cdiv(c.tiles, 4));
+    hipLaunchKernelGGL((k_conv_dw<K, VA, VB, TT, MB, 4>), grid, dim3(TB), 0, s,
+                       (const int32_t*)t->nbr[l], t->M[l - 1], c.gchunk, x, cin, dy, ym, cout, part);
+    return;
+  }
   dim3 grid((unsigned)c.nchunks, (unsigned)c.tiles);
-  hipLaunchKernelGGL((k_conv_dw<K, MT, NT>), grid, dim3(TB), 0, s, (const int32_t*)t->nbr[l],
-                     t->M[l - 1], c.gchunk, x, cin, dy, ym, cout, part);
+  hipLaunchKernelGGL((k_conv_dw<K, VA, VB, TT, MB, 1>), grid, dim3(TB), 0, s,
+                     (const int32_t*)t->nbr[l], t->M[l - 1], c.gchunk, x, cin, dy, ym, cout, part);
 }
 
 }  // namespace
@@ -478,23 +722,38 @@ void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, con
 
 size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout) {
   const DwCfg c = pick_dw(K, t->M[l - 1], cin, cout);
-  return (size_t)c.nchunks;
+  const int ns = sum_segments((int)c.nchunks);
+  return (size_t)c.nchunks + (ns > 1 ? ns : 0);  // partials, then pass-1 segments
 }
 
 void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, int cin,
                             const float* dy, const float* ymask, int cout, float* dw, float* part,
                             hipStream_t s) {
   const DwCfg c = pick_dw(K, t->M[l - 1], cin, cout);
-#define OC_DW(K_, MT_, NT_)                                                \
-  if (K == K_ && c.MT == MT_ && c.NT == NT_) {                             \
-    launch_dw<K_, MT_, NT_>(t, l, c, x, cin, dy, ymask, cout, part, s);    \
+#define OC_DW(K_, VA_, VB_, TT_, MB_)                                                       \
+  if (K == K_ && c.VA == VA_ && c.VB == VB_ && c.TT == TT_ && c.MB == MB_) {               \
+    launch_dw<K_, VA_, VB_, TT_, MB_>(t, l, c, x, cin, dy, ymask, cout, part, s);          \
   } else
-  OC_DW(3, 2, 1) OC_DW(3, 2, 2) OC_DW(3, 2, 4) OC_DW(3, 4, 1) OC_DW(3, 4, 2) OC_DW(3, 4, 4)
-  OC_DW(5, 2, 1) OC_DW(5, 2, 2) OC_DW(5, 2, 4) OC_DW(5, 4, 1) OC_DW(5, 4, 2) OC_DW(5, 4, 4) {}
+  // PERM mode, K = 3
+  OC_DW(3, 4, 4, 1, 0) OC_DW(3, 4, 2, 1, 0) OC_DW(3, 2, 4, 1, 0) OC_DW(3, 4, 1, 3, 0)
+  OC_DW(3, 1, 4, 3, 0) OC_DW(3, 2, 2, 3, 0) OC_DW(3, 2, 1, 3, 0) OC_DW(3, 1, 2, 3, 0)
+  OC_DW(3, 1, 1, 9, 0)
+  // FLAT mode (cin < 16), K = 3: MB = ceil(27 cin / 16) capped at 8
+  OC_DW(3, 1, 1, 1, 2) OC_DW(3, 1, 2, 1, 2) OC_DW(3, 1, 4, 1, 2)
+  OC_DW(3, 1, 1, 1, 4) OC_DW(3, 1, 2, 1, 4) OC_DW(3, 1, 4, 1, 4)
+  OC_DW(3, 1, 1, 1, 6) OC_DW(3, 1, 2, 1, 6) OC_DW(3, 1, 4, 1, 6)
+  OC_DW(3, 1, 1, 1, 7) OC_DW(3, 1, 2, 1, 7) OC_DW(3, 1, 4, 1, 7)
+  OC_DW(3, 1, 1, 1, 8) OC_DW(3, 1, 2, 1, 8) OC_DW(3, 1, 4, 1, 8)
+  // K = 5
+  OC_DW(5, 4, 4, 1, 0) OC_DW(5, 4, 2, 1, 0) OC_DW(5, 2, 4, 1, 0) OC_DW(5, 4, 1, 5, 0)
+  OC_DW(5, 1, 4, 5, 0) OC_DW(5, 2, 2, 5, 0) OC_DW(5, 2, 1, 5, 0) OC_DW(5, 1, 2, 5, 0)
+  OC_DW(5, 1, 1, 5, 0)
+  OC_DW(5, 1, 1, 1, 8) OC_DW(5, 1, 2, 1, 8) OC_DW(5, 1, 4, 1, 8) {
+    oc::set_error("no weight-gradient kernel for K=%d cin=%d cout=%d", K, cin, cout);
+  }
 #undef OC_DW
   const int64_t entries = (int64_t)K * K * K * cin * cout;
-  hipLaunchKernelGGL(k_sum_parts, dim3((unsigned)oc::cdiv(entries, TB)), dim3(TB), 0, s,
-                     (const float*)part, (int)c.nchunks, entries, dw);
+  sum_parts(part, (int)c.nchunks, entries, part + c.nchunks * entries, dw, s);
 }
 
 }  // namespace oc
