@@ -103,8 +103,11 @@ typedef struct oc_level {
  *   points       dev f32 [P][3], every coordinate in [0,1] (else
  *                OC_ERR_RANGE); shape b owns points
  *                shape_offsets[b] .. shape_offsets[b+1]-1.
- *   normals      dev f32 [P][3], averaged per non-empty leaf into the input
- *                signal (Sec. 3.1 "Input signal").
+ *   normals      dev f32 [P][3], finite (else OC_ERR_RANGE), averaged per
+ *                non-empty leaf into the input signal (Sec. 3.1 "Input
+ *                signal"); the sums are kept in 64-bit fixed point with a
+ *                step of 2^-62 times P times the largest |component|, so
+ *                the signal does not depend on the order of the additions.
  *   shape_offsets host i32 [batch+1], non-decreasing, shape_offsets[0] = 0.
  *   batch        1..256 (8-bit shape index in the key).
  *   depth        1..8 (3*depth key bits must fit below the shape byte).
@@ -113,6 +116,9 @@ typedef struct oc_level {
  *                (Sec. 4 uses 2).
  *   alloc        NULL for hipMalloc/hipFree.
  * Quantisation: cell = min(floor(p * 2^depth), 2^depth - 1) per axis, in fp32.
+ * Device scratch of about (8/7) B 8^depth / 4 bytes (occupancy bitmaps and
+ * their popcount prefix) plus 32 bytes per point is taken from `alloc` for the
+ * duration of the call.
  * On success *out owns its arrays until oc_octree_free.  Waits once on
  * `stream`. */
 oc_status oc_build(const float* points, const float* normals, const int32_t* shape_offsets,

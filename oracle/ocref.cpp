@@ -114,6 +114,9 @@ int ocref_build(const float* points, const float* normals, const int32_t* offset
     uint32_t c = (uint32_t)std::floor(v);
     q[i] = c > qmax ? qmax : c;
   }
+  // Normals are averaged into the input signal: they must be finite.
+  for (int64_t i = 0; i < 3 * P; ++i)
+    if (!std::isfinite(normals[i])) return ERR_RANGE;
   std::vector<int32_t> shape_of(P);
   for (int b = 0; b < batch; ++b)
     for (int64_t i = offsets[b]; i < offsets[b + 1]; ++i) shape_of[i] = b;

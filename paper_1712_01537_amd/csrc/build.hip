@@ -1,25 +1,30 @@
 // Octree construction on the GPU (Sec. 3.1 of O-CNN, arXiv 1712.01537).
 //
-// The paper builds octrees offline on the CPU by breadth-first subdivision.
-// Here the same structure is produced bottom-up with data-parallel passes:
-//   1. quantise every point at the leaf depth and form its compact key
-//      (shape index above the 3d shuffle-key bits);
-//   2. LSD radix sort of the compact keys (8-bit digits, stable ranks from
-//      wavefront ballots);
-//   3. adjacent-unique of the sorted keys gives the non-empty leaves; the
-//      points of a leaf are contiguous, so the mean normal is a segmented sum;
-//   4. parent keys are key >> 3, already sorted, so each shallower depth is
-//      another adjacent-unique (ballot/popcount scan), down to full_depth,
-//      below which every octant is forced non-empty (Sec. 4);
-//   5. after the single host read of the per-depth counts, every depth's
-//      keys, labels and label->row map are emitted top-down: the children of
-//      the j-th non-empty octant occupy rows 8j..8j+7 (Sec. 3.1 "Label");
-//   6. a hash table per depth maps a non-empty octant's key to its rank
-//      (Sec. 3.2, H: key -> index), and for every sibling group the 27
-//      parent-level neighbours are looked up once: the (K+1)^3 union
-//      neighbourhood of the eight siblings (Sec. 3.2, Fig. 4) is then a fixed
-//      function of those 27 entries.
+// The paper builds octrees offline on the CPU by breadth-first subdivision and
+// searches neighbours through a hash table from shuffle keys to indices.  Here
+// every depth l of the batch is an occupancy bitmap over its B 8^l cells, cell
+// index = shape << 3l | shuffle key, so that bit order is key order:
+//   1. each point sets the bit of its leaf cell (quantised at the leaf depth),
+//      through LDS bitmaps of consecutive cell ranges;
+//   2. the bit of a cell at depth l is the OR of its eight children at l+1,
+//      which are one byte of the depth-(l+1) bitmap; depths shallower than
+//      full_depth are all ones (Sec. 4: every octant down to depth 2 exists);
+//   3. one exclusive popcount scan over the words of all depths gives every
+//      set bit its rank, which is its label minus one (Sec. 3.1 "Label");
+//   4. after the one host read of the per-depth counts, each non-empty octant
+//      of depth l-1 with rank r emits its children, rows 8r..8r+7 of depth l
+//      (keys, labels, label->row map; Sec. 3.1 "Label"), and its row of the
+//      sibling-group neighbour table: the first-child row 8 rank of each of the
+//      27 depth-(l-1) octants around it, found by a bit test and a rank query
+//      (this replaces the hash table H of Sec. 3.2; every neighbour within
+//      offset +-2 of the eight siblings is reachable from these 27 entries,
+//      Fig. 4);
+//   5. the input signal (Sec. 3.1) is the mean normal of each leaf's points,
+//      summed in LDS in 64-bit fixed point scaled to the largest normal
+//      component in the batch, so that the sums do not depend on the order of
+//      the atomics.
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <vector>
 
@@ -27,8 +32,7 @@
 
 namespace {
 
-constexpr int TB = 256;  // threads per block in every kernel of this file
-constexpr int WAVE = 64;
+constexpr int TB = 256;
 
 // Bit i of v moves to bit 3i (v < 2^10).
 __device__ __forceinline__ uint32_t spread3(uint32_t v) {
@@ -55,376 +59,460 @@ __device__ __forceinline__ uint32_t shuffle_key(uint32_t x, uint32_t y, uint32_t
   return (spread3(x) << 2) | (spread3(y) << 1) | spread3(z);
 }
 
-__device__ __forceinline__ uint64_t lanemask_lt() {
-  const int lane = threadIdx.x & (WAVE - 1);
-  return lane == 0 ? 0ull : (~0ull >> (WAVE - lane));
+// Layout of the concatenated per-depth bitmaps (kernel argument).
+struct Levels {
+  int depth, full_depth, batch;
+  int64_t cells[OC_MAX_DEPTH + 1];  // B 8^l
+  int64_t wbase[OC_MAX_DEPTH + 2];  // first word of depth l; wbase[depth+1] = all words
+};
+
+// Shape offsets (kernel argument; batch <= 256).
+struct Shapes {
+  int32_t offs[257];
+};
+
+__device__ __forceinline__ int level_of_word(const Levels& L, int64_t w) {
+  int l = 0;
+  while (l < L.depth && w >= L.wbase[l + 1]) ++l;
+  return l;
+}
+
+// Rank of cell c among the set cells of depth l: exclusive prefix of the word
+// minus the count of shallower depths, plus the set bits below c in its word.
+__device__ __forceinline__ int32_t rank_in(const uint32_t* __restrict__ bits,
+                                           const int32_t* __restrict__ pre, const Levels& L,
+                                           int l, int32_t mbase, uint64_t c, uint32_t* word) {
+  const int64_t w = L.wbase[l] + (int64_t)(c >> 5);
+  const uint32_t v = bits[w];
+  *word = v;
+  return pre[w] - mbase + __popc(v & ((1u << (c & 31)) - 1u));
 }
 
 // ---------------------------------------------------------------------------
-// 1. quantise + compact key
+// 1. leaf occupancy.  k_quant: leaf cell of every point (~0 for a point outside
+//    [0,1]^3); bstat[block] = {flags: bit 0 such a point or NaN, bit 1 a
+//    non-finite normal; the largest |normal component| (float bits)}.
+//    k_mark: workgroup k owns leaf cells [k MK_CELLS, (k+1) MK_CELLS) as an LDS
+//    bitmap, scans the points of the shapes that overlap it, derives the words
+//    of up to MK_UP coarser depths from it (bit j of depth l = byte j of depth
+//    l+1 != 0) and stores all of them; the workgroups also fill the depths
+//    shallower than full_depth with ones.  No global atomics.
 
-__global__ __launch_bounds__(TB) void k_quant_key(const float* __restrict__ pts,
-                                                  const int32_t* __restrict__ offs, int B, int P,
-                                                  int depth, uint32_t* __restrict__ key,
-                                                  int32_t* __restrict__ idx, int* __restrict__ err) {
-  const int i = blockIdx.x * TB + threadIdx.x;
-  if (i >= P) return;
+__global__ __launch_bounds__(TB) void k_quant(const float* __restrict__ pts,
+                                              const float* __restrict__ nrm, Shapes S, int B,
+                                              int P, int d, uint32_t* __restrict__ leafcell,
+                                              uint2* __restrict__ bstat) {
+  const int i0 = blockIdx.x * TB + threadIdx.x;
+  const bool live = i0 < P;
+  const int i = live ? i0 : P - 1;  // the block reductions need every lane
   int lo = 0, hi = B - 1;  // last shape b with offs[b] <= i
   while (lo < hi) {
-    int mid = (lo + hi + 1) >> 1;
-    if (offs[mid] <= i) lo = mid;
+    const int mid = (lo + hi + 1) >> 1;
+    if (S.offs[mid] <= i) lo = mid;
     else hi = mid - 1;
   }
-  const float scale = (float)(1u << depth);  // exact power of two
-  const uint32_t qmax = (1u << depth) - 1u;
+  const float scale = (float)(1u << d);  // exact power of two
+  const uint32_t qmax = (1u << d) - 1u;
   uint32_t q[3];
   bool bad = false;
 #pragma unroll
   for (int a = 0; a < 3; ++a) {
-    float p = pts[3 * i + a];
-    bool ok = p >= 0.0f && p <= 1.0f;  // false for NaN
+    const float p = pts[3 * (int64_t)i + a];
+    const bool ok = p >= 0.0f && p <= 1.0f;  // false for NaN
     bad |= !ok;
-    uint32_t c = ok ? (uint32_t)floorf(p * scale) : 0u;
+    const uint32_t c = ok ? (uint32_t)floorf(p * scale) : 0u;
     q[a] = c > qmax ? qmax : c;
   }
-  if (bad) atomicOr(err, 1);
-  key[i] = ((uint32_t)lo << (3 * depth)) | shuffle_key(q[0], q[1], q[2]);
-  idx[i] = i;
-}
-
-// ---------------------------------------------------------------------------
-// 2. LSD radix sort of (key, index) pairs, 8-bit digits.
-
-constexpr int RS_ITEMS = 32;
-constexpr int RS_TILE = TB * RS_ITEMS;
-
-// Per-tile digit histogram, stored digit-major: hist[d * nblk + tile].
-__global__ __launch_bounds__(TB) void k_radix_hist(const uint32_t* __restrict__ keys, int n,
-                                                   int shift, uint32_t* __restrict__ hist,
-                                                   int nblk) {
-  __shared__ uint32_t h[256];
-  h[threadIdx.x] = 0;
-  __syncthreads();
-  const int base = blockIdx.x * RS_TILE;
-  for (int j = 0; j < RS_ITEMS; ++j) {
-    int i = base + j * TB + threadIdx.x;
-    if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
-  }
-  __syncthreads();
-  hist[threadIdx.x * nblk + blockIdx.x] = h[threadIdx.x];
-}
-
-// Exclusive scan of the digit-major histogram (one block, thread = digit).
-__global__ __launch_bounds__(TB) void k_radix_scan(uint32_t* __restrict__ hist, int nblk) {
-  __shared__ uint32_t s[256];
-  const int d = threadIdx.x;
-  uint32_t tot = 0;
-  for (int b = 0; b < nblk; ++b) tot += hist[d * nblk + b];
-  s[d] = tot;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {  // Hillis-Steele inclusive scan
-    uint32_t v = d >= off ? s[d - off] : 0u;
-    __syncthreads();
-    s[d] += v;
-    __syncthreads();
-  }
-  uint32_t run = s[d] - tot;
-  for (int b = 0; b < nblk; ++b) {
-    uint32_t v = hist[d * nblk + b];
-    hist[d * nblk + b] = run;
-    run += v;
-  }
-}
-
-// Stable scatter.  The tile is walked in slices of TB consecutive elements;
-// within a slice, lanes holding the same digit are found with 8 ballots, and
-// per-wave digit counts in LDS order the waves.
-__global__ __launch_bounds__(TB) void k_radix_scatter(const uint32_t* __restrict__ kin,
-                                                      const int32_t* __restrict__ vin,
-                                                      uint32_t* __restrict__ kout,
-                                                      int32_t* __restrict__ vout, int n, int shift,
-                                                      const uint32_t* __restrict__ offs, int nblk) {
-  __shared__ uint32_t base[256];
-  __shared__ uint32_t run[256];
-  __shared__ uint32_t wcnt[TB / WAVE][256];
-  const int tid = threadIdx.x, wave = tid / WAVE, lane = tid % WAVE;
-  base[tid] = offs[tid * nblk + blockIdx.x];
-  run[tid] = 0;
-  const uint64_t lt = lanemask_lt();
-  for (int j = 0; j < RS_ITEMS; ++j) {
-    const int i = blockIdx.x * RS_TILE + j * TB + tid;
-    const bool valid = i < n;
-    const uint32_t key = valid ? kin[i] : 0u;
-    const int32_t val = valid ? vin[i] : 0;
-    const uint32_t d = (key >> shift) & 255u;
+  float m = 0.f;
+  bool nbad = false;
 #pragma unroll
-    for (int w = 0; w < TB / WAVE; ++w) wcnt[w][tid] = 0;
-    __syncthreads();
-    uint64_t peers = __ballot(valid);
-#pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const bool bit = (d >> b) & 1u;
-      const uint64_t m = __ballot(bit);
-      peers &= bit ? m : ~m;
-    }
-    const uint32_t rank = __popcll(peers & lt);
-    if (valid && rank == 0) wcnt[wave][d] = __popcll(peers);
-    __syncthreads();
-    if (valid) {
-      uint32_t pos = base[d] + run[d] + rank;
-      for (int w = 0; w < wave; ++w) pos += wcnt[w][d];
-      kout[pos] = key;
-      vout[pos] = val;
-    }
-    __syncthreads();
-    uint32_t add = 0;
-#pragma unroll
-    for (int w = 0; w < TB / WAVE; ++w) add += wcnt[w][tid];
-    run[tid] += add;
+  for (int a = 0; a < 3; ++a) {
+    const float n = nrm[3 * (int64_t)i + a];
+    nbad |= !isfinite(n);
+    m = fmaxf(m, fabsf(n));
   }
-}
-
-// ---------------------------------------------------------------------------
-// 3./4. adjacent-unique of a sorted key array, keys compared after >> shift.
-//   pass 1: per-tile count of run starts;  pass 2: scan of the tile counts
-//   (one block), total -> *count;  pass 3: unique keys, the run index of every
-//   element (optional) and the first element of every run (optional).
-// The input length may live on the device (n_dev) so that these passes can
-// be enqueued before any host read; grids are sized for an upper bound.
-
-constexpr int UQ_ITEMS = 8;
-constexpr int UQ_TILE = TB * UQ_ITEMS;
-
-__device__ __forceinline__ bool run_start(const uint32_t* keys, int i, int shift) {
-  return i == 0 || (keys[i] >> shift) != (keys[i - 1] >> shift);
-}
-
-__device__ __forceinline__ int load_n(const int* n_dev, int n_host) {
-  return n_dev ? *n_dev : n_host;
-}
-
-__global__ __launch_bounds__(TB) void k_unique_count(const uint32_t* __restrict__ keys,
-                                                     const int* n_dev, int n_host, int shift,
-                                                     uint32_t* __restrict__ tile_cnt) {
-  __shared__ uint32_t part[TB / WAVE];
-  const int n = load_n(n_dev, n_host);
-  uint32_t c = 0;
-  for (int j = 0; j < UQ_ITEMS; ++j) {
-    int i = blockIdx.x * UQ_TILE + j * TB + threadIdx.x;
-    if (i < n && run_start(keys, i, shift)) ++c;
+  // flags and the largest |component| of the workgroup (float bits order
+  // non-negative floats)
+  __shared__ uint2 ws[TB / 64];
+  uint32_t fl = (bad ? 1u : 0u) | (nbad ? 2u : 0u), mb = nbad ? 0u : __float_as_uint(m);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint32_t o = __shfl_xor(mb, off, 64);
+    fl |= __shfl_xor(fl, off, 64);
+    mb = o > mb ? o : mb;
   }
-  // wave reduction, then across waves
-  for (int off = WAVE / 2; off > 0; off >>= 1) c += __shfl_down(c, off, WAVE);
-  if ((threadIdx.x & (WAVE - 1)) == 0) part[threadIdx.x / WAVE] = c;
+  if ((threadIdx.x & 63) == 0) ws[threadIdx.x >> 6] = make_uint2(fl, mb);
   __syncthreads();
   if (threadIdx.x == 0) {
-    uint32_t s = 0;
-    for (int w = 0; w < TB / WAVE; ++w) s += part[w];
-    tile_cnt[blockIdx.x] = s;
+    uint2 v = make_uint2(0u, 0u);
+#pragma unroll
+    for (int k = 0; k < TB / 64; ++k) {
+      v.x |= ws[k].x;
+      v.y = ws[k].y > v.y ? ws[k].y : v.y;
+    }
+    bstat[blockIdx.x] = v;
+  }
+  if (!live) return;
+  const uint64_t c = ((uint64_t)lo << (3 * d)) | shuffle_key(q[0], q[1], q[2]);
+  leafcell[i] = bad ? 0xFFFFFFFFu : (uint32_t)c;
+}
+
+constexpr int MK_TB = 1024;
+constexpr int MK_WORDS = 16384;                // 64 KB of LDS for the leaf depth
+constexpr int64_t MK_CELLS = 32ll * MK_WORDS;  // leaf cells per workgroup
+constexpr int MK_UP = 4;                       // coarser depths derived in LDS
+
+__global__ __launch_bounds__(MK_TB) void k_mark(const uint32_t* __restrict__ leafcell, Shapes S,
+                                                Levels L, uint32_t* __restrict__ bits) {
+  __shared__ uint32_t w[MK_WORDS + MK_WORDS / 8 + MK_WORDS / 64 + MK_WORDS / 512 + MK_WORDS / 4096];
+  const int d = L.depth;
+  // depths shallower than full_depth: all ones (grid-stride over their words)
+  const int64_t nforced = L.wbase[L.full_depth];
+  for (int64_t k = (int64_t)blockIdx.x * MK_TB + threadIdx.x; k < nforced;
+       k += (int64_t)gridDim.x * MK_TB) {
+    const int l = level_of_word(L, k);
+    const int64_t left = L.cells[l] - (k - L.wbase[l]) * 32;
+    bits[k] = left >= 32 ? ~0u : ((1u << left) - 1u);
+  }
+  const int64_t c0 = (int64_t)blockIdx.x * MK_CELLS;
+  const int64_t c1 = c0 + MK_CELLS < L.cells[d] ? c0 + MK_CELLS : L.cells[d];
+  const int nwd = (int)((c1 - c0 + 31) >> 5);
+  for (int k = threadIdx.x; k < nwd; k += MK_TB) w[k] = 0u;
+  __syncthreads();
+  const int64_t per = (int64_t)1 << (3 * d);  // cells per shape
+  const int b0 = (int)(c0 / per), b1 = (int)((c1 - 1) / per);
+  for (int i = S.offs[b0] + threadIdx.x; i < S.offs[b1 + 1]; i += MK_TB) {
+    const uint32_t c = leafcell[i];
+    if (c == 0xFFFFFFFFu || (int64_t)c < c0 || (int64_t)c >= c1) continue;
+    atomicOr(&w[(c - c0) >> 5], 1u << (c & 31));
+  }
+  __syncthreads();
+  if (d >= L.full_depth) {
+    uint32_t* dst = bits + L.wbase[d] + (c0 >> 5);
+    for (int k = threadIdx.x; k < nwd; k += MK_TB) dst[k] = w[k];
+  }
+  // coarser depths d-1 .. d-MK_UP: the chunk's cells there start on a word
+  // boundary (MK_CELLS / 8^MK_UP is a multiple of 32)
+  uint32_t* fine = w;
+  int nfine = nwd;
+  int off = MK_WORDS;
+  for (int j = 1; j <= MK_UP && d - j >= L.full_depth; ++j) {
+    const int l = d - j;
+    uint32_t* coarse = w + off;
+    const int64_t cc0 = c0 >> (3 * j), ncell = (c1 - c0) >> (3 * j);
+    const int ncw = (int)((ncell + 31) >> 5);
+    for (int k = threadIdx.x; k < ncw; k += MK_TB) {
+      uint32_t v = 0u;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const uint32_t cw = 8 * k + t < nfine ? fine[8 * k + t] : 0u;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) v |= ((cw >> (8 * b)) & 0xFFu) ? (1u << (4 * t + b)) : 0u;
+      }
+      coarse[k] = v;
+      bits[L.wbase[l] + (cc0 >> 5) + k] = v;
+    }
+    __syncthreads();
+    fine = coarse;
+    nfine = ncw;
+    off += MK_WORDS >> (3 * j);
   }
 }
 
-// Exclusive scan of ntile counts in one block; total to *count.
-__global__ __launch_bounds__(TB) void k_scan_tiles(uint32_t* __restrict__ tile_cnt, int ntile,
-                                                   int* __restrict__ count) {
-  __shared__ uint32_t s[TB];
-  const int t = threadIdx.x;
-  const int per = (ntile + TB - 1) / TB;  // contiguous chunk per thread
-  uint32_t tot = 0;
-  for (int k = 0; k < per; ++k) {
-    int i = t * per + k;
-    if (i < ntile) tot += tile_cnt[i];
+// ---------------------------------------------------------------------------
+// 2. depths more than MK_UP above the leaves (and not forced): bit j of depth
+//    l = (byte j of depth l+1 != 0).
+
+__global__ __launch_bounds__(TB) void k_reduce(Levels L, int l, uint32_t* __restrict__ bits) {
+  const int64_t w = (int64_t)blockIdx.x * TB + threadIdx.x;
+  const int64_t nw = L.wbase[l + 1] - L.wbase[l], nc = L.wbase[l + 2] - L.wbase[l + 1];
+  if (w >= nw) return;
+  const uint32_t* child = bits + L.wbase[l + 1] + 8 * w;
+  uint32_t v = 0u;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const uint32_t cw = 8 * w + k < nc ? child[k] : 0u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v |= ((cw >> (8 * j)) & 0xFFu) ? (1u << (4 * k + j)) : 0u;
   }
-  s[t] = tot;
+  bits[L.wbase[l] + w] = v;
+}
+
+// ---------------------------------------------------------------------------
+// 3. exclusive scan of the word popcounts of all depths: pre[w] = set bits
+//    before word w; pre[nw] = total.  Blocks of SCAN_W words.
+
+constexpr int SCAN_PER = 8;
+constexpr int SCAN_W = TB * SCAN_PER;
+
+__device__ __forceinline__ int32_t block_excl_scan(int32_t v, int32_t* total) {
+  __shared__ int32_t ws[TB / 64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int32_t x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int32_t y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) ws[wv] = x;
   __syncthreads();
-  for (int off = 1; off < TB; off <<= 1) {
-    uint32_t v = t >= off ? s[t - off] : 0u;
-    __syncthreads();
-    s[t] += v;
-    __syncthreads();
+  int32_t before = 0, all = 0;
+#pragma unroll
+  for (int k = 0; k < TB / 64; ++k) {
+    if (k < wv) before += ws[k];
+    all += ws[k];
   }
-  uint32_t run = s[t] - tot;
-  for (int k = 0; k < per; ++k) {
-    int i = t * per + k;
-    if (i < ntile) {
-      uint32_t v = tile_cnt[i];
-      tile_cnt[i] = run;
+  __syncthreads();
+  *total = all;
+  return before + x - v;
+}
+
+__global__ __launch_bounds__(TB) void k_scan_a(const uint32_t* __restrict__ bits, int64_t nw,
+                                               int32_t* __restrict__ bsum) {
+  const int64_t w0 = (int64_t)blockIdx.x * SCAN_W + threadIdx.x * SCAN_PER;
+  int32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < SCAN_PER; ++k)
+    if (w0 + k < nw) s += __popc(bits[w0 + k]);
+  int32_t total;
+  block_excl_scan(s, &total);
+  if (threadIdx.x == 0) bsum[blockIdx.x] = total;
+}
+
+// One block: exclusive scan of nb block sums in place; grand total at bsum[nb].
+__global__ __launch_bounds__(TB) void k_scan_b(int32_t* __restrict__ bsum, int nb) {
+  const int per = (nb + TB - 1) / TB;
+  const int b0 = threadIdx.x * per;
+  int32_t s = 0;
+  for (int k = 0; k < per; ++k)
+    if (b0 + k < nb) s += bsum[b0 + k];
+  int32_t total;
+  int32_t run = block_excl_scan(s, &total);
+  for (int k = 0; k < per; ++k)
+    if (b0 + k < nb) {
+      const int32_t v = bsum[b0 + k];
+      bsum[b0 + k] = run;
       run += v;
     }
-  }
-  if (t == TB - 1) *count = (int)s[TB - 1];
+  if (threadIdx.x == 0) bsum[nb] = total;
 }
 
-__global__ __launch_bounds__(TB) void k_unique_write(const uint32_t* __restrict__ keys,
-                                                     const int* n_dev, int n_host, int shift,
-                                                     const uint32_t* __restrict__ tile_off,
-                                                     uint32_t* __restrict__ uniq,
-                                                     int32_t* __restrict__ run_of,
-                                                     int32_t* __restrict__ first) {
-  __shared__ uint32_t wsum[TB / WAVE];
-  const int n = load_n(n_dev, n_host);
-  const int tid = threadIdx.x, wave = tid / WAVE;
-  const uint64_t lt = lanemask_lt();
-  uint32_t off = tile_off[blockIdx.x];
-  if (blockIdx.x * UQ_TILE >= n) return;
-  for (int j = 0; j < UQ_ITEMS; ++j) {
-    const int i = blockIdx.x * UQ_TILE + j * TB + tid;
-    const bool f = i < n && run_start(keys, i, shift);
-    const uint64_t m = __ballot(f);
-    if ((tid & (WAVE - 1)) == 0) wsum[wave] = __popcll(m);
-    __syncthreads();
-    uint32_t before = off, slice = 0;
-    for (int w = 0; w < TB / WAVE; ++w) {
-      if (w < wave) before += wsum[w];
-      slice += wsum[w];
+__global__ __launch_bounds__(TB) void k_scan_c(const uint32_t* __restrict__ bits, int64_t nw,
+                                               const int32_t* __restrict__ bsum,
+                                               int32_t* __restrict__ pre, int nb) {
+  const int64_t w0 = (int64_t)blockIdx.x * SCAN_W + threadIdx.x * SCAN_PER;
+  int32_t c[SCAN_PER], s = 0;
+#pragma unroll
+  for (int k = 0; k < SCAN_PER; ++k) {
+    c[k] = w0 + k < nw ? __popc(bits[w0 + k]) : 0;
+    s += c[k];
+  }
+  int32_t total;
+  int32_t run = bsum[blockIdx.x] + block_excl_scan(s, &total);
+#pragma unroll
+  for (int k = 0; k < SCAN_PER; ++k)
+    if (w0 + k < nw) {
+      pre[w0 + k] = run;
+      run += c[k];
     }
-    // inclusive count of run starts up to and including element i
-    const uint32_t incl = before + __popcll(m & lt) + (f ? 1u : 0u);
-    if (i < n) {
-      const uint32_t r = incl - 1u;
-      if (f) {
-        uniq[r] = keys[i] >> shift;
-        if (first) first[r] = i;
+  if (blockIdx.x == 0 && threadIdx.x == 0) pre[nw] = bsum[nb];
+}
+
+// ---------------------------------------------------------------------------
+// 4. cell of every set bit, in rank order over all depths: ucell[pre + k].
+//    Workgroup 0 also reports the per-depth counts M_l (info[2 + l]) and the
+//    flags and largest |normal component| of the nq blocks of k_quant
+//    (info[0], info[1]).
+
+__global__ __launch_bounds__(TB) void k_compact(Levels L, const uint32_t* __restrict__ bits,
+                                                const int32_t* __restrict__ pre,
+                                                uint32_t* __restrict__ ucell,
+                                                const uint2* __restrict__ bstat, int nq,
+                                                uint32_t* __restrict__ info) {
+  const int64_t w = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (w < L.wbase[L.depth + 1]) {
+    uint32_t v = bits[w];
+    if (v) {
+      const int l = level_of_word(L, w);
+      const uint32_t base = (uint32_t)((w - L.wbase[l]) * 32);
+      int32_t r = pre[w];
+      while (v) {
+        const int b = __ffs(v) - 1;
+        ucell[r++] = base + (uint32_t)b;
+        v &= v - 1u;
       }
-      if (run_of) run_of[i] = (int32_t)r;
     }
-    off += slice;
-    __syncthreads();
   }
-}
-
-// Complete depth (shallower than full_depth): every octant non-empty; the
-// compact key of the r-th octant is r.
-__global__ __launch_bounds__(TB) void k_iota(uint32_t* __restrict__ u, int n) {
-  int i = blockIdx.x * TB + threadIdx.x;
-  if (i < n) u[i] = (uint32_t)i;
+  if (blockIdx.x != 0) return;
+  __shared__ uint2 ws[TB / 64];
+  const int t = threadIdx.x;
+  if (t <= L.depth) info[2 + t] = (uint32_t)(pre[L.wbase[t + 1]] - pre[L.wbase[t]]);
+  uint32_t fl = 0u, mb = 0u;
+  for (int k = t; k < nq; k += TB) {
+    const uint2 v = bstat[k];
+    fl |= v.x;
+    mb = v.y > mb ? v.y : mb;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint32_t o = __shfl_xor(mb, off, 64);
+    fl |= __shfl_xor(fl, off, 64);
+    mb = o > mb ? o : mb;
+  }
+  if ((t & 63) == 0) ws[t >> 6] = make_uint2(fl, mb);
+  __syncthreads();
+  if (t == 0) {
+    uint2 v = make_uint2(0u, 0u);
+#pragma unroll
+    for (int k = 0; k < TB / 64; ++k) {
+      v.x |= ws[k].x;
+      v.y = ws[k].y > v.y ? ws[k].y : v.y;
+    }
+    info[0] = v.x;
+    info[1] = v.y;
+  }
 }
 
 // ---------------------------------------------------------------------------
-// 5. top-down emission of keys / labels / label->row map.
+// 5. mean normal of every leaf.  The leaves of shape b hold a contiguous range
+//    of ranks; workgroup (b, k) owns ranks lo .. lo + LM_LEAVES - 1 of it (a
+//    contiguous cell range), scans the shape's points and adds the normals of
+//    those in range into LDS in 64-bit fixed point, 2^s units with
+//    s = 62 - e for P * max|n| < 2^e: no sum can overflow and integer
+//    additions make the result independent of their order.
 
-// Keys of depth l: row t is child (t & 7) of the (t >> 3)-th non-empty octant
-// of depth l-1.  Labels are zeroed here and set by k_emit_labels.
-__global__ __launch_bounds__(TB) void k_emit_keys(const uint32_t* __restrict__ uparent, int n, int l,
-                                                  uint32_t* __restrict__ keys,
-                                                  int32_t* __restrict__ labels) {
-  const int t = blockIdx.x * TB + threadIdx.x;
-  if (t >= n) return;
-  uint32_t sk;
-  if (l == 0) {
-    sk = (uint32_t)t << 24;
-  } else {
-    const uint32_t ck = (uparent[t >> 3] << 3) | (uint32_t)(t & 7);
-    const uint32_t kb = 3u * (uint32_t)l;
-    sk = ((ck >> kb) << 24) | (ck & ((1u << kb) - 1u));
-  }
-  keys[t] = sk;
-  labels[t] = 0;
+constexpr int LM_TB = 1024;
+constexpr int LM_LEAVES = 3072;  // 3072 * (3 * 8 + 4) bytes of LDS
+
+__device__ __forceinline__ int fixed_shift(uint32_t maxbits, int P) {
+  const double m = (double)__uint_as_float(maxbits) * (double)P;
+  int e = 0;
+  if (m > 0.0) frexp(m, &e);  // m < 2^e
+  return 62 - e;
 }
 
-// Non-empty octant r of depth l sits at row 8 parent(r) + (key & 7).
-// parent_complete: depth l-1 is complete, so parent(r) = key >> 3.
-__global__ __launch_bounds__(TB) void k_emit_labels(const uint32_t* __restrict__ u,
-                                                    const int32_t* __restrict__ parent_of, int m,
-                                                    int l, int parent_complete,
-                                                    int32_t* __restrict__ labels,
-                                                    int32_t* __restrict__ rows) {
-  const int r = blockIdx.x * TB + threadIdx.x;
-  if (r >= m) return;
-  const uint32_t ck = u[r];
-  int32_t row;
-  if (l == 0) row = (int32_t)ck;  // the shape index
-  else {
-    const int32_t p = parent_complete ? (int32_t)(ck >> 3) : parent_of[r];
-    row = 8 * p + (int32_t)(ck & 7u);
+__global__ __launch_bounds__(LM_TB) void k_leaf_mean(const float* __restrict__ nrm,
+                                                     const uint32_t* __restrict__ leafcell,
+                                                     Shapes S, int P,
+                                                     Levels L, const uint32_t* __restrict__ bits,
+                                                     const int32_t* __restrict__ pre,
+                                                     const uint32_t* __restrict__ ucell,
+                                                     const uint32_t* __restrict__ info,
+                                                     float* __restrict__ leafmean) {
+  __shared__ unsigned long long sum[3 * LM_LEAVES];
+  __shared__ int32_t cnt[LM_LEAVES];
+  if (info[0]) return;  // the build fails on any bad input
+  const int b = blockIdx.x, d = L.depth;
+  const int32_t mb = pre[L.wbase[d]], md = pre[L.wbase[d + 1]] - mb;
+  const uint64_t cfirst = (uint64_t)b << (3 * d), cend = (uint64_t)(b + 1) << (3 * d);
+  uint32_t word;
+  const int32_t r0 = rank_in(bits, pre, L, d, mb, cfirst, &word);
+  const int32_t r1 = cend >= (uint64_t)L.cells[d] ? md : rank_in(bits, pre, L, d, mb, cend, &word);
+  const int32_t lo = r0 + (int32_t)blockIdx.y * LM_LEAVES;
+  if (lo >= r1) return;
+  const int32_t hi = lo + LM_LEAVES < r1 ? lo + LM_LEAVES : r1;
+  const uint32_t clo = ucell[mb + lo];
+  const uint64_t chi = hi < r1 ? (uint64_t)ucell[mb + hi] : cend;  // cells [clo, chi)
+  for (int j = threadIdx.x; j < hi - lo; j += LM_TB) {
+    sum[3 * j] = sum[3 * j + 1] = sum[3 * j + 2] = 0ull;
+    cnt[j] = 0;
   }
-  labels[row] = r + 1;
-  rows[r] = row;
-}
-
-// Mean normal of leaf r (points first[r] .. first[r+1]-1 of the sorted order),
-// accumulated in double, written to its row of the signal.
-__global__ __launch_bounds__(TB) void k_leaf_mean(const int32_t* __restrict__ first, int m, int P,
-                                                  const int32_t* __restrict__ perm,
-                                                  const float* __restrict__ normals,
-                                                  const int32_t* __restrict__ rows,
-                                                  float* __restrict__ signal) {
-  const int r = blockIdx.x * TB + threadIdx.x;
-  if (r >= m) return;
-  const int s = first[r], e = r + 1 < m ? first[r + 1] : P;
-  double a = 0.0, b = 0.0, c = 0.0;
-  for (int i = s; i < e; ++i) {
-    const int p = perm[i];
-    a += (double)normals[3 * p];
-    b += (double)normals[3 * p + 1];
-    c += (double)normals[3 * p + 2];
+  __syncthreads();
+  const int s = fixed_shift(info[1], P);
+  for (int i = S.offs[b] + threadIdx.x; i < S.offs[b + 1]; i += LM_TB) {
+    const uint32_t c = leafcell[i];
+    if (c < clo || (uint64_t)c >= chi) continue;
+    const int32_t j = rank_in(bits, pre, L, d, mb, c, &word) - lo;
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      const long long v = llrint(ldexp((double)nrm[3 * (int64_t)i + a], s));
+      atomicAdd(&sum[3 * j + a], (unsigned long long)v);
+    }
+    atomicAdd(&cnt[j], 1);
   }
-  const double inv = (double)(e - s);
-  float* o = signal + 3 * (int64_t)rows[r];
-  o[0] = (float)(a / inv);
-  o[1] = (float)(b / inv);
-  o[2] = (float)(c / inv);
+  __syncthreads();
+  const double unit = ldexp(1.0, -s);
+  for (int j = threadIdx.x; j < hi - lo; j += LM_TB) {
+    const double inv = unit / (double)cnt[j];
+    float* o = leafmean + 3 * (int64_t)(lo + j);
+#pragma unroll
+    for (int a = 0; a < 3; ++a) o[a] = (float)((double)(long long)sum[3 * j + a] * inv);
+  }
 }
 
 // ---------------------------------------------------------------------------
-// 6. hash of non-empty keys -> rank, and the 27-entry sibling-group table.
+// 6. emission.  Item it < B: root b of depth 0.  Otherwise the non-empty
+//    octant of rank r at depth l-1 (items ibase[l] + r): its children are rows
+//    8r .. 8r+7 of depth l, its neighbour row is nbr_l[r].
 
-constexpr uint64_t HASH_EMPTY = ~0ull;
+struct Emit {
+  int32_t mbase[OC_MAX_DEPTH + 2];  // set bits before depth l (all depths)
+  int64_t ibase[OC_MAX_DEPTH + 2];  // first item of depth l (l >= 1); ibase[d+1] = items
+  uint32_t* keys[OC_MAX_DEPTH + 1];
+  int32_t* labels[OC_MAX_DEPTH + 1];
+  int32_t* rows[OC_MAX_DEPTH + 1];
+  int32_t* nbr[OC_MAX_DEPTH + 1];
+  float* signal;
+};
 
-__device__ __forceinline__ uint32_t hash_slot(uint32_t ck, uint32_t mask_bits) {
-  return (ck * 0x9E3779B1u) >> (32u - mask_bits);  // Fibonacci hashing
-}
-
-__global__ __launch_bounds__(TB) void k_hash_insert(const uint32_t* __restrict__ u, int m,
-                                                    unsigned long long* __restrict__ table,
-                                                    int log_cap) {
-  const int r = blockIdx.x * TB + threadIdx.x;
-  if (r >= m) return;
-  const uint32_t ck = u[r];
-  const uint32_t mask = (1u << log_cap) - 1u;
-  const unsigned long long entry = ((unsigned long long)(uint32_t)r << 32) | ck;
-  uint32_t s = hash_slot(ck, log_cap);
-  for (uint32_t probe = 0; probe <= mask; ++probe, s = (s + 1) & mask) {
-    unsigned long long prev = atomicCAS(&table[s], (unsigned long long)HASH_EMPTY, entry);
-    if (prev == HASH_EMPTY) return;
+__global__ __launch_bounds__(TB) void k_emit(Levels L, Emit E, const uint32_t* __restrict__ bits,
+                                             const int32_t* __restrict__ pre,
+                                             const uint32_t* __restrict__ ucell,
+                                             const float* __restrict__ leafmean) {
+  // 32 lanes per item: lane j < 8 emits child j, lane j < 27 neighbour j
+  const int64_t it = ((int64_t)blockIdx.x * TB + threadIdx.x) >> 5;
+  const int j = threadIdx.x & 31;
+  const int d = L.depth;
+  if (it >= E.ibase[d + 1]) return;
+  uint32_t word;
+  if (it < L.batch) {  // depth 0: one root per shape
+    if (j != 0) return;
+    const int b = (int)it;
+    const int32_t r = rank_in(bits, pre, L, 0, E.mbase[0], (uint64_t)b, &word);
+    const bool on = (word >> (b & 31)) & 1u;
+    E.keys[0][b] = (uint32_t)b << 24;
+    E.labels[0][b] = on ? r + 1 : 0;
+    if (on) E.rows[0][r] = b;
+    return;
   }
-}
-
-__device__ __forceinline__ int32_t hash_find(const unsigned long long* table, uint32_t ck,
-                                             int log_cap) {
-  const uint32_t mask = (1u << log_cap) - 1u;
-  uint32_t s = hash_slot(ck, log_cap);
-  for (uint32_t probe = 0; probe <= mask; ++probe, s = (s + 1) & mask) {
-    const unsigned long long e = table[s];
-    if (e == HASH_EMPTY) return -1;
-    if ((uint32_t)e == ck) return (int32_t)(e >> 32);
-  }
-  return -1;
-}
-
-// nbr[g][o]: first-child row 8 rank of the depth-(l-1) octant at parent
-// offset o from group g's parent, -1 if outside the cube or not non-empty.
-__global__ __launch_bounds__(TB) void k_nbr(const uint32_t* __restrict__ uparent, int m, int l,
-                                            const unsigned long long* __restrict__ table,
-                                            int log_cap, int32_t* __restrict__ nbr) {
-  const int t = blockIdx.x * TB + threadIdx.x;
-  if (t >= 27 * m) return;
-  const int g = t / 27, o = t - 27 * g;
+  int l = 1;
+  while (l < d && it >= E.ibase[l + 1]) ++l;
+  const int32_t r = (int32_t)(it - E.ibase[l]);
   const int pl = l - 1;
-  const uint32_t ck = uparent[g];
-  const uint32_t kb = 3u * (uint32_t)pl;
-  const uint32_t b = ck >> kb, key = ck & ((1u << kb) - 1u);
-  const int side = 1 << pl;
-  const int x = (int)squeeze3(key >> 2) + (o / 9 - 1);
-  const int y = (int)squeeze3(key >> 1) + ((o / 3) % 3 - 1);
-  const int z = (int)squeeze3(key) + (o % 3 - 1);
-  int32_t v = -1;
-  if (x >= 0 && x < side && y >= 0 && y < side && z >= 0 && z < side) {
-    const uint32_t nk = (b << kb) | shuffle_key((uint32_t)x, (uint32_t)y, (uint32_t)z);
-    const int32_t r = hash_find(table, nk, log_cap);
-    v = r >= 0 ? 8 * r : -1;
+  const uint64_t p = ucell[E.mbase[pl] + r];  // parent cell at depth l-1
+
+  if (j < 8) {  // child j: cell 8p + j of depth l, row 8r + j
+    const uint64_t cc = (p << 3) + (uint64_t)j;
+    const int32_t rk = rank_in(bits, pre, L, l, E.mbase[l], cc, &word);
+    const bool on = (word >> (cc & 31)) & 1u;
+    const uint32_t kb = 3u * (uint32_t)l;
+    const int64_t row = 8 * (int64_t)r + j;
+    E.keys[l][row] = ((uint32_t)(cc >> kb) << 24) | ((uint32_t)cc & (uint32_t)((1ull << kb) - 1ull));
+    E.labels[l][row] = on ? rk + 1 : 0;
+    if (on) E.rows[l][rk] = (int32_t)row;
+    if (l == d) {
+      float* o = E.signal + 3 * row;
+#pragma unroll
+      for (int a = 0; a < 3; ++a) o[a] = on ? leafmean[3 * (int64_t)rk + a] : 0.f;
+    }
   }
-  nbr[t] = v;
+  if (j < 27) {  // neighbour j of the parent at depth l-1: first-child row or -1
+    const uint32_t pkb = 3u * (uint32_t)pl;
+    const uint32_t pshape = (uint32_t)(p >> pkb);
+    const uint32_t pkey = (uint32_t)p & (uint32_t)((1ull << pkb) - 1ull);
+    const int side = 1 << pl;
+    const int nx = (int)squeeze3(pkey >> 2) + j / 9 - 1;
+    const int ny = (int)squeeze3(pkey >> 1) + (j / 3) % 3 - 1;
+    const int nz = (int)squeeze3(pkey) + j % 3 - 1;
+    int32_t v = -1;
+    if (nx >= 0 && nx < side && ny >= 0 && ny < side && nz >= 0 && nz < side) {
+      const uint64_t q = ((uint64_t)pshape << pkb) |
+                         shuffle_key((uint32_t)nx, (uint32_t)ny, (uint32_t)nz);
+      const int32_t rq = rank_in(bits, pre, L, pl, E.mbase[pl], q, &word);
+      v = ((word >> (q & 31)) & 1u) ? 8 * rq : -1;
+    }
+    E.nbr[l][27 * (int64_t)r + j] = v;
+  }
 }
 
 __global__ __launch_bounds__(TB) void k_fill_u32(uint32_t* __restrict__ p, uint32_t v, int64_t n) {
@@ -432,12 +520,12 @@ __global__ __launch_bounds__(TB) void k_fill_u32(uint32_t* __restrict__ p, uint3
   if (i < n) p[i] = v;
 }
 
-inline int blocks_for(int64_t n) { return (int)oc::cdiv(n, TB); }
+inline unsigned blocks_for(int64_t n) { return (unsigned)oc::cdiv(n, TB); }
 
-// Scratch bump allocator over one device allocation.
+// Bump allocator over one device allocation.
 struct Arena {
   char* base = nullptr;
-  size_t used = 0, cap = 0;
+  size_t used = 0;
   template <class T>
   T* take(int64_t n) {
     T* p = reinterpret_cast<T*>(base + used);
@@ -445,6 +533,28 @@ struct Arena {
     return p;
   }
 };
+
+struct Scratch {
+  uint32_t* bits;
+  int32_t* pre;
+  int32_t* bsum;
+  uint32_t* leafcell;
+  uint2* bstat;
+  uint32_t* ucell;
+  float* leafmean;
+  uint32_t* info;  // [0] flags, [1] max |normal|, [2 + l] M_l
+};
+
+void carve(Arena& a, int B, int64_t P, int64_t nw, int nb, int64_t ucap, Scratch& s) {
+  s.bits = a.take<uint32_t>(nw);
+  s.pre = a.take<int32_t>(nw + 1);
+  s.bsum = a.take<int32_t>(nb + 1);
+  s.leafcell = a.take<uint32_t>(P);
+  s.bstat = a.take<uint2>(oc::cdiv(P, TB));
+  s.ucell = a.take<uint32_t>(ucap);
+  s.leafmean = a.take<float>(3 * P);
+  s.info = a.take<uint32_t>(16);
+}
 
 }  // namespace
 
@@ -456,61 +566,6 @@ void fill_u32(void* p, uint32_t v, int64_t n, hipStream_t s) {
 }
 
 }  // namespace oc
-
-// ---------------------------------------------------------------------------
-// Host orchestration.
-
-namespace {
-
-struct Scratch {
-  uint32_t *k0, *k1;
-  int32_t *v0, *v1;
-  uint32_t* hist;
-  int32_t* offs;
-  uint32_t* tiles;
-  int* counts;  // [l] = M_l for l >= full_depth, [OC_MAX_DEPTH + 1] = range error flag
-  uint32_t* U[OC_MAX_DEPTH + 1];  // compact keys of the non-empty octants of depth l
-  int32_t* J[OC_MAX_DEPTH + 1];   // J[l][r]: index in U[l-1] of the parent of U[l][r]
-  int32_t* first;                 // first sorted point of every non-empty leaf
-};
-
-constexpr int ERR_SLOT = OC_MAX_DEPTH + 1;
-
-void carve(Arena& a, int B, int d, int fd, int64_t P, const int64_t* ub, int nblk_sort,
-           int64_t ntile_max, Scratch& s) {
-  s.k0 = a.take<uint32_t>(P);
-  s.k1 = a.take<uint32_t>(P);
-  s.v0 = a.take<int32_t>(P);
-  s.v1 = a.take<int32_t>(P);
-  s.hist = a.take<uint32_t>(256 * (int64_t)nblk_sort);
-  s.offs = a.take<int32_t>(B + 1);
-  s.tiles = a.take<uint32_t>(ntile_max);
-  s.counts = a.take<int>(16);
-  for (int l = 0; l <= d; ++l) {
-    s.U[l] = a.take<uint32_t>(ub[l]);
-    s.J[l] = l > fd ? a.take<int32_t>(ub[l]) : nullptr;
-  }
-  s.first = a.take<int32_t>(ub[d]);
-}
-
-// Adjacent-unique of n (device count n_dev, or host n_host) sorted keys >> shift.
-void unique_pass(const uint32_t* keys, const int* n_dev, int64_t n_bound, int shift, Scratch& s,
-                 uint32_t* uniq, int32_t* run_of, int32_t* first, int* count, hipStream_t st) {
-  const int ntile = (int)oc::cdiv(n_bound, UQ_TILE);
-  const int nh = n_dev ? 0 : (int)n_bound;
-  hipLaunchKernelGGL(k_unique_count, dim3(ntile), dim3(TB), 0, st, keys, n_dev, nh, shift, s.tiles);
-  hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(TB), 0, st, s.tiles, ntile, count);
-  hipLaunchKernelGGL(k_unique_write, dim3(ntile), dim3(TB), 0, st, keys, n_dev, nh, shift,
-                     (const uint32_t*)s.tiles, uniq, run_of, first);
-}
-
-int ceil_log2(int64_t v) {
-  int b = 0;
-  while ((int64_t(1) << b) < v) ++b;
-  return b;
-}
-
-}  // namespace
 
 extern "C" oc_status oc_build(const float* points, const float* normals,
                               const int32_t* shape_offsets, int32_t batch, int32_t depth,
@@ -530,7 +585,8 @@ extern "C" oc_status oc_build(const float* points, const float* normals,
     if (shape_offsets[b + 1] < shape_offsets[b])
       return fail(OC_ERR_ARG, "oc_build: shape_offsets decrease at %d", b);
   const int64_t P = shape_offsets[batch];
-  if (P > (int64_t(1) << 28)) return fail(OC_ERR_UNSUPPORTED, "oc_build: %lld points > 2^28", (long long)P);
+  if (P > (int64_t(1) << 28))
+    return fail(OC_ERR_UNSUPPORTED, "oc_build: %lld points > 2^28", (long long)P);
   if (P > 0 && (!points || !normals)) return fail(OC_ERR_ARG, "oc_build: points/normals NULL");
   if (((int64_t)batch << (3 * full_depth)) > (int64_t(1) << 28))
     return fail(OC_ERR_UNSUPPORTED, "oc_build: batch * 8^full_depth too large");
@@ -538,72 +594,73 @@ extern "C" oc_status oc_build(const float* points, const float* normals,
   const oc_allocator A = alloc ? *alloc : oc_allocator{nullptr, nullptr, nullptr};
   const int B = batch, d = depth, fd = full_depth;
 
-  // Upper bounds of M_l (exact below full_depth).
-  int64_t ub[OC_MAX_DEPTH + 1] = {};
+  Levels L{};
+  L.depth = d, L.full_depth = fd, L.batch = B;
+  int64_t ucap = 0;  // bound on the set bits of all depths
+  L.wbase[0] = 0;
   for (int l = 0; l <= d; ++l) {
-    const int64_t full = (int64_t)B << (3 * l);
-    ub[l] = l < fd ? full : std::min<int64_t>(P, full);
+    L.cells[l] = (int64_t)B << (3 * l);
+    L.wbase[l + 1] = L.wbase[l] + oc::cdiv(L.cells[l], 32);
+    ucap += l < fd ? L.cells[l] : std::min<int64_t>(P, L.cells[l]);
   }
-  const int nblk_sort = (int)std::max<int64_t>(1, oc::cdiv(P, RS_TILE));
-  const int64_t ntile_max = std::max<int64_t>(1, oc::cdiv(std::max<int64_t>(P, 1), UQ_TILE));
+  const int64_t nw = L.wbase[d + 1];
+  const int nb = (int)oc::cdiv(nw, SCAN_W);
 
   Arena meas;
   Scratch s{};
-  carve(meas, B, d, fd, P, ub, nblk_sort, ntile_max, s);
+  carve(meas, B, P, nw, nb, ucap, s);
   Arena ar;
   ar.base = (char*)oc::dev_alloc(A, meas.used, stream);
   if (!ar.base) return fail(OC_ERR_NOMEM, "oc_build: scratch allocation of %zu bytes failed", meas.used);
-  carve(ar, B, d, fd, P, ub, nblk_sort, ntile_max, s);
+  carve(ar, B, P, nw, nb, ucap, s);
   auto release = [&](void* p) { oc::dev_free(A, p, stream); };
 
-  hipError_t he = hipMemcpyAsync(s.offs, shape_offsets, sizeof(int32_t) * (B + 1),
-                                 hipMemcpyHostToDevice, stream);
-  if (he != hipSuccess) {
-    release(ar.base);
-    return fail(OC_ERR_DEVICE, "oc_build: offsets copy: %s", hipGetErrorString(he));
-  }
-  oc::fill_u32(s.counts, 0u, 16, stream);
-
-  // 1.-2. keys and sort
-  uint32_t* ks = s.k0;
-  int32_t* vs = s.v0;
+  Shapes S;
+  for (int b = 0; b <= B; ++b) S.offs[b] = shape_offsets[b];
+  const int nq = (int)oc::cdiv(P, TB);
+  if (P > 0)
+    hipLaunchKernelGGL(k_quant, dim3(nq), dim3(TB), 0, stream, points, normals, S, B, (int)P, d,
+                       s.leafcell, s.bstat);
+  hipLaunchKernelGGL(k_mark, dim3((unsigned)oc::cdiv(L.cells[d], MK_CELLS)), dim3(MK_TB), 0,
+                     stream, (const uint32_t*)s.leafcell, S, L, s.bits);
+  for (int l = d - MK_UP - 1; l >= fd; --l)
+    hipLaunchKernelGGL(k_reduce, dim3(blocks_for(L.wbase[l + 1] - L.wbase[l])), dim3(TB), 0,
+                       stream, L, l, s.bits);
+  hipLaunchKernelGGL(k_scan_a, dim3(nb), dim3(TB), 0, stream, (const uint32_t*)s.bits, nw, s.bsum);
+  hipLaunchKernelGGL(k_scan_b, dim3(1), dim3(TB), 0, stream, s.bsum, nb);
+  hipLaunchKernelGGL(k_scan_c, dim3(nb), dim3(TB), 0, stream, (const uint32_t*)s.bits, nw,
+                     (const int32_t*)s.bsum, s.pre, nb);
+  hipLaunchKernelGGL(k_compact, dim3(blocks_for(nw)), dim3(TB), 0, stream, L,
+                     (const uint32_t*)s.bits, (const int32_t*)s.pre, s.ucell,
+                     (const uint2*)s.bstat, nq, s.info);
   if (P > 0) {
-    hipLaunchKernelGGL(k_quant_key, dim3(blocks_for(P)), dim3(TB), 0, stream, points, s.offs, B,
-                       (int)P, d, s.k0, s.v0, s.counts + ERR_SLOT);
-    const int bits = 3 * d + ceil_log2(B);
-    uint32_t* kt = s.k1;
-    int32_t* vt = s.v1;
-    for (int shift = 0; shift < bits; shift += 8) {
-      hipLaunchKernelGGL(k_radix_hist, dim3(nblk_sort), dim3(TB), 0, stream, ks, (int)P, shift,
-                         s.hist, nblk_sort);
-      hipLaunchKernelGGL(k_radix_scan, dim3(1), dim3(TB), 0, stream, s.hist, nblk_sort);
-      hipLaunchKernelGGL(k_radix_scatter, dim3(nblk_sort), dim3(TB), 0, stream, ks, vs, kt, vt,
-                         (int)P, shift, (const uint32_t*)s.hist, nblk_sort);
-      std::swap(ks, kt);
-      std::swap(vs, vt);
-    }
-    // 3. non-empty leaves and their first points
-    unique_pass(ks, nullptr, P, 0, s, s.U[d], nullptr, s.first, s.counts + d, stream);
-    // 4. shallower depths down to full_depth
-    for (int l = d - 1; l >= fd; --l)
-      unique_pass(s.U[l + 1], s.counts + (l + 1), std::max<int64_t>(ub[l + 1], 1), 3, s, s.U[l],
-                  s.J[l + 1], nullptr, s.counts + l, stream);
+    int64_t kmax = 1;  // leaf chunks of the largest shape
+    for (int b = 0; b < B; ++b)
+      kmax = std::max<int64_t>(
+          kmax, oc::cdiv(std::min<int64_t>(shape_offsets[b + 1] - shape_offsets[b], L.cells[d] / B),
+                         LM_LEAVES));
+    hipLaunchKernelGGL(k_leaf_mean, dim3((unsigned)B, (unsigned)kmax), dim3(LM_TB), 0, stream,
+                       normals, (const uint32_t*)s.leafcell, S, (int)P, L,
+                       (const uint32_t*)s.bits, (const int32_t*)s.pre, (const uint32_t*)s.ucell,
+                       (const uint32_t*)s.info, s.leafmean);
   }
-  for (int l = 0; l < fd; ++l)
-    hipLaunchKernelGGL(k_iota, dim3(blocks_for(ub[l])), dim3(TB), 0, stream, s.U[l], (int)ub[l]);
 
-  int host_counts[16] = {};
-  he = hipGetLastError();
+  uint32_t info[16] = {};
+  hipError_t he = hipGetLastError();
   if (he == hipSuccess)
-    he = hipMemcpyAsync(host_counts, s.counts, sizeof(host_counts), hipMemcpyDeviceToHost, stream);
+    he = hipMemcpyAsync(info, s.info, sizeof(info), hipMemcpyDeviceToHost, stream);
   if (he == hipSuccess) he = hipStreamSynchronize(stream);
   if (he != hipSuccess) {
     release(ar.base);
     return fail(OC_ERR_DEVICE, "oc_build: %s", hipGetErrorString(he));
   }
-  if (host_counts[ERR_SLOT]) {
+  if (info[0] & 1u) {
     release(ar.base);
     return fail(OC_ERR_RANGE, "oc_build: a point is outside [0,1]^3 or NaN");
+  }
+  if (info[0] & 2u) {
+    release(ar.base);
+    return fail(OC_ERR_RANGE, "oc_build: a normal is not finite");
   }
 
   oc_octree* t = new oc_octree;
@@ -613,7 +670,7 @@ extern "C" oc_status oc_build(const float* points, const float* normals,
   t->alloc = A;
   t->stream = stream;
   for (int l = 0; l <= d; ++l) {
-    t->M[l] = l < fd ? ub[l] : host_counts[l];
+    t->M[l] = info[2 + l];
     t->N[l] = l == 0 ? B : 8 * t->M[l - 1];
     if (t->N[l] > INT32_MAX / 2) {
       release(ar.base);
@@ -648,52 +705,26 @@ extern "C" oc_status oc_build(const float* points, const float* normals,
   }
   t->signal = (float*)take(12 * (size_t)t->N[d]);
 
-  // 5. top-down emission
+  Emit E{};
+  int32_t m = 0;
+  for (int l = 0; l <= d + 1; ++l) {
+    E.mbase[l] = m;
+    if (l <= d) m += (int32_t)t->M[l];
+  }
+  E.ibase[0] = 0;
+  E.ibase[1] = B;
+  for (int l = 1; l <= d; ++l) E.ibase[l + 1] = E.ibase[l] + t->M[l - 1];
   for (int l = 0; l <= d; ++l) {
-    if (t->N[l] > 0)
-      hipLaunchKernelGGL(k_emit_keys, dim3(blocks_for(t->N[l])), dim3(TB), 0, stream,
-                         l > 0 ? (const uint32_t*)s.U[l - 1] : nullptr, (int)t->N[l], l, t->keys[l],
-                         t->labels[l]);
-    if (t->M[l] > 0)
-      hipLaunchKernelGGL(k_emit_labels, dim3(blocks_for(t->M[l])), dim3(TB), 0, stream,
-                         (const uint32_t*)s.U[l], (const int32_t*)s.J[l], (int)t->M[l], l,
-                         (l == 0 || l - 1 < fd) ? 1 : 0, t->labels[l], t->rows[l]);
+    E.keys[l] = t->keys[l];
+    E.labels[l] = t->labels[l];
+    E.rows[l] = t->rows[l];
+    E.nbr[l] = t->nbr[l];
   }
-  // input signal
-  oc::fill_u32(t->signal, 0u, 3 * t->N[d], stream);
-  if (t->M[d] > 0)
-    hipLaunchKernelGGL(k_leaf_mean, dim3(blocks_for(t->M[d])), dim3(TB), 0, stream,
-                       (const int32_t*)s.first, (int)t->M[d], (int)P, (const int32_t*)vs, normals,
-                       (const int32_t*)t->rows[d], t->signal);
-
-  // 6. hash tables and sibling-group neighbour tables
-  int logc[OC_MAX_DEPTH + 1] = {};
-  size_t hbytes = 0;
-  for (int l = 1; l <= d; ++l) {
-    logc[l] = std::max(6, ceil_log2(2 * t->M[l - 1]));
-    if (t->M[l - 1] > 0) hbytes += oc::align256(8ull << logc[l]);
-  }
-  char* hb = hbytes ? (char*)oc::dev_alloc(A, hbytes, stream) : nullptr;
-  if (hbytes && !hb) {
-    release(ar.base);
-    oc_octree_free(t);
-    return fail(OC_ERR_NOMEM, "oc_build: hash allocation of %zu bytes failed", hbytes);
-  }
-  size_t hoff = 0;
-  for (int l = 1; l <= d; ++l) {
-    const int64_t m = t->M[l - 1];
-    if (m == 0) continue;
-    auto* table = (unsigned long long*)(hb + hoff);
-    hoff += oc::align256(8ull << logc[l]);
-    oc::fill_u32(table, 0xFFFFFFFFu, int64_t(2) << logc[l], stream);
-    hipLaunchKernelGGL(k_hash_insert, dim3(blocks_for(m)), dim3(TB), 0, stream,
-                       (const uint32_t*)s.U[l - 1], (int)m, table, logc[l]);
-    hipLaunchKernelGGL(k_nbr, dim3(blocks_for(27 * m)), dim3(TB), 0, stream,
-                       (const uint32_t*)s.U[l - 1], (int)m, l, (const unsigned long long*)table,
-                       logc[l], t->nbr[l]);
-  }
+  E.signal = t->signal;
+  hipLaunchKernelGGL(k_emit, dim3(blocks_for(32 * E.ibase[d + 1])), dim3(TB), 0, stream, L, E,
+                     (const uint32_t*)s.bits, (const int32_t*)s.pre, (const uint32_t*)s.ucell,
+                     (const float*)s.leafmean);
   he = hipGetLastError();
-  if (hb) release(hb);
   release(ar.base);
   if (he != hipSuccess) {
     oc_octree_free(t);

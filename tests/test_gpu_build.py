@@ -85,6 +85,14 @@ def test_build_all_empty_and_errors():
     with pytest.raises(oc.OcError) as e:
         oc.oc_build(nan, nan, [0, 1], 3, 2)
     assert e.value.code == 2
+    good = torch.tensor([[0.5, 0.25, 0.2]], dtype=torch.float32, device="cuda")
+    inf = torch.tensor([[0.0, float("inf"), 0.0]], dtype=torch.float32, device="cuda")
+    with pytest.raises(oc.OcError) as e:
+        oc.oc_build(good, inf, [0, 1], 3, 2)
+    assert e.value.code == 2 and "normal" in str(e.value)
+    # the library stays usable after a rejected build
+    ref, tree = _build_both(good.cpu().numpy(), good.cpu().numpy(), [0, 1], 3, 2)
+    _compare_tree(ref, tree)
 
 
 def test_build_deterministic():

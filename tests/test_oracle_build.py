@@ -123,6 +123,11 @@ def test_boundary_and_errors():
         assert e.value.code == oracle.ERR_RANGE
     with pytest.raises(oracle.OracleError):
         oracle.Octree(np.zeros((1, 3), np.float32), np.ones((1, 3), np.float32), [0, 1], 9, 0)
+    # normals are averaged into the signal, so they must be finite
+    for bad in ([[np.inf, 0, 0]], [[0, np.nan, 0]]):
+        with pytest.raises(oracle.OracleError) as e:
+            oracle.Octree(np.full((1, 3), 0.5, np.float32), np.array(bad, np.float32), [0, 1], 2, 0)
+        assert e.value.code == oracle.ERR_RANGE
 
 
 def test_empty_shape_and_full_depth():
