@@ -160,6 +160,16 @@ oc_status oc_conv_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32
                       oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
                       float* y, void* ws, size_t ws_bytes, int32_t flags, hipStream_t stream);
 
+/* Name, template arguments included (as profilers such as rocprofv3 print
+ * it), of the kernel that does the arithmetic of one pass of a convolution
+ * call with these arguments: pass 0 = oc_conv_fwd, 1 = the input gradient and
+ * 2 = the weight gradient of oc_conv_bwd.  Lets a caller attribute measured
+ * kernel time to the operation it belongs to.  The string lives in
+ * thread-local storage until the next call on the thread; "" (and
+ * oc_last_error set) for invalid arguments. */
+const char* oc_conv_kernel(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                           oc_dtype dt, int32_t cin, int32_t cout, int32_t pass);
+
 /* Bytes of device workspace oc_conv_fwd needs for these arguments. */
 size_t oc_conv_fwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
                              oc_dtype dt, int32_t cin, int32_t cout);
@@ -210,6 +220,13 @@ oc_status oc_unpool_fwd(const oc_octree* tree, int32_t depth, const float* x, co
  *   dy dev f32 [N_l][c];  dx dev f32 [N_{l-1}][c]. */
 oc_status oc_unpool_bwd(const oc_octree* tree, int32_t depth, const float* dy, const uint8_t* sw,
                         int32_t c, float* dx, hipStream_t stream);
+
+/* Profiling: the next launch, on the calling thread, of a kernel that
+ * oc_conv_kernel names is bracketed by these events (recorded at the start
+ * and the end of that kernel on its stream, as hipExtLaunchKernelGGL does),
+ * so that its duration can be measured without host-side gaps.  Both NULL
+ * clears a pending pair.  The caller owns the events. */
+oc_status oc_profile_next(hipEvent_t start, hipEvent_t stop);
 
 const char* oc_status_str(oc_status s);
 const char* oc_last_error(void); /* thread-local message of the last failure */

@@ -24,6 +24,8 @@ __all__ = [
     "load",
     "oc_build",
     "oc_conv_fwd",
+    "oc_conv_kernel",
+    "oc_profile_next",
     "oc_conv_bwd",
     "oc_pool_fwd",
     "oc_pool_bwd",
@@ -42,8 +44,8 @@ STATUS = {0: "OC_OK", 1: "OC_ERR_ARG", 2: "OC_ERR_RANGE", 3: "OC_ERR_NOMEM", 4: 
 # Every symbol include/oc.h declares.
 EXPORTS = (
     "oc_build", "oc_octree_level", "oc_octree_info", "oc_octree_signal", "oc_octree_free",
-    "oc_conv_fwd", "oc_conv_fwd_workspace", "oc_conv_bwd_workspace", "oc_conv_bwd", "oc_pool_fwd", "oc_pool_bwd",
-    "oc_unpool_fwd", "oc_unpool_bwd", "oc_status_str", "oc_last_error",
+    "oc_conv_fwd", "oc_conv_kernel", "oc_conv_fwd_workspace", "oc_conv_bwd_workspace", "oc_conv_bwd", "oc_pool_fwd", "oc_pool_bwd",
+    "oc_unpool_fwd", "oc_unpool_bwd", "oc_status_str", "oc_last_error", "oc_profile_next",
 )
 
 
@@ -119,6 +121,7 @@ def load():
         "oc_octree_free": ([p], None),
         "oc_conv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, sz, i32, p], C.c_int),
         "oc_conv_fwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
+        "oc_conv_kernel": ([p, i32, i32, i32, C.c_int, i32, i32, i32], C.c_char_p),
         "oc_conv_bwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
         "oc_conv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, p, sz, i32, p],
                         C.c_int),
@@ -128,6 +131,7 @@ def load():
         "oc_unpool_bwd": ([p, i32, p, p, i32, p, p], C.c_int),
         "oc_status_str": ([C.c_int], C.c_char_p),
         "oc_last_error": ([], C.c_char_p),
+        "oc_profile_next": ([p, p], C.c_int),
     }
     for name, (args, res) in sigs.items():
         f = getattr(L, name)
@@ -209,6 +213,20 @@ class Octree:
         n = self.num(self.depth)
         return self._view(load().oc_octree_signal(self._h), 3 * n, torch.float32, (n, 3))
 
+    def record_stream(self, stream) -> None:
+        """Mark the octree's arrays as used on `stream` (torch's caching
+        allocator then keeps them until that stream's pending work is done)."""
+        for ptr in self._blocks():
+            _live[ptr].record_stream(stream)
+
+    def _blocks(self):
+        ptrs = set()
+        for lv in self._lv:
+            for p in (lv.keys, lv.labels, lv.rows_of_label, lv.nbr):
+                if p:
+                    ptrs.update(b for b, t in _live.items() if b <= p < b + t.numel())
+        return ptrs
+
     def free(self):
         if getattr(self, "_h", None) is not None and self._h.value:
             load().oc_octree_free(self._h)
@@ -254,6 +272,24 @@ def _conv_dims(tree: Octree, depth: int, stride: int, x, w):
     if x is not None and tuple(x.shape) != (n_in, cin):
         raise OcError(1, f"x has shape {tuple(x.shape)}, expected {(n_in, cin)}")
     return K3, cin, cout, n_in, n_out
+
+
+def oc_profile_next(start, stop) -> None:
+    """Bracket the next conv-pass kernel launch of this thread with two
+    torch.cuda.Event objects (created with enable_timing=True and recorded at
+    least once, so that they exist)."""
+    _check(load().oc_profile_next(C.c_void_p(start.cuda_event) if start is not None else None,
+                                  C.c_void_p(stop.cuda_event) if stop is not None else None))
+
+
+def oc_conv_kernel(tree: Octree, depth: int, ksize: int, stride: int, cin: int, cout: int,
+                   pass_: int, dtype=torch.float32) -> str:
+    """Name of the kernel doing pass 0 (fwd), 1 (input grad) or 2 (weight grad)."""
+    dt = OC_F32 if dtype == torch.float32 else OC_BF16
+    name = load().oc_conv_kernel(tree.handle, depth, ksize, stride, dt, cin, cout, pass_)
+    if not name:
+        raise OcError(1, load().oc_last_error().decode())
+    return name.decode()
 
 
 def oc_conv_fwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tensor,

@@ -5,6 +5,7 @@
 
 namespace {
 thread_local char g_msg[512] = "";
+thread_local hipEvent_t g_prof_start = nullptr, g_prof_stop = nullptr;
 }
 
 namespace oc {
@@ -40,6 +41,12 @@ void dev_free(const oc_allocator& a, void* p, hipStream_t s) {
   }
   // hipFree waits for the device, so pending work on the buffer completes.
   (void)hipFree(p);
+}
+
+void take_profile_events(hipEvent_t* start, hipEvent_t* stop) {
+  *start = g_prof_start;
+  *stop = g_prof_stop;
+  g_prof_start = g_prof_stop = nullptr;
 }
 
 oc_status check_tree_level(const oc_octree* t, int32_t l, int32_t min_l) {
@@ -96,5 +103,13 @@ const char* oc_status_str(oc_status s) {
 }
 
 const char* oc_last_error(void) { return g_msg; }
+
+oc_status oc_profile_next(hipEvent_t start, hipEvent_t stop) {
+  if ((start == nullptr) != (stop == nullptr))
+    return oc::fail(OC_ERR_ARG, "oc_profile_next: give both events or neither");
+  g_prof_start = start;
+  g_prof_stop = stop;
+  return OC_OK;
+}
 
 }  // extern "C"

@@ -1,6 +1,7 @@
 // Internal declarations shared by the HIP sources of liboc.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdarg>
@@ -43,6 +44,19 @@ oc_status check_tree_level(const oc_octree* t, int32_t l, int32_t min_l);
 
 // Fill n 32-bit words of dev memory with v (a kernel, not a memset node).
 void fill_u32(void* p, uint32_t v, int64_t n, hipStream_t s);
+
+// Events set by oc_profile_next for the calling thread, returned once and
+// cleared (both null when none are pending).
+void take_profile_events(hipEvent_t* start, hipEvent_t* stop);
+
+// Launch the kernel that does a convolution pass's arithmetic; it takes the
+// pending profiling events of the thread, if any.
+template <typename F, typename... Args>
+inline void launch_main(F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
+  hipEvent_t a, b;
+  take_profile_events(&a, &b);
+  hipExtLaunchKernelGGL(kernel, grid, block, 0, s, a, b, 0, args...);
+}
 
 }  // namespace oc
 

@@ -252,6 +252,29 @@ size_t bwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype
 
 extern "C" {
 
+const char* oc_conv_kernel(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,
+                           int32_t cin, int32_t cout, int32_t pass) {
+  static thread_local char name[128];
+  name[0] = 0;
+  ConvShape sh;
+  if (pass < 0 || pass > 2) {
+    oc::fail(OC_ERR_ARG, "oc_conv_kernel: pass %d not 0, 1 or 2", pass);
+    return name;
+  }
+  if (check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_kernel") != OC_OK) return name;
+  if (dt == OC_F32 && stride == 1) {
+    oc::conv_s1_kernel_name(t, l, K, cin, cout, pass, name, sizeof(name));
+  } else {
+    const char* ty = dt == OC_F32 ? "float" : "unsigned short";
+    const char* k = pass == 0   ? "k_conv_fwd_simple"
+                    : pass == 2 ? "k_conv_dw_partial_simple"
+                    : stride == 1 ? "k_conv_bwd_data_s1_simple"
+                                  : "k_conv_bwd_data_s2_simple";
+    snprintf(name, sizeof(name), "%s<%s>", k, ty);
+  }
+  return name;
+}
+
 size_t oc_conv_fwd_workspace(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,
                              int32_t cin, int32_t cout) {
   ConvShape sh;
@@ -279,11 +302,11 @@ oc_status oc_conv_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   }
   const unsigned grid = grid_for(sh.n_out * cout);
   if (dt == OC_F32)
-    hipLaunchKernelGGL(k_conv_fwd_simple<float>, dim3(grid), dim3(TB), 0, s,
+    oc::launch_main(k_conv_fwd_simple<float>, dim3(grid), dim3(TB), s,
                        (const int32_t*)t->nbr[l], (const int32_t*)t->labels[l - 1], sh.n_out, stride,
                        K, (const float*)x, cin, (const float*)w, cout, y, relu);
   else
-    hipLaunchKernelGGL(k_conv_fwd_simple<uint16_t>, dim3(grid), dim3(TB), 0, s,
+    oc::launch_main(k_conv_fwd_simple<uint16_t>, dim3(grid), dim3(TB), s,
                        (const int32_t*)t->nbr[l], (const int32_t*)t->labels[l - 1], sh.n_out, stride,
                        K, (const uint16_t*)x, cin, (const uint16_t*)w, cout, y, relu);
   OC_LAUNCH_CHECK();
@@ -323,17 +346,17 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
     const unsigned grid = grid_for(sh.n_in * cin);
     if (stride == 1) {
       if (dt == OC_F32)
-        hipLaunchKernelGGL(k_conv_bwd_data_s1_simple<float>, dim3(grid), dim3(TB), 0, s, nbr,
+        oc::launch_main(k_conv_bwd_data_s1_simple<float>, dim3(grid), dim3(TB), s, nbr,
                            sh.n_in, K, dy, ym, cout, (const float*)w, cin, dx);
       else
-        hipLaunchKernelGGL(k_conv_bwd_data_s1_simple<uint16_t>, dim3(grid), dim3(TB), 0, s, nbr,
+        oc::launch_main(k_conv_bwd_data_s1_simple<uint16_t>, dim3(grid), dim3(TB), s, nbr,
                            sh.n_in, K, dy, ym, cout, (const uint16_t*)w, cin, dx);
     } else {
       if (dt == OC_F32)
-        hipLaunchKernelGGL(k_conv_bwd_data_s2_simple<float>, dim3(grid), dim3(TB), 0, s, nbr,
+        oc::launch_main(k_conv_bwd_data_s2_simple<float>, dim3(grid), dim3(TB), s, nbr,
                            rows_out, sh.n_in, dy, ym, cout, (const float*)w, cin, dx);
       else
-        hipLaunchKernelGGL(k_conv_bwd_data_s2_simple<uint16_t>, dim3(grid), dim3(TB), 0, s, nbr,
+        oc::launch_main(k_conv_bwd_data_s2_simple<uint16_t>, dim3(grid), dim3(TB), s, nbr,
                            rows_out, sh.n_in, dy, ym, cout, (const uint16_t*)w, cin, dx);
     }
   }
@@ -346,10 +369,10 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
       float* part = (float*)ws;
       dim3 grid(grid_for(entries), nparts);
       if (dt == OC_F32)
-        hipLaunchKernelGGL(k_conv_dw_partial_simple<float>, grid, dim3(TB), 0, s, nbr, rows_out,
+        oc::launch_main(k_conv_dw_partial_simple<float>, grid, dim3(TB), s, nbr, rows_out,
                            sh.units, stride, K, (const float*)x, cin, dy, ym, cout, chunk, part);
       else
-        hipLaunchKernelGGL(k_conv_dw_partial_simple<uint16_t>, grid, dim3(TB), 0, s, nbr, rows_out,
+        oc::launch_main(k_conv_dw_partial_simple<uint16_t>, grid, dim3(TB), s, nbr, rows_out,
                            sh.units, stride, K, (const uint16_t*)x, cin, dy, ym, cout, chunk, part);
       hipLaunchKernelGGL(k_reduce_parts, dim3(grid_for(entries)), dim3(TB), 0, s,
                          (const float*)part, nparts, entries, dw);

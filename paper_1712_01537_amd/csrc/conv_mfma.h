@@ -5,6 +5,11 @@
 
 namespace oc {
 
+// Name (with template arguments) of the main kernel of pass 0 (forward),
+// 1 (input gradient) or 2 (weight gradient) of a stride-1 convolution.
+void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, int pass, char* buf,
+                         size_t n);
+
 // Bytes of split-reduction workspace the stride-1 group-tile kernel needs for
 // kk reduction channels and nn output channels at depth l (0: none).
 size_t conv_s1_tile_ws(const oc_octree* t, int l, int K, int kk, int nn);

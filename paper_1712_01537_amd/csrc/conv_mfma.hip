@@ -624,8 +624,8 @@ void launch_tile(const oc_octree* t, int l, const TileCfg& c, const float* x, co
   const int64_t G = t->M[l - 1];
   constexpr int BM = 16 * WM * MR, BN = 16 * (WAVES / WM) * NR;
   dim3 grid((unsigned)oc::cdiv(G, BM / 8), (unsigned)oc::cdiv(nn, BN), (unsigned)c.splits);
-  hipLaunchKernelGGL((k_conv_tile<K, V, MR, NR, WM, FLIP>), grid, dim3(TB), 0, s,
-                     (const int32_t*)t->nbr[l], G, x, xmask, kk, w, nn, out, relu, c.cps, part);
+  oc::launch_main(k_conv_tile<K, V, MR, NR, WM, FLIP>, grid, dim3(TB), s,
+                  (const int32_t*)t->nbr[l], G, x, xmask, kk, w, nn, out, relu, c.cps, part);
   if (c.splits > 1) {
     const int64_t n = t->N[l] * (int64_t)nn;
     hipLaunchKernelGGL(k_sum_split, dim3((unsigned)oc::cdiv(n, TB)), dim3(TB), 0, s,
@@ -692,18 +692,31 @@ void launch_dw(const oc_octree* t, int l, const DwCfg& c, const float* x, int ci
                const float* dy, const float* ym, int cout, float* part, hipStream_t s) {
   if (c.WT == 4) {
     dim3 grid((unsigned)c.nchunks, (unsigned)oc::cdiv(c.tiles, 4));
-    hipLaunchKernelGGL((k_conv_dw<K, VA, VB, TT, MB, 4>), grid, dim3(TB), 0, s,
-                       (const int32_t*)t->nbr[l], t->M[l - 1], c.gchunk, x, cin, dy, ym, cout, part);
+    oc::launch_main(k_conv_dw<K, VA, VB, TT, MB, 4>, grid, dim3(TB), s,
+                    (const int32_t*)t->nbr[l], t->M[l - 1], c.gchunk, x, cin, dy, ym, cout, part);
     return;
   }
   dim3 grid((unsigned)c.nchunks, (unsigned)c.tiles);
-  hipLaunchKernelGGL((k_conv_dw<K, VA, VB, TT, MB, 1>), grid, dim3(TB), 0, s,
+  oc::launch_main(k_conv_dw<K, VA, VB, TT, MB, 1>, grid, dim3(TB), s,
                      (const int32_t*)t->nbr[l], t->M[l - 1], c.gchunk, x, cin, dy, ym, cout, part);
 }
 
 }  // namespace
 
 namespace oc {
+
+void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, int pass, char* buf,
+                         size_t n) {
+  if (pass == 2) {
+    const DwCfg c = pick_dw(K, t->M[l - 1], cin, cout);
+    snprintf(buf, n, "k_conv_dw<%d, %d, %d, %d, %d, %d>", K, c.VA, c.VB, c.TT, c.MB, c.WT);
+    return;
+  }
+  const int kk = pass == 0 ? cin : cout, nn = pass == 0 ? cout : cin;
+  const TileCfg c = pick_tile(K, t->M[l - 1], kk, nn);
+  snprintf(buf, n, "k_conv_tile<%d, %d, %d, %d, %d, %s>", K, c.V, c.MR, c.NR, c.WM,
+           pass == 0 ? "false" : "true");
+}
 
 size_t conv_s1_tile_ws(const oc_octree* t, int l, int K, int kk, int nn) {
   const TileCfg c = pick_tile(K, t->M[l - 1], kk, nn);
