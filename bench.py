@@ -132,12 +132,14 @@ class Step:
 
     # --- accounting -------------------------------------------------------
     def conv_flops(self):
-        """Nominal fwd+bwd flops and output octants of every conv layer."""
+        """Algorithmic flops of the step's conv passes (forward, weight gradient,
+        and input gradient except for the first layer, whose input is the
+        octree's signal) and the output octants of every conv layer."""
         f = o = 0
-        for L in self.wl.layers:
+        for li, L in enumerate(self.wl.layers):
             if L.op == "conv":
                 n = self._n_out(L)
-                f += 6 * n * L.ksize ** 3 * L.cin * L.cout
+                f += (6 if li > 0 else 4) * n * L.ksize ** 3 * L.cin * L.cout
                 o += n
         return f, o
 
@@ -228,19 +230,28 @@ class Step:
                 saved.append((li, x, p, sw))
                 x = p
         g = self.dy_last
+        masked = False  # g already went through the ReLU of the conv below it
         for li, xin, yout, sw in reversed(saved):
             L = wl.layers[li]
             if L.op == "conv":
                 w = self.weights[li]
-                dx, _ = self._run("conv_bwd_data", li, lambda: oc.oc_conv_bwd(
-                    tree, L.depth, L.ksize, L.stride, xin, w, g, y=yout, relu=L.relu,
-                    need_dx=True, need_dw=False))
+                relu = L.relu and not masked
+                if li > 0:  # the first layer's input, the signal, needs no gradient
+                    dx, _ = self._run("conv_bwd_data", li, lambda: oc.oc_conv_bwd(
+                        tree, L.depth, L.ksize, L.stride, xin, w, g, y=yout, relu=relu,
+                        need_dx=True, need_dw=False))
+                else:
+                    dx = None
                 _, dw = self._run("conv_bwd_weight", li, lambda: oc.oc_conv_bwd(
-                    tree, L.depth, L.ksize, L.stride, xin, w, g, y=yout, relu=L.relu,
+                    tree, L.depth, L.ksize, L.stride, xin, w, g, y=yout, relu=relu,
                     need_dx=False, need_dw=True))
-                g = dx
+                g, masked = dx, False
             elif L.op == "pool":
-                g = self._run("pool_bwd", li, lambda: oc.oc_pool_bwd(tree, L.depth, g, sw))
+                # a ReLU right below the pooling: its backward goes into the routing
+                P = wl.layers[li - 1] if li > 0 else None
+                masked = P is not None and P.op == "conv" and P.relu
+                ym = yout if masked else None
+                g = self._run("pool_bwd", li, lambda: oc.oc_pool_bwd(tree, L.depth, g, sw, y=ym))
         return g
 
     def collect(self):
@@ -278,7 +289,7 @@ def cpu_baseline(synth, wl, shapes):
                 pre = oracle.renew(ref.labels(l - 1), pre)
             y = oracle.relu_fwd(pre) if L.relu else pre
             saved.append((li, nb, x, w, pre))
-            flops += 6 * y.shape[0] * L.ksize ** 3 * L.cin * L.cout
+            flops += (6 if li > 0 else 4) * y.shape[0] * L.ksize ** 3 * L.cin * L.cout
             x = y
         elif L.op == "pool":
             y, sw = oracle.pool_fwd(ref.labels(l - 1), x)
@@ -293,7 +304,7 @@ def cpu_baseline(synth, wl, shapes):
             if L.stride == 2:
                 ge = oracle.renew_bwd(ref.labels(l - 1), ge, nb.shape[0])
             oracle.conv_bwd_weight(nb, xin, ge, L.ksize ** 3)
-            g = oracle.conv_bwd_data(nb, ge, w_or_sw, xin.shape[0])
+            g = oracle.conv_bwd_data(nb, ge, w_or_sw, xin.shape[0]) if li > 0 else None
         else:
             g = oracle.pool_bwd(ref.labels(l - 1), g, w_or_sw, ref.num(l))
     dt = time.perf_counter() - t0

@@ -174,7 +174,8 @@ const char* oc_conv_kernel(const oc_octree* tree, int32_t depth, int32_t ksize, 
 size_t oc_conv_fwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
                              oc_dtype dt, int32_t cin, int32_t cout);
 
-/* Bytes of device workspace oc_conv_bwd needs for these arguments. */
+/* Bytes of device workspace oc_conv_bwd needs for these arguments (with or
+ * without OC_FUSE_RELU). */
 size_t oc_conv_bwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
                              oc_dtype dt, int32_t cin, int32_t cout);
 
@@ -204,9 +205,14 @@ oc_status oc_pool_fwd(const oc_octree* tree, int32_t depth, const float* x, int3
 /* Gradient of oc_pool_fwd: dx[8(p-1) + sw[p-1][c]][c] = dy[i][c] for the row
  * i of label p at depth l-1; every other entry of dx is 0.
  *   dy dev f32 [N_{l-1}][c];  sw as produced by oc_pool_fwd;
+ *   y  NULL, or dev f32 [N_{l-1}][c], the pooled output of oc_pool_fwd when
+ *      its input came out of a ReLU (an oc_conv_fwd with OC_FUSE_RELU): the
+ *      ReLU's backward is then applied as well, dx[...][c] = 0 where
+ *      y[i][c] <= 0 (the routed child holds the value y[i][c]), so that dx is
+ *      the gradient w.r.t. the convolution's pre-activation output;
  *   dx dev f32 [N_l][c]. */
 oc_status oc_pool_bwd(const oc_octree* tree, int32_t depth, const float* dy, const uint8_t* sw,
-                      int32_t c, float* dx, hipStream_t stream);
+                      int32_t c, const float* y, float* dx, hipStream_t stream);
 
 /* 2x2x2 max-unpooling from depth l-1 to l (Sec. 3.2 "Unpooling", Fig. 5):
  * y[8(p-1) + sw[p-1][c]][c] = x[i][c] for the row i of label p at depth

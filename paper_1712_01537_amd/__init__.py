@@ -126,7 +126,7 @@ def load():
         "oc_conv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, p, sz, i32, p],
                         C.c_int),
         "oc_pool_fwd": ([p, i32, p, i32, p, p, p], C.c_int),
-        "oc_pool_bwd": ([p, i32, p, p, i32, p, p], C.c_int),
+        "oc_pool_bwd": ([p, i32, p, p, i32, p, p, p], C.c_int),
         "oc_unpool_fwd": ([p, i32, p, p, i32, p, p], C.c_int),
         "oc_unpool_bwd": ([p, i32, p, p, i32, p, p], C.c_int),
         "oc_status_str": ([C.c_int], C.c_char_p),
@@ -344,12 +344,17 @@ def oc_pool_fwd(tree: Octree, depth: int, x: torch.Tensor):
     return y, sw
 
 
-def oc_pool_bwd(tree: Octree, depth: int, dy: torch.Tensor, sw: torch.Tensor) -> torch.Tensor:
+def oc_pool_bwd(tree: Octree, depth: int, dy: torch.Tensor, sw: torch.Tensor,
+                y: torch.Tensor | None = None) -> torch.Tensor:
+    """y: the pooled output, when a ReLU came before the pooling: its backward
+    is then applied too (entries with y <= 0 get no gradient)."""
     c = dy.shape[1]
     n_in, n_out, m = tree.num(depth), tree.num(depth - 1), tree.nonempty(depth - 1)
     dx = torch.empty((n_in, c), dtype=torch.float32, device=dy.device)
+    yp = _dev(y, "y", torch.float32, (n_out, c)) if y is not None else None
     _check(load().oc_pool_bwd(tree.handle, depth, _dev(dy, "dy", torch.float32, (n_out, c)),
-                              _dev(sw, "sw", torch.uint8, (m, c)), c, _dev(dx, "dx"), _stream()))
+                              _dev(sw, "sw", torch.uint8, (m, c)), c, yp, _dev(dx, "dx"),
+                              _stream()))
     return dx
 
 

@@ -1,6 +1,8 @@
 // Error reporting, allocation and octree accessors of the C ABI.
 #include <cstring>
 
+#include <atomic>
+
 #include "common.h"
 
 namespace {
@@ -41,6 +43,19 @@ void dev_free(const oc_allocator& a, void* p, hipStream_t s) {
   }
   // hipFree waits for the device, so pending work on the buffer completes.
   (void)hipFree(p);
+}
+
+int cu_count() {
+  static std::atomic<int> cached[64];
+  int d = 0;
+  if (hipGetDevice(&d) != hipSuccess || d < 0) d = 0;
+  std::atomic<int>* slot = d < 64 ? &cached[d] : nullptr;
+  int n = slot ? slot->load(std::memory_order_relaxed) : 0;
+  if (n > 0) return n;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, d) != hipSuccess || n < 1)
+    n = 1;
+  if (slot) slot->store(n, std::memory_order_relaxed);
+  return n;
 }
 
 void take_profile_events(hipEvent_t* start, hipEvent_t* stop) {

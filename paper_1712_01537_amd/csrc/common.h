@@ -42,6 +42,9 @@ inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 // Check a level argument and return its sizes.
 oc_status check_tree_level(const oc_octree* t, int32_t l, int32_t min_l);
 
+// Compute units of the current device (cached per device).
+int cu_count();
+
 // Fill n 32-bit words of dev memory with v (a kernel, not a memset node).
 void fill_u32(void* p, uint32_t v, int64_t n, hipStream_t s);
 

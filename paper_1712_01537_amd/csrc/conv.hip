@@ -39,6 +39,22 @@ __device__ __forceinline__ int32_t tap_row(const int32_t* nb, int c, int dx, int
   return base < 0 ? -1 : base + 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
 }
 
+// ReLU backward: dym[e] = y[e] > 0 ? dy[e] : 0, four entries per thread.
+__global__ __launch_bounds__(TB) void k_relu_mask(const float* __restrict__ y,
+                                                  const float* __restrict__ dy, int64_t n,
+                                                  int vec, float* __restrict__ dym) {
+  const int64_t e = 4 * ((int64_t)blockIdx.x * TB + threadIdx.x);
+  if (e >= n) return;
+  if (vec && e + 4 <= n) {  // vec: y, dy (and dym) are 16-byte aligned
+    const float4 a = *reinterpret_cast<const float4*>(y + e);
+    const float4 g = *reinterpret_cast<const float4*>(dy + e);
+    *reinterpret_cast<float4*>(dym + e) = float4{a.x > 0.f ? g.x : 0.f, a.y > 0.f ? g.y : 0.f,
+                                                 a.z > 0.f ? g.z : 0.f, a.w > 0.f ? g.w : 0.f};
+  } else {
+    for (int64_t i = e; i < n; ++i) dym[i] = y[i] > 0.f ? dy[i] : 0.f;
+  }
+}
+
 // Forward.  stride 1: output row i = group i>>3, child i&7.  stride 2:
 // output row i of depth l-1 with label L > 0 evaluates child 0 of group L-1.
 template <typename T>
@@ -233,15 +249,22 @@ size_t fwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype
   return 0;
 }
 
+// The matrix-core path applies the ReLU backward once, into the workspace,
+// ahead of both gradients.
+size_t mask_ws_bytes(const ConvShape& sh, int cout) {
+  return oc::align256((size_t)sh.n_out * cout * sizeof(float));
+}
+
 size_t bwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,
                     int cout) {
   if (sh.units == 0) return 0;
   const size_t entries = (size_t)sh.K3 * cin * cout;
   if (dt == OC_F32 && sh.stride == 1) {
-    // input gradient, then weight gradient: the same bytes serve both in stream order
+    // the ReLU-masked upstream gradient, then the input gradient's and the
+    // weight gradient's partial sums: the same bytes serve both in stream order
     const size_t a = oc::conv_s1_tile_ws(t, l, sh.K, cout, cin);
     const size_t b = oc::conv_s1_dw_parts(t, l, sh.K, cin, cout) * entries * sizeof(float);
-    return std::max(a, b);
+    return mask_ws_bytes(sh, cout) + std::max(a, b);
   }
   int nparts;
   dw_chunk(sh, cin, cout, &nparts);
@@ -337,11 +360,22 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   int nparts = 0;
   const int64_t chunk = dw_chunk(sh, cin, cout, &nparts);
   const bool mfma = dt == OC_F32 && stride == 1;
+  float* wsf = (float*)ws;
+  if (mfma && (dx || dw)) {
+    if (ym && sh.n_out > 0) {  // dy masked once, read by both gradients
+      const int64_t n = sh.n_out * (int64_t)cout;
+      const int vec = ((uintptr_t)y % 16 == 0 && (uintptr_t)dy % 16 == 0 && (uintptr_t)wsf % 16 == 0);
+      hipLaunchKernelGGL(k_relu_mask, dim3((unsigned)oc::cdiv(n, 4 * TB)), dim3(TB), 0, s, y, dy,
+                         n, vec, wsf);
+      dy = wsf;
+    }
+    wsf += mask_ws_bytes(sh, cout) / sizeof(float);
+  }
   const int64_t entries = (int64_t)sh.K3 * cin * cout;
   const int32_t* nbr = t->nbr[l];
   const int32_t* rows_out = t->rows[l - 1];
   if (dx && sh.n_in > 0 && mfma) {
-    oc::conv_s1_bwd_data_f32(t, l, K, dy, ym, cout, (const float*)w, cin, dx, (float*)ws, s);
+    oc::conv_s1_bwd_data_f32(t, l, K, dy, cout, (const float*)w, cin, dx, wsf, s);
   } else if (dx && sh.n_in > 0) {
     const unsigned grid = grid_for(sh.n_in * cin);
     if (stride == 1) {
@@ -364,7 +398,7 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
     if (sh.units == 0) {
       oc::fill_u32(dw, 0u, entries, s);
     } else if (mfma) {
-      oc::conv_s1_bwd_weight_f32(t, l, K, (const float*)x, cin, dy, ym, cout, dw, (float*)ws, s);
+      oc::conv_s1_bwd_weight_f32(t, l, K, (const float*)x, cin, dy, cout, dw, wsf, s);
     } else {
       float* part = (float*)ws;
       dim3 grid(grid_for(entries), nparts);

@@ -21,10 +21,9 @@ void conv_s1_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin, 
                      int cout, float* y, int relu, float* ws, hipStream_t s);
 
 // dx [N_l][cin] = input gradient of a stride-1 convolution for upstream
-// gradient dy [N_l][cout]; ymask (nullable) masks dy with [ymask > 0].
-// ws: conv_s1_tile_ws(t, l, K, cout, cin) bytes.
-void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, const float* ymask,
-                          int cout, const float* w, int cin, float* dx, float* ws, hipStream_t s);
+// gradient dy [N_l][cout].  ws: conv_s1_tile_ws(t, l, K, cout, cin) bytes.
+void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, int cout,
+                          const float* w, int cin, float* dx, float* ws, hipStream_t s);
 
 // Number of [K^3][cin][cout] fp32 partial sums conv_s1_bwd_weight_f32 needs.
 size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout);
@@ -32,7 +31,6 @@ size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout);
 // dw [K^3][cin][cout] = weight gradient of a stride-1 convolution; part holds
 // conv_s1_dw_parts() partial sums.
 void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, int cin,
-                            const float* dy, const float* ymask, int cout, float* dw, float* part,
-                            hipStream_t s);
+                            const float* dy, int cout, float* dw, float* part, hipStream_t s);
 
 }  // namespace oc

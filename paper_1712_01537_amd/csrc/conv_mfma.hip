@@ -10,9 +10,9 @@
 // output child c, tap d reads tile position c + d + r, with no indirection.
 //
 //   forward      out[i][n] = sum_k sum_c x[nb(i,k)][c] W[k][c][n]
-//   input grad   the same with x = dY (optionally masked by [y > 0]) and
-//                W'[k][c][n] = W[K^3-1-k][n][c]: for stride 1 the
-//                neighbour relation is symmetric under d -> -d.
+//   input grad   the same with x = dY and W'[k][c][n] = W[K^3-1-k][n][c]:
+//                for stride 1 the neighbour relation is symmetric under
+//                d -> -d.
 //
 // MFMA operand layout (16x16x4, fp32): lane l supplies A[l%16][l/16] and
 // B[l/16][l%16] and receives D[4(l/16)+j][l%16] in accumulator j.  Rows of
@@ -66,14 +66,21 @@ __device__ __forceinline__ int32_t tile_src(const int32_t* __restrict__ nb, int 
 // padding rows per x-slab and rows of RS = CC + 4 floats, which puts the
 // eight children of a group (and 16 consecutive weight columns) on distinct
 // LDS banks.
-// Grid: x = ceil(groups / (BM/8)), y = ceil(nn / BN), z = splits of the
+// Workgroups are persistent over a contiguous range of row tiles.  The loads
+// of the next step (the next weight slab; at the end of a chunk also the next
+// chunk's or the next tile's group tiles) are issued before each step's
+// MFMAs, the neighbour entries a whole tile ahead.  Every prefetch writes the
+// same registers on one straight-line path: addresses are clamped to valid
+// memory and out-of-range elements are zeroed when the registers are stored
+// to LDS, so no load result is copied (and waited for) before the MFMAs.
+// VEC: kk and nn are multiples of 4, so rows of x and W are read as float4.
+// Grid: x = persistent workgroups, y = ceil(nn / BN), z = splits of the
 // reduction channels, cps chunks each.  With one split the result (ReLU
 // applied if relu) goes to out; otherwise split z writes its partial sum to
 // part[z][row][n] and k_sum_split finishes.
-template <int K, int V, int MR, int NR, int WM, bool FLIP>
+template <int K, int V, int MR, int NR, int WM, bool FLIP, bool VEC>
 __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nbr, int64_t ngroups,
-                                                  const float* __restrict__ x,
-                                                  const float* __restrict__ xmask, int kk,
+                                                  const float* __restrict__ x, int kk,
                                                   const float* __restrict__ w, int nn,
                                                   float* __restrict__ out, int relu, int cps,
                                                   float* __restrict__ part) {
@@ -94,24 +101,27 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
   constexpr int GPP = TB / (S3 * F4) > 0 ? TB / (S3 * F4) : 1;
   constexpr int NA = GPB / GPP;
   constexpr int NB = (TSL * BN * F4 + TB - 1) / TB;
+  static_assert(S3 * F4 <= TB && GPB % GPP == 0, "tile staging must cover every position");
+  static_assert(NA <= 32 && NB <= 32, "validity bits fit a word");
   __shared__ __attribute__((aligned(16))) float At[GPB * P3 * RS];
   __shared__ __attribute__((aligned(16))) float Bt[TSL * BN * RS];
-  __shared__ int32_t Src[GPB * S3];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int li = lane & 15, q = lane >> 4;
   const int wm = wave % WM, wn = wave / WM;
-  const int64_t g0 = (int64_t)blockIdx.x * GPB;
   const int n0 = blockIdx.y * BN;
   const int cb = blockIdx.z * cps * CC;
   const int ce = cb + cps * CC < kk ? cb + cps * CC : kk;
-
-  // source rows of every tile position of the workgroup's groups, once
-  for (int e = tid; e < GPB * S3; e += TB) {
-    const int gl = e / S3, p = e - gl * S3;
-    const int64_t g = g0 + gl;
-    Src[e] = g < ngroups ? tile_src<R>(nbr + 27 * g, p / (S * S), (p / S) % S, p % S) : -1;
-  }
+  const int nchunk = cb < ce ? (ce - cb + CC - 1) / CC : 0;
+  // Row tiles, a contiguous range per workgroup.  The workgroup of linear
+  // index b runs on XCD b % 8, so the ranges are handed out XCD by XCD:
+  // neighbouring tiles, whose gathers share halo rows, then run under the
+  // same L2 (gridDim.x is a multiple of 8 when it is >= 8).
+  const int64_t ntile = (ngroups + GPB - 1) / GPB;
+  const int nx = gridDim.x, bx = blockIdx.x;
+  const int lb = nx >= 8 ? (bx % 8) * (nx / 8) + bx / 8 : bx;
+  const int64_t tile0 = ntile * lb / nx, mytiles = ntile * (lb + 1) / nx - tile0;
+  if (mytiles <= 0 || nchunk <= 0) return;  // uniform over the workgroup
 
   const int c = li & 7;
   const int cx = c >> 2, cy = (c >> 1) & 1, cz = c & 1;
@@ -132,182 +142,218 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
   // this thread's tile element: group a_g + GPP i, position a_p, channels 4 a_f..
   const bool a_on = tid < GPP * S3 * F4;
   const int a_g = tid / (S3 * F4), a_p = (tid / F4) % S3, a_f = tid % F4;
-  const int a_lds = (a_g * P3 + (a_p / (S * S)) * PX + ((a_p / S) % S) * S + a_p % S) * RS + 4 * a_f;
-  v4f ra[NA], rm[FLIP ? NA : 1];
+  const int a_px = a_p / (S * S), a_py = (a_p / S) % S, a_pz = a_p % S;
+  const int a_lds = (a_g * P3 + a_px * PX + a_py * S + a_pz) * RS + 4 * a_f;
+  // the position's parent-offset slot in the 27-entry neighbour row, and child
+  const int a_ux = a_px - R, a_uy = a_py - R, a_uz = a_pz - R;
+  const int a_slot = ((a_ux >> 1) + 1) * 9 + ((a_uy >> 1) + 1) * 3 + ((a_uz >> 1) + 1);
+  const int a_coff = 4 * (a_ux & 1) + 2 * (a_uy & 1) + (a_uz & 1);
 
-  // global -> registers: the tile of channel chunk c0 (mask values are kept
-  // apart so that no wait is needed before the compute that follows)
-  auto load_a = [&](int c0) {
-    const int ch = c0 + 4 * a_f;
+  // neighbour entries of this thread's positions: nbc for the tile being
+  // gathered, nbn for the one after; entries of groups past the end read
+  // entry 0 and are flagged -1 when used
+  int32_t nbc[NA], nbn[NA];
+  uint32_t okc = 0, okn = 0;
+  auto load_nb = [&](int64_t t, int32_t (&v)[NA], uint32_t& ok) {
+    const int64_t g0 = (tile0 + t) * GPB;
+    ok = 0;
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
-      const int32_t src = a_on ? Src[(a_g + GPP * i) * S3 + a_p] : -1;
-      v4f v = {0.f, 0.f, 0.f, 0.f}, m = {1.f, 1.f, 1.f, 1.f};
-      if (src >= 0 && ch < kk) {
-        const float* xr = x + (int64_t)src * kk + ch;
-        const float* xm = xmask ? xmask + (int64_t)src * kk + ch : nullptr;
-        if (ch + 4 <= kk && (kk & 3) == 0) {
-          v = *reinterpret_cast<const v4f*>(xr);
-          if (FLIP && xm) m = *reinterpret_cast<const v4f*>(xm);
-        } else {
+      const int64_t g = g0 + a_g + GPP * i;
+      const bool live = a_on && t < mytiles && g < ngroups;
+      v[i] = nbr[live ? 27 * g + a_slot : 0];
+      ok |= (uint32_t)live << i;
+    }
+  };
+
+  // global -> registers: the tile of channel chunk c0
+  v4f ra[NA];
+  uint32_t aok = 0;
+  int a_c0 = 0;
+  auto load_a = [&](int c0) {
+    const int ch = c0 + 4 * a_f;
+    a_c0 = c0;
+    aok = 0;
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (ch + j < kk) {
-              v[j] = xr[j];
-              if (FLIP && xm) m[j] = xm[j];
-            }
-        }
+    for (int i = 0; i < NA; ++i) {
+      const bool live = ((okc >> i) & 1) && nbc[i] >= 0 && ch < kk;
+      const int64_t off = live ? (int64_t)(nbc[i] + a_coff) * kk + ch : 0;
+      if constexpr (VEC) {
+        ra[i] = *reinterpret_cast<const v4f*>(x + off);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) ra[i][j] = x[off + (live && ch + j < kk ? j : 0)];
       }
-      ra[i] = v;
-      if constexpr (FLIP) rm[i] = m;
+      aok |= (uint32_t)live << i;
     }
   };
   auto store_a = [&]() {
     if (!a_on) return;
+    const int ch = a_c0 + 4 * a_f;
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       v4f v = ra[i];
-      if constexpr (FLIP) {
+      const bool live = (aok >> i) & 1;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = rm[i][j] > 0.f ? v[j] : 0.f;
-      }
+      for (int j = 0; j < 4; ++j) v[j] = live && ch + j < kk ? v[j] : 0.f;
       *reinterpret_cast<v4f*>(&At[a_lds + i * GPP * P3 * RS]) = v;
     }
   };
 
   // weight slab element of this thread, pass i
   float4 rb[NB];
+  uint32_t bok = 0;
+  int b_c0 = 0;
   auto load_b = [&](int c0, int k0) {
+    b_c0 = c0;
+    bok = 0;
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int e = tid + i * TB;
-      float4 v = {0.f, 0.f, 0.f, 0.f};
       if constexpr (FLIP) {  // (t, n, f): 4 consecutive channels of W[K3-1-k][n]
         const int f = e % F4, n = (e / F4) % BN, t = e / (F4 * BN);
         const int gn = n0 + n, ch = c0 + 4 * f;
-        if (t < TSL && gn < nn && ch < kk) {
-          const float* wr = w + ((int64_t)(K3 - 1 - (k0 + t)) * nn + gn) * kk + ch;
-          if (ch + 4 <= kk && (kk & 3) == 0) {
-            v = *reinterpret_cast<const float4*>(wr);
-          } else {
-            v.x = wr[0];
-            if (ch + 1 < kk) v.y = wr[1];
-            if (ch + 2 < kk) v.z = wr[2];
-            if (ch + 3 < kk) v.w = wr[3];
-          }
+        const bool live = t < TSL && gn < nn && ch < kk;
+        const int64_t off = live ? ((int64_t)(K3 - 1 - (k0 + t)) * nn + gn) * kk + ch : 0;
+        if constexpr (VEC) {
+          rb[i] = *reinterpret_cast<const float4*>(w + off);
+        } else {
+          rb[i].x = w[off];
+          rb[i].y = w[off + (live && ch + 1 < kk ? 1 : 0)];
+          rb[i].z = w[off + (live && ch + 2 < kk ? 2 : 0)];
+          rb[i].w = w[off + (live && ch + 3 < kk ? 3 : 0)];
         }
+        bok |= (uint32_t)live << i;
       } else {  // (t, cc, n4): 4 consecutive columns of W[k][ch]
         const int n4 = e % (BN / 4), cc = (e / (BN / 4)) % CC, t = e / (BN / 4 * CC);
         const int gn = n0 + 4 * n4, ch = c0 + cc;
-        if (t < TSL && ch < kk) {
-          const float* wr = w + ((int64_t)(k0 + t) * kk + ch) * nn + gn;
-          if (gn + 4 <= nn && (nn & 3) == 0) {
-            v = *reinterpret_cast<const float4*>(wr);
-          } else {
-            if (gn < nn) v.x = wr[0];
-            if (gn + 1 < nn) v.y = wr[1];
-            if (gn + 2 < nn) v.z = wr[2];
-            if (gn + 3 < nn) v.w = wr[3];
-          }
+        const bool live = t < TSL && ch < kk && gn < nn;
+        const int64_t off = live ? ((int64_t)(k0 + t) * kk + ch) * nn + gn : 0;
+        if constexpr (VEC) {
+          rb[i] = *reinterpret_cast<const float4*>(w + off);
+        } else {
+          rb[i].x = w[off];
+          rb[i].y = w[off + (live && gn + 1 < nn ? 1 : 0)];
+          rb[i].z = w[off + (live && gn + 2 < nn ? 2 : 0)];
+          rb[i].w = w[off + (live && gn + 3 < nn ? 3 : 0)];
         }
+        bok |= (uint32_t)live << i;
       }
-      rb[i] = v;
     }
   };
   auto store_b = [&]() {
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int e = tid + i * TB;
+      const bool live = (bok >> i) & 1;
       if constexpr (FLIP) {
         const int f = e % F4, n = (e / F4) % BN, t = e / (F4 * BN);
-        if (t < TSL) *reinterpret_cast<float4*>(&Bt[(t * BN + n) * RS + 4 * f]) = rb[i];
+        const int ch = b_c0 + 4 * f;
+        if (t < TSL) {
+          const float4 v = rb[i];
+          *reinterpret_cast<float4*>(&Bt[(t * BN + n) * RS + 4 * f]) =
+              float4{live ? v.x : 0.f, live && ch + 1 < kk ? v.y : 0.f,
+                     live && ch + 2 < kk ? v.z : 0.f, live && ch + 3 < kk ? v.w : 0.f};
+        }
       } else {
         const int n4 = e % (BN / 4), cc = (e / (BN / 4)) % CC, t = e / (BN / 4 * CC);
+        const int gn = n0 + 4 * n4;
         if (t < TSL) {
           float* d = &Bt[(t * BN + 4 * n4) * RS + cc];
-          d[0] = rb[i].x;
-          d[RS] = rb[i].y;
-          d[2 * RS] = rb[i].z;
-          d[3 * RS] = rb[i].w;
+          d[0] = live ? rb[i].x : 0.f;
+          d[RS] = live && gn + 1 < nn ? rb[i].y : 0.f;
+          d[2 * RS] = live && gn + 2 < nn ? rb[i].z : 0.f;
+          d[3 * RS] = live && gn + 3 < nn ? rb[i].w : 0.f;
         }
       }
     }
   };
 
-  __syncthreads();  // Src ready
-  if (cb < ce) {
-    load_a(cb);
-    load_b(cb, 0);
-  }
-  for (int c0 = cb; c0 < ce; c0 += CC) {
-    for (int sl = 0; sl < NSL; ++sl) {
-      const int k0 = sl * TSL;
-      __syncthreads();  // the previous step's LDS reads are done
-      if (sl == 0) store_a();
-      store_b();
-      __syncthreads();
-      // prefetch the next step while this one computes
-      if (sl + 1 < NSL) {
-        load_b(c0, k0 + TSL);
-      } else if (c0 + CC < ce) {
-        load_a(c0 + CC);
-        load_b(c0 + CC, 0);
-      }
+  auto compute = [&](int k0) {
 #pragma unroll 3
-      for (int t = 0; t < TSL; ++t) {
-        const int k = k0 + t;
-        const int toff = (k / K2) * PX + ((k / K) % K) * S + k % K;
-        float a[MR][V], b[NR][V];
+    for (int tp = 0; tp < TSL; ++tp) {
+      const int k = k0 + tp;
+      const int toff = (k / K2) * PX + ((k / K) % K) * S + k % K;
+      float a[MR][V], b[NR][V];
 #pragma unroll
-        for (int mr = 0; mr < MR; ++mr) {
-          const float* tp = &At[(tbase[mr] + toff) * RS + V * q];
-          if constexpr (V == 4) {
-            const v4f u = *reinterpret_cast<const v4f*>(tp);
+      for (int mr = 0; mr < MR; ++mr) {
+        const float* tpp = &At[(tbase[mr] + toff) * RS + V * q];
+        if constexpr (V == 4) {
+          const v4f u = *reinterpret_cast<const v4f*>(tpp);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) a[mr][j] = u[j];
-          } else {
-            a[mr][0] = tp[0];
-          }
+          for (int j = 0; j < 4; ++j) a[mr][j] = u[j];
+        } else {
+          a[mr][0] = tpp[0];
         }
+      }
 #pragma unroll
-        for (int nr = 0; nr < NR; ++nr) {
-          const float* bp = &Bt[(t * BN + bcol[nr]) * RS + V * q];
-          if constexpr (V == 4) {
-            const v4f u = *reinterpret_cast<const v4f*>(bp);
+      for (int nr = 0; nr < NR; ++nr) {
+        const float* bp = &Bt[(tp * BN + bcol[nr]) * RS + V * q];
+        if constexpr (V == 4) {
+          const v4f u = *reinterpret_cast<const v4f*>(bp);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) b[nr][j] = u[j];
-          } else {
-            b[nr][0] = bp[0];
-          }
+          for (int j = 0; j < 4; ++j) b[nr][j] = u[j];
+        } else {
+          b[nr][0] = bp[0];
         }
+      }
 #pragma unroll
-        for (int j = 0; j < V; ++j)
+      for (int j = 0; j < V; ++j)
 #pragma unroll
-          for (int mr = 0; mr < MR; ++mr)
+        for (int mr = 0; mr < MR; ++mr)
 #pragma unroll
-            for (int nr = 0; nr < NR; ++nr) acc[mr][nr] = mfma4(a[mr][j], b[nr][j], acc[mr][nr]);
+          for (int nr = 0; nr < NR; ++nr) acc[mr][nr] = mfma4(a[mr][j], b[nr][j], acc[mr][nr]);
+    }
+  };
+
+  load_nb(0, nbc, okc);
+  load_nb(1, nbn, okn);
+  load_a(cb);
+  load_b(cb, 0);
+  for (int64_t t = 0; t < mytiles; ++t) {
+    for (int ci = 0; ci < nchunk; ++ci) {
+      const int c0 = cb + ci * CC;
+      const bool last = ci + 1 == nchunk;
+#pragma unroll
+      for (int sl = 0; sl < NSL; ++sl) {
+        __syncthreads();  // the previous step's LDS reads are done
+        if (sl == 0) store_a();
+        store_b();
+        __syncthreads();
+        if (sl + 1 < NSL) {
+          load_b(c0, (sl + 1) * TSL);
+        } else {  // the next chunk of this tile, or the first chunk of the next tile
+#pragma unroll
+          for (int i = 0; i < NA; ++i) nbc[i] = last ? nbn[i] : nbc[i];
+          okc = last ? okn : okc;
+          load_nb(last ? t + 2 : t + 1, nbn, okn);
+          const int nc0 = last ? cb : c0 + CC;
+          load_a(nc0);
+          load_b(nc0, 0);
+        }
+        compute(sl * TSL);
       }
     }
-  }
-
-  // epilogue: accumulator j of lane l is row 4(l/16)+j, column l%16
-  const int64_t nrows = 8 * ngroups;
-  const bool split = gridDim.z > 1;
-  float* dst = split ? part + (int64_t)blockIdx.z * nrows * nn : out;
+    // the tile is complete: accumulator j of lane l is row 4(l/16)+j, column l%16
+    const int64_t g0 = (tile0 + t) * GPB;
+    const int64_t nrows = 8 * ngroups;
+    const bool split = gridDim.z > 1;
+    float* dst = split ? part + (int64_t)blockIdx.z * nrows * nn : out;
 #pragma unroll
-  for (int mr = 0; mr < MR; ++mr) {
-    const int64_t rbase = 8 * g0 + (wm * MR + mr) * 16 + 4 * q;
+    for (int mr = 0; mr < MR; ++mr) {
+      const int64_t rbase = 8 * g0 + (wm * MR + mr) * 16 + 4 * q;
 #pragma unroll
-    for (int nr = 0; nr < NR; ++nr) {
-      const int n = n0 + bcol[nr];
-      if (n >= nn) continue;
+      for (int nr = 0; nr < NR; ++nr) {
+        const int n = n0 + bcol[nr];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int64_t row = rbase + j;
-        if (row < nrows) {
-          const float v = acc[mr][nr][j];
-          dst[row * nn + n] = (!split && relu) ? fmaxf(v, 0.f) : v;
+        for (int j = 0; j < 4; ++j) {
+          const int64_t row = rbase + j;
+          if (n < nn && row < nrows) {
+            const float v = acc[mr][nr][j];
+            dst[row * nn + n] = (!split && relu) ? fmaxf(v, 0.f) : v;
+          }
         }
+        acc[mr][nr] = v4f{0.f, 0.f, 0.f, 0.f};
       }
     }
   }
@@ -325,9 +371,8 @@ __global__ __launch_bounds__(TB) void k_sum_split(const float* __restrict__ part
 
 // ---------------------------------------------------------------------------
 // Weight gradient partial sums, stride 1:
-//   dW[k][c][n] = sum over octants i of x[nb(i,k)][c] * dY[i][n]  (dY masked by
-//   [y > 0] when ymask is given), an M x N = (tap, channel) x (output channel)
-//   GEMM whose reduction runs over the octants, four per MFMA step: the
+//   dW[k][c][n] = sum over octants i of x[nb(i,k)][c] * dY[i][n], an M x N =
+//   (tap, channel) x (output channel) GEMM whose reduction runs over the octants, four per MFMA step: the
 //   children 4h + q (q = lane / 16) of one sibling group.
 // Operand loads go straight to global memory, where one 16-lane slice reads
 // one row: with VA > 1 lane i loads channels VA i .. VA i + VA - 1 of it in one
@@ -363,8 +408,7 @@ __device__ __forceinline__ void ldv(const float* p, int valid, float (&v)[V]) {
 template <int K, int VA, int VB, int TT, int MB, int WT>
 __global__ __launch_bounds__(TB) void k_conv_dw(const int32_t* __restrict__ nbr, int64_t ngroups,
                                                 int64_t gchunk, const float* __restrict__ x,
-                                                int cin, const float* __restrict__ dy,
-                                                const float* __restrict__ ymask, int cout,
+                                                int cin, const float* __restrict__ dy, int cout,
                                                 float* __restrict__ part) {
   constexpr int R = (K - 1) / 2, K3 = K * K * K;
   constexpr bool FLAT = MB > 0;
@@ -437,14 +481,8 @@ __global__ __launch_bounds__(TB) void k_conv_dw(const int32_t* __restrict__ nbr,
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int64_t orow = 8 * g + 4 * h + q;
-      float b[VB], m[VB];
-      const bool live = g < ge;
-      ldv<VB>(dy + orow * cout + n0, live ? nval : 0, b);
-      if (ymask) {
-        ldv<VB>(ymask + orow * cout + n0, live ? nval : 0, m);
-#pragma unroll
-        for (int s = 0; s < VB; ++s) b[s] = m[s] > 0.f ? b[s] : 0.f;
-      }
+      float b[VB];
+      ldv<VB>(dy + orow * cout + n0, g < ge ? nval : 0, b);
 #pragma unroll
       for (int s = 0; s < VB; ++s) Bv[h][s] = b[s];
 #pragma unroll
@@ -594,13 +632,15 @@ void sum_parts(const float* part, int np, int64_t n, float* seg, float* out, hip
 
 struct TileCfg {
   int V, MR, NR, WM, splits, cps;
+  bool VEC;
 };
 
 // Workgroup tile and split of the reduction for a stride-1 layer of G groups
 // (chosen from measurements of the depth-2..6 layers of the 32-shape batch).
 TileCfg pick_tile(int K, int64_t G, int kk, int nn) {
   TileCfg c;
-  c.V = (K == 3 && kk >= 16) ? 4 : 1;
+  c.VEC = kk % 4 == 0 && nn % 4 == 0;
+  c.V = (K == 3 && kk >= 16 && c.VEC) ? 4 : 1;
   c.WM = 4;
   if (c.V == 1 && K == 3) {
     c.MR = 2, c.NR = 1;  // 128 x 16
@@ -617,15 +657,26 @@ TileCfg pick_tile(int K, int64_t G, int kk, int nn) {
   return c;
 }
 
-template <int K, int V, int MR, int NR, int WM, bool FLIP>
-void launch_tile(const oc_octree* t, int l, const TileCfg& c, const float* x, const float* xmask,
-                 int kk, const float* w, int nn, float* out, int relu, float* part,
-                 hipStream_t s) {
+template <int K, int V, int MR, int NR, int WM, bool FLIP, bool VEC>
+void launch_tile(const oc_octree* t, int l, const TileCfg& c, const float* x, int kk,
+                 const float* w, int nn, float* out, int relu, float* part, hipStream_t s) {
+  const auto kernel = k_conv_tile<K, V, MR, NR, WM, FLIP, VEC>;
+  static const int occ = [&] {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, TB, 0) != hipSuccess || n < 1)
+      n = 1;
+    return n;
+  }();
   const int64_t G = t->M[l - 1];
   constexpr int BM = 16 * WM * MR, BN = 16 * (WAVES / WM) * NR;
-  dim3 grid((unsigned)oc::cdiv(G, BM / 8), (unsigned)oc::cdiv(nn, BN), (unsigned)c.splits);
-  oc::launch_main(k_conv_tile<K, V, MR, NR, WM, FLIP>, grid, dim3(TB), s,
-                  (const int32_t*)t->nbr[l], G, x, xmask, kk, w, nn, out, relu, c.cps, part);
+  const int64_t ntile = oc::cdiv(G, BM / 8);
+  const int64_t gyz = oc::cdiv(nn, BN) * c.splits;
+  // one resident wave of workgroups, each over a contiguous range of tiles
+  int64_t px = std::min<int64_t>(ntile, std::max<int64_t>(1, (int64_t)oc::cu_count() * occ / gyz));
+  if (px >= 8) px -= px % 8;
+  dim3 grid((unsigned)px, (unsigned)oc::cdiv(nn, BN), (unsigned)c.splits);
+  oc::launch_main(kernel, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, kk, w, nn, out, relu,
+                  c.cps, part);
   if (c.splits > 1) {
     const int64_t n = t->N[l] * (int64_t)nn;
     hipLaunchKernelGGL(k_sum_split, dim3((unsigned)oc::cdiv(n, TB)), dim3(TB), 0, s,
@@ -634,16 +685,18 @@ void launch_tile(const oc_octree* t, int l, const TileCfg& c, const float* x, co
 }
 
 template <bool FLIP>
-void dispatch_tile(const oc_octree* t, int l, int K, const float* x, const float* xmask, int kk,
-                   const float* w, int nn, float* out, int relu, float* part, hipStream_t s) {
+void dispatch_tile(const oc_octree* t, int l, int K, const float* x, int kk, const float* w,
+                   int nn, float* out, int relu, float* part, hipStream_t s) {
   const TileCfg c = pick_tile(K, t->M[l - 1], kk, nn);
-#define OC_TILE(K_, V_, MR_, NR_, WM_)                                                     \
-  if (K == K_ && c.V == V_ && c.MR == MR_ && c.NR == NR_ && c.WM == WM_) {                 \
-    launch_tile<K_, V_, MR_, NR_, WM_, FLIP>(t, l, c, x, xmask, kk, w, nn, out, relu, part, s); \
-    return;                                                                                \
+#define OC_TILE(K_, V_, MR_, NR_, WM_, VEC_)                                                \
+  if (K == K_ && c.V == V_ && c.MR == MR_ && c.NR == NR_ && c.WM == WM_ && c.VEC == VEC_) { \
+    launch_tile<K_, V_, MR_, NR_, WM_, FLIP, VEC_>(t, l, c, x, kk, w, nn, out, relu, part, s); \
+    return;                                                                                 \
   }
-  OC_TILE(3, 4, 1, 1, 4) OC_TILE(3, 4, 1, 2, 4) OC_TILE(3, 1, 2, 1, 4)
-  OC_TILE(5, 1, 1, 1, 4) OC_TILE(5, 1, 1, 2, 4)
+  OC_TILE(3, 4, 1, 1, 4, true) OC_TILE(3, 4, 1, 2, 4, true)
+  OC_TILE(3, 1, 2, 1, 4, true) OC_TILE(3, 1, 2, 1, 4, false)
+  OC_TILE(5, 1, 1, 1, 4, true) OC_TILE(5, 1, 1, 1, 4, false)
+  OC_TILE(5, 1, 1, 2, 4, true) OC_TILE(5, 1, 1, 2, 4, false)
 #undef OC_TILE
 }
 
@@ -689,16 +742,16 @@ DwCfg pick_dw(int K, int64_t G, int cin, int cout) {
 
 template <int K, int VA, int VB, int TT, int MB>
 void launch_dw(const oc_octree* t, int l, const DwCfg& c, const float* x, int cin,
-               const float* dy, const float* ym, int cout, float* part, hipStream_t s) {
+               const float* dy, int cout, float* part, hipStream_t s) {
   if (c.WT == 4) {
     dim3 grid((unsigned)c.nchunks, (unsigned)oc::cdiv(c.tiles, 4));
     oc::launch_main(k_conv_dw<K, VA, VB, TT, MB, 4>, grid, dim3(TB), s,
-                    (const int32_t*)t->nbr[l], t->M[l - 1], c.gchunk, x, cin, dy, ym, cout, part);
+                    (const int32_t*)t->nbr[l], t->M[l - 1], c.gchunk, x, cin, dy, cout, part);
     return;
   }
   dim3 grid((unsigned)c.nchunks, (unsigned)c.tiles);
   oc::launch_main(k_conv_dw<K, VA, VB, TT, MB, 1>, grid, dim3(TB), s,
-                     (const int32_t*)t->nbr[l], t->M[l - 1], c.gchunk, x, cin, dy, ym, cout, part);
+                     (const int32_t*)t->nbr[l], t->M[l - 1], c.gchunk, x, cin, dy, cout, part);
 }
 
 }  // namespace
@@ -714,8 +767,8 @@ void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, in
   }
   const int kk = pass == 0 ? cin : cout, nn = pass == 0 ? cout : cin;
   const TileCfg c = pick_tile(K, t->M[l - 1], kk, nn);
-  snprintf(buf, n, "k_conv_tile<%d, %d, %d, %d, %d, %s>", K, c.V, c.MR, c.NR, c.WM,
-           pass == 0 ? "false" : "true");
+  snprintf(buf, n, "k_conv_tile<%d, %d, %d, %d, %d, %s, %s>", K, c.V, c.MR, c.NR, c.WM,
+           pass == 0 ? "false" : "true", c.VEC ? "true" : "false");
 }
 
 size_t conv_s1_tile_ws(const oc_octree* t, int l, int K, int kk, int nn) {
@@ -725,12 +778,12 @@ size_t conv_s1_tile_ws(const oc_octree* t, int l, int K, int kk, int nn) {
 
 void conv_s1_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin, const float* w,
                      int cout, float* y, int relu, float* ws, hipStream_t s) {
-  dispatch_tile<false>(t, l, K, x, nullptr, cin, w, cout, y, relu, ws, s);
+  dispatch_tile<false>(t, l, K, x, cin, w, cout, y, relu, ws, s);
 }
 
-void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, const float* ymask,
-                          int cout, const float* w, int cin, float* dx, float* ws, hipStream_t s) {
-  dispatch_tile<true>(t, l, K, dy, ymask, cout, w, cin, dx, 0, ws, s);
+void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, int cout,
+                          const float* w, int cin, float* dx, float* ws, hipStream_t s) {
+  dispatch_tile<true>(t, l, K, dy, cout, w, cin, dx, 0, ws, s);
 }
 
 size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout) {
@@ -740,12 +793,12 @@ size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout) {
 }
 
 void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, int cin,
-                            const float* dy, const float* ymask, int cout, float* dw, float* part,
+                            const float* dy, int cout, float* dw, float* part,
                             hipStream_t s) {
   const DwCfg c = pick_dw(K, t->M[l - 1], cin, cout);
 #define OC_DW(K_, VA_, VB_, TT_, MB_)                                                       \
   if (K == K_ && c.VA == VA_ && c.VB == VB_ && c.TT == TT_ && c.MB == MB_) {               \
-    launch_dw<K_, VA_, VB_, TT_, MB_>(t, l, c, x, cin, dy, ymask, cout, part, s);          \
+    launch_dw<K_, VA_, VB_, TT_, MB_>(t, l, c, x, cin, dy, cout, part, s);                 \
   } else
   // PERM mode, K = 3
   OC_DW(3, 4, 4, 1, 0) OC_DW(3, 4, 2, 1, 0) OC_DW(3, 2, 4, 1, 0) OC_DW(3, 4, 1, 3, 0)

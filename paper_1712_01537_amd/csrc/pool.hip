@@ -90,8 +90,10 @@ __global__ __launch_bounds__(TB) void k_pool_fwd(const float* __restrict__ x,
 
 // Routing through the switches (pool backward == unpool forward):
 // out[8g + k][c] = (sw[g][c] == k) ? in[rows[g]][c] : 0 for every child row.
+// With ymask, the routed value is also zeroed where ymask[rows[g]][c] <= 0.
 template <int VEC>
 __global__ __launch_bounds__(TB) void k_route_down(const float* __restrict__ in,
+                                                   const float* __restrict__ ymask,
                                                    const uint8_t* __restrict__ sw,
                                                    const int32_t* __restrict__ rows, int64_t n_l,
                                                    int cv, float* __restrict__ out) {
@@ -104,10 +106,14 @@ __global__ __launch_bounds__(TB) void k_route_down(const float* __restrict__ in,
   const int64_t g = row >> 3;
   const uint8_t k = (uint8_t)(row & 7);
   const U s = reinterpret_cast<const U*>(sw)[g * cv + cc];
-  const F v = reinterpret_cast<const F*>(in)[(int64_t)rows[g] * cv + cc];
+  const int64_t src = (int64_t)rows[g] * cv + cc;
+  const F v = reinterpret_cast<const F*>(in)[src];
+  F m;
+  if (ymask) m = reinterpret_cast<const F*>(ymask)[src];
   F o;
 #pragma unroll
-  for (int e = 0; e < VEC; ++e) set(o, e, comp(s, e) == k ? comp(v, e) : 0.0f);
+  for (int e = 0; e < VEC; ++e)
+    set(o, e, comp(s, e) == k && (!ymask || comp(m, e) > 0.0f) ? comp(v, e) : 0.0f);
   reinterpret_cast<F*>(out)[t] = o;
 }
 
@@ -175,18 +181,19 @@ oc_status oc_pool_fwd(const oc_octree* t, int32_t l, const float* x, int32_t c, 
   return OC_OK;
 }
 
-static oc_status route_down(const oc_octree* t, int32_t l, const float* in, const uint8_t* sw,
-                            int32_t c, float* out, hipStream_t s, const char* who) {
+static oc_status route_down(const oc_octree* t, int32_t l, const float* in, const float* ymask,
+                            const uint8_t* sw, int32_t c, float* out, hipStream_t s,
+                            const char* who) {
   oc_status st = check_common(t, l, c, in, out, sw, who);
   if (st != OC_OK) return st;
   const int64_t n = t->N[l];
   if (n == 0) return OC_OK;
-  if (vec4_ok(c, in, out, sw)) {
+  if (vec4_ok(c, in, out, sw) && (uintptr_t)ymask % 16 == 0) {
     const int cv = c / 4;
-    hipLaunchKernelGGL(k_route_down<4>, dim3(grid_for(n * cv)), dim3(TB), 0, s, in, sw,
+    hipLaunchKernelGGL(k_route_down<4>, dim3(grid_for(n * cv)), dim3(TB), 0, s, in, ymask, sw,
                        (const int32_t*)t->rows[l - 1], n, cv, out);
   } else {
-    hipLaunchKernelGGL(k_route_down<1>, dim3(grid_for(n * c)), dim3(TB), 0, s, in, sw,
+    hipLaunchKernelGGL(k_route_down<1>, dim3(grid_for(n * c)), dim3(TB), 0, s, in, ymask, sw,
                        (const int32_t*)t->rows[l - 1], n, c, out);
   }
   OC_LAUNCH_CHECK();
@@ -194,13 +201,13 @@ static oc_status route_down(const oc_octree* t, int32_t l, const float* in, cons
 }
 
 oc_status oc_pool_bwd(const oc_octree* t, int32_t l, const float* dy, const uint8_t* sw, int32_t c,
-                      float* dx, hipStream_t s) {
-  return route_down(t, l, dy, sw, c, dx, s, "oc_pool_bwd");
+                      const float* y, float* dx, hipStream_t s) {
+  return route_down(t, l, dy, y, sw, c, dx, s, "oc_pool_bwd");
 }
 
 oc_status oc_unpool_fwd(const oc_octree* t, int32_t l, const float* x, const uint8_t* sw,
                         int32_t c, float* y, hipStream_t s) {
-  return route_down(t, l, x, sw, c, y, s, "oc_unpool_fwd");
+  return route_down(t, l, x, nullptr, sw, c, y, s, "oc_unpool_fwd");
 }
 
 oc_status oc_unpool_bwd(const oc_octree* t, int32_t l, const float* dy, const uint8_t* sw,

@@ -142,6 +142,15 @@ def test_pool_unpool_small(seed, B, n, depth, c):
                                   oracle.pool_bwd(ref.labels(l - 1), dy, swr, ref.num(l)))
     np.testing.assert_array_equal(oc.oc_unpool_fwd(tree, l, _cuda(dy), sw).cpu().numpy(),
                                   oracle.unpool_fwd(ref.labels(l - 1), dy, swr, ref.num(l)))
+    # ReLU before the pooling: pool_bwd with y applies the ReLU's backward too
+    z = x.copy()
+    z[1::7] = 0.0
+    a = np.maximum(z, 0.0)
+    ya, swa = oc.oc_pool_fwd(tree, l, _cuda(a))
+    _, swar = oracle.pool_fwd(ref.labels(l - 1), a)
+    np.testing.assert_array_equal(
+        oc.oc_pool_bwd(tree, l, _cuda(dy), swa, y=ya).cpu().numpy(),
+        oracle.relu_bwd(z, oracle.pool_bwd(ref.labels(l - 1), dy, swar, ref.num(l))))
     g = rng.standard_normal((ref.num(l), c)).astype(np.float32)
     np.testing.assert_array_equal(oc.oc_unpool_bwd(tree, l, _cuda(g), sw).cpu().numpy(),
                                   oracle.unpool_bwd(ref.labels(l - 1), g, swr))
