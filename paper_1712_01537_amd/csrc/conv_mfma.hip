@@ -579,6 +579,236 @@ __global__ __launch_bounds__(TB) void k_conv_dw(const int32_t* __restrict__ nbr,
         }
 }
 
+// ---------------------------------------------------------------------------
+// Weight gradient through LDS, K = 3:
+//   dW[k][c][n] = sum over octants i of x[nb(i,k)][c] * dY[i][n]
+// A workgroup takes a chunk of sibling groups and, GS groups at a time,
+// stages their (K+1)^3 x CW tiles of x and their 8 GS rows x BN columns of dY
+// in LDS (register-staged one stage ahead, the neighbour entries two).  The
+// MFMA reduction index is the octant: the children 4h + q (q = lane / 16) of
+// a group, so lane l supplies A[c = l%16][child] from the tile position of
+// that child's tap and B[child][n = l%16] from the dY rows; one staged dY
+// value feeds the MFMAs of every tap.
+// Tiled mode (cin >= 16): the workgroup owns channels 16 cbk.. 16 cbk+15 and
+// columns BN nbk..; wave w takes taps w, w+4, ... (NJ at most).
+// FLAT mode (cin < 16): M runs over (tap, channel) pairs m = tap cin + c,
+// which is the row of dW itself; blocks of 16 pairs are dealt to the waves
+// (rotated by workgroup so that no SIMD always gets the short share).
+// Workgroup (chunk, tile) writes part[chunk][K3 cin][cout] for its block of
+// dW (every entry of the block, zeros included); a second kernel adds the
+// chunks in a fixed order.  XV: cin is a multiple of 4 (x rows read as
+// float4); cout must be a multiple of 4.
+template <bool FLAT, int CW, int NBN, int GS, bool XV>
+__global__ __launch_bounds__(TB) void k_conv_dwt(const int32_t* __restrict__ nbr, int64_t ngroups,
+                                                 int64_t gchunk, const float* __restrict__ x,
+                                                 int cin, const float* __restrict__ dy, int cout,
+                                                 float* __restrict__ part) {
+  constexpr int R = 1, S = 4, K3 = 27, S3 = 64;
+  // M blocks per wave at most: 27 taps, or ceil(27 cin / 16) <= 7, 14, 27 pairs
+  constexpr int NJ = !FLAT ? 7 : CW == 4 ? 2 : CW == 8 ? 4 : 7;
+  constexpr int SY = S + 2, PX = S * SY, P3 = S * PX;  // tile row of (px,py,pz): px PX + py SY + pz
+  constexpr int RS = CW, F4 = CW / 4;
+  constexpr int BN = 16 * NBN;
+  constexpr int BNS = (BN % 32 == 0) ? BN + 16 : BN;  // dY rows of 4 children on distinct banks
+  constexpr int GPP = TB / (S3 * F4);                 // groups per staging pass
+  constexpr int NX = GS / GPP;
+  constexpr int NYE = 8 * GS * (BN / 4);  // float4 elements of a dY stage
+  constexpr int NY = (NYE + TB - 1) / TB;
+  static_assert(TB % (S3 * F4) == 0 && GS % GPP == 0, "x staging covers the stage");
+  static_assert(NX <= 32 && NY <= 32, "validity bits fit a word");
+  __shared__ __attribute__((aligned(16))) float At[GS * P3 * RS];
+  __shared__ __attribute__((aligned(16))) float Bt[8 * GS * BNS];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
+  const int li = lane & 15, q = lane >> 4;
+  const int nCB = FLAT ? 1 : (cin + 15) / 16;
+  const int cbk = (int)(blockIdx.y % nCB), nbk = (int)(blockIdx.y / nCB);
+  const int c0 = FLAT ? 0 : 16 * cbk, n0 = BN * nbk;
+  const int64_t gb = (int64_t)blockIdx.x * gchunk;
+  const int64_t ge = gb + gchunk < ngroups ? gb + gchunk : ngroups;
+  const int nsub = gb < ge ? (int)((ge - gb + GS - 1) / GS) : 0;
+  const int nmb = FLAT ? (K3 * cin + 15) / 16 : K3;  // M blocks (taps when tiled)
+  const int rot = FLAT ? (int)(blockIdx.x % WAVES) : 0;
+  const int mb0 = (wave + rot) % WAVES;
+  const int njw = nmb > mb0 ? (nmb - mb0 + WAVES - 1) / WAVES : 0;  // blocks of this wave
+
+  // M blocks of this wave: block mb[j] = 4 j + mb0; the lane's LDS offset
+  // (tap position and channel) and, in FLAT mode, validity
+  int aoff[NJ];
+  bool alive[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int mb = 4 * j + mb0;
+    int tap, ch;
+    if constexpr (FLAT) {
+      const int m = 16 * mb + li;
+      alive[j] = m < K3 * cin;
+      tap = alive[j] ? m / cin : 0;
+      ch = alive[j] ? m - tap * cin : 0;
+    } else {
+      alive[j] = true;
+      tap = mb < K3 ? mb : 0;
+      ch = li;
+    }
+    aoff[j] = ((tap / 9) * PX + ((tap / 3) % 3) * SY + tap % 3) * RS + ch;
+  }
+  // tile row of child 4h + q at tap offset -R on every axis: h PX + (q>>1) SY + (q&1)
+  const int hoff = ((q >> 1) * SY + (q & 1)) * RS;
+
+  v4f acc[NJ][NBN];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int nb = 0; nb < NBN; ++nb) acc[j][nb] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  // x staging: thread -> (group a_g + GPP i, position a_p, channel quad a_f)
+  const int a_g = tid / (S3 * F4), a_p = (tid / F4) % S3, a_f = tid % F4;
+  const int a_px = a_p / 16, a_py = (a_p / 4) % 4, a_pz = a_p % 4;
+  const int a_lds = (a_g * P3 + a_px * PX + a_py * SY + a_pz) * RS + 4 * a_f;
+  const int a_ux = a_px - R, a_uy = a_py - R, a_uz = a_pz - R;
+  const int a_slot = ((a_ux >> 1) + 1) * 9 + ((a_uy >> 1) + 1) * 3 + ((a_uz >> 1) + 1);
+  const int a_coff = 4 * (a_ux & 1) + 2 * (a_uy & 1) + (a_uz & 1);
+  const int a_ch = c0 + 4 * a_f;
+
+  int32_t nbc[NX], nbn[NX];
+  uint32_t okc = 0, okn = 0;
+  auto load_nb = [&](int s, int32_t (&v)[NX], uint32_t& ok) {
+    ok = 0;
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+      const int64_t g = gb + (int64_t)s * GS + a_g + GPP * i;
+      const bool live = g < ge;
+      v[i] = nbr[live ? 27 * g + a_slot : 0];
+      ok |= (uint32_t)live << i;
+    }
+  };
+  v4f rx[NX];
+  uint32_t xok = 0;
+  auto load_x = [&]() {
+    xok = 0;
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+      const bool live = ((okc >> i) & 1) && nbc[i] >= 0 && a_ch < cin;
+      const int64_t off = live ? (int64_t)(nbc[i] + a_coff) * cin + a_ch : 0;
+      if constexpr (XV) {
+        rx[i] = *reinterpret_cast<const v4f*>(x + off);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) rx[i][j] = x[off + (live && a_ch + j < cin ? j : 0)];
+      }
+      xok |= (uint32_t)live << i;
+    }
+  };
+  auto store_x = [&]() {
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+      const bool live = (xok >> i) & 1;
+      v4f v = rx[i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = live && a_ch + j < cin ? v[j] : 0.f;
+      *reinterpret_cast<v4f*>(&At[a_lds + i * GPP * P3 * RS]) = v;
+    }
+  };
+  // dY staging: element e = tid + i TB -> stage row e / (BN/4), columns 4 (e % (BN/4))..
+  v4f ry[NY];
+  uint32_t yok = 0;
+  auto load_dy = [&](int s) {
+    yok = 0;
+#pragma unroll
+    for (int i = 0; i < NY; ++i) {
+      const int e = tid + i * TB;
+      const int r = e / (BN / 4), gn = n0 + 4 * (e % (BN / 4));
+      const int64_t g = gb + (int64_t)s * GS + r / 8;
+      const bool live = e < NYE && g < ge && gn < cout;
+      const int64_t off = live ? (8 * (gb + (int64_t)s * GS) + r) * cout + gn : 0;
+      ry[i] = *reinterpret_cast<const v4f*>(dy + off);
+      yok |= (uint32_t)live << i;
+    }
+  };
+  auto store_dy = [&]() {
+#pragma unroll
+    for (int i = 0; i < NY; ++i) {
+      const int e = tid + i * TB;
+      if (NYE % TB == 0 || e < NYE) {
+        const int r = e / (BN / 4), f = e % (BN / 4);
+        const bool live = (yok >> i) & 1;
+        const v4f v = ry[i];
+        *reinterpret_cast<v4f*>(&Bt[r * BNS + 4 * f]) =
+            v4f{live ? v[0] : 0.f, live ? v[1] : 0.f, live ? v[2] : 0.f, live ? v[3] : 0.f};
+      }
+    }
+  };
+
+  load_nb(0, nbc, okc);
+  load_nb(1, nbn, okn);
+  load_x();
+  load_dy(0);
+  for (int s = 0; s < nsub; ++s) {
+    __syncthreads();  // the previous stage's LDS reads are done
+    store_x();
+    store_dy();
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < NX; ++i) nbc[i] = nbn[i];
+    okc = okn;
+    load_nb(s + 2, nbn, okn);
+    load_x();
+    load_dy(s + 1);
+#pragma unroll 4
+    for (int g = 0; g < GS; ++g) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        float b[NBN];
+#pragma unroll
+        for (int nb = 0; nb < NBN; ++nb) b[nb] = Bt[(8 * g + 4 * h + q) * BNS + 16 * nb + li];
+        const float* ag = &At[g * P3 * RS + h * PX * RS + hoff];
+        float a[NJ];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) a[j] = ag[aoff[j]];  // all reads in flight first
+        if constexpr (FLAT) {
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) a[j] = alive[j] ? a[j] : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          if (j < njw) {  // scalar branch
+#pragma unroll
+            for (int nb = 0; nb < NBN; ++nb) acc[j][nb] = mfma4(a[j], b[nb], acc[j][nb]);
+          }
+        }
+      }
+    }
+  }
+
+  // accumulator r of lane l: M row 4(l/16) + r, column l % 16
+  const int64_t entries = (int64_t)K3 * cin * cout;
+  float* pp = part + (int64_t)blockIdx.x * entries;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int mb = 4 * j + mb0;
+    if (j >= njw) continue;
+#pragma unroll
+    for (int nb = 0; nb < NBN; ++nb) {
+      const int n = n0 + 16 * nb + li;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 4 * q + r;
+        int m;
+        bool ok;
+        if constexpr (FLAT) {
+          m = 16 * mb + i;
+          ok = m < K3 * cin;
+        } else {
+          ok = c0 + i < cin;
+          m = mb * cin + c0 + i;
+        }
+        if (ok && n < cout) pp[(int64_t)m * cout + n] = acc[j][nb][r];
+      }
+    }
+  }
+}
+
 // Fixed-order sum of np partials of n entries, in two passes: pass 1 adds
 // segment y (partials y*sp .. y*sp+sp-1) of 64 entries per workgroup, four
 // interleaved sub-sums per entry combined in order; pass 2 adds the segments.
@@ -651,7 +881,7 @@ TileCfg pick_tile(int K, int64_t G, int kk, int nn) {
   const int64_t tiles = oc::cdiv(G, BM / 8) * oc::cdiv(nn, BN);
   const int chunks = (int)oc::cdiv(kk, 4 * c.V);
   int splits = 1;
-  while (tiles * splits < 1024 && splits * 2 <= chunks) splits *= 2;
+  while (tiles * splits < 2048 && splits * 2 <= chunks) splits *= 2;
   c.cps = (int)oc::cdiv(chunks, splits);
   c.splits = (int)oc::cdiv(chunks, c.cps);
   return c;
@@ -698,6 +928,64 @@ void dispatch_tile(const oc_octree* t, int l, int K, const float* x, int kk, con
   OC_TILE(5, 1, 1, 1, 4, true) OC_TILE(5, 1, 1, 1, 4, false)
   OC_TILE(5, 1, 1, 2, 4, true) OC_TILE(5, 1, 1, 2, 4, false)
 #undef OC_TILE
+}
+
+// Weight gradient through LDS (k_conv_dwt): K = 3 with cout a multiple of 4,
+// and cin a multiple of 4 when cin >= 16.
+struct DwtCfg {
+  bool flat, xv;
+  int CW, NBN, GS, tiles;
+  int64_t gchunk, nchunks;
+};
+
+bool pick_dwt(int K, int64_t G, int cin, int cout, DwtCfg* c) {
+  if (K != 3 || cout % 4 != 0) return false;
+  c->flat = cin < 16;
+  c->xv = cin % 4 == 0;
+  if (!c->flat && !c->xv) return false;
+  if (c->flat) {
+    c->CW = cin <= 4 ? 4 : cin <= 8 ? 8 : 16;
+    c->GS = 64 / c->CW;
+    c->NBN = cout <= 16 ? 1 : 2;
+  } else {
+    c->CW = 16, c->GS = 4;
+    c->NBN = cout >= 64 ? 4 : cout >= 32 ? 2 : 1;
+  }
+  const int nCB = c->flat ? 1 : (int)oc::cdiv(cin, 16);
+  c->tiles = nCB * (int)oc::cdiv(cout, 16 * c->NBN);
+  const int64_t entries = (int64_t)27 * cin * cout;
+  // about 2048 workgroups, partial sums capped at 16M floats
+  int64_t chunks = std::max<int64_t>(1, 2048 / c->tiles);
+  chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, (int64_t(16) << 20) / entries));
+  c->gchunk = oc::cdiv(oc::cdiv(std::max<int64_t>(G, 1), chunks), c->GS) * c->GS;
+  c->nchunks = std::max<int64_t>(1, oc::cdiv(G, c->gchunk));
+  return true;
+}
+
+template <bool FLAT, int CW, int NBN, int GS, bool XV>
+void launch_dwt(const oc_octree* t, int l, const DwtCfg& c, const float* x, int cin,
+                const float* dy, int cout, float* part, hipStream_t s) {
+  dim3 grid((unsigned)c.nchunks, (unsigned)c.tiles);
+  oc::launch_main(k_conv_dwt<FLAT, CW, NBN, GS, XV>, grid, dim3(TB), s, (const int32_t*)t->nbr[l],
+                  t->M[l - 1], c.gchunk, x, cin, dy, cout, part);
+}
+
+bool dispatch_dwt(const oc_octree* t, int l, const DwtCfg& c, const float* x, int cin,
+                  const float* dy, int cout, float* part, hipStream_t s) {
+#define OC_DWT(FLAT_, CW_, NBN_, GS_, XV_)                                                  \
+  if (c.flat == FLAT_ && c.CW == CW_ && c.NBN == NBN_ && c.GS == GS_ && c.xv == XV_) {    \
+    launch_dwt<FLAT_, CW_, NBN_, GS_, XV_>(t, l, c, x, cin, dy, cout, part, s);           \
+    return true;                                                                          \
+  }
+  OC_DWT(false, 16, 1, 4, true) OC_DWT(false, 16, 2, 4, true) OC_DWT(false, 16, 4, 4, true)
+  OC_DWT(true, 4, 1, 16, true) OC_DWT(true, 4, 2, 16, true)
+  OC_DWT(true, 4, 1, 16, false) OC_DWT(true, 4, 2, 16, false)
+  OC_DWT(true, 8, 1, 8, true) OC_DWT(true, 8, 2, 8, true)
+  OC_DWT(true, 8, 1, 8, false) OC_DWT(true, 8, 2, 8, false)
+  OC_DWT(true, 16, 1, 4, true) OC_DWT(true, 16, 2, 4, true)
+  OC_DWT(true, 16, 1, 4, false) OC_DWT(true, 16, 2, 4, false)
+#undef OC_DWT
+  return false;
 }
 
 struct DwCfg {
@@ -761,6 +1049,12 @@ namespace oc {
 void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, int pass, char* buf,
                          size_t n) {
   if (pass == 2) {
+    DwtCfg d;
+    if (pick_dwt(K, t->M[l - 1], cin, cout, &d)) {
+      snprintf(buf, n, "k_conv_dwt<%s, %d, %d, %d, %s>", d.flat ? "true" : "false", d.CW, d.NBN,
+               d.GS, d.xv ? "true" : "false");
+      return;
+    }
     const DwCfg c = pick_dw(K, t->M[l - 1], cin, cout);
     snprintf(buf, n, "k_conv_dw<%d, %d, %d, %d, %d, %d>", K, c.VA, c.VB, c.TT, c.MB, c.WT);
     return;
@@ -787,14 +1081,30 @@ void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, int
 }
 
 size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout) {
-  const DwCfg c = pick_dw(K, t->M[l - 1], cin, cout);
-  const int ns = sum_segments((int)c.nchunks);
-  return (size_t)c.nchunks + (ns > 1 ? ns : 0);  // partials, then pass-1 segments
+  DwtCfg d;
+  int64_t np;
+  if (pick_dwt(K, t->M[l - 1], cin, cout, &d)) {
+    np = d.nchunks;
+  } else {
+    np = pick_dw(K, t->M[l - 1], cin, cout).nchunks;
+  }
+  const int ns = sum_segments((int)np);
+  return (size_t)np + (ns > 1 ? ns : 0);  // partials, then pass-1 segments
 }
 
 void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, int cin,
                             const float* dy, int cout, float* dw, float* part,
                             hipStream_t s) {
+  const int64_t entries = (int64_t)K * K * K * cin * cout;
+  DwtCfg d;
+  if (pick_dwt(K, t->M[l - 1], cin, cout, &d)) {
+    if (dispatch_dwt(t, l, d, x, cin, dy, cout, part, s)) {
+      sum_parts(part, (int)d.nchunks, entries, part + d.nchunks * entries, dw, s);
+    } else {
+      oc::set_error("no weight-gradient kernel for cin=%d cout=%d", cin, cout);
+    }
+    return;
+  }
   const DwCfg c = pick_dw(K, t->M[l - 1], cin, cout);
 #define OC_DW(K_, VA_, VB_, TT_, MB_)                                                       \
   if (K == K_ && c.VA == VA_ && c.VB == VB_ && c.TT == TT_ && c.MB == MB_) {               \
@@ -818,7 +1128,6 @@ void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, in
     oc::set_error("no weight-gradient kernel for K=%d cin=%d cout=%d", K, cin, cout);
   }
 #undef OC_DW
-  const int64_t entries = (int64_t)K * K * K * cin * cout;
   sum_parts(part, (int)c.nchunks, entries, part + c.nchunks * entries, dw, s);
 }
 
