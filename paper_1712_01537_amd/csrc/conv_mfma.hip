@@ -30,12 +30,33 @@
 // order, so results do not depend on scheduling.
 #include "conv_mfma.h"
 
+#include <algorithm>
+#include <cmath>
+
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int TB = 256;
 constexpr int WAVES = TB / 64;
+
+typedef __attribute__((address_space(3))) void* lptr_t;  // LDS
+
+// 16 zero bytes: the source of direct-to-LDS loads of absent rows.
+__device__ __attribute__((aligned(16))) float oc_zero16[4];
+
+// Direct global->LDS load of 16 bytes per lane: lane i's bytes land at LDS
+// byte address lds + 16 i (lds uniform over the wave).  Written as inline
+// assembly so that the compiler's wait insertion, which does not know the
+// instruction, keeps exact LDS counters for the surrounding code; the caller
+// waits for completion itself (vm_wait0) before other waves read the data.
+__device__ __forceinline__ void lds_load16(const void* src, const void* lds) {
+  const uint32_t a = (uint32_t)(uintptr_t)(lptr_t)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(a), "v"(src)
+               : "memory", "m0");
+}
+// s_waitcnt vmcnt(0): all of this wave's vector memory operations are done.
+__device__ __forceinline__ void vm_wait0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 __device__ __forceinline__ v4f mfma4(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -357,6 +378,188 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
       }
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Stride-1, K = 3 convolution, weights in registers (k_conv_tile3):
+// out[i][n] = sum_k sum_c x[nb(i,k)][c] W'[k][c][n] for the 16-channel chunk
+// c0 = 16 blockIdx.z of the reduction (partial sums when there are several).
+// The MFMA computes out^T: A = W'^T (16 output channels x 4 reduction
+// channels), B = the gathered rows (4 channels x 16 octants).  Each wave
+// keeps the chunk's weights of its 16 output channels in registers for the
+// whole launch (27 taps x 4 channels per lane), so the only LDS traffic is
+// the group tiles: one 16-byte read per lane feeds four MFMAs.
+// Workgroups (two per CU) are persistent over a contiguous range of tiles of
+// GPB sibling groups (GPB/2 blocks of 16 rows).  Wave w takes output channels
+// 16 (w % WN).. and row blocks RB (w / WN) + r, r < RB.  The
+// (K+1)^3 x 16-channel group tiles are streamed with direct global->LDS
+// loads into two static buffers: tile t+1 lands while tile t is multiplied,
+// with one barrier per tile.  Absent neighbours and channels past kk read a
+// zero row.
+// Group tile layout, in 16-byte chunks: group g at 274 g, x-slab at 65 x,
+// position (y, z) at slot 4z + ((y + 2z) & 3), channel quad last.  A 16-lane
+// read of one tap touches 2 groups x 2 slabs x 2 y x 2 z positions, which
+// this order puts on distinct banks.  Each x-slab of a group (16 positions x
+// 4 quads) is one wave's load instruction.
+// FLIP: input gradient, W'[k][c][n] = W[26-k][n][c].
+template <int WN, int GPB, bool FLIP>
+__global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_conv_tile3(const int32_t* __restrict__ nbr,
+                                                   int64_t ngroups, const float* __restrict__ x,
+                                                   int kk, const float* __restrict__ w, int nn,
+                                                   float* __restrict__ out, int relu,
+                                                   float* __restrict__ part) {
+  constexpr int K3 = 27, BN = 16 * WN, WM = WAVES / WN;
+  constexpr int RB = GPB / 2 / WM;  // row blocks per wave
+  static_assert(RB >= 1 && RB * WM * 2 == GPB, "every row block has one wave");
+  constexpr int GSTR = 274, XSTR = 65, BUFC = GPB * GSTR;  // in 16-byte chunks
+  __shared__ __attribute__((aligned(16))) v4f X0[BUFC];
+  __shared__ __attribute__((aligned(16))) v4f X1[BUFC];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int li = lane & 15, q = lane >> 4;
+  const int wn = wave % WN, wm = wave / WN;
+  const int n0 = blockIdx.y * BN + 16 * wn, c0 = 16 * blockIdx.z;
+  const int64_t ntile = (ngroups + GPB - 1) / GPB;
+  const int nx = gridDim.x, bx = blockIdx.x;
+  const int lb = nx >= 8 ? (bx % 8) * (nx / 8) + bx / 8 : bx;  // XCD-contiguous ranges
+  const int64_t tile0 = ntile * lb / nx;
+  const int T = (int)(ntile * (lb + 1) / nx - tile0);
+  if (T <= 0) return;  // uniform over the workgroup
+
+  // loads: wave w fills x-slab w of every group; lane -> (slot s, quad f)
+  const int s_ = lane >> 2, f_ = lane & 3;
+  const int pz = s_ >> 2, py = (s_ - 2 * pz) & 3, px = wave;
+  const int ux = px - 1, uy = py - 1, uz = pz - 1;
+  const int l_slot = ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1);
+  const int l_coff = 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
+  const int l_ch = c0 + 4 * f_;
+  int32_t nbc[GPB], nbn[GPB];
+  uint32_t okc = 0, okn = 0;
+  auto load_nb = [&](int t, int32_t (&v)[GPB], uint32_t& ok) {
+    ok = 0;
+#pragma unroll
+    for (int i = 0; i < GPB; ++i) {
+      const int64_t g = (tile0 + t) * GPB + i;
+      const bool live = t < T && g < ngroups;
+      v[i] = nbr[live ? 27 * g + l_slot : 0];
+      ok |= (uint32_t)live << i;
+    }
+  };
+  auto dma = [&](v4f* buf) {
+#pragma unroll
+    for (int i = 0; i < GPB; ++i) {
+      const bool live = ((okc >> i) & 1) && nbc[i] >= 0 && l_ch < kk;
+      const float* src = live ? x + (int64_t)(nbc[i] + l_coff) * kk + l_ch : oc_zero16;
+      lds_load16(src, buf + i * GSTR + px * XSTR);
+    }
+  };
+
+  // reads: lane (li, q) supplies row li of row block rb: child li & 7 of
+  // group 2 rb + (li >> 3), channels 4q..4q+3
+  int aoff[9];
+  {
+    const int g = 2 * (wm * RB) + (li >> 3), c = li & 7;
+    const int cx = c >> 2, cy = (c >> 1) & 1, cz = c & 1;
+#pragma unroll
+    for (int j = 0; j < 9; ++j) {
+      const int y = cy + j / 3, z = cz + j % 3;
+      aoff[j] = g * GSTR + cx * XSTR + 4 * (4 * z + ((y + 2 * z) & 3)) + q;
+    }
+  }
+
+  v4f acc0[RB], acc1[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) acc0[r] = acc1[r] = v4f{0.f, 0.f, 0.f, 0.f};
+  v4f wr[K3];  // this lane's weights, loaded after the first neighbour entries
+
+  // the rows of tap k+1 are read before the MFMAs of tap k
+  auto compute = [&](const v4f* buf, v4f (&acc)[RB]) {
+    v4f b[2][RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) b[0][r] = buf[aoff[0] + 2 * r * GSTR];
+#pragma unroll
+    for (int k = 0; k < K3; ++k) {
+      const int cu = k & 1, nx2 = cu ^ 1;
+      if (k + 1 < K3) {
+#pragma unroll
+        for (int r = 0; r < RB; ++r)
+          b[nx2][r] = buf[aoff[(k + 1) % 9] + ((k + 1) / 9) * XSTR + 2 * r * GSTR];
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int r = 0; r < RB; ++r) acc[r] = mfma4(wr[k][s], b[cu][r][s], acc[r]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  const int64_t nrows = 8 * ngroups;
+  const bool split = gridDim.z > 1;
+  float* dst = split ? part + (int64_t)blockIdx.z * nrows * nn : out;
+  // accumulator j of lane l: output channel 4(l/16) + j, row l % 16
+  auto epilogue = [&](int t, v4f (&acc)[RB]) {
+    const int n = n0 + 4 * q;
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      const int64_t row = 8 * (tile0 + t) * GPB + 16 * (wm * RB + r) + li;
+      if (n < nn && row < nrows) {
+        v4f v = acc[r];
+        if (!split && relu) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = fmaxf(v[j], 0.f);
+        }
+        *reinterpret_cast<v4f*>(dst + row * nn + n) = v;
+      }
+      acc[r] = v4f{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  // tile t: wait for its loads everywhere (and for tile t-1's reads), write
+  // tile t-1, start tile t+1's loads, multiply tile t
+  auto step = [&](int t, const v4f* cur, v4f* nxt, v4f (&accc)[RB], v4f (&accp)[RB]) {
+    vm_wait0();  // this wave's loads into cur have landed
+    __syncthreads();
+    if (t > 0) epilogue(t - 1, accp);
+#pragma unroll
+    for (int i = 0; i < GPB; ++i) nbc[i] = nbn[i];
+    okc = okn;
+    if (t + 1 < T) {
+      load_nb(t + 2, nbn, okn);
+      dma(nxt);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    compute(cur, accc);
+  };
+
+  load_nb(0, nbc, okc);
+  load_nb(1, nbn, okn);
+  // this lane's weights: wr[k][s] = W'[k][c0 + 4q + s][n0 + li]
+  {
+    const int n = n0 + li, c = c0 + 4 * q;
+#pragma unroll
+    for (int k = 0; k < K3; ++k) {
+      v4f v = {0.f, 0.f, 0.f, 0.f};
+      if (n < nn && c < kk) {
+        if constexpr (FLIP) {
+          v = *reinterpret_cast<const v4f*>(w + ((int64_t)(K3 - 1 - k) * nn + n) * kk + c);
+        } else {
+#pragma unroll
+          for (int s = 0; s < 4; ++s) v[s] = w[((int64_t)k * kk + c + s) * nn + n];
+        }
+      }
+      wr[k] = v;
+    }
+  }
+
+  dma(X0);
+  for (int t = 0; t < T; t += 2) {
+    step(t, X0, X1, acc0, acc1);
+    if (t + 1 < T) step(t + 1, X1, X0, acc1, acc0);
+  }
+  if ((T - 1) % 2 == 0)
+    epilogue(T - 1, acc0);
+  else
+    epilogue(T - 1, acc1);
 }
 
 // out[e] = sum over splits of part[z][e] (in split order), ReLU if relu.
@@ -863,6 +1066,8 @@ void sum_parts(const float* part, int np, int64_t n, float* seg, float* out, hip
 struct TileCfg {
   int V, MR, NR, WM, splits, cps;
   bool VEC;
+  bool v2;  // k_conv_tile3: K = 3, 16-channel chunks, one chunk per split
+  int gpb;  // k_conv_tile3: sibling groups per tile
 };
 
 // Workgroup tile and split of the reduction for a stride-1 layer of G groups
@@ -870,6 +1075,26 @@ struct TileCfg {
 TileCfg pick_tile(int K, int64_t G, int kk, int nn) {
   TileCfg c;
   c.VEC = kk % 4 == 0 && nn % 4 == 0;
+  c.v2 = K == 3 && c.VEC && kk >= 16;
+  if (c.v2) {
+    c.V = 4, c.MR = 1, c.WM = 4;
+    c.NR = nn <= 16 ? 1 : nn <= 32 ? 2 : 4;  // column blocks per workgroup (WN)
+    c.cps = 1;
+    c.splits = (int)oc::cdiv(kk, 16);
+    // tile size: the best balance of tiles over two workgroups per CU, with
+    // a small preference for larger tiles (fewer barriers and loads per MFMA)
+    const int64_t slots = 2 * (int64_t)oc::cu_count();
+    const int64_t gyz = oc::cdiv(nn, 16 * c.NR) * c.splits;
+    double best = -1.0;
+    c.gpb = 8;
+    for (int gpb = 8; gpb >= 2; gpb /= 2) {
+      if (gpb / 2 < WAVES / c.NR) break;  // a row block for every wave
+      const double units = (double)oc::cdiv(G, gpb) * gyz / slots;
+      const double eff = units / std::ceil(units) * (gpb == 8 ? 1.0 : gpb == 4 ? 0.97 : 0.92);
+      if (eff > best + 1e-9) best = eff, c.gpb = gpb;
+    }
+    return c;
+  }
   c.V = (K == 3 && kk >= 16 && c.VEC) ? 4 : 1;
   c.WM = 4;
   if (c.V == 1 && K == 3) {
@@ -914,10 +1139,46 @@ void launch_tile(const oc_octree* t, int l, const TileCfg& c, const float* x, in
   }
 }
 
+template <int NR, int GPB, bool FLIP>
+void launch_tile2(const oc_octree* t, int l, const TileCfg& c, const float* x, int kk,
+                  const float* w, int nn, float* out, int relu, float* part, hipStream_t s) {
+  const auto kernel = k_conv_tile3<NR, GPB, FLIP>;
+  static const int occ = [&] {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, TB, 0) != hipSuccess || n < 1)
+      n = 1;
+    return n;
+  }();
+  const int64_t G = t->M[l - 1];
+  const int64_t ntile = oc::cdiv(G, GPB);
+  const int64_t gy = oc::cdiv(nn, 16 * NR), gyz = gy * c.splits;
+  // one resident workgroup per slot, each over a contiguous range of tiles
+  int64_t px = std::min<int64_t>(ntile, std::max<int64_t>(1, (int64_t)oc::cu_count() * occ / gyz));
+  if (px >= 8) px -= px % 8;
+  dim3 grid((unsigned)px, (unsigned)gy, (unsigned)c.splits);
+  oc::launch_main(kernel, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, kk, w, nn, out,
+                  relu, part);
+  if (c.splits > 1) {
+    const int64_t n = t->N[l] * (int64_t)nn;
+    hipLaunchKernelGGL(k_sum_split, dim3((unsigned)oc::cdiv(n, TB)), dim3(TB), 0, s,
+                       (const float*)part, c.splits, n, out, relu);
+  }
+}
+
 template <bool FLIP>
 void dispatch_tile(const oc_octree* t, int l, int K, const float* x, int kk, const float* w,
                    int nn, float* out, int relu, float* part, hipStream_t s) {
   const TileCfg c = pick_tile(K, t->M[l - 1], kk, nn);
+  if (c.v2) {
+#define OC_T3(NR_, GPB_)                                                       \
+  if (c.NR == NR_ && c.gpb == GPB_) {                                          \
+    launch_tile2<NR_, GPB_, FLIP>(t, l, c, x, kk, w, nn, out, relu, part, s);  \
+    return;                                                                    \
+  }
+    OC_T3(1, 8) OC_T3(2, 8) OC_T3(2, 4) OC_T3(4, 8) OC_T3(4, 4) OC_T3(4, 2)
+#undef OC_T3
+    return;
+  }
 #define OC_TILE(K_, V_, MR_, NR_, WM_, VEC_)                                                \
   if (K == K_ && c.V == V_ && c.MR == MR_ && c.NR == NR_ && c.WM == WM_ && c.VEC == VEC_) { \
     launch_tile<K_, V_, MR_, NR_, WM_, FLIP, VEC_>(t, l, c, x, kk, w, nn, out, relu, part, s); \
@@ -1061,6 +1322,10 @@ void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, in
   }
   const int kk = pass == 0 ? cin : cout, nn = pass == 0 ? cout : cin;
   const TileCfg c = pick_tile(K, t->M[l - 1], kk, nn);
+  if (c.v2) {
+    snprintf(buf, n, "k_conv_tile3<%d, %d, %s>", c.NR, c.gpb, pass == 0 ? "false" : "true");
+    return;
+  }
   snprintf(buf, n, "k_conv_tile<%d, %d, %d, %d, %d, %s, %s>", K, c.V, c.MR, c.NR, c.WM,
            pass == 0 ? "false" : "true", c.VEC ? "true" : "false");
 }
