@@ -850,8 +850,8 @@ __global__ __launch_bounds__(TB) void k_conv_dwt(const int32_t* __restrict__ nbr
       tap = alive[j] ? m / cin : 0;
       ch = alive[j] ? m - tap * cin : 0;
     } else {
-      alive[j] = true;
-      tap = mb < K3 ? mb : 0;
+      alive[j] = mb < K3;
+      tap = alive[j] ? mb : 0;
       ch = li;
     }
     aoff[j] = ((tap / 9) * PX + ((tap / 3) % 3) * SY + tap % 3) * RS + ch;
@@ -958,29 +958,31 @@ __global__ __launch_bounds__(TB) void k_conv_dwt(const int32_t* __restrict__ nbr
     load_nb(s + 2, nbn, okn);
     load_x();
     load_dy(s + 1);
-#pragma unroll 4
-    for (int g = 0; g < GS; ++g) {
+    // operands of step st = (group st/2, children 4(st%2)+q), one step ahead
+    // of the MFMAs; blocks past the wave's share multiply zeros (the longest
+    // share sets the pace anyway)
+    float a[2][NJ], b[2][NBN];
+    auto rd = [&](int st, float (&av)[NJ], float (&bv)[NBN]) {
+      const int g = st >> 1, h = st & 1;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        float b[NBN];
+      for (int nb = 0; nb < NBN; ++nb) bv[nb] = Bt[(8 * g + 4 * h + q) * BNS + 16 * nb + li];
+      const float* ag = &At[g * P3 * RS + h * PX * RS + hoff];
 #pragma unroll
-        for (int nb = 0; nb < NBN; ++nb) b[nb] = Bt[(8 * g + 4 * h + q) * BNS + 16 * nb + li];
-        const float* ag = &At[g * P3 * RS + h * PX * RS + hoff];
-        float a[NJ];
+      for (int j = 0; j < NJ; ++j) av[j] = ag[aoff[j]];
+    };
+    rd(0, a[0], b[0]);
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) a[j] = ag[aoff[j]];  // all reads in flight first
-        if constexpr (FLAT) {
+    for (int st = 0; st < 2 * GS; ++st) {
+      const int cu = st & 1, nx = cu ^ 1;
+      if (st + 1 < 2 * GS) rd(st + 1, a[nx], b[nx]);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int j = 0; j < NJ; ++j) a[j] = alive[j] ? a[j] : 0.f;
-        }
+      for (int j = 0; j < NJ; ++j) {
+        const float av = alive[j] ? a[cu][j] : 0.f;
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-          if (j < njw) {  // scalar branch
-#pragma unroll
-            for (int nb = 0; nb < NBN; ++nb) acc[j][nb] = mfma4(a[j], b[nb], acc[j][nb]);
-          }
-        }
+        for (int nb = 0; nb < NBN; ++nb) acc[j][nb] = mfma4(av, b[cu][nb], acc[j][nb]);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
