@@ -1201,6 +1201,8 @@ struct DwtCfg {
   int64_t gchunk, nchunks;
 };
 
+int dwt_occupancy(const DwtCfg& c);
+
 bool pick_dwt(int K, int64_t G, int cin, int cout, DwtCfg* c) {
   if (K != 3 || cout % 4 != 0) return false;
   c->flat = cin < 16;
@@ -1217,10 +1219,12 @@ bool pick_dwt(int K, int64_t G, int cin, int cout, DwtCfg* c) {
   const int nCB = c->flat ? 1 : (int)oc::cdiv(cin, 16);
   c->tiles = nCB * (int)oc::cdiv(cout, 16 * c->NBN);
   const int64_t entries = (int64_t)27 * cin * cout;
-  // about 2048 workgroups, partial sums capped at 16M floats
-  int64_t chunks = std::max<int64_t>(1, 2048 / c->tiles);
+  // one round of resident workgroups (at least one stage of groups each),
+  // partial sums capped at 16M floats
+  const int64_t slots = (int64_t)oc::cu_count() * dwt_occupancy(*c);
+  int64_t chunks = std::max<int64_t>(1, slots / c->tiles);
   chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, (int64_t(16) << 20) / entries));
-  c->gchunk = oc::cdiv(oc::cdiv(std::max<int64_t>(G, 1), chunks), c->GS) * c->GS;
+  c->gchunk = std::max<int64_t>(c->GS, oc::cdiv(std::max<int64_t>(G, 1), chunks));
   c->nchunks = std::max<int64_t>(1, oc::cdiv(G, c->gchunk));
   return true;
 }
@@ -1233,6 +1237,36 @@ void launch_dwt(const oc_octree* t, int l, const DwtCfg& c, const float* x, int 
                   t->M[l - 1], c.gchunk, x, cin, dy, cout, part);
 }
 
+// Resident workgroups per CU of the configuration's kernel (cached).
+template <bool FLAT, int CW, int NBN, int GS, bool XV>
+int dwt_occ() {
+  static const int occ = [] {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_conv_dwt<FLAT, CW, NBN, GS, XV>, TB, 0) !=
+            hipSuccess ||
+        n < 1)
+      n = 1;
+    return n;
+  }();
+  return occ;
+}
+
+#define OC_DWT_LIST(X)                                                                       \
+  X(false, 16, 1, 4, true) X(false, 16, 2, 4, true) X(false, 16, 4, 4, true)                \
+  X(true, 4, 1, 16, true) X(true, 4, 2, 16, true) X(true, 4, 1, 16, false)                   \
+  X(true, 4, 2, 16, false) X(true, 8, 1, 8, true) X(true, 8, 2, 8, true)                     \
+  X(true, 8, 1, 8, false) X(true, 8, 2, 8, false) X(true, 16, 1, 4, true)                    \
+  X(true, 16, 2, 4, true) X(true, 16, 1, 4, false) X(true, 16, 2, 4, false)
+
+int dwt_occupancy(const DwtCfg& c) {
+#define OC_DWT_OCC(FLAT_, CW_, NBN_, GS_, XV_)                                              \
+  if (c.flat == FLAT_ && c.CW == CW_ && c.NBN == NBN_ && c.GS == GS_ && c.xv == XV_)       \
+    return dwt_occ<FLAT_, CW_, NBN_, GS_, XV_>();
+  OC_DWT_LIST(OC_DWT_OCC)
+#undef OC_DWT_OCC
+  return 1;
+}
+
 bool dispatch_dwt(const oc_octree* t, int l, const DwtCfg& c, const float* x, int cin,
                   const float* dy, int cout, float* part, hipStream_t s) {
 #define OC_DWT(FLAT_, CW_, NBN_, GS_, XV_)                                                  \
@@ -1240,13 +1274,7 @@ bool dispatch_dwt(const oc_octree* t, int l, const DwtCfg& c, const float* x, in
     launch_dwt<FLAT_, CW_, NBN_, GS_, XV_>(t, l, c, x, cin, dy, cout, part, s);           \
     return true;                                                                          \
   }
-  OC_DWT(false, 16, 1, 4, true) OC_DWT(false, 16, 2, 4, true) OC_DWT(false, 16, 4, 4, true)
-  OC_DWT(true, 4, 1, 16, true) OC_DWT(true, 4, 2, 16, true)
-  OC_DWT(true, 4, 1, 16, false) OC_DWT(true, 4, 2, 16, false)
-  OC_DWT(true, 8, 1, 8, true) OC_DWT(true, 8, 2, 8, true)
-  OC_DWT(true, 8, 1, 8, false) OC_DWT(true, 8, 2, 8, false)
-  OC_DWT(true, 16, 1, 4, true) OC_DWT(true, 16, 2, 4, true)
-  OC_DWT(true, 16, 1, 4, false) OC_DWT(true, 16, 2, 4, false)
+  OC_DWT_LIST(OC_DWT)
 #undef OC_DWT
   return false;
 }
