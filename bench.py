@@ -35,6 +35,7 @@ import math
 import os
 import sys
 import time
+from concurrent.futures import ThreadPoolExecutor
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
@@ -201,18 +202,27 @@ class Step:
 
     def __call__(self):
         """One step: the network forward and backward on the octree built during
-        the previous step, while the octree of the next step is built."""
+        the previous step, while the octree of the next step is built.  As in
+        the paper's training (Sec. 3.2, last paragraph), the next build runs on
+        a host thread of its own: its one wait for the per-depth counts then
+        never stalls the thread that queues the network."""
         torch = self.torch
         if getattr(self, "bstream", None) is None:
             self.nstream = torch.cuda.current_stream()
             self.bstream = torch.cuda.Stream()  # default priority
-            self.pending = self.build()
-        tree, ev = self.pending
+            self.pool = ThreadPoolExecutor(max_workers=1)
+            self.pending = self.pool.submit(self.build)
+        tree, ev = self.pending.result()
         self.nstream.wait_event(ev)
+        self.pending = self.pool.submit(self.build)
         g = self.network(tree)
-        self.pending = self.build()
         tree.free()
         return g
+
+    def drain(self):
+        """Wait until the pending build has been queued (before a device sync)."""
+        if getattr(self, "pending", None) is not None:
+            self.pending.result()
 
     def network(self, tree):
         oc, wl = self.oc, self.wl
@@ -344,6 +354,7 @@ def main():
     step.events, step.traced = {}, {"*"}
     for _ in range(max(args.warmup, 1)):
         step()
+    step.drain()
     torch.cuda.synchronize()
     warm = step.collect()
     # the build is many kernels on its own stream, overlapped with the network
@@ -356,6 +367,7 @@ def main():
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
+    step.drain()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms = (t1 - t0) * 1e3 / args.steps
