@@ -173,7 +173,7 @@ class Step:
             torch = self.torch
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
-            if tag.startswith("conv"):
+            if tag != "build":
                 # recorded by the library at the start and end of the kernel itself
                 a.record()
                 b.record()  # instantiates the events

@@ -227,11 +227,13 @@ oc_status oc_unpool_fwd(const oc_octree* tree, int32_t depth, const float* x, co
 oc_status oc_unpool_bwd(const oc_octree* tree, int32_t depth, const float* dy, const uint8_t* sw,
                         int32_t c, float* dx, hipStream_t stream);
 
-/* Profiling: the next launch, on the calling thread, of a kernel that
- * oc_conv_kernel names is bracketed by these events (recorded at the start
- * and the end of that kernel on its stream, as hipExtLaunchKernelGGL does),
- * so that its duration can be measured without host-side gaps.  Both NULL
- * clears a pending pair.  The caller owns the events. */
+/* Profiling: the next launch, on the calling thread, of the kernel that does
+ * the main work of an entry point (the kernel oc_conv_kernel names for a
+ * convolution pass; the pooling, routing or unpooling kernel of oc_pool_* /
+ * oc_unpool_*) is bracketed by these events, recorded at the start and the
+ * end of that kernel on its stream (as hipExtLaunchKernelGGL does), so that
+ * its duration is measured without host-side gaps.  Both NULL clears a
+ * pending pair.  The caller owns the events. */
 oc_status oc_profile_next(hipEvent_t start, hipEvent_t stop);
 
 const char* oc_status_str(oc_status s);

@@ -171,10 +171,10 @@ oc_status oc_pool_fwd(const oc_octree* t, int32_t l, const float* x, int32_t c, 
   if (n == 0) return OC_OK;
   if (vec4_ok(c, x, y, sw)) {
     const int cv = c / 4;
-    hipLaunchKernelGGL(k_pool_fwd<4>, dim3(grid_for(n * cv)), dim3(TB), 0, s, x,
+    oc::launch_main(k_pool_fwd<4>, dim3(grid_for(n * cv)), dim3(TB), s, x,
                        (const int32_t*)t->labels[l - 1], n, cv, y, sw);
   } else {
-    hipLaunchKernelGGL(k_pool_fwd<1>, dim3(grid_for(n * c)), dim3(TB), 0, s, x,
+    oc::launch_main(k_pool_fwd<1>, dim3(grid_for(n * c)), dim3(TB), s, x,
                        (const int32_t*)t->labels[l - 1], n, c, y, sw);
   }
   OC_LAUNCH_CHECK();
@@ -190,10 +190,10 @@ static oc_status route_down(const oc_octree* t, int32_t l, const float* in, cons
   if (n == 0) return OC_OK;
   if (vec4_ok(c, in, out, sw) && (uintptr_t)ymask % 16 == 0) {
     const int cv = c / 4;
-    hipLaunchKernelGGL(k_route_down<4>, dim3(grid_for(n * cv)), dim3(TB), 0, s, in, ymask, sw,
+    oc::launch_main(k_route_down<4>, dim3(grid_for(n * cv)), dim3(TB), s, in, ymask, sw,
                        (const int32_t*)t->rows[l - 1], n, cv, out);
   } else {
-    hipLaunchKernelGGL(k_route_down<1>, dim3(grid_for(n * c)), dim3(TB), 0, s, in, ymask, sw,
+    oc::launch_main(k_route_down<1>, dim3(grid_for(n * c)), dim3(TB), s, in, ymask, sw,
                        (const int32_t*)t->rows[l - 1], n, c, out);
   }
   OC_LAUNCH_CHECK();
@@ -218,10 +218,10 @@ oc_status oc_unpool_bwd(const oc_octree* t, int32_t l, const float* dy, const ui
   if (n == 0) return OC_OK;
   if (vec4_ok(c, dy, dx, sw)) {
     const int cv = c / 4;
-    hipLaunchKernelGGL(k_route_up<4>, dim3(grid_for(n * cv)), dim3(TB), 0, s, dy, sw,
+    oc::launch_main(k_route_up<4>, dim3(grid_for(n * cv)), dim3(TB), s, dy, sw,
                        (const int32_t*)t->labels[l - 1], n, cv, dx);
   } else {
-    hipLaunchKernelGGL(k_route_up<1>, dim3(grid_for(n * c)), dim3(TB), 0, s, dy, sw,
+    oc::launch_main(k_route_up<1>, dim3(grid_for(n * c)), dim3(TB), s, dy, sw,
                        (const int32_t*)t->labels[l - 1], n, c, dx);
   }
   OC_LAUNCH_CHECK();
