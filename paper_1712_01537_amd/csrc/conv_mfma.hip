@@ -42,19 +42,36 @@ constexpr int WAVES = TB / 64;
 
 typedef __attribute__((address_space(3))) void* lptr_t;  // LDS
 
-// 16 zero bytes: the source of direct-to-LDS loads of absent rows.
-__device__ __attribute__((aligned(16))) float oc_zero16[4];
-
 // Direct global->LDS load of 16 bytes per lane: lane i's bytes land at LDS
 // byte address lds + 16 i (lds uniform over the wave).  Written as inline
 // assembly so that the compiler's wait insertion, which does not know the
 // instruction, keeps exact LDS counters for the surrounding code; the caller
 // waits for completion itself (vm_wait0) before other waves read the data.
-__device__ __forceinline__ void lds_load16(const void* src, const void* lds) {
-  const uint32_t a = (uint32_t)(uintptr_t)(lptr_t)lds;
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(a), "v"(src)
+// LDS byte address of a wave-uniform LDS pointer, in a scalar register.
+__device__ __forceinline__ uint32_t lds_addr(const void* lds) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lptr_t)lds);
+}
+__device__ __forceinline__ void lds_load16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(src)
                : "memory", "m0");
 }
+// The same for 12 bytes per lane (the lane stride in LDS stays 16 bytes).
+__device__ __forceinline__ void lds_load12(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx3 %1, off" ::"s"(lds), "v"(src)
+               : "memory", "m0");
+}
+// A 16x16 MFMA result held as D[4(l/16)+j][l%16] in lane l (j = 0..3) is
+// handed over so that lane l holds D[4(l%4)+j][l/4]: with rows l%16 of the
+// result as output rows, consecutive lanes then store consecutive 16 bytes.
+__device__ __forceinline__ v4f store_order(v4f d, int lane) {
+  const int src = (((lane & 3) << 4) + (lane >> 2)) << 2;  // byte lane index
+  v4f r;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    r[j] = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(d[j])));
+  return r;
+}
+
 // s_waitcnt vmcnt(0): all of this wave's vector memory operations are done.
 __device__ __forceinline__ void vm_wait0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
@@ -446,12 +463,18 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
       ok |= (uint32_t)live << i;
     }
   };
+  // lanes of absent rows write their zeros themselves (a shared zero row
+  // would put every absent lane of the grid on one cache line)
   auto dma = [&](v4f* buf) {
 #pragma unroll
     for (int i = 0; i < GPB; ++i) {
       const bool live = ((okc >> i) & 1) && nbc[i] >= 0 && l_ch < kk;
-      const float* src = live ? x + (int64_t)(nbc[i] + l_coff) * kk + l_ch : oc_zero16;
-      lds_load16(src, buf + i * GSTR + px * XSTR);
+      v4f* blk = buf + i * GSTR + px * XSTR;
+      const uint32_t a = lds_addr(blk);
+      if (live)
+        lds_load16(x + (int64_t)(nbc[i] + l_coff) * kk + l_ch, a);
+      else
+        blk[lane] = v4f{0.f, 0.f, 0.f, 0.f};
     }
   };
 
@@ -497,14 +520,16 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const int64_t nrows = 8 * ngroups;
   const bool split = gridDim.z > 1;
   float* dst = split ? part + (int64_t)blockIdx.z * nrows * nn : out;
-  // accumulator j of lane l: output channel 4(l/16) + j, row l % 16
+  // accumulator j of lane l: output channel 4(l/16) + j, row l % 16; stored
+  // after store_order: lane l writes row l/4, channels 4(l%4)..
   auto epilogue = [&](int t, v4f (&acc)[RB]) {
-    const int n = n0 + 4 * q;
+    const int n = n0 + 4 * (lane & 3);
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
-      const int64_t row = 8 * (tile0 + t) * GPB + 16 * (wm * RB + r) + li;
+      const int64_t row = 8 * (tile0 + t) * GPB + 16 * (wm * RB + r) + (lane >> 2);
+      const v4f sv = store_order(acc[r], lane);
       if (n < nn && row < nrows) {
-        v4f v = acc[r];
+        v4f v = sv;
         if (!split && relu) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) v[j] = fmaxf(v[j], 0.f);
@@ -560,6 +585,100 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
     epilogue(T - 1, acc0);
   else
     epilogue(T - 1, acc1);
+}
+
+// ---------------------------------------------------------------------------
+// Stride-1, K = 3 forward for Cin = 3 or 4 (k_conv_cin): the first layer,
+// whose rows are too short for the channel-quad kernels.  MFMA step s is tap
+// s; within it, lane group q supplies input channel q (a zero weight when
+// q >= Cin), so a row block of 16 octants takes 27 MFMAs and every operand
+// read is one base register plus a compile-time offset.  The MFMA computes
+// out^T: A = W^T (16 output channels x 4 channels of tap s), B = the gathered
+// rows (4 channels x 16 octants).
+// A workgroup takes 8 sibling groups (64 rows, one block of 16 per wave) and
+// 16 output channels (blockIdx.y).  Each group's (K+1)^3 tile is one wave
+// load instruction (direct global->LDS, 12 or 16 bytes per position at a
+// 16-byte lane stride), position (x, y, z) in slot 16x + 4y + z.  The weight
+// block goes through LDS with 16-byte loads.
+template <int CIN>
+__global__ __launch_bounds__(TB) void k_conv_cin(const int32_t* __restrict__ nbr, int64_t ngroups,
+                                                 const float* __restrict__ x,
+                                                 const float* __restrict__ w, int nn,
+                                                 float* __restrict__ out, int relu) {
+  constexpr int K3 = 27, GPB = 8;
+  constexpr int GSTR = 64 * 4 + 8;  // floats per group tile; 8 mod 32 separates the two groups' banks
+  constexpr int NW4 = K3 * 4 * 4;   // float4 elements of the weight block [27][4][16]
+  __shared__ __attribute__((aligned(16))) float Xs[GPB * GSTR];
+  __shared__ __attribute__((aligned(16))) v4f Ws[NW4];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int li = lane & 15, q = lane >> 4;
+  const int n0 = blockIdx.y * 16;
+  const int64_t g0 = (int64_t)blockIdx.x * GPB;
+
+  // loads: wave w fills the tiles of groups 2w and 2w+1, lane = slot
+  {
+    const int px = lane >> 4, py = (lane >> 2) & 3, pz = lane & 3;
+    const int ux = px - 1, uy = py - 1, uz = pz - 1;
+    const int slot = ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1);
+    const int coff = 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
+    int32_t nb[2];
+#pragma unroll
+    for (int gg = 0; gg < 2; ++gg) {
+      const int64_t g = g0 + 2 * wave + gg;
+      nb[gg] = g < ngroups ? nbr[27 * g + slot] : -1;
+    }
+#pragma unroll
+    for (int gg = 0; gg < 2; ++gg) {
+      float* dst = Xs + (2 * wave + gg) * GSTR;
+      const uint32_t a = lds_addr(dst);
+      if (nb[gg] >= 0) {  // absent rows: the lane writes zeros itself
+        const float* src = x + (int64_t)(nb[gg] + coff) * CIN;
+        if constexpr (CIN == 4) {
+          lds_load16(src, a);
+        } else {
+          lds_load12(src, a);
+        }
+      } else {
+        *reinterpret_cast<v4f*>(dst + 4 * lane) = v4f{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  }
+  // the weight block: Ws[(k * 4 + c) * 4 + f] = W[k][c][n0 + 4f..] (zero for
+  // c >= Cin or past nn), 16-byte loads
+#pragma unroll
+  for (int i = 0; i < (NW4 + TB - 1) / TB; ++i) {
+    const int e = tid + i * TB;
+    if (e < NW4) {
+      const int f = e & 3, c = (e >> 2) & 3, k = e >> 4, n = n0 + 4 * f;
+      Ws[e] = c < CIN && n < nn ? *reinterpret_cast<const v4f*>(w + ((int64_t)k * CIN + c) * nn + n)
+                                : v4f{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+  vm_wait0();  // this wave's tile loads have landed
+  __syncthreads();
+  // lane (li, q): row li of the wave's block (child li & 7 of group
+  // 2 wave + (li >> 3)), input channel q (channel 0 with weight 0 past Cin)
+  const int c = li & 7;
+  const float* xb = Xs + (2 * wave + (li >> 3)) * GSTR +
+                    4 * (16 * (c >> 2) + 4 * ((c >> 1) & 1) + (c & 1)) + (q < CIN ? q : 0);
+  const float* wb = reinterpret_cast<const float*>(Ws) + q * 16 + li;
+  v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k = 0; k < K3; ++k)
+    acc = mfma4(wb[k * 64], xb[4 * (16 * (k / 9) + 4 * ((k / 3) % 3) + k % 3)], acc);
+  // accumulator j of lane l: output channel n0 + 4(l/16) + j, row l % 16;
+  // after store_order lane l writes row l/4, channels n0 + 4(l%4)..
+  acc = store_order(acc, lane);
+  const int64_t row = 8 * g0 + 16 * wave + (lane >> 2);
+  const int n = n0 + 4 * (lane & 3);
+  if (row < 8 * ngroups && n < nn) {
+    if (relu) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = fmaxf(acc[j], 0.f);
+    }
+    *reinterpret_cast<v4f*>(out + row * nn + n) = acc;
+  }
 }
 
 // out[e] = sum over splits of part[z][e] (in split order), ReLU if relu.
@@ -1333,6 +1452,11 @@ void launch_dw(const oc_octree* t, int l, const DwCfg& c, const float* x, int ci
                      (const int32_t*)t->nbr[l], t->M[l - 1], c.gchunk, x, cin, dy, cout, part);
 }
 
+// Forward of a 3- or 4-channel input (the first layer): k_conv_cin.
+inline bool use_cin_kernel(int K, int cin, int cout) {
+  return K == 3 && (cin == 3 || cin == 4) && cout % 4 == 0;
+}
+
 }  // namespace
 
 namespace oc {
@@ -1348,6 +1472,10 @@ void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, in
     }
     const DwCfg c = pick_dw(K, t->M[l - 1], cin, cout);
     snprintf(buf, n, "k_conv_dw<%d, %d, %d, %d, %d, %d>", K, c.VA, c.VB, c.TT, c.MB, c.WT);
+    return;
+  }
+  if (pass == 0 && use_cin_kernel(K, cin, cout)) {
+    snprintf(buf, n, "k_conv_cin<%d>", cin);
     return;
   }
   const int kk = pass == 0 ? cin : cout, nn = pass == 0 ? cout : cin;
@@ -1367,6 +1495,17 @@ size_t conv_s1_tile_ws(const oc_octree* t, int l, int K, int kk, int nn) {
 
 void conv_s1_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin, const float* w,
                      int cout, float* y, int relu, float* ws, hipStream_t s) {
+  if (use_cin_kernel(K, cin, cout)) {
+    const int64_t G = t->M[l - 1];
+    const dim3 grid((unsigned)oc::cdiv(G, 8), (unsigned)oc::cdiv(cout, 16));
+    if (cin == 3)
+      oc::launch_main(k_conv_cin<3>, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, w, cout,
+                      y, relu);
+    else
+      oc::launch_main(k_conv_cin<4>, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, w, cout,
+                      y, relu);
+    return;
+  }
   dispatch_tile<false>(t, l, K, x, cin, w, cout, y, relu, ws, s);
 }
 

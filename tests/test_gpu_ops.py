@@ -52,6 +52,8 @@ SMALL = [  # seed, B, n, depth, K, stride, cin, cout, relu
     (6, 1, 300, 3, 3, 1, 3, 16, True),
     (7, 4, 300, 4, 5, 1, 12, 20, True),
     (8, 2, 900, 5, 3, 1, 64, 128, False),
+    (9, 3, 400, 4, 3, 1, 4, 32, True),  # 4-channel input, two column blocks
+    (10, 2, 300, 5, 3, 1, 3, 20, False),  # 3-channel input, ragged column block
 ]
 
 
