@@ -413,11 +413,13 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
 // loads into two static buffers: tile t+1 lands while tile t is multiplied,
 // with one barrier per tile.  Absent neighbours and channels past kk read a
 // zero row.
-// Group tile layout, in 16-byte chunks: group g at 274 g, x-slab at 65 x,
-// position (y, z) at slot 4z + ((y + 2z) & 3), channel quad last.  A 16-lane
-// read of one tap touches 2 groups x 2 slabs x 2 y x 2 z positions, which
-// this order puts on distinct banks.  Each x-slab of a group (16 positions x
-// 4 quads) is one wave's load instruction.
+// Group tile layout, in 16-byte chunks: group g at 280 g, x-slab at 68 x,
+// position (y, z) at slot 4y + z, channel quad f stored at f ^ ((y + 2z) & 3).
+// A read of one tap by 8 (or 16) lanes touches 2 slabs x 2 y x 2 z positions
+// (of 1 or 2 groups) at one quad; the quad swizzle and the strides (68 = 4
+// mod 8, 280 = 8 mod 16) put them on distinct banks whether the LDS serves 8
+// lanes from 32 banks or 16 lanes from 64.  Each x-slab of a group (16
+// positions x 4 quads) is one wave's load instruction.
 // FLIP: input gradient, W'[k][c][n] = W[26-k][n][c].
 template <int WN, int GPB, bool FLIP>
 __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_conv_tile3(const int32_t* __restrict__ nbr,
@@ -428,7 +430,7 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
   constexpr int K3 = 27, BN = 16 * WN, WM = WAVES / WN;
   constexpr int RB = GPB / 2 / WM;  // row blocks per wave
   static_assert(RB >= 1 && RB * WM * 2 == GPB, "every row block has one wave");
-  constexpr int GSTR = 274, XSTR = 65, BUFC = GPB * GSTR;  // in 16-byte chunks
+  constexpr int GSTR = 280, XSTR = 68, BUFC = GPB * GSTR;  // in 16-byte chunks
   __shared__ __attribute__((aligned(16))) v4f X0[BUFC];
   __shared__ __attribute__((aligned(16))) v4f X1[BUFC];
 
@@ -444,9 +446,10 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const int T = (int)(ntile * (lb + 1) / nx - tile0);
   if (T <= 0) return;  // uniform over the workgroup
 
-  // loads: wave w fills x-slab w of every group; lane -> (slot s, quad f)
-  const int s_ = lane >> 2, f_ = lane & 3;
-  const int pz = s_ >> 2, py = (s_ - 2 * pz) & 3, px = wave;
+  // loads: wave w fills x-slab w of every group; lane -> chunk (slot 4y + z,
+  // stored quad), holding channel quad (stored ^ ((y + 2z) & 3))
+  const int py = lane >> 4, pz = (lane >> 2) & 3, px = wave;
+  const int f_ = (lane & 3) ^ ((py + 2 * pz) & 3);
   const int ux = px - 1, uy = py - 1, uz = pz - 1;
   const int l_slot = ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1);
   const int l_coff = 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
@@ -487,7 +490,7 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
 #pragma unroll
     for (int j = 0; j < 9; ++j) {
       const int y = cy + j / 3, z = cz + j % 3;
-      aoff[j] = g * GSTR + cx * XSTR + 4 * (4 * z + ((y + 2 * z) & 3)) + q;
+      aoff[j] = g * GSTR + cx * XSTR + 4 * (4 * y + z) + (q ^ ((y + 2 * z) & 3));
     }
   }
 
