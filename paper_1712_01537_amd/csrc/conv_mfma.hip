@@ -685,13 +685,45 @@ __global__ __launch_bounds__(TB) void k_conv_cin(const int32_t* __restrict__ nbr
 }
 
 // out[e] = sum over splits of part[z][e] (in split order), ReLU if relu.
+// Four consecutive entries per thread (16-byte loads when vec, i.e. n is a
+// multiple of 4 and the buffers are 16-byte aligned), four splits in flight.
 __global__ __launch_bounds__(TB) void k_sum_split(const float* __restrict__ part, int splits,
-                                                  int64_t n, float* __restrict__ out, int relu) {
-  const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
+                                                  int64_t n, float* __restrict__ out, int relu,
+                                                  int vec) {
+  const int64_t e = 4 * ((int64_t)blockIdx.x * TB + threadIdx.x);
   if (e >= n) return;
-  float s = 0.f;
-  for (int z = 0; z < splits; ++z) s += part[(int64_t)z * n + e];
-  out[e] = relu ? fmaxf(s, 0.f) : s;
+  if (vec) {
+    const v4f* p = reinterpret_cast<const v4f*>(part + e);
+    const int64_t n4 = n / 4;
+    v4f s = {0.f, 0.f, 0.f, 0.f};
+    int z = 0;
+    for (; z + 4 <= splits; z += 4) {
+      const v4f a = p[z * n4], b = p[(z + 1) * n4], c = p[(z + 2) * n4], d = p[(z + 3) * n4];
+      s += a;
+      s += b;
+      s += c;
+      s += d;
+    }
+    for (; z < splits; ++z) s += p[z * n4];
+    if (relu) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) s[j] = fmaxf(s[j], 0.f);
+    }
+    *reinterpret_cast<v4f*>(out + e) = s;
+    return;
+  }
+  for (int64_t i = e; i < e + 4 && i < n; ++i) {
+    float s = 0.f;
+    for (int z = 0; z < splits; ++z) s += part[(int64_t)z * n + i];
+    out[i] = relu ? fmaxf(s, 0.f) : s;
+  }
+}
+
+// Launch of k_sum_split over n entries.
+void sum_split(const float* part, int splits, int64_t n, float* out, int relu, hipStream_t s) {
+  const int vec = n % 4 == 0 && (uintptr_t)part % 16 == 0 && (uintptr_t)out % 16 == 0;
+  hipLaunchKernelGGL(k_sum_split, dim3((unsigned)oc::cdiv(n, 4 * TB)), dim3(TB), 0, s, part, splits,
+                     n, out, relu, vec);
 }
 
 // ---------------------------------------------------------------------------
@@ -1163,6 +1195,36 @@ __global__ __launch_bounds__(TB) void k_sum_parts1(const float* __restrict__ par
   if (sg == 0 && e < n) seg[(int64_t)blockIdx.y * n + e] = ((r[0][el] + r[1][el]) + r[2][el]) + r[3][el];
 }
 
+// k_sum_parts1 with four consecutive entries per lane (n a multiple of 4,
+// 16-byte aligned buffers): 256 entries per workgroup, the same order of
+// additions per entry.
+__global__ __launch_bounds__(TB) void k_sum_parts1v(const float* __restrict__ part, int np, int sp,
+                                                    int64_t n, float* __restrict__ seg) {
+  __shared__ v4f r[4][64];
+  const int el = threadIdx.x & 63, sg = threadIdx.x >> 6;
+  const int64_t e4 = (int64_t)blockIdx.x * 64 + el, n4 = n / 4;
+  const int p0 = blockIdx.y * sp, p1 = p0 + sp < np ? p0 + sp : np;
+  const v4f* pv = reinterpret_cast<const v4f*>(part);
+  v4f s = {0.f, 0.f, 0.f, 0.f};
+  if (e4 < n4) {
+    int p = p0 + sg;
+    for (; p + 12 < p1; p += 16) {  // four independent loads in flight
+      const v4f a = pv[(int64_t)p * n4 + e4], b = pv[(int64_t)(p + 4) * n4 + e4];
+      const v4f c = pv[(int64_t)(p + 8) * n4 + e4], d = pv[(int64_t)(p + 12) * n4 + e4];
+      s += a;
+      s += b;
+      s += c;
+      s += d;
+    }
+    for (; p < p1; p += 4) s += pv[(int64_t)p * n4 + e4];
+  }
+  r[sg][el] = s;
+  __syncthreads();
+  if (sg == 0 && e4 < n4)
+    reinterpret_cast<v4f*>(seg)[(int64_t)blockIdx.y * n4 + e4] =
+        ((r[0][el] + r[1][el]) + r[2][el]) + r[3][el];
+}
+
 __global__ __launch_bounds__(TB) void k_sum_parts2(const float* __restrict__ seg, int ns, int64_t n,
                                                    float* __restrict__ out) {
   const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
@@ -1177,8 +1239,13 @@ inline int sum_segments(int np) { return np <= 64 ? 1 : (int)oc::cdiv(np, 64); }
 
 void sum_parts(const float* part, int np, int64_t n, float* seg, float* out, hipStream_t s) {
   const int ns = sum_segments(np), sp = (int)oc::cdiv(np, ns);
-  hipLaunchKernelGGL(k_sum_parts1, dim3((unsigned)oc::cdiv(n, 64), (unsigned)ns), dim3(TB), 0, s,
-                     part, np, sp, n, ns == 1 ? out : seg);
+  float* dst = ns == 1 ? out : seg;
+  if (n % 4 == 0 && (uintptr_t)part % 16 == 0 && (uintptr_t)dst % 16 == 0)
+    hipLaunchKernelGGL(k_sum_parts1v, dim3((unsigned)oc::cdiv(n, 256), (unsigned)ns), dim3(TB), 0, s,
+                       part, np, sp, n, dst);
+  else
+    hipLaunchKernelGGL(k_sum_parts1, dim3((unsigned)oc::cdiv(n, 64), (unsigned)ns), dim3(TB), 0, s,
+                       part, np, sp, n, dst);
   if (ns > 1)
     hipLaunchKernelGGL(k_sum_parts2, dim3((unsigned)oc::cdiv(n, TB)), dim3(TB), 0, s,
                        (const float*)seg, ns, n, out);
@@ -1257,9 +1324,7 @@ void launch_tile(const oc_octree* t, int l, const TileCfg& c, const float* x, in
   oc::launch_main(kernel, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, kk, w, nn, out, relu,
                   c.cps, part);
   if (c.splits > 1) {
-    const int64_t n = t->N[l] * (int64_t)nn;
-    hipLaunchKernelGGL(k_sum_split, dim3((unsigned)oc::cdiv(n, TB)), dim3(TB), 0, s,
-                       (const float*)part, c.splits, n, out, relu);
+    sum_split(part, c.splits, t->N[l] * (int64_t)nn, out, relu, s);
   }
 }
 
@@ -1283,9 +1348,7 @@ void launch_tile2(const oc_octree* t, int l, const TileCfg& c, const float* x, i
   oc::launch_main(kernel, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, kk, w, nn, out,
                   relu, part);
   if (c.splits > 1) {
-    const int64_t n = t->N[l] * (int64_t)nn;
-    hipLaunchKernelGGL(k_sum_split, dim3((unsigned)oc::cdiv(n, TB)), dim3(TB), 0, s,
-                       (const float*)part, c.splits, n, out, relu);
+    sum_split(part, c.splits, t->N[l] * (int64_t)nn, out, relu, s);
   }
 }
 
