@@ -951,15 +951,22 @@ __global__ __launch_bounds__(TB) void k_conv_dw(const int32_t* __restrict__ nbr,
 // FLAT mode (cin < 16): M runs over (tap, channel) pairs m = tap cin + c,
 // which is the row of dW itself; blocks of 16 pairs are dealt to the waves
 // (rotated by workgroup so that no SIMD always gets the short share).
+// HV = 2 (tiled mode only): the workgroup is two such 4-wave halves that
+// take alternate stages of the chunk, each with its own staging buffers; at
+// the end they add their accumulators through LDS (half 0 keeps the first
+// ceil(NJ/2) blocks, half 1 the rest), so a workgroup holds twice the
+// octants per partial and the partial traffic halves.
 // Workgroup (chunk, tile) writes part[chunk][K3 cin][cout] for its block of
 // dW (every entry of the block, zeros included); a second kernel adds the
 // chunks in a fixed order.  XV: cin is a multiple of 4 (x rows read as
 // float4); cout must be a multiple of 4.
-template <bool FLAT, int CW, int NBN, int GS, bool XV>
-__global__ __launch_bounds__(TB) void k_conv_dwt(const int32_t* __restrict__ nbr, int64_t ngroups,
-                                                 int64_t gchunk, const float* __restrict__ x,
-                                                 int cin, const float* __restrict__ dy, int cout,
-                                                 float* __restrict__ part) {
+template <bool FLAT, int CW, int NBN, int GS, bool XV, int HV>
+__global__ __launch_bounds__(TB * HV) void k_conv_dwt(const int32_t* __restrict__ nbr,
+                                                      int64_t ngroups, int64_t gchunk,
+                                                      const float* __restrict__ x, int cin,
+                                                      const float* __restrict__ dy, int cout,
+                                                      float* __restrict__ part) {
+  static_assert(HV == 1 || (HV == 2 && !FLAT), "two halves in tiled mode only");
   constexpr int R = 1, S = 4, K3 = 27, S3 = 64;
   // M blocks per wave at most: 27 taps, or ceil(27 cin / 16) <= 7, 14, 27 pairs
   constexpr int NJ = !FLAT ? 7 : CW == 4 ? 2 : CW == 8 ? 4 : 7;
@@ -973,18 +980,24 @@ __global__ __launch_bounds__(TB) void k_conv_dwt(const int32_t* __restrict__ nbr
   constexpr int NY = (NYE + TB - 1) / TB;
   static_assert(TB % (S3 * F4) == 0 && GS % GPP == 0, "x staging covers the stage");
   static_assert(NX <= 32 && NY <= 32, "validity bits fit a word");
-  __shared__ __attribute__((aligned(16))) float At[GS * P3 * RS];
-  __shared__ __attribute__((aligned(16))) float Bt[8 * GS * BNS];
+  constexpr int NA = GS * P3 * RS, NB = 8 * GS * BNS;      // floats of one half's buffers
+  constexpr int NRED = HV == 2 ? NJ * NBN * WAVES * 64 * 4 : 0;  // floats of the reduction
+  constexpr int NSM = HV * (NA + NB) > NRED ? HV * (NA + NB) : NRED;
+  __shared__ __attribute__((aligned(16))) float smem[NSM];
 
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = threadIdx.x & (TB - 1), lane = tid & 63;
+  const int half = HV == 1 ? 0 : __builtin_amdgcn_readfirstlane(threadIdx.x >> 8);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
+  float* const At = smem + half * (NA + NB);
+  float* const Bt = At + NA;
   const int li = lane & 15, q = lane >> 4;
   const int nCB = FLAT ? 1 : (cin + 15) / 16;
   const int cbk = (int)(blockIdx.y % nCB), nbk = (int)(blockIdx.y / nCB);
   const int c0 = FLAT ? 0 : 16 * cbk, n0 = BN * nbk;
   const int64_t gb = (int64_t)blockIdx.x * gchunk;
   const int64_t ge = gb + gchunk < ngroups ? gb + gchunk : ngroups;
-  const int nsub = gb < ge ? (int)((ge - gb + GS - 1) / GS) : 0;
+  // stages of GS groups; half h takes stages h, h + HV, ...
+  const int nsub = gb < ge ? (int)((ge - gb + GS * HV - 1) / (GS * HV)) : 0;
   const int nmb = FLAT ? (K3 * cin + 15) / 16 : K3;  // M blocks (taps when tiled)
   const int rot = FLAT ? (int)(blockIdx.x % WAVES) : 0;
   const int mb0 = (wave + rot) % WAVES;
@@ -1034,7 +1047,7 @@ __global__ __launch_bounds__(TB) void k_conv_dwt(const int32_t* __restrict__ nbr
     ok = 0;
 #pragma unroll
     for (int i = 0; i < NX; ++i) {
-      const int64_t g = gb + (int64_t)s * GS + a_g + GPP * i;
+      const int64_t g = gb + (int64_t)(HV * s + half) * GS + a_g + GPP * i;
       const bool live = g < ge;
       v[i] = nbr[live ? 27 * g + a_slot : 0];
       ok |= (uint32_t)live << i;
@@ -1076,9 +1089,9 @@ __global__ __launch_bounds__(TB) void k_conv_dwt(const int32_t* __restrict__ nbr
     for (int i = 0; i < NY; ++i) {
       const int e = tid + i * TB;
       const int r = e / (BN / 4), gn = n0 + 4 * (e % (BN / 4));
-      const int64_t g = gb + (int64_t)s * GS + r / 8;
-      const bool live = e < NYE && g < ge && gn < cout;
-      const int64_t off = live ? (8 * (gb + (int64_t)s * GS) + r) * cout + gn : 0;
+      const int64_t g0 = gb + (int64_t)(HV * s + half) * GS;
+      const bool live = e < NYE && g0 + r / 8 < ge && gn < cout;
+      const int64_t off = live ? (8 * g0 + r) * cout + gn : 0;
       ry[i] = *reinterpret_cast<const v4f*>(dy + off);
       yok |= (uint32_t)live << i;
     }
@@ -1140,13 +1153,35 @@ __global__ __launch_bounds__(TB) void k_conv_dwt(const int32_t* __restrict__ nbr
     }
   }
 
+  // halves add their accumulators: block j goes to half j < JH ? 0 : 1
+  constexpr int JH = (NJ + 1) / 2;
+  if constexpr (HV == 2) {
+    v4f* red = reinterpret_cast<v4f*>(smem);
+    __syncthreads();  // the last stage's LDS reads are done
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if ((j < JH) != (half == 0))
+#pragma unroll
+        for (int nb = 0; nb < NBN; ++nb) red[((j * NBN + nb) * WAVES + wave) * 64 + lane] = acc[j][nb];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if ((j < JH) == (half == 0))
+#pragma unroll
+        for (int nb = 0; nb < NBN; ++nb) {
+          const v4f o = red[((j * NBN + nb) * WAVES + wave) * 64 + lane];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[j][nb][r] += o[r];
+        }
+  }
+
   // accumulator r of lane l: M row 4(l/16) + r, column l % 16
   const int64_t entries = (int64_t)K3 * cin * cout;
   float* pp = part + (int64_t)blockIdx.x * entries;
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     const int mb = 4 * j + mb0;
-    if (j >= njw) continue;
+    if (j >= njw || (HV == 2 && (j < JH) != (half == 0))) continue;
 #pragma unroll
     for (int nb = 0; nb < NBN; ++nb) {
       const int n = n0 + 16 * nb + li;
@@ -1382,7 +1417,7 @@ void dispatch_tile(const oc_octree* t, int l, int K, const float* x, int kk, con
 // and cin a multiple of 4 when cin >= 16.
 struct DwtCfg {
   bool flat, xv;
-  int CW, NBN, GS, tiles;
+  int CW, NBN, GS, HV, tiles;
   int64_t gchunk, nchunks;
 };
 
@@ -1401,6 +1436,7 @@ bool pick_dwt(int K, int64_t G, int cin, int cout, DwtCfg* c) {
     c->CW = 16, c->GS = 4;
     c->NBN = cout >= 64 ? 4 : cout >= 32 ? 2 : 1;
   }
+  c->HV = c->flat ? 1 : 2;
   const int nCB = c->flat ? 1 : (int)oc::cdiv(cin, 16);
   c->tiles = nCB * (int)oc::cdiv(cout, 16 * c->NBN);
   const int64_t entries = (int64_t)27 * cin * cout;
@@ -1414,20 +1450,20 @@ bool pick_dwt(int K, int64_t G, int cin, int cout, DwtCfg* c) {
   return true;
 }
 
-template <bool FLAT, int CW, int NBN, int GS, bool XV>
+template <bool FLAT, int CW, int NBN, int GS, bool XV, int HV>
 void launch_dwt(const oc_octree* t, int l, const DwtCfg& c, const float* x, int cin,
                 const float* dy, int cout, float* part, hipStream_t s) {
   dim3 grid((unsigned)c.nchunks, (unsigned)c.tiles);
-  oc::launch_main(k_conv_dwt<FLAT, CW, NBN, GS, XV>, grid, dim3(TB), s, (const int32_t*)t->nbr[l],
+  oc::launch_main(k_conv_dwt<FLAT, CW, NBN, GS, XV, HV>, grid, dim3(TB * HV), s, (const int32_t*)t->nbr[l],
                   t->M[l - 1], c.gchunk, x, cin, dy, cout, part);
 }
 
 // Resident workgroups per CU of the configuration's kernel (cached).
-template <bool FLAT, int CW, int NBN, int GS, bool XV>
+template <bool FLAT, int CW, int NBN, int GS, bool XV, int HV>
 int dwt_occ() {
   static const int occ = [] {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_conv_dwt<FLAT, CW, NBN, GS, XV>, TB, 0) !=
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_conv_dwt<FLAT, CW, NBN, GS, XV, HV>, TB * HV, 0) !=
             hipSuccess ||
         n < 1)
       n = 1;
@@ -1437,16 +1473,17 @@ int dwt_occ() {
 }
 
 #define OC_DWT_LIST(X)                                                                       \
-  X(false, 16, 1, 4, true) X(false, 16, 2, 4, true) X(false, 16, 4, 4, true)                \
-  X(true, 4, 1, 16, true) X(true, 4, 2, 16, true) X(true, 4, 1, 16, false)                   \
-  X(true, 4, 2, 16, false) X(true, 8, 1, 8, true) X(true, 8, 2, 8, true)                     \
-  X(true, 8, 1, 8, false) X(true, 8, 2, 8, false) X(true, 16, 1, 4, true)                    \
-  X(true, 16, 2, 4, true) X(true, 16, 1, 4, false) X(true, 16, 2, 4, false)
+  X(false, 16, 1, 4, true, 2) X(false, 16, 2, 4, true, 2) X(false, 16, 4, 4, true, 2)       \
+  X(true, 4, 1, 16, true, 1) X(true, 4, 2, 16, true, 1) X(true, 4, 1, 16, false, 1)          \
+  X(true, 4, 2, 16, false, 1) X(true, 8, 1, 8, true, 1) X(true, 8, 2, 8, true, 1)            \
+  X(true, 8, 1, 8, false, 1) X(true, 8, 2, 8, false, 1) X(true, 16, 1, 4, true, 1)           \
+  X(true, 16, 2, 4, true, 1) X(true, 16, 1, 4, false, 1) X(true, 16, 2, 4, false, 1)
 
 int dwt_occupancy(const DwtCfg& c) {
-#define OC_DWT_OCC(FLAT_, CW_, NBN_, GS_, XV_)                                              \
-  if (c.flat == FLAT_ && c.CW == CW_ && c.NBN == NBN_ && c.GS == GS_ && c.xv == XV_)       \
-    return dwt_occ<FLAT_, CW_, NBN_, GS_, XV_>();
+#define OC_DWT_OCC(FLAT_, CW_, NBN_, GS_, XV_, HV_)                                         \
+  if (c.flat == FLAT_ && c.CW == CW_ && c.NBN == NBN_ && c.GS == GS_ && c.xv == XV_ &&      \
+      c.HV == HV_)                                                                          \
+    return dwt_occ<FLAT_, CW_, NBN_, GS_, XV_, HV_>();
   OC_DWT_LIST(OC_DWT_OCC)
 #undef OC_DWT_OCC
   return 1;
@@ -1454,9 +1491,10 @@ int dwt_occupancy(const DwtCfg& c) {
 
 bool dispatch_dwt(const oc_octree* t, int l, const DwtCfg& c, const float* x, int cin,
                   const float* dy, int cout, float* part, hipStream_t s) {
-#define OC_DWT(FLAT_, CW_, NBN_, GS_, XV_)                                                  \
-  if (c.flat == FLAT_ && c.CW == CW_ && c.NBN == NBN_ && c.GS == GS_ && c.xv == XV_) {    \
-    launch_dwt<FLAT_, CW_, NBN_, GS_, XV_>(t, l, c, x, cin, dy, cout, part, s);           \
+#define OC_DWT(FLAT_, CW_, NBN_, GS_, XV_, HV_)                                             \
+  if (c.flat == FLAT_ && c.CW == CW_ && c.NBN == NBN_ && c.GS == GS_ && c.xv == XV_ &&    \
+      c.HV == HV_) {                                                                        \
+    launch_dwt<FLAT_, CW_, NBN_, GS_, XV_, HV_>(t, l, c, x, cin, dy, cout, part, s);      \
     return true;                                                                          \
   }
   OC_DWT_LIST(OC_DWT)
@@ -1532,8 +1570,8 @@ void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, in
   if (pass == 2) {
     DwtCfg d;
     if (pick_dwt(K, t->M[l - 1], cin, cout, &d)) {
-      snprintf(buf, n, "k_conv_dwt<%s, %d, %d, %d, %s>", d.flat ? "true" : "false", d.CW, d.NBN,
-               d.GS, d.xv ? "true" : "false");
+      snprintf(buf, n, "k_conv_dwt<%s, %d, %d, %d, %s, %d>", d.flat ? "true" : "false", d.CW,
+               d.NBN, d.GS, d.xv ? "true" : "false", d.HV);
       return;
     }
     const DwCfg c = pick_dw(K, t->M[l - 1], cin, cout);
