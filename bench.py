@@ -7,8 +7,11 @@ points and normals are already in HBM:
   tables) and the workload's network forward (conv + fused ReLU, max-pool) and
   backward (pool routing, conv input and weight gradients).  Like the paper's
   precomputation of the next iteration's hash table in a separate thread, the
-  octree of step i+1 is built on a second stream while the network of step i
-  runs; every timed step builds one octree and runs one forward and backward.
+  octree of step i+1 is built during step i: the part that decides the
+  per-depth counts (quantisation, occupancy bitmaps, their scan) at the head
+  of the step on the network stream, the rest (leaf signal, keys, labels,
+  neighbour tables) on a second stream while the network of step i runs;
+  every timed step builds one octree and runs one forward and backward.
 The default workload is the 32-shape depth-6 network: conv3 3->16 @d6,
 16->32 @d5, 32->64 @d4, 64->128 @d3 (each + ReLU + 2x2x2 max-pool), then
 conv3 + ReLU 128->256 @d2, fp32.
@@ -35,7 +38,6 @@ import math
 import os
 import sys
 import time
-from concurrent.futures import ThreadPoolExecutor
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
@@ -57,6 +59,7 @@ BOUND = {
     "unpool_fwd": "hbm",
     "unpool_bwd": "hbm",
     "build": "hbm",
+    "build_emit": "hbm",
 }
 
 
@@ -147,6 +150,8 @@ class Step:
     def work(self, tag, L):
         """Algorithmic flops (MFMA-bound classes) or HBM bytes of one launch."""
         N, M = self.N, self.M
+        if tag == "build_emit":  # counted with the first half
+            return 0
         if tag == "build":
             d = self.wl.depth
             return (self.npoints * 24 + sum(8 * N[k] + 4 * M[k] for k in range(d + 1))
@@ -173,7 +178,7 @@ class Step:
             torch = self.torch
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
-            if tag != "build":
+            if not tag.startswith("build"):
                 # recorded by the library at the start and end of the kernel itself
                 a.record()
                 b.record()  # instantiates the events
@@ -187,42 +192,49 @@ class Step:
             return r
         return fn()
 
-    def build(self):
-        """Build the next batch's octree on the build stream (the host waits only
-        for that stream, once, for the per-depth counts); the network stream
-        waits for it on the device."""
-        torch, oc, wl = self.torch, self.oc, self.wl
+    def _begin(self):
+        """First half of the next batch's build (up to the per-depth counts),
+        enqueued on the network stream at the head of the step."""
+        oc, wl = self.oc, self.wl
+        return self._run("build", None, lambda: oc.oc_build_async(
+            self.pts, self.nrm, self.offs, wl.depth, wl.full_depth))
+
+    def _finish(self, job):
+        """Wait for the counts of `job` and enqueue the rest of its build (leaf
+        signal, keys, labels and neighbour tables) on the build stream; the
+        network stream waits for it on the device, one step later."""
+        torch = self.torch
         with torch.cuda.stream(self.bstream):
-            tree = self._run("build", None, lambda: oc.oc_build(self.pts, self.nrm, self.offs,
-                                                                wl.depth, wl.full_depth))
+            tree = self._run("build_emit", None, lambda: job.finish(self.bstream))
             ev = torch.cuda.Event()
             ev.record(self.bstream)
         tree.record_stream(self.nstream)
         return tree, ev
 
     def __call__(self):
-        """One step: the network forward and backward on the octree built during
-        the previous step, while the octree of the next step is built.  As in
-        the paper's training (Sec. 3.2, last paragraph), the next build runs on
-        a host thread of its own: its one wait for the per-depth counts then
-        never stalls the thread that queues the network."""
+        """One step: the first half of the next batch's build, then the network
+        forward and backward on the octree built during the previous step, then
+        (once the next build's counts are known, which happens early in the
+        step on the device) the rest of the next build on the build stream,
+        where it overlaps the network.  As in the paper's training (Sec. 3.2,
+        last paragraph) the next batch's octree is built while the current
+        one trains."""
         torch = self.torch
         if getattr(self, "bstream", None) is None:
             self.nstream = torch.cuda.current_stream()
             self.bstream = torch.cuda.Stream()  # default priority
-            self.pool = ThreadPoolExecutor(max_workers=1)
-            self.pending = self.pool.submit(self.build)
-        tree, ev = self.pending.result()
+            self.cur = self._finish(self._begin())
+        job = self._begin()
+        tree, ev = self.cur
         self.nstream.wait_event(ev)
-        self.pending = self.pool.submit(self.build)
         g = self.network(tree)
         tree.free()
+        self.cur = self._finish(job)
         return g
 
     def drain(self):
-        """Wait until the pending build has been queued (before a device sync)."""
-        if getattr(self, "pending", None) is not None:
-            self.pending.result()
+        """Nothing of a step is left on the host once it returns."""
+        return None
 
     def network(self, tree):
         oc, wl = self.oc, self.wl
@@ -357,8 +369,10 @@ def main():
     step.drain()
     torch.cuda.synchronize()
     warm = step.collect()
-    # the build is many kernels on its own stream, overlapped with the network
-    dominant = max((k for k in warm if warm[k]["op"] != "build"), key=lambda k: warm[k]["ms"])
+    # the build (part at the head of the step, part on its own stream) is not a
+    # convolution or pooling class
+    dominant = max((k for k in warm if not warm[k]["op"].startswith("build")),
+                   key=lambda k: warm[k]["ms"])
     print(f"[bench] warmup done; dominant kernel: {dominant}", file=sys.stderr, flush=True)
 
     # timed region: K steps; events bracket only the dominant class

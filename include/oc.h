@@ -23,7 +23,8 @@
  *    "host" pointers are host memory.  The caller owns every buffer it passes;
  *    the library never frees them.  Buffers must not alias unless stated.
  *  - Every call enqueues work on `stream` and returns without waiting, except
- *    oc_build, which waits exactly once (to read the per-depth counts).
+ *    oc_build and oc_build_finish, which wait exactly once (to read the
+ *    per-depth counts), and oc_build_cancel.
  *  - Argument errors are detected before any work is enqueued and returned
  *    as a status; nothing is written in that case.  Asynchronous device
  *    faults surface as OC_ERR_DEVICE from a later call.  oc_last_error()
@@ -124,6 +125,40 @@ typedef struct oc_level {
 oc_status oc_build(const float* points, const float* normals, const int32_t* shape_offsets,
                    int32_t batch, int32_t depth, int32_t full_depth, const oc_allocator* alloc,
                    hipStream_t stream, oc_octree** out);
+
+/* The two halves of oc_build, for callers that overlap building the next
+ * batch's octree with other work (Sec. 3.2, last paragraph: the paper builds
+ * the next batch in a separate thread).  oc_build(..., s, out) is exactly
+ * oc_build_async(..., s, &job) followed by oc_build_finish(job, s, out).
+ *
+ * oc_build_async takes the same arguments as oc_build, checks them, takes
+ * the scratch from `alloc` on `stream` and enqueues on `stream` the part of
+ * the build that decides the per-depth counts: quantisation, the occupancy
+ * bitmaps of every depth and their popcount scan, then a copy of the counts
+ * to pinned host memory.  It returns without waiting; *job (host, opaque)
+ * owns the scratch until oc_build_finish or oc_build_cancel, and
+ * shape_offsets is copied, so the caller may reuse it at once.  points and
+ * normals must stay valid until the work of oc_build_finish is done.
+ *
+ * oc_build_finish waits for the job's counts (the one wait; only the work
+ * oc_build_async enqueued is waited for, not what follows it on its stream),
+ * allocates the octree from the job's allocator on `stream` (which may differ
+ * from the job's stream; it is made to wait for the job's work), enqueues on
+ * `stream` the leaf signal and the emission of keys, labels, rows_of_label
+ * and nbr, releases the scratch in stream order on `stream`, and returns
+ * without waiting for that work.  The octree's arrays are released on
+ * `stream` by oc_octree_free.  The job is consumed whatever the status; a
+ * point outside [0,1]^3 or a non-finite normal is reported here
+ * (OC_ERR_RANGE).
+ *
+ * oc_build_cancel waits for the job's work and releases the job without
+ * building (NULL is ignored). */
+typedef struct oc_build_job oc_build_job;
+oc_status oc_build_async(const float* points, const float* normals, const int32_t* shape_offsets,
+                         int32_t batch, int32_t depth, int32_t full_depth,
+                         const oc_allocator* alloc, hipStream_t stream, oc_build_job** job);
+oc_status oc_build_finish(oc_build_job* job, hipStream_t stream, oc_octree** out);
+void oc_build_cancel(oc_build_job* job);
 
 /* Sizes and device arrays of depth l (0..depth). */
 oc_status oc_octree_level(const oc_octree* tree, int32_t l, oc_level* out);

@@ -23,6 +23,8 @@ __all__ = [
     "lib_path",
     "load",
     "oc_build",
+    "oc_build_async",
+    "BuildJob",
     "oc_conv_fwd",
     "oc_conv_kernel",
     "oc_profile_next",
@@ -43,7 +45,8 @@ STATUS = {0: "OC_OK", 1: "OC_ERR_ARG", 2: "OC_ERR_RANGE", 3: "OC_ERR_NOMEM", 4: 
 
 # Every symbol include/oc.h declares.
 EXPORTS = (
-    "oc_build", "oc_octree_level", "oc_octree_info", "oc_octree_signal", "oc_octree_free",
+    "oc_build", "oc_build_async", "oc_build_finish", "oc_build_cancel",
+    "oc_octree_level", "oc_octree_info", "oc_octree_signal", "oc_octree_free",
     "oc_conv_fwd", "oc_conv_kernel", "oc_conv_fwd_workspace", "oc_conv_bwd_workspace", "oc_conv_bwd", "oc_pool_fwd", "oc_pool_bwd",
     "oc_unpool_fwd", "oc_unpool_bwd", "oc_status_str", "oc_last_error", "oc_profile_next",
 )
@@ -79,21 +82,30 @@ class _Allocator(C.Structure):
     _fields_ = [("alloc", _ALLOC_FN), ("free", _FREE_FN), ("ctx", C.c_void_p)]
 
 
-# Live device allocations made for the library: data_ptr -> backing tensor.
+# Live device allocations made for the library: data_ptr -> backing tensor,
+# and the stream each was allocated on.
 _live: dict[int, torch.Tensor] = {}
+_live_stream: dict[int, int] = {}
 
 
 def _torch_alloc(ctx, nbytes, stream):
+    # the wrappers make `stream` torch's current stream during the call
     try:
         t = torch.empty(int(nbytes), dtype=torch.uint8, device="cuda")
     except Exception:  # out of memory -> NULL -> OC_ERR_NOMEM
         return None
     _live[t.data_ptr()] = t
+    _live_stream[t.data_ptr()] = int(stream or 0)
     return t.data_ptr()
 
 
 def _torch_free(ctx, ptr, stream):
-    _live.pop(int(ptr), None)
+    # released in stream order on `stream`: when that is not the allocation
+    # stream, torch keeps the block until the work queued there is done
+    t = _live.pop(int(ptr), None)
+    s0 = _live_stream.pop(int(ptr), 0)
+    if t is not None and int(stream or 0) != s0:
+        t.record_stream(torch.cuda.ExternalStream(int(stream or 0)))
 
 
 _alloc_cb = _ALLOC_FN(_torch_alloc)
@@ -115,6 +127,9 @@ def load():
     p, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
     sigs = {
         "oc_build": ([p, p, p, i32, i32, i32, p, p, C.POINTER(p)], C.c_int),
+        "oc_build_async": ([p, p, p, i32, i32, i32, p, p, C.POINTER(p)], C.c_int),
+        "oc_build_finish": ([p, p, C.POINTER(p)], C.c_int),
+        "oc_build_cancel": ([p], None),
         "oc_octree_level": ([p, i32, C.POINTER(_Level)], C.c_int),
         "oc_octree_info": ([p, p, p, p], C.c_int),
         "oc_octree_signal": ([p], p),
@@ -253,6 +268,54 @@ def oc_build(points: torch.Tensor, normals: torch.Tensor, shape_offsets, depth: 
     _check(L.oc_build(pp, nn, C.c_void_p(offs.data_ptr()), len(offs) - 1, depth, full_depth,
                       C.byref(_allocator), _stream(), C.byref(h)))
     return Octree(h)
+
+
+class BuildJob:
+    """The first half of a build (oc_build_async), enqueued on the stream
+    that was current; finish() completes it into an Octree."""
+
+    def __init__(self, handle: C.c_void_p, keep):
+        self._h = handle
+        self._keep = keep  # points and normals stay alive until finish()
+
+    def finish(self, stream=None) -> Octree:
+        """Wait for the counts and enqueue the rest of the build on `stream`
+        (a torch stream; the current one when None)."""
+        if self._h is None:
+            raise OcError(1, "build job already finished or cancelled")
+        h, self._h = self._h, None
+        st = stream if stream is not None else torch.cuda.current_stream()
+        out = C.c_void_p()
+        with torch.cuda.stream(st):
+            _check(load().oc_build_finish(h, C.c_void_p(st.cuda_stream), C.byref(out)))
+        return Octree(out)
+
+    def cancel(self) -> None:
+        if self._h is not None:
+            h, self._h = self._h, None
+            load().oc_build_cancel(h)
+
+    def __del__(self):
+        try:
+            self.cancel()
+        except Exception:
+            pass
+
+
+def oc_build_async(points: torch.Tensor, normals: torch.Tensor, shape_offsets, depth: int,
+                   full_depth: int = 2) -> BuildJob:
+    """Enqueue the first half of a build on the current stream (oc_build_async)."""
+    L = load()
+    offs = torch.as_tensor(shape_offsets, dtype=torch.int32).cpu().contiguous()
+    P = int(offs[-1])
+    if points.numel() != 3 * P or normals.numel() != 3 * P:
+        raise OcError(1, f"points/normals must hold {P} x 3 values")
+    pp = _dev(points, "points", torch.float32)
+    nn = _dev(normals, "normals", torch.float32)
+    h = C.c_void_p()
+    _check(L.oc_build_async(pp, nn, C.c_void_p(offs.data_ptr()), len(offs) - 1, depth,
+                            full_depth, C.byref(_allocator), _stream(), C.byref(h)))
+    return BuildJob(h, (points, normals))
 
 
 def _dtype_code(x: torch.Tensor):

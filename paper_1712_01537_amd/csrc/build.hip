@@ -26,6 +26,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "common.h"
@@ -92,23 +93,28 @@ __device__ __forceinline__ int32_t rank_in(const uint32_t* __restrict__ bits,
 // 1. leaf occupancy.  k_quant: leaf cell of every point (~0 for a point outside
 //    [0,1]^3); bstat[block] = {flags: bit 0 such a point or NaN, bit 1 a
 //    non-finite normal; the largest |normal component| (float bits)}.
-//    k_mark: workgroup k owns leaf cells [k MK_CELLS, (k+1) MK_CELLS) as an LDS
-//    bitmap, scans the points of the shapes that overlap it, derives the words
-//    of up to MK_UP coarser depths from it (bit j of depth l = byte j of depth
-//    l+1 != 0) and stores all of them; the workgroups also fill the depths
-//    shallower than full_depth with ones.  No global atomics.
+//    k_mark: workgroup k owns leaf cells [k 32 nwd, (k+1) 32 nwd) as an LDS
+//    bitmap of nwd words (a power of two from 1024 to 8192, so that a few
+//    hundred workgroups cover the leaf depth), scans the points of the shapes
+//    that overlap it, derives the words of the coarser depths whose part of
+//    the chunk is whole words (up = log8(32 nwd / 32) of them; bit j of depth
+//    l = byte j of depth l+1 != 0) and stores all of them; the workgroups also
+//    fill the depths shallower than full_depth with ones.  No global atomics.
 
 __global__ __launch_bounds__(TB) void k_quant(const float* __restrict__ pts,
                                               const float* __restrict__ nrm, Shapes S, int B,
                                               int P, int d, uint32_t* __restrict__ leafcell,
                                               uint2* __restrict__ bstat) {
+  __shared__ int32_t so[257];
+  for (int k = threadIdx.x; k <= B; k += TB) so[k] = S.offs[k];
+  __syncthreads();
   const int i0 = blockIdx.x * TB + threadIdx.x;
   const bool live = i0 < P;
   const int i = live ? i0 : P - 1;  // the block reductions need every lane
   int lo = 0, hi = B - 1;  // last shape b with offs[b] <= i
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (S.offs[mid] <= i) lo = mid;
+    if (so[mid] <= i) lo = mid;
     else hi = mid - 1;
   }
   const float scale = (float)(1u << d);  // exact power of two
@@ -158,14 +164,33 @@ __global__ __launch_bounds__(TB) void k_quant(const float* __restrict__ pts,
 }
 
 constexpr int MK_TB = 1024;
-constexpr int MK_WORDS = 16384;                // 64 KB of LDS for the leaf depth
-constexpr int64_t MK_CELLS = 32ll * MK_WORDS;  // leaf cells per workgroup
-constexpr int MK_UP = 4;                       // coarser depths derived in LDS
+constexpr int MK_UNROLL = 4;  // points in flight per thread
+
+// Leaf-depth words per k_mark workgroup and the coarser depths it derives.
+struct MarkCfg {
+  int words, up;
+  size_t lds;  // bytes: the chunk's words at every derived depth
+};
+MarkCfg mark_cfg(int64_t leaf_cells) {
+  MarkCfg m;
+  m.words = 1024;
+  while (m.words < 8192 && (int64_t)m.words * 32 * 256 < leaf_cells) m.words *= 2;
+  m.up = 0;
+  while (((int64_t)m.words * 32 >> (3 * (m.up + 1))) % 32 == 0 &&
+         ((int64_t)m.words * 32 >> (3 * (m.up + 1))) > 0)
+    ++m.up;
+  int64_t n = 0;
+  for (int j = 0; j <= m.up; ++j) n += (int64_t)m.words >> (3 * j);
+  m.lds = 4 * (size_t)n;
+  return m;
+}
 
 __global__ __launch_bounds__(MK_TB) void k_mark(const uint32_t* __restrict__ leafcell, Shapes S,
-                                                Levels L, uint32_t* __restrict__ bits) {
-  __shared__ uint32_t w[MK_WORDS + MK_WORDS / 8 + MK_WORDS / 64 + MK_WORDS / 512 + MK_WORDS / 4096];
+                                                Levels L, int chunk_words, int up,
+                                                uint32_t* __restrict__ bits) {
+  extern __shared__ uint32_t w[];
   const int d = L.depth;
+  const int64_t MK_CELLS = 32ll * chunk_words;
   // depths shallower than full_depth: all ones (grid-stride over their words)
   const int64_t nforced = L.wbase[L.full_depth];
   for (int64_t k = (int64_t)blockIdx.x * MK_TB + threadIdx.x; k < nforced;
@@ -181,22 +206,28 @@ __global__ __launch_bounds__(MK_TB) void k_mark(const uint32_t* __restrict__ lea
   __syncthreads();
   const int64_t per = (int64_t)1 << (3 * d);  // cells per shape
   const int b0 = (int)(c0 / per), b1 = (int)((c1 - 1) / per);
-  for (int i = S.offs[b0] + threadIdx.x; i < S.offs[b1 + 1]; i += MK_TB) {
-    const uint32_t c = leafcell[i];
-    if (c == 0xFFFFFFFFu || (int64_t)c < c0 || (int64_t)c >= c1) continue;
-    atomicOr(&w[(c - c0) >> 5], 1u << (c & 31));
+  const int i1 = S.offs[b1 + 1];
+  for (int i = S.offs[b0] + threadIdx.x; i < i1; i += MK_UNROLL * MK_TB) {
+    uint32_t c[MK_UNROLL];
+#pragma unroll
+    for (int u = 0; u < MK_UNROLL; ++u)
+      c[u] = i + u * MK_TB < i1 ? leafcell[i + u * MK_TB] : 0xFFFFFFFFu;
+#pragma unroll
+    for (int u = 0; u < MK_UNROLL; ++u)
+      if (c[u] != 0xFFFFFFFFu && (int64_t)c[u] >= c0 && (int64_t)c[u] < c1)
+        atomicOr(&w[(c[u] - c0) >> 5], 1u << (c[u] & 31));
   }
   __syncthreads();
   if (d >= L.full_depth) {
     uint32_t* dst = bits + L.wbase[d] + (c0 >> 5);
     for (int k = threadIdx.x; k < nwd; k += MK_TB) dst[k] = w[k];
   }
-  // coarser depths d-1 .. d-MK_UP: the chunk's cells there start on a word
-  // boundary (MK_CELLS / 8^MK_UP is a multiple of 32)
+  // coarser depths d-1 .. d-up: the chunk's cells there start on a word
+  // boundary (32 chunk_words / 8^up is a multiple of 32)
   uint32_t* fine = w;
   int nfine = nwd;
-  int off = MK_WORDS;
-  for (int j = 1; j <= MK_UP && d - j >= L.full_depth; ++j) {
+  int off = chunk_words;
+  for (int j = 1; j <= up && d - j >= L.full_depth; ++j) {
     const int l = d - j;
     uint32_t* coarse = w + off;
     const int64_t cc0 = c0 >> (3 * j), ncell = (c1 - c0) >> (3 * j);
@@ -215,12 +246,12 @@ __global__ __launch_bounds__(MK_TB) void k_mark(const uint32_t* __restrict__ lea
     __syncthreads();
     fine = coarse;
     nfine = ncw;
-    off += MK_WORDS >> (3 * j);
+    off += chunk_words >> (3 * j);
   }
 }
 
 // ---------------------------------------------------------------------------
-// 2. depths more than MK_UP above the leaves (and not forced): bit j of depth
+// 2. depths more than `up` above the leaves (and not forced): bit j of depth
 //    l = (byte j of depth l+1 != 0).
 
 __global__ __launch_bounds__(TB) void k_reduce(Levels L, int l, uint32_t* __restrict__ bits) {
@@ -240,9 +271,11 @@ __global__ __launch_bounds__(TB) void k_reduce(Levels L, int l, uint32_t* __rest
 
 // ---------------------------------------------------------------------------
 // 3. exclusive scan of the word popcounts of all depths: pre[w] = set bits
-//    before word w; pre[nw] = total.  Blocks of SCAN_W words.
+//    before word w; pre[nw] = total.  Blocks of SCAN_W words: k_scan_a sums
+//    each block, k_scan_c adds the sums of the blocks before its own, scans
+//    its words and, for every set bit, writes the cell in rank order (step 4).
 
-constexpr int SCAN_PER = 8;
+constexpr int SCAN_PER = 2;
 constexpr int SCAN_W = TB * SCAN_PER;
 
 __device__ __forceinline__ int32_t block_excl_scan(int32_t v, int32_t* total) {
@@ -279,74 +312,59 @@ __global__ __launch_bounds__(TB) void k_scan_a(const uint32_t* __restrict__ bits
   if (threadIdx.x == 0) bsum[blockIdx.x] = total;
 }
 
-// One block: exclusive scan of nb block sums in place; grand total at bsum[nb].
-__global__ __launch_bounds__(TB) void k_scan_b(int32_t* __restrict__ bsum, int nb) {
-  const int per = (nb + TB - 1) / TB;
-  const int b0 = threadIdx.x * per;
-  int32_t s = 0;
-  for (int k = 0; k < per; ++k)
-    if (b0 + k < nb) s += bsum[b0 + k];
-  int32_t total;
-  int32_t run = block_excl_scan(s, &total);
-  for (int k = 0; k < per; ++k)
-    if (b0 + k < nb) {
-      const int32_t v = bsum[b0 + k];
-      bsum[b0 + k] = run;
-      run += v;
-    }
-  if (threadIdx.x == 0) bsum[nb] = total;
-}
-
-__global__ __launch_bounds__(TB) void k_scan_c(const uint32_t* __restrict__ bits, int64_t nw,
-                                               const int32_t* __restrict__ bsum,
-                                               int32_t* __restrict__ pre, int nb) {
+// 4. (in k_scan_c) cell of every set bit, in rank order over all depths:
+//    ucell[pre + k].  The thread holding the first word of depth l reports
+//    pre there (info[2 + l], l <= depth + 1, the last one the total), so
+//    that M_l = info[3 + l] - info[2 + l]; workgroup 0 also reports the flags
+//    and largest |normal component| of the nq blocks of k_quant (info[0],
+//    info[1]).
+__global__ __launch_bounds__(TB) void k_scan_c(Levels L, const uint32_t* __restrict__ bits,
+                                               int64_t nw, const int32_t* __restrict__ bsum,
+                                               int32_t* __restrict__ pre,
+                                               uint32_t* __restrict__ ucell,
+                                               const uint2* __restrict__ bstat, int nq,
+                                               uint32_t* __restrict__ info) {
+  // set bits of the blocks before this one
+  int32_t sb = 0;
+  for (int k = threadIdx.x; k < (int)blockIdx.x; k += TB) sb += bsum[k];
+  int32_t before;
+  block_excl_scan(sb, &before);
   const int64_t w0 = (int64_t)blockIdx.x * SCAN_W + threadIdx.x * SCAN_PER;
+  uint32_t wd[SCAN_PER];
   int32_t c[SCAN_PER], s = 0;
 #pragma unroll
   for (int k = 0; k < SCAN_PER; ++k) {
-    c[k] = w0 + k < nw ? __popc(bits[w0 + k]) : 0;
+    wd[k] = w0 + k < nw ? bits[w0 + k] : 0u;
+    c[k] = __popc(wd[k]);
     s += c[k];
   }
   int32_t total;
-  int32_t run = bsum[blockIdx.x] + block_excl_scan(s, &total);
+  int32_t run = before + block_excl_scan(s, &total);
+  int l = level_of_word(L, w0 < nw ? w0 : nw - 1);
 #pragma unroll
-  for (int k = 0; k < SCAN_PER; ++k)
-    if (w0 + k < nw) {
-      pre[w0 + k] = run;
+  for (int k = 0; k < SCAN_PER; ++k) {
+    const int64_t w = w0 + k;
+    if (w < nw) {
+      while (l < L.depth && w >= L.wbase[l + 1]) ++l;
+      if (w == L.wbase[l]) info[2 + l] = (uint32_t)run;
+      pre[w] = run;
+      const uint32_t base = (uint32_t)((w - L.wbase[l]) * 32);
+      int32_t r = run;
+      uint32_t m = wd[k];
+      while (m) {
+        ucell[r++] = base + (uint32_t)(__ffs(m) - 1);
+        m &= m - 1u;
+      }
       run += c[k];
     }
-  if (blockIdx.x == 0 && threadIdx.x == 0) pre[nw] = bsum[nb];
-}
-
-// ---------------------------------------------------------------------------
-// 4. cell of every set bit, in rank order over all depths: ucell[pre + k].
-//    Workgroup 0 also reports the per-depth counts M_l (info[2 + l]) and the
-//    flags and largest |normal component| of the nq blocks of k_quant
-//    (info[0], info[1]).
-
-__global__ __launch_bounds__(TB) void k_compact(Levels L, const uint32_t* __restrict__ bits,
-                                                const int32_t* __restrict__ pre,
-                                                uint32_t* __restrict__ ucell,
-                                                const uint2* __restrict__ bstat, int nq,
-                                                uint32_t* __restrict__ info) {
-  const int64_t w = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (w < L.wbase[L.depth + 1]) {
-    uint32_t v = bits[w];
-    if (v) {
-      const int l = level_of_word(L, w);
-      const uint32_t base = (uint32_t)((w - L.wbase[l]) * 32);
-      int32_t r = pre[w];
-      while (v) {
-        const int b = __ffs(v) - 1;
-        ucell[r++] = base + (uint32_t)b;
-        v &= v - 1u;
-      }
-    }
+  }
+  if (w0 < nw && w0 + SCAN_PER >= nw) {  // the thread of the last word
+    pre[nw] = run;
+    info[3 + L.depth] = (uint32_t)run;
   }
   if (blockIdx.x != 0) return;
   __shared__ uint2 ws[TB / 64];
   const int t = threadIdx.x;
-  if (t <= L.depth) info[2 + t] = (uint32_t)(pre[L.wbase[t + 1]] - pre[L.wbase[t]]);
   uint32_t fl = 0u, mb = 0u;
   for (int k = t; k < nq; k += TB) {
     const uint2 v = bstat[k];
@@ -382,7 +400,8 @@ __global__ __launch_bounds__(TB) void k_compact(Levels L, const uint32_t* __rest
 //    additions make the result independent of their order.
 
 constexpr int LM_TB = 1024;
-constexpr int LM_LEAVES = 3072;  // 3072 * (3 * 8 + 4) bytes of LDS
+constexpr int LM_LEAVES = 512;  // 512 * (3 * 8 + 4) bytes of LDS
+constexpr int LM_UNROLL = 4;    // points in flight per thread
 
 __device__ __forceinline__ int fixed_shift(uint32_t maxbits, int P) {
   const double m = (double)__uint_as_float(maxbits) * (double)P;
@@ -419,16 +438,40 @@ __global__ __launch_bounds__(LM_TB) void k_leaf_mean(const float* __restrict__ n
   }
   __syncthreads();
   const int s = fixed_shift(info[1], P);
-  for (int i = S.offs[b] + threadIdx.x; i < S.offs[b + 1]; i += LM_TB) {
-    const uint32_t c = leafcell[i];
-    if (c < clo || (uint64_t)c >= chi) continue;
-    const int32_t j = rank_in(bits, pre, L, d, mb, c, &word) - lo;
+  const int i1 = S.offs[b + 1];
+  for (int i = S.offs[b] + threadIdx.x; i < i1; i += LM_UNROLL * LM_TB) {
+    uint32_t cu[LM_UNROLL];
 #pragma unroll
-    for (int a = 0; a < 3; ++a) {
-      const long long v = llrint(ldexp((double)nrm[3 * (int64_t)i + a], s));
-      atomicAdd(&sum[3 * j + a], (unsigned long long)v);
+    for (int u = 0; u < LM_UNROLL; ++u)
+      cu[u] = i + u * LM_TB < i1 ? leafcell[i + u * LM_TB] : 0xFFFFFFFFu;
+    // every load of the in-range points first, then their additions
+    bool in[LM_UNROLL];
+    uint32_t wv[LM_UNROLL];
+    int32_t pv[LM_UNROLL];
+    float nv[LM_UNROLL][3];
+#pragma unroll
+    for (int u = 0; u < LM_UNROLL; ++u) {
+      in[u] = cu[u] >= clo && (uint64_t)cu[u] < chi;
+      if (in[u]) {
+        const int64_t wi = L.wbase[d] + (int64_t)(cu[u] >> 5);
+        wv[u] = bits[wi];
+        pv[u] = pre[wi];
+        const int64_t pi = i + u * LM_TB;
+#pragma unroll
+        for (int a = 0; a < 3; ++a) nv[u][a] = nrm[3 * pi + a];
+      }
     }
-    atomicAdd(&cnt[j], 1);
+#pragma unroll
+    for (int u = 0; u < LM_UNROLL; ++u) {
+      if (!in[u]) continue;
+      const int32_t j = pv[u] - mb + __popc(wv[u] & ((1u << (cu[u] & 31)) - 1u)) - lo;
+#pragma unroll
+      for (int a = 0; a < 3; ++a) {
+        const long long v = llrint(ldexp((double)nv[u][a], s));
+        atomicAdd(&sum[3 * j + a], (unsigned long long)v);
+      }
+      atomicAdd(&cnt[j], 1);
+    }
   }
   __syncthreads();
   const double unit = ldexp(1.0, -s);
@@ -459,9 +502,10 @@ __global__ __launch_bounds__(TB) void k_emit(Levels L, Emit E, const uint32_t* _
                                              const int32_t* __restrict__ pre,
                                              const uint32_t* __restrict__ ucell,
                                              const float* __restrict__ leafmean) {
-  // 32 lanes per item: lane j < 8 emits child j, lane j < 27 neighbour j
-  const int64_t it = ((int64_t)blockIdx.x * TB + threadIdx.x) >> 5;
-  const int j = threadIdx.x & 31;
+  // 16 lanes per item: lane j < 8 emits child j and every lane neighbours j
+  // and j + 16 (< 27), their lookups in flight together
+  const int64_t it = ((int64_t)blockIdx.x * TB + threadIdx.x) >> 4;
+  const int j = threadIdx.x & 15;
   const int d = L.depth;
   if (it >= E.ibase[d + 1]) return;
   uint32_t word;
@@ -481,10 +525,45 @@ __global__ __launch_bounds__(TB) void k_emit(Levels L, Emit E, const uint32_t* _
   const int pl = l - 1;
   const uint64_t p = ucell[E.mbase[pl] + r];  // parent cell at depth l-1
 
-  if (j < 8) {  // child j: cell 8p + j of depth l, row 8r + j
-    const uint64_t cc = (p << 3) + (uint64_t)j;
-    const int32_t rk = rank_in(bits, pre, L, l, E.mbase[l], cc, &word);
-    const bool on = (word >> (cc & 31)) & 1u;
+  // every rank lookup of the lane first (clamped to a valid word when
+  // absent), then the stores
+  const uint32_t pkb = 3u * (uint32_t)pl;
+  const uint32_t pshape = (uint32_t)(p >> pkb);
+  const uint32_t pkey = (uint32_t)p & (uint32_t)((1ull << pkb) - 1ull);
+  const int side = 1 << pl;
+  const int px = (int)squeeze3(pkey >> 2), py = (int)squeeze3(pkey >> 1), pz = (int)squeeze3(pkey);
+  uint64_t q[2];
+  bool in[2];
+  uint32_t qw[2];
+  int32_t qp[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {  // neighbour jj = j + 16 h of the parent at depth l-1
+    const int jj = j + 16 * h;
+    const int nx = px + jj / 9 - 1, ny = py + (jj / 3) % 3 - 1, nz = pz + jj % 3 - 1;
+    in[h] = jj < 27 && nx >= 0 && nx < side && ny >= 0 && ny < side && nz >= 0 && nz < side;
+    q[h] = in[h] ? ((uint64_t)pshape << pkb) |
+                       shuffle_key((uint32_t)nx, (uint32_t)ny, (uint32_t)nz)
+                 : p;
+    const int64_t w = L.wbase[pl] + (int64_t)(q[h] >> 5);
+    qw[h] = bits[w];
+    qp[h] = pre[w];
+  }
+  const uint64_t cc = (p << 3) + (uint64_t)(j & 7);  // child j: cell 8p + j of depth l
+  const int64_t cwi = L.wbase[l] + (int64_t)(cc >> 5);
+  const uint32_t cw = bits[cwi];
+  const int32_t cp = pre[cwi];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int jj = j + 16 * h;
+    if (jj < 27) {  // first-child row of the neighbour, or -1
+      const bool on = in[h] && ((qw[h] >> (q[h] & 31)) & 1u);
+      const int32_t rq = qp[h] - E.mbase[pl] + __popc(qw[h] & ((1u << (q[h] & 31)) - 1u));
+      E.nbr[l][27 * (int64_t)r + jj] = on ? 8 * rq : -1;
+    }
+  }
+  if (j < 8) {  // child j, row 8r + j
+    const int32_t rk = cp - E.mbase[l] + __popc(cw & ((1u << (cc & 31)) - 1u));
+    const bool on = (cw >> (cc & 31)) & 1u;
     const uint32_t kb = 3u * (uint32_t)l;
     const int64_t row = 8 * (int64_t)r + j;
     E.keys[l][row] = ((uint32_t)(cc >> kb) << 24) | ((uint32_t)cc & (uint32_t)((1ull << kb) - 1ull));
@@ -495,23 +574,6 @@ __global__ __launch_bounds__(TB) void k_emit(Levels L, Emit E, const uint32_t* _
 #pragma unroll
       for (int a = 0; a < 3; ++a) o[a] = on ? leafmean[3 * (int64_t)rk + a] : 0.f;
     }
-  }
-  if (j < 27) {  // neighbour j of the parent at depth l-1: first-child row or -1
-    const uint32_t pkb = 3u * (uint32_t)pl;
-    const uint32_t pshape = (uint32_t)(p >> pkb);
-    const uint32_t pkey = (uint32_t)p & (uint32_t)((1ull << pkb) - 1ull);
-    const int side = 1 << pl;
-    const int nx = (int)squeeze3(pkey >> 2) + j / 9 - 1;
-    const int ny = (int)squeeze3(pkey >> 1) + (j / 3) % 3 - 1;
-    const int nz = (int)squeeze3(pkey) + j % 3 - 1;
-    int32_t v = -1;
-    if (nx >= 0 && nx < side && ny >= 0 && ny < side && nz >= 0 && nz < side) {
-      const uint64_t q = ((uint64_t)pshape << pkb) |
-                         shuffle_key((uint32_t)nx, (uint32_t)ny, (uint32_t)nz);
-      const int32_t rq = rank_in(bits, pre, L, pl, E.mbase[pl], q, &word);
-      v = ((word >> (q & 31)) & 1u) ? 8 * rq : -1;
-    }
-    E.nbr[l][27 * (int64_t)r + j] = v;
   }
 }
 
@@ -567,13 +629,82 @@ void fill_u32(void* p, uint32_t v, int64_t n, hipStream_t s) {
 
 }  // namespace oc
 
-extern "C" oc_status oc_build(const float* points, const float* normals,
-                              const int32_t* shape_offsets, int32_t batch, int32_t depth,
-                              int32_t full_depth, const oc_allocator* alloc, hipStream_t stream,
-                              oc_octree** out) {
+namespace {
+
+// Pinned host word block and event for the counts of one build in flight
+// (reused across builds; one pool per process, each slot tied to a device).
+struct CountSlot {
+  uint32_t* host = nullptr;
+  hipEvent_t ready = nullptr;
+  int device = -1;
+};
+
+std::mutex g_slot_mu;
+std::vector<CountSlot> g_slots;
+
+bool take_slot(CountSlot* out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  {
+    std::lock_guard<std::mutex> lk(g_slot_mu);
+    for (size_t k = 0; k < g_slots.size(); ++k)
+      if (g_slots[k].device == dev) {
+        *out = g_slots[k];
+        g_slots.erase(g_slots.begin() + (long)k);
+        return true;
+      }
+  }
+  CountSlot c;
+  c.device = dev;
+  if (hipHostMalloc((void**)&c.host, 16 * sizeof(uint32_t), hipHostMallocDefault) != hipSuccess)
+    return false;
+  if (hipEventCreateWithFlags(&c.ready, hipEventDisableTiming) != hipSuccess) {
+    (void)hipHostFree(c.host);
+    return false;
+  }
+  *out = c;
+  return true;
+}
+
+void give_slot(const CountSlot& c) {
+  std::lock_guard<std::mutex> lk(g_slot_mu);
+  g_slots.push_back(c);
+}
+
+}  // namespace
+
+// State of a build between oc_build_async and oc_build_finish.
+struct oc_build_job {
+  Levels L{};
+  Shapes S{};
+  std::vector<int32_t> offs;
+  int B = 0, d = 0, fd = 0, nq = 0;
+  int64_t P = 0;
+  const float* normals = nullptr;
+  oc_allocator A{};
+  hipStream_t stream = nullptr;  // of the first half and of the scratch
+  char* scratch = nullptr;
+  Scratch s{};
+  CountSlot slot;
+};
+
+namespace {
+
+void drop_job(oc_build_job* j, hipStream_t s) {
+  if (j->scratch) oc::dev_free(j->A, j->scratch, s);
+  give_slot(j->slot);
+  delete j;
+}
+
+}  // namespace
+
+extern "C" oc_status oc_build_async(const float* points, const float* normals,
+                                    const int32_t* shape_offsets, int32_t batch, int32_t depth,
+                                    int32_t full_depth, const oc_allocator* alloc,
+                                    hipStream_t stream, oc_build_job** job) {
   using oc::fail;
-  if (!out) return fail(OC_ERR_ARG, "oc_build: out is NULL");
-  *out = nullptr;
+  if (!job) return fail(OC_ERR_ARG, "oc_build_async: job is NULL");
+  *job = nullptr;
   if (!shape_offsets) return fail(OC_ERR_ARG, "oc_build: shape_offsets is NULL");
   if (batch < 1 || batch > 256) return fail(OC_ERR_ARG, "oc_build: batch %d not in 1..256", batch);
   if (depth < 1 || depth > OC_MAX_DEPTH)
@@ -591,10 +722,19 @@ extern "C" oc_status oc_build(const float* points, const float* normals,
   if (((int64_t)batch << (3 * full_depth)) > (int64_t(1) << 28))
     return fail(OC_ERR_UNSUPPORTED, "oc_build: batch * 8^full_depth too large");
 
-  const oc_allocator A = alloc ? *alloc : oc_allocator{nullptr, nullptr, nullptr};
+  oc_build_job* j = new oc_build_job;
+  if (!take_slot(&j->slot)) {
+    delete j;
+    return fail(OC_ERR_DEVICE, "oc_build: pinned count buffer or event unavailable");
+  }
+  j->A = alloc ? *alloc : oc_allocator{nullptr, nullptr, nullptr};
+  j->B = batch, j->d = depth, j->fd = full_depth, j->P = P;
+  j->normals = normals;
+  j->stream = stream;
+  j->offs.assign(shape_offsets, shape_offsets + batch + 1);
   const int B = batch, d = depth, fd = full_depth;
 
-  Levels L{};
+  Levels& L = j->L;
   L.depth = d, L.full_depth = fd, L.batch = B;
   int64_t ucap = 0;  // bound on the set bits of all depths
   L.wbase[0] = 0;
@@ -607,73 +747,87 @@ extern "C" oc_status oc_build(const float* points, const float* normals,
   const int nb = (int)oc::cdiv(nw, SCAN_W);
 
   Arena meas;
-  Scratch s{};
+  Scratch& s = j->s;
   carve(meas, B, P, nw, nb, ucap, s);
   Arena ar;
-  ar.base = (char*)oc::dev_alloc(A, meas.used, stream);
-  if (!ar.base) return fail(OC_ERR_NOMEM, "oc_build: scratch allocation of %zu bytes failed", meas.used);
+  ar.base = (char*)oc::dev_alloc(j->A, meas.used, stream);
+  if (!ar.base) {
+    drop_job(j, stream);
+    return fail(OC_ERR_NOMEM, "oc_build: scratch allocation of %zu bytes failed", meas.used);
+  }
+  j->scratch = ar.base;
   carve(ar, B, P, nw, nb, ucap, s);
-  auto release = [&](void* p) { oc::dev_free(A, p, stream); };
 
-  Shapes S;
+  Shapes& S = j->S;
   for (int b = 0; b <= B; ++b) S.offs[b] = shape_offsets[b];
   const int nq = (int)oc::cdiv(P, TB);
+  j->nq = nq;
   if (P > 0)
     hipLaunchKernelGGL(k_quant, dim3(nq), dim3(TB), 0, stream, points, normals, S, B, (int)P, d,
                        s.leafcell, s.bstat);
-  hipLaunchKernelGGL(k_mark, dim3((unsigned)oc::cdiv(L.cells[d], MK_CELLS)), dim3(MK_TB), 0,
-                     stream, (const uint32_t*)s.leafcell, S, L, s.bits);
-  for (int l = d - MK_UP - 1; l >= fd; --l)
+  const MarkCfg mc = mark_cfg(L.cells[d]);
+  hipLaunchKernelGGL(k_mark, dim3((unsigned)oc::cdiv(L.cells[d], 32ll * mc.words)), dim3(MK_TB),
+                     mc.lds, stream, (const uint32_t*)s.leafcell, S, L, mc.words, mc.up, s.bits);
+  for (int l = d - mc.up - 1; l >= fd; --l)
     hipLaunchKernelGGL(k_reduce, dim3(blocks_for(L.wbase[l + 1] - L.wbase[l])), dim3(TB), 0,
                        stream, L, l, s.bits);
   hipLaunchKernelGGL(k_scan_a, dim3(nb), dim3(TB), 0, stream, (const uint32_t*)s.bits, nw, s.bsum);
-  hipLaunchKernelGGL(k_scan_b, dim3(1), dim3(TB), 0, stream, s.bsum, nb);
-  hipLaunchKernelGGL(k_scan_c, dim3(nb), dim3(TB), 0, stream, (const uint32_t*)s.bits, nw,
-                     (const int32_t*)s.bsum, s.pre, nb);
-  hipLaunchKernelGGL(k_compact, dim3(blocks_for(nw)), dim3(TB), 0, stream, L,
-                     (const uint32_t*)s.bits, (const int32_t*)s.pre, s.ucell,
-                     (const uint2*)s.bstat, nq, s.info);
-  if (P > 0) {
-    int64_t kmax = 1;  // leaf chunks of the largest shape
-    for (int b = 0; b < B; ++b)
-      kmax = std::max<int64_t>(
-          kmax, oc::cdiv(std::min<int64_t>(shape_offsets[b + 1] - shape_offsets[b], L.cells[d] / B),
-                         LM_LEAVES));
-    hipLaunchKernelGGL(k_leaf_mean, dim3((unsigned)B, (unsigned)kmax), dim3(LM_TB), 0, stream,
-                       normals, (const uint32_t*)s.leafcell, S, (int)P, L,
-                       (const uint32_t*)s.bits, (const int32_t*)s.pre, (const uint32_t*)s.ucell,
-                       (const uint32_t*)s.info, s.leafmean);
-  }
-
-  uint32_t info[16] = {};
+  hipLaunchKernelGGL(k_scan_c, dim3(nb), dim3(TB), 0, stream, L, (const uint32_t*)s.bits, nw,
+                     (const int32_t*)s.bsum, s.pre, s.ucell, (const uint2*)s.bstat, nq, s.info);
   hipError_t he = hipGetLastError();
   if (he == hipSuccess)
-    he = hipMemcpyAsync(info, s.info, sizeof(info), hipMemcpyDeviceToHost, stream);
-  if (he == hipSuccess) he = hipStreamSynchronize(stream);
+    he = hipMemcpyAsync(j->slot.host, s.info, 16 * sizeof(uint32_t), hipMemcpyDeviceToHost,
+                        stream);
+  if (he == hipSuccess) he = hipEventRecord(j->slot.ready, stream);
   if (he != hipSuccess) {
-    release(ar.base);
+    (void)hipStreamSynchronize(stream);
+    drop_job(j, stream);
     return fail(OC_ERR_DEVICE, "oc_build: %s", hipGetErrorString(he));
   }
+  *job = j;
+  return OC_OK;
+}
+
+extern "C" oc_status oc_build_finish(oc_build_job* j, hipStream_t stream, oc_octree** out) {
+  using oc::fail;
+  if (out) *out = nullptr;
+  if (!j) return fail(OC_ERR_ARG, "oc_build_finish: job is NULL");
+  if (!out) {
+    oc_build_cancel(j);
+    return fail(OC_ERR_ARG, "oc_build_finish: out is NULL");
+  }
+  const int B = j->B, d = j->d;
+  const Levels& L = j->L;
+  const Scratch& s = j->s;
+  // the one wait: the first half's counts
+  hipError_t he = hipEventSynchronize(j->slot.ready);
+  if (he == hipSuccess && stream != j->stream) he = hipStreamWaitEvent(stream, j->slot.ready, 0);
+  if (he != hipSuccess) {
+    drop_job(j, j->stream);
+    return fail(OC_ERR_DEVICE, "oc_build: %s", hipGetErrorString(he));
+  }
+  uint32_t info[16];
+  std::memcpy(info, j->slot.host, sizeof(info));
   if (info[0] & 1u) {
-    release(ar.base);
+    drop_job(j, stream);
     return fail(OC_ERR_RANGE, "oc_build: a point is outside [0,1]^3 or NaN");
   }
   if (info[0] & 2u) {
-    release(ar.base);
+    drop_job(j, stream);
     return fail(OC_ERR_RANGE, "oc_build: a normal is not finite");
   }
 
   oc_octree* t = new oc_octree;
   t->depth = d;
-  t->full_depth = fd;
+  t->full_depth = j->fd;
   t->batch = B;
-  t->alloc = A;
+  t->alloc = j->A;
   t->stream = stream;
   for (int l = 0; l <= d; ++l) {
-    t->M[l] = info[2 + l];
+    t->M[l] = info[3 + l] - info[2 + l];
     t->N[l] = l == 0 ? B : 8 * t->M[l - 1];
     if (t->N[l] > INT32_MAX / 2) {
-      release(ar.base);
+      drop_job(j, stream);
       delete t;
       return fail(OC_ERR_UNSUPPORTED, "oc_build: depth %d has too many octants", l);
     }
@@ -684,9 +838,9 @@ extern "C" oc_status oc_build(const float* points, const float* normals,
     if (l > 0) bytes += oc::align256(4 * 27 * (size_t)t->M[l - 1]);
   }
   bytes += oc::align256(12 * (size_t)t->N[d]);
-  char* blk = (char*)oc::dev_alloc(A, bytes, stream);
+  char* blk = (char*)oc::dev_alloc(j->A, bytes, stream);
   if (!blk) {
-    release(ar.base);
+    drop_job(j, stream);
     delete t;
     return fail(OC_ERR_NOMEM, "oc_build: octree allocation of %zu bytes failed", bytes);
   }
@@ -705,6 +859,18 @@ extern "C" oc_status oc_build(const float* points, const float* normals,
   }
   t->signal = (float*)take(12 * (size_t)t->N[d]);
 
+  // leaf signal (needs only device data of the first half), then emission
+  if (j->P > 0) {
+    int64_t kmax = 1;  // leaf chunks of the largest shape
+    for (int b = 0; b < B; ++b)
+      kmax = std::max<int64_t>(
+          kmax, oc::cdiv(std::min<int64_t>(j->offs[b + 1] - j->offs[b], L.cells[d] / B),
+                         LM_LEAVES));
+    hipLaunchKernelGGL(k_leaf_mean, dim3((unsigned)B, (unsigned)kmax), dim3(LM_TB), 0, stream,
+                       j->normals, (const uint32_t*)s.leafcell, j->S, (int)j->P, L,
+                       (const uint32_t*)s.bits, (const int32_t*)s.pre, (const uint32_t*)s.ucell,
+                       (const uint32_t*)s.info, s.leafmean);
+  }
   Emit E{};
   int32_t m = 0;
   for (int l = 0; l <= d + 1; ++l) {
@@ -721,15 +887,34 @@ extern "C" oc_status oc_build(const float* points, const float* normals,
     E.nbr[l] = t->nbr[l];
   }
   E.signal = t->signal;
-  hipLaunchKernelGGL(k_emit, dim3(blocks_for(32 * E.ibase[d + 1])), dim3(TB), 0, stream, L, E,
+  hipLaunchKernelGGL(k_emit, dim3(blocks_for(16 * E.ibase[d + 1])), dim3(TB), 0, stream, L, E,
                      (const uint32_t*)s.bits, (const int32_t*)s.pre, (const uint32_t*)s.ucell,
                      (const float*)s.leafmean);
   he = hipGetLastError();
-  release(ar.base);
+  drop_job(j, stream);  // the scratch is released in stream order after the emission
   if (he != hipSuccess) {
     oc_octree_free(t);
     return fail(OC_ERR_DEVICE, "oc_build: launch failed: %s", hipGetErrorString(he));
   }
   *out = t;
   return OC_OK;
+}
+
+extern "C" void oc_build_cancel(oc_build_job* j) {
+  if (!j) return;
+  (void)hipEventSynchronize(j->slot.ready);
+  drop_job(j, j->stream);
+}
+
+extern "C" oc_status oc_build(const float* points, const float* normals,
+                              const int32_t* shape_offsets, int32_t batch, int32_t depth,
+                              int32_t full_depth, const oc_allocator* alloc, hipStream_t stream,
+                              oc_octree** out) {
+  if (!out) return oc::fail(OC_ERR_ARG, "oc_build: out is NULL");
+  *out = nullptr;
+  oc_build_job* j = nullptr;
+  const oc_status st =
+      oc_build_async(points, normals, shape_offsets, batch, depth, full_depth, alloc, stream, &j);
+  if (st != OC_OK) return st;
+  return oc_build_finish(j, stream, out);
 }

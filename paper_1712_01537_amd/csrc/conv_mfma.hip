@@ -406,9 +406,11 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
 // keeps the chunk's weights of its 16 output channels in registers for the
 // whole launch (27 taps x 4 channels per lane), so the only LDS traffic is
 // the group tiles: one 16-byte read per lane feeds four MFMAs.
-// Workgroups (two per CU) are persistent over a contiguous range of tiles of
-// GPB sibling groups (GPB/2 blocks of 16 rows).  Wave w takes output channels
-// 16 (w % WN).. and row blocks RB (w / WN) + r, r < RB.  The
+// Workgroups (two or three per CU) are persistent over a contiguous range of
+// sibling groups, taken in tiles of GPB groups (GPB/2 blocks of 16 rows).
+// Wave w takes output channels 16 (w % WN).. and row blocks RB (w / WN) + r,
+// r < RB; in the range's last tile, which may be partial, the live row
+// blocks are dealt round the WM waves of a column instead.  The
 // (K+1)^3 x 16-channel group tiles are streamed with direct global->LDS
 // loads into two static buffers: tile t+1 lands while tile t is multiplied,
 // with one barrier per tile.  Absent neighbours and channels past kk read a
@@ -439,11 +441,10 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const int li = lane & 15, q = lane >> 4;
   const int wn = wave % WN, wm = wave / WN;
   const int n0 = blockIdx.y * BN + 16 * wn, c0 = 16 * blockIdx.z;
-  const int64_t ntile = (ngroups + GPB - 1) / GPB;
   const int nx = gridDim.x, bx = blockIdx.x;
   const int lb = nx >= 8 ? (bx % 8) * (nx / 8) + bx / 8 : bx;  // XCD-contiguous ranges
-  const int64_t tile0 = ntile * lb / nx;
-  const int T = (int)(ntile * (lb + 1) / nx - tile0);
+  const int64_t g0 = ngroups * lb / nx, g1 = ngroups * (lb + 1) / nx;  // groups [g0, g1)
+  const int T = (int)((g1 - g0 + GPB - 1) / GPB);
   if (T <= 0) return;  // uniform over the workgroup
 
   // loads: wave w fills x-slab w of every group; lane -> chunk (slot 4y + z,
@@ -460,8 +461,8 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
     ok = 0;
 #pragma unroll
     for (int i = 0; i < GPB; ++i) {
-      const int64_t g = (tile0 + t) * GPB + i;
-      const bool live = t < T && g < ngroups;
+      const int64_t g = g0 + (int64_t)t * GPB + i;
+      const bool live = t < T && g < g1;
       v[i] = nbr[live ? 27 * g + l_slot : 0];
       ok |= (uint32_t)live << i;
     }
@@ -497,7 +498,26 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
   v4f acc0[RB], acc1[RB];
 #pragma unroll
   for (int r = 0; r < RB; ++r) acc0[r] = acc1[r] = v4f{0.f, 0.f, 0.f, 0.f};
-  v4f wr[K3];  // this lane's weights, loaded after the first neighbour entries
+  v4f wr[K3];  // this lane's weights: wr[k][s] = W'[k][c0 + 4q + s][n0 + li]
+  constexpr int KLO = 13;
+  auto load_w = [&](bool hi) {  // taps k < KLO, or k >= KLO
+    const int n = n0 + li, c = c0 + 4 * q;
+    const bool ok = n < nn && c < kk;
+#pragma unroll
+    for (int k = 0; k < K3; ++k) {
+      if ((k >= KLO) != hi) continue;
+      v4f v = {0.f, 0.f, 0.f, 0.f};
+      if (ok) {
+        if constexpr (FLIP) {
+          v = *reinterpret_cast<const v4f*>(w + ((int64_t)(K3 - 1 - k) * nn + n) * kk + c);
+        } else {
+#pragma unroll
+          for (int s = 0; s < 4; ++s) v[s] = w[((int64_t)k * kk + c + s) * nn + n];
+        }
+      }
+      wr[k] = v;
+    }
+  };
 
   // the rows of tap k+1 are read before the MFMAs of tap k
   auto compute = [&](const v4f* buf, v4f (&acc)[RB]) {
@@ -520,31 +540,51 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
       __builtin_amdgcn_sched_barrier(0);
     }
   };
+  // one row block rb of the tile (the partial last tile), into acc
+  auto compute1 = [&](const v4f* buf, int rb, v4f& acc) {
+    const v4f* bb = buf + 2 * (rb - wm * RB) * GSTR;
+    v4f b[2];
+    b[0] = bb[aoff[0]];
+#pragma unroll
+    for (int k = 0; k < K3; ++k) {
+      const int cu = k & 1, nx2 = cu ^ 1;
+      if (k + 1 < K3) b[nx2] = bb[aoff[(k + 1) % 9] + ((k + 1) / 9) * XSTR];
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) acc = mfma4(wr[k][s], b[cu][s], acc);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
   const int64_t nrows = 8 * ngroups;
   const bool split = gridDim.z > 1;
   float* dst = split ? part + (int64_t)blockIdx.z * nrows * nn : out;
   // accumulator j of lane l: output channel 4(l/16) + j, row l % 16; stored
   // after store_order: lane l writes row l/4, channels 4(l%4)..
-  auto epilogue = [&](int t, v4f (&acc)[RB]) {
+  const int64_t rowe = 8 * g1;  // rows past the range are not stored
+  auto store_rb = [&](int t, int rb, const v4f& acc) {
     const int n = n0 + 4 * (lane & 3);
+    const int64_t row = 8 * (g0 + (int64_t)t * GPB) + 16 * rb + (lane >> 2);
+    const v4f sv = store_order(acc, lane);
+    if (n < nn && row < rowe) {
+      v4f v = sv;
+      if (!split && relu) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = fmaxf(v[j], 0.f);
+      }
+      *reinterpret_cast<v4f*>(dst + row * nn + n) = v;
+    }
+  };
+  auto epilogue = [&](int t, v4f (&acc)[RB]) {
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
-      const int64_t row = 8 * (tile0 + t) * GPB + 16 * (wm * RB + r) + (lane >> 2);
-      const v4f sv = store_order(acc[r], lane);
-      if (n < nn && row < nrows) {
-        v4f v = sv;
-        if (!split && relu) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] = fmaxf(v[j], 0.f);
-        }
-        *reinterpret_cast<v4f*>(dst + row * nn + n) = v;
-      }
+      store_rb(t, wm * RB + r, acc[r]);
       acc[r] = v4f{0.f, 0.f, 0.f, 0.f};
     }
   };
   // tile t: wait for its loads everywhere (and for tile t-1's reads), write
   // tile t-1, start tile t+1's loads, multiply tile t
-  auto step = [&](int t, const v4f* cur, v4f* nxt, v4f (&accc)[RB], v4f (&accp)[RB]) {
+  auto step = [&](int t, const v4f* cur, v4f* nxt, v4f (&accc)[RB], v4f (&accp)[RB],
+                  bool first) {
     vm_wait0();  // this wave's loads into cur have landed
     __syncthreads();
     if (t > 0) epilogue(t - 1, accp);
@@ -555,39 +595,43 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
       load_nb(t + 2, nbn, okn);
       dma(nxt);
     }
+    if (first) load_w(true);  // the later taps' weights land during tile 0
     __builtin_amdgcn_sched_barrier(0);
     compute(cur, accc);
   };
 
+  // the first tile's neighbour entries, the first KLO taps' weights and the
+  // first tile's rows are in flight together; the other taps' weights are
+  // loaded at the start of tile 0 and waited for tap by tap
   load_nb(0, nbc, okc);
-  load_nb(1, nbn, okn);
-  // this lane's weights: wr[k][s] = W'[k][c0 + 4q + s][n0 + li]
-  {
-    const int n = n0 + li, c = c0 + 4 * q;
-#pragma unroll
-    for (int k = 0; k < K3; ++k) {
-      v4f v = {0.f, 0.f, 0.f, 0.f};
-      if (n < nn && c < kk) {
-        if constexpr (FLIP) {
-          v = *reinterpret_cast<const v4f*>(w + ((int64_t)(K3 - 1 - k) * nn + n) * kk + c);
-        } else {
-#pragma unroll
-          for (int s = 0; s < 4; ++s) v[s] = w[((int64_t)k * kk + c + s) * nn + n];
-        }
-      }
-      wr[k] = v;
-    }
-  }
-
+  load_w(false);
   dma(X0);
-  for (int t = 0; t < T; t += 2) {
-    step(t, X0, X1, acc0, acc1);
-    if (t + 1 < T) step(t + 1, X1, X0, acc1, acc0);
+  load_nb(1, nbn, okn);
+
+  // tiles 0 .. T-2 (tile 0 apart, with the rest of the weights), then the
+  // last one (in X0 when T-1 is even)
+  if (T > 1) step(0, X0, X1, acc0, acc1, true);
+  for (int t = 1; t + 1 < T; t += 2) {
+    step(t, X1, X0, acc1, acc0, false);
+    if (t + 2 < T) step(t + 1, X0, X1, acc0, acc1, false);
   }
-  if ((T - 1) % 2 == 0)
-    epilogue(T - 1, acc0);
-  else
-    epilogue(T - 1, acc1);
+  const bool last0 = (T - 1) % 2 == 0;
+  vm_wait0();
+  __syncthreads();
+  if (T > 1) {
+    if (last0)
+      epilogue(T - 2, acc1);
+    else
+      epilogue(T - 2, acc0);
+  }
+  if (T == 1) load_w(true);
+  // live row blocks of the last tile, rb = wm + WM i
+  const int rbl = (int)((g1 - g0 - (int64_t)(T - 1) * GPB + 1) / 2);
+  for (int rb = wm; rb < rbl; rb += WM) {
+    v4f a = v4f{0.f, 0.f, 0.f, 0.f};
+    compute1(last0 ? X0 : X1, rb, a);
+    store_rb(T - 1, rb, a);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1307,17 +1351,22 @@ TileCfg pick_tile(int K, int64_t G, int kk, int nn) {
     c.NR = nn <= 16 ? 1 : nn <= 32 ? 2 : 4;  // column blocks per workgroup (WN)
     c.cps = 1;
     c.splits = (int)oc::cdiv(kk, 16);
-    // tile size: the best balance of tiles over two workgroups per CU, with
-    // a small preference for larger tiles (fewer barriers and loads per MFMA)
+    // tile size: the least time for the longest range of groups (two
+    // workgroups per CU), counting a wave's row blocks plus a fixed cost per
+    // tile (barrier, loads, stores) of about 3/4 of a row block
     const int64_t slots = 2 * (int64_t)oc::cu_count();
     const int64_t gyz = oc::cdiv(nn, 16 * c.NR) * c.splits;
-    double best = -1.0;
+    const int64_t ng = oc::cdiv(G, std::max<int64_t>(1, slots / gyz));
+    const int wm = WAVES / c.NR;
+    double best = 1e30;
     c.gpb = 8;
     for (int gpb = 8; gpb >= 2; gpb /= 2) {
-      if (gpb / 2 < WAVES / c.NR) break;  // a row block for every wave
-      const double units = (double)oc::cdiv(G, gpb) * gyz / slots;
-      const double eff = units / std::ceil(units) * (gpb == 8 ? 1.0 : gpb == 4 ? 0.97 : 0.92);
-      if (eff > best + 1e-9) best = eff, c.gpb = gpb;
+      if (gpb / 2 < wm) break;  // a row block for every wave
+      const int rb = gpb / 2 / wm;
+      const int64_t full = ng / gpb, tail = ng - full * gpb;
+      const double cost = full * (rb + 0.75) +
+                          (tail > 0 ? (double)oc::cdiv(oc::cdiv(tail, 2), wm) + 0.75 : 0.0);
+      if (cost < best - 1e-9) best = cost, c.gpb = gpb;
     }
     return c;
   }
@@ -1374,10 +1423,9 @@ void launch_tile2(const oc_octree* t, int l, const TileCfg& c, const float* x, i
     return n;
   }();
   const int64_t G = t->M[l - 1];
-  const int64_t ntile = oc::cdiv(G, GPB);
   const int64_t gy = oc::cdiv(nn, 16 * NR), gyz = gy * c.splits;
-  // one resident workgroup per slot, each over a contiguous range of tiles
-  int64_t px = std::min<int64_t>(ntile, std::max<int64_t>(1, (int64_t)oc::cu_count() * occ / gyz));
+  // one resident workgroup per slot, each over a contiguous range of groups
+  int64_t px = std::min<int64_t>(G, std::max<int64_t>(1, (int64_t)oc::cu_count() * occ / gyz));
   if (px >= 8) px -= px % 8;
   dim3 grid((unsigned)px, (unsigned)gy, (unsigned)c.splits);
   oc::launch_main(kernel, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, kk, w, nn, out,

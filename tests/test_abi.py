@@ -41,6 +41,13 @@ def test_argument_errors_without_device():
     assert L.oc_build(None, None, bad, 2, 3, 2, None, None, C.byref(out)) == 1    # decreasing
     assert b"decrease" in L.oc_last_error()
     assert L.oc_build(None, None, (C.c_int32 * 2)(0, 4), 1, 3, 2, None, None, C.byref(out)) == 1
+    job = C.c_void_p(1)
+    assert L.oc_build_async(None, None, offs, 0, 3, 2, None, None, C.byref(job)) == 1
+    assert not job.value  # no job on failure
+    assert L.oc_build_async(None, None, bad, 2, 3, 2, None, None, C.byref(job)) == 1
+    assert L.oc_build_async(None, None, offs, 2, 3, 2, None, None, None) == 1
+    assert L.oc_build_finish(None, None, C.byref(out)) == 1
+    L.oc_build_cancel(None)
     assert L.oc_conv_fwd(None, 1, 3, 1, 0, None, 3, None, 4, None, None, 0, 0, None) == 1
     assert L.oc_pool_fwd(None, 1, None, 3, None, None, None) == 1
     assert L.oc_octree_signal(None) is None

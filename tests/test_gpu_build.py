@@ -116,3 +116,54 @@ def test_build_workloads_full_size(name):
     _compare_tree(ref, tree, nb_depths=[w.depth])
     print(f"[build] {name}: N = {[tree.num(l) for l in range(w.depth + 1)]}, "
           f"M = {[tree.nonempty(l) for l in range(w.depth + 1)]}", flush=True)
+
+
+def test_build_async_finish_two_streams():
+    """oc_build_async on one stream, oc_build_finish on another: the same
+    octree as the oracle and as oc_build, also with several jobs in flight
+    finished out of order (each with its own count buffer)."""
+    oc = _gpu()
+    cases = [synth.random_cloud(5, 5, 2000, "union"), synth.random_cloud(7, 17, 300, "union"),
+             synth.make_points("net_d5", batch=4)]
+    depths = [(6, 2), (5, 2), (5, 2)]
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    jobs = []
+    with torch.cuda.stream(sa):
+        for (pts, nrm, offs), (d, fd) in zip(cases, depths):
+            print(f"[build async] P={len(pts)} B={len(offs) - 1} depth={d}", flush=True)
+            p, n = torch.as_tensor(pts).cuda(), torch.as_tensor(nrm).cuda()
+            jobs.append(oc.oc_build_async(p, n, offs, d, fd))
+            # unrelated work queued behind the job on its stream
+            torch.mm(torch.ones(512, 512, device="cuda"), torch.ones(512, 512, device="cuda"))
+    trees = [None] * len(jobs)
+    for k in reversed(range(len(jobs))):
+        trees[k] = jobs[k].finish(sb)
+    torch.cuda.synchronize()
+    for (pts, nrm, offs), (d, fd), tree in zip(cases, depths, trees):
+        ref = oracle.Octree(pts, nrm, offs, d, fd)
+        _compare_tree(ref, tree)
+        whole = oc.oc_build(torch.as_tensor(pts).cuda(), torch.as_tensor(nrm).cuda(), offs, d, fd)
+        torch.cuda.synchronize()
+        for l in range(d + 1):
+            assert torch.equal(whole.keys(l), tree.keys(l)) and torch.equal(whole.labels(l), tree.labels(l))
+            if l:
+                assert torch.equal(whole.nbr(l), tree.nbr(l))
+        assert torch.equal(whole.signal().view(torch.int32), tree.signal().view(torch.int32))
+
+
+def test_build_async_errors_and_cancel():
+    oc = _gpu()
+    bad = torch.tensor([[0.5, 1.5, 0.2]], dtype=torch.float32, device="cuda")
+    job = oc.oc_build_async(bad, bad, [0, 1], 3, 2)  # the range check happens on the device
+    with pytest.raises(oc.OcError) as e:
+        job.finish()
+    assert e.value.code == 2
+    with pytest.raises(oc.OcError):
+        job.finish()  # consumed
+    good = torch.tensor([[0.5, 0.25, 0.2], [0.1, 0.9, 0.3]], dtype=torch.float32, device="cuda")
+    oc.oc_build_async(good, good, [0, 2], 4, 2).cancel()
+    with pytest.raises(oc.OcError) as e:
+        oc.oc_build_async(good, good, [0, 2], 9, 2)  # argument errors come back at once
+    assert e.value.code == 1
+    ref, tree = _build_both(good.cpu().numpy(), good.cpu().numpy(), [0, 2], 4, 2)
+    _compare_tree(ref, tree)
