@@ -9,8 +9,8 @@ points and normals are already in HBM:
   precomputation of the next iteration's hash table in a separate thread, the
   octree of step i+1 is built during step i: the part that decides the
   per-depth counts (quantisation, occupancy bitmaps, their scan) at the head
-  of the step on the network stream, the rest (leaf signal, keys, labels,
-  neighbour tables) on a second stream while the network of step i runs;
+  of the step, so that the host has the counts while the network of step i
+  runs, the rest (leaf signal, keys, labels, neighbour tables) after it;
   every timed step builds one octree and runs one forward and backward.
 The default workload is the 32-shape depth-6 network: conv3 3->16 @d6,
 16->32 @d5, 32->64 @d4, 64->128 @d3 (each + ReLU + 2x2x2 max-pool), then
@@ -25,7 +25,9 @@ The printed JSON line reports:
                  warmup): its algorithmic flops (or bytes) per launch over its
                  mean launch time, from HIP events that the library records at
                  the start and end of that kernel (hipExtLaunchKernelGGL) on the
-                 stream it runs on, against the MI355X peak;
+                 stream it runs on, against the MI355X peak.  In the timed
+                 steps one launch of it per step is bracketed, its launches
+                 (layers) in turn, each layer's mean taken first;
   cpu_baseline   the plain CPU oracle on a bounded sample of the same workload.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
@@ -116,6 +118,11 @@ class Step:
                 self.x0 = self.x0.to(torch.bfloat16)
         self.events = None  # {key: [(start, end, layer), ...]} when recording
         self.traced = set()
+        # when set: only the (step number % rotate)-th launch of a traced key
+        # in each step is bracketed (each bracketing costs the step time)
+        self.rotate = None
+        self.nstep = 0
+        self.ncall = {}
         # the kernel that does the arithmetic of each conv pass, as profilers name it
         tree = oc.oc_build(self.pts, self.nrm, offs, wl.depth, wl.full_depth)
         self.kname = {}
@@ -175,6 +182,11 @@ class Step:
         L = self.wl.layers[li] if li is not None else None
         k = self.key(tag, li)
         if self.events is not None and (k in self.traced or "*" in self.traced):
+            if self.rotate:
+                n = self.ncall.get(k, 0)
+                self.ncall[k] = n + 1
+                if n != self.nstep % self.rotate:
+                    return fn()
             torch = self.torch
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
@@ -194,42 +206,36 @@ class Step:
 
     def _begin(self):
         """First half of the next batch's build (up to the per-depth counts),
-        enqueued on the network stream at the head of the step."""
+        enqueued at the head of the step."""
         oc, wl = self.oc, self.wl
         return self._run("build", None, lambda: oc.oc_build_async(
             self.pts, self.nrm, self.offs, wl.depth, wl.full_depth))
 
     def _finish(self, job):
-        """Wait for the counts of `job` and enqueue the rest of its build (leaf
-        signal, keys, labels and neighbour tables) on the build stream; the
-        network stream waits for it on the device, one step later."""
-        torch = self.torch
-        with torch.cuda.stream(self.bstream):
-            tree = self._run("build_emit", None, lambda: job.finish(self.bstream))
-            ev = torch.cuda.Event()
-            ev.record(self.bstream)
-        tree.record_stream(self.nstream)
-        return tree, ev
+        """Wait for the counts of `job` (queued at the head of the step, so
+        they are known while the network still runs) and enqueue the rest of
+        its build (leaf signal, keys, labels, neighbour tables) after the
+        network, on the same stream."""
+        return self._run("build_emit", None, lambda: job.finish())
 
     def __call__(self):
-        """One step: the first half of the next batch's build, then the network
-        forward and backward on the octree built during the previous step, then
-        (once the next build's counts are known, which happens early in the
-        step on the device) the rest of the next build on the build stream,
-        where it overlaps the network.  As in the paper's training (Sec. 3.2,
-        last paragraph) the next batch's octree is built while the current
-        one trains."""
-        torch = self.torch
-        if getattr(self, "bstream", None) is None:
-            self.nstream = torch.cuda.current_stream()
-            self.bstream = torch.cuda.Stream()  # default priority
+        """One step: the first half of the next batch's build, the network
+        forward and backward on the octree built during the previous step,
+        then the rest of the next build.  As in the paper's training (Sec. 3.2,
+        last paragraph) the next batch's octree is prepared while the current
+        one trains: the host waits for the next build's counts while the device
+        runs the network.  The device work of the build is not run beside the
+        network: the network's persistent kernels hold every CU, and a build
+        kernel queued beside them delays them more than it costs in line."""
+        self.ncall = {}
+        if getattr(self, "cur", None) is None:
             self.cur = self._finish(self._begin())
         job = self._begin()
-        tree, ev = self.cur
-        self.nstream.wait_event(ev)
+        tree = self.cur
         g = self.network(tree)
         tree.free()
         self.cur = self._finish(job)
+        self.nstep += 1
         return g
 
     def drain(self):
@@ -375,8 +381,10 @@ def main():
                    key=lambda k: warm[k]["ms"])
     print(f"[bench] warmup done; dominant kernel: {dominant}", file=sys.stderr, flush=True)
 
-    # timed region: K steps; events bracket only the dominant class
-    step.events, step.traced = {}, {dominant}
+    # timed region: K steps; events bracket one launch of the dominant kernel
+    # per step, the launches taken in turn
+    nper = max(1, warm[dominant]["launches"] // max(args.warmup, 1))
+    step.events, step.traced, step.rotate, step.nstep = {}, {dominant}, nper, 0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -388,8 +396,15 @@ def main():
     dom = step.collect()[dominant]
     print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
 
-    per_launch_ms = dom["ms"] / dom["launches"]
-    per_launch_work = dom["work"] / dom["launches"]
+    # mean time of each launch of the step (layer), then their sum against
+    # their work: every launch weighs the same however often it was sampled
+    by = {}
+    for a, b, L, tag in step.events[dominant]:
+        t = by.setdefault((tag, L.depth if L is not None else -1), [0.0, 0, step.work(tag, L)])
+        t[0] += a.elapsed_time(b)
+        t[1] += 1
+    per_launch_ms = sum(t[0] / t[1] for t in by.values()) / len(by)
+    per_launch_work = sum(t[2] for t in by.values()) / len(by)
     bound = BOUND[dom["op"]]
     if bound == "mfma":
         achieved = per_launch_work / (per_launch_ms * 1e-3) / 1e12
@@ -399,7 +414,7 @@ def main():
         peak, unit = PEAK["hbm_GBps"], "GB/s"
     roofline = {"bound": bound, "kernel": dominant, "op": dom["op"], "achieved": round(achieved, 3),
                 "peak": peak, "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
-                "launches_per_step": dom["launches"] // args.steps,
+                "launches_per_step": nper,
                 "mean_launch_us": round(per_launch_ms * 1e3, 2)}
 
     if args.layers:
