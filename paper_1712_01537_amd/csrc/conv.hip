@@ -39,6 +39,33 @@ __device__ __forceinline__ int32_t tap_row(const int32_t* nb, int c, int dx, int
   return base < 0 ? -1 : base + 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
 }
 
+// bf16 -> fp32 (exact), eight elements per thread when the buffers allow.
+__global__ __launch_bounds__(TB) void k_bf16_to_f32(const uint16_t* __restrict__ in, int64_t n,
+                                                    int vec, float* __restrict__ out) {
+  const int64_t e = 8 * ((int64_t)blockIdx.x * TB + threadIdx.x);
+  if (e >= n) return;
+  if (vec && e + 8 <= n) {  // vec: in 16-byte and out 32-byte aligned
+    const uint4 u = *reinterpret_cast<const uint4*>(in + e);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+    float4 a, b;
+    a.x = __uint_as_float(w[0] << 16), a.y = __uint_as_float(w[0] & 0xFFFF0000u);
+    a.z = __uint_as_float(w[1] << 16), a.w = __uint_as_float(w[1] & 0xFFFF0000u);
+    b.x = __uint_as_float(w[2] << 16), b.y = __uint_as_float(w[2] & 0xFFFF0000u);
+    b.z = __uint_as_float(w[3] << 16), b.w = __uint_as_float(w[3] & 0xFFFF0000u);
+    *reinterpret_cast<float4*>(out + e) = a;
+    *reinterpret_cast<float4*>(out + e + 4) = b;
+  } else {
+    for (int64_t i = e; i < n && i < e + 8; ++i) out[i] = __uint_as_float((uint32_t)in[i] << 16);
+  }
+}
+
+void bf16_to_f32(const void* in, int64_t n, float* out, hipStream_t s) {
+  if (n <= 0) return;
+  const int vec = (uintptr_t)in % 16 == 0 && (uintptr_t)out % 32 == 0;
+  hipLaunchKernelGGL(k_bf16_to_f32, dim3((unsigned)oc::cdiv(n, 8 * TB)), dim3(TB), 0, s,
+                     (const uint16_t*)in, n, vec, out);
+}
+
 // ReLU backward: dym[e] = y[e] > 0 ? dy[e] : 0, four entries per thread.
 __global__ __launch_bounds__(TB) void k_relu_mask(const float* __restrict__ y,
                                                   const float* __restrict__ dy, int64_t n,
@@ -242,11 +269,22 @@ int64_t dw_chunk(const ConvShape& sh, int cin, int cout, int* nparts) {
   return chunk;
 }
 
-// Workspace bytes of each part of a convolution call.
+// Workspace bytes of each part of a convolution call.  A bf16 stride-1 call
+// first widens its bf16 operands to fp32 in the workspace (exact) and runs
+// the fp32 matrix-core kernels on them: x32 [n_in][cin], w32 [K^3][cin][cout]
+// at the front of the workspace.
+size_t x32_bytes(const ConvShape& sh, int cin) {
+  return oc::align256((size_t)sh.n_in * cin * sizeof(float));
+}
+size_t w32_bytes(const ConvShape& sh, int cin, int cout) {
+  return oc::align256((size_t)sh.K3 * cin * cout * sizeof(float));
+}
+
 size_t fwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,
                     int cout) {
-  if (dt == OC_F32 && sh.stride == 1 && sh.n_in > 0) return oc::conv_s1_tile_ws(t, l, sh.K, cin, cout);
-  return 0;
+  if (sh.stride != 1 || sh.n_in == 0) return 0;
+  const size_t tile = oc::conv_s1_tile_ws(t, l, sh.K, cin, cout);
+  return dt == OC_F32 ? tile : x32_bytes(sh, cin) + w32_bytes(sh, cin, cout) + tile;
 }
 
 // The matrix-core path applies the ReLU backward once, into the workspace,
@@ -259,12 +297,14 @@ size_t bwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype
                     int cout) {
   if (sh.units == 0) return 0;
   const size_t entries = (size_t)sh.K3 * cin * cout;
-  if (dt == OC_F32 && sh.stride == 1) {
-    // the ReLU-masked upstream gradient, then the input gradient's and the
-    // weight gradient's partial sums: the same bytes serve both in stream order
+  if (sh.stride == 1) {
+    // (bf16: the widened w and x,) the ReLU-masked upstream gradient, then
+    // the input gradient's and the weight gradient's partial sums: the same
+    // bytes serve both in stream order
     const size_t a = oc::conv_s1_tile_ws(t, l, sh.K, cout, cin);
     const size_t b = oc::conv_s1_dw_parts(t, l, sh.K, cin, cout) * entries * sizeof(float);
-    return mask_ws_bytes(sh, cout) + std::max(a, b);
+    const size_t wide = dt == OC_F32 ? 0 : w32_bytes(sh, cin, cout) + x32_bytes(sh, cin);
+    return wide + mask_ws_bytes(sh, cout) + std::max(a, b);
   }
   int nparts;
   dw_chunk(sh, cin, cout, &nparts);
@@ -285,7 +325,7 @@ const char* oc_conv_kernel(const oc_octree* t, int32_t l, int32_t K, int32_t str
     return name;
   }
   if (check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_kernel") != OC_OK) return name;
-  if (dt == OC_F32 && stride == 1) {
+  if (stride == 1) {  // bf16 runs the fp32 kernels on widened operands
     oc::conv_s1_kernel_name(t, l, K, cin, cout, pass, name, sizeof(name));
   } else {
     const char* ty = dt == OC_F32 ? "float" : "unsigned short";
@@ -317,9 +357,18 @@ oc_status oc_conv_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   if (need && (!ws || ws_bytes < need))
     return oc::fail(OC_ERR_ARG, "oc_conv_fwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0, need);
   const int relu = (flags & OC_FUSE_RELU) ? 1 : 0;
-  if (dt == OC_F32 && stride == 1) {
-    oc::conv_s1_fwd_f32(t, l, K, (const float*)x, cin, (const float*)w, cout, y, relu, (float*)ws,
-                        s);
+  if (stride == 1) {
+    const float *x32 = (const float*)x, *w32 = (const float*)w;
+    char* rest = (char*)ws;
+    if (dt == OC_BF16) {
+      float* xw = (float*)rest;
+      float* ww = (float*)(rest + x32_bytes(sh, cin));
+      bf16_to_f32(x, sh.n_in * (int64_t)cin, xw, s);
+      bf16_to_f32(w, (int64_t)sh.K3 * cin * cout, ww, s);
+      x32 = xw, w32 = ww;
+      rest += x32_bytes(sh, cin) + w32_bytes(sh, cin, cout);
+    }
+    oc::conv_s1_fwd_f32(t, l, K, x32, cin, w32, cout, y, relu, (float*)rest, s);
     OC_LAUNCH_CHECK();
     return OC_OK;
   }
@@ -359,8 +408,17 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   const float* ym = (flags & OC_FUSE_RELU) ? y : nullptr;
   int nparts = 0;
   const int64_t chunk = dw_chunk(sh, cin, cout, &nparts);
-  const bool mfma = dt == OC_F32 && stride == 1;
+  const bool mfma = stride == 1;
   float* wsf = (float*)ws;
+  if (mfma && dt == OC_BF16 && (dx || dw)) {  // the bf16 operands widened to fp32 (exact)
+    float* ww = wsf;
+    float* xw = (float*)((char*)ws + w32_bytes(sh, cin, cout));
+    if (dx) bf16_to_f32(w, (int64_t)sh.K3 * cin * cout, ww, s);
+    if (dw) bf16_to_f32(x, sh.n_in * (int64_t)cin, xw, s);
+    w = ww;
+    x = xw;
+    wsf = (float*)((char*)ws + w32_bytes(sh, cin, cout) + x32_bytes(sh, cin));
+  }
   if (mfma && (dx || dw)) {
     if (ym && sh.n_out > 0) {  // dy masked once, read by both gradients
       const int64_t n = sh.n_out * (int64_t)cout;
@@ -369,7 +427,7 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
                          n, vec, wsf);
       dy = wsf;
     }
-    wsf += mask_ws_bytes(sh, cout) / sizeof(float);
+    wsf = (float*)((char*)wsf + mask_ws_bytes(sh, cout));
   }
   const int64_t entries = (int64_t)sh.K3 * cin * cout;
   const int32_t* nbr = t->nbr[l];
