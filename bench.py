@@ -171,6 +171,10 @@ class Step:
             return N[l] * c * 4 + N[l - 1] * 4 + N[l - 1] * c * 4 + M[l - 1] * c
         if tag == "pool_bwd":
             return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l] * c * 4
+        if tag == "unpool_fwd":  # parent rows and switches in, every child row out
+            return M[l - 1] * c * 5 + M[l - 1] * 4 + N[l] * c * 4
+        if tag == "unpool_bwd":  # the routed child of each (parent, channel) in, parent rows out
+            return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l - 1] * c * 4
         return 0
 
     # --- one step ----------------------------------------------------------
@@ -246,9 +250,12 @@ class Step:
         oc, wl = self.oc, self.wl
         x = tree.signal() if wl.signal_input else self.x0
         saved = []
+        sws = {}  # switches of the pooling at each depth, for the unpooling
         for li, L in enumerate(wl.layers):
             if L.op == "conv":
                 w = self.weights[li]
+                if x.dtype != w.dtype:  # a bf16 layer after an fp32 output
+                    x = x.to(w.dtype)
                 y = self._run("conv_fwd", li, lambda: oc.oc_conv_fwd(
                     tree, L.depth, L.ksize, L.stride, x, w, relu=L.relu))
                 saved.append((li, x, y, None))
@@ -256,7 +263,13 @@ class Step:
             elif L.op == "pool":
                 p, sw = self._run("pool_fwd", li, lambda: oc.oc_pool_fwd(tree, L.depth, x))
                 saved.append((li, x, p, sw))
+                sws[L.depth] = sw
                 x = p
+            elif L.op == "unpool":
+                sw = sws[L.depth]
+                u = self._run("unpool_fwd", li, lambda: oc.oc_unpool_fwd(tree, L.depth, x, sw))
+                saved.append((li, x, u, sw))
+                x = u
         g = self.dy_last
         masked = False  # g already went through the ReLU of the conv below it
         for li, xin, yout, sw in reversed(saved):
@@ -280,6 +293,9 @@ class Step:
                 masked = P is not None and P.op == "conv" and P.relu
                 ym = yout if masked else None
                 g = self._run("pool_bwd", li, lambda: oc.oc_pool_bwd(tree, L.depth, g, sw, y=ym))
+            elif L.op == "unpool":
+                g = self._run("unpool_bwd", li, lambda: oc.oc_unpool_bwd(tree, L.depth, g, sw))
+                masked = False
         return g
 
     def collect(self):
@@ -408,7 +424,8 @@ def main():
     bound = BOUND[dom["op"]]
     if bound == "mfma":
         achieved = per_launch_work / (per_launch_ms * 1e-3) / 1e12
-        peak, unit = PEAK["fp32_TFLOPs"], "TFLOP/s"
+        bf16 = any(L is not None and L.dtype == "bf16" for _, _, L, _ in step.events[dominant])
+        peak, unit = PEAK["bf16_TFLOPs" if bf16 else "fp32_TFLOPs"], "TFLOP/s"
     else:
         achieved = per_launch_work / (per_launch_ms * 1e-3) / 1e9
         peak, unit = PEAK["hbm_GBps"], "GB/s"

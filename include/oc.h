@@ -183,12 +183,18 @@ void oc_octree_free(oc_octree* tree);
  *              parent; rows of empty parents are zero (Sec. 3.2 stride-2
  *              paragraphs, Fig. 2(d)).
  *   dt      OC_F32: x, w fp32.  OC_BF16: x, w bf16 (round-to-nearest-even
- *           values held as uint16); products accumulate in fp32.
+ *           values held as uint16); products accumulate in fp32, so the
+ *           result is the fp32 convolution of the bf16 values.
  *   x       dev [N_l][cin].      w  dev [K^3][cin][cout].
  *   y       dev f32 [N_out][cout], N_out = N_l (stride 1) or N_{l-1}.
  *   ws      dev workspace of at least oc_conv_fwd_workspace() bytes (may be
  *           NULL when that is 0): partial sums of a reduction split across
- *           workgroups, added in a fixed order (results are reproducible).
+ *           workgroups, added in a fixed order (results are reproducible);
+ *           for OC_BF16 also x and w widened to fp32; for stride 2 the
+ *           column buffer (at most 256 MB, the groups taken in chunks) and
+ *           the per-group outputs.  Stride 2 multiplies the column buffer by
+ *           w with the ROCm GEMM library (atomics disabled, so the result is
+ *           reproducible too).
  *   flags   0 or OC_FUSE_RELU.
  * cin, cout in 1..1024. */
 oc_status oc_conv_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
@@ -198,8 +204,10 @@ oc_status oc_conv_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32
 /* Name, template arguments included (as profilers such as rocprofv3 print
  * it), of the kernel that does the arithmetic of one pass of a convolution
  * call with these arguments: pass 0 = oc_conv_fwd, 1 = the input gradient and
- * 2 = the weight gradient of oc_conv_bwd.  Lets a caller attribute measured
- * kernel time to the operation it belongs to.  The string lives in
+ * 2 = the weight gradient of oc_conv_bwd.  A stride-2 pass is several
+ * kernels and a GEMM; it is named "conv_s2_<fwd|bwd_data|bwd_weight><dtype>"
+ * instead.  Lets a caller attribute measured kernel time to the operation it
+ * belongs to.  The string lives in
  * thread-local storage until the next call on the thread; "" (and
  * oc_last_error set) for invalid arguments. */
 const char* oc_conv_kernel(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
@@ -223,7 +231,9 @@ size_t oc_conv_bwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize
  *   dw   dev f32 [K^3][cin][cout] or NULL: gradient w.r.t. w (overwritten).
  *   ws   dev workspace of at least oc_conv_bwd_workspace() bytes.
  * Deterministic: no floating-point atomics; repeated calls give identical
- * bits. */
+ * bits.  The stride-2 workspace holds the per-group upstream gradient and
+ * either the column-buffer gradient of every group (input gradient) or a
+ * column-buffer chunk (weight gradient). */
 oc_status oc_conv_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
                       oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
                       const float* y, const float* dy, float* dx, float* dw, void* ws,
@@ -267,7 +277,8 @@ oc_status oc_unpool_bwd(const oc_octree* tree, int32_t depth, const float* dy, c
  * convolution pass; the pooling, routing or unpooling kernel of oc_pool_* /
  * oc_unpool_*) is bracketed by these events, recorded at the start and the
  * end of that kernel on its stream (as hipExtLaunchKernelGGL does), so that
- * its duration is measured without host-side gaps.  Both NULL clears a
+ * its duration is measured without host-side gaps.  A stride-2 convolution
+ * pass records them around all of its kernels and GEMMs.  Both NULL clears a
  * pending pair.  The caller owns the events. */
 oc_status oc_profile_next(hipEvent_t start, hipEvent_t stop);
 

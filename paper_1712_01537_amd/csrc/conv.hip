@@ -9,35 +9,19 @@
 // first-child row (or -1), so every tap is one table read plus an add: the
 // (K+1)^3 union neighbourhood of the eight siblings (Sec. 3.2, Fig. 4).
 //
-// Backward w.r.t. the input.  For stride 1, j is the neighbour of i at
-// offset d iff i is the neighbour of j at offset -d, and every octant of
-// depth l is both an input and an output row; hence dX = conv(dY, W') with
-// W'[k] = W[K^3-1-k]^T, evaluated by the forward gather.  For stride 2 each
-// input octant receives from at most 2^(number of odd child bits) outputs,
-// reached through the same table.
-// Backward w.r.t. the weights: dW[k] = sum_i X[n(i,k)]^T dY[i], split over
-// row chunks into partial sums that a second kernel adds in a fixed order
-// (no floating-point atomics, so results are reproducible bit for bit).
+// Stride 1 runs on the matrix-core kernels of conv_mfma.hip (bf16 operands
+// widened to fp32 first, which is exact); stride 2 on the column buffers and
+// GEMMs of conv_s2.hip.  This file checks arguments, sizes the workspaces and
+// applies the ReLU backward ahead of the stride-1 gradients.
 #include <algorithm>
 
 #include "common.h"
 #include "conv_mfma.h"
+#include "conv_s2.h"
 
 namespace {
 
 constexpr int TB = 256;
-
-__device__ __forceinline__ float ld(const float* p, int64_t i) { return p[i]; }
-__device__ __forceinline__ float ld(const uint16_t* p, int64_t i) {
-  return __uint_as_float((uint32_t)p[i] << 16);
-}
-
-// Source row of tap (dx,dy,dz) of child c in group g, or -1.
-__device__ __forceinline__ int32_t tap_row(const int32_t* nb, int c, int dx, int dy, int dz) {
-  const int ux = (c >> 2) + dx, uy = ((c >> 1) & 1) + dy, uz = (c & 1) + dz;
-  const int32_t base = nb[((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1)];
-  return base < 0 ? -1 : base + 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
-}
 
 // bf16 -> fp32 (exact), eight elements per thread when the buffers allow.
 __global__ __launch_bounds__(TB) void k_bf16_to_f32(const uint16_t* __restrict__ in, int64_t n,
@@ -82,157 +66,6 @@ __global__ __launch_bounds__(TB) void k_relu_mask(const float* __restrict__ y,
   }
 }
 
-// Forward.  stride 1: output row i = group i>>3, child i&7.  stride 2:
-// output row i of depth l-1 with label L > 0 evaluates child 0 of group L-1.
-template <typename T>
-__global__ __launch_bounds__(TB) void k_conv_fwd_simple(const int32_t* __restrict__ nbr,
-                                                        const int32_t* __restrict__ labels_out,
-                                                        int64_t n_out, int stride, int K,
-                                                        const T* __restrict__ x, int cin,
-                                                        const T* __restrict__ w, int cout,
-                                                        float* __restrict__ y, int relu) {
-  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (t >= n_out * cout) return;
-  const int64_t i = t / cout;
-  const int co = (int)(t - i * cout);
-  int64_t g;
-  int c;
-  if (stride == 1) {
-    g = i >> 3;
-    c = (int)(i & 7);
-  } else {
-    const int32_t L = labels_out[i];
-    if (L == 0) {
-      y[t] = 0.0f;
-      return;
-    }
-    g = L - 1;
-    c = 0;
-  }
-  const int r = (K - 1) / 2;
-  const int32_t* nb = nbr + 27 * g;
-  float acc = 0.0f;
-  int k = 0;
-  for (int dx = -r; dx <= r; ++dx)
-    for (int dy = -r; dy <= r; ++dy)
-      for (int dz = -r; dz <= r; ++dz, ++k) {
-        const int32_t src = tap_row(nb, c, dx, dy, dz);
-        if (src < 0) continue;
-        for (int ci = 0; ci < cin; ++ci)
-          acc = fmaf(ld(x, (int64_t)src * cin + ci), ld(w, ((int64_t)k * cin + ci) * cout + co), acc);
-      }
-  y[t] = relu ? fmaxf(acc, 0.0f) : acc;
-}
-
-// Upstream gradient with the fused-ReLU mask applied.
-__device__ __forceinline__ float dy_eff(const float* dy, const float* y, int64_t idx) {
-  const float g = dy[idx];
-  return y ? (y[idx] > 0.0f ? g : 0.0f) : g;
-}
-
-// Backward data, stride 1: dX[j][ci] = sum_k sum_co dY[n(j,k)][co] W[K^3-1-k][ci][co].
-template <typename T>
-__global__ __launch_bounds__(TB) void k_conv_bwd_data_s1_simple(
-    const int32_t* __restrict__ nbr, int64_t n, int K, const float* __restrict__ dy,
-    const float* __restrict__ y, int cout, const T* __restrict__ w, int cin,
-    float* __restrict__ dx) {
-  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (t >= n * cin) return;
-  const int64_t j = t / cin;
-  const int ci = (int)(t - j * cin);
-  const int r = (K - 1) / 2, K3 = K * K * K;
-  const int32_t* nb = nbr + 27 * (j >> 3);
-  const int c = (int)(j & 7);
-  float acc = 0.0f;
-  int k = 0;
-  for (int ddx = -r; ddx <= r; ++ddx)
-    for (int ddy = -r; ddy <= r; ++ddy)
-      for (int ddz = -r; ddz <= r; ++ddz, ++k) {
-        const int32_t src = tap_row(nb, c, ddx, ddy, ddz);
-        if (src < 0) continue;
-        const int kf = K3 - 1 - k;
-        for (int co = 0; co < cout; ++co)
-          acc = fmaf(dy_eff(dy, y, (int64_t)src * cout + co), ld(w, ((int64_t)kf * cin + ci) * cout + co), acc);
-      }
-  dx[t] = acc;
-}
-
-// Backward data, stride 2 (K = 3): input row j = 8g' + c' receives from the
-// outputs whose first child sees it: parent offset p_a in {0} if c'_a = 0,
-// {0, 1} if c'_a = 1, with tap d_a = c'_a - 2 p_a.
-template <typename T>
-__global__ __launch_bounds__(TB) void k_conv_bwd_data_s2_simple(
-    const int32_t* __restrict__ nbr, const int32_t* __restrict__ rows_out, int64_t n,
-    const float* __restrict__ dy, const float* __restrict__ y, int cout, const T* __restrict__ w,
-    int cin, float* __restrict__ dx) {
-  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (t >= n * cin) return;
-  const int64_t j = t / cin;
-  const int ci = (int)(t - j * cin);
-  const int32_t* nb = nbr + 27 * (j >> 3);
-  const int c = (int)(j & 7);
-  const int cx = c >> 2, cy = (c >> 1) & 1, cz = c & 1;
-  float acc = 0.0f;
-  for (int px = 0; px <= cx; ++px)
-    for (int py = 0; py <= cy; ++py)
-      for (int pz = 0; pz <= cz; ++pz) {
-        const int32_t f = nb[(px + 1) * 9 + (py + 1) * 3 + (pz + 1)];
-        if (f < 0) continue;
-        const int64_t orow = rows_out[f >> 3];
-        const int k = ((cx - 2 * px + 1) * 3 + (cy - 2 * py + 1)) * 3 + (cz - 2 * pz + 1);
-        for (int co = 0; co < cout; ++co)
-          acc = fmaf(dy_eff(dy, y, orow * cout + co), ld(w, ((int64_t)k * cin + ci) * cout + co), acc);
-      }
-  dx[t] = acc;
-}
-
-// Backward weights, partial sums over chunk q of the output rows.
-// stride 1: rows i in [q*chunk, ...), child i&7 of group i>>3, upstream row i.
-// stride 2: groups g in the chunk, child 0, upstream row rows_out[g].
-template <typename T>
-__global__ __launch_bounds__(TB) void k_conv_dw_partial_simple(
-    const int32_t* __restrict__ nbr, const int32_t* __restrict__ rows_out, int64_t n_units,
-    int stride, int K, const T* __restrict__ x, int cin, const float* __restrict__ dy,
-    const float* __restrict__ y, int cout, int64_t chunk, float* __restrict__ part) {
-  const int64_t entries = (int64_t)K * K * K * cin * cout;
-  const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (e >= entries) return;
-  const int q = blockIdx.y;
-  const int k = (int)(e / ((int64_t)cin * cout));
-  const int ci = (int)((e / cout) % cin);
-  const int co = (int)(e % cout);
-  const int r = (K - 1) / 2;
-  const int dxo = k / (K * K) - r, dyo = (k / K) % K - r, dzo = k % K - r;
-  const int64_t u0 = (int64_t)q * chunk, u1 = min(n_units, u0 + chunk);
-  float acc = 0.0f;
-  for (int64_t u = u0; u < u1; ++u) {
-    int64_t g, orow;
-    int c;
-    if (stride == 1) {
-      g = u >> 3;
-      c = (int)(u & 7);
-      orow = u;
-    } else {
-      g = u;
-      c = 0;
-      orow = rows_out[u];
-    }
-    const int32_t src = tap_row(nbr + 27 * g, c, dxo, dyo, dzo);
-    if (src < 0) continue;
-    acc = fmaf(ld(x, (int64_t)src * cin + ci), dy_eff(dy, y, orow * cout + co), acc);
-  }
-  part[(int64_t)q * entries + e] = acc;
-}
-
-__global__ __launch_bounds__(TB) void k_reduce_parts(const float* __restrict__ part, int nparts,
-                                                     int64_t entries, float* __restrict__ out) {
-  const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (e >= entries) return;
-  float s = 0.0f;
-  for (int q = 0; q < nparts; ++q) s += part[(int64_t)q * entries + e];
-  out[e] = s;
-}
-
 inline unsigned grid_for(int64_t n) { return (unsigned)oc::cdiv(n, TB); }
 
 struct ConvShape {
@@ -260,15 +93,6 @@ oc_status check_conv(const oc_octree* t, int32_t l, int32_t K, int32_t stride, o
   return OC_OK;
 }
 
-int64_t dw_chunk(const ConvShape& sh, int cin, int cout, int* nparts) {
-  const int64_t entries = (int64_t)sh.K3 * cin * cout;
-  const int64_t max_parts = std::max<int64_t>(1, (int64_t(64) << 20) / entries);
-  int64_t parts = std::min<int64_t>(max_parts, std::max<int64_t>(1, oc::cdiv(sh.units, 2048)));
-  int64_t chunk = std::max<int64_t>(1, oc::cdiv(sh.units, parts));
-  *nparts = (int)std::max<int64_t>(1, oc::cdiv(sh.units, chunk));
-  return chunk;
-}
-
 // Workspace bytes of each part of a convolution call.  A bf16 stride-1 call
 // first widens its bf16 operands to fp32 in the workspace (exact) and runs
 // the fp32 matrix-core kernels on them: x32 [n_in][cin], w32 [K^3][cin][cout]
@@ -282,7 +106,8 @@ size_t w32_bytes(const ConvShape& sh, int cin, int cout) {
 
 size_t fwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,
                     int cout) {
-  if (sh.stride != 1 || sh.n_in == 0) return 0;
+  if (sh.stride == 2) return oc::conv_s2_fwd_ws(t, l, cin, cout, dt == OC_BF16);
+  if (sh.n_in == 0) return 0;
   const size_t tile = oc::conv_s1_tile_ws(t, l, sh.K, cin, cout);
   return dt == OC_F32 ? tile : x32_bytes(sh, cin) + w32_bytes(sh, cin, cout) + tile;
 }
@@ -306,9 +131,7 @@ size_t bwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype
     const size_t wide = dt == OC_F32 ? 0 : w32_bytes(sh, cin, cout) + x32_bytes(sh, cin);
     return wide + mask_ws_bytes(sh, cout) + std::max(a, b);
   }
-  int nparts;
-  dw_chunk(sh, cin, cout, &nparts);
-  return (size_t)nparts * entries * sizeof(float);
+  return oc::conv_s2_bwd_ws(t, l, cin, cout, dt == OC_BF16, true, true);
 }
 
 }  // namespace
@@ -327,13 +150,10 @@ const char* oc_conv_kernel(const oc_octree* t, int32_t l, int32_t K, int32_t str
   if (check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_kernel") != OC_OK) return name;
   if (stride == 1) {  // bf16 runs the fp32 kernels on widened operands
     oc::conv_s1_kernel_name(t, l, K, cin, cout, pass, name, sizeof(name));
-  } else {
-    const char* ty = dt == OC_F32 ? "float" : "unsigned short";
-    const char* k = pass == 0   ? "k_conv_fwd_simple"
-                    : pass == 2 ? "k_conv_dw_partial_simple"
-                    : stride == 1 ? "k_conv_bwd_data_s1_simple"
-                                  : "k_conv_bwd_data_s2_simple";
-    snprintf(name, sizeof(name), "%s<%s>", k, ty);
+  } else {  // several kernels and a GEMM: the pass is named
+    snprintf(name, sizeof(name), "conv_s2_%s<%s>",
+             pass == 0 ? "fwd" : pass == 1 ? "bwd_data" : "bwd_weight",
+             dt == OC_F32 ? "f32" : "bf16");
   }
   return name;
 }
@@ -372,15 +192,8 @@ oc_status oc_conv_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
     OC_LAUNCH_CHECK();
     return OC_OK;
   }
-  const unsigned grid = grid_for(sh.n_out * cout);
-  if (dt == OC_F32)
-    oc::launch_main(k_conv_fwd_simple<float>, dim3(grid), dim3(TB), s,
-                       (const int32_t*)t->nbr[l], (const int32_t*)t->labels[l - 1], sh.n_out, stride,
-                       K, (const float*)x, cin, (const float*)w, cout, y, relu);
-  else
-    oc::launch_main(k_conv_fwd_simple<uint16_t>, dim3(grid), dim3(TB), s,
-                       (const int32_t*)t->nbr[l], (const int32_t*)t->labels[l - 1], sh.n_out, stride,
-                       K, (const uint16_t*)x, cin, (const uint16_t*)w, cout, y, relu);
+  st = oc::conv_s2_fwd(t, l, x, cin, w, cout, dt == OC_BF16, y, relu, ws, s);
+  if (st != OC_OK) return st;
   OC_LAUNCH_CHECK();
   return OC_OK;
 }
@@ -406,11 +219,15 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   if (need && (!ws || ws_bytes < need))
     return oc::fail(OC_ERR_ARG, "oc_conv_bwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0, need);
   const float* ym = (flags & OC_FUSE_RELU) ? y : nullptr;
-  int nparts = 0;
-  const int64_t chunk = dw_chunk(sh, cin, cout, &nparts);
-  const bool mfma = stride == 1;
+  if (stride == 2) {
+    st = oc::conv_s2_bwd(t, l, x, cin, w, cout, dt == OC_BF16, ym, dy, dx, dw, ws, s);
+    if (st != OC_OK) return st;
+    OC_LAUNCH_CHECK();
+    return OC_OK;
+  }
+  // stride 1: matrix-core kernels
   float* wsf = (float*)ws;
-  if (mfma && dt == OC_BF16 && (dx || dw)) {  // the bf16 operands widened to fp32 (exact)
+  if (dt == OC_BF16 && (dx || dw)) {  // the bf16 operands widened to fp32 (exact)
     float* ww = wsf;
     float* xw = (float*)((char*)ws + w32_bytes(sh, cin, cout));
     if (dx) bf16_to_f32(w, (int64_t)sh.K3 * cin * cout, ww, s);
@@ -419,7 +236,7 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
     x = xw;
     wsf = (float*)((char*)ws + w32_bytes(sh, cin, cout) + x32_bytes(sh, cin));
   }
-  if (mfma && (dx || dw)) {
+  if (dx || dw) {
     if (ym && sh.n_out > 0) {  // dy masked once, read by both gradients
       const int64_t n = sh.n_out * (int64_t)cout;
       const int vec = ((uintptr_t)y % 16 == 0 && (uintptr_t)dy % 16 == 0 && (uintptr_t)wsf % 16 == 0);
@@ -429,46 +246,12 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
     }
     wsf = (float*)((char*)wsf + mask_ws_bytes(sh, cout));
   }
-  const int64_t entries = (int64_t)sh.K3 * cin * cout;
-  const int32_t* nbr = t->nbr[l];
-  const int32_t* rows_out = t->rows[l - 1];
-  if (dx && sh.n_in > 0 && mfma) {
-    oc::conv_s1_bwd_data_f32(t, l, K, dy, cout, (const float*)w, cin, dx, wsf, s);
-  } else if (dx && sh.n_in > 0) {
-    const unsigned grid = grid_for(sh.n_in * cin);
-    if (stride == 1) {
-      if (dt == OC_F32)
-        oc::launch_main(k_conv_bwd_data_s1_simple<float>, dim3(grid), dim3(TB), s, nbr,
-                           sh.n_in, K, dy, ym, cout, (const float*)w, cin, dx);
-      else
-        oc::launch_main(k_conv_bwd_data_s1_simple<uint16_t>, dim3(grid), dim3(TB), s, nbr,
-                           sh.n_in, K, dy, ym, cout, (const uint16_t*)w, cin, dx);
-    } else {
-      if (dt == OC_F32)
-        oc::launch_main(k_conv_bwd_data_s2_simple<float>, dim3(grid), dim3(TB), s, nbr,
-                           rows_out, sh.n_in, dy, ym, cout, (const float*)w, cin, dx);
-      else
-        oc::launch_main(k_conv_bwd_data_s2_simple<uint16_t>, dim3(grid), dim3(TB), s, nbr,
-                           rows_out, sh.n_in, dy, ym, cout, (const uint16_t*)w, cin, dx);
-    }
-  }
+  if (dx && sh.n_in > 0) oc::conv_s1_bwd_data_f32(t, l, K, dy, cout, (const float*)w, cin, dx, wsf, s);
   if (dw) {
-    if (sh.units == 0) {
-      oc::fill_u32(dw, 0u, entries, s);
-    } else if (mfma) {
+    if (sh.units == 0)
+      oc::fill_u32(dw, 0u, (int64_t)sh.K3 * cin * cout, s);
+    else
       oc::conv_s1_bwd_weight_f32(t, l, K, (const float*)x, cin, dy, cout, dw, wsf, s);
-    } else {
-      float* part = (float*)ws;
-      dim3 grid(grid_for(entries), nparts);
-      if (dt == OC_F32)
-        oc::launch_main(k_conv_dw_partial_simple<float>, grid, dim3(TB), s, nbr, rows_out,
-                           sh.units, stride, K, (const float*)x, cin, dy, ym, cout, chunk, part);
-      else
-        oc::launch_main(k_conv_dw_partial_simple<uint16_t>, grid, dim3(TB), s, nbr, rows_out,
-                           sh.units, stride, K, (const uint16_t*)x, cin, dy, ym, cout, chunk, part);
-      hipLaunchKernelGGL(k_reduce_parts, dim3(grid_for(entries)), dim3(TB), 0, s,
-                         (const float*)part, nparts, entries, dw);
-    }
   }
   OC_LAUNCH_CHECK();
   return OC_OK;
