@@ -385,12 +385,19 @@ def main():
 
     # warmup, every op timed; the kernel (conv passes) or op class with the
     # largest share of the step is the dominant one
+    # (the first step's one-time costs, such as loading GEMM kernels, are not
+    # counted)
     step.events, step.traced = {}, {"*"}
-    for _ in range(max(args.warmup, 1)):
+    nwarm = max(args.warmup, 2)
+    for i in range(nwarm):
+        if i == 1:
+            torch.cuda.synchronize()
+            step.events = {}
         step()
     step.drain()
     torch.cuda.synchronize()
     warm = step.collect()
+    nwarm -= 1
     # the build (part at the head of the step, part on its own stream) is not a
     # convolution or pooling class
     dominant = max((k for k in warm if not warm[k]["op"].startswith("build")),
@@ -399,7 +406,7 @@ def main():
 
     # timed region: K steps; events bracket one launch of the dominant kernel
     # per step, the launches taken in turn
-    nper = max(1, warm[dominant]["launches"] // max(args.warmup, 1))
+    nper = max(1, warm[dominant]["launches"] // nwarm)
     step.events, step.traced, step.rotate, step.nstep = {}, {dominant}, nper, 0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -438,8 +445,8 @@ def main():
         for key, v in sorted(warm.items(), key=lambda kv: -kv[1]["ms"]):
             per = {}
             for name, t in v["per_layer"]:
-                per[name] = per.get(name, 0.0) + t / max(args.warmup, 1)
-            print(f"[bench] {key:42s} {v['ms'] / max(args.warmup, 1):8.3f} ms/step  "
+                per[name] = per.get(name, 0.0) + t / nwarm
+            print(f"[bench] {key:42s} {v['ms'] / nwarm:8.3f} ms/step  "
                   + "  ".join(f"{k}:{t:.3f}" for k, t in per.items()), file=sys.stderr)
 
     cpu = None
