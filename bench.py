@@ -29,15 +29,30 @@ The printed JSON line reports:
                  steps one launch of it per step is bracketed, its launches
                  (layers) in turn, each layer's mean taken first;
   cpu_baseline   the plain CPU oracle on a bounded sample of the same workload.
+  roofline.traffic  HBM bytes per launch of the dominant kernel from rocprofv3
+                 FETCH_SIZE and WRITE_SIZE counters (two runs of this script
+                 with --copy-probe), each scaled by what the same counter reads
+                 for a plain device copy of known size; taken from
+                 profiles/hbm_counters_<workload>.md, and null when a source
+                 file that defines or launches the kernel (or the shared
+                 header) differs from the one the counters were taken on.
+
+Counter summary: python bench.py --summarize-counters FETCH_DIR WRITE_DIR
+  --copy-probe MIB --workload NAME reads the counter_collection CSV files of
+  the two rocprofv3 runs and prints the summary (markdown with a JSON block).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -74,7 +89,141 @@ def parse():
     ap.add_argument("--cpu-shapes", type=int, default=32,
                     help="shapes of the batch the CPU oracle runs (0: skip)")
     ap.add_argument("--layers", action="store_true", help="also print per-layer timings to stderr")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="after the steps, run an elementwise copy (y = -x) of MIB MiB three "
+                         "times: the known-size kernel that calibrates the HBM byte counters")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print the HBM counter summary of two rocprofv3 --pmc runs and exit")
     return ap.parse_args()
+
+
+SRC_GLOBS = ("paper_1712_01537_amd/csrc/*", "include/*.h")
+
+
+def source_hashes():
+    """sha256 of each source file liboc.so is built from, by repository path."""
+    out = {}
+    for pat in SRC_GLOBS:
+        for f in sorted(glob.glob(os.path.join(ROOT, pat))):
+            with open(f, "rb") as fh:
+                out[os.path.relpath(f, ROOT)] = hashlib.sha256(fh.read()).hexdigest()
+    return out
+
+
+def kernel_sources(kernel):
+    """Source files a kernel's code depends on: the files that define or launch
+    it (its base name followed by '<' or '('), the shared header and the ABI."""
+    base = kernel.split("<")[0]
+    deps = set()
+    for f in source_hashes():
+        with open(os.path.join(ROOT, f)) as fh:
+            text = fh.read()
+        if re.search(re.escape(base) + r"\s*[<(]", text):
+            deps.add(f)
+    if deps:
+        deps |= {"paper_1712_01537_amd/csrc/common.h", "include/oc.h"}
+    return sorted(deps)
+
+
+def counters_path(workload):
+    return os.path.join(ROOT, "profiles", f"hbm_counters_{workload}.md")
+
+
+def load_traffic(workload, kernel):
+    """Calibrated HBM bytes per launch of `kernel` (read + write) from the
+    committed counter summary, or None when there is none for this kernel or
+    the library sources changed since the counters were taken."""
+    try:
+        with open(counters_path(workload)) as fh:
+            text = fh.read()
+    except OSError:
+        return None
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    k = rec.get("kernels", {}).get(kernel)
+    if not k:
+        return None
+    now, then = source_hashes(), rec.get("sources", {})
+    deps = kernel_sources(kernel)
+    if not deps or any(now.get(f) is None or now.get(f) != then.get(f) for f in deps):
+        return None
+    return {"read_bytes": k["fetch_bytes_per_launch"], "write_bytes": k["write_bytes_per_launch"],
+            "bytes": k["fetch_bytes_per_launch"] + k["write_bytes_per_launch"],
+            "source": os.path.relpath(counters_path(workload), ROOT)}
+
+
+def _counter_rows(d, counter):
+    """(kernel name, value) per dispatch from the counter_collection CSV files
+    under directory d."""
+    rows = []
+    for f in sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)):
+        with open(f, newline="") as fh:
+            for r in csv.DictReader(fh):
+                if r.get("Counter_Name") == counter:
+                    rows.append((int(r.get("Dispatch_Id", 0)), r["Kernel_Name"],
+                                 float(r["Counter_Value"])))
+    rows.sort()
+    return [(k, v) for _, k, v in rows]
+
+
+def _short_name(k):
+    """Kernel name with its template arguments, without namespaces of the
+    anonymous kind and without the argument list."""
+    k = k.replace("(anonymous namespace)::", "")
+    k = re.sub(r"^void ", "", k)
+    depth = 0
+    for i, ch in enumerate(k):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return k[:i].strip()
+    return k.strip()
+
+
+def summarize_counters(fetch_dir, write_dir, copy_mib, workload):
+    """Per-kernel mean FETCH_SIZE / WRITE_SIZE per dispatch (KiB, as rocprofv3
+    reports them), calibrated by the copy probe: a copy of S bytes must read S
+    and write S bytes, so bytes = counter * 1024 / (copy counter * 1024 / S)."""
+    out = {}
+    for name, d, ctr in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
+        for k, v in _counter_rows(d, ctr):
+            e = out.setdefault(_short_name(k), {}).setdefault(name, [])
+            e.append(v)
+    size = copy_mib * 2 ** 20
+    copy = [k for k in out if "neg" in k.lower() and "fetch" in out[k] and "write" in out[k]
+            and max(out[k]["fetch"]) * 1024 > 0.5 * size]
+    if not copy or size <= 0:
+        raise SystemExit("no copy-probe kernel of the given size in the counter runs")
+    ck = copy[0]
+    # the probe's largest dispatches are the copies of `size` bytes
+    cf = max(out[ck]["fetch"]) * 1024 / size
+    cw = max(out[ck]["write"]) * 1024 / size
+    kernels = {}
+    for k, v in sorted(out.items()):
+        # the bench's own input generation (torch kernels) is not the library's
+        if "fetch" not in v or "write" not in v or k == ck or k.startswith("at::"):
+            continue
+        f = sum(v["fetch"]) / len(v["fetch"]) * 1024 / cf
+        w = sum(v["write"]) / len(v["write"]) * 1024 / cw
+        kernels[k] = {"dispatches": len(v["fetch"]), "fetch_bytes_per_launch": round(f),
+                      "write_bytes_per_launch": round(w)}
+    rec = {"workload": workload, "sources": source_hashes(),
+           "copy_probe": {"kernel": ck, "bytes": size, "fetch_factor": round(cf, 4),
+                          "write_factor": round(cw, 4)},
+           "kernels": kernels}
+    print(f"Copy probe `{ck}` of {copy_mib} MiB: FETCH_SIZE reads {cf:.4f} x and WRITE_SIZE "
+          f"{cw:.4f} x the bytes copied; every figure below is divided by these factors.\n")
+    print("| kernel | dispatches | read MB / launch | write MB / launch |")
+    print("|---|---|---|---|")
+    for k, v in sorted(kernels.items(), key=lambda kv: -(kv[1]["fetch_bytes_per_launch"]
+                                                          + kv[1]["write_bytes_per_launch"])):
+        print(f"| `{k}` | {v['dispatches']} | {v['fetch_bytes_per_launch'] / 1e6:.3f} | "
+              f"{v['write_bytes_per_launch'] / 1e6:.3f} |")
+    print("\n```json\n" + json.dumps(rec, indent=1) + "\n```")
 
 
 class Step:
@@ -361,6 +510,9 @@ def cpu_baseline(synth, wl, shapes):
 
 def main():
     args = parse()
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters, args.copy_probe, args.workload)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
               f"(the path would shard by shape with one dW all-reduce per layer, not built)",
@@ -436,10 +588,14 @@ def main():
     else:
         achieved = per_launch_work / (per_launch_ms * 1e-3) / 1e9
         peak, unit = PEAK["hbm_GBps"], "GB/s"
+    traffic = load_traffic(wl.name, dominant)
     roofline = {"bound": bound, "kernel": dominant, "op": dom["op"], "achieved": round(achieved, 3),
-                "peak": peak, "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                "peak": peak, "unit": unit, "frac": round(achieved / peak, 4),
+                "traffic": traffic["bytes"] if traffic else None,
                 "launches_per_step": nper,
                 "mean_launch_us": round(per_launch_ms * 1e3, 2)}
+    if traffic:
+        roofline["traffic_detail"] = traffic
 
     if args.layers:
         for key, v in sorted(warm.items(), key=lambda kv: -kv[1]["ms"]):
@@ -448,6 +604,16 @@ def main():
                 per[name] = per.get(name, 0.0) + t / nwarm
             print(f"[bench] {key:42s} {v['ms'] / nwarm:8.3f} ms/step  "
                   + "  ".join(f"{k}:{t:.3f}" for k, t in per.items()), file=sys.stderr)
+
+    if args.copy_probe > 0:
+        n = args.copy_probe * 2 ** 20 // 4
+        src = torch.randn(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):  # an elementwise kernel (a plain copy could go to a DMA engine)
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        print(f"[bench] copy probe: 3 copies of {args.copy_probe} MiB", file=sys.stderr, flush=True)
 
     cpu = None
     if args.cpu_shapes > 0:
