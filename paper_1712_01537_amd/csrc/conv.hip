@@ -9,13 +9,15 @@
 // first-child row (or -1), so every tap is one table read plus an add: the
 // (K+1)^3 union neighbourhood of the eight siblings (Sec. 3.2, Fig. 4).
 //
-// Stride 1 runs on the matrix-core kernels of conv_mfma.hip (bf16 operands
-// widened to fp32 first, which is exact); stride 2 on the column buffers and
-// GEMMs of conv_s2.hip.  This file checks arguments, sizes the workspaces and
+// Stride 1 runs on the matrix-core kernels of conv_mfma.hip (fp32) and
+// conv_bf16.hip (bf16 with both channel counts multiples of 16; other bf16
+// shapes widen their operands to fp32, which is exact, and run the fp32
+// kernels); stride 2 on the column buffers and GEMMs of conv_s2.hip.  This file checks arguments, sizes the workspaces and
 // applies the ReLU backward ahead of the stride-1 gradients.
 #include <algorithm>
 
 #include "common.h"
+#include "conv_bf16.h"
 #include "conv_mfma.h"
 #include "conv_s2.h"
 
@@ -50,19 +52,34 @@ void bf16_to_f32(const void* in, int64_t n, float* out, hipStream_t s) {
                      (const uint16_t*)in, n, vec, out);
 }
 
-// ReLU backward: dym[e] = y[e] > 0 ? dy[e] : 0, four entries per thread.
+// fp32 value rounded to the nearest bf16 (ties to even), kept as fp32.
+__device__ __forceinline__ float round_bf16(float f) {
+  const uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return f;  // inf, NaN
+  return __uint_as_float((u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u);
+}
+
+// ReLU backward: dym[e] = y[e] > 0 ? dy[e] : 0 (y NULL: no mask), rounded to
+// bf16 when rnd != 0, four entries per thread.
 __global__ __launch_bounds__(TB) void k_relu_mask(const float* __restrict__ y,
                                                   const float* __restrict__ dy, int64_t n,
-                                                  int vec, float* __restrict__ dym) {
+                                                  int vec, int rnd, float* __restrict__ dym) {
   const int64_t e = 4 * ((int64_t)blockIdx.x * TB + threadIdx.x);
   if (e >= n) return;
   if (vec && e + 4 <= n) {  // vec: y, dy (and dym) are 16-byte aligned
-    const float4 a = *reinterpret_cast<const float4*>(y + e);
-    const float4 g = *reinterpret_cast<const float4*>(dy + e);
-    *reinterpret_cast<float4*>(dym + e) = float4{a.x > 0.f ? g.x : 0.f, a.y > 0.f ? g.y : 0.f,
-                                                 a.z > 0.f ? g.z : 0.f, a.w > 0.f ? g.w : 0.f};
+    float4 g = *reinterpret_cast<const float4*>(dy + e);
+    if (y) {
+      const float4 a = *reinterpret_cast<const float4*>(y + e);
+      g = float4{a.x > 0.f ? g.x : 0.f, a.y > 0.f ? g.y : 0.f, a.z > 0.f ? g.z : 0.f,
+                 a.w > 0.f ? g.w : 0.f};
+    }
+    if (rnd) g = float4{round_bf16(g.x), round_bf16(g.y), round_bf16(g.z), round_bf16(g.w)};
+    *reinterpret_cast<float4*>(dym + e) = g;
   } else {
-    for (int64_t i = e; i < n; ++i) dym[i] = y[i] > 0.f ? dy[i] : 0.f;
+    for (int64_t i = e; i < n && i < e + 4; ++i) {
+      const float g = y && !(y[i] > 0.f) ? 0.f : dy[i];
+      dym[i] = rnd ? round_bf16(g) : g;
+    }
   }
 }
 
@@ -104,10 +121,16 @@ size_t w32_bytes(const ConvShape& sh, int cin, int cout) {
   return oc::align256((size_t)sh.K3 * cin * cout * sizeof(float));
 }
 
+// bf16 stride-1 calls whose channel counts the bf16 matrix-core kernels take
+bool bf16_native(const ConvShape& sh, oc_dtype dt, int cin, int cout) {
+  return dt == OC_BF16 && sh.stride == 1 && oc::conv_bf16_supported(sh.K, cin, cout);
+}
+
 size_t fwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,
                     int cout) {
   if (sh.stride == 2) return oc::conv_s2_fwd_ws(t, l, cin, cout, dt == OC_BF16);
   if (sh.n_in == 0) return 0;
+  if (bf16_native(sh, dt, cin, cout)) return oc::conv_bf16_fwd_ws(sh.K, cin, cout);
   const size_t tile = oc::conv_s1_tile_ws(t, l, sh.K, cin, cout);
   return dt == OC_F32 ? tile : x32_bytes(sh, cin) + w32_bytes(sh, cin, cout) + tile;
 }
@@ -122,6 +145,7 @@ size_t bwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype
                     int cout) {
   if (sh.units == 0) return 0;
   const size_t entries = (size_t)sh.K3 * cin * cout;
+  if (bf16_native(sh, dt, cin, cout)) return oc::conv_bf16_bwd_ws(t, l, sh.K, cin, cout);
   if (sh.stride == 1) {
     // (bf16: the widened w and x,) the ReLU-masked upstream gradient, then
     // the input gradient's and the weight gradient's partial sums: the same
@@ -148,7 +172,9 @@ const char* oc_conv_kernel(const oc_octree* t, int32_t l, int32_t K, int32_t str
     return name;
   }
   if (check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_kernel") != OC_OK) return name;
-  if (stride == 1) {  // bf16 runs the fp32 kernels on widened operands
+  if (bf16_native(sh, dt, cin, cout)) {
+    oc::conv_bf16_kernel_name(K, pass, name, sizeof(name));
+  } else if (stride == 1) {  // other bf16 shapes run the fp32 kernels on widened operands
     oc::conv_s1_kernel_name(t, l, K, cin, cout, pass, name, sizeof(name));
   } else {  // several kernels and a GEMM: the pass is named
     snprintf(name, sizeof(name), "conv_s2_%s<%s>",
@@ -177,6 +203,11 @@ oc_status oc_conv_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   if (need && (!ws || ws_bytes < need))
     return oc::fail(OC_ERR_ARG, "oc_conv_fwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0, need);
   const int relu = (flags & OC_FUSE_RELU) ? 1 : 0;
+  if (bf16_native(sh, dt, cin, cout)) {
+    oc::conv_bf16_fwd(t, l, K, (const uint16_t*)x, cin, (const uint16_t*)w, cout, y, relu, ws, s);
+    OC_LAUNCH_CHECK();
+    return OC_OK;
+  }
   if (stride == 1) {
     const float *x32 = (const float*)x, *w32 = (const float*)w;
     char* rest = (char*)ws;
@@ -225,6 +256,16 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
     OC_LAUNCH_CHECK();
     return OC_OK;
   }
+  if (bf16_native(sh, dt, cin, cout)) {
+    if (sh.units == 0) {
+      if (dw) oc::fill_u32(dw, 0u, (int64_t)sh.K3 * cin * cout, s);
+    } else if (dx || dw) {
+      oc::conv_bf16_bwd(t, l, K, (const uint16_t*)x, cin, (const uint16_t*)w, cout, ym, dy, dx, dw,
+                        ws, s);
+    }
+    OC_LAUNCH_CHECK();
+    return OC_OK;
+  }
   // stride 1: matrix-core kernels
   float* wsf = (float*)ws;
   if (dt == OC_BF16 && (dx || dw)) {  // the bf16 operands widened to fp32 (exact)
@@ -237,11 +278,15 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
     wsf = (float*)((char*)ws + w32_bytes(sh, cin, cout) + x32_bytes(sh, cin));
   }
   if (dx || dw) {
-    if (ym && sh.n_out > 0) {  // dy masked once, read by both gradients
+    // dy masked once (and for bf16 rounded to bf16, the operand precision of
+    // the bf16 backward), read by both gradients
+    const int rnd = dt == OC_BF16;
+    if ((ym || rnd) && sh.n_out > 0) {
       const int64_t n = sh.n_out * (int64_t)cout;
-      const int vec = ((uintptr_t)y % 16 == 0 && (uintptr_t)dy % 16 == 0 && (uintptr_t)wsf % 16 == 0);
-      hipLaunchKernelGGL(k_relu_mask, dim3((unsigned)oc::cdiv(n, 4 * TB)), dim3(TB), 0, s, y, dy,
-                         n, vec, wsf);
+      const int vec = ((!ym || (uintptr_t)ym % 16 == 0) && (uintptr_t)dy % 16 == 0 &&
+                       (uintptr_t)wsf % 16 == 0);
+      hipLaunchKernelGGL(k_relu_mask, dim3((unsigned)oc::cdiv(n, 4 * TB)), dim3(TB), 0, s, ym, dy,
+                         n, vec, rnd, wsf);
       dy = wsf;
     }
     wsf = (float*)((char*)wsf + mask_ws_bytes(sh, cout));

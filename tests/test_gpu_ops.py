@@ -118,12 +118,57 @@ def test_conv_small_bf16(K, stride):
     dy = rng.standard_normal(yref.shape).astype(np.float32)
     dx, dw = oc.oc_conv_bwd(tree, l, K, stride, _cuda(x, torch.bfloat16), _cuda(w, torch.bfloat16), _cuda(dy))
     if stride == 1:
-        dxr = oracle.conv_bwd_data(nb, dy, w, ref.num(l))
-        dwr = oracle.conv_bwd_weight(nb, x, dy, K ** 3)
+        # the stride-1 bf16 backward multiplies dy rounded to bf16
+        dyq = bf16_round(dy)
+        dxr = oracle.conv_bwd_data(nb, dyq, w, ref.num(l))
+        dwr = oracle.conv_bwd_weight(nb, x, dyq, K ** 3)
+        assert_bf16_close(dx.cpu().numpy(), oracle.conv_bwd_data(nb, dy, w32, ref.num(l)),
+                          "dx vs fp32 oracle")
+        assert_bf16_close(dw.cpu().numpy(), oracle.conv_bwd_weight(nb, x32, dy, K ** 3),
+                          "dw vs fp32 oracle")
     else:
         dxr, dwr = oracle.conv_s2_bwd(ref, l, x, w, dy)
     assert_f32_close(dx.cpu().numpy(), dxr, "dx bf16 weights")
     assert_dw_close(dw.cpu().numpy(), dwr, "dw bf16 inputs")
+
+
+BF16_NATIVE = [  # seed, B, n, depth, K, cin, cout, relu: tiles with ragged tails, one or two
+    # 64-channel chunks of the reduction, one or two 64-column output blocks
+    (41, 2, 700, 5, 5, 64, 64, False),
+    (42, 3, 400, 4, 3, 16, 48, True),
+    (43, 1, 900, 5, 5, 80, 32, True),
+    (44, 2, 300, 4, 3, 128, 96, False),
+    (45, 1, 200, 3, 5, 32, 16, False),
+]
+
+
+@pytest.mark.parametrize("seed,B,n,depth,K,cin,cout,relu", BF16_NATIVE)
+def test_conv_bf16_matrix_core(seed, B, n, depth, K, cin, cout, relu):
+    """bf16 stride-1 shapes with channel counts that are multiples of 16 (the
+    bf16 matrix-core kernels), against the oracle on the same bf16 values."""
+    oc = _oc()
+    pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
+    ref, tree = _trees(pts, nrm, offs, depth)
+    l = depth
+    rng = np.random.default_rng(seed)
+    x = bf16_round(rng.standard_normal((ref.num(l), cin)).astype(np.float32))
+    w = bf16_round((rng.standard_normal((K ** 3, cin, cout)) / np.sqrt(K ** 3 * cin)).astype(np.float32))
+    nb = ref.neighbors(l, K)
+    pre = oracle.conv_fwd(nb, x, w)
+    print(f"[bf16 {seed}] d{l} K{K} {cin}->{cout} rows {ref.num(l)} relu {relu}", flush=True)
+    y = oc.oc_conv_fwd(tree, l, K, 1, _cuda(x, torch.bfloat16), _cuda(w, torch.bfloat16), relu=relu)
+    assert_f32_close(y.cpu().numpy(), oracle.relu_fwd(pre) if relu else pre, "y")
+    dy = _mask_ambiguous(rng.standard_normal(pre.shape).astype(np.float32), pre, relu)
+    dye = bf16_round(oracle.relu_bwd(pre, dy) if relu else dy)
+    dx, dw = oc.oc_conv_bwd(tree, l, K, 1, _cuda(x, torch.bfloat16), _cuda(w, torch.bfloat16),
+                            _cuda(dy), y=y, relu=relu)
+    assert_f32_close(dx.cpu().numpy(), oracle.conv_bwd_data(nb, dye, w, ref.num(l)), "dx")
+    rule = assert_dw_close(dw.cpu().numpy(), oracle.conv_bwd_weight(nb, x, dye, K ** 3), "dw")
+    print(f"[bf16 {seed}] dw rule: {rule}", flush=True)
+    # reproducible bit for bit
+    dx2, dw2 = oc.oc_conv_bwd(tree, l, K, 1, _cuda(x, torch.bfloat16), _cuda(w, torch.bfloat16),
+                              _cuda(dy), y=y, relu=relu)
+    assert torch.equal(dx, dx2) and torch.equal(dw, dw2)
 
 
 @pytest.mark.parametrize("seed,B,n,depth,c", [(31, 2, 500, 4, 8), (32, 3, 300, 5, 3), (33, 1, 100, 3, 32)])
@@ -210,6 +255,8 @@ def _check_conv_full(ref, tree, l, K, stride, x, w, relu, dy, tag, dtype=torch.f
     want[_sample(rng, n_in, 3000)] = True
     ent = _sample(rng, w.size, 300)
     if stride == 1:
+        if dtype == torch.bfloat16:  # the stride-1 bf16 backward multiplies dy rounded to bf16
+            dye = bf16_round(dye)
         dxr = oracle.conv_bwd_data(nb, dye, wq, n_in, want=want)
         dwr = oracle.conv_bwd_weight(nb, xq, dye, K ** 3, entries=ent)
     else:
