@@ -28,11 +28,10 @@
 // from row-major tiles (lane i of a 16-lane group receives element i % 4 of
 // the 8-byte rows read by lanes 4r + i / 4, r = 0..3), so the staged x
 // positions and dY rows keep the layout of HBM.  A workgroup owns the taps
-// of one x-offset and two (K = 5) or three (K = 3) y-offsets for every input
-// channel block,
-// the waves split those (tap, channel block) pairs and keep their dW blocks
-// in registers, and the workgroup streams a range of sibling groups, four
-// per step.  Ranges write partial sums that a second kernel adds in a fixed
+// of one x-offset and up to two (K = 5) or three (K = 3) y-offsets for every
+// input channel block, the waves split those (tap, channel block) pairs and
+// keep their dW blocks in registers, and the workgroup streams a range of
+// sibling groups, eight per step.  Ranges write partial sums that a second kernel adds in a fixed
 // order, so results do not depend on scheduling.
 //
 // LDS layouts place the 16-byte pieces (8 channels) of a position or row at
@@ -42,6 +41,7 @@
 #include "conv_bf16.h"
 
 #include <algorithm>
+#include <utility>
 
 namespace {
 
@@ -54,6 +54,13 @@ typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) void* lptr_t;
 
 constexpr int TB = 256;
+
+// Zero rows: the source of masked-off loads (absent neighbours, channels or
+// columns past the end), so that every lane of every load instruction loads
+// and each wave's count of outstanding loads is known in advance.  64 KB, so
+// that absent lanes spread over many cache lines.
+constexpr int ZROWS = 4096;
+__device__ __attribute__((aligned(16))) uint32_t g_zero_rows[ZROWS][4];
 
 __device__ __forceinline__ uint32_t lds_addr(const void* lds) {
   return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lptr_t)lds);
@@ -68,6 +75,39 @@ __device__ __forceinline__ void lds_load16(const void* src, uint32_t lds) {
 }
 // s_waitcnt vmcnt(0): all of this wave's vector memory operations are done.
 __device__ __forceinline__ void vm_wait0() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// 16-byte global load into registers, issued from inline assembly: the
+// compiler neither waits for it nor counts it, so the caller waits with
+// vm_wait_for() before the registers are read.
+__device__ __forceinline__ void gload16(v4u& r, const void* src) {
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(src) : "memory");
+}
+// Wait until at most N vector memory operations of this wave are outstanding
+// (they complete in issue order), then hand the registers w over as written.
+template <int N>
+__device__ __forceinline__ void vm_wait_for(v4u (&w)[4]) {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%4)" : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]) : "n"(N));
+}
+template <int N>
+__device__ __forceinline__ void vm_wait_n() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// f(std::integral_constant<int, 0>), ..., f(std::integral_constant<int, N-1>).
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_(f, std::make_integer_sequence<int, N>{});
+}
+// Workgroup barrier without the memory fence of __syncthreads (which would
+// wait for every outstanding global load); LDS operations are complete first.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 __device__ __forceinline__ v4f mfma_bf(v4u a, v4u b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a),
@@ -90,13 +130,13 @@ __device__ __forceinline__ uint32_t f2bf(float f) {
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-// Neighbour row of tile position (px, py, pz) of group g (positions are
-// offsets +R from the group's first child, per axis in [0, K]), or -1.
+// Neighbour row of tile position (px, py, pz) of a group whose 27-entry
+// parent-neighbour row is nb (positions are offsets +R from the group's first
+// child, per axis in [0, K]), or -1.
 template <int R>
-__device__ __forceinline__ int32_t tile_row(const int32_t* __restrict__ nbr, int64_t g, int px,
-                                            int py, int pz) {
+__device__ __forceinline__ int32_t tile_row(const int32_t* nb, int px, int py, int pz) {
   const int ux = px - R, uy = py - R, uz = pz - R;
-  const int32_t b = nbr[27 * g + ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1)];
+  const int32_t b = nb[((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1)];
   return b < 0 ? -1 : b + 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
 }
 
@@ -149,69 +189,97 @@ __global__ __launch_bounds__(TB) void k_bf_sum(const float* __restrict__ part, i
 }
 
 // ---------------------------------------------------------------------------
-// Forward / input gradient.  x [8 ngroups][kk] bf16 (kk % 8 == 0), wp as
-// produced by k_bf_wprep, out [8 ngroups][nn] fp32 (nn % 16 == 0).
-// Grid: x = tiles of 8 groups, y = blocks of 64 output channels; 512 threads.
-// Slab j of channel chunk c (64 channels) is global slab G = c S + j and
-// lives in ring buffer G % 3: 8 groups x S^2 positions x 8 pieces, piece o
-// of position (j, py, pz) at o ^ ((j&1) << 2 | (py&1) << 1 | (pz&1)).
+// Forward / input gradient, one chunk of at most 64 reduction channels.
+// x [8 ngroups][kk] bf16 (kk % 8 == 0), wp as produced by k_bf_wprep, out
+// [8 ngroups][nn] fp32 (nn % 16 == 0).  The chunk is the channel octets
+// 8 chunk .. 8 chunk + 4 HC - 1 (HC halves of 32 channels); with acc the
+// result is added to out (chunks are launched in order), relu applies
+// max(0, .) to the sum.  Grid: x = tiles of 8 groups, y = blocks of 64
+// output channels; 512 threads.  Slab j lives in ring buffer j % 3: 8 groups
+// x S^2 positions x 8 pieces, piece o of position (j, py, pz) at
+// o ^ ((j&1) << 2 | (py&1) << 1 | (pz&1)).
+// A phase (x-offset) has HC K^2 steps (tap, half).  Each wave takes the same
+// number MI of items: whole steps wave + NW i, then the leftover steps split
+// into their four row blocks (one per wave; waves left without one take an
+// empty item, whose loads are still issued).  The K phases are one unrolled
+// sequence of K MI items.  Every wave issues its global loads in a fixed
+// order and waits with counts (they complete in issue order): the slab DMA
+// at the start of a phase, the weights of item n + RW - 1 right after item n
+// is multiplied, into the register set item n - 1 used (RW sets).
 // FLIP only names the pass (the weights decide what is computed).
-template <int K, bool FLIP>
+template <int K, int HC, bool FLIP>
 __global__ __launch_bounds__(512) void k_conv_bf(const int32_t* __restrict__ nbr, int64_t ngroups,
                                                   const uint16_t* __restrict__ x, int kk,
                                                   const uint16_t* __restrict__ wp, int nn,
-                                                  float* __restrict__ out, int relu) {
+                                                  int chunk, float* __restrict__ out, int acc_in,
+                                                  int relu) {
   constexpr int R = (K - 1) / 2, S = K + 1, S2 = S * S, K2 = K * K, K3 = K2 * K;
   constexpr int GT = 8, NW = 8;
   constexpr int SLAB = GT * S2 * 8;  // 16-byte pieces of one slab buffer
   constexpr int RS = 68;             // floats per row of a reduction slot
   constexpr int RED = NW * 32 * RS;  // floats of one reduction round
   constexpr int NV = (3 * SLAB * 16 > RED * 4 ? 3 * SLAB * 16 : RED * 4) / 16;
+  constexpr int NE = HC * K2;                 // steps per phase
+  constexpr int NFULL = NE / NW, LEFT = NE % NW;
+  constexpr int MI = NFULL + (LEFT ? 1 : 0);  // items per phase and wave
+  constexpr int NI = K * MI;                  // items of the tile
+  constexpr int RW = 4;                       // weight register sets
+  constexpr int DC = (S2 + NW - 1) / NW;      // DMA instructions of a stage per wave
+  static_assert(4 * LEFT <= NW, "leftover row blocks fit the waves");
   __shared__ __attribute__((aligned(16))) v4u lds[NV];
+  __shared__ __attribute__((aligned(16))) v4u trash[64];  // destination of padding loads
+  __shared__ int32_t nbs[GT * 27];  // neighbour rows of the tile's groups
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int li = lane & 15, q = lane >> 4;
   const int64_t g0 = (int64_t)blockIdx.x * GT;
   const int n0 = blockIdx.y * 64;
-  const int KO = kk >> 3;           // channel octets of the reduction
-  const int nch = (KO + 7) >> 3;    // chunks of 64 channels
+  const int KO = kk >> 3;  // channel octets of the reduction
+  const int ob = 8 * chunk;
+  if (tid < GT * 27)
+    nbs[tid] = g0 + tid / 27 < ngroups ? nbr[27 * g0 + tid] : -1;
+  __syncthreads();
 
-  auto stage = [&](int G) {
-    const int c = G / S, j = G - c * S;
-    v4u* buf = lds + (G % 3) * SLAB;
-    for (int i = wave; i < S2; i += NW) {  // 64 pieces = 8 positions per instruction
+  // a stage is S2 DMA instructions of 64 pieces (8 positions), DC per wave;
+  // waves with one fewer issue a last load of zeros into a trash slot, so
+  // that every wave issues DC
+  auto stage = [&](int j) {
+    v4u* buf = lds + (j % 3) * SLAB;
+#pragma unroll
+    for (int k = 0; k < DC; ++k) {
+      const int i = wave + NW * k;
       const int s = i * 64 + lane;
       const int pos = s >> 3, g = pos / S2, p = pos - g * S2;
       const int py = p / S, pz = p - py * S;
-      const int o = (s & 7) ^ (((j & 1) << 2) | ((py & 1) << 1) | (pz & 1));
-      const int oc = 8 * c + o;
-      const int64_t gg = g0 + g;
-      const int32_t row = gg < ngroups && oc < KO ? tile_row<R>(nbr, gg, j, py, pz) : -1;
-      v4u* dst = buf + i * 64;
-      if (row >= 0)
-        lds_load16(x + (int64_t)row * kk + 8 * oc, lds_addr(dst));
-      else
-        dst[lane] = v4u{0u, 0u, 0u, 0u};
+      const int o = ob + ((s & 7) ^ (((j & 1) << 2) | ((py & 1) << 1) | (pz & 1)));
+      const int32_t row = i < S2 && o < KO ? tile_row<R>(nbs + 27 * g, j, py, pz) : -1;
+      const void* src = row >= 0 ? (const void*)(x + (int64_t)row * kk + 8 * o)
+                                 : (const void*)g_zero_rows[(s + 64 * (int)blockIdx.x) & (ZROWS - 1)];
+      lds_load16(src, lds_addr(i < S2 ? buf + i * 64 : trash));
     }
   };
 
   // lane (li, q) of row block b supplies row li: child li & 7 of group
   // 2b + (li >> 3), channels 8q..8q+7 of the step's 32
   const int cc = li & 7, cx = cc >> 2, cy = (cc >> 1) & 1, cz = cc & 1, gl = li >> 3;
-  auto halves = [&](int c) { return KO - 8 * c > 4 ? 2 : 1; };
-  // step e of phase ph (x-offset ph - R) of chunk c: tap (ph, e / hc), half e % hc
-  auto load_w = [&](v4u (&wv)[4], int c, int ph, int e) {
-    const int hc = halves(c);
-    const int tap2 = e / hc, h = e - tap2 * hc;
+  // item i of a phase: step e (tap e / HC, half e % HC) and the row blocks
+  // it covers: all (-1), one (0..3) or none (-2)
+  auto item_e = [&](int i) { return i < NFULL ? wave + NW * i : NFULL * NW + (wave >> 2); };
+  auto item_only = [&](int i) { return i < NFULL ? -1 : (wave < 4 * LEFT ? (wave & 3) : -2); };
+  auto load_w = [&](v4u (&wv)[4], int n) {  // item n of the tile
+    const int ph = n / MI, i = n % MI;
+    const int e = item_e(i), only = item_only(i);
+    const int tap2 = e / HC, h = e - tap2 * HC;
     const int t = ph * K2 + tap2;
-    const int o = 8 * c + 4 * h + q;
+    const int o = ob + 4 * h + q;
 #pragma unroll
     for (int nf = 0; nf < 4; ++nf) {
-      const int n = n0 + 16 * nf + li;
-      wv[nf] = (n < nn && o < KO)
-                   ? *reinterpret_cast<const v4u*>(wp + ((int64_t)(o * K3 + t) * nn + n) * 8)
-                   : v4u{0u, 0u, 0u, 0u};
+      const int nc = n0 + 16 * nf + li;
+      const void* src = only != -2 && nc < nn && o < KO
+                            ? (const void*)(wp + ((int64_t)(o * K3 + t) * nn + nc) * 8)
+                            : (const void*)g_zero_rows[lane];
+      gload16(wv[nf], src);
     }
   };
   v4f acc[4][4];
@@ -219,67 +287,78 @@ __global__ __launch_bounds__(512) void k_conv_bf(const int32_t* __restrict__ nbr
   for (int b = 0; b < 4; ++b)
 #pragma unroll
     for (int nf = 0; nf < 4; ++nf) acc[b][nf] = v4f{0.f, 0.f, 0.f, 0.f};
-  auto compute = [&](const v4u (&wv)[4], int c, int ph, int e) {
-    const int hc = halves(c);
-    const int tap2 = e / hc, h = e - tap2 * hc;
+  auto compute = [&](const v4u (&wv)[4], int n) {
+    const int ph = n / MI, i = n % MI;
+    const int e = item_e(i), only = item_only(i);
+    const int tap2 = e / HC, h = e - tap2 * HC;
     const int dyi = tap2 / K, dzi = tap2 - dyi * K;
     const int px = ph + cx, py = dyi + cy, pz = dzi + cz;
-    const v4u* buf = lds + ((c * S + px) % 3) * SLAB;
+    const v4u* buf = lds + (px % 3) * SLAB;
     const int f = ((px & 1) << 2) | ((py & 1) << 1) | (pz & 1);
     const int base = (py * S + pz) * 8 + ((4 * h + q) ^ f);
-    v4u a[4];
+    if (only == -1) {
+      v4u a[4];
 #pragma unroll
-    for (int b = 0; b < 4; ++b) a[b] = buf[(2 * b + gl) * S2 * 8 + base];
+      for (int b = 0; b < 4; ++b) a[b] = buf[(2 * b + gl) * S2 * 8 + base];
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
+      for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int nf = 0; nf < 4; ++nf) acc[b][nf] = mfma_bf(a[b], wv[nf], acc[b][nf]);
+        for (int nf = 0; nf < 4; ++nf) acc[b][nf] = mfma_bf(a[b], wv[nf], acc[b][nf]);
+    } else {
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        if (b == only) {
+          const v4u a = buf[(2 * b + gl) * S2 * 8 + base];
+#pragma unroll
+          for (int nf = 0; nf < 4; ++nf) acc[b][nf] = mfma_bf(a, wv[nf], acc[b][nf]);
+        }
+      }
+    }
   };
-  // the first step of the phase after (c, ph), if any
-  auto load_next_phase = [&](v4u (&wv)[4], int c, int ph) {
-    if (ph + 1 < K)
-      load_w(wv, c, ph + 1, wave);
-    else if (c + 1 < nch)
-      load_w(wv, c + 1, 0, wave);
+  // Load order of a wave: stage 0, stage 1, W(0 .. RW-2); at the start of
+  // phase p <= K-2, stage p+2; after item n, W(n + RW - 1).
+  // Loads younger than W(n) when item n starts: W(n+1 .. n+RW-2), and the
+  // stages of the phases p whose first item pMI lies in [n-RW+2, n].
+  struct Counts {
+    static constexpr int younger_w(int n) {
+      int c = 0;
+      for (int j = n + 1; j <= n + RW - 2; ++j) c += j < NI ? 4 : 0;
+      for (int p = 0; p <= K - 2; ++p) c += (p * MI >= n - RW + 2 && p * MI <= n) ? DC : 0;
+      return c;
+    }
+    // Loads younger than stage p+1 (the newer of the two slabs phase p reads)
+    // when phase p starts: W(0 .. RW-2) for p = 0, otherwise the weights
+    // issued after the items of phase p-1, W((p-1)MI + RW-1 .. pMI + RW-2).
+    static constexpr int younger_stage(int p) {
+      const int lo = p == 0 ? 0 : (p - 1) * MI + RW - 1;
+      int hi = p == 0 ? RW - 2 : p * MI + RW - 2;
+      hi = hi < NI - 1 ? hi : NI - 1;
+      return hi >= lo ? 4 * (hi - lo + 1) : 0;
+    }
   };
 
-  v4u wa[4], wb[4];
+  v4u W[RW][4];
   stage(0);
   stage(1);
-  load_w(wa, 0, 0, wave);
-  for (int c = 0; c < nch; ++c) {
-    const int ne = halves(c) * K2;  // steps per phase (> NW)
-    for (int ph = 0; ph < K; ++ph) {
-      vm_wait0();
-      __syncthreads();  // slabs ph and ph+1 have landed; phase ph-1 is done
-      if (ph + 2 < S)
-        stage(c * S + ph + 2);
-      else if (c + 1 < nch)
-        stage((c + 1) * S);
-      int e = wave;
-      for (; e + NW < ne; e += 2 * NW) {
-        load_w(wb, c, ph, e + NW);
-        compute(wa, c, ph, e);
-        if (e + 2 * NW < ne)
-          load_w(wa, c, ph, e + 2 * NW);
-        else
-          load_next_phase(wa, c, ph);
-        compute(wb, c, ph, e + NW);
-      }
-      if (e < ne) {
-        load_next_phase(wb, c, ph);
-        compute(wa, c, ph, e);
 #pragma unroll
-        for (int nf = 0; nf < 4; ++nf) wa[nf] = wb[nf];
-      }
+  for (int j = 0; j <= RW - 2; ++j)
+    if (j < NI) load_w(W[j], j);
+  static_for<NI>([&](auto nc) {
+    constexpr int n = decltype(nc)::value;
+    if constexpr (n % MI == 0) {
+      constexpr int p = n / MI;
+      vm_wait_n<Counts::younger_stage(p)>();  // slabs p, p+1 have landed
+      lds_barrier();                          // ... everywhere; phase p-1 is done
+      if constexpr (p + 2 < S) stage(p + 2);
     }
-    if (c + 1 < nch) {
-      __syncthreads();  // slab (c, K-1) is no longer read
-      stage((c + 1) * S + 1);
-    }
-  }
+    vm_wait_for<Counts::younger_w(n)>(W[n % RW]);
+    compute(W[n % RW], n);
+    if constexpr (n + RW - 1 < NI) load_w(W[(n + RW - 1) % RW], n + RW - 1);
+  });
+  vm_wait0();
 
-  // add the waves' tiles in wave order, 32 rows per round
+  // add the waves' tiles in wave order, 32 rows per round (and to out for
+  // a later chunk)
   __syncthreads();
   float* red = reinterpret_cast<float*>(lds);
   const int64_t nrows = 8 * ngroups;
@@ -294,17 +373,19 @@ __global__ __launch_bounds__(512) void k_conv_bf(const int32_t* __restrict__ nbr
           red[(wave * 32 + bb * 16 + 4 * q + j) * RS + 16 * nf + li] = acc[2 * rd + bb][nf][j];
     __syncthreads();
     const int r = tid >> 4, cq = (tid & 15) * 4;
-    v4f s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int w = 0; w < NW; ++w) s += *reinterpret_cast<const v4f*>(&red[(w * 32 + r) * RS + cq]);
     const int64_t row = 8 * g0 + 32 * rd + r;
     const int n = n0 + cq;
+    v4f sum = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < NW; ++w) sum += *reinterpret_cast<const v4f*>(&red[(w * 32 + r) * RS + cq]);
     if (row < nrows && n < nn) {
+      v4f* dst = reinterpret_cast<v4f*>(out + row * nn + n);
+      if (acc_in) sum = *dst + sum;
       if (relu) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) s[j] = fmaxf(s[j], 0.f);
+        for (int j = 0; j < 4; ++j) sum[j] = fmaxf(sum[j], 0.f);
       }
-      *reinterpret_cast<v4f*>(out + row * nn + n) = s;
+      *dst = sum;
     }
     __syncthreads();
   }
@@ -312,14 +393,18 @@ __global__ __launch_bounds__(512) void k_conv_bf(const int32_t* __restrict__ nbr
 
 // ---------------------------------------------------------------------------
 // Weight gradient.  x [8 ngroups][cin] bf16, dy [8 ngroups][cout] bf16
-// (cin, cout % 16 == 0).  Grid: x = units x ranges (unit = x-offset and a
-// set of up to three y-offsets, range = a contiguous run of groups), y =
-// blocks of 64 output channels, z = blocks of 64 input channels; 256 threads.
-// A unit takes the y-offsets [ya, yb) (at most 2 for K = 5, 3 for K = 3).
-// Per step of four groups the workgroup stages the x positions its taps read
-// (x-slabs dx+R, dx+R+1; y in [ya, yb]; every z) and the 32 dY rows.  x
-// piece o of box position (ix, iy, iz) sits at o ^ 2((iz + 2 iy) & 3), dY
-// piece o of row r at o ^ 2(r & 3).  part [ranges][K^3][cin][cout].
+// (cin, cout % 16 == 0).  A unit is an x-offset and a set of y-offsets
+// [ya, yb): YR of them, or fewer in a last, shorter set (K = 5: sets {0,1},
+// {2,3}, {4}).  Grid: x = work items, y = blocks of 64 output channels, z =
+// blocks of 64 input channels; 256 threads.  Items 0 .. NFU nranges - 1 are
+// (full unit, range) pairs, the others (short unit, range) pairs with half as
+// many ranges, each twice as long, so that every item does the same work;
+// a short unit's range r writes slot r of the partial sums and zeros slot
+// r + nranges / 2.  Per step of eight groups the workgroup stages the x
+// positions its taps read (x-slabs dx+R, dx+R+1; y in [ya, yb]; every z) and
+// the 64 dY rows.  x piece o of box position (ix, iy, iz) sits at
+// o ^ 2((iz + 2 iy) & 3), dY piece o of row r at o ^ 2(r & 3).
+// part [nranges][K^3][cin][cout].
 template <int K, int MAXC>
 __global__ __launch_bounds__(TB, 1) void k_conv_bf_dw(const int32_t* __restrict__ nbr,
                                                       int64_t ngroups,
@@ -327,19 +412,31 @@ __global__ __launch_bounds__(TB, 1) void k_conv_bf_dw(const int32_t* __restrict_
                                                       const uint16_t* __restrict__ dy, int cout,
                                                       int nranges, float* __restrict__ part) {
   constexpr int R = (K - 1) / 2, S = K + 1, K3 = K * K * K;
-  constexpr int YR = K == 5 ? 2 : 3;            // y-offsets per unit
-  constexpr int NSET = (K + YR - 1) / YR;       // units per x-offset
-  constexpr int MAXPOS = 2 * (YR + 1) * S;      // staged positions per group
-  constexpr int XP = 4 * MAXPOS * 8;     // pieces of the staged x (four groups)
-  constexpr int YP = 32 * 8;             // pieces of the staged dY rows
+  constexpr int YR = K == 5 ? 2 : 3;         // y-offsets of a full unit
+  constexpr int NSF = K / YR;                // full units per x-offset
+  constexpr int NFU = K * NSF;               // full units
+  constexpr int GS = 8;                      // groups per step
+  constexpr int MAXPOS = 2 * (YR + 1) * S;   // staged positions per group
+  constexpr int XP = GS * MAXPOS * 8;        // pieces of the staged x
+  constexpr int YP = GS * 8 * 8;             // pieces of the staged dY rows
   constexpr int BUF = XP + YP;
   __shared__ __attribute__((aligned(16))) v4u lds[2 * BUF];
+  __shared__ int32_t nbs[2][GS * 27];  // neighbour rows of a step's groups, two steps
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int li = lane & 15, q = lane >> 4;
-  const int unit = blockIdx.x % (K * NSET), range = blockIdx.x / (K * NSET);
-  const int dxi = unit / NSET, set = unit % NSET;
+  int dxi, set, range, nr;
+  {
+    const int b = blockIdx.x;
+    if (b < NFU * nranges) {
+      const int u = b % NFU;
+      dxi = u / NSF, set = u % NSF, range = b / NFU, nr = nranges;
+    } else {
+      const int b2 = b - NFU * nranges;
+      dxi = b2 % K, set = NSF, range = b2 / K, nr = nranges / 2;
+    }
+  }
   const int ya = YR * set, yb = ya + YR < K ? ya + YR : K;
   const int NY = yb - ya + 1;
   const int npos = 2 * NY * S;
@@ -347,21 +444,21 @@ __global__ __launch_bounds__(TB, 1) void k_conv_bf_dw(const int32_t* __restrict_
   const int c0 = blockIdx.z * 64, n0 = blockIdx.y * 64;
   const int CB = (cin - c0 < 64 ? cin - c0 : 64) / 16;
   const int ncombo = ntap * CB;
-  const int64_t gbeg = ngroups * range / nranges, gend = ngroups * (range + 1) / nranges;
-  const int nsteps = (int)((gend - gbeg + 3) / 4);
+  const int64_t gbeg = ngroups * range / nr, gend = ngroups * (range + 1) / nr;
+  const int nsteps = (int)((gend - gbeg + GS - 1) / GS);
 
   auto stage = [&](int st, v4u* buf) {
-    const int64_t gs = gbeg + 4 * (int64_t)st;
-    const int nxi = npos / 2;  // instructions of 64 pieces for the x positions
-    for (int i = wave; i < nxi + 4; i += 4) {
+    const int64_t gs = gbeg + GS * (int64_t)st;
+    const int nxi = npos;  // instructions of 64 pieces for the x positions
+    for (int i = wave; i < nxi + GS; i += 4) {
       if (i < nxi) {
         const int s = i * 64 + lane;
         const int pos = s >> 3, g = pos / npos, p = pos - g * npos;
         const int ix = p / (NY * S), rem = p - ix * (NY * S), iy = rem / S, iz = rem - iy * S;
         const int o = (s & 7) ^ (2 * ((iz + 2 * iy) & 3));
         const int ch = c0 + 8 * o;
-        const int64_t gg = gs + g;
-        const int32_t row = gg < gend && ch < cin ? tile_row<R>(nbr, gg, dxi + ix, ya + iy, iz) : -1;
+        const int32_t row =
+            ch < cin ? tile_row<R>(nbs[st & 1] + 27 * g, dxi + ix, ya + iy, iz) : -1;
         v4u* dst = buf + i * 64;
         if (row >= 0)
           lds_load16(x + (int64_t)row * cin + ch, lds_addr(dst));
@@ -389,53 +486,73 @@ __global__ __launch_bounds__(TB, 1) void k_conv_bf_dw(const int32_t* __restrict_
     for (int nb = 0; nb < 4; ++nb) acc[m][nb] = v4f{0.f, 0.f, 0.f, 0.f};
 
   // transposing loads: source lane li reads row 4h + (li >> 2) of its
-  // 16-lane group's eight, channels 4 (li & 3).. of the 16-channel block
+  // 16-lane group's eight, channels 4 (li & 3).. of the 16-channel block;
+  // the 16-lane group q takes group 4 sub + q of the step
   const int r4 = li >> 2, tq = li & 3;
   auto compute = [&](const v4u* buf) {
-    v4u bfr[4];
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
-      v4s hv[2];
+    for (int sub = 0; sub < GS / 4; ++sub) {
+      const int gq = 4 * sub + q;
+      v4u bfr[4];
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int rl = 8 * q + 4 * hh + r4;
-        const int o = 2 * nb + (tq >> 1);
-        hv[hh] = lds_tr16(buf, (XP + rl * 8 + (o ^ (2 * (rl & 3)))) * 16 + (tq & 1) * 8);
-      }
-      bfr[nb] = join(hv[0], hv[1]);
-    }
-#pragma unroll
-    for (int mi = 0; mi < MAXC; ++mi) {
-      const int m = wave + 4 * mi;
-      if (m < ncombo) {
-        const int it = m / CB, cb = m - it * CB;
-        const int dyl = it / K, dzi = it - dyl * K;
+      for (int nb = 0; nb < 4; ++nb) {
         v4s hv[2];
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {  // child 4 hh + r4 of group q
-          const int iy = dyl + (r4 >> 1), iz = dzi + (r4 & 1);
-          const int p = (hh * NY + iy) * S + iz;
-          const int o = 2 * cb + (tq >> 1);
-          hv[hh] = lds_tr16(buf, ((q * npos + p) * 8 + (o ^ (2 * ((iz + 2 * iy) & 3)))) * 16 +
-                                     (tq & 1) * 8);
+        for (int hh = 0; hh < 2; ++hh) {
+          const int rl = 8 * gq + 4 * hh + r4;
+          const int o = 2 * nb + (tq >> 1);
+          hv[hh] = lds_tr16(buf, (XP + rl * 8 + (o ^ (2 * (rl & 3)))) * 16 + (tq & 1) * 8);
         }
-        const v4u a = join(hv[0], hv[1]);
+        bfr[nb] = join(hv[0], hv[1]);
+      }
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) acc[mi][nb] = mfma_bf(a, bfr[nb], acc[mi][nb]);
+      for (int mi = 0; mi < MAXC; ++mi) {
+        const int m = wave + 4 * mi;
+        if (m < ncombo) {
+          const int it = m / CB, cb = m - it * CB;
+          const int dyl = it / K, dzi = it - dyl * K;
+          v4s hv[2];
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {  // child 4 hh + r4 of group gq
+            const int iy = dyl + (r4 >> 1), iz = dzi + (r4 & 1);
+            const int p = (hh * NY + iy) * S + iz;
+            const int o = 2 * cb + (tq >> 1);
+            hv[hh] = lds_tr16(buf, ((gq * npos + p) * 8 + (o ^ (2 * ((iz + 2 * iy) & 3)))) * 16 +
+                                       (tq & 1) * 8);
+          }
+          const v4u a = join(hv[0], hv[1]);
+#pragma unroll
+          for (int nb = 0; nb < 4; ++nb) acc[mi][nb] = mfma_bf(a, bfr[nb], acc[mi][nb]);
+        }
       }
     }
   };
 
+  // neighbour rows of step st's groups (-1 past the range) go to nbs[st & 1];
+  // those of step st+2 are loaded into a register during step st and stored
+  // at its end, when step st's rows are no longer read
+  auto nb_entry = [&](int st) -> int32_t {
+    const int64_t gg = gbeg + GS * (int64_t)st + tid / 27;
+    return tid < GS * 27 && gg < gend ? nbr[27 * gg + tid % 27] : -1;
+  };
+  if (tid < GS * 27) {
+    nbs[0][tid] = nb_entry(0);
+    nbs[1][tid] = nb_entry(1);
+  }
+  __syncthreads();
   if (nsteps > 0) stage(0, lds);
   for (int st = 0; st < nsteps; ++st) {
     vm_wait0();
     __syncthreads();  // step st has landed; step st-1 is no longer read
+    const int32_t nb2 = nb_entry(st + 2);
     if (st + 1 < nsteps) stage(st + 1, lds + ((st + 1) & 1) * BUF);
     compute(lds + (st & 1) * BUF);
+    if (tid < GS * 27) nbs[st & 1][tid] = nb2;
   }
 
   // partial dW of this range: lane (li, q), accumulator j holds input channel
   // c0 + 16 cb + 4q + j, output channel n0 + 16 nb + li
+  const bool shortu = nr != nranges;
 #pragma unroll
   for (int mi = 0; mi < MAXC; ++mi) {
     const int m = wave + 4 * mi;
@@ -443,12 +560,17 @@ __global__ __launch_bounds__(TB, 1) void k_conv_bf_dw(const int32_t* __restrict_
       const int it = m / CB, cb = m - it * CB;
       const int t = (dxi * K + ya + it / K) * K + it % K;
       float* dst = part + ((int64_t)range * K3 + t) * cin * cout;
+      float* dz = part + ((int64_t)(range + nr) * K3 + t) * cin * cout;
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) {
         const int n = n0 + 16 * nb + li;
         if (n < cout) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) dst[(int64_t)(c0 + 16 * cb + 4 * q + j) * cout + n] = acc[mi][nb][j];
+          for (int j = 0; j < 4; ++j) {
+            const int64_t e = (int64_t)(c0 + 16 * cb + 4 * q + j) * cout + n;
+            dst[e] = acc[mi][nb][j];
+            if (shortu) dz[e] = 0.f;
+          }
         }
       }
     }
@@ -459,14 +581,19 @@ inline unsigned blocks(int64_t n, int per) { return (unsigned)oc::cdiv(n, per); 
 
 size_t wp_bytes(int K, int kk, int nn) { return oc::align256((size_t)kk * K * K * K * nn * 2); }
 
-int dw_units(int K) { return K == 5 ? 5 * 3 : 3; }  // x-offsets x sets of y-offsets
+// Work items of the weight gradient for nranges ranges: K = 5 has 10 full
+// units and 5 short ones (half as many ranges), K = 3 three full units.
+int dw_items(int K, int nranges) { return K == 5 ? 10 * nranges + 5 * (nranges / 2) : 3 * nranges; }
 
 int dw_ranges(const oc_octree* t, int l, int K, int cin, int cout) {
   const int64_t G = t->M[l - 1];
-  const int per = dw_units(K) * (int)oc::cdiv(cout, 64) * (int)oc::cdiv(cin, 64);
-  int64_t r = oc::cdiv(2 * (int64_t)oc::cu_count(), per);
-  r = std::min<int64_t>(r, std::max<int64_t>(1, oc::cdiv(G, 16)));  // 16+ groups per range
-  return (int)std::max<int64_t>(1, r);
+  const int64_t per = oc::cdiv(cout, 64) * oc::cdiv(cin, 64);
+  // about two items per compute unit (one resident at a time), at least 16
+  // groups per range; K = 5 needs an even count
+  const int64_t full = K == 5 ? 25 : 6;  // items per 2 ranges
+  int64_t r = 2 * std::max<int64_t>(1, (2 * (int64_t)oc::cu_count()) / (full * per));
+  r = std::min<int64_t>(r, std::max<int64_t>(2, 2 * (G / 32)));
+  return (int)std::max<int64_t>(2, r);
 }
 
 void wprep(const uint16_t* w, int K, int kk, int nn, int flip, uint16_t* wp, hipStream_t s) {
@@ -475,17 +602,41 @@ void wprep(const uint16_t* w, int K, int kk, int nn, int flip, uint16_t* wp, hip
                      kk, nn, flip, wp);
 }
 
+template <int K, int HC, bool FLIP>
+void launch_chunk(const oc_octree* t, int l, const uint16_t* x, int kk, const uint16_t* wp, int nn,
+                  int chunk, float* out, int acc_in, int relu, bool main, hipStream_t s) {
+  const int64_t G = t->M[l - 1];
+  const dim3 grid(blocks(G, 8), blocks(nn, 64));
+  const auto kern = k_conv_bf<K, HC, FLIP>;
+  if (main)
+    oc::launch_main(kern, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, kk, wp, nn, chunk,
+                    out, acc_in, relu);
+  else
+    hipLaunchKernelGGL(kern, grid, dim3(512), 0, s, (const int32_t*)t->nbr[l], G, x, kk, wp, nn,
+                       chunk, out, acc_in, relu);
+}
+
+// out = conv over kk reduction channels, in chunks of 64 added in order; the
+// first chunk's launch carries the profiling events.
 template <bool FLIP>
 void launch_conv(const oc_octree* t, int l, int K, const uint16_t* x, int kk, const uint16_t* wp,
                  int nn, float* out, int relu, hipStream_t s) {
-  const int64_t G = t->M[l - 1];
-  const dim3 grid(blocks(G, 8), blocks(nn, 64));
-  if (K == 5)
-    oc::launch_main(k_conv_bf<5, FLIP>, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, kk,
-                    wp, nn, out, relu);
-  else
-    oc::launch_main(k_conv_bf<3, FLIP>, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, kk,
-                    wp, nn, out, relu);
+  const int nch = (int)oc::cdiv(kk, 64);
+  for (int c = 0; c < nch; ++c) {
+    const bool two = kk - 64 * c > 32;  // the chunk has a second half of 32 channels
+    const int acc_in = c > 0, r = c + 1 == nch ? relu : 0;
+    if (K == 5) {
+      if (two)
+        launch_chunk<5, 2, FLIP>(t, l, x, kk, wp, nn, c, out, acc_in, r, c == 0, s);
+      else
+        launch_chunk<5, 1, FLIP>(t, l, x, kk, wp, nn, c, out, acc_in, r, c == 0, s);
+    } else {
+      if (two)
+        launch_chunk<3, 2, FLIP>(t, l, x, kk, wp, nn, c, out, acc_in, r, c == 0, s);
+      else
+        launch_chunk<3, 1, FLIP>(t, l, x, kk, wp, nn, c, out, acc_in, r, c == 0, s);
+    }
+  }
 }
 
 }  // namespace
@@ -496,11 +647,12 @@ bool conv_bf16_supported(int K, int cin, int cout) {
   return (K == 3 || K == 5) && cin % 16 == 0 && cout % 16 == 0;
 }
 
-void conv_bf16_kernel_name(int K, int pass, char* buf, size_t n) {
+void conv_bf16_kernel_name(int K, int cin, int cout, int pass, char* buf, size_t n) {
+  const int kk = pass == 1 ? cout : cin;  // reduction channels of the first chunk
   if (pass == 2)
     snprintf(buf, n, "k_conv_bf_dw<%d, %d>", K, K == 5 ? 10 : 9);
   else
-    snprintf(buf, n, "k_conv_bf<%d, %s>", K, pass == 1 ? "true" : "false");
+    snprintf(buf, n, "k_conv_bf<%d, %d, %s>", K, kk > 32 ? 2 : 1, pass == 1 ? "true" : "false");
 }
 
 size_t conv_bf16_fwd_ws(int K, int cin, int cout) { return wp_bytes(K, cin, cout); }
@@ -539,7 +691,7 @@ void conv_bf16_bwd(const oc_octree* t, int l, int K, const uint16_t* x, int cin,
   if (dw) {
     const int K3 = K * K * K;
     const int nr = dw_ranges(t, l, K, cin, cout);
-    const dim3 grid((unsigned)(dw_units(K) * nr), blocks(cout, 64), blocks(cin, 64));
+    const dim3 grid((unsigned)dw_items(K, nr), blocks(cout, 64), blocks(cin, 64));
     if (K == 5)
       launch_main(k_conv_bf_dw<5, 10>, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, cin,
                   dy16, cout, nr, part);
