@@ -406,7 +406,7 @@ __global__ __launch_bounds__(512) void k_conv_bf(const int32_t* __restrict__ nbr
 // o ^ 2((iz + 2 iy) & 3), dY piece o of row r at o ^ 2(r & 3).
 // part [nranges][K^3][cin][cout].
 template <int K, int MAXC>
-__global__ __launch_bounds__(TB, 1) void k_conv_bf_dw(const int32_t* __restrict__ nbr,
+__global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ nbr,
                                                       int64_t ngroups,
                                                       const uint16_t* __restrict__ x, int cin,
                                                       const uint16_t* __restrict__ dy, int cout,
@@ -420,6 +420,7 @@ __global__ __launch_bounds__(TB, 1) void k_conv_bf_dw(const int32_t* __restrict_
   constexpr int XP = GS * MAXPOS * 8;        // pieces of the staged x
   constexpr int YP = GS * 8 * 8;             // pieces of the staged dY rows
   constexpr int BUF = XP + YP;
+  constexpr int NW = 8;                      // waves
   __shared__ __attribute__((aligned(16))) v4u lds[2 * BUF];
   __shared__ int32_t nbs[2][GS * 27];  // neighbour rows of a step's groups, two steps
 
@@ -450,7 +451,7 @@ __global__ __launch_bounds__(TB, 1) void k_conv_bf_dw(const int32_t* __restrict_
   auto stage = [&](int st, v4u* buf) {
     const int64_t gs = gbeg + GS * (int64_t)st;
     const int nxi = npos;  // instructions of 64 pieces for the x positions
-    for (int i = wave; i < nxi + GS; i += 4) {
+    for (int i = wave; i < nxi + GS; i += NW) {
       if (i < nxi) {
         const int s = i * 64 + lane;
         const int pos = s >> 3, g = pos / npos, p = pos - g * npos;
@@ -507,7 +508,7 @@ __global__ __launch_bounds__(TB, 1) void k_conv_bf_dw(const int32_t* __restrict_
       }
 #pragma unroll
       for (int mi = 0; mi < MAXC; ++mi) {
-        const int m = wave + 4 * mi;
+        const int m = wave + NW * mi;
         if (m < ncombo) {
           const int it = m / CB, cb = m - it * CB;
           const int dyl = it / K, dzi = it - dyl * K;
@@ -555,7 +556,7 @@ __global__ __launch_bounds__(TB, 1) void k_conv_bf_dw(const int32_t* __restrict_
   const bool shortu = nr != nranges;
 #pragma unroll
   for (int mi = 0; mi < MAXC; ++mi) {
-    const int m = wave + 4 * mi;
+    const int m = wave + NW * mi;
     if (m < ncombo) {
       const int it = m / CB, cb = m - it * CB;
       const int t = (dxi * K + ya + it / K) * K + it % K;
@@ -650,7 +651,7 @@ bool conv_bf16_supported(int K, int cin, int cout) {
 void conv_bf16_kernel_name(int K, int cin, int cout, int pass, char* buf, size_t n) {
   const int kk = pass == 1 ? cout : cin;  // reduction channels of the first chunk
   if (pass == 2)
-    snprintf(buf, n, "k_conv_bf_dw<%d, %d>", K, K == 5 ? 10 : 9);
+    snprintf(buf, n, "k_conv_bf_dw<%d, 5>", K);
   else
     snprintf(buf, n, "k_conv_bf<%d, %d, %s>", K, kk > 32 ? 2 : 1, pass == 1 ? "true" : "false");
 }
@@ -693,10 +694,10 @@ void conv_bf16_bwd(const oc_octree* t, int l, int K, const uint16_t* x, int cin,
     const int nr = dw_ranges(t, l, K, cin, cout);
     const dim3 grid((unsigned)dw_items(K, nr), blocks(cout, 64), blocks(cin, 64));
     if (K == 5)
-      launch_main(k_conv_bf_dw<5, 10>, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, cin,
+      launch_main(k_conv_bf_dw<5, 5>, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, cin,
                   dy16, cout, nr, part);
     else
-      launch_main(k_conv_bf_dw<3, 9>, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, cin,
+      launch_main(k_conv_bf_dw<3, 5>, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, cin,
                   dy16, cout, nr, part);
     const int64_t E = (int64_t)K3 * cin * cout;
     hipLaunchKernelGGL(k_bf_sum, dim3(blocks(E, 4 * TB)), dim3(TB), 0, s, part, nr, E, dw);
