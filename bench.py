@@ -35,7 +35,8 @@ The printed JSON line reports:
                  for a plain device copy of known size; taken from
                  profiles/hbm_counters_<workload>.md, and null when a source
                  file that defines or launches the kernel (or the shared
-                 header) differs from the one the counters were taken on.
+                 internal header) differs from the one the counters were
+                 taken on.
 
 Counter summary: python bench.py --summarize-counters FETCH_DIR WRITE_DIR
   --copy-probe MIB --workload NAME reads the counter_collection CSV files of
@@ -112,7 +113,7 @@ def source_hashes():
 
 def kernel_sources(kernel):
     """Source files a kernel's code depends on: the files that define or launch
-    it (its base name followed by '<' or '('), the shared header and the ABI."""
+    it (its base name followed by '<' or '(') and the shared header."""
     base = kernel.split("<")[0]
     deps = set()
     for f in source_hashes():
@@ -121,7 +122,7 @@ def kernel_sources(kernel):
         if re.search(re.escape(base) + r"\s*[<(]", text):
             deps.add(f)
     if deps:
-        deps |= {"paper_1712_01537_amd/csrc/common.h", "include/oc.h"}
+        deps.add("paper_1712_01537_amd/csrc/common.h")
     return sorted(deps)
 
 
