@@ -226,17 +226,18 @@ size_t oc_conv_bwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize
  * forward).  Arguments as oc_conv_fwd, plus
  *   y    dev f32 [N_out][cout], the forward output, read only when flags has
  *        OC_FUSE_RELU (then dy is masked with [y > 0]); may be NULL otherwise.
- *   dy   dev f32 [N_out][cout] upstream gradient.  OC_BF16, stride 1: the
+ *   dy   dev f32 [N_out][cout] upstream gradient.  OC_BF16: the
  *        matrix-core operand is dy (after the ReLU mask) rounded to bf16,
  *        nearest-even; dx and dw are the fp32-accumulated products of those
- *        bf16 values with the bf16 w and x.  Stride 2 uses dy in fp32.
+ *        bf16 values with the bf16 w and x.
  *   dx   dev f32 [N_l][cin] or NULL: gradient w.r.t. x (overwritten).
  *   dw   dev f32 [K^3][cin][cout] or NULL: gradient w.r.t. w (overwritten).
  *   ws   dev workspace of at least oc_conv_bwd_workspace() bytes.
  * Deterministic: no floating-point atomics; repeated calls give identical
  * bits.  The stride-2 workspace holds the per-group upstream gradient and
- * either the column-buffer gradient of every group (input gradient) or a
- * column-buffer chunk (weight gradient). */
+ * either the gathered upstream gradients of every group's eight parent-offset
+ * neighbours with the expanded weight (input gradient) or a column-buffer
+ * chunk (weight gradient). */
 oc_status oc_conv_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
                       oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
                       const float* y, const float* dy, float* dx, float* dw, void* ws,

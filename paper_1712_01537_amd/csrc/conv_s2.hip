@@ -6,14 +6,19 @@
 // (0 for an absent neighbour; only parent offsets {-1,0}^3 are reached from
 // child 0), a library GEMM multiplies it by W viewed as [27 Cin][Cout], and
 // a second kernel moves each group's row to its parent's row.
-//   input gradient: dCol = dY_g W^T (GEMM), then dX[j] = sum of the dCol
-//     entries whose tap reads j (gather form of col2im, no atomics);
 //   weight gradient: dW = Col^T dY_g (GEMM over the groups, in chunks added
-//     in a fixed order through the GEMM's beta).
+//     in a fixed order through the GEMM's beta);
+//   input gradient: input row 8h + c (child c of group h) is read by the
+//     groups at parent offsets o in {0,1}^3 from h's parent with o_a = 0
+//     where c_a = 0, through tap d = c - 2o.  So the eight rows of group h
+//     are one product: dX[8h..8h+7] = D[h] Wx with D[h][o][:] = dY_g of the
+//     group at offset o (0 if absent) and the expanded weight
+//     Wx[o][co][c][ci] = W[c - 2o][ci][co] (0 where c - 2o leaves {-1,0,1}^3):
+//     a gather and one GEMM whose output is dX itself, no atomics.
 // dY_g[g] = dY[row of g's parent], masked by [y > 0] when the forward applied
-// a ReLU.  bf16: the forward multiplies bf16 Col and W with fp32
-// accumulation (exact products); the backward widens to fp32 (the upstream
-// gradient is fp32).  GEMM atomics are disabled, so results are bit-for-bit
+// a ReLU.  bf16: every GEMM multiplies bf16 operands with fp32 accumulation;
+// the backward's dY_g is rounded to bf16 (nearest even), like the stride-1
+// backward.  GEMM atomics are disabled, so results are bit-for-bit
 // reproducible.
 #include <mutex>
 
@@ -30,90 +35,182 @@ constexpr size_t COL_CAP = size_t(256) << 20;  // bytes of one column-buffer chu
 __device__ __forceinline__ float to_f(float v) { return v; }
 __device__ __forceinline__ float to_f(uint16_t v) { return __uint_as_float((uint32_t)v << 16); }
 
-// Column buffer of groups g0 .. g0+ng-1: col[g-g0][k][c], four channels per
-// thread; TI -> TO is a copy or an exact bf16 -> fp32 widening.
-template <typename TI, typename TO>
-__global__ __launch_bounds__(TB) void k_s2_col(const int32_t* __restrict__ nbr, int64_t g0,
-                                               int64_t ng, const TI* __restrict__ x, int cin,
-                                               TO* __restrict__ col) {
-  const int c4n = (cin + 3) / 4;
-  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (t >= ng * 27 * c4n) return;
-  const int c4 = (int)(t % c4n);
-  const int k = (int)((t / c4n) % 27);
-  const int64_t gi = t / ((int64_t)27 * c4n);
-  const int dx = k / 9 - 1, dy = (k / 3) % 3 - 1, dz = k % 3 - 1;  // child 0 + d
-  const int32_t base = nbr[27 * (g0 + gi) + ((dx >> 1) + 1) * 9 + ((dy >> 1) + 1) * 3 + ((dz >> 1) + 1)];
-  const int32_t src = base < 0 ? -1 : base + 4 * (dx & 1) + 2 * (dy & 1) + (dz & 1);
-  TO* o = col + (gi * 27 + k) * cin + 4 * c4;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (4 * c4 + j >= cin) break;
-    if constexpr (sizeof(TI) == sizeof(TO)) {
-      o[j] = src < 0 ? TO(0) : x[(int64_t)src * cin + 4 * c4 + j];
-    } else {
-      o[j] = src < 0 ? 0.f : to_f(x[(int64_t)src * cin + 4 * c4 + j]);
-    }
-  }
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+  return (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
 }
 
-// y[i] (depth l-1) = label L > 0 ? yg[L-1] : 0, ReLU applied if relu.
+// Row of x that tap k of group g reads (child 0 + d), or -1.
+__device__ __forceinline__ int32_t s2_src(const int32_t* __restrict__ nbr, int64_t g, int k) {
+  const int dx = k / 9 - 1, dy = (k / 3) % 3 - 1, dz = k % 3 - 1;
+  const int32_t base = nbr[27 * g + ((dx >> 1) + 1) * 9 + ((dy >> 1) + 1) * 3 + ((dz >> 1) + 1)];
+  return base < 0 ? -1 : base + 4 * (dx & 1) + 2 * (dy & 1) + (dz & 1);
+}
+
+// Column buffer of groups g0 .. g0+ng-1: col[g-g0][k][:] = x[src][:] (T = fp32
+// or bf16), one 16-byte piece per thread; rows of rb bytes, rb % 16 == 0.
+template <typename T>
+__global__ __launch_bounds__(TB) void k_s2_col(const int32_t* __restrict__ nbr, int64_t g0,
+                                               int64_t ng, const T* __restrict__ x, int rb,
+                                               T* __restrict__ col) {
+  const int np = rb / 16;
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= ng * 27 * np) return;
+  const int pc = (int)(t % np);
+  const int64_t gk = t / np;  // (g - g0) * 27 + k
+  const int32_t src = s2_src(nbr, g0 + gk / 27, (int)(gk % 27));
+  uint4 v = {0u, 0u, 0u, 0u};
+  if (src >= 0) v = *reinterpret_cast<const uint4*>((const char*)x + (int64_t)src * rb + 16 * pc);
+  *reinterpret_cast<uint4*>((char*)col + gk * rb + 16 * pc) = v;
+}
+
+// Element-wise fallback for rows that are not a multiple of 16 bytes.
+template <typename T>
+__global__ __launch_bounds__(TB) void k_s2_col1(const int32_t* __restrict__ nbr, int64_t g0,
+                                                int64_t ng, const T* __restrict__ x, int cin,
+                                                T* __restrict__ col) {
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= ng * 27 * cin) return;
+  const int c = (int)(t % cin);
+  const int64_t gk = t / cin;
+  const int32_t src = s2_src(nbr, g0 + gk / 27, (int)(gk % 27));
+  col[t] = src < 0 ? T(0) : x[(int64_t)src * cin + c];
+}
+
+// y[i] (depth l-1) = label L > 0 ? yg[L-1] : 0, ReLU applied if relu; four
+// channels per thread (cout % 4 == 0).
 __global__ __launch_bounds__(TB) void k_s2_rows_out(const int32_t* __restrict__ labels,
                                                     int64_t n_out, const float* __restrict__ yg,
                                                     int cout, int relu, float* __restrict__ y) {
+  const int c4n = cout / 4;
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= n_out * c4n) return;
+  const int64_t i = t / c4n;
+  const int c = 4 * (int)(t - i * c4n);
+  const int32_t L = labels[i];
+  float4 v = {0.f, 0.f, 0.f, 0.f};
+  if (L > 0) v = *reinterpret_cast<const float4*>(yg + (int64_t)(L - 1) * cout + c);
+  if (relu) v = float4{fmaxf(v.x, 0.f), fmaxf(v.y, 0.f), fmaxf(v.z, 0.f), fmaxf(v.w, 0.f)};
+  *reinterpret_cast<float4*>(y + i * cout + c) = v;
+}
+
+// dyg[g] = dy[rows[g]], zero where ym[rows[g]] <= 0 (ym: the forward output
+// through a fused ReLU, or null); T = bf16 rounds to nearest even.  Four
+// channels per thread (cout % 4 == 0).
+template <typename T>
+__global__ __launch_bounds__(TB) void k_s2_dy_rows(const int32_t* __restrict__ rows, int64_t ng,
+                                                   const float* __restrict__ dy,
+                                                   const float* __restrict__ ym, int cout,
+                                                   T* __restrict__ dyg) {
+  const int c4n = cout / 4;
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= ng * c4n) return;
+  const int64_t g = t / c4n;
+  const int c = 4 * (int)(t - g * c4n);
+  const int64_t src = (int64_t)rows[g] * cout + c;
+  float4 v = *reinterpret_cast<const float4*>(dy + src);
+  if (ym) {
+    const float4 m = *reinterpret_cast<const float4*>(ym + src);
+    v = float4{m.x > 0.f ? v.x : 0.f, m.y > 0.f ? v.y : 0.f, m.z > 0.f ? v.z : 0.f,
+               m.w > 0.f ? v.w : 0.f};
+  }
+  T* o = dyg + g * cout + c;
+  if constexpr (sizeof(T) == 2) {
+    *reinterpret_cast<uint2*>(o) = uint2{bf16_rne(v.x) | ((uint32_t)bf16_rne(v.y) << 16),
+                                         bf16_rne(v.z) | ((uint32_t)bf16_rne(v.w) << 16)};
+  } else {
+    *reinterpret_cast<float4*>(o) = v;
+  }
+}
+
+// Expanded weight of the input gradient: wx[(o cout + co) 8 cin + c cin + ci]
+// = W[c - 2o][ci][co] where c - 2o lies in {-1,0,1}^3 per axis, else 0
+// (o, c: parent offset and child, x-bit 4, y-bit 2, z-bit 1).
+template <typename T>
+__global__ __launch_bounds__(TB) void k_s2_wx(const T* __restrict__ w, int cin, int cout,
+                                              T* __restrict__ wx) {
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  const int64_t n = (int64_t)64 * cin * cout;
+  if (t >= n) return;
+  const int ci = (int)(t % cin);
+  const int c = (int)((t / cin) % 8);
+  const int co = (int)((t / (8 * cin)) % cout);
+  const int o = (int)(t / ((int64_t)8 * cin * cout));
+  int k = 0;
+  bool ok = true;
+#pragma unroll
+  for (int a = 2; a >= 0; --a) {
+    const int d = ((c >> a) & 1) - 2 * ((o >> a) & 1);
+    ok = ok && d >= -1;
+    k = 3 * k + (d + 1);
+  }
+  wx[t] = ok ? w[((int64_t)k * cin + ci) * cout + co] : T(0);
+}
+
+// D[h][o][:] = dyg[group of the parent neighbour at offset o in {0,1}^3] (0
+// if absent), one 16-byte piece per thread; rows of rb bytes, rb % 16 == 0.
+template <typename T>
+__global__ __launch_bounds__(TB) void k_s2_dgather(const int32_t* __restrict__ nbr, int64_t G,
+                                                   const T* __restrict__ dyg, int rb,
+                                                   T* __restrict__ D) {
+  const int np = rb / 16;
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= G * 8 * np) return;
+  const int pc = (int)(t % np);
+  const int64_t ho = t / np;
+  const int64_t h = ho / 8;
+  const int o = (int)(ho % 8);
+  const int32_t f = nbr[27 * h + ((o >> 2) + 1) * 9 + (((o >> 1) & 1) + 1) * 3 + ((o & 1) + 1)];
+  uint4 v = {0u, 0u, 0u, 0u};
+  if (f >= 0) v = *reinterpret_cast<const uint4*>((const char*)dyg + (int64_t)(f >> 3) * rb + 16 * pc);
+  *reinterpret_cast<uint4*>((char*)D + ho * rb + 16 * pc) = v;
+}
+
+// Element-wise forms of k_s2_rows_out, k_s2_dy_rows and k_s2_dgather for
+// channel counts or pointers that do not allow 16-byte accesses.
+__global__ __launch_bounds__(TB) void k_s2_rows_out1(const int32_t* __restrict__ labels,
+                                                     int64_t n_out, const float* __restrict__ yg,
+                                                     int cout, int relu, float* __restrict__ y) {
   const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
   if (t >= n_out * cout) return;
   const int64_t i = t / cout;
   const int c = (int)(t - i * cout);
   const int32_t L = labels[i];
-  float v = L > 0 ? yg[(int64_t)(L - 1) * cout + c] : 0.f;
+  const float v = L > 0 ? yg[(int64_t)(L - 1) * cout + c] : 0.f;
   y[t] = relu ? fmaxf(v, 0.f) : v;
 }
 
-// dyg[g] = dy[rows[g]], zero where ym[rows[g]] <= 0 (ym: the forward output
-// through a fused ReLU, or null).
-__global__ __launch_bounds__(TB) void k_s2_dy_rows(const int32_t* __restrict__ rows, int64_t ng,
-                                                   const float* __restrict__ dy,
-                                                   const float* __restrict__ ym, int cout,
-                                                   float* __restrict__ dyg) {
+template <typename T>
+__global__ __launch_bounds__(TB) void k_s2_dy_rows1(const int32_t* __restrict__ rows, int64_t ng,
+                                                    const float* __restrict__ dy,
+                                                    const float* __restrict__ ym, int cout,
+                                                    T* __restrict__ dyg) {
   const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
   if (t >= ng * cout) return;
   const int64_t g = t / cout;
   const int c = (int)(t - g * cout);
   const int64_t src = (int64_t)rows[g] * cout + c;
-  const float v = dy[src];
-  dyg[t] = (ym && !(ym[src] > 0.f)) ? 0.f : v;
+  const float v = (ym && !(ym[src] > 0.f)) ? 0.f : dy[src];
+  if constexpr (sizeof(T) == 2)
+    dyg[t] = bf16_rne(v);
+  else
+    dyg[t] = v;
 }
 
-// dx[j][c] for input row j = 8h + c' (child c' of group h): the outputs whose
-// first child sees j sit at parent offsets p with p_a in {0} when c'_a = 0 and
-// {0, 1} when c'_a = 1 (from h's parent), reading j through tap d = c' - 2p.
-__global__ __launch_bounds__(TB) void k_s2_col2im(const int32_t* __restrict__ nbr, int64_t n_in,
-                                                  const float* __restrict__ dcol, int cin,
-                                                  float* __restrict__ dx) {
+template <typename T>
+__global__ __launch_bounds__(TB) void k_s2_dgather1(const int32_t* __restrict__ nbr, int64_t G,
+                                                    const T* __restrict__ dyg, int cout,
+                                                    T* __restrict__ D) {
   const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (t >= n_in * cin) return;
-  const int64_t j = t / cin;
-  const int ci = (int)(t - j * cin);
-  const int32_t* nb = nbr + 27 * (j >> 3);
-  const int c = (int)(j & 7);
-  const int cx = c >> 2, cy = (c >> 1) & 1, cz = c & 1;
-  float acc = 0.f;
-  for (int px = 0; px <= cx; ++px)
-    for (int py = 0; py <= cy; ++py)
-      for (int pz = 0; pz <= cz; ++pz) {
-        const int32_t f = nb[(px + 1) * 9 + (py + 1) * 3 + (pz + 1)];
-        if (f < 0) continue;
-        const int k = ((cx - 2 * px + 1) * 3 + (cy - 2 * py + 1)) * 3 + (cz - 2 * pz + 1);
-        acc += dcol[((int64_t)(f >> 3) * 27 + k) * cin + ci];
-      }
-  dx[t] = acc;
-}
-
-__global__ __launch_bounds__(TB) void k_s2_widen(const uint16_t* __restrict__ in, int64_t n,
-                                                 float* __restrict__ out) {
-  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (t < n) out[t] = __uint_as_float((uint32_t)in[t] << 16);
+  if (t >= G * 8 * cout) return;
+  const int c = (int)(t % cout);
+  const int64_t ho = t / cout;
+  const int64_t h = ho / 8;
+  const int o = (int)(ho % 8);
+  const int32_t f = nbr[27 * h + ((o >> 2) + 1) * 9 + (((o >> 1) & 1) + 1) * 3 + ((o & 1) + 1)];
+  D[t] = f >= 0 ? dyg[(int64_t)(f >> 3) * cout + c] : T(0);
 }
 
 inline unsigned grid_for(int64_t n) { return (unsigned)oc::cdiv(n, TB); }
@@ -203,14 +300,43 @@ size_t conv_s2_fwd_ws(const oc_octree* t, int l, int cin, int cout, bool bf16) {
 }
 
 size_t conv_s2_bwd_ws(const oc_octree* t, int l, int cin, int cout, bool bf16, bool dx, bool dw) {
-  const S2Shape h = s2_shape(t, l, cin, 4);
+  const size_t es = bf16 ? 2 : 4;
+  const S2Shape h = s2_shape(t, l, cin, es);
   if (h.G == 0 || (!dx && !dw)) return 0;
-  size_t b = align256((size_t)h.G * cout * 4);                        // dY_g
-  if (bf16) b += align256((size_t)h.kc * cout * 4);                   // widened W
-  const size_t a = dx ? align256((size_t)h.G * h.kc * 4) : 0;         // dCol
-  const size_t c = dw ? align256((size_t)h.gc * h.kc * 4) : 0;        // Col chunk
+  const size_t b = align256((size_t)h.G * cout * es);                         // dY_g
+  const size_t a = dx ? align256((size_t)64 * cin * cout * es) +              // Wx
+                            align256((size_t)h.G * 8 * cout * es)             // D
+                      : 0;
+  const size_t c = dw ? align256((size_t)h.gc * h.kc * es) : 0;              // Col chunk
   return b + std::max(a, c);
 }
+
+namespace {
+
+// Column buffer of ng groups from g0, 16-byte pieces when the rows allow.
+void launch_col(hipStream_t s, const int32_t* nbr, int64_t g0, int64_t ng, const void* x, int cin,
+                bool bf16, void* col) {
+  const int rb = cin * (bf16 ? 2 : 4);
+  if (rb % 16 == 0) {
+    const int64_t nt = ng * 27 * (rb / 16);
+    if (bf16)
+      hipLaunchKernelGGL(k_s2_col<uint16_t>, dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0, ng,
+                         (const uint16_t*)x, rb, (uint16_t*)col);
+    else
+      hipLaunchKernelGGL(k_s2_col<float>, dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0, ng,
+                         (const float*)x, rb, (float*)col);
+  } else {
+    const int64_t nt = ng * 27 * cin;
+    if (bf16)
+      hipLaunchKernelGGL(k_s2_col1<uint16_t>, dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0, ng,
+                         (const uint16_t*)x, cin, (uint16_t*)col);
+    else
+      hipLaunchKernelGGL(k_s2_col1<float>, dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0, ng,
+                         (const float*)x, cin, (float*)col);
+  }
+}
+
+}  // namespace
 
 oc_status conv_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const void* w, int cout,
                       bool bf16, float* y, int relu, void* ws, hipStream_t s) {
@@ -223,20 +349,18 @@ oc_status conv_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const v
   const rocblas_datatype dt = bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
   for (int64_t g0 = 0; g0 < h.G; g0 += h.gc) {
     const int64_t ng = std::min<int64_t>(h.gc, h.G - g0);
-    const int64_t nt = ng * 27 * ((cin + 3) / 4);
-    if (bf16)
-      hipLaunchKernelGGL((k_s2_col<uint16_t, uint16_t>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr,
-                         g0, ng, (const uint16_t*)x, cin, (uint16_t*)col);
-    else
-      hipLaunchKernelGGL((k_s2_col<float, float>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0, ng,
-                         (const float*)x, cin, (float*)col);
+    launch_col(s, nbr, g0, ng, x, cin, bf16, col);
     // yg^T [cout][ng] = W^T-view [cout][27 cin] x Col^T-view [27 cin][ng] (column-major)
     oc_status st = gemm(s, false, false, cout, ng, h.kc, w, dt, cout, col, dt, h.kc, 0.f,
                         yg + g0 * cout, cout);
     if (st != OC_OK) return st;
   }
-  hipLaunchKernelGGL(k_s2_rows_out, dim3(grid_for(h.n_out * cout)), dim3(TB), 0, s,
-                     (const int32_t*)t->labels[l - 1], h.n_out, (const float*)yg, cout, relu, y);
+  if (cout % 4 == 0 && (uintptr_t)y % 16 == 0)
+    hipLaunchKernelGGL(k_s2_rows_out, dim3(grid_for(h.n_out * (cout / 4))), dim3(TB), 0, s,
+                       (const int32_t*)t->labels[l - 1], h.n_out, (const float*)yg, cout, relu, y);
+  else
+    hipLaunchKernelGGL(k_s2_rows_out1, dim3(grid_for(h.n_out * cout)), dim3(TB), 0, s,
+                       (const int32_t*)t->labels[l - 1], h.n_out, (const float*)yg, cout, relu, y);
   return OC_OK;
 }
 
@@ -244,7 +368,8 @@ oc_status conv_s2_bwd(const oc_octree* t, int l, const void* x, int cin, const v
                       bool bf16, const float* ym, const float* dy, float* dx, float* dw, void* ws,
                       hipStream_t s) {
   PassEvents ev(s);
-  const S2Shape h = s2_shape(t, l, cin, 4);
+  const size_t es = bf16 ? 2 : 4;
+  const S2Shape h = s2_shape(t, l, cin, es);
   const int64_t entries = h.kc * cout;
   if (h.G == 0) {
     if (dx && h.n_in > 0) fill_u32(dx, 0u, h.n_in * cin, s);
@@ -252,43 +377,62 @@ oc_status conv_s2_bwd(const oc_octree* t, int l, const void* x, int cin, const v
     return OC_OK;
   }
   const int32_t* nbr = t->nbr[l];
+  const rocblas_datatype dt = bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
   char* p = (char*)ws;
-  float* dyg = (float*)p;
-  p += align256((size_t)h.G * cout * 4);
-  const float* w32 = (const float*)w;
-  if (bf16) {
-    if (dx) {
-      hipLaunchKernelGGL(k_s2_widen, dim3(grid_for(entries)), dim3(TB), 0, s, (const uint16_t*)w,
-                         entries, (float*)p);
-      w32 = (const float*)p;
-    }
-    p += align256((size_t)h.kc * cout * 4);
-  }
-  float* buf = (float*)p;
-  hipLaunchKernelGGL(k_s2_dy_rows, dim3(grid_for(h.G * cout)), dim3(TB), 0, s,
-                     (const int32_t*)t->rows[l - 1], h.G, dy, ym, cout, dyg);
+  void* dyg = p;
+  p += align256((size_t)h.G * cout * es);
+  const bool vec = cout % 4 == 0 && (uintptr_t)dy % 16 == 0 && (uintptr_t)ym % 16 == 0;
+  const int32_t* prow = (const int32_t*)t->rows[l - 1];
+  if (vec && bf16)
+    hipLaunchKernelGGL(k_s2_dy_rows<uint16_t>, dim3(grid_for(h.G * (cout / 4))), dim3(TB), 0, s,
+                       prow, h.G, dy, ym, cout, (uint16_t*)dyg);
+  else if (vec)
+    hipLaunchKernelGGL(k_s2_dy_rows<float>, dim3(grid_for(h.G * (cout / 4))), dim3(TB), 0, s,
+                       prow, h.G, dy, ym, cout, (float*)dyg);
+  else if (bf16)
+    hipLaunchKernelGGL(k_s2_dy_rows1<uint16_t>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow,
+                       h.G, dy, ym, cout, (uint16_t*)dyg);
+  else
+    hipLaunchKernelGGL(k_s2_dy_rows1<float>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow,
+                       h.G, dy, ym, cout, (float*)dyg);
   if (dx) {
-    // dCol^T [27 cin][G] = W-view^T ... : column-major (27 cin x cout) op(A) = A^T of the
-    // [cout][27 cin] view of W, times dyg^T-view [cout][G]
-    oc_status st = gemm(s, true, false, h.kc, h.G, cout, w32, rocblas_datatype_f32_r, cout, dyg,
-                        rocblas_datatype_f32_r, cout, 0.f, buf, h.kc);
+    void* wx = p;
+    void* D = p + align256((size_t)64 * cin * cout * es);
+    const int64_t nw = (int64_t)64 * cin * cout;
+    const int rb = (int)(cout * es);  // bytes of a dY_g row (16-byte aligned rows when rb % 16 == 0)
+    const unsigned gd = rb % 16 == 0 ? grid_for(h.G * 8 * (int64_t)(rb / 16)) : grid_for(h.G * 8 * (int64_t)cout);
+    if (bf16) {
+      hipLaunchKernelGGL(k_s2_wx<uint16_t>, dim3(grid_for(nw)), dim3(TB), 0, s,
+                         (const uint16_t*)w, cin, cout, (uint16_t*)wx);
+      if (rb % 16 == 0)
+        hipLaunchKernelGGL(k_s2_dgather<uint16_t>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
+                           (const uint16_t*)dyg, rb, (uint16_t*)D);
+      else
+        hipLaunchKernelGGL(k_s2_dgather1<uint16_t>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
+                           (const uint16_t*)dyg, cout, (uint16_t*)D);
+    } else {
+      hipLaunchKernelGGL(k_s2_wx<float>, dim3(grid_for(nw)), dim3(TB), 0, s, (const float*)w, cin,
+                         cout, (float*)wx);
+      if (rb % 16 == 0)
+        hipLaunchKernelGGL(k_s2_dgather<float>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
+                           (const float*)dyg, rb, (float*)D);
+      else
+        hipLaunchKernelGGL(k_s2_dgather1<float>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
+                           (const float*)dyg, cout, (float*)D);
+    }
+    // dX-view^T [8 cin][G] = Wx-view^T [8 cin][8 cout] x D-view^T [8 cout][G] (column-major)
+    oc_status st = gemm(s, false, false, 8 * (int64_t)cin, h.G, 8 * (int64_t)cout, wx, dt,
+                        8 * (int64_t)cin, D, dt, 8 * (int64_t)cout, 0.f, dx, 8 * (int64_t)cin);
     if (st != OC_OK) return st;
-    hipLaunchKernelGGL(k_s2_col2im, dim3(grid_for(h.n_in * cin)), dim3(TB), 0, s, nbr, h.n_in,
-                       (const float*)buf, cin, dx);
   }
   if (dw) {
+    void* col = p;
     for (int64_t g0 = 0; g0 < h.G; g0 += h.gc) {
       const int64_t ng = std::min<int64_t>(h.gc, h.G - g0);
-      const int64_t nt = ng * 27 * ((cin + 3) / 4);
-      if (bf16)
-        hipLaunchKernelGGL((k_s2_col<uint16_t, float>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0,
-                           ng, (const uint16_t*)x, cin, buf);
-      else
-        hipLaunchKernelGGL((k_s2_col<float, float>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0,
-                           ng, (const float*)x, cin, buf);
+      launch_col(s, nbr, g0, ng, x, cin, bf16, col);
       // dW^T [cout][27 cin] (+)= dyg^T-view [cout][ng] x Col-view^T [ng][27 cin]
-      oc_status st = gemm(s, false, true, cout, h.kc, ng, dyg + g0 * cout, rocblas_datatype_f32_r,
-                          cout, buf, rocblas_datatype_f32_r, h.kc, g0 == 0 ? 0.f : 1.f, dw, cout);
+      oc_status st = gemm(s, false, true, cout, h.kc, ng, (const char*)dyg + g0 * cout * es, dt,
+                          cout, col, dt, h.kc, g0 == 0 ? 0.f : 1.f, dw, cout);
       if (st != OC_OK) return st;
     }
   }

@@ -126,8 +126,11 @@ def test_conv_small_bf16(K, stride):
                           "dx vs fp32 oracle")
         assert_bf16_close(dw.cpu().numpy(), oracle.conv_bwd_weight(nb, x32, dy, K ** 3),
                           "dw vs fp32 oracle")
-    else:
-        dxr, dwr = oracle.conv_s2_bwd(ref, l, x, w, dy)
+    else:  # the stride-2 bf16 backward multiplies dy rounded to bf16 as well
+        dxr, dwr = oracle.conv_s2_bwd(ref, l, x, w, bf16_round(dy))
+        dx32, dw32 = oracle.conv_s2_bwd(ref, l, x32, w32, dy)
+        assert_bf16_close(dx.cpu().numpy(), dx32, "dx vs fp32 oracle")
+        assert_bf16_close(dw.cpu().numpy(), dw32, "dw vs fp32 oracle")
     assert_f32_close(dx.cpu().numpy(), dxr, "dx bf16 weights")
     assert_dw_close(dw.cpu().numpy(), dwr, "dw bf16 inputs")
 
@@ -254,9 +257,9 @@ def _check_conv_full(ref, tree, l, K, stride, x, w, relu, dy, tag, dtype=torch.f
     want = np.zeros(n_in, bool)
     want[_sample(rng, n_in, 3000)] = True
     ent = _sample(rng, w.size, 300)
+    if dtype == torch.bfloat16:  # the bf16 backward multiplies dy rounded to bf16
+        dye = bf16_round(dye)
     if stride == 1:
-        if dtype == torch.bfloat16:  # the stride-1 bf16 backward multiplies dy rounded to bf16
-            dye = bf16_round(dye)
         dxr = oracle.conv_bwd_data(nb, dye, wq, n_in, want=want)
         dwr = oracle.conv_bwd_weight(nb, xq, dye, K ** 3, entries=ent)
     else:
