@@ -61,6 +61,8 @@ constexpr int TB = 256;
 // that absent lanes spread over many cache lines.
 constexpr int ZROWS = 4096;
 __device__ __attribute__((aligned(16))) uint32_t g_zero_rows[ZROWS][4];
+// -1: the neighbour entry loaded for groups past a range (absent neighbour).
+__device__ const int32_t g_minus1 = -1;
 
 __device__ __forceinline__ uint32_t lds_addr(const void* lds) {
   return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lptr_t)lds);
@@ -71,6 +73,11 @@ __device__ __forceinline__ uint32_t lds_addr(const void* lds) {
 // caller waits for completion (vm_wait0) before other waves read the data.
 __device__ __forceinline__ void lds_load16(const void* src, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(src)
+               : "memory", "m0");
+}
+// The same for 4 bytes per lane (lane i's dword lands at lds + 4 i).
+__device__ __forceinline__ void lds_load4(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(lds), "v"(src)
                : "memory", "m0");
 }
 // s_waitcnt vmcnt(0): all of this wave's vector memory operations are done.
@@ -421,8 +428,12 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   constexpr int YP = GS * 8 * 8;             // pieces of the staged dY rows
   constexpr int BUF = XP + YP;
   constexpr int NW = 8;                      // waves
-  __shared__ __attribute__((aligned(16))) v4u lds[2 * BUF];
-  __shared__ int32_t nbs[2][GS * 27];  // neighbour rows of a step's groups, two steps
+  constexpr int NB = 3;                      // stage buffers (two steps in flight)
+  constexpr int NBP = NW * 64;               // dwords of a neighbour-row slot (8 groups use 216)
+  constexpr int DC = (MAXPOS + GS + NW - 1) / NW;  // DMA instructions of a stage per wave
+  __shared__ __attribute__((aligned(16))) v4u lds[NB * BUF];
+  __shared__ __attribute__((aligned(16))) int32_t nbs[3][NBP];  // neighbour rows of a step's groups
+  __shared__ __attribute__((aligned(16))) v4u trash[64];        // destination of padding loads
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -448,36 +459,48 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   const int64_t gbeg = ngroups * range / nr, gend = ngroups * (range + 1) / nr;
   const int nsteps = (int)((gend - gbeg + GS - 1) / GS);
 
+  // stage st: x positions (npos instructions of 64 pieces), then the 64 dY
+  // rows (GS instructions); every wave issues DC DMA instructions (padding
+  // loads of zeros into the trash slot)
   auto stage = [&](int st, v4u* buf) {
     const int64_t gs = gbeg + GS * (int64_t)st;
-    const int nxi = npos;  // instructions of 64 pieces for the x positions
-    for (int i = wave; i < nxi + GS; i += NW) {
+    const int nxi = npos;
+    const int32_t* nb = nbs[st % 3];
+#pragma unroll
+    for (int k = 0; k < DC; ++k) {
+      const int i = wave + NW * k;
+      const void* src = g_zero_rows[(lane + 64 * k + 512 * (int)blockIdx.x) & (ZROWS - 1)];
+      v4u* dst = trash;
       if (i < nxi) {
         const int s = i * 64 + lane;
         const int pos = s >> 3, g = pos / npos, p = pos - g * npos;
         const int ix = p / (NY * S), rem = p - ix * (NY * S), iy = rem / S, iz = rem - iy * S;
         const int o = (s & 7) ^ (2 * ((iz + 2 * iy) & 3));
         const int ch = c0 + 8 * o;
-        const int32_t row =
-            ch < cin ? tile_row<R>(nbs[st & 1] + 27 * g, dxi + ix, ya + iy, iz) : -1;
-        v4u* dst = buf + i * 64;
-        if (row >= 0)
-          lds_load16(x + (int64_t)row * cin + ch, lds_addr(dst));
-        else
-          dst[lane] = v4u{0u, 0u, 0u, 0u};
-      } else {
+        const int32_t row = ch < cin ? tile_row<R>(nb + 27 * g, dxi + ix, ya + iy, iz) : -1;
+        if (row >= 0) src = x + (int64_t)row * cin + ch;
+        dst = buf + i * 64;
+      } else if (i < nxi + GS) {
         const int s = (i - nxi) * 64 + lane;
         const int rl = s >> 3;
         const int o = (s & 7) ^ (2 * (rl & 3));
         const int co = n0 + 8 * o;
         const int64_t gg = gs + (rl >> 3);
-        v4u* dst = buf + XP + (i - nxi) * 64;
-        if (gg < gend && co < cout)
-          lds_load16(dy + (8 * gg + (rl & 7)) * cout + co, lds_addr(dst));
-        else
-          dst[lane] = v4u{0u, 0u, 0u, 0u};
+        if (gg < gend && co < cout) src = dy + (8 * gg + (rl & 7)) * cout + co;
+        dst = buf + XP + (i - nxi) * 64;
       }
+      lds_load16(src, lds_addr(dst));
     }
+  };
+  // neighbour rows of step st's groups into slot st % 3: one dword DMA
+  // instruction per wave (entries past the range read -1 from the zero rows'
+  // neighbour, see below)
+  auto nb_dma = [&](int st) {
+    const int e = wave * 64 + lane;  // entry of the slot
+    const int64_t g = gbeg + GS * (int64_t)st + e / 27;
+    const void* src = e < GS * 27 && g < gend ? (const void*)(nbr + 27 * g + e % 27)
+                                             : (const void*)&g_minus1;
+    lds_load4(src, lds_addr(&nbs[st % 3][wave * 64]));
   };
 
   v4f acc[MAXC][4];
@@ -529,27 +552,26 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
     }
   };
 
-  // neighbour rows of step st's groups (-1 past the range) go to nbs[st & 1];
-  // those of step st+2 are loaded into a register during step st and stored
-  // at its end, when step st's rows are no longer read
-  auto nb_entry = [&](int st) -> int32_t {
-    const int64_t gg = gbeg + GS * (int64_t)st + tid / 27;
-    return tid < GS * 27 && gg < gend ? nbr[27 * gg + tid % 27] : -1;
-  };
-  if (tid < GS * 27) {
-    nbs[0][tid] = nb_entry(0);
-    nbs[1][tid] = nb_entry(1);
-  }
-  __syncthreads();
-  if (nsteps > 0) stage(0, lds);
+  // Load order of a wave: nb(0), nb(1) (waited for); stage(0), nb(2),
+  // stage(1), nb(3); at step st, after the barrier: stage(st+2), nb(st+4).
+  // When step st starts, the loads younger than stage(st) and nb(st+2) are
+  // those of step st-1: DC + 1.
+  nb_dma(0);
+  nb_dma(1);
+  vm_wait0();
+  lds_barrier();
+  stage(0, lds);
+  nb_dma(2);
+  stage(1, lds + BUF);
+  nb_dma(3);
   for (int st = 0; st < nsteps; ++st) {
-    vm_wait0();
-    __syncthreads();  // step st has landed; step st-1 is no longer read
-    const int32_t nb2 = nb_entry(st + 2);
-    if (st + 1 < nsteps) stage(st + 1, lds + ((st + 1) & 1) * BUF);
-    compute(lds + (st & 1) * BUF);
-    if (tid < GS * 27) nbs[st & 1][tid] = nb2;
+    vm_wait_n<DC + 1>();  // stage st and the neighbour rows of step st+2 have landed
+    lds_barrier();        // ... everywhere; step st-1 is no longer read
+    stage(st + 2, lds + ((st + 2) % NB) * BUF);
+    nb_dma(st + 4);
+    compute(lds + (st % NB) * BUF);
   }
+  vm_wait0();
 
   // partial dW of this range: lane (li, q), accumulator j holds input channel
   // c0 + 16 cb + 4q + j, output channel n0 + 16 nb + li
