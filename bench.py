@@ -90,6 +90,8 @@ def parse():
     ap.add_argument("--cpu-shapes", type=int, default=32,
                     help="shapes of the batch the CPU oracle runs (0: skip)")
     ap.add_argument("--layers", action="store_true", help="also print per-layer timings to stderr")
+    ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
+                    help="2: weight gradients on a second stream beside the rest of the backward")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="after the steps, run an elementwise copy (y = -x) of MIB MiB three "
                          "times: the known-size kernel that calibrates the HBM byte counters")
@@ -266,6 +268,7 @@ class Step:
                                                           L0.cin)).to(dev)
             if L0.dtype == "bf16":
                 self.x0 = self.x0.to(torch.bfloat16)
+        self.side = None  # stream for the weight gradients (None: all on one stream)
         self.events = None  # {key: [(start, end, layer), ...]} when recording
         self.traced = set()
         # when set: only the (step number % rotate)-th launch of a traced key
@@ -433,9 +436,24 @@ class Step:
                         need_dx=True, need_dw=False))
                 else:
                     dx = None
-                _, dw = self._run("conv_bwd_weight", li, lambda: oc.oc_conv_bwd(
+                dwf = (lambda: oc.oc_conv_bwd(
                     tree, L.depth, L.ksize, L.stride, xin, w, g, y=yout, relu=relu,
                     need_dx=False, need_dw=True))
+                if self.side is None:
+                    _, dw = self._run("conv_bwd_weight", li, dwf)
+                else:
+                    # the weight gradient depends on nothing that follows: it
+                    # runs on the side stream beside the rest of the backward
+                    torch = self.torch
+                    ev = torch.cuda.Event()
+                    ev.record()
+                    self.side.wait_event(ev)
+                    with torch.cuda.stream(self.side):
+                        _, dw = self._run("conv_bwd_weight", li, dwf)
+                    for t in (xin, g, yout, w):
+                        if t is not None:
+                            t.record_stream(self.side)
+                    tree.record_stream(self.side)
                 g, masked = dx, False
             elif L.op == "pool":
                 # a ReLU right below the pooling: its backward goes into the routing
@@ -446,6 +464,8 @@ class Step:
             elif L.op == "unpool":
                 g = self._run("unpool_bwd", li, lambda: oc.oc_unpool_bwd(tree, L.depth, g, sw))
                 masked = False
+        if self.side is not None:
+            self.torch.cuda.current_stream().wait_stream(self.side)
         return g
 
     def collect(self):
@@ -533,6 +553,8 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     print(f"[bench] workload {wl.name}: generating inputs", file=sys.stderr, flush=True)
     step = Step(oc, torch, synth, wl)
+    if args.streams == 2:
+        step.side = torch.cuda.Stream()  # default priority, like the main stream
     flops, octants = step.conv_flops()
     print(f"[bench] N_l = {step.N}, M_l = {step.M}", file=sys.stderr, flush=True)
 
