@@ -400,17 +400,19 @@ __global__ __launch_bounds__(512) void k_conv_bf(const int32_t* __restrict__ nbr
 
 // ---------------------------------------------------------------------------
 // Weight gradient.  x [8 ngroups][cin] bf16, dy [8 ngroups][cout] bf16
-// (cin, cout % 16 == 0).  A unit is an x-offset and a set of y-offsets
-// [ya, yb): YR of them, or fewer in a last, shorter set (K = 5: sets {0,1},
-// {2,3}, {4}).  Grid: x = work items, y = blocks of 64 output channels, z =
-// blocks of 64 input channels; 256 threads.  Items 0 .. NFU nranges - 1 are
-// (full unit, range) pairs, the others (short unit, range) pairs with half as
-// many ranges, each twice as long, so that every item does the same work;
-// a short unit's range r writes slot r of the partial sums and zeros slot
-// r + nranges / 2.  Per step of eight groups the workgroup stages the x
-// positions its taps read (x-slabs dx+R, dx+R+1; y in [ya, yb]; every z) and
-// the 64 dY rows.  x piece o of box position (ix, iy, iz) sits at
-// o ^ 2((iz + 2 iy) & 3), dY piece o of row r at o ^ 2(r & 3).
+// (cin, cout % 16 == 0).  A unit is a box of tap offsets, x-offsets
+// [x0, x1] by y-offsets [y0, y1] by every z-offset, whose taps read a box of
+// positions (x1-x0+2) by (y1-y0+2) by K+1 around a group.  K = 5: ten units
+// of one x-offset and two y-offsets, two of two x-offsets and y-offset 4,
+// and one of x- and y-offset 4 (half the taps); K = 3: three units of one
+// x-offset and every y-offset.  Every unit but the last K = 5 one has
+// 10 (K = 5) or 9 (K = 3) taps and at most 36 positions.
+// Grid: x = units x ranges (a range is a contiguous run of groups), y =
+// blocks of 64 output channels, z = blocks of 64 input channels; 512
+// threads (two waves per SIMD, so that one wave's LDS waits overlap the
+// other's MFMAs).  Per step of eight groups the workgroup stages the unit's
+// positions and the 64 dY rows; x piece o of box position (ix, iy, iz) sits
+// at o ^ 2((iz + 2 iy) & 3), dY piece o of row r at o ^ 2(r & 3).
 // part [nranges][K^3][cin][cout].
 template <int K, int MAXC>
 __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ nbr,
@@ -419,11 +421,9 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
                                                       const uint16_t* __restrict__ dy, int cout,
                                                       int nranges, float* __restrict__ part) {
   constexpr int R = (K - 1) / 2, S = K + 1, K3 = K * K * K;
-  constexpr int YR = K == 5 ? 2 : 3;         // y-offsets of a full unit
-  constexpr int NSF = K / YR;                // full units per x-offset
-  constexpr int NFU = K * NSF;               // full units
+  constexpr int NU = K == 5 ? 13 : 3;        // units
   constexpr int GS = 8;                      // groups per step
-  constexpr int MAXPOS = 2 * (YR + 1) * S;   // staged positions per group
+  constexpr int MAXPOS = 36;                 // staged positions per group, at most
   constexpr int XP = GS * MAXPOS * 8;        // pieces of the staged x
   constexpr int YP = GS * 8 * 8;             // pieces of the staged dY rows
   constexpr int BUF = XP + YP;
@@ -438,21 +438,19 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int li = lane & 15, q = lane >> 4;
-  int dxi, set, range, nr;
-  {
-    const int b = blockIdx.x;
-    if (b < NFU * nranges) {
-      const int u = b % NFU;
-      dxi = u / NSF, set = u % NSF, range = b / NFU, nr = nranges;
-    } else {
-      const int b2 = b - NFU * nranges;
-      dxi = b2 % K, set = NSF, range = b2 / K, nr = nranges / 2;
-    }
+  const int unit = blockIdx.x % NU, range = blockIdx.x / NU, nr = nranges;
+  int x0, x1, y0, y1;  // the unit's box of tap offsets (indices 0..K-1)
+  if (K == 3) {
+    x0 = x1 = unit, y0 = 0, y1 = 2;
+  } else if (unit < 10) {
+    x0 = x1 = unit >> 1, y0 = 2 * (unit & 1), y1 = y0 + 1;
+  } else {
+    x0 = 2 * (unit - 10), x1 = x0 + 1 < K ? x0 + 1 : x0, y0 = y1 = 4;
   }
-  const int ya = YR * set, yb = ya + YR < K ? ya + YR : K;
-  const int NY = yb - ya + 1;
-  const int npos = 2 * NY * S;
-  const int ntap = (yb - ya) * K;
+  const int NXT = x1 - x0 + 1, NYT = y1 - y0 + 1;  // tap offsets per axis
+  const int NY = NYT + 1;                          // positions along y
+  const int npos = (NXT + 1) * NY * S;
+  const int ntap = NXT * NYT * K;
   const int c0 = blockIdx.z * 64, n0 = blockIdx.y * 64;
   const int CB = (cin - c0 < 64 ? cin - c0 : 64) / 16;
   const int ncombo = ntap * CB;
@@ -477,7 +475,7 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
         const int ix = p / (NY * S), rem = p - ix * (NY * S), iy = rem / S, iz = rem - iy * S;
         const int o = (s & 7) ^ (2 * ((iz + 2 * iy) & 3));
         const int ch = c0 + 8 * o;
-        const int32_t row = ch < cin ? tile_row<R>(nb + 27 * g, dxi + ix, ya + iy, iz) : -1;
+        const int32_t row = ch < cin ? tile_row<R>(nb + 27 * g, x0 + ix, y0 + iy, iz) : -1;
         if (row >= 0) src = x + (int64_t)row * cin + ch;
         dst = buf + i * 64;
       } else if (i < nxi + GS) {
@@ -513,41 +511,45 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   // 16-lane group's eight, channels 4 (li & 3).. of the 16-channel block;
   // the 16-lane group q takes group 4 sub + q of the step
   const int r4 = li >> 2, tq = li & 3;
-  auto compute = [&](const v4u* buf) {
+  // Each wave multiplies MAXC (tap, 16-channel block) pairs: combo m = wave +
+  // NW mi of the unit's ncombo; pairs past ncombo read pair 0's operands and
+  // their sums are dropped, so that the loop has no branches.  Each pair's A loads are issued before the MFMAs
+  // of the pair before it.
+  auto a_off = [&](int m, int gq, int hh) {  // byte offset of pair m's A load hh
+    const int mm = m < ncombo ? m : 0;
+    const int it = mm / CB, cb = mm - it * CB;
+    const int dxl = it / (NYT * K), dyl = (it / K) % NYT, dzi = it % K;
+    const int iy = dyl + (r4 >> 1), iz = dzi + (r4 & 1);  // child 4 hh + r4 of group gq
+    const int p = ((dxl + hh) * NY + iy) * S + iz;
+    const int o = 2 * cb + (tq >> 1);
+    return ((gq * npos + p) * 8 + (o ^ (2 * ((iz + 2 * iy) & 3)))) * 16 + (tq & 1) * 8;
+  };
+  auto b_off = [&](int nb, int gq, int hh) {  // byte offset of dY fragment nb, load hh
+    const int rl = 8 * gq + 4 * hh + r4;
+    const int o = 2 * nb + (tq >> 1);
+    return (XP + rl * 8 + (o ^ (2 * (rl & 3)))) * 16 + (tq & 1) * 8;
+  };
+  auto compute = [&](const v4u* buf, auto ncc) {
+    constexpr int NC = decltype(ncc)::value;
+    constexpr int SUBS = GS / 4;
 #pragma unroll
-    for (int sub = 0; sub < GS / 4; ++sub) {
+    for (int sub = 0; sub < SUBS; ++sub) {
       const int gq = 4 * sub + q;
       v4u bfr[4];
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        v4s hv[2];
+      for (int nb = 0; nb < 4; ++nb)
+        bfr[nb] = join(lds_tr16(buf, b_off(nb, gq, 0)), lds_tr16(buf, b_off(nb, gq, 1)));
+      v4u a[2];
+      a[0] = join(lds_tr16(buf, a_off(wave, gq, 0)), lds_tr16(buf, a_off(wave, gq, 1)));
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int rl = 8 * gq + 4 * hh + r4;
-          const int o = 2 * nb + (tq >> 1);
-          hv[hh] = lds_tr16(buf, (XP + rl * 8 + (o ^ (2 * (rl & 3)))) * 16 + (tq & 1) * 8);
+      for (int mi = 0; mi < NC; ++mi) {
+        if (mi + 1 < NC) {
+          const int m1 = wave + NW * (mi + 1);
+          a[(mi + 1) & 1] = join(lds_tr16(buf, a_off(m1, gq, 0)), lds_tr16(buf, a_off(m1, gq, 1)));
         }
-        bfr[nb] = join(hv[0], hv[1]);
-      }
 #pragma unroll
-      for (int mi = 0; mi < MAXC; ++mi) {
-        const int m = wave + NW * mi;
-        if (m < ncombo) {
-          const int it = m / CB, cb = m - it * CB;
-          const int dyl = it / K, dzi = it - dyl * K;
-          v4s hv[2];
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {  // child 4 hh + r4 of group gq
-            const int iy = dyl + (r4 >> 1), iz = dzi + (r4 & 1);
-            const int p = (hh * NY + iy) * S + iz;
-            const int o = 2 * cb + (tq >> 1);
-            hv[hh] = lds_tr16(buf, ((gq * npos + p) * 8 + (o ^ (2 * ((iz + 2 * iy) & 3)))) * 16 +
-                                       (tq & 1) * 8);
-          }
-          const v4u a = join(hv[0], hv[1]);
-#pragma unroll
-          for (int nb = 0; nb < 4; ++nb) acc[mi][nb] = mfma_bf(a, bfr[nb], acc[mi][nb]);
-        }
+        for (int nb = 0; nb < 4; ++nb)
+          acc[mi][nb] = mfma_bf(a[mi & 1], bfr[nb], acc[mi][nb]);
       }
     }
   };
@@ -569,31 +571,27 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
     lds_barrier();        // ... everywhere; step st-1 is no longer read
     stage(st + 2, lds + ((st + 2) % NB) * BUF);
     nb_dma(st + 4);
-    compute(lds + (st % NB) * BUF);
+    compute(lds + (st % NB) * BUF, std::integral_constant<int, MAXC>{});
   }
   vm_wait0();
 
   // partial dW of this range: lane (li, q), accumulator j holds input channel
   // c0 + 16 cb + 4q + j, output channel n0 + 16 nb + li
-  const bool shortu = nr != nranges;
 #pragma unroll
   for (int mi = 0; mi < MAXC; ++mi) {
     const int m = wave + NW * mi;
     if (m < ncombo) {
       const int it = m / CB, cb = m - it * CB;
-      const int t = (dxi * K + ya + it / K) * K + it % K;
+      const int dxl = it / (NYT * K), dyl = (it / K) % NYT, dzi = it % K;
+      const int t = ((x0 + dxl) * K + y0 + dyl) * K + dzi;
       float* dst = part + ((int64_t)range * K3 + t) * cin * cout;
-      float* dz = part + ((int64_t)(range + nr) * K3 + t) * cin * cout;
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) {
         const int n = n0 + 16 * nb + li;
         if (n < cout) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int64_t e = (int64_t)(c0 + 16 * cb + 4 * q + j) * cout + n;
-            dst[e] = acc[mi][nb][j];
-            if (shortu) dz[e] = 0.f;
-          }
+          for (int j = 0; j < 4; ++j)
+            dst[(int64_t)(c0 + 16 * cb + 4 * q + j) * cout + n] = acc[mi][nb][j];
         }
       }
     }
@@ -604,19 +602,17 @@ inline unsigned blocks(int64_t n, int per) { return (unsigned)oc::cdiv(n, per); 
 
 size_t wp_bytes(int K, int kk, int nn) { return oc::align256((size_t)kk * K * K * K * nn * 2); }
 
-// Work items of the weight gradient for nranges ranges: K = 5 has 10 full
-// units and 5 short ones (half as many ranges), K = 3 three full units.
-int dw_items(int K, int nranges) { return K == 5 ? 10 * nranges + 5 * (nranges / 2) : 3 * nranges; }
+// Work items of the weight gradient for nranges ranges: units x ranges.
+int dw_items(int K, int nranges) { return (K == 5 ? 13 : 3) * nranges; }
 
 int dw_ranges(const oc_octree* t, int l, int K, int cin, int cout) {
   const int64_t G = t->M[l - 1];
-  const int64_t per = oc::cdiv(cout, 64) * oc::cdiv(cin, 64);
+  const int64_t per = oc::cdiv(cout, 64) * oc::cdiv(cin, 64) * (K == 5 ? 13 : 3);
   // about two items per compute unit (one resident at a time), at least 16
-  // groups per range; K = 5 needs an even count
-  const int64_t full = K == 5 ? 25 : 6;  // items per 2 ranges
-  int64_t r = 2 * std::max<int64_t>(1, (2 * (int64_t)oc::cu_count()) / (full * per));
-  r = std::min<int64_t>(r, std::max<int64_t>(2, 2 * (G / 32)));
-  return (int)std::max<int64_t>(2, r);
+  // groups per range
+  int64_t r = std::max<int64_t>(1, (2 * (int64_t)oc::cu_count()) / per);
+  r = std::min<int64_t>(r, std::max<int64_t>(1, G / 16));
+  return (int)std::max<int64_t>(1, r);
 }
 
 void wprep(const uint16_t* w, int K, int kk, int nn, int flip, uint16_t* wp, hipStream_t s) {
