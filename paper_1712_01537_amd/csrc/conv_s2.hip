@@ -6,8 +6,8 @@
 // (0 for an absent neighbour; only parent offsets {-1,0}^3 are reached from
 // child 0), a library GEMM multiplies it by W viewed as [27 Cin][Cout], and
 // a second kernel moves each group's row to its parent's row.
-//   weight gradient: dW = Col^T dY_g (GEMM over the groups, in chunks added
-//     in a fixed order through the GEMM's beta);
+//   weight gradient: dW = Col^T dY_g (GEMMs over runs of groups into eight
+//     partial sums, added in a fixed order);
 //   input gradient: input row 8h + c (child c of group h) is read by the
 //     groups at parent offsets o in {0,1}^3 from h's parent with o_a = 0
 //     where c_a = 0, through tap d = c - 2o.  So the eight rows of group h
@@ -273,6 +273,46 @@ oc_status gemm(hipStream_t s, bool ta, bool tb, int64_t m, int64_t n, int64_t k,
   return OC_OK;
 }
 
+// The same for `batch` GEMMs whose operands lie sa, sb and sd elements apart.
+oc_status gemm_batched(hipStream_t s, bool ta, bool tb, int64_t m, int64_t n, int64_t k,
+                       const void* A, rocblas_datatype at, int64_t lda, int64_t sa, const void* B,
+                       rocblas_datatype bt, int64_t ldb, int64_t sb, float beta, float* D,
+                       int64_t ldd, int64_t sd, int64_t batch) {
+  if (m == 0 || n == 0 || batch == 0) return OC_OK;
+  if (m > INT32_MAX || n > INT32_MAX || k > INT32_MAX || lda > INT32_MAX || ldb > INT32_MAX ||
+      batch > INT32_MAX)
+    return oc::fail(OC_ERR_UNSUPPORTED, "stride-2 convolution: GEMM size beyond 32 bits");
+  std::lock_guard<std::mutex> lk(g_blas_mu);
+  rocblas_handle h;
+  oc_status st = blas_for(s, &h);
+  if (st != OC_OK) return st;
+  const float alpha = 1.f;
+  const rocblas_status r = rocblas_gemm_strided_batched_ex(
+      h, ta ? rocblas_operation_transpose : rocblas_operation_none,
+      tb ? rocblas_operation_transpose : rocblas_operation_none, (rocblas_int)m, (rocblas_int)n,
+      (rocblas_int)k, &alpha, A, at, (rocblas_int)lda, sa, B, bt, (rocblas_int)ldb, sb, &beta, D,
+      rocblas_datatype_f32_r, (rocblas_int)ldd, sd, D, rocblas_datatype_f32_r, (rocblas_int)ldd, sd,
+      (rocblas_int)batch, rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+  if (r != rocblas_status_success)
+    return oc::fail(OC_ERR_DEVICE, "stride-2 convolution: batched GEMM failed (%d)", (int)r);
+  return OC_OK;
+}
+
+// out[e] = sum_{b < nb} part[b][e] in the order b = 0, 1, ...
+__global__ __launch_bounds__(TB) void k_s2_sum(const float* __restrict__ part, int nb, int64_t n,
+                                               float* __restrict__ out) {
+  const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (e >= n) return;
+  float v = 0.f;
+  for (int b = 0; b < nb; ++b) v += part[b * n + e];
+  out[e] = v;
+}
+
+// Batches of the weight gradient's GEMM: the groups of a column-buffer chunk
+// are split into DW_BATCH runs whose products go to separate partial sums (a
+// single GEMM over the groups has too few output tiles to fill the GPU).
+constexpr int DW_BATCH = 8;
+
 struct S2Shape {
   int64_t G, n_in, n_out;
   int64_t kc;  // 27 cin
@@ -307,7 +347,9 @@ size_t conv_s2_bwd_ws(const oc_octree* t, int l, int cin, int cout, bool bf16, b
   const size_t a = dx ? align256((size_t)64 * cin * cout * es) +              // Wx
                             align256((size_t)h.G * 8 * cout * es)             // D
                       : 0;
-  const size_t c = dw ? align256((size_t)h.gc * h.kc * es) : 0;              // Col chunk
+  const size_t c = dw ? align256((size_t)h.gc * h.kc * es) +                 // Col chunk
+                            align256((size_t)DW_BATCH * h.kc * cout * 4)      // partial dW
+                      : 0;
   return b + std::max(a, c);
 }
 
@@ -427,14 +469,28 @@ oc_status conv_s2_bwd(const oc_octree* t, int l, const void* x, int cin, const v
   }
   if (dw) {
     void* col = p;
+    float* pw = (float*)(p + align256((size_t)h.gc * h.kc * es));  // [DW_BATCH][27 cin][cout]
+    const int64_t E = h.kc * cout;
+    fill_u32(pw, 0u, DW_BATCH * E, s);
     for (int64_t g0 = 0; g0 < h.G; g0 += h.gc) {
       const int64_t ng = std::min<int64_t>(h.gc, h.G - g0);
       launch_col(s, nbr, g0, ng, x, cin, bf16, col);
-      // dW^T [cout][27 cin] (+)= dyg^T-view [cout][ng] x Col-view^T [ng][27 cin]
-      oc_status st = gemm(s, false, true, cout, h.kc, ng, (const char*)dyg + g0 * cout * es, dt,
-                          cout, col, dt, h.kc, g0 == 0 ? 0.f : 1.f, dw, cout);
+      // partial b: dW^T [cout][27 cin] += dyg^T-view [cout][sz] x Col-view^T [sz][27 cin]
+      // over groups g0 + b sz .. g0 + (b+1) sz; the rest of the chunk adds to partial 0
+      const int64_t sz = ng / DW_BATCH, done = sz * DW_BATCH;
+      const char* dy0 = (const char*)dyg + g0 * cout * es;
+      oc_status st = gemm_batched(s, false, true, cout, h.kc, sz, dy0, dt, cout, sz * cout,
+                                  col, dt, h.kc, sz * h.kc, 1.f, pw, cout, E,
+                                  sz > 0 ? DW_BATCH : 0);
       if (st != OC_OK) return st;
+      if (ng > done) {
+        st = gemm(s, false, true, cout, h.kc, ng - done, dy0 + done * cout * es, dt, cout,
+                  (const char*)col + done * h.kc * es, dt, h.kc, 1.f, pw, cout);
+        if (st != OC_OK) return st;
+      }
     }
+    hipLaunchKernelGGL(k_s2_sum, dim3(grid_for(E)), dim3(TB), 0, s, (const float*)pw, DW_BATCH, E,
+                       dw);
   }
   return OC_OK;
 }
