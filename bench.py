@@ -38,6 +38,16 @@ The printed JSON line reports:
                  internal header) differs from the one the counters were
                  taken on.
 
+  ops            every op class's main kernels in the warmup (HIP events)
+                 against its work: TFLOP/s of the conv passes, GB/s of the
+                 pooling, and conv_fwd_bwd over all conv passes.
+
+Trace summary: python bench.py --summarize-trace PROF_DIR PROF_LOG reads the
+  kernel statistics of a rocprofv3 --kernel-trace --stats run of this script
+  and that run's own output, and prints each kernel class's time per step
+  against its work (build and pooling GB/s, conv fwd+bwd TFLOP/s with and
+  without the helper kernels) and the per-kernel table.
+
 Counter summary: python bench.py --summarize-counters FETCH_DIR WRITE_DIR
   --copy-probe MIB --workload NAME reads the counter_collection CSV files of
   the two rocprofv3 runs and prints the summary (markdown with a JSON block).
@@ -97,6 +107,9 @@ def parse():
                          "times: the known-size kernel that calibrates the HBM byte counters")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the HBM counter summary of two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("PROF_DIR", "PROF_LOG"),
+                    help="print the per-class kernel time of a rocprofv3 --kernel-trace --stats "
+                         "run of this script (its output directory and its stdout) and exit")
     return ap.parse_args()
 
 
@@ -229,7 +242,176 @@ def summarize_counters(fetch_dir, write_dir, copy_mib, workload):
     print("\n```json\n" + json.dumps(rec, indent=1) + "\n```")
 
 
-class Step:
+def op_rate(cls, work, us, bf16):
+    """Achieved rate of an op class from its algorithmic work (flops of a conv
+    class, HBM bytes otherwise) and its time per step, against the peak."""
+    if cls.startswith("conv"):
+        a = work / (us * 1e-6) / 1e12
+        peak, unit = PEAK["bf16_TFLOPs" if bf16 else "fp32_TFLOPs"], "TFLOP/s"
+    else:
+        a = work / (us * 1e-6) / 1e9
+        peak, unit = PEAK["hbm_GBps"], "GB/s"
+    return {"us_per_step": round(us, 2), "achieved": round(a, 3), "unit": unit, "peak": peak,
+            "frac": round(a / peak, 4)}
+
+
+# Kernel classes of a rocprofv3 trace of this script, by kernel name: the
+# build's kernels, the pooling/unpooling kernels, the convolutions' main
+# kernels (the MFMA contraction: hand-written kernels and, for stride 2, the
+# ROCm GEMM library's) and their helpers (split sums, ReLU masks, operand
+# conversion and gathers).  Anything else (the bench's own torch casts) is
+# "other".
+TRACE_CLASSES = (
+    ("build", ("k_quant", "k_mark", "k_reduce", "k_scan_a", "k_scan_c", "k_leaf_mean", "k_emit",
+               "__amd_rocclr_copyBuffer")),
+    ("pool", ("k_pool_fwd", "k_route_down", "k_route_up")),
+    ("conv_main", ("k_conv_", "Cijk_")),
+    ("conv_helper", ("k_sum_", "k_relu_mask", "k_bf_", "k_bf16_to_f32", "k_s2_", "k_fill_u32")),
+)
+
+
+def trace_class(name):
+    for cls, prefixes in TRACE_CLASSES:
+        if any(name.startswith(p) for p in prefixes):
+            return cls
+    return "other"
+
+
+def summarize_trace(prof_dir, prof_log):
+    """Time per step of each kernel class of a rocprofv3 --kernel-trace --stats
+    run of this script, against the algorithmic work of the class: conv
+    fwd+bwd flops (every kernel of the conv passes, helpers included, and the
+    main kernels alone), HBM bytes of the build and of the pooling.  The
+    profiled run's own JSON line (in prof_log) gives the workload's sizes and
+    step counts."""
+    import synth
+
+    line = None
+    with open(prof_log) as fh:
+        for ln in fh:
+            ln = ln.strip()
+            if ln.startswith("{") and '"metric"' in ln:
+                line = json.loads(ln)
+    if line is None:
+        raise SystemExit(f"no bench JSON line in {prof_log}")
+    cfg = line["config"]
+    wl = synth.WORKLOADS[cfg["workload"]]
+    acc = Accounting(wl, cfg["octants_per_depth"], cfg["nonempty_per_depth"], cfg["points"])
+    nsteps = max(line["warmup"], 2) + line["steps"]
+    files = glob.glob(os.path.join(prof_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_stats.csv under {prof_dir}")
+    kern, table = {}, []
+    for f in files:
+        with open(f, newline="") as fh:
+            for r in csv.DictReader(fh):
+                k = _short_name(r["Name"])
+                c = kern.setdefault(k, [0, 0.0])
+                c[0] += int(r["Calls"])
+                c[1] += float(r["TotalDurationNs"]) / 1e3
+                table.append((k, int(r["Calls"]), float(r["AverageNs"]) / 1e3,
+                              float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
+                              float(r["TotalDurationNs"]) / 1e6, float(r["Percentage"])))
+    builds = kern.get("k_quant", [0])[0]
+    if builds <= 0:
+        raise SystemExit("no build kernel (k_quant) in the trace")
+    us, names = {}, {}
+    for k, (calls, tot) in kern.items():
+        cls = trace_class(k)
+        us[cls] = us.get(cls, 0.0) + tot / (builds if cls == "build" else nsteps)
+        names.setdefault(cls, []).append(k)
+    bf16 = any(L.op == "conv" and L.dtype == "bf16" for L in wl.layers)
+    flops, _ = acc.conv_flops()
+    pool_bytes = sum(acc.work(t, L) for L in wl.layers if L.op in ("pool", "unpool")
+                     for t in (L.op + "_fwd", L.op + "_bwd"))
+    rows = []
+    if us.get("build"):
+        rows.append(("build", "build", acc.work("build", None), us["build"]))
+    if us.get("pool"):
+        rows.append(("pool + unpool, fwd + bwd", "pool", pool_bytes, us["pool"]))
+    conv_all = us.get("conv_main", 0.0) + us.get("conv_helper", 0.0)
+    rows.append(("conv fwd + bwd, every kernel", "conv", flops, conv_all))
+    rows.append(("conv fwd + bwd, main kernels", "conv", flops, us.get("conv_main", 0.0)))
+    print(f"Workload `{wl.name}`: {nsteps} network steps and {builds} builds in the trace; "
+          f"per-step figures divide each class's total kernel time by those counts. The "
+          f"profiled run's own line: {line['ms_per_step']} ms/step.\n")
+    print("| class | kernel time per step (us) | algorithmic work per step | achieved | peak | "
+          "share of peak |")
+    print("|---|---|---|---|---|---|")
+    for label, cls, work, t in rows:
+        r = op_rate(cls, work, t, bf16)
+        w = f"{work / 1e9:.3f} GFLOP" if cls == "conv" else f"{work / 1e6:.2f} MB"
+        print(f"| {label} | {t:.1f} | {w} | {r['achieved']:.1f} {r['unit']} | {r['peak']:g} | "
+              f"{100 * r['frac']:.1f}% |")
+    for cls in ("conv_helper", "other"):
+        if us.get(cls):
+            print(f"| {cls.replace('_', ' ')} kernels ({', '.join(sorted(names[cls]))}) | "
+                  f"{us[cls]:.1f} | | | | |")
+    print(f"\nSum of kernel time per step: {sum(us.values()):.1f} us.\n")
+    print("Per kernel (rocprofv3 statistics; names longer than 90 characters cut):\n")
+    print("| kernel | calls | avg us | min us | max us | total ms | % |")
+    print("|---|---|---|---|---|---|---|")
+    for k, n, avg, mn, mx, tot, pc in sorted(table, key=lambda r: -r[5]):
+        k = k if len(k) <= 90 else k[:87] + "..."
+        print(f"| `{k}` | {n} | {avg:.2f} | {mn:.2f} | {mx:.2f} | {tot:.3f} | {pc:.2f} |")
+
+
+class Accounting:
+    """Algorithmic work of a workload's ops from its per-depth sizes: N[l]
+    octants and M[l] non-empty octants at depth l, npoints points."""
+
+    def __init__(self, wl, N, M, npoints):
+        self.wl, self.N, self.M, self.npoints = wl, list(N), list(M), npoints
+
+    def _n_out(self, L):
+        if L.op == "conv":
+            return self.N[L.depth] if L.stride == 1 else self.N[L.depth - 1]
+        if L.op == "pool":
+            return self.N[L.depth - 1]
+        return self.N[L.depth]
+
+    def conv_flops(self):
+        """Algorithmic flops of the step's conv passes (forward, weight gradient,
+        and input gradient except for the first layer, whose input is the
+        octree's signal) and the output octants of every conv layer."""
+        f = o = 0
+        for li, L in enumerate(self.wl.layers):
+            if L.op == "conv":
+                n = self._n_out(L)
+                f += (6 if li > 0 else 4) * n * L.ksize ** 3 * L.cin * L.cout
+                o += n
+        return f, o
+
+    def work(self, tag, L):
+        """Algorithmic flops (MFMA-bound classes) or HBM bytes of one launch."""
+        N, M = self.N, self.M
+        if tag == "build_emit":  # counted with the first half
+            return 0
+        if tag == "build":
+            d = self.wl.depth
+            return (self.npoints * 24 + sum(8 * N[k] + 4 * M[k] for k in range(d + 1))
+                    + 16 * N[d] + sum(108 * M[k - 1] for k in range(1, d + 1)))
+        if tag.startswith("conv"):
+            n = self._n_out(L)
+            return 2 * n * L.ksize ** 3 * L.cin * L.cout
+        l, c = L.depth, L.cin
+        if tag == "pool_fwd":
+            return N[l] * c * 4 + N[l - 1] * 4 + N[l - 1] * c * 4 + M[l - 1] * c
+        if tag == "pool_bwd":
+            return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l] * c * 4
+        if tag == "unpool_fwd":  # parent rows and switches in, every child row out
+            return M[l - 1] * c * 5 + M[l - 1] * 4 + N[l] * c * 4
+        if tag == "unpool_bwd":  # the routed child of each (parent, channel) in, parent rows out
+            return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l - 1] * c * 4
+        return 0
+
+
+    def op_class(self, tag):
+        """Op class of a tag: the build's two halves are one class."""
+        return "build" if tag.startswith("build") else tag
+
+
+class Step(Accounting):
     """Enqueue one build + forward + backward of a workload's network."""
 
     def __init__(self, oc, torch, synth, wl):
@@ -286,49 +468,6 @@ class Step:
                     self.kname[(li, tag)] = oc.oc_conv_kernel(tree, L.depth, L.ksize, L.stride,
                                                               L.cin, L.cout, ps, dt)
         tree.free()
-
-    def _n_out(self, L):
-        if L.op == "conv":
-            return self.N[L.depth] if L.stride == 1 else self.N[L.depth - 1]
-        if L.op == "pool":
-            return self.N[L.depth - 1]
-        return self.N[L.depth]
-
-    # --- accounting -------------------------------------------------------
-    def conv_flops(self):
-        """Algorithmic flops of the step's conv passes (forward, weight gradient,
-        and input gradient except for the first layer, whose input is the
-        octree's signal) and the output octants of every conv layer."""
-        f = o = 0
-        for li, L in enumerate(self.wl.layers):
-            if L.op == "conv":
-                n = self._n_out(L)
-                f += (6 if li > 0 else 4) * n * L.ksize ** 3 * L.cin * L.cout
-                o += n
-        return f, o
-
-    def work(self, tag, L):
-        """Algorithmic flops (MFMA-bound classes) or HBM bytes of one launch."""
-        N, M = self.N, self.M
-        if tag == "build_emit":  # counted with the first half
-            return 0
-        if tag == "build":
-            d = self.wl.depth
-            return (self.npoints * 24 + sum(8 * N[k] + 4 * M[k] for k in range(d + 1))
-                    + 16 * N[d] + sum(108 * M[k - 1] for k in range(1, d + 1)))
-        if tag.startswith("conv"):
-            n = self._n_out(L)
-            return 2 * n * L.ksize ** 3 * L.cin * L.cout
-        l, c = L.depth, L.cin
-        if tag == "pool_fwd":
-            return N[l] * c * 4 + N[l - 1] * 4 + N[l - 1] * c * 4 + M[l - 1] * c
-        if tag == "pool_bwd":
-            return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l] * c * 4
-        if tag == "unpool_fwd":  # parent rows and switches in, every child row out
-            return M[l - 1] * c * 5 + M[l - 1] * 4 + N[l] * c * 4
-        if tag == "unpool_bwd":  # the routed child of each (parent, channel) in, parent rows out
-            return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l - 1] * c * 4
-        return 0
 
     # --- one step ----------------------------------------------------------
     def key(self, tag, li):
@@ -534,6 +673,9 @@ def main():
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters, args.copy_probe, args.workload)
         return
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
               f"(the path would shard by shape with one dW all-reduce per layer, not built)",
@@ -620,6 +762,22 @@ def main():
     if traffic:
         roofline["traffic_detail"] = traffic
 
+    # every op class's main kernels in the warmup, against its work
+    ops = {}
+    for v in warm.values():
+        c = ops.setdefault(step.op_class(v["op"]), [0.0, 0.0])
+        c[0] += v["ms"] * 1e3 / nwarm
+        c[1] += v["work"] / nwarm
+    bf16 = any(L.op == "conv" and L.dtype == "bf16" for L in wl.layers)
+    # the build's events also span host work (the wait for its counts): its
+    # rate comes from a kernel trace (--summarize-trace) instead
+    ops.pop("build", None)
+    ops_out = {c: op_rate(c, w, t, bf16) for c, (t, w) in sorted(ops.items()) if t > 0 and w > 0}
+    conv = [v for c, v in ops.items() if c.startswith("conv")]
+    if conv:
+        ops_out["conv_fwd_bwd"] = op_rate("conv", sum(w for _, w in conv),
+                                          sum(t for t, _ in conv), bf16)
+
     if args.layers:
         for key, v in sorted(warm.items(), key=lambda kv: -kv[1]["ms"]):
             per = {}
@@ -668,6 +826,9 @@ def main():
         },
         "octants_per_s": round(octants / (ms * 1e-3), 1),
         "roofline": roofline,
+        "ops": ops_out,
+        "ops_scope": "warmup HIP events around the main kernel of each op (conv split sums and "
+                     "ReLU masks not included; the build is measured from a kernel trace)",
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -397,11 +397,14 @@ __global__ __launch_bounds__(TB) void k_scan_c(Levels L, const uint32_t* __restr
 //    contiguous cell range), scans the shape's points and adds the normals of
 //    those in range into LDS in 64-bit fixed point, 2^s units with
 //    s = 62 - e for P * max|n| < 2^e: no sum can overflow and integer
-//    additions make the result independent of their order.
+//    additions make the result independent of their order.  The scan reads
+//    four cells per 16-byte load; each wave queues its in-range points in LDS
+//    and adds them with all lanes, so the few in-range points of a pass cost
+//    one round of lookups and atomics rather than one per point slot.
 
 constexpr int LM_TB = 1024;
-constexpr int LM_LEAVES = 512;  // 512 * (3 * 8 + 4) bytes of LDS
-constexpr int LM_UNROLL = 4;    // points in flight per thread
+constexpr int LM_LEAVES = 2048;  // 2048 * (3 * 8 + 4) bytes of LDS, plus the queues
+constexpr int LM_UNROLL = 2;     // 16-byte loads (four points each) per thread and pass
 
 __device__ __forceinline__ int fixed_shift(uint32_t maxbits, int P) {
   const double m = (double)__uint_as_float(maxbits) * (double)P;
@@ -418,8 +421,10 @@ __global__ __launch_bounds__(LM_TB) void k_leaf_mean(const float* __restrict__ n
                                                      const uint32_t* __restrict__ ucell,
                                                      const uint32_t* __restrict__ info,
                                                      float* __restrict__ leafmean) {
+  constexpr int NP = 4 * LM_UNROLL;  // points per lane and pass
   __shared__ unsigned long long sum[3 * LM_LEAVES];
   __shared__ int32_t cnt[LM_LEAVES];
+  __shared__ uint2 queue[LM_TB / 64][NP * 64];  // per wave: (point, cell) in range
   if (info[0]) return;  // the build fails on any bad input
   const int b = blockIdx.x, d = L.depth;
   const int32_t mb = pre[L.wbase[d]], md = pre[L.wbase[d + 1]] - mb;
@@ -438,40 +443,71 @@ __global__ __launch_bounds__(LM_TB) void k_leaf_mean(const float* __restrict__ n
   }
   __syncthreads();
   const int s = fixed_shift(info[1], P);
-  const int i1 = S.offs[b + 1];
-  for (int i = S.offs[b] + threadIdx.x; i < i1; i += LM_UNROLL * LM_TB) {
-    uint32_t cu[LM_UNROLL];
+  auto in_range = [&](uint32_t c) { return c >= clo && (uint64_t)c < chi; };
+  // a point of the shape whose leaf is in range adds its normal and a count
+  auto add = [&](int64_t i, uint32_t c) {
+    const int64_t wi = L.wbase[d] + (int64_t)(c >> 5);
+    const int32_t j = pre[wi] - mb + __popc(bits[wi] & ((1u << (c & 31)) - 1u)) - lo;
 #pragma unroll
-    for (int u = 0; u < LM_UNROLL; ++u)
-      cu[u] = i + u * LM_TB < i1 ? leafcell[i + u * LM_TB] : 0xFFFFFFFFu;
-    // every load of the in-range points first, then their additions
-    bool in[LM_UNROLL];
-    uint32_t wv[LM_UNROLL];
-    int32_t pv[LM_UNROLL];
-    float nv[LM_UNROLL][3];
+    for (int a = 0; a < 3; ++a) {
+      const long long v = llrint(ldexp((double)nrm[3 * i + a], s));
+      atomicAdd(&sum[3 * j + a], (unsigned long long)v);
+    }
+    atomicAdd(&cnt[j], 1);
+  };
+  // the shape's points: a 16-byte-aligned body read four cells per load, and
+  // the points before and after it
+  const int i0 = S.offs[b], i1 = S.offs[b + 1];
+  const int a0 = ((i0 + 3) & ~3) < i1 ? ((i0 + 3) & ~3) : i1;
+  const int a1 = (i1 & ~3) > a0 ? (i1 & ~3) : a0;
+  const int t = threadIdx.x;
+  if (t < a0 - i0 && in_range(leafcell[i0 + t])) add(i0 + t, leafcell[i0 + t]);
+  if (t < i1 - a1 && in_range(leafcell[a1 + t])) add(a1 + t, leafcell[a1 + t]);
+  // body: LM_UNROLL 16-byte loads per thread and pass.  Most points of a
+  // pass are out of range, so each wave compacts its in-range points into a
+  // queue in LDS (ballot + lane count) and then adds them with every lane
+  // busy, after issuing the next pass's cell loads.
+  const uint4* lc4 = reinterpret_cast<const uint4*>(leafcell);
+  const int v1 = a1 >> 2;
+  const int lane = t & 63;
+  uint2* qw = queue[t >> 6];
+  auto load_cells = [&](int v, uint32_t (&c)[NP]) {
 #pragma unroll
     for (int u = 0; u < LM_UNROLL; ++u) {
-      in[u] = cu[u] >= clo && (uint64_t)cu[u] < chi;
-      if (in[u]) {
-        const int64_t wi = L.wbase[d] + (int64_t)(cu[u] >> 5);
-        wv[u] = bits[wi];
-        pv[u] = pre[wi];
-        const int64_t pi = i + u * LM_TB;
-#pragma unroll
-        for (int a = 0; a < 3; ++a) nv[u][a] = nrm[3 * pi + a];
-      }
+      uint4 q = make_uint4(0u, 0u, 0u, 0u);
+      if (v + u * LM_TB < v1) q = lc4[v + u * LM_TB];
+      c[4 * u] = q.x, c[4 * u + 1] = q.y, c[4 * u + 2] = q.z, c[4 * u + 3] = q.w;
     }
+  };
+  uint32_t cc[NP];
+  const int vb = (a0 >> 2) + t - lane;  // the wave's first load index
+  load_cells(vb + lane, cc);
+  // every lane of a wave runs the same passes (wave-uniform loop bounds)
+  for (int v = vb; v < v1; v += LM_UNROLL * LM_TB) {
+    int n = 0;  // in-range points queued by the wave
 #pragma unroll
-    for (int u = 0; u < LM_UNROLL; ++u) {
-      if (!in[u]) continue;
-      const int32_t j = pv[u] - mb + __popc(wv[u] & ((1u << (cu[u] & 31)) - 1u)) - lo;
-#pragma unroll
-      for (int a = 0; a < 3; ++a) {
-        const long long v = llrint(ldexp((double)nv[u][a], s));
-        atomicAdd(&sum[3 * j + a], (unsigned long long)v);
+    for (int k = 0; k < NP; ++k) {
+      const int vi = v + lane + (k / 4) * LM_TB;
+      const bool in = vi < v1 && in_range(cc[k]);
+      const uint64_t m = __ballot(in);
+      if (in) {
+        const int pos = n + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        qw[pos] = make_uint2((uint32_t)(4 * vi + (k & 3)), cc[k]);
       }
-      atomicAdd(&cnt[j], 1);
+      n += __popcll(m);
     }
+    load_cells(v + LM_UNROLL * LM_TB + lane, cc);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int r = lane; r < n; r += 64) {
+      const uint2 e = qw[r];
+      add((int64_t)e.x, e.y);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   __syncthreads();
   const double unit = ldexp(1.0, -s);
