@@ -265,7 +265,7 @@ TRACE_CLASSES = (
     ("build", ("k_quant", "k_mark", "k_reduce", "k_scan_a", "k_scan_c", "k_leaf_mean", "k_emit",
                "__amd_rocclr_copyBuffer")),
     ("pool", ("k_pool_fwd", "k_route_down", "k_route_up")),
-    ("conv_main", ("k_conv_", "Cijk_")),
+    ("conv_main", ("k_conv_", "k_cin_", "Cijk_")),
     ("conv_helper", ("k_sum_", "k_relu_mask", "k_bf_", "k_bf16_to_f32", "k_s2_", "k_fill_u32")),
 )
 

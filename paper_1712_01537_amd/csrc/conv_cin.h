@@ -1,0 +1,32 @@
+// Launchers of the first-layer convolution kernels (conv_cin.hip): K = 3 with
+// 3 or 4 input channels (the input signal), fp32.
+#pragma once
+
+#include "common.h"
+
+namespace oc {
+
+// True when conv_cin_fwd / conv_cin_dw take this shape (K = 3, cin 3 or 4,
+// cout a positive multiple of 16).
+bool conv_cin_supported(int K, int cin, int cout);
+
+// y [N_l][cout] = conv(x [N_l][cin], w [27][cin][cout]), stride 1; relu != 0
+// applies max(0, .).
+void conv_cin_fwd(const oc_octree* t, int l, const float* x, int cin, const float* w, int cout,
+                  float* y, int relu, hipStream_t s);
+
+// Number of [27][cin][cout] fp32 partial sums conv_cin_dw needs.
+size_t conv_cin_dw_parts(const oc_octree* t, int l, int cin, int cout);
+
+// dw [27][cin][cout] = weight gradient for upstream gradient dy [N_l][cout];
+// part holds conv_cin_dw_parts() partial sums.
+void conv_cin_dw(const oc_octree* t, int l, const float* x, int cin, const float* dy, int cout,
+                 float* dw, float* part, hipStream_t s);
+
+// Name of the kernel of pass 0 (forward) or 2 (weight gradient).
+void conv_cin_kernel_name(int cin, int pass, char* buf, size_t n);
+
+// Fixed-order sum of np partials of n fp32 entries (conv_mfma.hip).
+void sum_partials(const float* part, int np, int64_t n, float* out, hipStream_t s);
+
+}  // namespace oc

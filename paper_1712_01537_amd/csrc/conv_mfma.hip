@@ -30,8 +30,11 @@
 // order, so results do not depend on scheduling.
 #include "conv_mfma.h"
 
+#include "conv_cin.h"
+
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 namespace {
 
@@ -1247,87 +1250,57 @@ __global__ __launch_bounds__(TB * HV) void k_conv_dwt(const int32_t* __restrict_
   }
 }
 
-// Fixed-order sum of np partials of n entries, in two passes: pass 1 adds
-// segment y (partials y*sp .. y*sp+sp-1) of 64 entries per workgroup, four
-// interleaved sub-sums per entry combined in order; pass 2 adds the segments.
-__global__ __launch_bounds__(TB) void k_sum_parts1(const float* __restrict__ part, int np, int sp,
-                                                   int64_t n, float* __restrict__ seg) {
-  __shared__ float r[4][64];
-  const int el = threadIdx.x & 63, sg = threadIdx.x >> 6;
-  const int64_t e = (int64_t)blockIdx.x * 64 + el;
-  const int p0 = blockIdx.y * sp, p1 = p0 + sp < np ? p0 + sp : np;
-  float s = 0.f;
-  if (e < n) {
-    int p = p0 + sg;
-    for (; p + 12 < p1; p += 16) {  // four independent loads in flight
-      const float a = part[(int64_t)p * n + e], b = part[(int64_t)(p + 4) * n + e];
-      const float c = part[(int64_t)(p + 8) * n + e], d = part[(int64_t)(p + 12) * n + e];
-      s += a;
-      s += b;
-      s += c;
-      s += d;
+// Fixed-order sum of np partials of n entries in one pass: a workgroup takes
+// TB / SUB entry slots (four consecutive entries each when V = 4: n a multiple
+// of 4, 16-byte aligned buffers), and thread (slot, k) adds partials k,
+// k + SUB, k + 2 SUB, ... in order, four loads in flight; the SUB sub-sums of
+// a slot are then added in k order.  SUB = 64 gives small n enough threads.
+template <int SUB, int V>
+__global__ __launch_bounds__(TB) void k_sum_parts(const float* __restrict__ part, int np,
+                                                  int64_t n, float* __restrict__ out) {
+  using vec = std::conditional_t<V == 4, v4f, float>;
+  constexpr int SLOTS = TB / SUB;
+  __shared__ vec r[SUB][SLOTS];
+  const int el = threadIdx.x % SLOTS, sg = threadIdx.x / SLOTS;
+  const int64_t nv = n / V, e = (int64_t)blockIdx.x * SLOTS + el;
+  const vec* pv = reinterpret_cast<const vec*>(part);
+  vec acc = {};
+  if (e < nv) {
+    int p = sg;
+    for (; p + 3 * SUB < np; p += 4 * SUB) {  // four independent loads in flight
+      const vec a = pv[(int64_t)p * nv + e], b = pv[(int64_t)(p + SUB) * nv + e];
+      const vec c = pv[(int64_t)(p + 2 * SUB) * nv + e], d = pv[(int64_t)(p + 3 * SUB) * nv + e];
+      acc += a;
+      acc += b;
+      acc += c;
+      acc += d;
     }
-    for (; p < p1; p += 4) s += part[(int64_t)p * n + e];
+    for (; p < np; p += SUB) acc += pv[(int64_t)p * nv + e];
   }
-  r[sg][el] = s;
+  r[sg][el] = acc;
   __syncthreads();
-  if (sg == 0 && e < n) seg[(int64_t)blockIdx.y * n + e] = ((r[0][el] + r[1][el]) + r[2][el]) + r[3][el];
-}
-
-// k_sum_parts1 with four consecutive entries per lane (n a multiple of 4,
-// 16-byte aligned buffers): 256 entries per workgroup, the same order of
-// additions per entry.
-__global__ __launch_bounds__(TB) void k_sum_parts1v(const float* __restrict__ part, int np, int sp,
-                                                    int64_t n, float* __restrict__ seg) {
-  __shared__ v4f r[4][64];
-  const int el = threadIdx.x & 63, sg = threadIdx.x >> 6;
-  const int64_t e4 = (int64_t)blockIdx.x * 64 + el, n4 = n / 4;
-  const int p0 = blockIdx.y * sp, p1 = p0 + sp < np ? p0 + sp : np;
-  const v4f* pv = reinterpret_cast<const v4f*>(part);
-  v4f s = {0.f, 0.f, 0.f, 0.f};
-  if (e4 < n4) {
-    int p = p0 + sg;
-    for (; p + 12 < p1; p += 16) {  // four independent loads in flight
-      const v4f a = pv[(int64_t)p * n4 + e4], b = pv[(int64_t)(p + 4) * n4 + e4];
-      const v4f c = pv[(int64_t)(p + 8) * n4 + e4], d = pv[(int64_t)(p + 12) * n4 + e4];
-      s += a;
-      s += b;
-      s += c;
-      s += d;
-    }
-    for (; p < p1; p += 4) s += pv[(int64_t)p * n4 + e4];
+  if (sg == 0 && e < nv) {
+    vec t = r[0][el];
+#pragma unroll 8
+    for (int k = 1; k < SUB; ++k) t += r[k][el];
+    reinterpret_cast<vec*>(out)[e] = t;
   }
-  r[sg][el] = s;
-  __syncthreads();
-  if (sg == 0 && e4 < n4)
-    reinterpret_cast<v4f*>(seg)[(int64_t)blockIdx.y * n4 + e4] =
-        ((r[0][el] + r[1][el]) + r[2][el]) + r[3][el];
 }
 
-__global__ __launch_bounds__(TB) void k_sum_parts2(const float* __restrict__ seg, int ns, int64_t n,
-                                                   float* __restrict__ out) {
-  const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (e >= n) return;
-  float s = 0.f;
-  for (int y = 0; y < ns; ++y) s += seg[(int64_t)y * n + e];
-  out[e] = s;
-}
-
-// Segments of the two-pass sum: about 64 partials each, enough workgroups.
-inline int sum_segments(int np) { return np <= 64 ? 1 : (int)oc::cdiv(np, 64); }
-
-void sum_parts(const float* part, int np, int64_t n, float* seg, float* out, hipStream_t s) {
-  const int ns = sum_segments(np), sp = (int)oc::cdiv(np, ns);
-  float* dst = ns == 1 ? out : seg;
-  if (n % 4 == 0 && (uintptr_t)part % 16 == 0 && (uintptr_t)dst % 16 == 0)
-    hipLaunchKernelGGL(k_sum_parts1v, dim3((unsigned)oc::cdiv(n, 256), (unsigned)ns), dim3(TB), 0, s,
-                       part, np, sp, n, dst);
+void sum_parts(const float* part, int np, int64_t n, float* out, hipStream_t s) {
+  const bool v4 = n % 4 == 0 && (uintptr_t)part % 16 == 0 && (uintptr_t)out % 16 == 0;
+  const int64_t nv = v4 ? n / 4 : n;
+  // 16 sub-sums per slot when that gives two workgroups per CU, else 64
+  const bool wide = oc::cdiv(nv, TB / 16) >= 2 * (int64_t)oc::cu_count();
+  const unsigned grid = (unsigned)oc::cdiv(nv, TB / (wide ? 16 : 64));
+  if (v4 && wide)
+    hipLaunchKernelGGL((k_sum_parts<16, 4>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
+  else if (v4)
+    hipLaunchKernelGGL((k_sum_parts<64, 4>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
+  else if (wide)
+    hipLaunchKernelGGL((k_sum_parts<16, 1>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
   else
-    hipLaunchKernelGGL(k_sum_parts1, dim3((unsigned)oc::cdiv(n, 64), (unsigned)ns), dim3(TB), 0, s,
-                       part, np, sp, n, dst);
-  if (ns > 1)
-    hipLaunchKernelGGL(k_sum_parts2, dim3((unsigned)oc::cdiv(n, TB)), dim3(TB), 0, s,
-                       (const float*)seg, ns, n, out);
+    hipLaunchKernelGGL((k_sum_parts<64, 1>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
 }
 
 // ---------------------------------------------------------------------------
@@ -1615,6 +1588,10 @@ namespace oc {
 
 void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, int pass, char* buf,
                          size_t n) {
+  if (pass != 1 && conv_cin_supported(K, cin, cout)) {
+    conv_cin_kernel_name(cin, pass, buf, n);
+    return;
+  }
   if (pass == 2) {
     DwtCfg d;
     if (pick_dwt(K, t->M[l - 1], cin, cout, &d)) {
@@ -1647,6 +1624,10 @@ size_t conv_s1_tile_ws(const oc_octree* t, int l, int K, int kk, int nn) {
 
 void conv_s1_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin, const float* w,
                      int cout, float* y, int relu, float* ws, hipStream_t s) {
+  if (conv_cin_supported(K, cin, cout)) {
+    conv_cin_fwd(t, l, x, cin, w, cout, y, relu, s);
+    return;
+  }
   if (use_cin_kernel(K, cin, cout)) {
     const int64_t G = t->M[l - 1];
     const dim3 grid((unsigned)oc::cdiv(G, 8), (unsigned)oc::cdiv(cout, 16));
@@ -1667,6 +1648,7 @@ void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, int
 }
 
 size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout) {
+  if (conv_cin_supported(K, cin, cout)) return conv_cin_dw_parts(t, l, cin, cout);
   DwtCfg d;
   int64_t np;
   if (pick_dwt(K, t->M[l - 1], cin, cout, &d)) {
@@ -1674,18 +1656,21 @@ size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout) {
   } else {
     np = pick_dw(K, t->M[l - 1], cin, cout).nchunks;
   }
-  const int ns = sum_segments((int)np);
-  return (size_t)np + (ns > 1 ? ns : 0);  // partials, then pass-1 segments
+  return (size_t)np;
 }
 
 void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, int cin,
                             const float* dy, int cout, float* dw, float* part,
                             hipStream_t s) {
   const int64_t entries = (int64_t)K * K * K * cin * cout;
+  if (conv_cin_supported(K, cin, cout)) {
+    conv_cin_dw(t, l, x, cin, dy, cout, dw, part, s);
+    return;
+  }
   DwtCfg d;
   if (pick_dwt(K, t->M[l - 1], cin, cout, &d)) {
     if (dispatch_dwt(t, l, d, x, cin, dy, cout, part, s)) {
-      sum_parts(part, (int)d.nchunks, entries, part + d.nchunks * entries, dw, s);
+      sum_parts(part, (int)d.nchunks, entries, dw, s);
     } else {
       oc::set_error("no weight-gradient kernel for cin=%d cout=%d", cin, cout);
     }
@@ -1714,7 +1699,11 @@ void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, in
     oc::set_error("no weight-gradient kernel for K=%d cin=%d cout=%d", K, cin, cout);
   }
 #undef OC_DW
-  sum_parts(part, (int)c.nchunks, entries, part + c.nchunks * entries, dw, s);
+  sum_parts(part, (int)c.nchunks, entries, dw, s);
+}
+
+void sum_partials(const float* part, int np, int64_t n, float* out, hipStream_t s) {
+  sum_parts(part, np, n, out, s);
 }
 
 }  // namespace oc
