@@ -1455,7 +1455,10 @@ bool pick_dwt(int K, int64_t G, int cin, int cout, DwtCfg* c) {
     c->NBN = cout <= 16 ? 1 : 2;
   } else {
     c->CW = 16, c->GS = 4;
-    c->NBN = cout >= 64 ? 4 : cout >= 32 ? 2 : 1;
+    // 32 output channels per workgroup: 64 writes twice the partial sums (one
+    // per resident workgroup) and 16 stages x twice as often; both were
+    // measured slower on the depth-2..5 layers of the 32-shape batch
+    c->NBN = cout >= 32 ? 2 : 1;
   }
   c->HV = c->flat ? 1 : 2;
   const int nCB = c->flat ? 1 : (int)oc::cdiv(cin, 16);
