@@ -1,0 +1,102 @@
+"""Host-side accounting of bench.py (no GPU): kernel-name handling, the op
+rates against the MI355X peaks, and the per-class summary of a kernel trace,
+on small hand-made rocprofv3-style files."""
+import json
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+import synth  # noqa: E402
+
+
+def test_short_name_strips_namespace_and_arguments():
+    n = "void (anonymous namespace)::k_conv_tile3<4, 8, false>(int const*, long, float const*)"
+    assert bench._short_name(n) == "k_conv_tile3<4, 8, false>"
+    assert bench._short_name("k_sum_split(float const*, int)") == "k_sum_split"
+    # template arguments that hold parentheses stay whole
+    assert bench._short_name("k_x<(anonymous namespace)::T(1)>(int)") == "k_x<T(1)>"
+
+
+def test_op_rate_units_and_peaks():
+    r = bench.op_rate("conv_fwd", 2e9, 1000.0, False)  # 2 GFLOP in 1 ms
+    assert r["unit"] == "TFLOP/s" and r["achieved"] == pytest.approx(2.0)
+    assert r["frac"] == pytest.approx(2.0 / 157.3, abs=1e-4)  # rounded to 4 places
+    r = bench.op_rate("conv", 2e9, 1000.0, True)
+    assert r["peak"] == 2500.0
+    r = bench.op_rate("pool_fwd", 8e6, 10.0, False)  # 8 MB in 10 us
+    assert r["unit"] == "GB/s" and r["achieved"] == pytest.approx(800.0)
+    assert r["frac"] == pytest.approx(0.1)
+
+
+def test_trace_classes():
+    assert bench.trace_class("k_quant") == "build"
+    assert bench.trace_class("k_leaf_mean") == "build"
+    assert bench.trace_class("k_route_down<4>") == "pool"
+    assert bench.trace_class("k_conv_dwt<false, 16, 2, 4, true, 2>") == "conv_main"
+    assert bench.trace_class("k_cin_fwd<3>") == "conv_main"
+    assert bench.trace_class("Cijk_Ailk_Bljk_BSS_BH") == "conv_main"
+    assert bench.trace_class("k_sum_parts<16, 4>") == "conv_helper"
+    assert bench.trace_class("k_s2_col<unsigned short>") == "conv_helper"
+    assert bench.trace_class("at::native::vectorized_elementwise_kernel") == "other"
+
+
+def _sizes(wl):
+    """Small made-up per-depth sizes: N[l] = 8 M[l-1]."""
+    M = [wl.batch * 2 ** l for l in range(wl.depth + 1)]
+    N = [wl.batch] + [8 * M[l - 1] for l in range(1, wl.depth + 1)]
+    return N, M
+
+
+def test_conv_flops_by_hand():
+    wl = synth.WORKLOADS["net_d5"]
+    N, M = _sizes(wl)
+    acc = bench.Accounting(wl, N, M, 1000)
+    f, o = acc.conv_flops()
+    want = 0
+    for li, L in enumerate(wl.layers):
+        if L.op == "conv":
+            passes = 3 if li > 0 else 2  # the first layer has no input gradient
+            want += passes * 2 * N[L.depth] * 27 * L.cin * L.cout
+    assert f == want
+    assert o == sum(N[L.depth] for L in wl.layers if L.op == "conv")
+
+
+def test_summarize_trace(tmp_path, capsys):
+    wl = synth.WORKLOADS["net_d5"]
+    N, M = _sizes(wl)
+    acc = bench.Accounting(wl, N, M, 1000)
+    flops, _ = acc.conv_flops()
+    line = {"metric": "m", "steps": 3, "warmup": 2, "ms_per_step": 1.0,
+            "config": {"workload": "net_d5", "octants_per_depth": N, "nonempty_per_depth": M,
+                       "points": 1000}}
+    (tmp_path / "run.log").write_text("[bench] noise\n" + json.dumps(line) + "\n")
+    d = tmp_path / "prof"
+    d.mkdir()
+    # 5 network steps (warmup 2 + 3 timed), 6 builds; times in ns
+    rows = [("void (anonymous namespace)::k_conv_tile3<4, 8, false>(int)", 15, 15 * 40000),
+            ("k_sum_split(float const*)", 10, 10 * 5000),
+            ("k_pool_fwd<4>(float const*)", 20, 20 * 4000),
+            ("k_quant(float const*)", 6, 6 * 7000),
+            ("k_emit(int)", 6, 6 * 10000),
+            ("at::native::copy(int)", 5, 5 * 2000)]
+    with open(d / "run_kernel_stats.csv", "w") as fh:
+        fh.write('"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs","StdDev"\n')
+        for name, calls, tot in rows:
+            fh.write(f'"{name}",{calls},{tot},{tot / calls},1.0,{tot / calls},{tot / calls},0\n')
+    bench.summarize_trace(str(d), str(tmp_path / "run.log"))
+    out = capsys.readouterr().out
+    # per step: conv main 15 * 40 / 5 = 120 us, helpers 10 * 5 / 5 = 10 us;
+    # build (7 + 10) us per build; pooling 20 * 4 / 5 = 16 us
+    assert "| conv fwd + bwd, main kernels | 120.0 |" in out
+    assert "| conv fwd + bwd, every kernel | 130.0 |" in out
+    assert "| build | 17.0 |" in out
+    assert "| pool + unpool, fwd + bwd | 16.0 |" in out
+    tf = flops / 120e-6 / 1e12
+    assert f"{tf:.1f} TFLOP/s" in out
+    assert "other kernels (at::native::copy)" in out
+    assert "`k_conv_tile3<4, 8, false>` | 15 | 40.00 |" in out
