@@ -237,6 +237,47 @@ def conv_s2_bwd(tree: Octree, l, x, w, dy):
     return dx, dw
 
 
+def deconv_fwd(nb, x, w, n_out, want=None):
+    """Stride-1 octree deconvolution (Sec. 3.2 "Deconvolution"): the
+    convolution with its forward and backward passes swapped, so its forward
+    is the convolution's input gradient.  w [K^3][cout][cin] is the weight of
+    the convolution cout -> cin that it transposes; x [N_l][cin] -> [N_l][cout].
+    want: optional bool mask of output rows to compute."""
+    return conv_bwd_data(nb, x, w, n_out, want=want)
+
+
+def deconv_bwd(nb, x, w, dy, rows=None, entries=None):
+    """Backward of deconv_fwd, the convolution's forward and weight gradient:
+    dx = conv(dy; w) [N_l][cin]; dw[k][co][ci] = sum_i dy[nb(i,k)][co] x[i][ci].
+    rows / entries: optional subsets of dx rows and flat dw entries."""
+    dx = conv_fwd(nb, dy, w, rows=rows)
+    dw = conv_bwd_weight(nb, dy, x, w.shape[0], entries=entries)
+    return dx, dw
+
+
+def deconv_s2_fwd(tree: Octree, l, x, w, want=None):
+    """Stride-2 deconvolution from depth l-1 to depth l: the transpose of the
+    stride-2 convolution at depth l (Sec. 3.2).  Row i of x [N_{l-1}][cin]
+    counts only when its octant is non-empty (label p > 0); it reaches the
+    depth-l neighbourhood of the first sibling of group p-1.  -> [N_l][cout]."""
+    K = round(w.shape[0] ** (1 / 3))
+    nb = tree.neighbors(l, K, stride=2)
+    xhat = renew_bwd(tree.labels(l - 1), x, nb.shape[0])
+    return conv_bwd_data(nb, xhat, w, tree.num(l), want=want)
+
+
+def deconv_s2_bwd(tree: Octree, l, x, w, dy, entries=None):
+    """Backward of deconv_s2_fwd: dx = the stride-2 convolution of dy
+    [N_l][cout] ([N_{l-1}][cin], zero at empty octants), dw as in deconv_bwd
+    over the groups' first siblings."""
+    K = round(w.shape[0] ** (1 / 3))
+    nb = tree.neighbors(l, K, stride=2)
+    dx = renew(tree.labels(l - 1), conv_fwd(nb, dy, w))
+    xhat = renew_bwd(tree.labels(l - 1), x, nb.shape[0])
+    dw = conv_bwd_weight(nb, dy, xhat, w.shape[0], entries=entries)
+    return dx, dw
+
+
 def pool_fwd(labels_lm1, x):
     labels_lm1 = _i32(labels_lm1)
     x = _f64(x)

@@ -235,3 +235,75 @@ def test_relu():
     x = np.array([-1.0, 0.0, 2.0])
     assert oracle.relu_fwd(x).tolist() == [0.0, 0.0, 2.0]
     assert oracle.relu_bwd(x, np.array([5.0, 6.0, 7.0])).tolist() == [0.0, 0.0, 7.0]
+
+
+# Deconvolution (Sec. 3.2): the transpose of the octree convolution.  Dense
+# form: conv_transpose3d of the input scattered to the grid (zero where no
+# octant exists), read at the existing octants; its weight tensor is the one
+# of the convolution cout -> cin it transposes.
+
+@pytest.mark.parametrize("seed,B,depth,full,K", CASES)
+def test_deconv_equals_dense_conv_transpose3d(seed, B, depth, full, K):
+    t = _tree(seed, B, depth, full)
+    l = depth
+    cin, cout = 6, 5  # deconv channels; w [K^3][cout][cin]
+    rng = np.random.default_rng(200 + seed)
+    x = rng.standard_normal((t.num(l), cin))
+    w = rng.standard_normal((K ** 3, cout, cin))
+    nb = t.neighbors(l, K)
+    y = oracle.deconv_fwd(nb, x, w, t.num(l))
+    xt = torch.as_tensor(x).requires_grad_(True)
+    wt = torch.as_tensor(w).requires_grad_(True)
+    wd = wt.reshape(K, K, K, cout, cin).permute(4, 3, 0, 1, 2)  # [cin][cout][K][K][K]
+    out = _gather(t, l, F.conv_transpose3d(_scatter(t, l, xt), wd, padding=(K - 1) // 2))
+    np.testing.assert_allclose(y, out.detach().numpy(), rtol=1e-12, atol=1e-12)
+    dy = rng.standard_normal((t.num(l), cout))
+    out.backward(torch.as_tensor(dy))
+    dx, dw = oracle.deconv_bwd(nb, x, w, dy)
+    np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(dw, wt.grad.numpy(), rtol=1e-11, atol=1e-11)
+    # subsets agree with the full results
+    want = rng.random(t.num(l)) < 0.3
+    np.testing.assert_array_equal(oracle.deconv_fwd(nb, x, w, t.num(l), want=want)[want], y[want])
+    rows = rng.choice(t.num(l), size=min(9, t.num(l)), replace=False)
+    ent = rng.choice(w.size, size=7, replace=False)
+    dxs, dws = oracle.deconv_bwd(nb, x, w, dy, rows=rows, entries=ent)
+    np.testing.assert_allclose(dxs, dx[rows], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dws, dw.ravel()[ent], rtol=1e-12, atol=1e-12)
+
+
+def test_deconv_is_adjoint_of_conv():
+    # <conv(a; w), b> = <a, deconv(b; w)> for the same weight tensor
+    t = _tree(61, 2, 4, 2)
+    l, K, c1, c2 = 4, 3, 3, 5
+    rng = np.random.default_rng(61)
+    nb = t.neighbors(l, K)
+    w = rng.standard_normal((K ** 3, c1, c2))  # conv c1 -> c2, deconv c2 -> c1
+    a = rng.standard_normal((t.num(l), c1))
+    b = rng.standard_normal((t.num(l), c2))
+    lhs = np.sum(oracle.conv_fwd(nb, a, w) * b)
+    assert np.isclose(lhs, np.sum(a * oracle.deconv_fwd(nb, b, w, t.num(l))), rtol=1e-12)
+
+
+@pytest.mark.parametrize("seed,B,depth,full", [(71, 2, 4, 2), (72, 1, 3, 0), (73, 3, 4, 1)])
+def test_deconv_s2_equals_dense_strided_transpose(seed, B, depth, full):
+    t = _tree(seed, B, depth, full)
+    l, K, cin, cout = depth, 3, 5, 4
+    rng = np.random.default_rng(300 + seed)
+    x = rng.standard_normal((t.num(l - 1), cin))
+    w = rng.standard_normal((K ** 3, cout, cin))
+    y = oracle.deconv_s2_fwd(t, l, x, w)
+    nz = torch.as_tensor((t.labels(l - 1) > 0).astype(np.float64))[:, None]
+    xt = torch.as_tensor(x).requires_grad_(True)
+    wt = torch.as_tensor(w).requires_grad_(True)
+    wd = wt.reshape(K, K, K, cout, cin).permute(4, 3, 0, 1, 2)
+    # rows of empty parents carry nothing (the stride-2 convolution has no output there)
+    out = _gather(t, l, F.conv_transpose3d(_scatter(t, l - 1, xt * nz), wd, stride=2, padding=1,
+                                           output_padding=1))
+    np.testing.assert_allclose(y, out.detach().numpy(), rtol=1e-12, atol=1e-12)
+    dy = rng.standard_normal((t.num(l), cout))
+    out.backward(torch.as_tensor(dy))
+    dx, dw = oracle.deconv_s2_bwd(t, l, x, w, dy)
+    np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(dw, wt.grad.numpy(), rtol=1e-11, atol=1e-11)
+    assert np.all(dx[t.labels(l - 1) == 0] == 0)
