@@ -82,6 +82,9 @@ BOUND = {
     "conv_fwd": "mfma",
     "conv_bwd_data": "mfma",
     "conv_bwd_weight": "mfma",
+    "deconv_fwd": "mfma",
+    "deconv_bwd_data": "mfma",
+    "deconv_bwd_weight": "mfma",
     "pool_fwd": "hbm",
     "pool_bwd": "hbm",
     "unpool_fwd": "hbm",
@@ -245,7 +248,7 @@ def summarize_counters(fetch_dir, write_dir, copy_mib, workload):
 def op_rate(cls, work, us, bf16):
     """Achieved rate of an op class from its algorithmic work (flops of a conv
     class, HBM bytes otherwise) and its time per step, against the peak."""
-    if cls.startswith("conv"):
+    if cls.startswith(("conv", "deconv")):
         a = work / (us * 1e-6) / 1e12
         peak, unit = PEAK["bf16_TFLOPs" if bf16 else "fp32_TFLOPs"], "TFLOP/s"
     else:
@@ -370,16 +373,26 @@ class Accounting:
             return self.N[L.depth - 1]
         return self.N[L.depth]
 
+    def _n_in(self, L):
+        if L.op == "conv" or L.stride == 1:
+            return self.N[L.depth]
+        return self.N[L.depth - 1]  # stride-2 deconvolution, unpooling
+
+    def _n_conv(self, L):
+        """Output rows of the convolution a conv or deconv layer runs (a
+        deconvolution runs the passes of the convolution it transposes)."""
+        return self.N[L.depth] if L.stride == 1 else self.N[L.depth - 1]
+
     def conv_flops(self):
         """Algorithmic flops of the step's conv passes (forward, weight gradient,
         and input gradient except for the first layer, whose input is the
         octree's signal) and the output octants of every conv layer."""
         f = o = 0
         for li, L in enumerate(self.wl.layers):
-            if L.op == "conv":
-                n = self._n_out(L)
+            if L.op in ("conv", "deconv"):
+                n = self._n_conv(L)
                 f += (6 if li > 0 else 4) * n * L.ksize ** 3 * L.cin * L.cout
-                o += n
+                o += self._n_out(L)
         return f, o
 
     def work(self, tag, L):
@@ -391,9 +404,8 @@ class Accounting:
             d = self.wl.depth
             return (self.npoints * 24 + sum(8 * N[k] + 4 * M[k] for k in range(d + 1))
                     + 16 * N[d] + sum(108 * M[k - 1] for k in range(1, d + 1)))
-        if tag.startswith("conv"):
-            n = self._n_out(L)
-            return 2 * n * L.ksize ** 3 * L.cin * L.cout
+        if tag.startswith(("conv", "deconv")):
+            return 2 * self._n_conv(L) * L.ksize ** 3 * L.cin * L.cout
         l, c = L.depth, L.cin
         if tag == "pool_fwd":
             return N[l] * c * 4 + N[l - 1] * 4 + N[l - 1] * c * 4 + M[l - 1] * c
@@ -425,6 +437,9 @@ class Step(Accounting):
         self.dtype = torch.float32
         self.weights = {}
         for li, L in enumerate(wl.layers):
+            if L.op == "deconv":  # the weight of the convolution it transposes
+                w = synth.make_weights(wl, li, L.ksize, L.cout, L.cin)
+                self.weights[li] = torch.as_tensor(w).to(dev)
             if L.op == "conv":
                 w = synth.make_weights(wl, li, L.ksize, L.cin, L.cout)
                 t = torch.as_tensor(w).to(dev)
@@ -446,7 +461,7 @@ class Step(Accounting):
         self.x0 = None
         if not wl.signal_input:
             L0 = wl.layers[0]
-            self.x0 = torch.as_tensor(synth.make_features([wl.seed_id, 3000], self.N[L0.depth],
+            self.x0 = torch.as_tensor(synth.make_features([wl.seed_id, 3000], self._n_in(L0),
                                                           L0.cin)).to(dev)
             if L0.dtype == "bf16":
                 self.x0 = self.x0.to(torch.bfloat16)
@@ -467,6 +482,10 @@ class Step(Accounting):
                 for ps, tag in enumerate(("conv_fwd", "conv_bwd_data", "conv_bwd_weight")):
                     self.kname[(li, tag)] = oc.oc_conv_kernel(tree, L.depth, L.ksize, L.stride,
                                                               L.cin, L.cout, ps, dt)
+            elif L.op == "deconv":  # the transposed convolution's passes, swapped
+                for ps, tag in ((1, "deconv_fwd"), (0, "deconv_bwd_data"), (2, "deconv_bwd_weight")):
+                    self.kname[(li, tag)] = oc.oc_conv_kernel(tree, L.depth, L.ksize, L.stride,
+                                                              L.cout, L.cin, ps)
         tree.free()
 
     # --- one step ----------------------------------------------------------
@@ -552,6 +571,12 @@ class Step(Accounting):
                     tree, L.depth, L.ksize, L.stride, x, w, relu=L.relu))
                 saved.append((li, x, y, None))
                 x = y
+            elif L.op == "deconv":
+                w = self.weights[li]
+                y = self._run("deconv_fwd", li, lambda: oc.oc_deconv_fwd(
+                    tree, L.depth, L.ksize, L.stride, x, w))
+                saved.append((li, x, y, None))
+                x = y
             elif L.op == "pool":
                 p, sw = self._run("pool_fwd", li, lambda: oc.oc_pool_fwd(tree, L.depth, x))
                 saved.append((li, x, p, sw))
@@ -594,6 +619,13 @@ class Step(Accounting):
                             t.record_stream(self.side)
                     tree.record_stream(self.side)
                 g, masked = dx, False
+            elif L.op == "deconv":
+                w = self.weights[li]
+                dx, _ = self._run("deconv_bwd_data", li, lambda: oc.oc_deconv_bwd(
+                    tree, L.depth, L.ksize, L.stride, xin, w, g, need_dx=True, need_dw=False))
+                self._run("deconv_bwd_weight", li, lambda: oc.oc_deconv_bwd(
+                    tree, L.depth, L.ksize, L.stride, xin, w, g, need_dx=False, need_dw=True))
+                g, masked = dx, False
             elif L.op == "pool":
                 # a ReLU right below the pooling: its backward goes into the routing
                 P = wl.layers[li - 1] if li > 0 else None
@@ -629,9 +661,10 @@ def cpu_baseline(synth, wl, shapes):
     pts, nrm, offs = synth.make_points(wl, batch=shapes)
     t0 = time.perf_counter()
     ref = oracle.Octree(pts, nrm, offs, wl.depth, wl.full_depth)
+    L0 = wl.layers[0]
     x = ref.signal if wl.signal_input else synth.make_features(
-        [wl.seed_id, 3000], ref.num(wl.layers[0].depth), wl.layers[0].cin)
-    saved, flops = [], 0
+        [wl.seed_id, 3000], ref.num(L0.depth - (L0.op == "deconv" and L0.stride == 2)), L0.cin)
+    saved, flops, sws = [], 0, {}
     for li, L in enumerate(wl.layers):
         l = L.depth
         if L.op == "conv":
@@ -644,8 +677,25 @@ def cpu_baseline(synth, wl, shapes):
             saved.append((li, nb, x, w, pre))
             flops += (6 if li > 0 else 4) * y.shape[0] * L.ksize ** 3 * L.cin * L.cout
             x = y
+        elif L.op == "deconv":
+            w = synth.make_weights(wl, li, L.ksize, L.cout, L.cin)
+            if L.stride == 1:
+                nb = ref.neighbors(l, L.ksize)
+                y = oracle.deconv_fwd(nb, x, w, ref.num(l))
+            else:
+                y = oracle.deconv_s2_fwd(ref, l, x, w)
+            saved.append((li, None, x, w, None))
+            n = ref.num(l) if L.stride == 1 else ref.num(l - 1)
+            flops += 6 * n * L.ksize ** 3 * L.cin * L.cout
+            x = y
         elif L.op == "pool":
             y, sw = oracle.pool_fwd(ref.labels(l - 1), x)
+            saved.append((li, None, x, sw, None))
+            sws[l] = sw
+            x = y
+        elif L.op == "unpool":
+            sw = sws[l]
+            y = oracle.unpool_fwd(ref.labels(l - 1), x, sw, ref.num(l))
             saved.append((li, None, x, sw, None))
             x = y
     g = synth.make_upstream(wl, len(wl.layers) - 1, x.shape[0], x.shape[1])
@@ -658,6 +708,13 @@ def cpu_baseline(synth, wl, shapes):
                 ge = oracle.renew_bwd(ref.labels(l - 1), ge, nb.shape[0])
             oracle.conv_bwd_weight(nb, xin, ge, L.ksize ** 3)
             g = oracle.conv_bwd_data(nb, ge, w_or_sw, xin.shape[0]) if li > 0 else None
+        elif L.op == "deconv":
+            if L.stride == 1:
+                g, _ = oracle.deconv_bwd(ref.neighbors(l, L.ksize), xin, w_or_sw, g)
+            else:
+                g, _ = oracle.deconv_s2_bwd(ref, l, xin, w_or_sw, g)
+        elif L.op == "unpool":
+            g = oracle.unpool_bwd(ref.labels(l - 1), g, w_or_sw)
         else:
             g = oracle.pool_bwd(ref.labels(l - 1), g, w_or_sw, ref.num(l))
     dt = time.perf_counter() - t0
@@ -773,7 +830,7 @@ def main():
     # rate comes from a kernel trace (--summarize-trace) instead
     ops.pop("build", None)
     ops_out = {c: op_rate(c, w, t, bf16) for c, (t, w) in sorted(ops.items()) if t > 0 and w > 0}
-    conv = [v for c, v in ops.items() if c.startswith("conv")]
+    conv = [v for c, v in ops.items() if c.startswith(("conv", "deconv"))]
     if conv:
         ops_out["conv_fwd_bwd"] = op_rate("conv", sum(w for _, w in conv),
                                           sum(t for t, _ in conv), bf16)
@@ -844,6 +901,9 @@ WORKLOAD_TEXT = {
     "deep_d8": "8 shapes, 100k points each, depth 8; conv3 16->16 @d8, pool, unpool; fp32",
     "wide_d7": "16 shapes, 100k points each, depth 7; conv5 64->64 and stride-2 conv3 "
                "64->128, bf16 inputs with fp32 accumulation",
+    "seg_d6": "32 shapes, depth 6; encoder conv3+ReLU+maxpool 3->16 @d6, 16->32 @d5; decoder "
+              "stride-2 deconv3 32->16 d4->d5, max-unpool d5->d6, deconv3 16->16 @d6; fp32 "
+              "forward and backward",
 }
 
 

@@ -4,8 +4,8 @@
  * Implements the GPU side of O-CNN (Wang et al., "O-CNN: Octree-based
  * Convolutional Neural Networks for 3D Shape Analysis", arXiv 1712.01537):
  * building the per-depth packed super-octree of a batch of oriented point
- * clouds (Sec. 3.1), and convolution, max-pooling and max-unpooling restricted
- * to the octants of that octree (Sec. 3.2).
+ * clouds (Sec. 3.1), and convolution, deconvolution, max-pooling and
+ * max-unpooling restricted to the octants of that octree (Sec. 3.2).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -242,6 +242,60 @@ oc_status oc_conv_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32
                       oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
                       const float* y, const float* dy, float* dx, float* dw, void* ws,
                       size_t ws_bytes, int32_t flags, hipStream_t stream);
+
+/* Octree deconvolution, also called transposed convolution (Sec. 3.2
+ * "Deconvolution"): the transpose of the convolution cout -> cin with the
+ * same weight tensor, obtained as the paper does by swapping that
+ * convolution's forward and backward passes.
+ *   depth   l, the depth of the output (the finer depth for stride 2).
+ *   ksize   3 or 5 (stride 1); 3 (stride 2).
+ *   stride  1: x dev f32 [N_l][cin] -> y dev f32 [N_l][cout];
+ *             y[n] = sum over the rows i and taps k whose neighbour is n of
+ *             w[k] x[i] (the input gradient of oc_conv_fwd, cout -> cin).
+ *           2: x dev f32 [N_{l-1}][cin] -> y dev f32 [N_l][cout], the
+ *             transpose of the stride-2 convolution at depth l: row i of x
+ *             counts only when its octant is non-empty (label p > 0), and
+ *             then reaches the depth-l neighbourhood of the first sibling of
+ *             group p-1.
+ *   dt      OC_F32 only (else OC_ERR_UNSUPPORTED).
+ *   w       dev f32 [K^3][cout][cin], the weight of the convolution it
+ *           transposes (its index order: tap, that convolution's input
+ *           channel = this call's output channel, output channel).
+ *   ws      dev workspace of at least oc_deconv_fwd_workspace() bytes.
+ *   flags   0 (a deconvolution is followed by normalisation before its
+ *           ReLU in the paper's decoder unit, so none is fused).
+ * Each pass runs on the convolution's kernels: the forward on the kernel
+ * oc_conv_kernel(tree, depth, ksize, stride, dt, cout, cin, 1) names, the
+ * input gradient on pass 0 and the weight gradient on pass 2 of the same
+ * call.  Deterministic, as the convolution.  cin, cout in 1..1024. */
+oc_status oc_deconv_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                        oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
+                        float* y, void* ws, size_t ws_bytes, int32_t flags, hipStream_t stream);
+
+/* Bytes of device workspace oc_deconv_fwd needs for these arguments. */
+size_t oc_deconv_fwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize,
+                               int32_t stride, oc_dtype dt, int32_t cin, int32_t cout);
+
+/* Bytes of device workspace oc_deconv_bwd needs for these arguments. */
+size_t oc_deconv_bwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize,
+                               int32_t stride, oc_dtype dt, int32_t cin, int32_t cout);
+
+/* Backward of oc_deconv_fwd.  Arguments as oc_deconv_fwd, plus
+ *   x    the forward input (read only when dw is requested).
+ *   dy   dev f32 [N_l][cout] upstream gradient.
+ *   dx   dev f32, shaped as x, or NULL: the convolution cout -> cin of dy
+ *        (stride 2: rows of empty depth-(l-1) octants are 0).
+ *   dw   dev f32 [K^3][cout][cin] or NULL:
+ *        dw[k][co][ci] = sum over rows i of x and taps k of dy[nb(i,k)][co]
+ *        x[i][ci] (stride 2: rows of non-empty octants, at the first
+ *        sibling of their group).
+ *   ws   dev workspace of at least oc_deconv_bwd_workspace() bytes; both
+ *        passes use it in stream order.
+ * Every argument is checked before either pass is enqueued. */
+oc_status oc_deconv_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                        oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
+                        const float* dy, float* dx, float* dw, void* ws, size_t ws_bytes,
+                        int32_t flags, hipStream_t stream);
 
 /* 2x2x2 max-pooling from depth l to l-1 (Sec. 3.2 "Pooling", Fig. 5): for
  * every row i of depth l-1 with label p > 0, y[i] = channel-wise max of the

@@ -29,6 +29,8 @@ __all__ = [
     "oc_conv_kernel",
     "oc_profile_next",
     "oc_conv_bwd",
+    "oc_deconv_fwd",
+    "oc_deconv_bwd",
     "oc_pool_fwd",
     "oc_pool_bwd",
     "oc_unpool_fwd",
@@ -49,6 +51,7 @@ EXPORTS = (
     "oc_octree_level", "oc_octree_info", "oc_octree_signal", "oc_octree_free",
     "oc_conv_fwd", "oc_conv_kernel", "oc_conv_fwd_workspace", "oc_conv_bwd_workspace", "oc_conv_bwd", "oc_pool_fwd", "oc_pool_bwd",
     "oc_unpool_fwd", "oc_unpool_bwd", "oc_status_str", "oc_last_error", "oc_profile_next",
+    "oc_deconv_fwd", "oc_deconv_fwd_workspace", "oc_deconv_bwd", "oc_deconv_bwd_workspace",
 )
 
 
@@ -140,6 +143,12 @@ def load():
         "oc_conv_bwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
         "oc_conv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, p, sz, i32, p],
                         C.c_int),
+        "oc_deconv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, sz, i32, p],
+                          C.c_int),
+        "oc_deconv_fwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
+        "oc_deconv_bwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
+        "oc_deconv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, sz, i32, p],
+                          C.c_int),
         "oc_pool_fwd": ([p, i32, p, i32, p, p, p], C.c_int),
         "oc_pool_bwd": ([p, i32, p, p, i32, p, p, p], C.c_int),
         "oc_unpool_fwd": ([p, i32, p, p, i32, p, p], C.c_int),
@@ -394,6 +403,61 @@ def oc_conv_bwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tens
                          _dev(dx, "dx") if dx is not None else None,
                          _dev(dw, "dw") if dw is not None else None,
                          _dev(ws, "ws"), ws.numel(), OC_FUSE_RELU if relu else 0, _stream()))
+    return dx, dw
+
+
+def _deconv_dims(tree: Octree, depth: int, stride: int, x, w):
+    """Rows of the input and output of a deconvolution to depth `depth`, and
+    its channels (w is [K^3][cout][cin])."""
+    if not 1 <= depth <= tree.depth:
+        raise OcError(1, f"depth {depth} not in 1..{tree.depth}")
+    K3, cout, cin = w.shape
+    n_out = tree.num(depth)
+    n_in = n_out if stride == 1 else tree.num(depth - 1)
+    if x is not None and tuple(x.shape) != (n_in, cin):
+        raise OcError(1, f"x has shape {tuple(x.shape)}, expected {(n_in, cin)}")
+    return K3, cin, cout, n_in, n_out
+
+
+def oc_deconv_fwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tensor,
+                  w: torch.Tensor, y: torch.Tensor | None = None) -> torch.Tensor:
+    """Deconvolution to depth `depth` (Sec. 3.2); w [K^3][cout][cin] is the
+    weight of the convolution cout -> cin it transposes."""
+    K3, cin, cout, n_in, n_out = _deconv_dims(tree, depth, stride, x, w)
+    if K3 != ksize ** 3:
+        raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
+    dt = _dtype_code(x)
+    if y is None:
+        y = torch.empty((n_out, cout), dtype=torch.float32, device=x.device)
+    L = load()
+    ws_bytes = int(L.oc_deconv_fwd_workspace(tree.handle, depth, ksize, stride, dt, cin, cout))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device) if ws_bytes else None
+    _check(L.oc_deconv_fwd(tree.handle, depth, ksize, stride, dt, _dev(x, "x"), cin,
+                           _dev(w, "w", torch.float32), cout,
+                           _dev(y, "y", torch.float32, (n_out, cout)),
+                           _dev(ws, "ws") if ws is not None else None, ws_bytes, 0, _stream()))
+    return y
+
+
+def oc_deconv_bwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tensor,
+                  w: torch.Tensor, dy: torch.Tensor, need_dx: bool = True,
+                  need_dw: bool = True):
+    """Input and weight gradients of oc_deconv_fwd: (dx or None, dw or None)."""
+    K3, cin, cout, n_in, n_out = _deconv_dims(tree, depth, stride, x, w)
+    if K3 != ksize ** 3:
+        raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
+    dt = _dtype_code(w)
+    L = load()
+    dx = torch.empty((n_in, cin), dtype=torch.float32, device=w.device) if need_dx else None
+    dw = torch.empty((K3, cout, cin), dtype=torch.float32, device=w.device) if need_dw else None
+    ws_bytes = int(L.oc_deconv_bwd_workspace(tree.handle, depth, ksize, stride, dt, cin, cout))
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=w.device)
+    _check(L.oc_deconv_bwd(tree.handle, depth, ksize, stride, dt,
+                           _dev(x, "x") if x is not None else None, cin, _dev(w, "w"), cout,
+                           _dev(dy, "dy", torch.float32, (n_out, cout)),
+                           _dev(dx, "dx") if dx is not None else None,
+                           _dev(dw, "dw") if dw is not None else None,
+                           _dev(ws, "ws"), ws.numel(), 0, _stream()))
     return dx, dw
 
 

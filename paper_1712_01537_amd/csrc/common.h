@@ -42,6 +42,12 @@ inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 // Check a level argument and return its sizes.
 oc_status check_tree_level(const oc_octree* t, int32_t l, int32_t min_l);
 
+// Argument checks of a convolution call (depth, kernel size, stride, dtype,
+// channel counts), as oc_conv_fwd and oc_conv_bwd do them; `who` names the
+// caller in the message.
+oc_status conv_check(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,
+                     int32_t cin, int32_t cout, const char* who);
+
 // Compute units of the current device (cached per device).
 int cu_count();
 

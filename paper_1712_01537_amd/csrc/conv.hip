@@ -160,6 +160,12 @@ size_t bwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype
 
 }  // namespace
 
+oc_status oc::conv_check(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,
+                         int32_t cin, int32_t cout, const char* who) {
+  ConvShape sh;
+  return check_conv(t, l, K, stride, dt, cin, cout, &sh, who);
+}
+
 extern "C" {
 
 const char* oc_conv_kernel(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,

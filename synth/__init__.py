@@ -20,7 +20,15 @@ net_d5      5      32     20k       conv3 3->32 @5, pool, 32->64 @4, pool, 64->1
 net_d6      6      32     20k       conv3+ReLU+pool: 3->16 @6, 16->32 @5, 32->64 @4, 64->128 @3; conv3+ReLU 128->256 @2
 deep_d8     8      8      100k      conv3 16->16 @8, pool d8->d7, unpool d7->d8
 wide_d7     7      16     100k      conv5 64->64 @7 (bf16 and fp32), stride-2 conv3 64->128 d7->d6
+seg_d6      6      32     20k       conv3+ReLU+pool 3->16 @6, 16->32 @5; stride-2 deconv3 32->16
+                                    d4->d5; unpool d5->d6; deconv3 16->16 @6
 ==========  =====  =====  ========  ===============================================
+
+seg_d6 is the decoder side of the paper's segmentation network (Sec. 4,
+the deconvolution units that mirror the encoder) on the depth-6 shapes: an
+encoder of two conv+ReLU+pool stages, then a stride-2 deconvolution back up
+one depth and an unpooling + deconvolution unit.  Normalisation and the
+ReLU between the units are left out (not octree operations).
 """
 from __future__ import annotations
 
@@ -47,8 +55,8 @@ __all__ = [
 class Layer:
     """One operation of a workload's network."""
 
-    op: str  # "conv", "pool", "unpool"
-    depth: int  # input depth of the op
+    op: str  # "conv", "deconv", "pool", "unpool"
+    depth: int  # input depth of the op (deconv and unpool: its output depth)
     cin: int = 0
     cout: int = 0
     ksize: int = 3
@@ -108,6 +116,16 @@ WORKLOADS = {
             Layer("conv", 7, 64, 128, ksize=3, stride=2, dtype="bf16"),
         ),
         signal_input=False,
+    ),
+    "seg_d6": Workload(
+        "seg_d6", 6, 6, 32, 20_000, "union",
+        (
+            Layer("conv", 6, 3, 16, relu=True), Layer("pool", 6, 16, 16),
+            Layer("conv", 5, 16, 32, relu=True), Layer("pool", 5, 32, 32),
+            Layer("deconv", 5, 32, 16, stride=2),
+            Layer("unpool", 6, 16, 16),
+            Layer("deconv", 6, 16, 16),
+        ),
     ),
 }
 
@@ -247,7 +265,9 @@ def random_cloud(seed: int, shapes: int, pts_per_shape, spread: str = "uniform")
 
 
 def make_weights(w: Workload | str, layer: int, ksize: int, cin: int, cout: int):
-    """Weights f32 [K^3][cin][cout]: N(0, sigma^2), sigma fixed by the workload or He-normal."""
+    """Weights f32 [K^3][cin][cout]: N(0, sigma^2), sigma fixed by the workload or He-normal.
+    A deconvolution cin -> cout takes make_weights(..., cout, cin): the weight of
+    the convolution it transposes."""
     if isinstance(w, str):
         w = WORKLOADS[w]
     rng = np.random.default_rng([w.seed_id, 1000 + layer])

@@ -50,6 +50,10 @@ def test_argument_errors_without_device():
     L.oc_build_cancel(None)
     assert L.oc_conv_fwd(None, 1, 3, 1, 0, None, 3, None, 4, None, None, 0, 0, None) == 1
     assert L.oc_pool_fwd(None, 1, None, 3, None, None, None) == 1
+    assert L.oc_deconv_fwd(None, 1, 3, 1, 0, None, 4, None, 3, None, None, 0, 0, None) == 1
+    assert L.oc_deconv_bwd(None, 1, 3, 1, 0, None, 4, None, 3, None, None, None, None, 0, 0,
+                           None) == 1
+    assert L.oc_deconv_fwd_workspace(None, 1, 3, 1, 0, 4, 3) == 0
     assert L.oc_octree_signal(None) is None
     assert L.oc_status_str(2) == b"point outside the unit cube"
     L.oc_octree_free(None)

@@ -93,6 +93,64 @@ def test_conv_small_fp32(seed, B, n, depth, K, stride, cin, cout, relu):
     assert torch.equal(dw.view(torch.int32), dw2.view(torch.int32))
 
 
+DECONV_SMALL = [  # seed, B, n, depth, K, stride, cin, cout (deconv channels)
+    (81, 2, 400, 4, 3, 1, 7, 5),
+    (82, 2, 900, 5, 3, 1, 128, 64),  # split reduction in the forward (input-gradient kernel)
+    (83, 1, 800, 5, 5, 1, 8, 8),
+    (84, 2, 500, 4, 3, 2, 10, 6),
+    (85, 2, 500, 5, 3, 2, 32, 16),
+    (86, 3, 300, 4, 3, 1, 16, 3),  # down to 3 channels
+]
+
+
+@pytest.mark.parametrize("seed,B,n,depth,K,stride,cin,cout", DECONV_SMALL)
+def test_deconv_small_fp32(seed, B, n, depth, K, stride, cin, cout):
+    oc = _oc()
+    print(f"[deconv] seed={seed} B={B} d={depth} K={K} s={stride} {cin}->{cout}", flush=True)
+    pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
+    ref, tree = _trees(pts, nrm, offs, depth)
+    l = depth
+    rng = np.random.default_rng(seed)
+    n_in = ref.num(l) if stride == 1 else ref.num(l - 1)
+    x = rng.standard_normal((n_in, cin)).astype(np.float32)
+    w = (rng.standard_normal((K ** 3, cout, cin)) / np.sqrt(K ** 3 * cin)).astype(np.float32)
+    dy = rng.standard_normal((ref.num(l), cout)).astype(np.float32)
+    y = oc.oc_deconv_fwd(tree, l, K, stride, _cuda(x), _cuda(w))
+    dx, dw = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x), _cuda(w), _cuda(dy))
+    if stride == 1:
+        nb = ref.neighbors(l, K)
+        yr = oracle.deconv_fwd(nb, x, w, ref.num(l))
+        dxr, dwr = oracle.deconv_bwd(nb, x, w, dy)
+    else:
+        yr = oracle.deconv_s2_fwd(ref, l, x, w)
+        dxr, dwr = oracle.deconv_s2_bwd(ref, l, x, w, dy)
+    assert_f32_close(y.cpu().numpy(), yr, "y")
+    assert_f32_close(dx.cpu().numpy(), dxr, "dx")
+    assert_dw_close(dw.cpu().numpy(), dwr, "dw")
+    # deterministic: identical bits on a second call; each gradient alone equals the pair
+    y2 = oc.oc_deconv_fwd(tree, l, K, stride, _cuda(x), _cuda(w))
+    dx2, _ = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x), _cuda(w), _cuda(dy), need_dw=False)
+    _, dw2 = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x), _cuda(w), _cuda(dy), need_dx=False)
+    assert torch.equal(y.view(torch.int32), y2.view(torch.int32))
+    assert torch.equal(dx.view(torch.int32), dx2.view(torch.int32))
+    assert torch.equal(dw.view(torch.int32), dw2.view(torch.int32))
+
+
+def test_deconv_argument_errors():
+    oc = _oc()
+    pts = np.array([[0.3, 0.6, 0.9]], np.float32)
+    ref, tree = _trees(pts, np.ones((1, 3), np.float32), [0, 1], 3, 0)
+    x = _cuda(np.zeros((ref.num(3), 4)))
+    with pytest.raises(oc.OcError):  # bf16 is not supported
+        oc.oc_deconv_fwd(tree, 3, 3, 1, x.to(torch.bfloat16),
+                         _cuda(np.zeros((27, 2, 4))).to(torch.bfloat16))
+    with pytest.raises(oc.OcError):  # kernel size 7
+        oc.oc_deconv_fwd(tree, 3, 7, 1, x, _cuda(np.zeros((343, 2, 4))))
+    with pytest.raises(oc.OcError):  # stride 2 with K = 5
+        oc.oc_deconv_bwd(tree, 3, 5, 2, _cuda(np.zeros((ref.num(2), 4))),
+                         _cuda(np.zeros((125, 2, 4))), _cuda(np.zeros((ref.num(3), 2))))
+
+
 @pytest.mark.parametrize("K,stride", [(3, 1), (5, 1), (3, 2)])
 def test_conv_small_bf16(K, stride):
     oc = _oc()
@@ -272,7 +330,33 @@ def _check_conv_full(ref, tree, l, K, stride, x, w, relu, dy, tag, dtype=torch.f
     return y
 
 
-@pytest.mark.parametrize("name", ["sphere_d5", "net_d5", "net_d6", "deep_d8", "wide_d7"])
+def _check_deconv_full(ref, tree, l, K, stride, x, w, dy, tag):
+    oc = _oc()
+    rng = np.random.default_rng(1)
+    n_out = ref.num(l)
+    print(f"[{tag}] deconv d{l} K{K} s{stride} {x.shape[1]}->{w.shape[1]} rows {n_out}", flush=True)
+    y = oc.oc_deconv_fwd(tree, l, K, stride, _cuda(x), _cuda(w))
+    want = np.zeros(n_out, bool)
+    want[_sample(rng, n_out, 3000)] = True
+    ent = _sample(rng, w.size, 300)
+    dx, dw = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x), _cuda(w), _cuda(dy))
+    if stride == 1:
+        nb = ref.neighbors(l, K)
+        yr = oracle.deconv_fwd(nb, x, w, n_out, want=want)
+        rows = _sample(rng, x.shape[0], 3000)
+        dxr, dwr = oracle.deconv_bwd(nb, x, w, dy, rows=rows, entries=ent)
+        dxg = dx.cpu().numpy()[rows]
+    else:
+        yr = oracle.deconv_s2_fwd(ref, l, x, w, want=want)
+        dxr, dwr = oracle.deconv_s2_bwd(ref, l, x, w, dy, entries=ent)
+        dxg = dx.cpu().numpy()
+    assert_f32_close(y.cpu().numpy()[want], yr[want], f"{tag} y")
+    assert_f32_close(dxg, dxr, f"{tag} dx")
+    rule = assert_dw_close(dw.cpu().numpy().ravel()[ent], dwr, f"{tag} dw")
+    print(f"[{tag}] dw rule: {rule}", flush=True)
+
+
+@pytest.mark.parametrize("name", ["sphere_d5", "net_d5", "net_d6", "deep_d8", "wide_d7", "seg_d6"])
 def test_workload_full_size(name):
     oc = _oc()
     w_ = synth.WORKLOADS[name]
@@ -295,6 +379,12 @@ def test_workload_full_size(name):
             if L.dtype == "bf16":
                 _check_conv_full(ref, tree, l, K, L.stride, x, w, L.relu, dy, f"{name}/{li}/bf16",
                                  dtype=torch.bfloat16)
+        elif L.op == "deconv":
+            n_in = ref.num(l) if L.stride == 1 else ref.num(l - 1)
+            x = synth.make_features([w_.seed_id, 3000 + li], n_in, L.cin)
+            w = synth.make_weights(w_, li, L.ksize, L.cout, L.cin)
+            dy = synth.make_upstream(w_, li, ref.num(l), L.cout)
+            _check_deconv_full(ref, tree, l, L.ksize, L.stride, x, w, dy, f"{name}/{li}")
         elif L.op == "pool":
             x = synth.make_features([w_.seed_id, 3000 + li], ref.num(l), L.cin)
             print(f"[{name}/{li}] pool d{l} C{L.cin}", flush=True)
