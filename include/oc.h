@@ -190,11 +190,12 @@ void oc_octree_free(oc_octree* tree);
  *   ws      dev workspace of at least oc_conv_fwd_workspace() bytes (may be
  *           NULL when that is 0): partial sums of a reduction split across
  *           workgroups, added in a fixed order (results are reproducible);
- *           for OC_BF16 also x and w widened to fp32; for stride 2 the
+ *           for OC_BF16 also x and w widened to fp32; for stride 2 either
+ *           a transposed copy of w (fp32 with cin and cout multiples of 16:
+ *           one implicit-GEMM kernel gathers the inputs itself) or the
  *           column buffer (at most 256 MB, the groups taken in chunks) and
- *           the per-group outputs.  Stride 2 multiplies the column buffer by
- *           w with the ROCm GEMM library (atomics disabled, so the result is
- *           reproducible too).
+ *           the per-group outputs, multiplied by w with the ROCm GEMM
+ *           library (atomics disabled, so the result is reproducible too).
  *   flags   0 or OC_FUSE_RELU.
  * cin, cout in 1..1024. */
 oc_status oc_conv_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,

@@ -1,7 +1,9 @@
 // Stride-2 octree convolution, K = 3 (Sec. 3.2 of O-CNN, Fig. 2): the output
 // of sibling group g is the convolution evaluated at its first child (child
 // 0), written to the row of g's parent at depth l-1 (rows of empty parents
-// are 0).  The paper evaluates it as im2col + GEMM, and so does this file:
+// are 0).  The fp32 forward with channel counts that are multiples of 16 is
+// one implicit-GEMM kernel (k_s2_fwd, below).  Everything else follows the
+// paper's im2col + GEMM:
 // a gather kernel builds the column buffer Col[g][k][c] = x[n(8g, k)][c]
 // (0 for an absent neighbour; only parent offsets {-1,0}^3 are reached from
 // child 0), a library GEMM multiplies it by W viewed as [27 Cin][Cout], and
@@ -213,6 +215,180 @@ __global__ __launch_bounds__(TB) void k_s2_dgather1(const int32_t* __restrict__ 
   D[t] = f >= 0 ? dyg[(int64_t)(f >> 3) * cout + c] : T(0);
 }
 
+// ---------------------------------------------------------------------------
+// fp32 forward as an implicit GEMM on the matrix cores (k_s2_fwd), for cin
+// and cout multiples of 16: no column buffer.  The MFMA computes the output
+// transposed: A = W^T (16 output channels x reduction), B = the gathered
+// inputs (reduction x 16 sibling groups), so lane (i, q) (i = lane % 16,
+// q = lane / 16) supplies group i's input row at one tap, channels
+// c0 + 4q .. c0 + 4q + 3, from one 16-byte load to four consecutive
+// 16x16x4 MFMAs (channel 4q + s to the s-th), and holds the chunk's weights
+// W[k][c][n0 + i] of its channel slots for all 27 taps in registers (read
+// from a transposed copy wt[k][n][c], 16 bytes per tap).
+// Child 0 of group g reaches, per axis, offset -1 (child 1 of the parent
+// neighbour at -1), 0 and +1 (children 0 and 1 of its own parent's column),
+// so the 27 taps read the children of the 8 parent neighbours at offsets
+// {-1,0}^3; a lane keeps those 8 first-child rows of its group per row block
+// and every tap is then a compile-time child offset.  Loads run 16 / RB - 1
+// taps ahead of the MFMAs (a register ring), which covers the latency of
+// the gathers (mostly L2 hits).
+// A workgroup takes GT = 16 RB WM groups (a tile) and 16 WN output channels
+// (a column block): wave w owns channels 16 (w % WN) and RB row blocks of 16
+// groups.  Results go straight to the parents' rows (rows_of_label at depth
+// l-1), ReLU applied if relu; the workgroups of column block 0 also zero the
+// rows of empty depth-(l-1) octants, an equal share each.
+// bf16 stays on the column buffer and GEMM: with one 16x16x32 MFMA per
+// 16-byte gather, this kernel was bound by the vector-memory path (0.57 vs
+// 0.41 ms for the 16-shape depth-7 64 -> 128 layer).
+typedef float s2v4f __attribute__((ext_vector_type(4)));
+typedef uint32_t s2v4u __attribute__((ext_vector_type(4)));
+
+// wt[k][n][c] = w[k][c][n] (27 taps), so that a lane of k_s2_fwd reads its
+// channels of one output column with one 16-byte load.
+template <typename T>
+__global__ __launch_bounds__(TB) void k_s2_wt(const T* __restrict__ w, int cin, int cout,
+                                              T* __restrict__ wt) {
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= (int64_t)27 * cin * cout) return;
+  const int c = (int)(t % cin);
+  const int n = (int)((t / cin) % cout);
+  const int64_t k = t / ((int64_t)cin * cout);
+  wt[t] = w[(k * cin + c) * cout + n];
+}
+
+// Four 16x16x4 MFMAs, the s-th taking element s of a and b.
+__device__ __forceinline__ s2v4f s2_mfma4(s2v4u a, s2v4u b, s2v4f c) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[s]), __uint_as_float(b[s]), c, 0, 0,
+                                             0);
+  return c;
+}
+
+template <int WN, int RB>
+__global__ __launch_bounds__(TB) void k_s2_fwd(const int32_t* __restrict__ nbr, int64_t G,
+                                               const void* __restrict__ xv, int cin,
+                                               const void* __restrict__ wv, int cout,
+                                               const int32_t* __restrict__ prow,
+                                               const int32_t* __restrict__ labels, int64_t n_out,
+                                               float* __restrict__ y, int relu, int xbytes,
+                                               int wbytes, int ntiles, int gy) {
+  constexpr int WAVES = TB / 64, WM = WAVES / WN;
+  constexpr int CH = 16;                 // reduction channels per chunk
+  constexpr int EPL = 4;                 // channels per lane per load
+  constexpr int ES = 4;                  // element bytes
+  constexpr int GT = 16 * RB * WM;       // groups per workgroup
+  constexpr int PD = 16 / RB;            // taps of gathered loads in the ring
+  static_assert(WN * WM == WAVES, "waves");
+  // x through a buffer resource of xbytes bytes: offsets at or past the end
+  // read zeros, which is how absent neighbours are read
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(xv), (short)0, xbytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr_ =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(wv), (short)0, wbytes, 0x00020000);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int li = lane & 15, q = lane >> 4;
+  const int wn = wave % WN, wm = wave / WN;
+  // workgroup -> (tile, column block): the workgroups of one XCD (dispatch
+  // order modulo 8) take a contiguous run of tiles, all column blocks of a
+  // tile in a row, so neighbouring groups' rows are gathered from one L2
+  const int per = (int)(gridDim.x / 8), bid = (int)blockIdx.x;
+  const int lin = gridDim.x % 8 == 0 ? (bid % 8) * per + bid / 8 : bid;
+  if (lin >= ntiles * gy) return;  // uniform over the workgroup
+  const int tile = lin / gy, cbk = lin % gy;
+  const int n0 = cbk * 16 * WN + 16 * wn;
+  const int64_t gb = (int64_t)tile * GT + (int64_t)wm * 16 * RB;
+
+  // zero this workgroup's share of the rows of empty depth-(l-1) octants
+  if (cbk == 0) {
+    const int64_t r0 = n_out * tile / ntiles, r1 = n_out * (tile + 1) / ntiles;
+    const int c4 = cout / 4, ne = (int)(r1 - r0) * c4;
+    for (int e = tid; e < ne; e += TB) {
+      const int64_t i = r0 + e / c4;
+      if (labels[i] == 0)
+        *reinterpret_cast<s2v4f*>(y + i * cout + 4 * (e % c4)) = s2v4f{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+
+  // byte offsets of this lane's channels in the first-child rows of the 8
+  // parent neighbours at offsets {-1,0}^3 (index 4 ox + 2 oy + oz, o = 1 for
+  // offset 0); 2^31 (past the end of x, read as zeros) if absent.  The tap's
+  // child row and the chunk go into the scalar offset of each load.
+  const int lane_cb = q * EPL * ES;  // this lane's byte offset within a chunk's channels
+  uint32_t pbo[RB][8];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    const int64_t g = gb + 16 * r + li;
+#pragma unroll
+    for (int o = 0; o < 8; ++o) {
+      const int slot = ((o >> 2) & 1) * 9 + ((o >> 1) & 1) * 3 + (o & 1);
+      const int32_t f = g < G ? nbr[27 * g + slot] : -1;
+      pbo[r][o] = f < 0 ? 0x80000000u : (uint32_t)(f * cin * ES + lane_cb);
+    }
+  }
+  // tap k = 9 (dx+1) + 3 (dy+1) + (dz+1): parent offset index and child row
+  auto tap_o = [](int k) {
+    const int dx = k / 9 - 1, dy = (k / 3) % 3 - 1, dz = k % 3 - 1;
+    return 4 * (dx >= 0) + 2 * (dy >= 0) + (dz >= 0);
+  };
+  auto tap_c = [](int k) {
+    const int dx = k / 9 - 1, dy = (k / 3) % 3 - 1, dz = k % 3 - 1;
+    return 4 * (dx & 1) + 2 * (dy & 1) + (dz & 1);
+  };
+
+  s2v4f acc[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) acc[r] = s2v4f{0.f, 0.f, 0.f, 0.f};
+  s2v4u wr[27];
+  const uint32_t wlane = (uint32_t)((n0 + li) * cin * ES + lane_cb);
+
+  for (int c0 = 0; c0 < cin; c0 += CH) {
+    // the chunk's weights: wr[k] = W[k][c0 + EPL q + j][n0 + li], j < EPL,
+    // one 16-byte load from the transposed copy wt[k][n][c]
+#pragma unroll
+    for (int k = 0; k < 27; ++k)
+      wr[k] = __builtin_bit_cast(
+          s2v4u, __builtin_amdgcn_raw_buffer_load_b128(wr_, wlane, (k * cout * cin + c0) * ES, 0));
+    auto gload = [&](int r, int k) {
+      return __builtin_bit_cast(
+          s2v4u, __builtin_amdgcn_raw_buffer_load_b128(xr, pbo[r][tap_o(k)],
+                                                       (tap_c(k) * cin + c0) * ES, 0));
+    };
+    // a ring of PD taps' loads: tap k + PD - 1 is issued before tap k's MFMAs
+    s2v4u bv[PD][RB];
+#pragma unroll
+    for (int k = 0; k + 1 < PD; ++k)
+#pragma unroll
+      for (int r = 0; r < RB; ++r) bv[k][r] = gload(r, k);
+#pragma unroll
+    for (int k = 0; k < 27; ++k) {
+      if (k + PD - 1 < 27) {
+#pragma unroll
+        for (int r = 0; r < RB; ++r) bv[(k + PD - 1) % PD][r] = gload(r, k + PD - 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // PD - 1 taps of loads ahead, no more
+#pragma unroll
+      for (int r = 0; r < RB; ++r) acc[r] = s2_mfma4(wr[k], bv[k % PD][r], acc[r]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  // D[4q + j][i] = output channel n0 + 4q + j of group gb + 16 r + i
+#pragma unroll
+  for (int r = 0; r < RB; ++r) {
+    const int64_t g = gb + 16 * r + li;
+    if (g < G) {
+      s2v4f v = acc[r];
+      if (relu) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = fmaxf(v[j], 0.f);
+      }
+      *reinterpret_cast<s2v4f*>(y + (int64_t)prow[g] * cout + n0 + 4 * q) = v;
+    }
+  }
+}
+
 inline unsigned grid_for(int64_t n) { return (unsigned)oc::cdiv(n, TB); }
 
 // The profiling events pending for the calling thread (oc_profile_next)
@@ -329,6 +505,30 @@ S2Shape s2_shape(const oc_octree* t, int l, int cin, size_t elsize) {
   return h;
 }
 
+// Shapes the implicit-GEMM forward takes (the rest use the column buffer).
+bool s2_fwd_direct(const oc_octree* t, int l, int cin, int cout, bool bf16) {
+  return !bf16 && t->M[l - 1] > 0 && cin % 16 == 0 && cout % 16 == 0 &&
+         (int64_t)t->N[l] * cin * 4 < ((int64_t)1 << 31);
+}
+
+template <int WN, int RB>
+void launch_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const void* w, int cout,
+                   float* y, int relu, void* ws, hipStream_t s) {
+  const int64_t nw = (int64_t)27 * cin * cout;
+  hipLaunchKernelGGL(k_s2_wt<float>, dim3((unsigned)oc::cdiv(nw, TB)), dim3(TB), 0, s,
+                     (const float*)w, cin, cout, (float*)ws);
+  w = ws;
+  const int64_t G = t->M[l - 1];
+  constexpr int GT = 16 * RB * (TB / 64 / WN);
+  const int ntiles = (int)oc::cdiv(G, GT), gy = cout / (16 * WN);
+  const int64_t nwg = (int64_t)ntiles * gy;
+  const dim3 grid((unsigned)(nwg >= 8 ? oc::cdiv(nwg, 8) * 8 : nwg));
+  hipLaunchKernelGGL((k_s2_fwd<WN, RB>), grid, dim3(TB), 0, s, (const int32_t*)t->nbr[l], G,
+                     x, cin, w, cout, (const int32_t*)t->rows[l - 1],
+                     (const int32_t*)t->labels[l - 1], t->N[l - 1], y, relu,
+                     (int)(t->N[l] * cin * 4), (int)(nw * 4), ntiles, gy);
+}
+
 }  // namespace
 
 namespace oc {
@@ -336,6 +536,8 @@ namespace oc {
 size_t conv_s2_fwd_ws(const oc_octree* t, int l, int cin, int cout, bool bf16) {
   const S2Shape h = s2_shape(t, l, cin, bf16 ? 2 : 4);
   if (h.G == 0) return 0;
+  if (s2_fwd_direct(t, l, cin, cout, bf16))  // the transposed weights
+    return align256((size_t)27 * cin * cout * 4);
   return align256((size_t)h.gc * h.kc * (bf16 ? 2 : 4)) + align256((size_t)h.G * cout * 4);
 }
 
@@ -383,6 +585,25 @@ void launch_col(hipStream_t s, const int32_t* nbr, int64_t g0, int64_t ng, const
 oc_status conv_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const void* w, int cout,
                       bool bf16, float* y, int relu, void* ws, hipStream_t s) {
   PassEvents ev(s);
+  if (s2_fwd_direct(t, l, cin, cout, bf16)) {
+    if ((uintptr_t)x % 16 != 0 || (uintptr_t)y % 16 != 0)
+      return fail(OC_ERR_ARG, "oc_conv_fwd: stride 2 needs 16-byte aligned x and y");
+    // output channels per workgroup: 16 WN; row blocks per wave: the most
+    // that still gives two workgroups per compute unit
+    const int wn = cout % 64 == 0 ? 4 : cout % 32 == 0 ? 2 : 1;
+    const int64_t G = t->M[l - 1], gy = cout / (16 * wn), wm = 4 / wn;
+    int rb = 4;
+    while (rb > 1 && oc::cdiv(G, 16 * rb * wm) * gy < 2 * (int64_t)cu_count()) rb /= 2;
+#define OC_S2F(WN_, RB_)                                                  \
+  if (wn == WN_ && rb == RB_) {                                           \
+    launch_s2_fwd<WN_, RB_>(t, l, x, cin, w, cout, y, relu, ws, s);       \
+    return OC_OK;                                                         \
+  }
+    OC_S2F(4, 4) OC_S2F(4, 2) OC_S2F(4, 1) OC_S2F(2, 4) OC_S2F(2, 2) OC_S2F(2, 1)
+    OC_S2F(1, 4) OC_S2F(1, 2) OC_S2F(1, 1)
+#undef OC_S2F
+    return fail(OC_ERR_UNSUPPORTED, "stride-2 forward: no kernel for %d -> %d", cin, cout);
+  }
   const S2Shape h = s2_shape(t, l, cin, bf16 ? 2 : 4);
   const int32_t* nbr = t->nbr[l];
   char* p = (char*)ws;
