@@ -307,3 +307,63 @@ def test_deconv_s2_equals_dense_strided_transpose(seed, B, depth, full):
     np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-11, atol=1e-11)
     np.testing.assert_allclose(dw, wt.grad.numpy(), rtol=1e-11, atol=1e-11)
     assert np.all(dx[t.labels(l - 1) == 0] == 0)
+
+
+# General pooling (Sec. 3.2, last paragraph of "Pooling"): the stride-1 K^3
+# neighbourhood with absent neighbours read as zero.  Dense forms: the grid of
+# the octants' features (zeros elsewhere), zero-padded, then max_pool3d /
+# avg_pool3d (count_include_pad) with stride 1, read at the octants.
+
+@pytest.mark.parametrize("seed,B,depth,full,K", CASES)
+def test_gpool_equals_dense_pooling(seed, B, depth, full, K):
+    t = _tree(seed, B, depth, full)
+    l, c, r = depth, 5, (K - 1) // 2
+    rng = np.random.default_rng(400 + seed)
+    x = rng.standard_normal((t.num(l), c))  # continuous: ties only among zeros
+    nb = t.neighbors(l, K)
+    dy = rng.standard_normal((t.num(l), c))
+    # max
+    y, sw = oracle.gpool_fwd(nb, x, oracle.POOL_MAX)
+    xt = torch.as_tensor(x).requires_grad_(True)
+    g = F.pad(_scatter(t, l, xt), (r,) * 6, value=0.0)
+    dense, idx = F.max_pool3d(g, K, stride=1, return_indices=True)
+    out = _gather(t, l, dense)
+    np.testing.assert_array_equal(y, out.detach().numpy())
+    # the switch names the dense argmax cell (a zero cell when POOL_ABSENT)
+    s = 2 ** l + 2 * r
+    b, X, Y, Z = _coords(t, l)
+    fi = _gather(t, l, idx).numpy()
+    ix, iy, iz = fi // (s * s), (fi // s) % s, fi % s
+    tap = ((ix - X[:, None]) * K + (iy - Y[:, None])) * K + (iz - Z[:, None])
+    present = sw != oracle.POOL_ABSENT
+    np.testing.assert_array_equal(sw[present], tap[present])
+    assert np.all(y[~present] == 0)
+    out.backward(torch.as_tensor(dy))
+    np.testing.assert_allclose(oracle.gpool_bwd(nb, dy, sw, t.num(l), oracle.POOL_MAX),
+                               xt.grad.numpy(), rtol=1e-12, atol=1e-12)
+    # average
+    ya, swa = oracle.gpool_fwd(nb, x, oracle.POOL_AVG)
+    assert swa is None
+    xt = torch.as_tensor(x).requires_grad_(True)
+    out = _gather(t, l, F.avg_pool3d(_scatter(t, l, xt), K, stride=1, padding=r,
+                                     count_include_pad=True))
+    np.testing.assert_allclose(ya, out.detach().numpy(), rtol=1e-12, atol=1e-12)
+    out.backward(torch.as_tensor(dy))
+    np.testing.assert_allclose(oracle.gpool_bwd(nb, dy, None, t.num(l), oracle.POOL_AVG),
+                               xt.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_gpool_hand_case():
+    # one group of 8 siblings at depth 1 (the whole cube): every child sees the
+    # other seven plus 19 absent (outside-cube) neighbours
+    pts = np.array([[0.3, 0.3, 0.3]], np.float32)
+    t = oracle.Octree(pts, np.ones((1, 3), np.float32), [0, 1], 1, 0)
+    x = np.array([[-1.], [-2.], [-3.], [-4.], [-5.], [-6.], [-7.], [-0.5]])
+    nb = t.neighbors(1, 3)
+    y, sw = oracle.gpool_fwd(nb, x, oracle.POOL_MAX)
+    assert np.all(y == 0) and np.all(sw == oracle.POOL_ABSENT)  # an absent zero beats them
+    ya, _ = oracle.gpool_fwd(nb, x, oracle.POOL_AVG)
+    np.testing.assert_allclose(ya[:, 0], np.full(8, x.sum() / 27))  # all 8 in every window
+    y2, sw2 = oracle.gpool_fwd(nb, x + 10, oracle.POOL_MAX)
+    # child 7 (x=y=z=1) is the maximum; seen from child 0 at offset (+1,+1,+1): tap 26
+    assert y2[0, 0] == 9.5 and sw2[0, 0] == 26 and sw2[7, 0] == 13
