@@ -89,6 +89,8 @@ BOUND = {
     "pool_bwd": "hbm",
     "unpool_fwd": "hbm",
     "unpool_bwd": "hbm",
+    "gpool_fwd": "hbm",
+    "gpool_bwd": "hbm",
     "build": "hbm",
     "build_emit": "hbm",
 }
@@ -415,6 +417,8 @@ class Accounting:
             return M[l - 1] * c * 5 + M[l - 1] * 4 + N[l] * c * 4
         if tag == "unpool_bwd":  # the routed child of each (parent, channel) in, parent rows out
             return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l - 1] * c * 4
+        if tag in ("gpool_fwd", "gpool_bwd"):  # rows in and out, switches (max), 27 ints per group
+            return N[l] * c * 8 + (N[l] * c if L.mode == "max" else 0) + M[l - 1] * 108
         return 0
 
 
@@ -577,6 +581,12 @@ class Step(Accounting):
                     tree, L.depth, L.ksize, L.stride, x, w))
                 saved.append((li, x, y, None))
                 x = y
+            elif L.op == "gpool":
+                mode = oc.OC_POOL_MAX if L.mode == "max" else oc.OC_POOL_AVG
+                y, sw = self._run("gpool_fwd", li, lambda: oc.oc_gpool_fwd(
+                    tree, L.depth, L.ksize, mode, x))
+                saved.append((li, x, y, sw))
+                x = y
             elif L.op == "pool":
                 p, sw = self._run("pool_fwd", li, lambda: oc.oc_pool_fwd(tree, L.depth, x))
                 saved.append((li, x, p, sw))
@@ -626,6 +636,11 @@ class Step(Accounting):
                 self._run("deconv_bwd_weight", li, lambda: oc.oc_deconv_bwd(
                     tree, L.depth, L.ksize, L.stride, xin, w, g, need_dx=False, need_dw=True))
                 g, masked = dx, False
+            elif L.op == "gpool":
+                mode = oc.OC_POOL_MAX if L.mode == "max" else oc.OC_POOL_AVG
+                g = self._run("gpool_bwd", li, lambda: oc.oc_gpool_bwd(
+                    tree, L.depth, L.ksize, mode, g, sw))
+                masked = False
             elif L.op == "pool":
                 # a ReLU right below the pooling: its backward goes into the routing
                 P = wl.layers[li - 1] if li > 0 else None
@@ -698,6 +713,12 @@ def cpu_baseline(synth, wl, shapes):
             y = oracle.unpool_fwd(ref.labels(l - 1), x, sw, ref.num(l))
             saved.append((li, None, x, sw, None))
             x = y
+        elif L.op == "gpool":
+            nb = ref.neighbors(l, L.ksize)
+            mode = oracle.POOL_MAX if L.mode == "max" else oracle.POOL_AVG
+            y, sw = oracle.gpool_fwd(nb, x, mode)
+            saved.append((li, nb, x, sw, mode))
+            x = y
     g = synth.make_upstream(wl, len(wl.layers) - 1, x.shape[0], x.shape[1])
     for li, nb, xin, w_or_sw, pre in reversed(saved):
         L = wl.layers[li]
@@ -715,6 +736,8 @@ def cpu_baseline(synth, wl, shapes):
                 g, _ = oracle.deconv_s2_bwd(ref, l, xin, w_or_sw, g)
         elif L.op == "unpool":
             g = oracle.unpool_bwd(ref.labels(l - 1), g, w_or_sw)
+        elif L.op == "gpool":
+            g = oracle.gpool_bwd(nb, g, w_or_sw, ref.num(l), pre)
         else:
             g = oracle.pool_bwd(ref.labels(l - 1), g, w_or_sw, ref.num(l))
     dt = time.perf_counter() - t0
@@ -901,6 +924,9 @@ WORKLOAD_TEXT = {
     "deep_d8": "8 shapes, 100k points each, depth 8; conv3 16->16 @d8, pool, unpool; fp32",
     "wide_d7": "16 shapes, 100k points each, depth 7; conv5 64->64 and stride-2 conv3 "
                "64->128, bf16 inputs with fp32 accumulation",
+    "gpool_d6": "32 shapes, depth 6; conv3+ReLU 3->16 @d6, stride-1 3x3x3 max-pool and 5x5x5 "
+                "average-pool @d6 (the convolution's neighbourhood), 2x2x2 max-pool d6->d5; fp32 "
+                "forward and backward",
     "seg_d6": "32 shapes, depth 6; encoder conv3+ReLU+maxpool 3->16 @d6, 16->32 @d5; decoder "
               "stride-2 deconv3 32->16 d4->d5, max-unpool d5->d6, deconv3 16->16 @d6; fp32 "
               "forward and backward",

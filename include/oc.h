@@ -4,8 +4,9 @@
  * Implements the GPU side of O-CNN (Wang et al., "O-CNN: Octree-based
  * Convolutional Neural Networks for 3D Shape Analysis", arXiv 1712.01537):
  * building the per-depth packed super-octree of a batch of oriented point
- * clouds (Sec. 3.1), and convolution, deconvolution, max-pooling and
- * max-unpooling restricted to the octants of that octree (Sec. 3.2).
+ * clouds (Sec. 3.1), and convolution, deconvolution, max-pooling,
+ * max-unpooling and general pooling restricted to the octants of that
+ * octree (Sec. 3.2).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -330,6 +331,32 @@ oc_status oc_unpool_fwd(const oc_octree* tree, int32_t depth, const float* x, co
  *   dy dev f32 [N_l][c];  dx dev f32 [N_{l-1}][c]. */
 oc_status oc_unpool_bwd(const oc_octree* tree, int32_t depth, const float* dy, const uint8_t* sw,
                         int32_t c, float* dx, hipStream_t stream);
+
+/* General pooling, stride 1 (Sec. 3.2, last paragraph of "Pooling": pooling
+ * with other kernel sizes finds the neighbouring octants as the convolution
+ * does and applies the pooling operation to them).  For every octant i of
+ * depth l and channel c, over the K^3 taps k of its neighbourhood (index as
+ * the convolution's weights), where a neighbour that is not in the octree
+ * reads as 0:
+ *   OC_POOL_MAX  y[i][c] = the maximum; sw[i][c] = the tap of its first
+ *                occurrence in tap order, or 255 when that is an absent
+ *                neighbour (whose zero then gets no gradient);
+ *   OC_POOL_AVG  y[i][c] = the sum over the K^3 taps / K^3 (sw unused).
+ *   depth  1..depth of the tree.  ksize 3 or 5.
+ *   x  dev f32 [N_l][c];  y dev f32 [N_l][c];  sw dev u8 [N_l][c] (max) or NULL. */
+#define OC_POOL_MAX 0
+#define OC_POOL_AVG 1
+oc_status oc_gpool_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t mode,
+                       const float* x, int32_t c, float* y, uint8_t* sw, hipStream_t stream);
+
+/* Gradient of oc_gpool_fwd: dx[n][c] = the sum, in tap order, over the octants
+ * i whose tap k reaches n of dy[i][c] if sw[i][c] == k (max) or
+ * dy[i][c] / K^3 (average).  A gather (no atomics): deterministic.
+ *   dy dev f32 [N_l][c];  sw as produced by oc_gpool_fwd (max) or NULL;
+ *   dx dev f32 [N_l][c]. */
+oc_status oc_gpool_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t mode,
+                       const float* dy, const uint8_t* sw, int32_t c, float* dx,
+                       hipStream_t stream);
 
 /* Profiling: the next launch, on the calling thread, of the kernel that does
  * the main work of an entry point (the kernel oc_conv_kernel names for a

@@ -326,43 +326,57 @@ POOL_MAX, POOL_AVG = 0, 1
 POOL_ABSENT = 255  # switch value: the maximum was an absent neighbour's zero
 
 
-def gpool_fwd(nb, x, mode):
+def gpool_fwd(nb, x, mode, rows=None):
     """General pooling (Sec. 3.2 "Pooling", last paragraph): the K^3
     neighbourhood of every octant is found as for the stride-1 convolution,
     and each channel takes the max (mode POOL_MAX) or the average (POOL_AVG)
     over it.  A neighbour that is not in the octree counts as a zero, as in
     the convolution (so the average divides by K^3).  Returns y [N][C] and,
     for max, the switch sw [N][C] u8: the tap of the first maximum in tap
-    order, or POOL_ABSENT when that maximum is an absent neighbour."""
+    order, or POOL_ABSENT when that maximum is an absent neighbour.
+    rows: optional subset of output rows.  Rows are taken in chunks so that
+    the gathered [rows][K^3][C] block stays near 256 MB."""
     nb = _i32(nb)
     x = _f64(x)
+    if rows is not None:
+        nb = nb[np.asarray(rows, dtype=np.int64)]
     n, K3 = nb.shape
-    ext = np.vstack([x, np.zeros((1, x.shape[1]))])
-    src = np.where(nb >= 0, nb, x.shape[0])
-    vals = ext[src]  # [N][K^3][C]
-    if mode == POOL_AVG:
-        return vals.sum(axis=1) / K3, None
-    k = np.argmax(vals, axis=1)  # first maximum
-    y = np.take_along_axis(vals, k[:, None, :], axis=1)[:, 0, :]
-    absent = np.take_along_axis(nb, k, axis=1) < 0 if k.size else np.zeros_like(k, bool)
-    sw = np.where(absent, POOL_ABSENT, k).astype(np.uint8)
+    C = x.shape[1]
+    ext = np.vstack([x, np.zeros((1, C))])
+    y = np.zeros((n, C))
+    sw = None if mode == POOL_AVG else np.zeros((n, C), np.uint8)
+    step = max(1, (1 << 25) // max(1, K3 * C))
+    for r0 in range(0, n, step):
+        part = nb[r0:r0 + step]
+        vals = ext[np.where(part >= 0, part, x.shape[0])]  # [rows][K^3][C]
+        if mode == POOL_AVG:
+            y[r0:r0 + step] = vals.sum(axis=1) / K3
+            continue
+        k = np.argmax(vals, axis=1)  # first maximum
+        y[r0:r0 + step] = np.take_along_axis(vals, k[:, None, :], axis=1)[:, 0, :]
+        absent = np.take_along_axis(part, k, axis=1) < 0
+        sw[r0:r0 + step] = np.where(absent, POOL_ABSENT, k)
     return y, sw
 
 
 def gpool_bwd(nb, dy, sw, n_in, mode):
     """Gradient of gpool_fwd w.r.t. x [n_in][C]: every output's gradient goes
     to its switch's neighbour (max; nowhere for POOL_ABSENT) or, divided by
-    K^3, to each of its present neighbours (average)."""
+    K^3, to each of its present neighbours (average).  Added tap by tap; within
+    one tap no two octants share a neighbour (the neighbour at a fixed offset
+    is a position shift), so each tap is a plain indexed add."""
     nb = _i32(nb)
     dy = _f64(dy)
     n, K3 = nb.shape
     dx = np.zeros((n_in, dy.shape[1]))
     for k in range(K3):
         rows = np.nonzero(nb[:, k] >= 0)[0]
+        idx = nb[rows, k]
+        assert len(np.unique(idx)) == len(idx)
         if mode == POOL_AVG:
-            np.add.at(dx, nb[rows, k], dy[rows] / K3)
+            dx[idx] += dy[rows] / K3
         else:
-            np.add.at(dx, nb[rows, k], dy[rows] * (sw[rows] == k))
+            dx[idx] += dy[rows] * (sw[rows] == k)
     return dx
 
 

@@ -35,12 +35,17 @@ __all__ = [
     "oc_pool_bwd",
     "oc_unpool_fwd",
     "oc_unpool_bwd",
+    "oc_gpool_fwd",
+    "oc_gpool_bwd",
     "OC_FUSE_RELU",
+    "OC_POOL_MAX",
+    "OC_POOL_AVG",
     "EXPORTS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 OC_FUSE_RELU = 1
+OC_POOL_MAX, OC_POOL_AVG = 0, 1
 OC_F32, OC_BF16 = 0, 1
 STATUS = {0: "OC_OK", 1: "OC_ERR_ARG", 2: "OC_ERR_RANGE", 3: "OC_ERR_NOMEM", 4: "OC_ERR_DEVICE",
           5: "OC_ERR_UNSUPPORTED"}
@@ -52,6 +57,7 @@ EXPORTS = (
     "oc_conv_fwd", "oc_conv_kernel", "oc_conv_fwd_workspace", "oc_conv_bwd_workspace", "oc_conv_bwd", "oc_pool_fwd", "oc_pool_bwd",
     "oc_unpool_fwd", "oc_unpool_bwd", "oc_status_str", "oc_last_error", "oc_profile_next",
     "oc_deconv_fwd", "oc_deconv_fwd_workspace", "oc_deconv_bwd", "oc_deconv_bwd_workspace",
+    "oc_gpool_fwd", "oc_gpool_bwd",
 )
 
 
@@ -149,6 +155,8 @@ def load():
         "oc_deconv_bwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
         "oc_deconv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, sz, i32, p],
                           C.c_int),
+        "oc_gpool_fwd": ([p, i32, i32, i32, p, i32, p, p, p], C.c_int),
+        "oc_gpool_bwd": ([p, i32, i32, i32, p, p, i32, p, p], C.c_int),
         "oc_pool_fwd": ([p, i32, p, i32, p, p, p], C.c_int),
         "oc_pool_bwd": ([p, i32, p, p, i32, p, p, p], C.c_int),
         "oc_unpool_fwd": ([p, i32, p, p, i32, p, p], C.c_int),
@@ -500,4 +508,30 @@ def oc_unpool_bwd(tree: Octree, depth: int, dy: torch.Tensor, sw: torch.Tensor) 
     dx = torch.empty((n_p, c), dtype=torch.float32, device=dy.device)
     _check(load().oc_unpool_bwd(tree.handle, depth, _dev(dy, "dy", torch.float32, (n_l, c)),
                                 _dev(sw, "sw", torch.uint8, (m, c)), c, _dev(dx, "dx"), _stream()))
+    return dx
+
+
+def oc_gpool_fwd(tree: Octree, depth: int, ksize: int, mode: int, x: torch.Tensor):
+    """General stride-1 pooling over the K^3 neighbourhood (Sec. 3.2):
+    (y, sw) for OC_POOL_MAX, (y, None) for OC_POOL_AVG."""
+    n = tree.num(depth)
+    c = x.shape[1]
+    y = torch.empty((n, c), dtype=torch.float32, device=x.device)
+    sw = (torch.empty((n, c), dtype=torch.uint8, device=x.device) if mode == OC_POOL_MAX
+          else None)
+    _check(load().oc_gpool_fwd(tree.handle, depth, ksize, mode,
+                               _dev(x, "x", torch.float32, (n, c)), c, _dev(y, "y"),
+                               _dev(sw, "sw") if sw is not None else None, _stream()))
+    return y, sw
+
+
+def oc_gpool_bwd(tree: Octree, depth: int, ksize: int, mode: int, dy: torch.Tensor,
+                 sw: torch.Tensor | None) -> torch.Tensor:
+    n = tree.num(depth)
+    c = dy.shape[1]
+    dx = torch.empty((n, c), dtype=torch.float32, device=dy.device)
+    _check(load().oc_gpool_bwd(tree.handle, depth, ksize, mode,
+                               _dev(dy, "dy", torch.float32, (n, c)),
+                               _dev(sw, "sw", torch.uint8, (n, c)) if sw is not None else None,
+                               c, _dev(dx, "dx"), _stream()))
     return dx

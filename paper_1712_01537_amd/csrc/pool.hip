@@ -1,5 +1,6 @@
 // 2x2x2 max-pooling and max-unpooling across depths through the label
-// buffer (Sec. 3.2 "Pooling" and "Unpooling", Fig. 5 of O-CNN).
+// buffer (Sec. 3.2 "Pooling" and "Unpooling", Fig. 5 of O-CNN), and general
+// stride-1 pooling over the convolution's neighbourhood (k_gpool_*, below).
 //
 // The eight children of the non-empty octant with label p occupy rows
 // 8(p-1)..8(p-1)+7 of the finer depth, so pooling is a max over 8 contiguous
@@ -144,6 +145,139 @@ __global__ __launch_bounds__(TB) void k_route_up(const float* __restrict__ dy,
 }
 
 inline unsigned grid_for(int64_t n) { return (unsigned)oc::cdiv(n, TB); }
+// ---------------------------------------------------------------------------
+// General pooling, stride 1 (Sec. 3.2, last paragraph of "Pooling"): the K^3
+// neighbourhood of every octant is found as for the convolution, through the
+// sibling group's 27 parent-neighbour entries (neighbour of child c at offset
+// d: parent offset floor((c + d) / 2), child (c + d) & 1 of it), and each
+// channel takes the max or the average over it.  A neighbour that is not in
+// the octree reads as zero, as in the convolution.  One thread handles VEC
+// consecutive channels of one row; the forward takes the taps in blocks of
+// KB whose neighbour lookups, then row loads, are all issued before any is
+// used, so their latencies overlap.  (Staging the groups' (K+1)^3 union blocks in LDS
+// was measured slower: the blocks take so much LDS that too few waves run.)
+template <int R>
+__device__ __forceinline__ int64_t gp_src(const int32_t* __restrict__ nbr, int64_t i, int k) {
+  constexpr int K = 2 * R + 1;
+  const int c = (int)(i & 7);
+  const int ux = (c >> 2) + k / (K * K) - R, uy = ((c >> 1) & 1) + (k / K) % K - R,
+            uz = (c & 1) + k % K - R;
+  const int32_t base = nbr[27 * (i >> 3) + ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1)];
+  return base < 0 ? -1 : (int64_t)base + 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
+}
+
+// taps per block: the forward's whole neighbourhood (K = 3) or a fifth of it.
+// The backward takes one tap at a time: with blocks (of 9 or 5 taps, whose
+// switches it holds as well) it ran fewer waves and was measured slower.
+template <int R, bool BWD>
+constexpr int gp_kb() { return BWD ? 1 : (R == 1 ? 27 : 25); }
+
+// Forward: y = max (first maximum in tap order; sw = its tap, or 255 when it
+// is an absent neighbour's zero) or sum / K^3 over the taps.
+template <int R, bool AVG, int VEC>
+__global__ __launch_bounds__(TB) void k_gpool_fwd(const int32_t* __restrict__ nbr, int64_t n,
+                                                  const float* __restrict__ x, int cv,
+                                                  float* __restrict__ y,
+                                                  uint8_t* __restrict__ sw) {
+  using F = typename Vec<VEC>::f;
+  using U = typename Vec<VEC>::u8;
+  constexpr int K3 = (2 * R + 1) * (2 * R + 1) * (2 * R + 1), KB = gp_kb<R, false>();
+  static_assert(K3 % KB == 0, "tap blocks");
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= n * cv) return;
+  const int64_t i = t / cv;
+  const int q = (int)(t - i * cv);
+  const F* xv = reinterpret_cast<const F*>(x);
+  F acc;
+  U arg;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) set(acc, e, 0.f), set(arg, e, (uint8_t)255);
+#pragma unroll 1
+  for (int k0 = 0; k0 < K3; k0 += KB) {
+    int64_t src[KB];
+    F v[KB];
+#pragma unroll
+    for (int j = 0; j < KB; ++j) src[j] = gp_src<R>(nbr, i, k0 + j);
+#pragma unroll
+    for (int j = 0; j < KB; ++j) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) set(v[j], e, 0.f);
+      if (src[j] >= 0) v[j] = xv[src[j] * cv + q];
+    }
+#pragma unroll
+    for (int j = 0; j < KB; ++j) {
+      const int k = k0 + j;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float a = comp(v[j], e);
+        if constexpr (AVG) {
+          set(acc, e, comp(acc, e) + a);
+        } else if (k == 0 || a > comp(acc, e)) {
+          set(acc, e, a);
+          set(arg, e, src[j] >= 0 ? (uint8_t)k : (uint8_t)255);
+        }
+      }
+    }
+  }
+  if constexpr (AVG) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) set(acc, e, comp(acc, e) / (float)K3);
+  } else {
+    reinterpret_cast<U*>(sw)[t] = arg;
+  }
+  reinterpret_cast<F*>(y)[t] = acc;
+}
+
+// Backward as a gather, in tap order: input row n receives, from the octant
+// i whose tap k lands on n (i is n's neighbour at the mirrored offset, tap
+// K^3 - 1 - k), dy[i] if sw[i] == k (max) or dy[i] / K^3 (average).
+template <int R, bool AVG, int VEC>
+__global__ __launch_bounds__(TB) void k_gpool_bwd(const int32_t* __restrict__ nbr, int64_t n,
+                                                  const float* __restrict__ dy,
+                                                  const uint8_t* __restrict__ sw, int cv,
+                                                  float* __restrict__ dx) {
+  using F = typename Vec<VEC>::f;
+  using U = typename Vec<VEC>::u8;
+  constexpr int K3 = (2 * R + 1) * (2 * R + 1) * (2 * R + 1), KB = gp_kb<R, true>();
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= n * cv) return;
+  const int64_t j0 = t / cv;
+  const int q = (int)(t - j0 * cv);
+  const F* gv = reinterpret_cast<const F*>(dy);
+  const U* sv = reinterpret_cast<const U*>(sw);
+  F acc;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) set(acc, e, 0.f);
+#pragma unroll 1
+  for (int k0 = 0; k0 < K3; k0 += KB) {
+    int64_t src[KB];
+    F g[KB];
+    U s[KB];
+#pragma unroll
+    for (int j = 0; j < KB; ++j) src[j] = gp_src<R>(nbr, j0, K3 - 1 - (k0 + j));
+#pragma unroll
+    for (int j = 0; j < KB; ++j) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) set(g[j], e, 0.f), set(s[j], e, (uint8_t)255);
+      if (src[j] >= 0) {
+        g[j] = gv[src[j] * cv + q];
+        if constexpr (!AVG) s[j] = sv[src[j] * cv + q];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < KB; ++j) {
+      if (src[j] < 0) continue;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        if constexpr (AVG)
+          set(acc, e, comp(acc, e) + comp(g[j], e) / (float)K3);
+        else if (comp(s[j], e) == k0 + j)
+          set(acc, e, comp(acc, e) + comp(g[j], e));
+      }
+    }
+  }
+  reinterpret_cast<F*>(dx)[t] = acc;
+}
 
 oc_status check_common(const oc_octree* t, int32_t l, int32_t c, const void* a, const void* b,
                        const void* s, const char* who) {
@@ -157,6 +291,40 @@ oc_status check_common(const oc_octree* t, int32_t l, int32_t c, const void* a, 
 bool vec4_ok(int c, const void* a, const void* b, const void* s) {
   return c % 4 == 0 && ((uintptr_t)a % 16 == 0) && ((uintptr_t)b % 16 == 0) &&
          ((uintptr_t)s % 4 == 0);
+}
+
+template <bool BWD>
+oc_status gpool(const oc_octree* t, int32_t l, int32_t K, int32_t mode, const float* in,
+                const uint8_t* swin, uint8_t* swout, int32_t c, float* out, hipStream_t s,
+                const char* who) {
+  oc_status st = oc::check_tree_level(t, l, 1);
+  if (st != OC_OK) return st;
+  if (K != 3 && K != 5) return oc::fail(OC_ERR_UNSUPPORTED, "%s: kernel size %d not 3 or 5", who, K);
+  if (mode != OC_POOL_MAX && mode != OC_POOL_AVG)
+    return oc::fail(OC_ERR_ARG, "%s: mode %d not OC_POOL_MAX or OC_POOL_AVG", who, mode);
+  if (c < 1 || c > 65536) return oc::fail(OC_ERR_ARG, "%s: channels %d out of range", who, c);
+  const bool avg = mode == OC_POOL_AVG;
+  const uint8_t* swp = BWD ? swin : swout;
+  if (!in || !out || (!avg && !swp)) return oc::fail(OC_ERR_ARG, "%s: NULL buffer", who);
+  const int64_t n = t->N[l];
+  if (n == 0) return OC_OK;
+  const bool v4 = c % 4 == 0 && (uintptr_t)in % 16 == 0 && (uintptr_t)out % 16 == 0 &&
+                  (avg || (uintptr_t)swp % 4 == 0);
+  const int cv = v4 ? c / 4 : c;
+  const dim3 grid(grid_for(n * cv));
+  const int32_t* nbr = (const int32_t*)t->nbr[l];
+#define OC_GP(R_, AVG_, V_)                                                                   \
+  if (K == 2 * R_ + 1 && avg == AVG_ && (v4 ? 4 : 1) == V_) {                                 \
+    if constexpr (BWD)                                                                        \
+      oc::launch_main(k_gpool_bwd<R_, AVG_, V_>, grid, dim3(TB), s, nbr, n, in, swin, cv, out); \
+    else                                                                                      \
+      oc::launch_main(k_gpool_fwd<R_, AVG_, V_>, grid, dim3(TB), s, nbr, n, in, cv, out, swout); \
+  }
+  OC_GP(1, false, 4) OC_GP(1, false, 1) OC_GP(1, true, 4) OC_GP(1, true, 1)
+  OC_GP(2, false, 4) OC_GP(2, false, 1) OC_GP(2, true, 4) OC_GP(2, true, 1)
+#undef OC_GP
+  OC_LAUNCH_CHECK();
+  return OC_OK;
 }
 
 }  // namespace
@@ -226,6 +394,16 @@ oc_status oc_unpool_bwd(const oc_octree* t, int32_t l, const float* dy, const ui
   }
   OC_LAUNCH_CHECK();
   return OC_OK;
+}
+
+oc_status oc_gpool_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t mode, const float* x,
+                       int32_t c, float* y, uint8_t* sw, hipStream_t s) {
+  return gpool<false>(t, l, K, mode, x, nullptr, sw, c, y, s, "oc_gpool_fwd");
+}
+
+oc_status oc_gpool_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t mode, const float* dy,
+                       const uint8_t* sw, int32_t c, float* dx, hipStream_t s) {
+  return gpool<true>(t, l, K, mode, dy, sw, nullptr, c, dx, s, "oc_gpool_bwd");
 }
 
 }  // extern "C"

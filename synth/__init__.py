@@ -22,6 +22,8 @@ deep_d8     8      8      100k      conv3 16->16 @8, pool d8->d7, unpool d7->d8
 wide_d7     7      16     100k      conv5 64->64 @7 (bf16 and fp32), stride-2 conv3 64->128 d7->d6
 seg_d6      6      32     20k       conv3+ReLU+pool 3->16 @6, 16->32 @5; stride-2 deconv3 32->16
                                     d4->d5; unpool d5->d6; deconv3 16->16 @6
+gpool_d6    6      32     20k       conv3+ReLU 3->16 @6; 3x3x3 max-pool and 5x5x5 average-pool,
+                                    stride 1, @6; 2x2x2 max-pool d6->d5
 ==========  =====  =====  ========  ===============================================
 
 seg_d6 is the decoder side of the paper's segmentation network (Sec. 4,
@@ -55,7 +57,7 @@ __all__ = [
 class Layer:
     """One operation of a workload's network."""
 
-    op: str  # "conv", "deconv", "pool", "unpool"
+    op: str  # "conv", "deconv", "pool", "unpool", "gpool"
     depth: int  # input depth of the op (deconv and unpool: its output depth)
     cin: int = 0
     cout: int = 0
@@ -63,6 +65,7 @@ class Layer:
     stride: int = 1
     relu: bool = False
     dtype: str = "f32"  # "f32" or "bf16"
+    mode: str = "max"  # gpool: "max" or "avg"
 
 
 @dataclass(frozen=True)
@@ -125,6 +128,15 @@ WORKLOADS = {
             Layer("deconv", 5, 32, 16, stride=2),
             Layer("unpool", 6, 16, 16),
             Layer("deconv", 6, 16, 16),
+        ),
+    ),
+    "gpool_d6": Workload(
+        "gpool_d6", 7, 6, 32, 20_000, "union",
+        (
+            Layer("conv", 6, 3, 16, relu=True),
+            Layer("gpool", 6, 16, 16, ksize=3, mode="max"),
+            Layer("gpool", 6, 16, 16, ksize=5, mode="avg"),
+            Layer("pool", 6, 16, 16),
         ),
     ),
 }

@@ -232,6 +232,46 @@ def test_conv_bf16_matrix_core(seed, B, n, depth, K, cin, cout, relu):
     assert torch.equal(dx, dx2) and torch.equal(dw, dw2)
 
 
+GPOOL_SMALL = [  # seed, B, n, depth, K, c, relu (inputs through a ReLU: exact zeros, ties)
+    (91, 2, 400, 4, 3, 16, False),
+    (92, 3, 300, 4, 5, 5, False),
+    (93, 1, 800, 5, 3, 7, True),
+    (94, 2, 500, 4, 5, 32, True),
+]
+
+
+@pytest.mark.parametrize("seed,B,n,depth,K,c,relu", GPOOL_SMALL)
+def test_gpool_small(seed, B, n, depth, K, c, relu):
+    oc = _oc()
+    print(f"[gpool] seed={seed} B={B} d={depth} K={K} c={c} relu={relu}", flush=True)
+    pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
+    ref, tree = _trees(pts, nrm, offs, depth)
+    l = depth
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((ref.num(l), c)).astype(np.float32)
+    if relu:
+        x = np.maximum(x, 0)
+    dy = rng.standard_normal((ref.num(l), c)).astype(np.float32)
+    nb = ref.neighbors(l, K)
+    # max: values and switches bit-exact, the gradient within the fp32 rule
+    y, sw = oc.oc_gpool_fwd(tree, l, K, oc.OC_POOL_MAX, _cuda(x))
+    yr, swr = oracle.gpool_fwd(nb, x, oracle.POOL_MAX)
+    np.testing.assert_array_equal(y.cpu().numpy(), yr)
+    np.testing.assert_array_equal(sw.cpu().numpy(), swr)
+    dx = oc.oc_gpool_bwd(tree, l, K, oc.OC_POOL_MAX, _cuda(dy), sw)
+    assert_f32_close(dx.cpu().numpy(), oracle.gpool_bwd(nb, dy, swr, ref.num(l), oracle.POOL_MAX),
+                     "max dx")
+    # average
+    ya, _ = oc.oc_gpool_fwd(tree, l, K, oc.OC_POOL_AVG, _cuda(x))
+    assert_f32_close(ya.cpu().numpy(), oracle.gpool_fwd(nb, x, oracle.POOL_AVG)[0], "avg y")
+    dxa = oc.oc_gpool_bwd(tree, l, K, oc.OC_POOL_AVG, _cuda(dy), None)
+    assert_f32_close(dxa.cpu().numpy(), oracle.gpool_bwd(nb, dy, None, ref.num(l), oracle.POOL_AVG),
+                     "avg dx")
+    # deterministic
+    dx2 = oc.oc_gpool_bwd(tree, l, K, oc.OC_POOL_MAX, _cuda(dy), sw)
+    assert torch.equal(dx.view(torch.int32), dx2.view(torch.int32))
+
+
 @pytest.mark.parametrize("seed,B,n,depth,c", [(31, 2, 500, 4, 8), (32, 3, 300, 5, 3), (33, 1, 100, 3, 32)])
 def test_pool_unpool_small(seed, B, n, depth, c):
     oc = _oc()
@@ -356,7 +396,8 @@ def _check_deconv_full(ref, tree, l, K, stride, x, w, dy, tag):
     print(f"[{tag}] dw rule: {rule}", flush=True)
 
 
-@pytest.mark.parametrize("name", ["sphere_d5", "net_d5", "net_d6", "deep_d8", "wide_d7", "seg_d6"])
+@pytest.mark.parametrize("name", ["sphere_d5", "net_d5", "net_d6", "deep_d8", "wide_d7", "seg_d6",
+                                  "gpool_d6"])
 def test_workload_full_size(name):
     oc = _oc()
     w_ = synth.WORKLOADS[name]
@@ -385,6 +426,23 @@ def test_workload_full_size(name):
             w = synth.make_weights(w_, li, L.ksize, L.cout, L.cin)
             dy = synth.make_upstream(w_, li, ref.num(l), L.cout)
             _check_deconv_full(ref, tree, l, L.ksize, L.stride, x, w, dy, f"{name}/{li}")
+        elif L.op == "gpool":
+            x = np.maximum(synth.make_features([w_.seed_id, 3000 + li], ref.num(l), L.cin), 0)
+            nb = ref.neighbors(l, L.ksize)
+            print(f"[{name}/{li}] gpool {L.mode} K{L.ksize} d{l} C{L.cin}", flush=True)
+            mode = oc.OC_POOL_MAX if L.mode == "max" else oc.OC_POOL_AVG
+            rmode = oracle.POOL_MAX if L.mode == "max" else oracle.POOL_AVG
+            y, sw = oc.oc_gpool_fwd(tree, l, L.ksize, mode, _cuda(x))
+            yr, swr = oracle.gpool_fwd(nb, x, rmode)
+            dy = synth.make_upstream(w_, li, ref.num(l), L.cin)
+            dx = oc.oc_gpool_bwd(tree, l, L.ksize, mode, _cuda(dy), sw)
+            dxr = oracle.gpool_bwd(nb, dy, swr, ref.num(l), rmode)
+            if L.mode == "max":
+                np.testing.assert_array_equal(y.cpu().numpy(), yr)
+                np.testing.assert_array_equal(sw.cpu().numpy(), swr)
+            else:
+                assert_f32_close(y.cpu().numpy(), yr, f"{name}/{li} y")
+            assert_f32_close(dx.cpu().numpy(), dxr, f"{name}/{li} dx")
         elif L.op == "pool":
             x = synth.make_features([w_.seed_id, 3000 + li], ref.num(l), L.cin)
             print(f"[{name}/{li}] pool d{l} C{L.cin}", flush=True)
