@@ -269,8 +269,8 @@ def op_rate(cls, work, us, bf16):
 TRACE_CLASSES = (
     ("build", ("k_quant", "k_mark", "k_reduce", "k_scan_a", "k_scan_c", "k_leaf_mean", "k_emit",
                "__amd_rocclr_copyBuffer")),
-    ("pool", ("k_pool_fwd", "k_route_down", "k_route_up")),
-    ("conv_main", ("k_conv_", "k_cin_", "Cijk_")),
+    ("pool", ("k_pool_fwd", "k_route_down", "k_route_up", "k_gpool_")),
+    ("conv_main", ("k_conv_", "k_cin_", "Cijk_", "k_s2_fwd<")),
     ("conv_helper", ("k_sum_", "k_relu_mask", "k_bf_", "k_bf16_to_f32", "k_s2_", "k_fill_u32")),
 )
 
@@ -327,7 +327,7 @@ def summarize_trace(prof_dir, prof_log):
         names.setdefault(cls, []).append(k)
     bf16 = any(L.op == "conv" and L.dtype == "bf16" for L in wl.layers)
     flops, _ = acc.conv_flops()
-    pool_bytes = sum(acc.work(t, L) for L in wl.layers if L.op in ("pool", "unpool")
+    pool_bytes = sum(acc.work(t, L) for L in wl.layers if L.op in ("pool", "unpool", "gpool")
                      for t in (L.op + "_fwd", L.op + "_bwd"))
     rows = []
     if us.get("build"):
