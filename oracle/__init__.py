@@ -147,7 +147,8 @@ class Octree:
         return self.levels[l]["rows"]
 
     def neighbors(self, l, K=3, stride=1):
-        n = self.num(l) if stride == 1 else self.nonempty(l - 1)
+        r = int(stride).bit_length() - 1  # stride 2^r
+        n = self.num(l) if stride == 1 else self.nonempty(l - r)
         nb = np.zeros((n, K ** 3), np.int32)
         _check(lib().ocref_neighbors(self._h, l, K, stride, _ptr(nb)))
         return nb
@@ -275,6 +276,26 @@ def deconv_s2_bwd(tree: Octree, l, x, w, dy, entries=None):
     dx = renew(tree.labels(l - 1), conv_fwd(nb, dy, w))
     xhat = renew_bwd(tree.labels(l - 1), x, nb.shape[0])
     dw = conv_bwd_weight(nb, dy, xhat, w.shape[0], entries=entries)
+    return dx, dw
+
+
+def conv_sr_fwd(tree: Octree, l, x, w, stride):
+    """Convolution with stride 2^r (Sec. 3.2): evaluated at the first depth-l
+    position of the sub-tree of height r below each non-empty octant of depth
+    l-r, renewed into T_{l-r} through L_{l-r} (empty octants get 0)."""
+    r = int(stride).bit_length() - 1
+    K = round(w.shape[0] ** (1 / 3))
+    nb = tree.neighbors(l, K, stride=stride)
+    return renew(tree.labels(l - r), conv_fwd(nb, x, w))
+
+
+def conv_sr_bwd(tree: Octree, l, x, w, dy, stride):
+    r = int(stride).bit_length() - 1
+    K = round(w.shape[0] ** (1 / 3))
+    nb = tree.neighbors(l, K, stride=stride)
+    dyhat = renew_bwd(tree.labels(l - r), dy, nb.shape[0])
+    dx = conv_bwd_data(nb, dyhat, w, x.shape[0])
+    dw = conv_bwd_weight(nb, x, dyhat, w.shape[0])
     return dx, dw
 
 

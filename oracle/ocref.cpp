@@ -223,14 +223,20 @@ int ocref_signal(const void* tp, float* sig) {
 // re-encode, look the key up in H: key -> index over all octants of depth l.
 // Offset index k = ((dx+r)*K + (dy+r))*K + (dz+r), r = (K-1)/2.
 // stride 1: one row per octant of depth l, nb [N_l][K^3].
-// stride 2: one row per non-empty parent g at depth l-1, centred on its first
-//           child (row 8g of depth l), nb [M_{l-1}][K^3].
+// stride 2^r (r >= 1): one row per non-empty octant p of depth l-r, in label
+//           order, centred on the first depth-l octant of the sub-tree of
+//           height r below p (Sec. 3.2, stride paragraphs): position
+//           2^r * (coordinates of p), whether or not an octant is stored
+//           there; nb [M_{l-r}][K^3].  For r = 1 that is p's first child.
 // Missing neighbours (outside the cube, or not in the octree) are -1.
 int ocref_neighbors(const void* tp, int32_t l, int32_t K, int32_t stride, int32_t* nb) {
   const Tree* t = static_cast<const Tree*>(tp);
-  if (!t || !nb || l < 0 || l > t->depth || K < 1 || (K % 2) == 0 || (stride != 1 && stride != 2))
+  if (!t || !nb || l < 0 || l > t->depth || K < 1 || (K % 2) == 0 || stride < 1 ||
+      (stride & (stride - 1)) != 0)
     return ERR_ARG;
-  if (stride == 2 && l < 1) return ERR_ARG;
+  int sr = 0;
+  while ((1 << sr) < stride) ++sr;
+  if (sr > l) return ERR_ARG;
   const Level& L = t->lv[l];
   std::unordered_map<uint32_t, int32_t> H;
   H.reserve(L.key.size() * 2);
@@ -238,13 +244,21 @@ int ocref_neighbors(const void* tp, int32_t l, int32_t K, int32_t stride, int32_
 
   const int r = (K - 1) / 2, K3 = K * K * K;
   const int64_t side = int64_t(1) << l;
-  const int64_t n_out = stride == 1 ? (int64_t)L.key.size() : (int64_t)t->lv[l - 1].rows.size();
+  const int64_t n_out = stride == 1 ? (int64_t)L.key.size() : (int64_t)t->lv[l - sr].rows.size();
 #pragma omp parallel for schedule(static)
   for (int64_t o = 0; o < n_out; ++o) {
-    int64_t i = stride == 1 ? o : 8 * o;
-    uint32_t b = L.key[i] >> 24;
+    uint32_t b;
     int64_t x, y, z;
-    key_coords(L.key[i] & 0xFFFFFFu, l, &x, &y, &z);
+    if (stride == 1) {
+      b = L.key[o] >> 24;
+      key_coords(L.key[o] & 0xFFFFFFu, l, &x, &y, &z);
+    } else {  // the o-th non-empty octant of depth l - sr, scaled to depth l
+      const Level& P = t->lv[l - sr];
+      const uint32_t key = P.key[P.rows[o]];
+      b = key >> 24;
+      key_coords(key & 0xFFFFFFu, l - sr, &x, &y, &z);
+      x <<= sr, y <<= sr, z <<= sr;
+    }
     for (int dx = -r; dx <= r; ++dx)
       for (int dy = -r; dy <= r; ++dy)
         for (int dz = -r; dz <= r; ++dz) {

@@ -367,3 +367,38 @@ def test_gpool_hand_case():
     y2, sw2 = oracle.gpool_fwd(nb, x + 10, oracle.POOL_MAX)
     # child 7 (x=y=z=1) is the maximum; seen from child 0 at offset (+1,+1,+1): tap 26
     assert y2[0, 0] == 9.5 and sw2[0, 0] == 26 and sw2[7, 0] == 13
+
+
+# Stride 2^r (Sec. 3.2): the convolution at the first depth-l position of the
+# sub-tree of height r below each non-empty octant of depth l-r, i.e. dense
+# conv3d with stride 2^r read at the depth-(l-r) octants, 0 at empty ones.
+
+@pytest.mark.parametrize("seed,B,depth,full,stride", [(81, 2, 4, 2, 4), (82, 1, 4, 0, 4),
+                                                      (83, 3, 5, 1, 4), (84, 2, 5, 2, 8)])
+def test_stride_2r_equals_dense_strided_conv(seed, B, depth, full, stride):
+    t = _tree(seed, B, depth, full, n=300)
+    r = stride.bit_length() - 1
+    l, K, cin, cout = depth, 3, 3, 4
+    rng = np.random.default_rng(500 + seed)
+    x = rng.standard_normal((t.num(l), cin))
+    w = rng.standard_normal((K ** 3, cin, cout))
+    y = oracle.conv_sr_fwd(t, l, x, w, stride)
+    xt = torch.as_tensor(x).requires_grad_(True)
+    wt = torch.as_tensor(w).requires_grad_(True)
+    wd = wt.reshape(K, K, K, cin, cout).permute(4, 3, 0, 1, 2)
+    out = _gather(t, l - r, F.conv3d(_scatter(t, l, xt), wd, stride=stride, padding=1))
+    nz = torch.as_tensor((t.labels(l - r) > 0).astype(np.float64))[:, None]
+    np.testing.assert_allclose(y, (out * nz).detach().numpy(), rtol=1e-12, atol=1e-12)
+    dy = rng.standard_normal((t.num(l - r), cout))
+    (out * nz).backward(torch.as_tensor(dy))
+    dx, dw = oracle.conv_sr_bwd(t, l, x, w, dy, stride)
+    np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(dw, wt.grad.numpy(), rtol=1e-11, atol=1e-11)
+    if stride == 2:  # the same as the first-sibling form
+        np.testing.assert_array_equal(t.neighbors(l, K, 2), t.neighbors(l, K)[::8])
+
+
+def test_stride_2_neighbors_are_first_siblings():
+    t = _tree(85, 2, 4, 2)
+    np.testing.assert_array_equal(t.neighbors(4, 3, stride=2), t.neighbors(4, 3)[::8])
+    np.testing.assert_array_equal(t.neighbors(4, 5, stride=2), t.neighbors(4, 5)[::8])
