@@ -369,8 +369,8 @@ class Accounting:
         self.wl, self.N, self.M, self.npoints = wl, list(N), list(M), npoints
 
     def _n_out(self, L):
-        if L.op == "conv":
-            return self.N[L.depth] if L.stride == 1 else self.N[L.depth - 1]
+        if L.op == "conv":  # stride 2^r: depth - r
+            return self.N[L.depth - (L.stride.bit_length() - 1)]
         if L.op == "pool":
             return self.N[L.depth - 1]
         return self.N[L.depth]
@@ -378,12 +378,12 @@ class Accounting:
     def _n_in(self, L):
         if L.op == "conv" or L.stride == 1:
             return self.N[L.depth]
-        return self.N[L.depth - 1]  # stride-2 deconvolution, unpooling
+        return self.N[L.depth - (L.stride.bit_length() - 1)]  # strided deconvolution
 
     def _n_conv(self, L):
         """Output rows of the convolution a conv or deconv layer runs (a
         deconvolution runs the passes of the convolution it transposes)."""
-        return self.N[L.depth] if L.stride == 1 else self.N[L.depth - 1]
+        return self.N[L.depth - (L.stride.bit_length() - 1)]
 
     def conv_flops(self):
         """Algorithmic flops of the step's conv passes (forward, weight gradient,
@@ -686,8 +686,9 @@ def cpu_baseline(synth, wl, shapes):
             nb = ref.neighbors(l, L.ksize, stride=L.stride)
             w = synth.make_weights(wl, li, L.ksize, L.cin, L.cout)
             pre = oracle.conv_fwd(nb, x, w)
-            if L.stride == 2:
-                pre = oracle.renew(ref.labels(l - 1), pre)
+            r = L.stride.bit_length() - 1
+            if r > 0:
+                pre = oracle.renew(ref.labels(l - r), pre)
             y = oracle.relu_fwd(pre) if L.relu else pre
             saved.append((li, nb, x, w, pre))
             flops += (6 if li > 0 else 4) * y.shape[0] * L.ksize ** 3 * L.cin * L.cout
@@ -725,8 +726,9 @@ def cpu_baseline(synth, wl, shapes):
         l = L.depth
         if L.op == "conv":
             ge = oracle.relu_bwd(pre, g) if L.relu else g
-            if L.stride == 2:
-                ge = oracle.renew_bwd(ref.labels(l - 1), ge, nb.shape[0])
+            r = L.stride.bit_length() - 1
+            if r > 0:
+                ge = oracle.renew_bwd(ref.labels(l - r), ge, nb.shape[0])
             oracle.conv_bwd_weight(nb, xin, ge, L.ksize ** 3)
             g = oracle.conv_bwd_data(nb, ge, w_or_sw, xin.shape[0]) if li > 0 else None
         elif L.op == "deconv":
@@ -927,6 +929,8 @@ WORKLOAD_TEXT = {
     "gpool_d6": "32 shapes, depth 6; conv3+ReLU 3->16 @d6, stride-1 3x3x3 max-pool and 5x5x5 "
                 "average-pool @d6 (the convolution's neighbourhood), 2x2x2 max-pool d6->d5; fp32 "
                 "forward and backward",
+    "s4_d6": "32 shapes, depth 6; conv3+ReLU 3->16 @d6, stride-4 conv3+ReLU 16->64 d6->d4, "
+             "conv3 64->128 @d4; fp32 forward and backward",
     "seg_d6": "32 shapes, depth 6; encoder conv3+ReLU+maxpool 3->16 @d6, 16->32 @d5; decoder "
               "stride-2 deconv3 32->16 d4->d5, max-unpool d5->d6, deconv3 16->16 @d6; fp32 "
               "forward and backward",

@@ -183,11 +183,18 @@ void oc_octree_free(oc_octree* tree);
  *              first sibling of every group and written to the row of its
  *              parent; rows of empty parents are zero (Sec. 3.2 stride-2
  *              paragraphs, Fig. 2(d)).
+ *           4: output at depth l-2 (stride 2^r, r = 2, Sec. 3.2): evaluated
+ *              at the first depth-l position of the sub-tree of height 2
+ *              below every non-empty depth-(l-2) octant (4 times its
+ *              coordinates, whether or not an octant is stored there: the
+ *              neighbours of that position are read as usual) and written
+ *              to that octant's row; rows of empty octants are zero.
+ *              Strides 2 and 4 take ksize 3 only; stride 4 needs l >= 2.
  *   dt      OC_F32: x, w fp32.  OC_BF16: x, w bf16 (round-to-nearest-even
  *           values held as uint16); products accumulate in fp32, so the
  *           result is the fp32 convolution of the bf16 values.
  *   x       dev [N_l][cin].      w  dev [K^3][cin][cout].
- *   y       dev f32 [N_out][cout], N_out = N_l (stride 1) or N_{l-1}.
+ *   y       dev f32 [N_out][cout], N_out = N_l, N_{l-1} or N_{l-2}.
  *   ws      dev workspace of at least oc_conv_fwd_workspace() bytes (may be
  *           NULL when that is 0): partial sums of a reduction split across
  *           workgroups, added in a fixed order (results are reproducible);

@@ -348,7 +348,10 @@ def _conv_dims(tree: Octree, depth: int, stride: int, x, w):
         raise OcError(1, f"depth {depth} not in 1..{tree.depth}")
     K3, cin, cout = w.shape
     n_in = tree.num(depth)
-    n_out = n_in if stride == 1 else tree.num(depth - 1)
+    r = int(stride).bit_length() - 1  # stride 2^r
+    if not 0 <= r <= depth:
+        raise OcError(1, f"stride {stride} needs depth >= {r}")
+    n_out = tree.num(depth - r)
     if x is not None and tuple(x.shape) != (n_in, cin):
         raise OcError(1, f"x has shape {tuple(x.shape)}, expected {(n_in, cin)}")
     return K3, cin, cout, n_in, n_out

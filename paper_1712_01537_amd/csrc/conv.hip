@@ -86,7 +86,7 @@ __global__ __launch_bounds__(TB) void k_relu_mask(const float* __restrict__ y,
 inline unsigned grid_for(int64_t n) { return (unsigned)oc::cdiv(n, TB); }
 
 struct ConvShape {
-  int K, K3, stride;
+  int K, K3, stride, r;  // stride 2^r
   int64_t n_in, n_out, units;  // units: output positions (rows, or groups for stride 2)
 };
 
@@ -95,18 +95,22 @@ oc_status check_conv(const oc_octree* t, int32_t l, int32_t K, int32_t stride, o
   oc_status st = oc::check_tree_level(t, l, 1);
   if (st != OC_OK) return st;
   if (dt != OC_F32 && dt != OC_BF16) return oc::fail(OC_ERR_ARG, "%s: bad dtype %d", who, (int)dt);
-  if (stride != 1 && stride != 2) return oc::fail(OC_ERR_ARG, "%s: stride %d not 1 or 2", who, stride);
+  if (stride != 1 && stride != 2 && stride != 4)
+    return oc::fail(OC_ERR_ARG, "%s: stride %d not 1, 2 or 4", who, stride);
   if (K != 3 && K != 5) return oc::fail(OC_ERR_UNSUPPORTED, "%s: kernel size %d not 3 or 5", who, K);
-  if (stride == 2 && K != 3)
-    return oc::fail(OC_ERR_UNSUPPORTED, "%s: stride 2 supports kernel size 3 only", who);
+  if (stride > 1 && K != 3)
+    return oc::fail(OC_ERR_UNSUPPORTED, "%s: stride %d supports kernel size 3 only", who, stride);
+  const int r = stride == 4 ? 2 : stride == 2 ? 1 : 0;
+  if (l < r) return oc::fail(OC_ERR_ARG, "%s: stride %d needs depth >= %d", who, stride, r);
   if (cin < 1 || cin > 1024 || cout < 1 || cout > 1024)
     return oc::fail(OC_ERR_ARG, "%s: channels %d -> %d out of range", who, cin, cout);
   sh->K = K;
   sh->K3 = K * K * K;
   sh->stride = stride;
   sh->n_in = t->N[l];
-  sh->n_out = stride == 1 ? t->N[l] : t->N[l - 1];
-  sh->units = stride == 1 ? t->N[l] : t->M[l - 1];
+  sh->r = r;
+  sh->n_out = t->N[l - r];
+  sh->units = stride == 1 ? t->N[l] : t->M[l - r];
   return OC_OK;
 }
 
@@ -128,7 +132,7 @@ bool bf16_native(const ConvShape& sh, oc_dtype dt, int cin, int cout) {
 
 size_t fwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,
                     int cout) {
-  if (sh.stride == 2) return oc::conv_s2_fwd_ws(t, l, cin, cout, dt == OC_BF16);
+  if (sh.stride > 1) return oc::conv_s2_fwd_ws(t, l, sh.r, cin, cout, dt == OC_BF16);
   if (sh.n_in == 0) return 0;
   if (bf16_native(sh, dt, cin, cout)) return oc::conv_bf16_fwd_ws(sh.K, cin, cout);
   const size_t tile = oc::conv_s1_tile_ws(t, l, sh.K, cin, cout);
@@ -155,7 +159,7 @@ size_t bwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype
     const size_t wide = dt == OC_F32 ? 0 : w32_bytes(sh, cin, cout) + x32_bytes(sh, cin);
     return wide + mask_ws_bytes(sh, cout) + std::max(a, b);
   }
-  return oc::conv_s2_bwd_ws(t, l, cin, cout, dt == OC_BF16, true, true);
+  return oc::conv_s2_bwd_ws(t, l, sh.r, cin, cout, dt == OC_BF16, true, true);
 }
 
 }  // namespace
@@ -183,7 +187,7 @@ const char* oc_conv_kernel(const oc_octree* t, int32_t l, int32_t K, int32_t str
   } else if (stride == 1) {  // other bf16 shapes run the fp32 kernels on widened operands
     oc::conv_s1_kernel_name(t, l, K, cin, cout, pass, name, sizeof(name));
   } else {  // several kernels and a GEMM: the pass is named
-    snprintf(name, sizeof(name), "conv_s2_%s<%s>",
+    snprintf(name, sizeof(name), "conv_s%d_%s<%s>", stride,
              pass == 0 ? "fwd" : pass == 1 ? "bwd_data" : "bwd_weight",
              dt == OC_F32 ? "f32" : "bf16");
   }
@@ -229,7 +233,7 @@ oc_status oc_conv_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
     OC_LAUNCH_CHECK();
     return OC_OK;
   }
-  st = oc::conv_s2_fwd(t, l, x, cin, w, cout, dt == OC_BF16, y, relu, ws, s);
+  st = oc::conv_s2_fwd(t, l, sh.r, x, cin, w, cout, dt == OC_BF16, y, relu, ws, s);
   if (st != OC_OK) return st;
   OC_LAUNCH_CHECK();
   return OC_OK;
@@ -256,8 +260,8 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   if (need && (!ws || ws_bytes < need))
     return oc::fail(OC_ERR_ARG, "oc_conv_bwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0, need);
   const float* ym = (flags & OC_FUSE_RELU) ? y : nullptr;
-  if (stride == 2) {
-    st = oc::conv_s2_bwd(t, l, x, cin, w, cout, dt == OC_BF16, ym, dy, dx, dw, ws, s);
+  if (stride > 1) {
+    st = oc::conv_s2_bwd(t, l, sh.r, x, cin, w, cout, dt == OC_BF16, ym, dy, dx, dw, ws, s);
     if (st != OC_OK) return st;
     OC_LAUNCH_CHECK();
     return OC_OK;

@@ -1,5 +1,5 @@
-// Stride-2, K = 3 octree convolution through column buffers and a GEMM
-// (conv_s2.hip).
+// Stride-2 and stride-4 (r = 1, 2), K = 3 octree convolution through column
+// buffers and a GEMM (conv_s2.hip).
 #pragma once
 
 #include "common.h"
@@ -7,20 +7,21 @@
 namespace oc {
 
 // Workspace bytes of the forward, and of the backward for the requested
-// gradients, at input depth l (0 when nothing is needed).
-size_t conv_s2_fwd_ws(const oc_octree* t, int l, int cin, int cout, bool bf16);
-size_t conv_s2_bwd_ws(const oc_octree* t, int l, int cin, int cout, bool bf16, bool dx, bool dw);
+// gradients, at input depth l and stride 2^r (0 when nothing is needed).
+size_t conv_s2_fwd_ws(const oc_octree* t, int l, int r, int cin, int cout, bool bf16);
+size_t conv_s2_bwd_ws(const oc_octree* t, int l, int r, int cin, int cout, bool bf16, bool dx,
+                      bool dw);
 
-// y [N_{l-1}][cout] from x [N_l][cin] and w [27][cin][cout] (bf16: x and w
+// y [N_{l-r}][cout] from x [N_l][cin] and w [27][cin][cout] (bf16: x and w
 // bf16); relu applies max(0, .).
-oc_status conv_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const void* w, int cout,
-                      bool bf16, float* y, int relu, void* ws, hipStream_t s);
+oc_status conv_s2_fwd(const oc_octree* t, int l, int r, const void* x, int cin, const void* w,
+                      int cout, bool bf16, float* y, int relu, void* ws, hipStream_t s);
 
 // dx [N_l][cin] and/or dw [27][cin][cout] (either may be null) for upstream
-// gradient dy [N_{l-1}][cout]; ym: the forward output when the forward fused
+// gradient dy [N_{l-r}][cout]; ym: the forward output when the forward fused
 // a ReLU (dy is masked by [ym > 0]), else null.
-oc_status conv_s2_bwd(const oc_octree* t, int l, const void* x, int cin, const void* w, int cout,
-                      bool bf16, const float* ym, const float* dy, float* dx, float* dw, void* ws,
-                      hipStream_t s);
+oc_status conv_s2_bwd(const oc_octree* t, int l, int r, const void* x, int cin, const void* w,
+                      int cout, bool bf16, const float* ym, const float* dy, float* dx, float* dw,
+                      void* ws, hipStream_t s);
 
 }  // namespace oc

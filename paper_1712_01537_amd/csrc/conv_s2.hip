@@ -51,10 +51,39 @@ __device__ __forceinline__ int32_t s2_src(const int32_t* __restrict__ nbr, int64
   return base < 0 ? -1 : base + 4 * (dx & 1) + 2 * (dy & 1) + (dz & 1);
 }
 
+// Stride 4 (Sec. 3.2, stride 2^r with r = 2): row of x that tap k of
+// output p reads, or -1.  Output p (the p-th non-empty octant of depth l-2)
+// sits at depth-l position 4p; tap offset d reaches 4p + d = 2 (2p + a) +
+// (d & 1) with a = d >> 1 in {-1, 0}: the depth-(l-1) octant at 2p + a is
+// child (a & 1) of p's neighbour at offset a (through nbr1 = the depth-(l-1)
+// group table, whose group p holds p's children), and the depth-l octant is
+// child (d & 1) of it, when it is non-empty (lab1 = the depth-(l-1) labels).
+__device__ __forceinline__ int32_t s4_src(const int32_t* __restrict__ nbr1,
+                                          const int32_t* __restrict__ lab1, int64_t p, int k) {
+  const int dx = k / 9 - 1, dy = (k / 3) % 3 - 1, dz = k % 3 - 1;
+  const int ax = dx >> 1, ay = dy >> 1, az = dz >> 1;
+  const int32_t f = nbr1[27 * p + (ax + 1) * 9 + (ay + 1) * 3 + (az + 1)];
+  if (f < 0) return -1;
+  const int32_t L = lab1[f + 4 * (ax & 1) + 2 * (ay & 1) + (az & 1)];
+  return L <= 0 ? -1 : 8 * (L - 1) + 4 * (dx & 1) + 2 * (dy & 1) + (dz & 1);
+}
+
+// Source row of tap k of output g at stride 2^RR (RR = 1: nbr = the depth-l
+// table; RR = 2: nbr = the depth-(l-1) table, lab = the depth-(l-1) labels).
+template <int RR>
+__device__ __forceinline__ int32_t sr_src(const int32_t* __restrict__ nbr,
+                                          const int32_t* __restrict__ lab, int64_t g, int k) {
+  if constexpr (RR == 1)
+    return s2_src(nbr, g, k);
+  else
+    return s4_src(nbr, lab, g, k);
+}
+
 // Column buffer of groups g0 .. g0+ng-1: col[g-g0][k][:] = x[src][:] (T = fp32
 // or bf16), one 16-byte piece per thread; rows of rb bytes, rb % 16 == 0.
-template <typename T>
-__global__ __launch_bounds__(TB) void k_s2_col(const int32_t* __restrict__ nbr, int64_t g0,
+template <typename T, int RR>
+__global__ __launch_bounds__(TB) void k_s2_col(const int32_t* __restrict__ nbr,
+                                               const int32_t* __restrict__ lab, int64_t g0,
                                                int64_t ng, const T* __restrict__ x, int rb,
                                                T* __restrict__ col) {
   const int np = rb / 16;
@@ -62,22 +91,23 @@ __global__ __launch_bounds__(TB) void k_s2_col(const int32_t* __restrict__ nbr, 
   if (t >= ng * 27 * np) return;
   const int pc = (int)(t % np);
   const int64_t gk = t / np;  // (g - g0) * 27 + k
-  const int32_t src = s2_src(nbr, g0 + gk / 27, (int)(gk % 27));
+  const int32_t src = sr_src<RR>(nbr, lab, g0 + gk / 27, (int)(gk % 27));
   uint4 v = {0u, 0u, 0u, 0u};
   if (src >= 0) v = *reinterpret_cast<const uint4*>((const char*)x + (int64_t)src * rb + 16 * pc);
   *reinterpret_cast<uint4*>((char*)col + gk * rb + 16 * pc) = v;
 }
 
 // Element-wise fallback for rows that are not a multiple of 16 bytes.
-template <typename T>
-__global__ __launch_bounds__(TB) void k_s2_col1(const int32_t* __restrict__ nbr, int64_t g0,
+template <typename T, int RR>
+__global__ __launch_bounds__(TB) void k_s2_col1(const int32_t* __restrict__ nbr,
+                                                const int32_t* __restrict__ lab, int64_t g0,
                                                 int64_t ng, const T* __restrict__ x, int cin,
                                                 T* __restrict__ col) {
   const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
   if (t >= ng * 27 * cin) return;
   const int c = (int)(t % cin);
   const int64_t gk = t / cin;
-  const int32_t src = s2_src(nbr, g0 + gk / 27, (int)(gk % 27));
+  const int32_t src = sr_src<RR>(nbr, lab, g0 + gk / 27, (int)(gk % 27));
   col[t] = src < 0 ? T(0) : x[(int64_t)src * cin + c];
 }
 
@@ -389,6 +419,85 @@ __global__ __launch_bounds__(TB) void k_s2_fwd(const int32_t* __restrict__ nbr, 
   }
 }
 
+// Stride-4 input gradient.  Depth-l row n = 8h + c is child c of the
+// depth-(l-1) octant q with label h + 1, itself child a of its parent P.  Per
+// axis, n's position 4P + 2a + c is read by exactly one output when
+// 2a + c != 2: output P (tap offset c) when a = 0, output P + 1 (offset -1)
+// when a = 1 and c = 1.  So the eight rows of group h all read the same
+// output, P's neighbour at offset a (through P's depth-(l-1) group table),
+// and dx[n][ci] = sum_co W[d][ci][co] dyg[p][co]; rows that no output reads
+// get 0.  One thread per (row, input channel), four output channels per step.
+template <typename T>
+__global__ __launch_bounds__(TB) void k_s4_dx(const int32_t* __restrict__ rows1,
+                                              const int32_t* __restrict__ nbr1, int64_t n_in,
+                                              const T* __restrict__ dyg, const T* __restrict__ w,
+                                              int cin, int cout, float* __restrict__ dx) {
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= n_in * cin) return;
+  const int64_t n = t / cin;
+  const int ci = (int)(t - n * cin);
+  const int c = (int)(n & 7);
+  const int32_t rq = rows1[n >> 3];
+  const int a = rq & 7;
+  const int axx = a >> 2, ayy = (a >> 1) & 1, azz = a & 1;
+  const int cx = c >> 2, cy = (c >> 1) & 1, cz = c & 1;
+  float acc = 0.f;
+  if (!((axx && !cx) || (ayy && !cy) || (azz && !cz))) {
+    const int32_t f = nbr1[27 * (int64_t)(rq >> 3) + (axx + 1) * 9 + (ayy + 1) * 3 + (azz + 1)];
+    if (f >= 0) {
+      const int64_t p = f >> 3;
+      const int dxo = axx ? -1 : cx, dyo = ayy ? -1 : cy, dzo = azz ? -1 : cz;
+      const int k = (dxo + 1) * 9 + (dyo + 1) * 3 + (dzo + 1);
+      const T* wr = w + ((int64_t)k * cin + ci) * cout;
+      const T* gr = dyg + p * cout;
+      for (int co = 0; co < cout; ++co) acc += to_f(wr[co]) * to_f(gr[co]);
+    }
+  }
+  dx[t] = acc;
+}
+
+// The same for fp32 with cin and cout multiples of 4: one thread per (row,
+// 4 input channels), 4 x 4 weight blocks and 4 upstream channels per step.
+__global__ __launch_bounds__(TB) void k_s4_dx4(const int32_t* __restrict__ rows1,
+                                               const int32_t* __restrict__ nbr1, int64_t n_in,
+                                               const float* __restrict__ dyg,
+                                               const float* __restrict__ w, int cin, int cout,
+                                               float* __restrict__ dx) {
+  const int cq = cin / 4;
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= n_in * cq) return;
+  const int64_t n = t / cq;
+  const int ci = 4 * (int)(t - n * cq);
+  const int c = (int)(n & 7);
+  const int32_t rq = rows1[n >> 3];
+  const int a = rq & 7;
+  const int axx = a >> 2, ayy = (a >> 1) & 1, azz = a & 1;
+  const int cx = c >> 2, cy = (c >> 1) & 1, cz = c & 1;
+  float4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (!((axx && !cx) || (ayy && !cy) || (azz && !cz))) {
+    const int32_t f = nbr1[27 * (int64_t)(rq >> 3) + (axx + 1) * 9 + (ayy + 1) * 3 + (azz + 1)];
+    if (f >= 0) {
+      const int64_t p = f >> 3;
+      const int dxo = axx ? -1 : cx, dyo = ayy ? -1 : cy, dzo = azz ? -1 : cz;
+      const int k = (dxo + 1) * 9 + (dyo + 1) * 3 + (dzo + 1);
+      const float* wr = w + ((int64_t)k * cin + ci) * cout;
+      const float4* gr = reinterpret_cast<const float4*>(dyg + p * cout);
+      for (int co = 0; co < cout; co += 4) {
+        const float4 g = gr[co / 4];
+        const float4 w0 = *reinterpret_cast<const float4*>(wr + co);
+        const float4 w1 = *reinterpret_cast<const float4*>(wr + cout + co);
+        const float4 w2 = *reinterpret_cast<const float4*>(wr + 2 * cout + co);
+        const float4 w3 = *reinterpret_cast<const float4*>(wr + 3 * cout + co);
+        acc.x += w0.x * g.x + w0.y * g.y + w0.z * g.z + w0.w * g.w;
+        acc.y += w1.x * g.x + w1.y * g.y + w1.z * g.z + w1.w * g.w;
+        acc.z += w2.x * g.x + w2.y * g.y + w2.z * g.z + w2.w * g.w;
+        acc.w += w3.x * g.x + w3.y * g.y + w3.z * g.z + w3.w * g.w;
+      }
+    }
+  }
+  *reinterpret_cast<float4*>(dx + n * cin + ci) = acc;
+}
+
 inline unsigned grid_for(int64_t n) { return (unsigned)oc::cdiv(n, TB); }
 
 // The profiling events pending for the calling thread (oc_profile_next)
@@ -495,11 +604,11 @@ struct S2Shape {
   int64_t gc;  // groups per column-buffer chunk
 };
 
-S2Shape s2_shape(const oc_octree* t, int l, int cin, size_t elsize) {
+S2Shape s2_shape(const oc_octree* t, int l, int r, int cin, size_t elsize) {
   S2Shape h;
-  h.G = t->M[l - 1];
+  h.G = t->M[l - r];
   h.n_in = t->N[l];
-  h.n_out = t->N[l - 1];
+  h.n_out = t->N[l - r];
   h.kc = 27 * (int64_t)cin;
   h.gc = std::max<int64_t>(1, std::min<int64_t>(h.G, (int64_t)(COL_CAP / (h.kc * elsize))));
   return h;
@@ -533,22 +642,24 @@ void launch_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const void
 
 namespace oc {
 
-size_t conv_s2_fwd_ws(const oc_octree* t, int l, int cin, int cout, bool bf16) {
-  const S2Shape h = s2_shape(t, l, cin, bf16 ? 2 : 4);
+size_t conv_s2_fwd_ws(const oc_octree* t, int l, int r, int cin, int cout, bool bf16) {
+  const S2Shape h = s2_shape(t, l, r, cin, bf16 ? 2 : 4);
   if (h.G == 0) return 0;
-  if (s2_fwd_direct(t, l, cin, cout, bf16))  // the transposed weights
+  if (r == 1 && s2_fwd_direct(t, l, cin, cout, bf16))  // the transposed weights
     return align256((size_t)27 * cin * cout * 4);
   return align256((size_t)h.gc * h.kc * (bf16 ? 2 : 4)) + align256((size_t)h.G * cout * 4);
 }
 
-size_t conv_s2_bwd_ws(const oc_octree* t, int l, int cin, int cout, bool bf16, bool dx, bool dw) {
+size_t conv_s2_bwd_ws(const oc_octree* t, int l, int r, int cin, int cout, bool bf16, bool dx,
+                      bool dw) {
   const size_t es = bf16 ? 2 : 4;
-  const S2Shape h = s2_shape(t, l, cin, es);
+  const S2Shape h = s2_shape(t, l, r, cin, es);
   if (h.G == 0 || (!dx && !dw)) return 0;
   const size_t b = align256((size_t)h.G * cout * es);                         // dY_g
-  const size_t a = dx ? align256((size_t)64 * cin * cout * es) +              // Wx
-                            align256((size_t)h.G * 8 * cout * es)             // D
-                      : 0;
+  const size_t a = !dx ? 0
+                   : r == 2 ? 0                                               // (stride 4: none)
+                            : align256((size_t)64 * cin * cout * es) +        // Wx
+                                  align256((size_t)h.G * 8 * cout * es);      // D
   const size_t c = dw ? align256((size_t)h.gc * h.kc * es) +                 // Col chunk
                             align256((size_t)DW_BATCH * h.kc * cout * 4)      // partial dW
                       : 0;
@@ -557,35 +668,47 @@ size_t conv_s2_bwd_ws(const oc_octree* t, int l, int cin, int cout, bool bf16, b
 
 namespace {
 
-// Column buffer of ng groups from g0, 16-byte pieces when the rows allow.
-void launch_col(hipStream_t s, const int32_t* nbr, int64_t g0, int64_t ng, const void* x, int cin,
-                bool bf16, void* col) {
+// Column buffer of ng groups from g0, 16-byte pieces when the rows allow;
+// r = 1: nbr is the depth-l table; r = 2: the depth-(l-1) table with the
+// depth-(l-1) labels lab.
+template <int RR>
+void launch_col_r(hipStream_t s, const int32_t* nbr, const int32_t* lab, int64_t g0, int64_t ng,
+                  const void* x, int cin, bool bf16, void* col) {
   const int rb = cin * (bf16 ? 2 : 4);
   if (rb % 16 == 0) {
     const int64_t nt = ng * 27 * (rb / 16);
     if (bf16)
-      hipLaunchKernelGGL(k_s2_col<uint16_t>, dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0, ng,
-                         (const uint16_t*)x, rb, (uint16_t*)col);
+      hipLaunchKernelGGL((k_s2_col<uint16_t, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab,
+                         g0, ng, (const uint16_t*)x, rb, (uint16_t*)col);
     else
-      hipLaunchKernelGGL(k_s2_col<float>, dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0, ng,
-                         (const float*)x, rb, (float*)col);
+      hipLaunchKernelGGL((k_s2_col<float, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab, g0,
+                         ng, (const float*)x, rb, (float*)col);
   } else {
     const int64_t nt = ng * 27 * cin;
     if (bf16)
-      hipLaunchKernelGGL(k_s2_col1<uint16_t>, dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0, ng,
-                         (const uint16_t*)x, cin, (uint16_t*)col);
+      hipLaunchKernelGGL((k_s2_col1<uint16_t, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab,
+                         g0, ng, (const uint16_t*)x, cin, (uint16_t*)col);
     else
-      hipLaunchKernelGGL(k_s2_col1<float>, dim3(grid_for(nt)), dim3(TB), 0, s, nbr, g0, ng,
-                         (const float*)x, cin, (float*)col);
+      hipLaunchKernelGGL((k_s2_col1<float, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab,
+                         g0, ng, (const float*)x, cin, (float*)col);
   }
+}
+
+void launch_col(hipStream_t s, const oc_octree* t, int l, int r, int64_t g0, int64_t ng,
+                const void* x, int cin, bool bf16, void* col) {
+  if (r == 1)
+    launch_col_r<1>(s, (const int32_t*)t->nbr[l], nullptr, g0, ng, x, cin, bf16, col);
+  else
+    launch_col_r<2>(s, (const int32_t*)t->nbr[l - 1], (const int32_t*)t->labels[l - 1], g0, ng, x,
+                    cin, bf16, col);
 }
 
 }  // namespace
 
-oc_status conv_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const void* w, int cout,
-                      bool bf16, float* y, int relu, void* ws, hipStream_t s) {
+oc_status conv_s2_fwd(const oc_octree* t, int l, int r, const void* x, int cin, const void* w,
+                      int cout, bool bf16, float* y, int relu, void* ws, hipStream_t s) {
   PassEvents ev(s);
-  if (s2_fwd_direct(t, l, cin, cout, bf16)) {
+  if (r == 1 && s2_fwd_direct(t, l, cin, cout, bf16)) {
     if ((uintptr_t)x % 16 != 0 || (uintptr_t)y % 16 != 0)
       return fail(OC_ERR_ARG, "oc_conv_fwd: stride 2 needs 16-byte aligned x and y");
     // output channels per workgroup: 16 WN; row blocks per wave: the most
@@ -604,7 +727,7 @@ oc_status conv_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const v
 #undef OC_S2F
     return fail(OC_ERR_UNSUPPORTED, "stride-2 forward: no kernel for %d -> %d", cin, cout);
   }
-  const S2Shape h = s2_shape(t, l, cin, bf16 ? 2 : 4);
+  const S2Shape h = s2_shape(t, l, r, cin, bf16 ? 2 : 4);
   const int32_t* nbr = t->nbr[l];
   char* p = (char*)ws;
   void* col = p;
@@ -612,7 +735,7 @@ oc_status conv_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const v
   const rocblas_datatype dt = bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
   for (int64_t g0 = 0; g0 < h.G; g0 += h.gc) {
     const int64_t ng = std::min<int64_t>(h.gc, h.G - g0);
-    launch_col(s, nbr, g0, ng, x, cin, bf16, col);
+    launch_col(s, t, l, r, g0, ng, x, cin, bf16, col);
     // yg^T [cout][ng] = W^T-view [cout][27 cin] x Col^T-view [27 cin][ng] (column-major)
     oc_status st = gemm(s, false, false, cout, ng, h.kc, w, dt, cout, col, dt, h.kc, 0.f,
                         yg + g0 * cout, cout);
@@ -620,19 +743,19 @@ oc_status conv_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const v
   }
   if (cout % 4 == 0 && (uintptr_t)y % 16 == 0)
     hipLaunchKernelGGL(k_s2_rows_out, dim3(grid_for(h.n_out * (cout / 4))), dim3(TB), 0, s,
-                       (const int32_t*)t->labels[l - 1], h.n_out, (const float*)yg, cout, relu, y);
+                       (const int32_t*)t->labels[l - r], h.n_out, (const float*)yg, cout, relu, y);
   else
     hipLaunchKernelGGL(k_s2_rows_out1, dim3(grid_for(h.n_out * cout)), dim3(TB), 0, s,
-                       (const int32_t*)t->labels[l - 1], h.n_out, (const float*)yg, cout, relu, y);
+                       (const int32_t*)t->labels[l - r], h.n_out, (const float*)yg, cout, relu, y);
   return OC_OK;
 }
 
-oc_status conv_s2_bwd(const oc_octree* t, int l, const void* x, int cin, const void* w, int cout,
-                      bool bf16, const float* ym, const float* dy, float* dx, float* dw, void* ws,
-                      hipStream_t s) {
+oc_status conv_s2_bwd(const oc_octree* t, int l, int r, const void* x, int cin, const void* w,
+                      int cout, bool bf16, const float* ym, const float* dy, float* dx, float* dw,
+                      void* ws, hipStream_t s) {
   PassEvents ev(s);
   const size_t es = bf16 ? 2 : 4;
-  const S2Shape h = s2_shape(t, l, cin, es);
+  const S2Shape h = s2_shape(t, l, r, cin, es);
   const int64_t entries = h.kc * cout;
   if (h.G == 0) {
     if (dx && h.n_in > 0) fill_u32(dx, 0u, h.n_in * cin, s);
@@ -645,7 +768,7 @@ oc_status conv_s2_bwd(const oc_octree* t, int l, const void* x, int cin, const v
   void* dyg = p;
   p += align256((size_t)h.G * cout * es);
   const bool vec = cout % 4 == 0 && (uintptr_t)dy % 16 == 0 && (uintptr_t)ym % 16 == 0;
-  const int32_t* prow = (const int32_t*)t->rows[l - 1];
+  const int32_t* prow = (const int32_t*)t->rows[l - r];
   if (vec && bf16)
     hipLaunchKernelGGL(k_s2_dy_rows<uint16_t>, dim3(grid_for(h.G * (cout / 4))), dim3(TB), 0, s,
                        prow, h.G, dy, ym, cout, (uint16_t*)dyg);
@@ -658,7 +781,22 @@ oc_status conv_s2_bwd(const oc_octree* t, int l, const void* x, int cin, const v
   else
     hipLaunchKernelGGL(k_s2_dy_rows1<float>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow,
                        h.G, dy, ym, cout, (float*)dyg);
-  if (dx) {
+  if (dx && r == 2) {
+    const int64_t nt = h.n_in * (int64_t)cin;
+    if (bf16)
+      hipLaunchKernelGGL(k_s4_dx<uint16_t>, dim3(grid_for(nt)), dim3(TB), 0, s,
+                         (const int32_t*)t->rows[l - 1], (const int32_t*)t->nbr[l - 1], h.n_in,
+                         (const uint16_t*)dyg, (const uint16_t*)w, cin, cout, dx);
+    else if (cin % 4 == 0 && cout % 4 == 0 && (uintptr_t)w % 16 == 0 && (uintptr_t)dx % 16 == 0 &&
+             (uintptr_t)dyg % 16 == 0)
+      hipLaunchKernelGGL(k_s4_dx4, dim3(grid_for(nt / 4)), dim3(TB), 0, s,
+                         (const int32_t*)t->rows[l - 1], (const int32_t*)t->nbr[l - 1], h.n_in,
+                         (const float*)dyg, (const float*)w, cin, cout, dx);
+    else
+      hipLaunchKernelGGL(k_s4_dx<float>, dim3(grid_for(nt)), dim3(TB), 0, s,
+                         (const int32_t*)t->rows[l - 1], (const int32_t*)t->nbr[l - 1], h.n_in,
+                         (const float*)dyg, (const float*)w, cin, cout, dx);
+  } else if (dx) {
     void* wx = p;
     void* D = p + align256((size_t)64 * cin * cout * es);
     const int64_t nw = (int64_t)64 * cin * cout;
@@ -695,7 +833,7 @@ oc_status conv_s2_bwd(const oc_octree* t, int l, const void* x, int cin, const v
     fill_u32(pw, 0u, DW_BATCH * E, s);
     for (int64_t g0 = 0; g0 < h.G; g0 += h.gc) {
       const int64_t ng = std::min<int64_t>(h.gc, h.G - g0);
-      launch_col(s, nbr, g0, ng, x, cin, bf16, col);
+      launch_col(s, t, l, r, g0, ng, x, cin, bf16, col);
       // partial b: dW^T [cout][27 cin] += dyg^T-view [cout][sz] x Col-view^T [sz][27 cin]
       // over groups g0 + b sz .. g0 + (b+1) sz; the rest of the chunk adds to partial 0
       const int64_t sz = ng / DW_BATCH, done = sz * DW_BATCH;

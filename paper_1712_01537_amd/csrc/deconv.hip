@@ -17,9 +17,12 @@
 
 namespace {
 
-oc_status check_deconv(const oc_octree* t, int32_t l, oc_dtype dt, int32_t flags, const char* who) {
+oc_status check_deconv(const oc_octree* t, int32_t l, int32_t stride, oc_dtype dt, int32_t flags,
+                       const char* who) {
   oc_status st = oc::check_tree_level(t, l, 1);
   if (st != OC_OK) return st;
+  if (stride != 1 && stride != 2)
+    return oc::fail(OC_ERR_UNSUPPORTED, "%s: stride %d not 1 or 2", who, stride);
   if (dt != OC_F32) return oc::fail(OC_ERR_UNSUPPORTED, "%s: only OC_F32 is supported", who);
   if (flags != 0) return oc::fail(OC_ERR_ARG, "%s: flags must be 0", who);
   return OC_OK;
@@ -31,14 +34,14 @@ extern "C" {
 
 size_t oc_deconv_fwd_workspace(const oc_octree* t, int32_t l, int32_t K, int32_t stride,
                                oc_dtype dt, int32_t cin, int32_t cout) {
-  if (check_deconv(t, l, dt, 0, "oc_deconv_fwd_workspace") != OC_OK) return 0;
+  if (check_deconv(t, l, stride, dt, 0, "oc_deconv_fwd_workspace") != OC_OK) return 0;
   return oc_conv_bwd_workspace(t, l, K, stride, dt, cout, cin);
 }
 
 oc_status oc_deconv_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,
                         const void* x, int32_t cin, const void* w, int32_t cout, float* y,
                         void* ws, size_t ws_bytes, int32_t flags, hipStream_t s) {
-  oc_status st = check_deconv(t, l, dt, flags, "oc_deconv_fwd");
+  oc_status st = check_deconv(t, l, stride, dt, flags, "oc_deconv_fwd");
   if (st != OC_OK) return st;
   if (!x || !w || !y) return oc::fail(OC_ERR_ARG, "oc_deconv_fwd: NULL buffer");
   return oc_conv_bwd(t, l, K, stride, dt, nullptr, cout, w, cin, nullptr,
@@ -47,7 +50,7 @@ oc_status oc_deconv_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride
 
 size_t oc_deconv_bwd_workspace(const oc_octree* t, int32_t l, int32_t K, int32_t stride,
                                oc_dtype dt, int32_t cin, int32_t cout) {
-  if (check_deconv(t, l, dt, 0, "oc_deconv_bwd_workspace") != OC_OK) return 0;
+  if (check_deconv(t, l, stride, dt, 0, "oc_deconv_bwd_workspace") != OC_OK) return 0;
   return std::max(oc_conv_fwd_workspace(t, l, K, stride, dt, cout, cin),
                   oc_conv_bwd_workspace(t, l, K, stride, dt, cout, cin));
 }
@@ -56,7 +59,7 @@ oc_status oc_deconv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride
                         const void* x, int32_t cin, const void* w, int32_t cout, const float* dy,
                         float* dx, float* dw, void* ws, size_t ws_bytes, int32_t flags,
                         hipStream_t s) {
-  oc_status st = check_deconv(t, l, dt, flags, "oc_deconv_bwd");
+  oc_status st = check_deconv(t, l, stride, dt, flags, "oc_deconv_bwd");
   if (st != OC_OK) return st;
   if (!w || !dy) return oc::fail(OC_ERR_ARG, "oc_deconv_bwd: NULL w or dy");
   if (dw && !x) return oc::fail(OC_ERR_ARG, "oc_deconv_bwd: dw needs x");

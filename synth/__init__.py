@@ -24,6 +24,8 @@ seg_d6      6      32     20k       conv3+ReLU+pool 3->16 @6, 16->32 @5; stride-
                                     d4->d5; unpool d5->d6; deconv3 16->16 @6
 gpool_d6    6      32     20k       conv3+ReLU 3->16 @6; 3x3x3 max-pool and 5x5x5 average-pool,
                                     stride 1, @6; 2x2x2 max-pool d6->d5
+s4_d6       6      32     20k       conv3+ReLU 3->16 @6; stride-4 conv3+ReLU 16->64 d6->d4;
+                                    conv3 64->128 @4
 ==========  =====  =====  ========  ===============================================
 
 seg_d6 is the decoder side of the paper's segmentation network (Sec. 4,
@@ -137,6 +139,14 @@ WORKLOADS = {
             Layer("gpool", 6, 16, 16, ksize=3, mode="max"),
             Layer("gpool", 6, 16, 16, ksize=5, mode="avg"),
             Layer("pool", 6, 16, 16),
+        ),
+    ),
+    "s4_d6": Workload(
+        "s4_d6", 8, 6, 32, 20_000, "union",
+        (
+            Layer("conv", 6, 3, 16, relu=True),
+            Layer("conv", 6, 16, 64, stride=4, relu=True),
+            Layer("conv", 4, 64, 128),
         ),
     ),
 }

@@ -93,6 +93,46 @@ def test_conv_small_fp32(seed, B, n, depth, K, stride, cin, cout, relu):
     assert torch.equal(dw.view(torch.int32), dw2.view(torch.int32))
 
 
+S4_SMALL = [  # seed, B, n, depth, cin, cout, relu, bf16
+    (101, 2, 400, 4, 5, 7, False, False),
+    (102, 3, 600, 5, 16, 32, True, False),
+    (103, 1, 900, 5, 64, 16, False, False),  # column-buffer chunks of many channels
+    (104, 2, 500, 4, 8, 12, False, True),
+    (105, 2, 800, 5, 32, 32, True, True),
+]
+
+
+@pytest.mark.parametrize("seed,B,n,depth,cin,cout,relu,bf16", S4_SMALL)
+def test_conv_stride4(seed, B, n, depth, cin, cout, relu, bf16):
+    """Stride 4 (Sec. 3.2, stride 2^r with r = 2): depth l -> depth l-2."""
+    oc = _oc()
+    print(f"[s4] seed={seed} B={B} d={depth} {cin}->{cout} relu={relu} bf16={bf16}", flush=True)
+    pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
+    ref, tree = _trees(pts, nrm, offs, depth)
+    l = depth
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((ref.num(l), cin)).astype(np.float32)
+    w = (rng.standard_normal((27, cin, cout)) / np.sqrt(27 * cin)).astype(np.float32)
+    dt = torch.bfloat16 if bf16 else torch.float32
+    xq, wq = (bf16_round(x), bf16_round(w)) if bf16 else (x, w)
+    pre = oracle.conv_sr_fwd(ref, l, xq, wq, 4)
+    dy = _mask_ambiguous(rng.standard_normal((ref.num(l - 2), cout)).astype(np.float32), pre, relu)
+    y = oc.oc_conv_fwd(tree, l, 3, 4, _cuda(x, dt), _cuda(w, dt), relu=relu)
+    assert_f32_close(y.cpu().numpy(), oracle.relu_fwd(pre) if relu else pre, "y")
+    dx, dw = oc.oc_conv_bwd(tree, l, 3, 4, _cuda(x, dt), _cuda(w, dt), _cuda(dy), y=y, relu=relu)
+    dye = oracle.relu_bwd(pre, dy) if relu else dy
+    if bf16:  # the bf16 backward multiplies dy rounded to bf16
+        dye = bf16_round(dye)
+    dxr, dwr = oracle.conv_sr_bwd(ref, l, xq, wq, dye, 4)
+    assert_f32_close(dx.cpu().numpy(), dxr, "dx")
+    assert_dw_close(dw.cpu().numpy(), dwr, "dw")
+    dx2, dw2 = oc.oc_conv_bwd(tree, l, 3, 4, _cuda(x, dt), _cuda(w, dt), _cuda(dy), y=y, relu=relu)
+    assert torch.equal(dx.view(torch.int32), dx2.view(torch.int32))
+    assert torch.equal(dw.view(torch.int32), dw2.view(torch.int32))
+    with pytest.raises(oc.OcError):  # stride 4 takes K = 3 only
+        oc.oc_conv_fwd(tree, l, 5, 4, _cuda(x), _cuda(np.zeros((125, cin, cout))))
+
+
 DECONV_SMALL = [  # seed, B, n, depth, K, stride, cin, cout (deconv channels)
     (81, 2, 400, 4, 3, 1, 7, 5),
     (82, 2, 900, 5, 3, 1, 128, 64),  # split reduction in the forward (input-gradient kernel)
@@ -339,10 +379,11 @@ def _check_conv_full(ref, tree, l, K, stride, x, w, relu, dy, tag, dtype=torch.f
     print(f"[{tag}] conv d{l} K{K} s{stride} {x.shape[1]}->{w.shape[2]} rows {n_in}", flush=True)
     y = oc.oc_conv_fwd(tree, l, K, stride, _cuda(xq, dtype), _cuda(wq, dtype), relu=relu)
     yg = y.cpu().numpy()
-    if relu or stride == 2:
+    r = stride.bit_length() - 1  # stride 2^r
+    if relu or stride > 1:
         pre = oracle.conv_fwd(nb, xq, wq)
-        if stride == 2:
-            pre = oracle.renew(ref.labels(l - 1), pre)
+        if stride > 1:
+            pre = oracle.renew(ref.labels(l - r), pre)
         dy = _mask_ambiguous(dy, pre, relu)
         assert_f32_close(yg, oracle.relu_fwd(pre) if relu else pre, f"{tag} y")
         dye = oracle.relu_bwd(pre, dy) if relu else dy
@@ -361,7 +402,7 @@ def _check_conv_full(ref, tree, l, K, stride, x, w, relu, dy, tag, dtype=torch.f
         dxr = oracle.conv_bwd_data(nb, dye, wq, n_in, want=want)
         dwr = oracle.conv_bwd_weight(nb, xq, dye, K ** 3, entries=ent)
     else:
-        dyh = oracle.renew_bwd(ref.labels(l - 1), dye, nb.shape[0])
+        dyh = oracle.renew_bwd(ref.labels(l - r), dye, nb.shape[0])
         dxr = oracle.conv_bwd_data(nb, dyh, wq, n_in, want=want)
         dwr = oracle.conv_bwd_weight(nb, xq, dyh, K ** 3, entries=ent)
     assert_f32_close(dx.cpu().numpy()[want], dxr[want], f"{tag} dx")
@@ -397,7 +438,7 @@ def _check_deconv_full(ref, tree, l, K, stride, x, w, dy, tag):
 
 
 @pytest.mark.parametrize("name", ["sphere_d5", "net_d5", "net_d6", "deep_d8", "wide_d7", "seg_d6",
-                                  "gpool_d6"])
+                                  "gpool_d6", "s4_d6"])
 def test_workload_full_size(name):
     oc = _oc()
     w_ = synth.WORKLOADS[name]
@@ -414,7 +455,7 @@ def test_workload_full_size(name):
             first = False
             K = L.ksize
             w = synth.make_weights(w_, li, K, L.cin, L.cout)
-            n_out = ref.num(l) if L.stride == 1 else ref.num(l - 1)
+            n_out = ref.num(l - (L.stride.bit_length() - 1))
             dy = synth.make_upstream(w_, li, n_out, L.cout)
             _check_conv_full(ref, tree, l, K, L.stride, x, w, L.relu, dy, f"{name}/{li}")
             if L.dtype == "bf16":
