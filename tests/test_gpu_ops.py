@@ -362,6 +362,50 @@ def test_conv_edge_cases():
         oc.oc_conv_fwd(tree, 3, 7, 1, _cuda(np.zeros((ref.num(3), 2))), _cuda(np.zeros((343, 2, 3))))
 
 
+def test_new_ops_degenerate_trees():
+    """Deconvolution, general pooling and stride 4 on a one-point tree with
+    full depth 0 (one sibling group per depth, most neighbours outside the
+    cube) and at the shallowest depths they accept."""
+    oc = _oc()
+    pts = np.array([[0.3, 0.6, 0.9]], np.float32)
+    ref, tree = _trees(pts, np.ones((1, 3), np.float32), [0, 1], 3, 0)
+    rng = np.random.default_rng(7)
+    for l in (1, 2, 3):
+        n = ref.num(l)
+        for K in (3, 5):
+            x = rng.standard_normal((n, 4)).astype(np.float32)
+            nb = ref.neighbors(l, K)
+            for mode, rmode in ((oc.OC_POOL_MAX, oracle.POOL_MAX), (oc.OC_POOL_AVG, oracle.POOL_AVG)):
+                y, sw = oc.oc_gpool_fwd(tree, l, K, mode, _cuda(x))
+                yr, swr = oracle.gpool_fwd(nb, x, rmode)
+                assert_f32_close(y.cpu().numpy(), yr, f"gpool y l={l} K={K}")
+                if sw is not None:
+                    np.testing.assert_array_equal(sw.cpu().numpy(), swr)
+                dx = oc.oc_gpool_bwd(tree, l, K, mode, _cuda(x), sw)
+                assert_f32_close(dx.cpu().numpy(), oracle.gpool_bwd(nb, x, swr, n, rmode),
+                                 f"gpool dx l={l} K={K}")
+        w = rng.standard_normal((27, 3, 4)).astype(np.float32)  # deconv 4 -> 3
+        x = rng.standard_normal((n, 4)).astype(np.float32)
+        nb = ref.neighbors(l, 3)
+        assert_f32_close(oc.oc_deconv_fwd(tree, l, 3, 1, _cuda(x), _cuda(w)).cpu().numpy(),
+                         oracle.deconv_fwd(nb, x, w, n), f"deconv l={l}")
+        xs = rng.standard_normal((ref.num(l - 1), 4)).astype(np.float32)
+        assert_f32_close(oc.oc_deconv_fwd(tree, l, 3, 2, _cuda(xs), _cuda(w)).cpu().numpy(),
+                         oracle.deconv_s2_fwd(ref, l, xs, w), f"deconv s2 l={l}")
+    for l in (2, 3):  # stride 4 down to depths 0 and 1
+        x = rng.standard_normal((ref.num(l), 16)).astype(np.float32)
+        w = rng.standard_normal((27, 16, 16)).astype(np.float32)
+        y = oc.oc_conv_fwd(tree, l, 3, 4, _cuda(x), _cuda(w))
+        assert_f32_close(y.cpu().numpy(), oracle.conv_sr_fwd(ref, l, x, w, 4), f"s4 l={l}")
+        dy = rng.standard_normal((ref.num(l - 2), 16)).astype(np.float32)
+        dx, dw = oc.oc_conv_bwd(tree, l, 3, 4, _cuda(x), _cuda(w), _cuda(dy))
+        dxr, dwr = oracle.conv_sr_bwd(ref, l, x, w, dy, 4)
+        assert_f32_close(dx.cpu().numpy(), dxr, f"s4 dx l={l}")
+        assert_dw_close(dw.cpu().numpy(), dwr, f"s4 dw l={l}")
+    with pytest.raises(oc.OcError):  # stride 4 from depth 1
+        oc.oc_conv_fwd(tree, 1, 3, 4, _cuda(np.zeros((ref.num(1), 16))), _cuda(np.zeros((27, 16, 16))))
+
+
 # ----------------------------------------------------------------------------
 # full-size workloads, sampled
 
