@@ -759,7 +759,7 @@ def main():
         summarize_trace(*args.summarize_trace)
         return
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+        print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
               f"(the path would shard by shape with one dW all-reduce per layer, not built)",
               file=sys.stderr)
         sys.exit(2)
