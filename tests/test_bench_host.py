@@ -100,3 +100,35 @@ def test_summarize_trace(tmp_path, capsys):
     assert f"{tf:.1f} TFLOP/s" in out
     assert "other kernels (at::native::copy)" in out
     assert "`k_conv_tile3<4, 8, false>` | 15 | 40.00 |" in out
+
+
+def test_accounting_of_deconvolution_gpool_and_stride4():
+    """Flops and bytes of the ops added beside the convolution, computed by
+    hand from the per-depth sizes."""
+    N = [2, 16, 128, 1024, 8192]
+    M = [2, 16, 100, 700, 3000]
+    wl = synth.Workload("t", 0, 4, 2, 1000, "union", (
+        synth.Layer("conv", 4, 3, 16),
+        synth.Layer("conv", 4, 16, 32, stride=4),
+        synth.Layer("deconv", 4, 32, 8, stride=2),
+        synth.Layer("gpool", 4, 8, 8, ksize=5, mode="avg"),
+        synth.Layer("gpool", 4, 8, 8, ksize=3, mode="max"),
+    ), signal_input=False)
+    acc = bench.Accounting(wl, N, M, 2000)
+    c0, s4, dc, ga, gm = wl.layers
+    # stride 4 from depth 4 evaluates at the depth-2 rows; the stride-2
+    # deconvolution to depth 4 runs the stride-2 convolution at depth 4 (rows of depth 3)
+    assert acc.work("conv_fwd", s4) == 2 * N[2] * 27 * 16 * 32
+    assert acc.work("deconv_fwd", dc) == 2 * N[3] * 27 * 32 * 8
+    assert acc.work("deconv_bwd_weight", dc) == acc.work("deconv_fwd", dc)
+    flops, octs = acc.conv_flops()
+    assert flops == (4 * N[4] * 27 * 3 * 16 + 6 * N[2] * 27 * 16 * 32 + 6 * N[3] * 27 * 32 * 8)
+    assert octs == N[4] + N[2] + N[4]
+    # general pooling: rows in and out, switches for max, the groups' 27 entries
+    assert acc.work("gpool_fwd", ga) == N[4] * 8 * 8 + M[3] * 108
+    assert acc.work("gpool_bwd", gm) == N[4] * 8 * 8 + N[4] * 8 + M[3] * 108
+    assert bench.BOUND["gpool_fwd"] == "hbm" and bench.BOUND["deconv_fwd"] == "mfma"
+    assert bench.trace_class("k_gpool_fwd<2, true, 4>") == "pool"
+    assert bench.trace_class("k_s2_fwd<4, 4>") == "conv_main"
+    assert bench.trace_class("k_s2_col<float>") == "conv_helper"
+    assert bench.op_rate("deconv_fwd", 2e9, 1000.0, False)["unit"] == "TFLOP/s"
