@@ -357,8 +357,10 @@ oc_status oc_gpool_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int3
                        const float* x, int32_t c, float* y, uint8_t* sw, hipStream_t stream);
 
 /* Gradient of oc_gpool_fwd: dx[n][c] = the sum, in tap order, over the octants
- * i whose tap k reaches n of dy[i][c] if sw[i][c] == k (max) or
- * dy[i][c] / K^3 (average).  A gather (no atomics): deterministic.
+ * i whose tap k reaches n of dy[i][c] if sw[i][c] == k (max), or, for the
+ * average, the sum of dy over n's own neighbourhood divided by K^3 (the same
+ * octants: i reaches n at offset d exactly when n reaches i at -d; it is
+ * the forward applied to dy).  A gather (no atomics): deterministic.
  *   dy dev f32 [N_l][c];  sw as produced by oc_gpool_fwd (max) or NULL;
  *   dx dev f32 [N_l][c]. */
 oc_status oc_gpool_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t mode,

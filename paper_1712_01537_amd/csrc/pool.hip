@@ -228,10 +228,11 @@ __global__ __launch_bounds__(TB) void k_gpool_fwd(const int32_t* __restrict__ nb
   reinterpret_cast<F*>(y)[t] = acc;
 }
 
-// Backward as a gather, in tap order: input row n receives, from the octant
-// i whose tap k lands on n (i is n's neighbour at the mirrored offset, tap
-// K^3 - 1 - k), dy[i] if sw[i] == k (max) or dy[i] / K^3 (average).
-template <int R, bool AVG, int VEC>
+// Backward of the max as a gather, in tap order: input row n receives, from
+// the octant i whose tap k lands on n (i is n's neighbour at the mirrored
+// offset, tap K^3 - 1 - k), dy[i] where sw[i] == k.  (The average's
+// backward runs on the forward kernel; see gpool below.)
+template <int R, int VEC>
 __global__ __launch_bounds__(TB) void k_gpool_bwd(const int32_t* __restrict__ nbr, int64_t n,
                                                   const float* __restrict__ dy,
                                                   const uint8_t* __restrict__ sw, int cv,
@@ -261,19 +262,15 @@ __global__ __launch_bounds__(TB) void k_gpool_bwd(const int32_t* __restrict__ nb
       for (int e = 0; e < VEC; ++e) set(g[j], e, 0.f), set(s[j], e, (uint8_t)255);
       if (src[j] >= 0) {
         g[j] = gv[src[j] * cv + q];
-        if constexpr (!AVG) s[j] = sv[src[j] * cv + q];
+        s[j] = sv[src[j] * cv + q];
       }
     }
 #pragma unroll
     for (int j = 0; j < KB; ++j) {
       if (src[j] < 0) continue;
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        if constexpr (AVG)
-          set(acc, e, comp(acc, e) + comp(g[j], e) / (float)K3);
-        else if (comp(s[j], e) == k0 + j)
-          set(acc, e, comp(acc, e) + comp(g[j], e));
-      }
+      for (int e = 0; e < VEC; ++e)
+        if (comp(s[j], e) == k0 + j) set(acc, e, comp(acc, e) + comp(g[j], e));
     }
   }
   reinterpret_cast<F*>(dx)[t] = acc;
@@ -313,12 +310,23 @@ oc_status gpool(const oc_octree* t, int32_t l, int32_t K, int32_t mode, const fl
   const int cv = v4 ? c / 4 : c;
   const dim3 grid(grid_for(n * cv));
   const int32_t* nbr = (const int32_t*)t->nbr[l];
+  // The average's backward is the average itself applied to dy: the tap-k
+  // neighbour relation is symmetric (n sees i at offset d iff i sees n at
+  // -d), so both are dy summed over n's neighbourhood / K^3.  It runs on the
+  // forward kernel, whose taps are batched (the same sum, divided once).
 #define OC_GP(R_, AVG_, V_)                                                                   \
   if (K == 2 * R_ + 1 && avg == AVG_ && (v4 ? 4 : 1) == V_) {                                 \
-    if constexpr (BWD)                                                                        \
-      oc::launch_main(k_gpool_bwd<R_, AVG_, V_>, grid, dim3(TB), s, nbr, n, in, swin, cv, out); \
-    else                                                                                      \
-      oc::launch_main(k_gpool_fwd<R_, AVG_, V_>, grid, dim3(TB), s, nbr, n, in, cv, out, swout); \
+    if constexpr (BWD) {                                                                      \
+      if (AVG_)                                                                               \
+        oc::launch_main(k_gpool_fwd<R_, true, V_>, grid, dim3(TB), s, nbr, n, in, cv, out,    \
+                        (uint8_t*)nullptr);                                                   \
+      else                                                                                    \
+        oc::launch_main(k_gpool_bwd<R_, V_>, grid, dim3(TB), s, nbr, n, in, swin, cv,         \
+                        out);                                                                 \
+    } else {                                                                                  \
+      oc::launch_main(k_gpool_fwd<R_, AVG_, V_>, grid, dim3(TB), s, nbr, n, in, cv, out,      \
+                      swout);                                                                 \
+    }                                                                                         \
   }
   OC_GP(1, false, 4) OC_GP(1, false, 1) OC_GP(1, true, 4) OC_GP(1, true, 1)
   OC_GP(2, false, 4) OC_GP(2, false, 1) OC_GP(2, true, 4) OC_GP(2, true, 1)
