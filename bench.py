@@ -381,9 +381,13 @@ class Accounting:
         return self.N[L.depth - (L.stride.bit_length() - 1)]  # strided deconvolution
 
     def _n_conv(self, L):
-        """Output rows of the convolution a conv or deconv layer runs (a
-        deconvolution runs the passes of the convolution it transposes)."""
-        return self.N[L.depth - (L.stride.bit_length() - 1)]
+        """Rows at which the convolution a conv or deconv layer runs is
+        evaluated (a deconvolution runs the passes of the convolution it
+        transposes): every depth-l row at stride 1; at stride 2^r only the
+        M[l-r] non-empty depth-(l-r) octants (the empty ones get zero rows
+        without any arithmetic)."""
+        r = L.stride.bit_length() - 1
+        return self.N[L.depth] if r == 0 else self.M[L.depth - r]
 
     def conv_flops(self):
         """Algorithmic flops of the step's conv passes (forward, weight gradient,
@@ -471,6 +475,11 @@ class Step(Accounting):
                 self.x0 = self.x0.to(torch.bfloat16)
         self.side = None  # stream for the weight gradients (None: all on one stream)
         self.events = None  # {key: [(start, end, layer), ...]} when recording
+        # when a list: every op of the step (not the build) is run with all of
+        # its kernels bracketed (oc_profile_calls), one CallProfile per op
+        self.calls = None
+        self.record = None  # a dict: network() keeps its tensors there
+        self.call_pool = [oc.CallProfile(32) for _ in range(3 * len(wl.layers) + 2)]
         self.traced = set()
         # when set: only the (step number % rotate)-th launch of a traced key
         # in each step is bracketed (each bracketing costs the step time)
@@ -500,6 +509,16 @@ class Step(Accounting):
     def _run(self, tag, li, fn):
         L = self.wl.layers[li] if li is not None else None
         k = self.key(tag, li)
+        if self.calls is not None and not tag.startswith("build"):
+            # every kernel of the call, each bracketed by its own events
+            prof = self.call_pool[len(self.calls)]
+            prof.arm()
+            try:
+                r = fn()
+            finally:
+                prof.disarm()
+            self.calls.append((prof, li, tag))
+            return r
         if self.events is not None and (k in self.traced or "*" in self.traced):
             if self.rotate:
                 n = self.ncall.get(k, 0)
@@ -599,8 +618,13 @@ class Step(Accounting):
                 x = u
         g = self.dy_last
         masked = False  # g already went through the ReLU of the conv below it
+        rec = self.record
+        if rec is not None:  # the tensors of this step, for a parity test
+            rec["fwd"] = {li: (xin, yout, sw) for li, xin, yout, sw in saved}
+            rec["bwd"] = {}
         for li, xin, yout, sw in reversed(saved):
             L = wl.layers[li]
+            g_in, dw = g, None
             if L.op == "conv":
                 w = self.weights[li]
                 relu = L.relu and not masked
@@ -633,7 +657,7 @@ class Step(Accounting):
                 w = self.weights[li]
                 dx, _ = self._run("deconv_bwd_data", li, lambda: oc.oc_deconv_bwd(
                     tree, L.depth, L.ksize, L.stride, xin, w, g, need_dx=True, need_dw=False))
-                self._run("deconv_bwd_weight", li, lambda: oc.oc_deconv_bwd(
+                _, dw = self._run("deconv_bwd_weight", li, lambda: oc.oc_deconv_bwd(
                     tree, L.depth, L.ksize, L.stride, xin, w, g, need_dx=False, need_dw=True))
                 g, masked = dx, False
             elif L.op == "gpool":
@@ -650,9 +674,22 @@ class Step(Accounting):
             elif L.op == "unpool":
                 g = self._run("unpool_bwd", li, lambda: oc.oc_unpool_bwd(tree, L.depth, g, sw))
                 masked = False
+            if rec is not None:
+                rec["bwd"][li] = (g_in, g, dw)
         if self.side is not None:
             self.torch.cuda.current_stream().wait_stream(self.side)
         return g
+
+    def collect_calls(self, acc):
+        """Add the kernel time of every op of the last step run with
+        self.calls set (the device work must be done) to acc: {(layer, tag):
+        [ms, calls, launches]}, and reset the list."""
+        for prof, li, tag in self.calls:
+            a = acc.setdefault((li, tag), [0.0, 0, 0])
+            a[0] += prof.kernel_ms()
+            a[1] += 1
+            a[2] += prof.used
+        self.calls = []
 
     def collect(self):
         """Per-key (total ms, launches, total work, op) of the recorded events."""
@@ -666,11 +703,10 @@ class Step(Accounting):
         return out
 
 
-def cpu_baseline(synth, wl, shapes):
+def oracle_step(synth, wl, shapes):
     """The oracle on the first `shapes` shapes of the batch: build, neighbour
-    search and the network's forward and backward, timed on the host."""
-    import numpy as np
-
+    search and the network's forward and backward.  Returns (algorithmic conv
+    flops of the step, seconds on the host)."""
     import oracle
 
     pts, nrm, offs = synth.make_points(wl, batch=shapes)
@@ -691,7 +727,7 @@ def cpu_baseline(synth, wl, shapes):
                 pre = oracle.renew(ref.labels(l - r), pre)
             y = oracle.relu_fwd(pre) if L.relu else pre
             saved.append((li, nb, x, w, pre))
-            flops += (6 if li > 0 else 4) * y.shape[0] * L.ksize ** 3 * L.cin * L.cout
+            flops += (6 if li > 0 else 4) * nb.shape[0] * L.ksize ** 3 * L.cin * L.cout
             x = y
         elif L.op == "deconv":
             w = synth.make_weights(wl, li, L.ksize, L.cout, L.cin)
@@ -701,7 +737,7 @@ def cpu_baseline(synth, wl, shapes):
             else:
                 y = oracle.deconv_s2_fwd(ref, l, x, w)
             saved.append((li, None, x, w, None))
-            n = ref.num(l) if L.stride == 1 else ref.num(l - 1)
+            n = ref.num(l) if L.stride == 1 else ref.nonempty(l - 1)
             flops += 6 * n * L.ksize ** 3 * L.cin * L.cout
             x = y
         elif L.op == "pool":
@@ -742,12 +778,57 @@ def cpu_baseline(synth, wl, shapes):
             g = oracle.gpool_bwd(nb, g, w_or_sw, ref.num(l), pre)
         else:
             g = oracle.pool_bwd(ref.labels(l - 1), g, w_or_sw, ref.num(l))
-    dt = time.perf_counter() - t0
-    return {"value": round(flops / dt / 1e9, 4), "unit": "GFLOP/s",
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"first {shapes} of {wl.batch} shapes of the same workload, one step "
-                      f"(build, neighbour search, forward and backward; {flops / 1e9:.2f} GFLOP "
-                      f"in {dt:.2f} s, float64)"}
+    return flops, time.perf_counter() - t0
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_baseline(synth, wl, max_shapes, budget_s=4.0):
+    """The oracle (as it stands, float64) timed on the host: a warm-up run on
+    one shape, then, at all threads and at one thread, the median of three
+    runs on the first s shapes of the batch, s sized from the warm-up so that
+    one run takes about budget_s seconds (at most max_shapes).  The one-thread
+    leg is skipped when a single shape would take over 30 s."""
+    import oracle
+
+    threads = oracle.num_threads()
+    f1, t1 = oracle_step(synth, wl, 1)  # warm-up (page faults, thread start)
+
+    def leg(nthr):
+        oracle.set_num_threads(nthr)
+        per_shape = t1 * threads / nthr  # an upper bound: perfect scaling over the threads
+        if per_shape > 30.0 and nthr == 1:
+            return None
+        s = max(1, min(max_shapes, int(budget_s / max(per_shape, 1e-3))))
+        runs = sorted(oracle_step(synth, wl, s) for _ in range(3))
+        flops, dt = runs[1]
+        return {"value": round(flops / dt / 1e9, 4), "shapes": s, "seconds": round(dt, 3),
+                "gflop": round(flops / 1e9, 3)}
+
+    try:
+        one = leg(1)
+        full = leg(threads)
+    finally:
+        oracle.set_num_threads(threads)
+    return {"value": full["value"], "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
+            "value_all": full["value"], "value_1t": one["value"] if one else None,
+            "cpu_model": cpu_model(),
+            "sample": f"one step (build, neighbour search, forward and backward, float64) of the "
+                      f"first {full['shapes']} of {wl.batch} shapes at {threads} threads "
+                      f"({full['gflop']} GFLOP, median of 3: {full['seconds']} s)"
+                      + (f", and of the first {one['shapes']} shapes at 1 thread "
+                         f"({one['gflop']} GFLOP, median of 3: {one['seconds']} s)" if one else
+                         ", 1 thread skipped (over 30 s per shape)")
+                      + "; oracle built with g++ -O3"}
 
 
 def main():
@@ -786,17 +867,30 @@ def main():
     # largest share of the step is the dominant one
     # (the first step's one-time costs, such as loading GEMM kernels, are not
     # counted)
+    # warmup steps 1, 3, ... bracket each op's main kernel (oc_profile_next),
+    # steps 2, 4, ... every kernel of each op (oc_profile_calls)
     step.events, step.traced = {}, {"*"}
-    nwarm = max(args.warmup, 2)
+    nwarm = max(args.warmup, 3)
+    allk = {}
+    n_main = n_all = 0
     for i in range(nwarm):
         if i == 1:
             torch.cuda.synchronize()
             step.events = {}
-        step()
+        if i >= 1 and i % 2 == 0:
+            saved_events, step.events, step.calls = step.events, None, []
+            step()
+            torch.cuda.synchronize()
+            step.collect_calls(allk)
+            step.events, step.calls = saved_events, None
+            n_all += 1
+        else:
+            step()
+            n_main += i >= 1
     step.drain()
     torch.cuda.synchronize()
     warm = step.collect()
-    nwarm -= 1
+    nwarm = n_main
     # the build (part at the head of the step, part on its own stream) is not a
     # convolution or pooling class
     dominant = max((k for k in warm if not warm[k]["op"].startswith("build")),
@@ -859,6 +953,34 @@ def main():
     if conv:
         ops_out["conv_fwd_bwd"] = op_rate("conv", sum(w for _, w in conv),
                                           sum(t for t, _ in conv), bf16)
+    # every kernel of the conv passes (split sums, ReLU masks, operand
+    # conversions and gathers included), per layer and in total
+    layers, tot_us, tot_work = [], 0.0, 0.0
+    for li, L in enumerate(wl.layers):
+        if L.op not in ("conv", "deconv"):
+            continue
+        tags = (("conv_fwd", "conv_bwd_data", "conv_bwd_weight") if L.op == "conv" else
+                ("deconv_fwd", "deconv_bwd_data", "deconv_bwd_weight"))
+        us, work = {}, 0.0
+        for tag in tags:
+            a = allk.get((li, tag))
+            if a and a[1]:
+                us[tag.split("_", 1)[1]] = round(a[0] * 1e3 / a[1], 2)
+                work += step.work(tag, L)
+        t = sum(us.values())
+        if t <= 0:
+            continue
+        r = op_rate("conv", work, t, L.dtype == "bf16")
+        layers.append({"layer": li, "op": L.op, "depth": L.depth, "ksize": L.ksize,
+                       "stride": L.stride, "cin": L.cin, "cout": L.cout, "dtype": L.dtype,
+                       "rows": step._n_conv(L), "us": us, "us_total": round(t, 2),
+                       "gflops": round(work / (t * 1e-6) / 1e9, 1),
+                       "octants_per_s": round(step._n_out(L) / (t * 1e-6), 1),
+                       "frac": r["frac"]})
+        tot_us += t
+        tot_work += work
+    if tot_us > 0:
+        ops_out["conv_fwd_bwd_all"] = op_rate("conv", tot_work, tot_us, bf16)
 
     if args.layers:
         for key, v in sorted(warm.items(), key=lambda kv: -kv[1]["ms"]):
@@ -880,7 +1002,7 @@ def main():
 
     cpu = None
     if args.cpu_shapes > 0:
-        print(f"[bench] cpu oracle on {args.cpu_shapes} shapes", file=sys.stderr, flush=True)
+        print(f"[bench] cpu oracle, up to {args.cpu_shapes} shapes", file=sys.stderr, flush=True)
         cpu = cpu_baseline(synth, wl, min(args.cpu_shapes, wl.batch))
 
     line = {
@@ -909,8 +1031,11 @@ def main():
         "octants_per_s": round(octants / (ms * 1e-3), 1),
         "roofline": roofline,
         "ops": ops_out,
-        "ops_scope": "warmup HIP events around the main kernel of each op (conv split sums and "
-                     "ReLU masks not included; the build is measured from a kernel trace)",
+        "ops_scope": "warmup HIP events: per op class around its main kernel; conv_fwd_bwd_all "
+                     "and layers around every kernel of the conv passes (split sums, ReLU "
+                     "masks, conversions and gathers included); the build is measured from a "
+                     "kernel trace",
+        "layers": layers,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -377,6 +377,18 @@ oc_status oc_gpool_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int3
  * pending pair.  The caller owns the events. */
 oc_status oc_profile_next(hipEvent_t start, hipEvent_t stop);
 
+/* Profiling: while armed, every kernel the library launches from the calling
+ * thread is bracketed by the next pair starts[i], stops[i] (recorded at the
+ * start and the end of that kernel on its stream, as hipExtLaunchKernelGGL
+ * does), i = the value of *used before the launch, which is then incremented;
+ * launches past cap are not bracketed.  A kernel that oc_profile_next
+ * brackets takes that pair instead.  The sum of the pairs' durations is the
+ * kernel time of the calls made while armed, without host-side gaps.
+ * Arming sets *used = 0.  All four NULL/0 disarms.  The arrays and *used are
+ * the caller's and must stay valid while armed.  Host-side only: no device
+ * work is enqueued by this call. */
+oc_status oc_profile_calls(hipEvent_t* starts, hipEvent_t* stops, int32_t cap, int32_t* used);
+
 const char* oc_status_str(oc_status s);
 const char* oc_last_error(void); /* thread-local message of the last failure */
 

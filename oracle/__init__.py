@@ -25,7 +25,7 @@ def build(force: bool = False) -> str:
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp"
         subprocess.check_call(
-            ["g++", "-O2", "-std=c++17", "-fopenmp", "-shared", "-fPIC", _SRC, "-o", tmp]
+            ["g++", "-O3", "-std=c++17", "-fopenmp", "-shared", "-fPIC", _SRC, "-o", tmp]
         )
         os.replace(tmp, _LIB)
     return _LIB
@@ -64,6 +64,8 @@ def lib():
             f.restype = C.c_int
         L.ocref_num_threads.argtypes = []
         L.ocref_num_threads.restype = C.c_int
+        L.ocref_set_num_threads.argtypes = [C.c_int32]
+        L.ocref_set_num_threads.restype = C.c_int
         L.ocref_free.argtypes = [p]
         L.ocref_free.restype = None
         _lib = L
@@ -73,6 +75,11 @@ def lib():
 def num_threads() -> int:
     """OpenMP threads the oracle's parallel loops use."""
     return int(lib().ocref_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on (timing only)."""
+    _check(lib().ocref_set_num_threads(int(n)))
 
 
 def _ptr(a):

@@ -308,26 +308,33 @@ int ocref_conv_fwd(const int32_t* nb, int64_t n_out, int32_t K3, const double* x
 }
 
 // Convolution backward w.r.t. the input: dcol[i] = dY[i] . W^T, then col2im,
-// a serial scatter-add of dcol[i][k] into row nb[i][k].  want (nullable,
+// a serial scatter-add of dcol[i][k] into row nb[i][k] in (i, k) order.
+// Threads split the input channels (a channel's entries see the same
+// additions in the same order at any thread count).  want (nullable,
 // [n_in]): only accumulate into rows with want[j] != 0 (others stay 0).
 int ocref_conv_bwd_data(const int32_t* nb, int64_t n_out, int32_t K3, const double* dy,
                         int32_t cout, const double* w, int32_t cin, int64_t n_in,
                         const uint8_t* want, double* dx) {
   if (!nb || !dy || !w || !dx || K3 < 1 || cin < 1 || cout < 1) return ERR_ARG;
   std::fill(dx, dx + n_in * cin, 0.0);
-  std::vector<double> dcol(cin);
-  for (int64_t i = 0; i < n_out; ++i)
-    for (int k = 0; k < K3; ++k) {
-      int32_t j = nb[i * K3 + k];
-      if (j < 0 || j >= n_in || (want && !want[j])) continue;
-      for (int ci = 0; ci < cin; ++ci) {
-        double acc = 0.0;
-        const double* wk = w + ((int64_t)k * cin + ci) * cout;
-        for (int co = 0; co < cout; ++co) acc += wk[co] * dy[i * cout + co];
-        dcol[ci] = acc;
+#pragma omp parallel
+  {
+    const int64_t nt = omp_get_num_threads(), t = omp_get_thread_num();
+    const int c0 = (int)(cin * t / nt), c1 = (int)(cin * (t + 1) / nt);
+    std::vector<double> dcol(cin);
+    for (int64_t i = 0; c0 < c1 && i < n_out; ++i)
+      for (int k = 0; k < K3; ++k) {
+        int32_t j = nb[i * K3 + k];
+        if (j < 0 || j >= n_in || (want && !want[j])) continue;
+        for (int ci = c0; ci < c1; ++ci) {
+          double acc = 0.0;
+          const double* wk = w + ((int64_t)k * cin + ci) * cout;
+          for (int co = 0; co < cout; ++co) acc += wk[co] * dy[i * cout + co];
+          dcol[ci] = acc;
+        }
+        for (int ci = c0; ci < c1; ++ci) dx[j * cin + ci] += dcol[ci];
       }
-      for (int ci = 0; ci < cin; ++ci) dx[j * cin + ci] += dcol[ci];
-    }
+  }
   return OK;
 }
 
@@ -465,6 +472,13 @@ int ocref_unpool_bwd(const int32_t* labels, int64_t n_lm1, const double* dy, con
 
 // Threads the OpenMP loops above use (reported beside CPU timings).
 int ocref_num_threads(void) { return omp_get_max_threads(); }
+
+// Threads of the parallel loops that follow (n >= 1); timing only.
+int ocref_set_num_threads(int32_t n) {
+  if (n < 1) return 1;
+  omp_set_num_threads(n);
+  return 0;
+}
 
 // ReLU (Sec. 4): y = max(0, x); backward dx = dy * [x > 0].
 int ocref_relu_fwd(const double* x, int64_t n, double* y) {

@@ -28,6 +28,7 @@ __all__ = [
     "oc_conv_fwd",
     "oc_conv_kernel",
     "oc_profile_next",
+    "CallProfile",
     "oc_conv_bwd",
     "oc_deconv_fwd",
     "oc_deconv_bwd",
@@ -57,7 +58,7 @@ EXPORTS = (
     "oc_conv_fwd", "oc_conv_kernel", "oc_conv_fwd_workspace", "oc_conv_bwd_workspace", "oc_conv_bwd", "oc_pool_fwd", "oc_pool_bwd",
     "oc_unpool_fwd", "oc_unpool_bwd", "oc_status_str", "oc_last_error", "oc_profile_next",
     "oc_deconv_fwd", "oc_deconv_fwd_workspace", "oc_deconv_bwd", "oc_deconv_bwd_workspace",
-    "oc_gpool_fwd", "oc_gpool_bwd",
+    "oc_gpool_fwd", "oc_gpool_bwd", "oc_profile_calls",
 )
 
 
@@ -164,6 +165,7 @@ def load():
         "oc_status_str": ([C.c_int], C.c_char_p),
         "oc_last_error": ([], C.c_char_p),
         "oc_profile_next": ([p, p], C.c_int),
+        "oc_profile_calls": ([p, p, i32, p], C.c_int),
     }
     for name, (args, res) in sigs.items():
         f = getattr(L, name)
@@ -363,6 +365,35 @@ def oc_profile_next(start, stop) -> None:
     least once, so that they exist)."""
     _check(load().oc_profile_next(C.c_void_p(start.cuda_event) if start is not None else None,
                                   C.c_void_p(stop.cuda_event) if stop is not None else None))
+
+
+class CallProfile:
+    """Brackets every kernel the library launches from this thread between
+    arm() and disarm() with a pair of torch.cuda events (oc_profile_calls);
+    kernel_ms() is the sum of their durations once the work is done."""
+
+    def __init__(self, cap: int = 64):
+        self.cap = cap
+        self.start = [torch.cuda.Event(enable_timing=True) for _ in range(cap)]
+        self.stop = [torch.cuda.Event(enable_timing=True) for _ in range(cap)]
+        for e in self.start + self.stop:
+            e.record()  # instantiates the events
+        self._a = (C.c_void_p * cap)(*[e.cuda_event for e in self.start])
+        self._b = (C.c_void_p * cap)(*[e.cuda_event for e in self.stop])
+        self._used = C.c_int32(0)
+
+    def arm(self) -> None:
+        _check(load().oc_profile_calls(self._a, self._b, self.cap, C.byref(self._used)))
+
+    def disarm(self) -> None:
+        _check(load().oc_profile_calls(None, None, 0, None))
+
+    @property
+    def used(self) -> int:
+        return min(int(self._used.value), self.cap)
+
+    def kernel_ms(self) -> float:
+        return sum(self.start[i].elapsed_time(self.stop[i]) for i in range(self.used))
 
 
 def oc_conv_kernel(tree: Octree, depth: int, ksize: int, stride: int, cin: int, cout: int,

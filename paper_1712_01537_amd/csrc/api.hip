@@ -8,6 +8,11 @@
 namespace {
 thread_local char g_msg[512] = "";
 thread_local hipEvent_t g_prof_start = nullptr, g_prof_stop = nullptr;
+// oc_profile_calls: armed event arrays, their capacity and the count used
+thread_local hipEvent_t* g_call_start = nullptr;
+thread_local hipEvent_t* g_call_stop = nullptr;
+thread_local int32_t g_call_cap = 0;
+thread_local int32_t* g_call_used = nullptr;
 }
 
 namespace oc {
@@ -64,6 +69,14 @@ void take_profile_events(hipEvent_t* start, hipEvent_t* stop) {
   g_prof_start = g_prof_stop = nullptr;
 }
 
+void take_call_events(hipEvent_t* start, hipEvent_t* stop) {
+  *start = *stop = nullptr;
+  if (!g_call_used || *g_call_used >= g_call_cap) return;
+  const int32_t i = (*g_call_used)++;
+  *start = g_call_start[i];
+  *stop = g_call_stop[i];
+}
+
 oc_status check_tree_level(const oc_octree* t, int32_t l, int32_t min_l) {
   if (!t) return fail(OC_ERR_ARG, "octree is NULL");
   if (l < min_l || l > t->depth)
@@ -103,6 +116,23 @@ void oc_octree_free(oc_octree* t) {
   if (!t) return;
   oc::dev_free(t->alloc, t->block, t->stream);
   delete t;
+}
+
+oc_status oc_profile_calls(hipEvent_t* starts, hipEvent_t* stops, int32_t cap, int32_t* used) {
+  if (!starts && !stops && !used) {
+    g_call_start = g_call_stop = nullptr;
+    g_call_used = nullptr;
+    g_call_cap = 0;
+    return OC_OK;
+  }
+  if (!starts || !stops || !used || cap < 0)
+    return oc::fail(OC_ERR_ARG, "oc_profile_calls: give both arrays and the count, or none");
+  g_call_start = starts;
+  g_call_stop = stops;
+  g_call_cap = cap;
+  g_call_used = used;
+  *used = 0;
+  return OC_OK;
 }
 
 const char* oc_status_str(oc_status s) {

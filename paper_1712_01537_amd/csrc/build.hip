@@ -660,7 +660,7 @@ namespace oc {
 
 void fill_u32(void* p, uint32_t v, int64_t n, hipStream_t s) {
   if (n <= 0) return;
-  hipLaunchKernelGGL(k_fill_u32, dim3(blocks_for(n)), dim3(TB), 0, s, (uint32_t*)p, v, n);
+  oc::launch(k_fill_u32, dim3(blocks_for(n)), dim3(TB), 0, s, (uint32_t*)p, v, n);
 }
 
 }  // namespace oc
@@ -799,16 +799,16 @@ extern "C" oc_status oc_build_async(const float* points, const float* normals,
   const int nq = (int)oc::cdiv(P, TB);
   j->nq = nq;
   if (P > 0)
-    hipLaunchKernelGGL(k_quant, dim3(nq), dim3(TB), 0, stream, points, normals, S, B, (int)P, d,
+    oc::launch(k_quant, dim3(nq), dim3(TB), 0, stream, points, normals, S, B, (int)P, d,
                        s.leafcell, s.bstat);
   const MarkCfg mc = mark_cfg(L.cells[d]);
-  hipLaunchKernelGGL(k_mark, dim3((unsigned)oc::cdiv(L.cells[d], 32ll * mc.words)), dim3(MK_TB),
+  oc::launch(k_mark, dim3((unsigned)oc::cdiv(L.cells[d], 32ll * mc.words)), dim3(MK_TB),
                      mc.lds, stream, (const uint32_t*)s.leafcell, S, L, mc.words, mc.up, s.bits);
   for (int l = d - mc.up - 1; l >= fd; --l)
-    hipLaunchKernelGGL(k_reduce, dim3(blocks_for(L.wbase[l + 1] - L.wbase[l])), dim3(TB), 0,
+    oc::launch(k_reduce, dim3(blocks_for(L.wbase[l + 1] - L.wbase[l])), dim3(TB), 0,
                        stream, L, l, s.bits);
-  hipLaunchKernelGGL(k_scan_a, dim3(nb), dim3(TB), 0, stream, (const uint32_t*)s.bits, nw, s.bsum);
-  hipLaunchKernelGGL(k_scan_c, dim3(nb), dim3(TB), 0, stream, L, (const uint32_t*)s.bits, nw,
+  oc::launch(k_scan_a, dim3(nb), dim3(TB), 0, stream, (const uint32_t*)s.bits, nw, s.bsum);
+  oc::launch(k_scan_c, dim3(nb), dim3(TB), 0, stream, L, (const uint32_t*)s.bits, nw,
                      (const int32_t*)s.bsum, s.pre, s.ucell, (const uint2*)s.bstat, nq, s.info);
   hipError_t he = hipGetLastError();
   if (he == hipSuccess)
@@ -902,7 +902,7 @@ extern "C" oc_status oc_build_finish(oc_build_job* j, hipStream_t stream, oc_oct
       kmax = std::max<int64_t>(
           kmax, oc::cdiv(std::min<int64_t>(j->offs[b + 1] - j->offs[b], L.cells[d] / B),
                          LM_LEAVES));
-    hipLaunchKernelGGL(k_leaf_mean, dim3((unsigned)B, (unsigned)kmax), dim3(LM_TB), 0, stream,
+    oc::launch(k_leaf_mean, dim3((unsigned)B, (unsigned)kmax), dim3(LM_TB), 0, stream,
                        j->normals, (const uint32_t*)s.leafcell, j->S, (int)j->P, L,
                        (const uint32_t*)s.bits, (const int32_t*)s.pre, (const uint32_t*)s.ucell,
                        (const uint32_t*)s.info, s.leafmean);
@@ -923,7 +923,7 @@ extern "C" oc_status oc_build_finish(oc_build_job* j, hipStream_t stream, oc_oct
     E.nbr[l] = t->nbr[l];
   }
   E.signal = t->signal;
-  hipLaunchKernelGGL(k_emit, dim3(blocks_for(16 * E.ibase[d + 1])), dim3(TB), 0, stream, L, E,
+  oc::launch(k_emit, dim3(blocks_for(16 * E.ibase[d + 1])), dim3(TB), 0, stream, L, E,
                      (const uint32_t*)s.bits, (const int32_t*)s.pre, (const uint32_t*)s.ucell,
                      (const float*)s.leafmean);
   he = hipGetLastError();

@@ -58,12 +58,27 @@ void fill_u32(void* p, uint32_t v, int64_t n, hipStream_t s);
 // cleared (both null when none are pending).
 void take_profile_events(hipEvent_t* start, hipEvent_t* stop);
 
+// The next pair of the event arrays armed by oc_profile_calls for the calling
+// thread (both null when none is armed or the arrays are used up).
+void take_call_events(hipEvent_t* start, hipEvent_t* stop);
+
+// Launch a kernel of the library; while oc_profile_calls is armed on the
+// calling thread it is bracketed by the next pair of the armed events.
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s,
+                   Args... args) {
+  hipEvent_t a, b;
+  take_call_events(&a, &b);
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, a, b, 0, args...);
+}
+
 // Launch the kernel that does a convolution pass's arithmetic; it takes the
-// pending profiling events of the thread, if any.
+// pending events of oc_profile_next if any, else a pair of oc_profile_calls.
 template <typename F, typename... Args>
 inline void launch_main(F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
   hipEvent_t a, b;
   take_profile_events(&a, &b);
+  if (!a) take_call_events(&a, &b);
   hipExtLaunchKernelGGL(kernel, grid, block, 0, s, a, b, 0, args...);
 }
 

@@ -48,7 +48,7 @@ __global__ __launch_bounds__(TB) void k_bf16_to_f32(const uint16_t* __restrict__
 void bf16_to_f32(const void* in, int64_t n, float* out, hipStream_t s) {
   if (n <= 0) return;
   const int vec = (uintptr_t)in % 16 == 0 && (uintptr_t)out % 32 == 0;
-  hipLaunchKernelGGL(k_bf16_to_f32, dim3((unsigned)oc::cdiv(n, 8 * TB)), dim3(TB), 0, s,
+  oc::launch(k_bf16_to_f32, dim3((unsigned)oc::cdiv(n, 8 * TB)), dim3(TB), 0, s,
                      (const uint16_t*)in, n, vec, out);
 }
 
@@ -295,7 +295,7 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
       const int64_t n = sh.n_out * (int64_t)cout;
       const int vec = ((!ym || (uintptr_t)ym % 16 == 0) && (uintptr_t)dy % 16 == 0 &&
                        (uintptr_t)wsf % 16 == 0);
-      hipLaunchKernelGGL(k_relu_mask, dim3((unsigned)oc::cdiv(n, 4 * TB)), dim3(TB), 0, s, ym, dy,
+      oc::launch(k_relu_mask, dim3((unsigned)oc::cdiv(n, 4 * TB)), dim3(TB), 0, s, ym, dy,
                          n, vec, rnd, wsf);
       dy = wsf;
     }

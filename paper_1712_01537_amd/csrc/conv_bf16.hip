@@ -617,7 +617,7 @@ int dw_ranges(const oc_octree* t, int l, int K, int cin, int cout) {
 
 void wprep(const uint16_t* w, int K, int kk, int nn, int flip, uint16_t* wp, hipStream_t s) {
   const int K3 = K * K * K;
-  hipLaunchKernelGGL(k_bf_wprep, dim3(blocks((int64_t)kk * K3 * nn, TB)), dim3(TB), 0, s, w, K3,
+  oc::launch(k_bf_wprep, dim3(blocks((int64_t)kk * K3 * nn, TB)), dim3(TB), 0, s, w, K3,
                      kk, nn, flip, wp);
 }
 
@@ -631,7 +631,7 @@ void launch_chunk(const oc_octree* t, int l, const uint16_t* x, int kk, const ui
     oc::launch_main(kern, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, kk, wp, nn, chunk,
                     out, acc_in, relu);
   else
-    hipLaunchKernelGGL(kern, grid, dim3(512), 0, s, (const int32_t*)t->nbr[l], G, x, kk, wp, nn,
+    oc::launch(kern, grid, dim3(512), 0, s, (const int32_t*)t->nbr[l], G, x, kk, wp, nn,
                        chunk, out, acc_in, relu);
 }
 
@@ -702,7 +702,7 @@ void conv_bf16_bwd(const oc_octree* t, int l, int K, const uint16_t* x, int cin,
   float* part = (float*)p;
   const int64_t n = N * cout;
   const int vec = (uintptr_t)dy % 16 == 0 && (!ym || (uintptr_t)ym % 16 == 0);
-  hipLaunchKernelGGL(k_bf_cvt, dim3(blocks(n, 4 * TB)), dim3(TB), 0, s, dy, ym, n, vec, dy16);
+  oc::launch(k_bf_cvt, dim3(blocks(n, 4 * TB)), dim3(TB), 0, s, dy, ym, n, vec, dy16);
   if (dx) {
     wprep(w, K, cout, cin, 1, wpf, s);
     launch_conv<true>(t, l, K, dy16, cout, wpf, cin, dx, 0, s);
@@ -718,7 +718,7 @@ void conv_bf16_bwd(const oc_octree* t, int l, int K, const uint16_t* x, int cin,
       launch_main(k_conv_bf_dw<3, 5>, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, cin,
                   dy16, cout, nr, part);
     const int64_t E = (int64_t)K3 * cin * cout;
-    hipLaunchKernelGGL(k_bf_sum, dim3(blocks(E, 4 * TB)), dim3(TB), 0, s, part, nr, E, dw);
+    oc::launch(k_bf_sum, dim3(blocks(E, 4 * TB)), dim3(TB), 0, s, part, nr, E, dw);
   }
 }
 

@@ -769,7 +769,7 @@ __global__ __launch_bounds__(TB) void k_sum_split(const float* __restrict__ part
 // Launch of k_sum_split over n entries.
 void sum_split(const float* part, int splits, int64_t n, float* out, int relu, hipStream_t s) {
   const int vec = n % 4 == 0 && (uintptr_t)part % 16 == 0 && (uintptr_t)out % 16 == 0;
-  hipLaunchKernelGGL(k_sum_split, dim3((unsigned)oc::cdiv(n, 4 * TB)), dim3(TB), 0, s, part, splits,
+  oc::launch(k_sum_split, dim3((unsigned)oc::cdiv(n, 4 * TB)), dim3(TB), 0, s, part, splits,
                      n, out, relu, vec);
 }
 
@@ -1294,13 +1294,13 @@ void sum_parts(const float* part, int np, int64_t n, float* out, hipStream_t s) 
   const bool wide = oc::cdiv(nv, TB / 16) >= 2 * (int64_t)oc::cu_count();
   const unsigned grid = (unsigned)oc::cdiv(nv, TB / (wide ? 16 : 64));
   if (v4 && wide)
-    hipLaunchKernelGGL((k_sum_parts<16, 4>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
+    oc::launch((k_sum_parts<16, 4>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
   else if (v4)
-    hipLaunchKernelGGL((k_sum_parts<64, 4>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
+    oc::launch((k_sum_parts<64, 4>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
   else if (wide)
-    hipLaunchKernelGGL((k_sum_parts<16, 1>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
+    oc::launch((k_sum_parts<16, 1>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
   else
-    hipLaunchKernelGGL((k_sum_parts<64, 1>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
+    oc::launch((k_sum_parts<64, 1>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
 }
 
 // ---------------------------------------------------------------------------

@@ -624,7 +624,7 @@ template <int WN, int RB>
 void launch_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const void* w, int cout,
                    float* y, int relu, void* ws, hipStream_t s) {
   const int64_t nw = (int64_t)27 * cin * cout;
-  hipLaunchKernelGGL(k_s2_wt<float>, dim3((unsigned)oc::cdiv(nw, TB)), dim3(TB), 0, s,
+  oc::launch(k_s2_wt<float>, dim3((unsigned)oc::cdiv(nw, TB)), dim3(TB), 0, s,
                      (const float*)w, cin, cout, (float*)ws);
   w = ws;
   const int64_t G = t->M[l - 1];
@@ -632,7 +632,7 @@ void launch_s2_fwd(const oc_octree* t, int l, const void* x, int cin, const void
   const int ntiles = (int)oc::cdiv(G, GT), gy = cout / (16 * WN);
   const int64_t nwg = (int64_t)ntiles * gy;
   const dim3 grid((unsigned)(nwg >= 8 ? oc::cdiv(nwg, 8) * 8 : nwg));
-  hipLaunchKernelGGL((k_s2_fwd<WN, RB>), grid, dim3(TB), 0, s, (const int32_t*)t->nbr[l], G,
+  oc::launch((k_s2_fwd<WN, RB>), grid, dim3(TB), 0, s, (const int32_t*)t->nbr[l], G,
                      x, cin, w, cout, (const int32_t*)t->rows[l - 1],
                      (const int32_t*)t->labels[l - 1], t->N[l - 1], y, relu,
                      (int)(t->N[l] * cin * 4), (int)(nw * 4), ntiles, gy);
@@ -678,18 +678,18 @@ void launch_col_r(hipStream_t s, const int32_t* nbr, const int32_t* lab, int64_t
   if (rb % 16 == 0) {
     const int64_t nt = ng * 27 * (rb / 16);
     if (bf16)
-      hipLaunchKernelGGL((k_s2_col<uint16_t, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab,
+      oc::launch((k_s2_col<uint16_t, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab,
                          g0, ng, (const uint16_t*)x, rb, (uint16_t*)col);
     else
-      hipLaunchKernelGGL((k_s2_col<float, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab, g0,
+      oc::launch((k_s2_col<float, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab, g0,
                          ng, (const float*)x, rb, (float*)col);
   } else {
     const int64_t nt = ng * 27 * cin;
     if (bf16)
-      hipLaunchKernelGGL((k_s2_col1<uint16_t, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab,
+      oc::launch((k_s2_col1<uint16_t, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab,
                          g0, ng, (const uint16_t*)x, cin, (uint16_t*)col);
     else
-      hipLaunchKernelGGL((k_s2_col1<float, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab,
+      oc::launch((k_s2_col1<float, RR>), dim3(grid_for(nt)), dim3(TB), 0, s, nbr, lab,
                          g0, ng, (const float*)x, cin, (float*)col);
   }
 }
@@ -742,10 +742,10 @@ oc_status conv_s2_fwd(const oc_octree* t, int l, int r, const void* x, int cin, 
     if (st != OC_OK) return st;
   }
   if (cout % 4 == 0 && (uintptr_t)y % 16 == 0)
-    hipLaunchKernelGGL(k_s2_rows_out, dim3(grid_for(h.n_out * (cout / 4))), dim3(TB), 0, s,
+    oc::launch(k_s2_rows_out, dim3(grid_for(h.n_out * (cout / 4))), dim3(TB), 0, s,
                        (const int32_t*)t->labels[l - r], h.n_out, (const float*)yg, cout, relu, y);
   else
-    hipLaunchKernelGGL(k_s2_rows_out1, dim3(grid_for(h.n_out * cout)), dim3(TB), 0, s,
+    oc::launch(k_s2_rows_out1, dim3(grid_for(h.n_out * cout)), dim3(TB), 0, s,
                        (const int32_t*)t->labels[l - r], h.n_out, (const float*)yg, cout, relu, y);
   return OC_OK;
 }
@@ -770,30 +770,30 @@ oc_status conv_s2_bwd(const oc_octree* t, int l, int r, const void* x, int cin, 
   const bool vec = cout % 4 == 0 && (uintptr_t)dy % 16 == 0 && (uintptr_t)ym % 16 == 0;
   const int32_t* prow = (const int32_t*)t->rows[l - r];
   if (vec && bf16)
-    hipLaunchKernelGGL(k_s2_dy_rows<uint16_t>, dim3(grid_for(h.G * (cout / 4))), dim3(TB), 0, s,
+    oc::launch(k_s2_dy_rows<uint16_t>, dim3(grid_for(h.G * (cout / 4))), dim3(TB), 0, s,
                        prow, h.G, dy, ym, cout, (uint16_t*)dyg);
   else if (vec)
-    hipLaunchKernelGGL(k_s2_dy_rows<float>, dim3(grid_for(h.G * (cout / 4))), dim3(TB), 0, s,
+    oc::launch(k_s2_dy_rows<float>, dim3(grid_for(h.G * (cout / 4))), dim3(TB), 0, s,
                        prow, h.G, dy, ym, cout, (float*)dyg);
   else if (bf16)
-    hipLaunchKernelGGL(k_s2_dy_rows1<uint16_t>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow,
+    oc::launch(k_s2_dy_rows1<uint16_t>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow,
                        h.G, dy, ym, cout, (uint16_t*)dyg);
   else
-    hipLaunchKernelGGL(k_s2_dy_rows1<float>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow,
+    oc::launch(k_s2_dy_rows1<float>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow,
                        h.G, dy, ym, cout, (float*)dyg);
   if (dx && r == 2) {
     const int64_t nt = h.n_in * (int64_t)cin;
     if (bf16)
-      hipLaunchKernelGGL(k_s4_dx<uint16_t>, dim3(grid_for(nt)), dim3(TB), 0, s,
+      oc::launch(k_s4_dx<uint16_t>, dim3(grid_for(nt)), dim3(TB), 0, s,
                          (const int32_t*)t->rows[l - 1], (const int32_t*)t->nbr[l - 1], h.n_in,
                          (const uint16_t*)dyg, (const uint16_t*)w, cin, cout, dx);
     else if (cin % 4 == 0 && cout % 4 == 0 && (uintptr_t)w % 16 == 0 && (uintptr_t)dx % 16 == 0 &&
              (uintptr_t)dyg % 16 == 0)
-      hipLaunchKernelGGL(k_s4_dx4, dim3(grid_for(nt / 4)), dim3(TB), 0, s,
+      oc::launch(k_s4_dx4, dim3(grid_for(nt / 4)), dim3(TB), 0, s,
                          (const int32_t*)t->rows[l - 1], (const int32_t*)t->nbr[l - 1], h.n_in,
                          (const float*)dyg, (const float*)w, cin, cout, dx);
     else
-      hipLaunchKernelGGL(k_s4_dx<float>, dim3(grid_for(nt)), dim3(TB), 0, s,
+      oc::launch(k_s4_dx<float>, dim3(grid_for(nt)), dim3(TB), 0, s,
                          (const int32_t*)t->rows[l - 1], (const int32_t*)t->nbr[l - 1], h.n_in,
                          (const float*)dyg, (const float*)w, cin, cout, dx);
   } else if (dx) {
@@ -803,22 +803,22 @@ oc_status conv_s2_bwd(const oc_octree* t, int l, int r, const void* x, int cin, 
     const int rb = (int)(cout * es);  // bytes of a dY_g row (16-byte aligned rows when rb % 16 == 0)
     const unsigned gd = rb % 16 == 0 ? grid_for(h.G * 8 * (int64_t)(rb / 16)) : grid_for(h.G * 8 * (int64_t)cout);
     if (bf16) {
-      hipLaunchKernelGGL(k_s2_wx<uint16_t>, dim3(grid_for(nw)), dim3(TB), 0, s,
+      oc::launch(k_s2_wx<uint16_t>, dim3(grid_for(nw)), dim3(TB), 0, s,
                          (const uint16_t*)w, cin, cout, (uint16_t*)wx);
       if (rb % 16 == 0)
-        hipLaunchKernelGGL(k_s2_dgather<uint16_t>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
+        oc::launch(k_s2_dgather<uint16_t>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
                            (const uint16_t*)dyg, rb, (uint16_t*)D);
       else
-        hipLaunchKernelGGL(k_s2_dgather1<uint16_t>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
+        oc::launch(k_s2_dgather1<uint16_t>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
                            (const uint16_t*)dyg, cout, (uint16_t*)D);
     } else {
-      hipLaunchKernelGGL(k_s2_wx<float>, dim3(grid_for(nw)), dim3(TB), 0, s, (const float*)w, cin,
+      oc::launch(k_s2_wx<float>, dim3(grid_for(nw)), dim3(TB), 0, s, (const float*)w, cin,
                          cout, (float*)wx);
       if (rb % 16 == 0)
-        hipLaunchKernelGGL(k_s2_dgather<float>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
+        oc::launch(k_s2_dgather<float>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
                            (const float*)dyg, rb, (float*)D);
       else
-        hipLaunchKernelGGL(k_s2_dgather1<float>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
+        oc::launch(k_s2_dgather1<float>, dim3(gd), dim3(TB), 0, s, nbr, h.G,
                            (const float*)dyg, cout, (float*)D);
     }
     // dX-view^T [8 cin][G] = Wx-view^T [8 cin][8 cout] x D-view^T [8 cout][G] (column-major)
@@ -848,7 +848,7 @@ oc_status conv_s2_bwd(const oc_octree* t, int l, int r, const void* x, int cin, 
         if (st != OC_OK) return st;
       }
     }
-    hipLaunchKernelGGL(k_s2_sum, dim3(grid_for(E)), dim3(TB), 0, s, (const float*)pw, DW_BATCH, E,
+    oc::launch(k_s2_sum, dim3(grid_for(E)), dim3(TB), 0, s, (const float*)pw, DW_BATCH, E,
                        dw);
   }
   return OC_OK;

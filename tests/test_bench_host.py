@@ -116,13 +116,15 @@ def test_accounting_of_deconvolution_gpool_and_stride4():
     ), signal_input=False)
     acc = bench.Accounting(wl, N, M, 2000)
     c0, s4, dc, ga, gm = wl.layers
-    # stride 4 from depth 4 evaluates at the depth-2 rows; the stride-2
-    # deconvolution to depth 4 runs the stride-2 convolution at depth 4 (rows of depth 3)
-    assert acc.work("conv_fwd", s4) == 2 * N[2] * 27 * 16 * 32
-    assert acc.work("deconv_fwd", dc) == 2 * N[3] * 27 * 32 * 8
+    # stride 4 from depth 4 is evaluated at the M[2] non-empty depth-2 octants
+    # only; the stride-2 deconvolution to depth 4 runs the stride-2
+    # convolution at depth 4 (evaluated at the M[3] non-empty depth-3 octants)
+    assert acc.work("conv_fwd", s4) == 2 * M[2] * 27 * 16 * 32
+    assert acc.work("deconv_fwd", dc) == 2 * M[3] * 27 * 32 * 8
     assert acc.work("deconv_bwd_weight", dc) == acc.work("deconv_fwd", dc)
     flops, octs = acc.conv_flops()
-    assert flops == (4 * N[4] * 27 * 3 * 16 + 6 * N[2] * 27 * 16 * 32 + 6 * N[3] * 27 * 32 * 8)
+    assert flops == (4 * N[4] * 27 * 3 * 16 + 6 * M[2] * 27 * 16 * 32 + 6 * M[3] * 27 * 32 * 8)
+    # output rows written: all depth-2 rows (stride 4), all depth-4 rows
     assert octs == N[4] + N[2] + N[4]
     # general pooling: rows in and out, switches for max, the groups' 27 entries
     assert acc.work("gpool_fwd", ga) == N[4] * 8 * 8 + M[3] * 108

@@ -167,3 +167,53 @@ def test_build_async_errors_and_cancel():
     assert e.value.code == 1
     ref, tree = _build_both(good.cpu().numpy(), good.cpu().numpy(), [0, 2], 4, 2)
     _compare_tree(ref, tree)
+
+
+def test_allocator_failure_reports_nomem_without_leaks():
+    """oc_build with an allocator that fails at its k-th request returns
+    OC_ERR_NOMEM, nothing is left allocated, and with enough successes the
+    build succeeds and oc_octree_free returns everything."""
+    import ctypes as C
+
+    import paper_1712_01537_amd as oc
+
+    L = oc.load()
+    pts, nrm, offs = synth.random_cloud(3, 2, 500, "union")
+    dp = torch.as_tensor(pts).cuda()
+    dn = torch.as_tensor(nrm).cuda()
+    offs_h = (C.c_int32 * len(offs))(*[int(v) for v in offs])
+    live = {}
+    state = {"calls": 0, "fail_at": 0}
+
+    def alloc(ctx, nbytes, stream):
+        state["calls"] += 1
+        if state["calls"] == state["fail_at"]:
+            return None
+        t = torch.empty(int(nbytes), dtype=torch.uint8, device="cuda")
+        live[t.data_ptr()] = t
+        return t.data_ptr()
+
+    def free(ctx, ptr, stream):
+        assert live.pop(int(ptr), None) is not None, "freed a pointer it was not given"
+
+    a_cb, f_cb = oc._ALLOC_FN(alloc), oc._FREE_FN(free)
+    A = oc._Allocator(a_cb, f_cb, None)
+    s = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    for fail_at in (1, 2):  # the scratch, then the octree's arrays
+        state.update(calls=0, fail_at=fail_at)
+        h = C.c_void_p()
+        rc = L.oc_build(C.c_void_p(dp.data_ptr()), C.c_void_p(dn.data_ptr()), offs_h,
+                        len(offs) - 1, 4, 2, C.byref(A), s, C.byref(h))
+        torch.cuda.synchronize()
+        print(f"[nomem] fail at request {fail_at}: status {rc}, "
+              f"{L.oc_last_error().decode()}", flush=True)
+        assert rc == 3 and not h.value, (fail_at, rc)
+        assert live == {}, f"{len(live)} buffers left after a failed build"
+    state.update(calls=0, fail_at=0)
+    h = C.c_void_p()
+    assert L.oc_build(C.c_void_p(dp.data_ptr()), C.c_void_p(dn.data_ptr()), offs_h,
+                      len(offs) - 1, 4, 2, C.byref(A), s, C.byref(h)) == 0
+    assert state["calls"] == 2 and len(live) == 1  # the scratch went back, the tree stays
+    L.oc_octree_free(h)
+    torch.cuda.synchronize()
+    assert live == {}

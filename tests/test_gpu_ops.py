@@ -1,9 +1,11 @@
 """GPU parity of convolution, pooling and unpooling against the CPU oracle.
 
-Small cases compare every output element; the full-size workloads compare
-sampled output rows, sampled input-gradient rows and sampled weight-gradient
-entries, each computed one by one by the oracle, in the launch configuration
-the bench uses."""
+Small cases compare every output element.  The full-size workloads, in the
+launch configuration the bench uses, compare every output row, input-gradient
+row and weight-gradient entry, except the 5x5x5 64->64 layer of wide_d7,
+whose every row and entry is checked through random channel projections
+(each implied by the elementwise rule) beside exact contiguous tiles and
+exact entries of every (tap, 16 x 16 channel) block of dW."""
 import numpy as np
 import pytest
 import torch
@@ -407,24 +409,75 @@ def test_new_ops_degenerate_trees():
 
 
 # ----------------------------------------------------------------------------
-# full-size workloads, sampled
+# full-size workloads: every output row, input-gradient row and weight-gradient
+# entry against the oracle; for the 5x5x5 64->64 layer of wide_d7 (about 1.2
+# TFLOP per pass, minutes for the float64 oracle) every row and entry through
+# random channel projections plus exact contiguous tiles, as below
 
 
-def _sample(rng, n, k):
-    return np.sort(rng.choice(n, size=min(k, n), replace=False))
+def _proj_tol(g, b, atol):
+    """Bound on |g.b - r.b| implied by the elementwise rule |g - r| <= atol +
+    RTOL |r| for every entry of the row (then |g - r| <= (atol + RTOL |g|) /
+    (1 - RTOL))."""
+    from helpers import RTOL
+    return (np.abs(g) * RTOL + atol) @ np.abs(b) / (1 - RTOL) + 1e-12
+
+
+def _assert_proj(g, b, ref_proj, what, atol=None):
+    """Every row of g projected on b (a random channel vector) against the
+    oracle's projection ref_proj [rows].  atol: the absolute term of the
+    elementwise rule (the fp32 rule's by default; the scaled weight-gradient
+    rule's 1e-5 max(1, rms) for dW)."""
+    from helpers import ATOL
+    g = np.asarray(g, np.float64)
+    got = g @ b
+    tol = _proj_tol(g, b, ATOL if atol is None else atol)
+    err = np.abs(got - ref_proj)
+    bad = err > tol
+    if bad.any():
+        i = int(np.argmax(err - tol))
+        raise AssertionError(f"{what}: {int(bad.sum())} of {len(err)} rows fail the projected "
+                             f"rule; worst row {i}: got {got[i]!r} ref {ref_proj[i]!r}")
+
+
+def _tiles(n_rows, every, tile=64):
+    """Rows of every `every`-th tile of `tile` rows (with the first and last
+    two tiles), as a bool mask and as a sorted index array."""
+    nt = -(-n_rows // tile)
+    pick = set(range(0, nt, every)) | {0, 1, max(nt - 2, 0), nt - 1}
+    want = np.zeros(n_rows, bool)
+    for t in pick:
+        want[t * tile:(t + 1) * tile] = True
+    return want, np.nonzero(want)[0]
+
+
+def _dw_block_entries(K3, cin, cout, rng, per=2):
+    """`per` random entries of every (tap, 16 input x 16 output channel)
+    block of dW, as flat indices into [K3][cin][cout]."""
+    out = []
+    for k in range(K3):
+        for c0 in range(0, cin, 16):
+            for n0 in range(0, cout, 16):
+                ci = rng.integers(c0, min(c0 + 16, cin), size=per)
+                co = rng.integers(n0, min(n0 + 16, cout), size=per)
+                out.append((k * cin + ci) * cout + co)
+    return np.unique(np.concatenate(out))
 
 
 def _check_conv_full(ref, tree, l, K, stride, x, w, relu, dy, tag, dtype=torch.float32):
     oc = _oc()
-    rng = np.random.default_rng(0)
     n_in = ref.num(l)
     nb = ref.neighbors(l, K, stride=stride)
     xq, wq = (x, w) if dtype == torch.float32 else (bf16_round(x), bf16_round(w))
-    print(f"[{tag}] conv d{l} K{K} s{stride} {x.shape[1]}->{w.shape[2]} rows {n_in}", flush=True)
+    K3, cin, cout = w.shape
+    big = K3 * cin * cout * nb.shape[0] > 6e10  # float64 oracle minutes per pass
+    print(f"[{tag}] conv d{l} K{K} s{stride} {cin}->{cout} rows {n_in} "
+          f"{'projected + tiles' if big else 'every element'}", flush=True)
     y = oc.oc_conv_fwd(tree, l, K, stride, _cuda(xq, dtype), _cuda(wq, dtype), relu=relu)
     yg = y.cpu().numpy()
     r = stride.bit_length() - 1  # stride 2^r
-    if relu or stride > 1:
+    rng = np.random.default_rng(7)
+    if not big:
         pre = oracle.conv_fwd(nb, xq, wq)
         if stride > 1:
             pre = oracle.renew(ref.labels(l - r), pre)
@@ -432,52 +485,61 @@ def _check_conv_full(ref, tree, l, K, stride, x, w, relu, dy, tag, dtype=torch.f
         assert_f32_close(yg, oracle.relu_fwd(pre) if relu else pre, f"{tag} y")
         dye = oracle.relu_bwd(pre, dy) if relu else dy
     else:
-        rows = _sample(rng, yg.shape[0], 3000)
-        assert_f32_close(yg[rows], oracle.conv_fwd(nb, xq, wq, rows=rows), f"{tag} y")
+        assert stride == 1 and not relu
+        want, rows = _tiles(n_in, 16)
+        assert_f32_close(yg[rows], oracle.conv_fwd(nb, xq, wq, rows=rows), f"{tag} y tiles")
+        b = rng.standard_normal(cout)
+        _assert_proj(yg, b, oracle.conv_fwd(nb, xq, wq @ b[:, None])[:, 0], f"{tag} y proj")
         dye = dy
     dx, dw = oc.oc_conv_bwd(tree, l, K, stride, _cuda(xq, dtype), _cuda(wq, dtype), _cuda(dy),
                             y=y, relu=relu)
-    want = np.zeros(n_in, bool)
-    want[_sample(rng, n_in, 3000)] = True
-    ent = _sample(rng, w.size, 300)
+    dxg, dwg = dx.cpu().numpy(), dw.cpu().numpy()
     if dtype == torch.bfloat16:  # the bf16 backward multiplies dy rounded to bf16
         dye = bf16_round(dye)
-    if stride == 1:
-        dxr = oracle.conv_bwd_data(nb, dye, wq, n_in, want=want)
-        dwr = oracle.conv_bwd_weight(nb, xq, dye, K ** 3, entries=ent)
+    dyh = dye if stride == 1 else oracle.renew_bwd(ref.labels(l - r), dye, nb.shape[0])
+    if not big:
+        assert_f32_close(dxg, oracle.conv_bwd_data(nb, dyh, wq, n_in), f"{tag} dx")
+        rule = assert_dw_close(dwg, oracle.conv_bwd_weight(nb, xq, dyh, K3), f"{tag} dw")
     else:
-        dyh = oracle.renew_bwd(ref.labels(l - r), dye, nb.shape[0])
-        dxr = oracle.conv_bwd_data(nb, dyh, wq, n_in, want=want)
-        dwr = oracle.conv_bwd_weight(nb, xq, dyh, K ** 3, entries=ent)
-    assert_f32_close(dx.cpu().numpy()[want], dxr[want], f"{tag} dx")
-    rule = assert_dw_close(dw.cpu().numpy().ravel()[ent], dwr, f"{tag} dw")
+        assert_f32_close(dxg[rows], oracle.conv_bwd_data(nb, dyh, wq, n_in, want=want)[rows],
+                         f"{tag} dx tiles")
+        bi = rng.standard_normal(cin)
+        wb = np.einsum("kio,i->ko", wq.astype(np.float64), bi)[:, None, :]  # [K3][1][cout]
+        _assert_proj(dxg, bi, oracle.conv_bwd_data(nb, dyh, wb, n_in)[:, 0], f"{tag} dx proj")
+        # every entry of dW through both channel projections, and exact entries
+        # in every (tap, 16 x 16 channel) block
+        bo = rng.standard_normal(cout)
+        datol = 1e-5 * max(1.0, float(np.sqrt(np.mean(dwg.astype(np.float64) ** 2))))
+        _assert_proj(dwg.reshape(-1, cout), bo,
+                     oracle.conv_bwd_weight(nb, xq, dyh @ bo[:, None], K3).reshape(-1),
+                     f"{tag} dw proj out", atol=datol)
+        _assert_proj(dwg.transpose(0, 2, 1).reshape(-1, cin), bi,
+                     oracle.conv_bwd_weight(nb, xq @ bi[:, None], dyh, K3).reshape(-1),
+                     f"{tag} dw proj in", atol=datol)
+        ent = _dw_block_entries(K3, cin, cout, rng)
+        rule = assert_dw_close(dwg.ravel()[ent],
+                               oracle.conv_bwd_weight(nb, xq, dyh, K3, entries=ent),
+                               f"{tag} dw blocks")
     print(f"[{tag}] dw rule: {rule}", flush=True)
     return y
 
 
 def _check_deconv_full(ref, tree, l, K, stride, x, w, dy, tag):
     oc = _oc()
-    rng = np.random.default_rng(1)
     n_out = ref.num(l)
     print(f"[{tag}] deconv d{l} K{K} s{stride} {x.shape[1]}->{w.shape[1]} rows {n_out}", flush=True)
     y = oc.oc_deconv_fwd(tree, l, K, stride, _cuda(x), _cuda(w))
-    want = np.zeros(n_out, bool)
-    want[_sample(rng, n_out, 3000)] = True
-    ent = _sample(rng, w.size, 300)
     dx, dw = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x), _cuda(w), _cuda(dy))
     if stride == 1:
         nb = ref.neighbors(l, K)
-        yr = oracle.deconv_fwd(nb, x, w, n_out, want=want)
-        rows = _sample(rng, x.shape[0], 3000)
-        dxr, dwr = oracle.deconv_bwd(nb, x, w, dy, rows=rows, entries=ent)
-        dxg = dx.cpu().numpy()[rows]
+        yr = oracle.deconv_fwd(nb, x, w, n_out)
+        dxr, dwr = oracle.deconv_bwd(nb, x, w, dy)
     else:
-        yr = oracle.deconv_s2_fwd(ref, l, x, w, want=want)
-        dxr, dwr = oracle.deconv_s2_bwd(ref, l, x, w, dy, entries=ent)
-        dxg = dx.cpu().numpy()
-    assert_f32_close(y.cpu().numpy()[want], yr[want], f"{tag} y")
-    assert_f32_close(dxg, dxr, f"{tag} dx")
-    rule = assert_dw_close(dw.cpu().numpy().ravel()[ent], dwr, f"{tag} dw")
+        yr = oracle.deconv_s2_fwd(ref, l, x, w)
+        dxr, dwr = oracle.deconv_s2_bwd(ref, l, x, w, dy)
+    assert_f32_close(y.cpu().numpy(), yr, f"{tag} y")
+    assert_f32_close(dx.cpu().numpy(), dxr, f"{tag} dx")
+    rule = assert_dw_close(dw.cpu().numpy(), dwr, f"{tag} dw")
     print(f"[{tag}] dw rule: {rule}", flush=True)
 
 
@@ -538,6 +600,15 @@ def test_workload_full_size(name):
             dy = synth.make_upstream(w_, li, ref.num(l - 1), L.cin)
             np.testing.assert_array_equal(oc.oc_pool_bwd(tree, l, _cuda(dy), sw).cpu().numpy(),
                                           oracle.pool_bwd(ref.labels(l - 1), dy, swr, ref.num(l)))
+            # the ReLU-masked routing the network's backward uses (pool_bwd with
+            # the pooled output of a ReLU'd input)
+            a = np.maximum(x, 0.0)
+            ya, swa = oc.oc_pool_fwd(tree, l, _cuda(a))
+            _, swar = oracle.pool_fwd(ref.labels(l - 1), a)
+            np.testing.assert_array_equal(swa.cpu().numpy(), swar)
+            np.testing.assert_array_equal(
+                oc.oc_pool_bwd(tree, l, _cuda(dy), swa, y=ya).cpu().numpy(),
+                oracle.relu_bwd(x, oracle.pool_bwd(ref.labels(l - 1), dy, swar, ref.num(l))))
         elif L.op == "unpool":
             x = synth.make_features([w_.seed_id, 3000 + li], ref.num(l), L.cin)
             _, sw = oc.oc_pool_fwd(tree, l, _cuda(x))

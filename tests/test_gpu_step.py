@@ -1,0 +1,115 @@
+"""The timed step of the bench, end to end at full size: the call sequence
+bench.py runs (fused ReLU in the forward, the ReLU's backward inside the
+pooling's routing, no input gradient for the first layer, separate input-
+and weight-gradient calls) on the octree the GPU builds, every tensor of the
+step against the oracle.
+
+Each op is checked on the GPU's own inputs to that op, so errors do not
+compound, and the oracle takes the decisions that floating point makes
+(ReLU signs, pooling maxima) from the GPU's values: the ReLU mask of a
+backward is [y > 0] of the GPU's forward output, the routing uses the GPU's
+switches.  Those decisions are themselves checked: the forward output is
+within the fp32 rule of the oracle's ReLU(pre-activation) everywhere (ReLU is
+1-Lipschitz), and the switches are bit-exact against the oracle's pooling of
+the GPU's convolution output (a max over identical values is exact)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import assert_dw_close, assert_f32_close
+
+pytestmark = pytest.mark.gpu
+
+
+def _np(t):
+    return None if t is None else t.detach().cpu().numpy()
+
+
+@pytest.mark.parametrize("name", ["net_d6", "seg_d6"])
+def test_bench_step_end_to_end(name):
+    import bench
+    import paper_1712_01537_amd as oc
+
+    wl = synth.WORKLOADS[name]
+    print(f"[step] {name}: building the bench's step", flush=True)
+    step = bench.Step(oc, torch, synth, wl)
+    pts, nrm, offs = synth.make_points(wl)
+    tree = oc.oc_build(step.pts, step.nrm, offs, wl.depth, wl.full_depth)
+    ref = oracle.Octree(pts, nrm, offs, wl.depth, wl.full_depth)
+    for l in range(wl.depth + 1):
+        assert np.array_equal(tree.labels(l).cpu().numpy(), ref.labels(l)), l
+    step.record = {}
+    step.network(tree)
+    torch.cuda.synchronize()
+    fwd, bwd = step.record["fwd"], step.record["bwd"]
+    print(f"[step] {name}: forward", flush=True)
+    for li, L in enumerate(wl.layers):
+        x, y, sw = (_np(t) for t in fwd[li])
+        l = L.depth
+        if li == 0 and wl.signal_input:
+            assert_f32_close(x, ref.signal, "signal", rtol=1e-6, atol=1e-7)
+        if L.op == "conv":
+            nb = ref.neighbors(l, L.ksize, stride=L.stride)
+            pre = oracle.conv_fwd(nb, x, _np(step.weights[li]))
+            r = L.stride.bit_length() - 1
+            if r:
+                pre = oracle.renew(ref.labels(l - r), pre)
+            assert_f32_close(y, oracle.relu_fwd(pre) if L.relu else pre, f"{name}/{li} y")
+        elif L.op == "deconv":
+            w = _np(step.weights[li])
+            yr = (oracle.deconv_fwd(ref.neighbors(l, L.ksize), x, w, ref.num(l)) if L.stride == 1
+                  else oracle.deconv_s2_fwd(ref, l, x, w))
+            assert_f32_close(y, yr, f"{name}/{li} y")
+        elif L.op == "pool":
+            yr, swr = oracle.pool_fwd(ref.labels(l - 1), x)
+            np.testing.assert_array_equal(y, yr)
+            np.testing.assert_array_equal(sw, swr)
+        elif L.op == "unpool":
+            np.testing.assert_array_equal(
+                y, oracle.unpool_fwd(ref.labels(l - 1), x, sw, ref.num(l)))
+    print(f"[step] {name}: backward", flush=True)
+    np.testing.assert_array_equal(_np(bwd[len(wl.layers) - 1][0]), _np(step.dy_last))
+    for li in reversed(range(len(wl.layers))):
+        L = wl.layers[li]
+        l = L.depth
+        g_in, g_out, dw = (_np(t) for t in bwd[li])
+        x, y, sw = (_np(t) for t in fwd[li])
+        if L.op == "conv":
+            nb = ref.neighbors(l, L.ksize, stride=L.stride)
+            w = _np(step.weights[li])
+            # the ReLU's backward is in this call only when no pooling above
+            # applied it already (the bench's rule)
+            above = wl.layers[li + 1] if li + 1 < len(wl.layers) else None
+            masked_above = above is not None and above.op == "pool"
+            ge = oracle.relu_bwd(y, g_in) if (L.relu and not masked_above) else g_in
+            r = L.stride.bit_length() - 1
+            if r:
+                ge = oracle.renew_bwd(ref.labels(l - r), ge, nb.shape[0])
+            rule = assert_dw_close(dw, oracle.conv_bwd_weight(nb, x, ge, L.ksize ** 3),
+                                   f"{name}/{li} dw")
+            print(f"[step] {name}/{li} dw rule: {rule}", flush=True)
+            if li == 0:
+                assert g_out is None  # the signal needs no gradient
+            else:
+                assert_f32_close(g_out, oracle.conv_bwd_data(nb, ge, w, x.shape[0]),
+                                 f"{name}/{li} dx")
+        elif L.op == "deconv":
+            w = _np(step.weights[li])
+            if L.stride == 1:
+                dxr, dwr = oracle.deconv_bwd(ref.neighbors(l, L.ksize), x, w, g_in)
+            else:
+                dxr, dwr = oracle.deconv_s2_bwd(ref, l, x, w, g_in)
+            assert_f32_close(g_out, dxr, f"{name}/{li} dx")
+            assert_dw_close(dw, dwr, f"{name}/{li} dw")
+        elif L.op == "pool":
+            routed = oracle.pool_bwd(ref.labels(l - 1), g_in, sw, ref.num(l))
+            below = wl.layers[li - 1] if li > 0 else None
+            if below is not None and below.op == "conv" and below.relu:
+                routed = oracle.relu_bwd(x, routed)  # the ReLU below, on the GPU's values
+            np.testing.assert_array_equal(g_out, routed)
+        elif L.op == "unpool":
+            np.testing.assert_array_equal(g_out, oracle.unpool_bwd(ref.labels(l - 1), g_in, sw))
+    tree.free()
+    print(f"[step] {name}: every tensor of the step matches", flush=True)
