@@ -210,6 +210,20 @@ oc_status oc_conv_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32
                       oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
                       float* y, void* ws, size_t ws_bytes, int32_t flags, hipStream_t stream);
 
+/* oc_conv_fwd without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation): the workspace is a static device array of the
+ * library, 32 MiB per device, held from the first call on a device until the
+ * process ends; the call allocates nothing.  Arguments as oc_conv_fwd.
+ * Returns OC_ERR_UNSUPPORTED when the call would need more workspace than
+ * 32 MiB (oc_conv_fwd_workspace tells) and for strides other than 1.
+ * Results are identical, bit for bit, to oc_conv_fwd's.  Every call on a
+ * device shares that device's array: calls that overlap on one device (other
+ * streams, other threads) race and must be ordered by the caller. */
+oc_status oc_conv_fwd_noalloc(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                              oc_dtype dt, const void* x, int32_t cin, const void* w,
+                              int32_t cout, float* y, int32_t flags, hipStream_t stream);
+
 /* Name, template arguments included (as profilers such as rocprofv3 print
  * it), of the kernel that does the arithmetic of one pass of a convolution
  * call with these arguments: pass 0 = oc_conv_fwd, 1 = the input gradient and

@@ -26,6 +26,7 @@ __all__ = [
     "oc_build_async",
     "BuildJob",
     "oc_conv_fwd",
+    "oc_conv_fwd_noalloc",
     "oc_conv_kernel",
     "oc_profile_next",
     "CallProfile",
@@ -58,7 +59,7 @@ EXPORTS = (
     "oc_conv_fwd", "oc_conv_kernel", "oc_conv_fwd_workspace", "oc_conv_bwd_workspace", "oc_conv_bwd", "oc_pool_fwd", "oc_pool_bwd",
     "oc_unpool_fwd", "oc_unpool_bwd", "oc_status_str", "oc_last_error", "oc_profile_next",
     "oc_deconv_fwd", "oc_deconv_fwd_workspace", "oc_deconv_bwd", "oc_deconv_bwd_workspace",
-    "oc_gpool_fwd", "oc_gpool_bwd", "oc_profile_calls",
+    "oc_gpool_fwd", "oc_gpool_bwd", "oc_profile_calls", "oc_conv_fwd_noalloc",
 )
 
 
@@ -146,6 +147,8 @@ def load():
         "oc_octree_free": ([p], None),
         "oc_conv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, sz, i32, p], C.c_int),
         "oc_conv_fwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
+        "oc_conv_fwd_noalloc": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, i32, p],
+                                C.c_int),
         "oc_conv_kernel": ([p, i32, i32, i32, C.c_int, i32, i32, i32], C.c_char_p),
         "oc_conv_bwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
         "oc_conv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, p, sz, i32, p],
@@ -423,6 +426,23 @@ def oc_conv_fwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tens
                          _dev(w, "w"), cout, _dev(y, "y", torch.float32, (n_out, cout)),
                          _dev(ws, "ws") if ws is not None else None, ws_bytes,
                          OC_FUSE_RELU if relu else 0, _stream()))
+    return y
+
+
+def oc_conv_fwd_noalloc(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tensor,
+                        w: torch.Tensor, y: torch.Tensor, relu: bool = False) -> torch.Tensor:
+    """oc_conv_fwd with the library's static workspace (no allocation by the
+    library; y is the caller's)."""
+    K3, cin, cout, n_in, n_out = _conv_dims(tree, depth, stride, x, w)
+    if K3 != ksize ** 3:
+        raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
+    dt = _dtype_code(x)
+    if w.dtype != x.dtype:
+        raise OcError(1, "x and w must share a dtype")
+    _check(load().oc_conv_fwd_noalloc(tree.handle, depth, ksize, stride, dt, _dev(x, "x"), cin,
+                                      _dev(w, "w"), cout,
+                                      _dev(y, "y", torch.float32, (n_out, cout)),
+                                      OC_FUSE_RELU if relu else 0, _stream()))
     return y
 
 
