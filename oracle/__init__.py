@@ -263,27 +263,40 @@ def deconv_bwd(nb, x, w, dy, rows=None, entries=None):
     return dx, dw
 
 
-def deconv_s2_fwd(tree: Octree, l, x, w, want=None):
-    """Stride-2 deconvolution from depth l-1 to depth l: the transpose of the
-    stride-2 convolution at depth l (Sec. 3.2).  Row i of x [N_{l-1}][cin]
-    counts only when its octant is non-empty (label p > 0); it reaches the
-    depth-l neighbourhood of the first sibling of group p-1.  -> [N_l][cout]."""
+def deconv_sr_fwd(tree: Octree, l, x, w, stride=2, want=None):
+    """Strided deconvolution from depth l-r to depth l (stride 2^r): the
+    transpose of the stride-2^r convolution at depth l (Sec. 3.2).  Row i of
+    x [N_{l-r}][cin] counts only when its octant is non-empty (label p > 0);
+    it reaches the depth-l neighbourhood of the first depth-l position below
+    octant p-1.  -> [N_l][cout]."""
+    r = int(stride).bit_length() - 1
     K = round(w.shape[0] ** (1 / 3))
-    nb = tree.neighbors(l, K, stride=2)
-    xhat = renew_bwd(tree.labels(l - 1), x, nb.shape[0])
+    nb = tree.neighbors(l, K, stride=stride)
+    xhat = renew_bwd(tree.labels(l - r), x, nb.shape[0])
     return conv_bwd_data(nb, xhat, w, tree.num(l), want=want)
 
 
-def deconv_s2_bwd(tree: Octree, l, x, w, dy, entries=None):
-    """Backward of deconv_s2_fwd: dx = the stride-2 convolution of dy
-    [N_l][cout] ([N_{l-1}][cin], zero at empty octants), dw as in deconv_bwd
-    over the groups' first siblings."""
+def deconv_sr_bwd(tree: Octree, l, x, w, dy, stride=2, entries=None):
+    """Backward of deconv_sr_fwd: dx = the stride-2^r convolution of dy
+    [N_l][cout] ([N_{l-r}][cin], zero at empty octants), dw as in deconv_bwd
+    over the evaluated positions."""
+    r = int(stride).bit_length() - 1
     K = round(w.shape[0] ** (1 / 3))
-    nb = tree.neighbors(l, K, stride=2)
-    dx = renew(tree.labels(l - 1), conv_fwd(nb, dy, w))
-    xhat = renew_bwd(tree.labels(l - 1), x, nb.shape[0])
+    nb = tree.neighbors(l, K, stride=stride)
+    dx = renew(tree.labels(l - r), conv_fwd(nb, dy, w))
+    xhat = renew_bwd(tree.labels(l - r), x, nb.shape[0])
     dw = conv_bwd_weight(nb, dy, xhat, w.shape[0], entries=entries)
     return dx, dw
+
+
+def deconv_s2_fwd(tree: Octree, l, x, w, want=None):
+    """Stride-2 deconvolution (depth l-1 -> l): deconv_sr_fwd with stride 2."""
+    return deconv_sr_fwd(tree, l, x, w, 2, want=want)
+
+
+def deconv_s2_bwd(tree: Octree, l, x, w, dy, entries=None):
+    """Backward of deconv_s2_fwd: deconv_sr_bwd with stride 2."""
+    return deconv_sr_bwd(tree, l, x, w, dy, 2, entries=entries)
 
 
 def conv_sr_fwd(tree: Octree, l, x, w, stride):

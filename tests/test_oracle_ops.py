@@ -285,28 +285,36 @@ def test_deconv_is_adjoint_of_conv():
     assert np.isclose(lhs, np.sum(a * oracle.deconv_fwd(nb, b, w, t.num(l))), rtol=1e-12)
 
 
-@pytest.mark.parametrize("seed,B,depth,full", [(71, 2, 4, 2), (72, 1, 3, 0), (73, 3, 4, 1)])
-def test_deconv_s2_equals_dense_strided_transpose(seed, B, depth, full):
+@pytest.mark.parametrize("seed,B,depth,full,stride", [
+    (71, 2, 4, 2, 2), (72, 1, 3, 0, 2), (73, 3, 4, 1, 2),
+    (74, 2, 4, 2, 4), (75, 2, 4, 0, 8), (76, 1, 3, 1, 8)])
+def test_deconv_sr_equals_dense_strided_transpose(seed, B, depth, full, stride):
+    """Stride 2^r deconvolution (depth l-r -> l): dense conv_transpose3d with
+    stride 2^r, padding 1 and output_padding 2^r - 1 (the transpose of the
+    dense conv3d(stride=2^r, padding=1) that pins the strided convolution)."""
     t = _tree(seed, B, depth, full)
+    r = stride.bit_length() - 1
     l, K, cin, cout = depth, 3, 5, 4
     rng = np.random.default_rng(300 + seed)
-    x = rng.standard_normal((t.num(l - 1), cin))
+    x = rng.standard_normal((t.num(l - r), cin))
     w = rng.standard_normal((K ** 3, cout, cin))
-    y = oracle.deconv_s2_fwd(t, l, x, w)
-    nz = torch.as_tensor((t.labels(l - 1) > 0).astype(np.float64))[:, None]
+    y = oracle.deconv_sr_fwd(t, l, x, w, stride)
+    nz = torch.as_tensor((t.labels(l - r) > 0).astype(np.float64))[:, None]
     xt = torch.as_tensor(x).requires_grad_(True)
     wt = torch.as_tensor(w).requires_grad_(True)
     wd = wt.reshape(K, K, K, cout, cin).permute(4, 3, 0, 1, 2)
-    # rows of empty parents carry nothing (the stride-2 convolution has no output there)
-    out = _gather(t, l, F.conv_transpose3d(_scatter(t, l - 1, xt * nz), wd, stride=2, padding=1,
-                                           output_padding=1))
+    # rows of empty octants carry nothing (the strided convolution has no output there)
+    out = _gather(t, l, F.conv_transpose3d(_scatter(t, l - r, xt * nz), wd, stride=stride,
+                                           padding=1, output_padding=stride - 1))
     np.testing.assert_allclose(y, out.detach().numpy(), rtol=1e-12, atol=1e-12)
     dy = rng.standard_normal((t.num(l), cout))
     out.backward(torch.as_tensor(dy))
-    dx, dw = oracle.deconv_s2_bwd(t, l, x, w, dy)
+    dx, dw = oracle.deconv_sr_bwd(t, l, x, w, dy, stride)
     np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-11, atol=1e-11)
     np.testing.assert_allclose(dw, wt.grad.numpy(), rtol=1e-11, atol=1e-11)
-    assert np.all(dx[t.labels(l - 1) == 0] == 0)
+    assert np.all(dx[t.labels(l - r) == 0] == 0)
+    if stride == 2:  # the stride-2 names are the same functions
+        np.testing.assert_array_equal(oracle.deconv_s2_fwd(t, l, x, w), y)
 
 
 # General pooling (Sec. 3.2, last paragraph of "Pooling"): the stride-1 K^3
