@@ -183,13 +183,13 @@ void oc_octree_free(oc_octree* tree);
  *              first sibling of every group and written to the row of its
  *              parent; rows of empty parents are zero (Sec. 3.2 stride-2
  *              paragraphs, Fig. 2(d)).
- *           4: output at depth l-2 (stride 2^r, r = 2, Sec. 3.2): evaluated
- *              at the first depth-l position of the sub-tree of height 2
- *              below every non-empty depth-(l-2) octant (4 times its
- *              coordinates, whether or not an octant is stored there: the
- *              neighbours of that position are read as usual) and written
- *              to that octant's row; rows of empty octants are zero.
- *              Strides 2 and 4 take ksize 3 only; stride 4 needs l >= 2.
+ *           2^r, r = 1 .. l: output at depth l-r (Sec. 3.2, stride 2^r):
+ *              evaluated at the first depth-l position of the sub-tree of
+ *              height r below every non-empty depth-(l-r) octant (2^r times
+ *              its coordinates, whether or not an octant is stored there:
+ *              the neighbours of that position are read as usual) and
+ *              written to that octant's row; rows of empty octants are
+ *              zero.  Strided convolutions take ksize 3 only.
  *   dt      OC_F32: x, w fp32.  OC_BF16: x, w bf16 (round-to-nearest-even
  *           values held as uint16); products accumulate in fp32, so the
  *           result is the fp32 convolution of the bf16 values.
@@ -198,12 +198,9 @@ void oc_octree_free(oc_octree* tree);
  *   ws      dev workspace of at least oc_conv_fwd_workspace() bytes (may be
  *           NULL when that is 0): partial sums of a reduction split across
  *           workgroups, added in a fixed order (results are reproducible);
- *           for OC_BF16 also x and w widened to fp32; for stride 2 either
- *           a transposed copy of w (fp32 with cin and cout multiples of 16:
- *           one implicit-GEMM kernel gathers the inputs itself) or the
- *           column buffer (at most 256 MB, the groups taken in chunks) and
- *           the per-group outputs, multiplied by w with the ROCm GEMM
- *           library (atomics disabled, so the result is reproducible too).
+ *           for OC_BF16 shapes the bf16 matrix-core kernels do not take, x
+ *           and w widened to fp32; when strided, each output's eight
+ *           source-group rows (32 bytes per output) and w transposed.
  *   flags   0 or OC_FUSE_RELU.
  * cin, cout in 1..1024. */
 oc_status oc_conv_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
@@ -227,10 +224,8 @@ oc_status oc_conv_fwd_noalloc(const oc_octree* tree, int32_t depth, int32_t ksiz
 /* Name, template arguments included (as profilers such as rocprofv3 print
  * it), of the kernel that does the arithmetic of one pass of a convolution
  * call with these arguments: pass 0 = oc_conv_fwd, 1 = the input gradient and
- * 2 = the weight gradient of oc_conv_bwd.  A stride-2 pass is several
- * kernels and a GEMM; it is named "conv_s2_<fwd|bwd_data|bwd_weight><dtype>"
- * instead.  Lets a caller attribute measured kernel time to the operation it
- * belongs to.  The string lives in
+ * 2 = the weight gradient of oc_conv_bwd.  Lets a caller attribute measured
+ * kernel time to the operation it belongs to.  The string lives in
  * thread-local storage until the next call on the thread; "" (and
  * oc_last_error set) for invalid arguments. */
 const char* oc_conv_kernel(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
@@ -257,10 +252,9 @@ size_t oc_conv_bwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize
  *   dw   dev f32 [K^3][cin][cout] or NULL: gradient w.r.t. w (overwritten).
  *   ws   dev workspace of at least oc_conv_bwd_workspace() bytes.
  * Deterministic: no floating-point atomics; repeated calls give identical
- * bits.  The stride-2 workspace holds the per-group upstream gradient and
- * either the gathered upstream gradients of every group's eight parent-offset
- * neighbours with the expanded weight (input gradient) or a column-buffer
- * chunk (weight gradient). */
+ * bits.  The strided workspace holds each output's eight source-group rows,
+ * the upstream gradient gathered at the evaluated outputs and the weight
+ * gradient's partial sums over ranges of outputs. */
 oc_status oc_conv_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
                       oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
                       const float* y, const float* dy, float* dx, float* dw, void* ws,
@@ -270,18 +264,19 @@ oc_status oc_conv_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32
  * "Deconvolution"): the transpose of the convolution cout -> cin with the
  * same weight tensor, obtained as the paper does by swapping that
  * convolution's forward and backward passes.
- *   depth   l, the depth of the output (the finer depth for stride 2).
- *   ksize   3 or 5 (stride 1); 3 (stride 2).
- *   stride  1: x dev f32 [N_l][cin] -> y dev f32 [N_l][cout];
+ *   depth   l, the depth of the output (the finer depth when strided).
+ *   ksize   3 or 5 (stride 1); 3 (stride 2^r).
+ *   stride  1: x dev [N_l][cin] -> y dev f32 [N_l][cout];
  *             y[n] = sum over the rows i and taps k whose neighbour is n of
  *             w[k] x[i] (the input gradient of oc_conv_fwd, cout -> cin).
- *           2: x dev f32 [N_{l-1}][cin] -> y dev f32 [N_l][cout], the
- *             transpose of the stride-2 convolution at depth l: row i of x
- *             counts only when its octant is non-empty (label p > 0), and
- *             then reaches the depth-l neighbourhood of the first sibling of
- *             group p-1.
- *   dt      OC_F32 only (else OC_ERR_UNSUPPORTED).
- *   w       dev f32 [K^3][cout][cin], the weight of the convolution it
+ *           2^r (r = 1 .. depth): x dev [N_{l-r}][cin] -> y dev f32
+ *             [N_l][cout], the transpose of the stride-2^r convolution at
+ *             depth l: row i of x counts only when its octant is non-empty
+ *             (label p > 0), and then reaches the depth-l neighbourhood of
+ *             the first depth-l position below octant p-1.
+ *   dt      OC_F32: x, w fp32.  OC_BF16: x, w bf16; products accumulate in
+ *           fp32 (y is the fp32 deconvolution of the bf16 values).
+ *   w       dev [K^3][cout][cin], the weight of the convolution it
  *           transposes (its index order: tap, that convolution's input
  *           channel = this call's output channel, output channel).
  *   ws      dev workspace of at least oc_deconv_fwd_workspace() bytes.
@@ -305,13 +300,14 @@ size_t oc_deconv_bwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksi
 
 /* Backward of oc_deconv_fwd.  Arguments as oc_deconv_fwd, plus
  *   x    the forward input (read only when dw is requested).
- *   dy   dev f32 [N_l][cout] upstream gradient.
+ *   dy   dev f32 [N_l][cout] upstream gradient.  OC_BF16: the matrix-core
+ *        operand is dy rounded to bf16, nearest-even.
  *   dx   dev f32, shaped as x, or NULL: the convolution cout -> cin of dy
- *        (stride 2: rows of empty depth-(l-1) octants are 0).
+ *        (strided: rows of empty depth-(l-r) octants are 0).
  *   dw   dev f32 [K^3][cout][cin] or NULL:
  *        dw[k][co][ci] = sum over rows i of x and taps k of dy[nb(i,k)][co]
- *        x[i][ci] (stride 2: rows of non-empty octants, at the first
- *        sibling of their group).
+ *        x[i][ci] (strided: rows of non-empty octants, at the first depth-l
+ *        position below them).
  *   ws   dev workspace of at least oc_deconv_bwd_workspace() bytes; both
  *        passes use it in stream order.
  * Every argument is checked before either pass is enqueued. */
@@ -386,8 +382,7 @@ oc_status oc_gpool_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int3
  * convolution pass; the pooling, routing or unpooling kernel of oc_pool_* /
  * oc_unpool_*) is bracketed by these events, recorded at the start and the
  * end of that kernel on its stream (as hipExtLaunchKernelGGL does), so that
- * its duration is measured without host-side gaps.  A stride-2 convolution
- * pass records them around all of its kernels and GEMMs.  Both NULL clears a
+ * its duration is measured without host-side gaps.  Both NULL clears a
  * pending pair.  The caller owns the events. */
 oc_status oc_profile_next(hipEvent_t start, hipEvent_t stop);
 

@@ -474,8 +474,11 @@ def _deconv_dims(tree: Octree, depth: int, stride: int, x, w):
     if not 1 <= depth <= tree.depth:
         raise OcError(1, f"depth {depth} not in 1..{tree.depth}")
     K3, cout, cin = w.shape
+    r = int(stride).bit_length() - 1  # stride 2^r
+    if not 0 <= r <= depth:
+        raise OcError(1, f"stride {stride} needs depth >= {r}")
     n_out = tree.num(depth)
-    n_in = n_out if stride == 1 else tree.num(depth - 1)
+    n_in = tree.num(depth - r)
     if x is not None and tuple(x.shape) != (n_in, cin):
         raise OcError(1, f"x has shape {tuple(x.shape)}, expected {(n_in, cin)}")
     return K3, cin, cout, n_in, n_out
@@ -489,13 +492,15 @@ def oc_deconv_fwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Te
     if K3 != ksize ** 3:
         raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
     dt = _dtype_code(x)
+    if w.dtype != x.dtype:
+        raise OcError(1, "x and w must share a dtype")
     if y is None:
         y = torch.empty((n_out, cout), dtype=torch.float32, device=x.device)
     L = load()
     ws_bytes = int(L.oc_deconv_fwd_workspace(tree.handle, depth, ksize, stride, dt, cin, cout))
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device) if ws_bytes else None
     _check(L.oc_deconv_fwd(tree.handle, depth, ksize, stride, dt, _dev(x, "x"), cin,
-                           _dev(w, "w", torch.float32), cout,
+                           _dev(w, "w"), cout,
                            _dev(y, "y", torch.float32, (n_out, cout)),
                            _dev(ws, "ws") if ws is not None else None, ws_bytes, 0, _stream()))
     return y

@@ -12,14 +12,15 @@
 // Stride 1 runs on the matrix-core kernels of conv_mfma.hip (fp32) and
 // conv_bf16.hip (bf16 with both channel counts multiples of 16; other bf16
 // shapes widen their operands to fp32, which is exact, and run the fp32
-// kernels); stride 2 on the column buffers and GEMMs of conv_s2.hip.  This file checks arguments, sizes the workspaces and
-// applies the ReLU backward ahead of the stride-1 gradients.
+// kernels); strides 2^r on the gathered-row GEMMs of conv_sr.hip.  This file
+// checks arguments, sizes the workspaces and applies the ReLU backward ahead of
+// the stride-1 gradients.
 #include <algorithm>
 
 #include "common.h"
 #include "conv_bf16.h"
 #include "conv_mfma.h"
-#include "conv_s2.h"
+#include "conv_sr.h"
 
 namespace {
 
@@ -95,12 +96,13 @@ oc_status check_conv(const oc_octree* t, int32_t l, int32_t K, int32_t stride, o
   oc_status st = oc::check_tree_level(t, l, 1);
   if (st != OC_OK) return st;
   if (dt != OC_F32 && dt != OC_BF16) return oc::fail(OC_ERR_ARG, "%s: bad dtype %d", who, (int)dt);
-  if (stride != 1 && stride != 2 && stride != 4)
-    return oc::fail(OC_ERR_ARG, "%s: stride %d not 1, 2 or 4", who, stride);
+  if (stride < 1 || stride > (1 << OC_MAX_DEPTH) || (stride & (stride - 1)) != 0)
+    return oc::fail(OC_ERR_ARG, "%s: stride %d not a power of two in 1..%d", who, stride,
+                    1 << OC_MAX_DEPTH);
   if (K != 3 && K != 5) return oc::fail(OC_ERR_UNSUPPORTED, "%s: kernel size %d not 3 or 5", who, K);
   if (stride > 1 && K != 3)
     return oc::fail(OC_ERR_UNSUPPORTED, "%s: stride %d supports kernel size 3 only", who, stride);
-  const int r = stride == 4 ? 2 : stride == 2 ? 1 : 0;
+  const int r = __builtin_ctz((unsigned)stride);
   if (l < r) return oc::fail(OC_ERR_ARG, "%s: stride %d needs depth >= %d", who, stride, r);
   if (cin < 1 || cin > 1024 || cout < 1 || cout > 1024)
     return oc::fail(OC_ERR_ARG, "%s: channels %d -> %d out of range", who, cin, cout);
@@ -186,10 +188,8 @@ const char* oc_conv_kernel(const oc_octree* t, int32_t l, int32_t K, int32_t str
     oc::conv_bf16_kernel_name(K, cin, cout, pass, name, sizeof(name));
   } else if (stride == 1) {  // other bf16 shapes run the fp32 kernels on widened operands
     oc::conv_s1_kernel_name(t, l, K, cin, cout, pass, name, sizeof(name));
-  } else {  // several kernels and a GEMM: the pass is named
-    snprintf(name, sizeof(name), "conv_s%d_%s<%s>", stride,
-             pass == 0 ? "fwd" : pass == 1 ? "bwd_data" : "bwd_weight",
-             dt == OC_F32 ? "f32" : "bf16");
+  } else {
+    snprintf(name, sizeof(name), "%s", oc::conv_sr_kernel_name(pass, sh.r, dt == OC_BF16, cin, cout));
   }
   return name;
 }

@@ -1,5 +1,5 @@
-// Stride-2 and stride-4 (r = 1, 2), K = 3 octree convolution through column
-// buffers and a GEMM (conv_s2.hip).
+// Strided octree convolution (stride 2^r, r >= 1, K = 3) on the matrix cores
+// (conv_sr.hip): implicit GEMMs over gathered rows, no column buffer.
 #pragma once
 
 #include "common.h"
@@ -23,5 +23,9 @@ oc_status conv_s2_fwd(const oc_octree* t, int l, int r, const void* x, int cin, 
 oc_status conv_s2_bwd(const oc_octree* t, int l, int r, const void* x, int cin, const void* w,
                       int cout, bool bf16, const float* ym, const float* dy, float* dx, float* dw,
                       void* ws, hipStream_t s);
+
+// Name (template arguments included) of the kernel doing pass 0 (forward),
+// 1 (input gradient) or 2 (weight gradient); thread-local storage.
+const char* conv_sr_kernel_name(int pass, int r, bool bf16, int cin, int cout);
 
 }  // namespace oc

@@ -95,20 +95,30 @@ def test_conv_small_fp32(seed, B, n, depth, K, stride, cin, cout, relu):
     assert torch.equal(dw.view(torch.int32), dw2.view(torch.int32))
 
 
-S4_SMALL = [  # seed, B, n, depth, cin, cout, relu, bf16
-    (101, 2, 400, 4, 5, 7, False, False),
-    (102, 3, 600, 5, 16, 32, True, False),
-    (103, 1, 900, 5, 64, 16, False, False),  # column-buffer chunks of many channels
-    (104, 2, 500, 4, 8, 12, False, True),
-    (105, 2, 800, 5, 32, 32, True, True),
+SR_SMALL = [  # seed, B, n, depth, stride, cin, cout, relu, bf16
+    (101, 2, 400, 4, 4, 5, 7, False, False),
+    (102, 3, 600, 5, 4, 16, 32, True, False),
+    (103, 1, 900, 5, 4, 64, 16, False, False),
+    (104, 2, 500, 4, 4, 8, 12, False, True),
+    (105, 2, 800, 5, 4, 32, 32, True, True),
+    (106, 3, 700, 5, 8, 16, 48, True, False),  # r = 3: depth 5 -> 2
+    (107, 2, 900, 5, 8, 24, 16, False, True),
+    (108, 2, 600, 5, 16, 32, 64, False, False),  # r = 4: depth 5 -> 1
+    (109, 2, 500, 4, 16, 16, 16, True, True),   # r = 4: depth 4 -> 0 (the roots)
+    (110, 4, 400, 4, 2, 80, 96, True, True),    # several output-column tiles, 3 reduction chunks
+    (111, 2, 700, 5, 2, 3, 20, False, False),   # rows of 12 bytes (element-wise loads)
+    (112, 2, 700, 5, 2, 36, 130, True, False),  # ragged channel chunks and columns
 ]
 
 
-@pytest.mark.parametrize("seed,B,n,depth,cin,cout,relu,bf16", S4_SMALL)
-def test_conv_stride4(seed, B, n, depth, cin, cout, relu, bf16):
-    """Stride 4 (Sec. 3.2, stride 2^r with r = 2): depth l -> depth l-2."""
+@pytest.mark.parametrize("seed,B,n,depth,stride,cin,cout,relu,bf16", SR_SMALL)
+def test_conv_stride_pow2(seed, B, n, depth, stride, cin, cout, relu, bf16):
+    """Stride 2^r (Sec. 3.2): depth l -> depth l-r, evaluated at the first
+    depth-l position below every non-empty depth-(l-r) octant."""
     oc = _oc()
-    print(f"[s4] seed={seed} B={B} d={depth} {cin}->{cout} relu={relu} bf16={bf16}", flush=True)
+    print(f"[sr] seed={seed} B={B} d={depth} s={stride} {cin}->{cout} relu={relu} bf16={bf16}",
+          flush=True)
+    r = stride.bit_length() - 1
     pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
     ref, tree = _trees(pts, nrm, offs, depth)
     l = depth
@@ -117,62 +127,79 @@ def test_conv_stride4(seed, B, n, depth, cin, cout, relu, bf16):
     w = (rng.standard_normal((27, cin, cout)) / np.sqrt(27 * cin)).astype(np.float32)
     dt = torch.bfloat16 if bf16 else torch.float32
     xq, wq = (bf16_round(x), bf16_round(w)) if bf16 else (x, w)
-    pre = oracle.conv_sr_fwd(ref, l, xq, wq, 4)
-    dy = _mask_ambiguous(rng.standard_normal((ref.num(l - 2), cout)).astype(np.float32), pre, relu)
-    y = oc.oc_conv_fwd(tree, l, 3, 4, _cuda(x, dt), _cuda(w, dt), relu=relu)
+    pre = oracle.conv_sr_fwd(ref, l, xq, wq, stride)
+    dy = _mask_ambiguous(rng.standard_normal((ref.num(l - r), cout)).astype(np.float32), pre,
+                         relu)
+    y = oc.oc_conv_fwd(tree, l, 3, stride, _cuda(x, dt), _cuda(w, dt), relu=relu)
     assert_f32_close(y.cpu().numpy(), oracle.relu_fwd(pre) if relu else pre, "y")
-    dx, dw = oc.oc_conv_bwd(tree, l, 3, 4, _cuda(x, dt), _cuda(w, dt), _cuda(dy), y=y, relu=relu)
+    dx, dw = oc.oc_conv_bwd(tree, l, 3, stride, _cuda(x, dt), _cuda(w, dt), _cuda(dy), y=y,
+                            relu=relu)
     dye = oracle.relu_bwd(pre, dy) if relu else dy
     if bf16:  # the bf16 backward multiplies dy rounded to bf16
         dye = bf16_round(dye)
-    dxr, dwr = oracle.conv_sr_bwd(ref, l, xq, wq, dye, 4)
+    dxr, dwr = oracle.conv_sr_bwd(ref, l, xq, wq, dye, stride)
     assert_f32_close(dx.cpu().numpy(), dxr, "dx")
     assert_dw_close(dw.cpu().numpy(), dwr, "dw")
-    dx2, dw2 = oc.oc_conv_bwd(tree, l, 3, 4, _cuda(x, dt), _cuda(w, dt), _cuda(dy), y=y, relu=relu)
+    dx2, dw2 = oc.oc_conv_bwd(tree, l, 3, stride, _cuda(x, dt), _cuda(w, dt), _cuda(dy), y=y,
+                              relu=relu)
     assert torch.equal(dx.view(torch.int32), dx2.view(torch.int32))
     assert torch.equal(dw.view(torch.int32), dw2.view(torch.int32))
-    with pytest.raises(oc.OcError):  # stride 4 takes K = 3 only
-        oc.oc_conv_fwd(tree, l, 5, 4, _cuda(x), _cuda(np.zeros((125, cin, cout))))
+    with pytest.raises(oc.OcError):  # strided convolution takes K = 3 only
+        oc.oc_conv_fwd(tree, l, 5, stride, _cuda(x), _cuda(np.zeros((125, cin, cout))))
 
 
-DECONV_SMALL = [  # seed, B, n, depth, K, stride, cin, cout (deconv channels)
-    (81, 2, 400, 4, 3, 1, 7, 5),
-    (82, 2, 900, 5, 3, 1, 128, 64),  # split reduction in the forward (input-gradient kernel)
-    (83, 1, 800, 5, 5, 1, 8, 8),
-    (84, 2, 500, 4, 3, 2, 10, 6),
-    (85, 2, 500, 5, 3, 2, 32, 16),
-    (86, 3, 300, 4, 3, 1, 16, 3),  # down to 3 channels
+DECONV_SMALL = [  # seed, B, n, depth, K, stride, cin, cout (deconv channels), bf16
+    (81, 2, 400, 4, 3, 1, 7, 5, False),
+    (82, 2, 900, 5, 3, 1, 128, 64, False),  # split reduction in the forward (input-gradient kernel)
+    (83, 1, 800, 5, 5, 1, 8, 8, False),
+    (84, 2, 500, 4, 3, 2, 10, 6, False),
+    (85, 2, 500, 5, 3, 2, 32, 16, False),
+    (86, 3, 300, 4, 3, 1, 16, 3, False),  # down to 3 channels
+    (87, 2, 700, 5, 3, 4, 24, 16, False),  # stride 4: depth 3 -> 5
+    (88, 2, 600, 5, 3, 8, 16, 32, False),  # stride 8: depth 2 -> 5
+    (89, 2, 700, 5, 3, 1, 32, 48, True),   # bf16 matrix-core kernels
+    (90, 2, 500, 4, 5, 1, 12, 20, True),   # bf16 on widened operands
+    (91, 3, 600, 5, 3, 2, 64, 32, True),
+    (92, 2, 600, 5, 3, 4, 16, 16, True),
 ]
 
 
-@pytest.mark.parametrize("seed,B,n,depth,K,stride,cin,cout", DECONV_SMALL)
-def test_deconv_small_fp32(seed, B, n, depth, K, stride, cin, cout):
+@pytest.mark.parametrize("seed,B,n,depth,K,stride,cin,cout,bf16", DECONV_SMALL)
+def test_deconv_small(seed, B, n, depth, K, stride, cin, cout, bf16):
     oc = _oc()
-    print(f"[deconv] seed={seed} B={B} d={depth} K={K} s={stride} {cin}->{cout}", flush=True)
+    print(f"[deconv] seed={seed} B={B} d={depth} K={K} s={stride} {cin}->{cout} bf16={bf16}",
+          flush=True)
     pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
     ref, tree = _trees(pts, nrm, offs, depth)
     l = depth
+    r = stride.bit_length() - 1
     rng = np.random.default_rng(seed)
-    n_in = ref.num(l) if stride == 1 else ref.num(l - 1)
+    n_in = ref.num(l - r)
     x = rng.standard_normal((n_in, cin)).astype(np.float32)
     w = (rng.standard_normal((K ** 3, cout, cin)) / np.sqrt(K ** 3 * cin)).astype(np.float32)
     dy = rng.standard_normal((ref.num(l), cout)).astype(np.float32)
-    y = oc.oc_deconv_fwd(tree, l, K, stride, _cuda(x), _cuda(w))
-    dx, dw = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x), _cuda(w), _cuda(dy))
+    dt = torch.bfloat16 if bf16 else torch.float32
+    if bf16:  # the same bf16 values on both sides; the backward rounds dy to bf16
+        x, w = bf16_round(x), bf16_round(w)
+    dyq = bf16_round(dy) if bf16 else dy
+    y = oc.oc_deconv_fwd(tree, l, K, stride, _cuda(x, dt), _cuda(w, dt))
+    dx, dw = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x, dt), _cuda(w, dt), _cuda(dy))
     if stride == 1:
         nb = ref.neighbors(l, K)
         yr = oracle.deconv_fwd(nb, x, w, ref.num(l))
-        dxr, dwr = oracle.deconv_bwd(nb, x, w, dy)
+        dxr, dwr = oracle.deconv_bwd(nb, x, w, dyq)
     else:
-        yr = oracle.deconv_s2_fwd(ref, l, x, w)
-        dxr, dwr = oracle.deconv_s2_bwd(ref, l, x, w, dy)
+        yr = oracle.deconv_sr_fwd(ref, l, x, w, stride)
+        dxr, dwr = oracle.deconv_sr_bwd(ref, l, x, w, dyq, stride)
     assert_f32_close(y.cpu().numpy(), yr, "y")
     assert_f32_close(dx.cpu().numpy(), dxr, "dx")
     assert_dw_close(dw.cpu().numpy(), dwr, "dw")
     # deterministic: identical bits on a second call; each gradient alone equals the pair
-    y2 = oc.oc_deconv_fwd(tree, l, K, stride, _cuda(x), _cuda(w))
-    dx2, _ = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x), _cuda(w), _cuda(dy), need_dw=False)
-    _, dw2 = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x), _cuda(w), _cuda(dy), need_dx=False)
+    y2 = oc.oc_deconv_fwd(tree, l, K, stride, _cuda(x, dt), _cuda(w, dt))
+    dx2, _ = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x, dt), _cuda(w, dt), _cuda(dy),
+                              need_dw=False)
+    _, dw2 = oc.oc_deconv_bwd(tree, l, K, stride, _cuda(x, dt), _cuda(w, dt), _cuda(dy),
+                              need_dx=False)
     assert torch.equal(y.view(torch.int32), y2.view(torch.int32))
     assert torch.equal(dx.view(torch.int32), dx2.view(torch.int32))
     assert torch.equal(dw.view(torch.int32), dw2.view(torch.int32))
@@ -183,9 +210,11 @@ def test_deconv_argument_errors():
     pts = np.array([[0.3, 0.6, 0.9]], np.float32)
     ref, tree = _trees(pts, np.ones((1, 3), np.float32), [0, 1], 3, 0)
     x = _cuda(np.zeros((ref.num(3), 4)))
-    with pytest.raises(oc.OcError):  # bf16 is not supported
-        oc.oc_deconv_fwd(tree, 3, 3, 1, x.to(torch.bfloat16),
-                         _cuda(np.zeros((27, 2, 4))).to(torch.bfloat16))
+    with pytest.raises(oc.OcError):  # x and w of different dtypes
+        oc.oc_deconv_fwd(tree, 3, 3, 1, x.to(torch.bfloat16), _cuda(np.zeros((27, 2, 4))))
+    with pytest.raises(oc.OcError):  # stride 16 from depth 3
+        oc.oc_deconv_fwd(tree, 3, 3, 16, _cuda(np.zeros((ref.num(0), 4))),
+                         _cuda(np.zeros((27, 2, 4))))
     with pytest.raises(oc.OcError):  # kernel size 7
         oc.oc_deconv_fwd(tree, 3, 7, 1, x, _cuda(np.zeros((343, 2, 4))))
     with pytest.raises(oc.OcError):  # stride 2 with K = 5
@@ -394,16 +423,17 @@ def test_new_ops_degenerate_trees():
         xs = rng.standard_normal((ref.num(l - 1), 4)).astype(np.float32)
         assert_f32_close(oc.oc_deconv_fwd(tree, l, 3, 2, _cuda(xs), _cuda(w)).cpu().numpy(),
                          oracle.deconv_s2_fwd(ref, l, xs, w), f"deconv s2 l={l}")
-    for l in (2, 3):  # stride 4 down to depths 0 and 1
+    for l, st in ((2, 4), (3, 4), (3, 8)):  # strides 4 and 8 down to depths 0 and 1
+        r = st.bit_length() - 1
         x = rng.standard_normal((ref.num(l), 16)).astype(np.float32)
         w = rng.standard_normal((27, 16, 16)).astype(np.float32)
-        y = oc.oc_conv_fwd(tree, l, 3, 4, _cuda(x), _cuda(w))
-        assert_f32_close(y.cpu().numpy(), oracle.conv_sr_fwd(ref, l, x, w, 4), f"s4 l={l}")
-        dy = rng.standard_normal((ref.num(l - 2), 16)).astype(np.float32)
-        dx, dw = oc.oc_conv_bwd(tree, l, 3, 4, _cuda(x), _cuda(w), _cuda(dy))
-        dxr, dwr = oracle.conv_sr_bwd(ref, l, x, w, dy, 4)
-        assert_f32_close(dx.cpu().numpy(), dxr, f"s4 dx l={l}")
-        assert_dw_close(dw.cpu().numpy(), dwr, f"s4 dw l={l}")
+        y = oc.oc_conv_fwd(tree, l, 3, st, _cuda(x), _cuda(w))
+        assert_f32_close(y.cpu().numpy(), oracle.conv_sr_fwd(ref, l, x, w, st), f"s{st} l={l}")
+        dy = rng.standard_normal((ref.num(l - r), 16)).astype(np.float32)
+        dx, dw = oc.oc_conv_bwd(tree, l, 3, st, _cuda(x), _cuda(w), _cuda(dy))
+        dxr, dwr = oracle.conv_sr_bwd(ref, l, x, w, dy, st)
+        assert_f32_close(dx.cpu().numpy(), dxr, f"s{st} dx l={l}")
+        assert_dw_close(dw.cpu().numpy(), dwr, f"s{st} dw l={l}")
     with pytest.raises(oc.OcError):  # stride 4 from depth 1
         oc.oc_conv_fwd(tree, 1, 3, 4, _cuda(np.zeros((ref.num(1), 16))), _cuda(np.zeros((27, 16, 16))))
 
