@@ -421,6 +421,37 @@ def gpool_bwd(nb, dy, sw, n_in, mode):
     return dx
 
 
+def gpool_sr_fwd(tree: Octree, l, x, mode, stride):
+    """General pooling with stride 2^r (Sec. 3.2, pooling as a special kind of
+    convolution, here with another stride): the 3x3x3 neighbourhood the
+    stride-2^r convolution reads, evaluated at the first depth-l position
+    below every non-empty depth-(l-r) octant and written to that octant's
+    row; absent neighbours count as zeros (as at stride 1).  Rows of empty
+    depth-(l-r) octants get 0 and, for max, the switch POOL_ABSENT.
+    Returns y [N_{l-r}][C] and sw [N_{l-r}][C] u8 (max) or None."""
+    r = int(stride).bit_length() - 1
+    nb = tree.neighbors(l, 3, stride=stride)
+    yh, swh = gpool_fwd(nb, x, mode)
+    lab = tree.labels(l - r)
+    y = renew(lab, yh)
+    if mode == POOL_AVG:
+        return y, None
+    sw = np.full((len(lab), yh.shape[1]), POOL_ABSENT, np.uint8)
+    sw[lab > 0] = swh[lab[lab > 0] - 1]
+    return y, sw
+
+
+def gpool_sr_bwd(tree: Octree, l, dy, sw, n_in, mode, stride):
+    """Gradient of gpool_sr_fwd w.r.t. x [n_in][C]: the rows of the
+    non-empty depth-(l-r) octants carry their gradient (and switch) to the
+    stride-1 rule of gpool_bwd over the strided neighbourhood."""
+    r = int(stride).bit_length() - 1
+    nb = tree.neighbors(l, 3, stride=stride)
+    dyh = renew_bwd(tree.labels(l - r), dy, nb.shape[0])
+    swh = None if mode == POOL_AVG else np.asarray(sw)[tree.rows(l - r)]
+    return gpool_bwd(nb, dyh, swh, n_in, mode)
+
+
 def relu_fwd(x):
     x = _f64(x)
     y = np.zeros_like(x)

@@ -361,6 +361,49 @@ def test_gpool_equals_dense_pooling(seed, B, depth, full, K):
                                xt.grad.numpy(), rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("seed,B,depth,full,stride", [
+    (41, 2, 4, 2, 2), (42, 1, 3, 0, 2), (43, 3, 4, 1, 4), (44, 2, 4, 2, 8), (45, 1, 3, 3, 2)])
+def test_gpool_strided_equals_dense_pooling(seed, B, depth, full, stride):
+    """Strided general pooling: dense zero-padded max_pool3d / avg_pool3d
+    (count_include_pad) with kernel 3 and stride 2^r, read at the non-empty
+    depth-(l-r) octants (zero rows at empty ones), and their autograd."""
+    t = _tree(seed, B, depth, full)
+    l, c = depth, 4
+    r = stride.bit_length() - 1
+    rng = np.random.default_rng(500 + seed)
+    x = rng.standard_normal((t.num(l), c))
+    dy = rng.standard_normal((t.num(l - r), c))
+    nz = t.labels(l - r) > 0
+    y, sw = oracle.gpool_sr_fwd(t, l, x, oracle.POOL_MAX, stride)
+    xt = torch.as_tensor(x).requires_grad_(True)
+    g = F.pad(_scatter(t, l, xt), (1,) * 6, value=0.0)
+    dense, idx = F.max_pool3d(g, 3, stride=stride, return_indices=True)
+    out = _gather(t, l - r, dense) * torch.as_tensor(nz.astype(np.float64))[:, None]
+    np.testing.assert_array_equal(y, out.detach().numpy())
+    sp = 2 ** l + 2
+    b, X, Y, Z = _coords(t, l - r)
+    fi = _gather(t, l - r, idx).numpy()
+    ix, iy, iz = fi // (sp * sp), (fi // sp) % sp, fi % sp
+    tap = ((ix - stride * X[:, None]) * 3 + (iy - stride * Y[:, None])) * 3 + (iz - stride * Z[:, None])
+    present = sw != oracle.POOL_ABSENT
+    np.testing.assert_array_equal(sw[present], tap[present])
+    assert np.all(y[~present] == 0) and np.all(sw[~nz] == oracle.POOL_ABSENT)
+    out.backward(torch.as_tensor(dy))
+    np.testing.assert_allclose(oracle.gpool_sr_bwd(t, l, dy, sw, t.num(l), oracle.POOL_MAX, stride),
+                               xt.grad.numpy(), rtol=1e-12, atol=1e-12)
+    ya, swa = oracle.gpool_sr_fwd(t, l, x, oracle.POOL_AVG, stride)
+    assert swa is None
+    xt = torch.as_tensor(x).requires_grad_(True)
+    out = _gather(t, l - r, F.avg_pool3d(_scatter(t, l, xt), 3, stride=stride, padding=1,
+                                         count_include_pad=True))
+    out = out * torch.as_tensor(nz.astype(np.float64))[:, None]
+    np.testing.assert_allclose(ya, out.detach().numpy(), rtol=1e-12, atol=1e-12)
+    out.backward(torch.as_tensor(dy))
+    np.testing.assert_allclose(oracle.gpool_sr_bwd(t, l, dy, None, t.num(l), oracle.POOL_AVG,
+                                                   stride),
+                               xt.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
 def test_gpool_hand_case():
     # one group of 8 siblings at depth 1 (the whole cube): every child sees the
     # other seven plus 19 absent (outside-cube) neighbours
