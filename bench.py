@@ -373,6 +373,8 @@ class Accounting:
             return self.N[L.depth - (L.stride.bit_length() - 1)]
         if L.op == "pool":
             return self.N[L.depth - 1]
+        if L.op == "gpool":  # stride 2^r: depth - r
+            return self.N[L.depth - (L.stride.bit_length() - 1)]
         return self.N[L.depth]
 
     def _n_in(self, L):
@@ -421,8 +423,14 @@ class Accounting:
             return M[l - 1] * c * 5 + M[l - 1] * 4 + N[l] * c * 4
         if tag == "unpool_bwd":  # the routed child of each (parent, channel) in, parent rows out
             return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l - 1] * c * 4
-        if tag in ("gpool_fwd", "gpool_bwd"):  # rows in and out, switches (max), 27 ints per group
-            return N[l] * c * 8 + (N[l] * c if L.mode == "max" else 0) + M[l - 1] * 108
+        if tag in ("gpool_fwd", "gpool_bwd"):
+            r = L.stride.bit_length() - 1
+            if r == 0:  # rows in and out, switches (max), 27 ints per group
+                return N[l] * c * 8 + (N[l] * c if L.mode == "max" else 0) + M[l - 1] * 108
+            # strided: the depth-l rows and the depth-(l-r) rows, switches (max),
+            # the 8 group-table entries of every output and its label
+            return ((N[l] + N[l - r]) * c * 4 + (N[l - r] * c if L.mode == "max" else 0)
+                    + N[l - r] * 4 + M[l - r] * 32)
         return 0
 
 
@@ -603,7 +611,7 @@ class Step(Accounting):
             elif L.op == "gpool":
                 mode = oc.OC_POOL_MAX if L.mode == "max" else oc.OC_POOL_AVG
                 y, sw = self._run("gpool_fwd", li, lambda: oc.oc_gpool_fwd(
-                    tree, L.depth, L.ksize, mode, x))
+                    tree, L.depth, L.ksize, mode, x, stride=L.stride))
                 saved.append((li, x, y, sw))
                 x = y
             elif L.op == "pool":
@@ -663,7 +671,7 @@ class Step(Accounting):
             elif L.op == "gpool":
                 mode = oc.OC_POOL_MAX if L.mode == "max" else oc.OC_POOL_AVG
                 g = self._run("gpool_bwd", li, lambda: oc.oc_gpool_bwd(
-                    tree, L.depth, L.ksize, mode, g, sw))
+                    tree, L.depth, L.ksize, mode, g, sw, stride=L.stride))
                 masked = False
             elif L.op == "pool":
                 # a ReLU right below the pooling: its backward goes into the routing
@@ -735,9 +743,9 @@ def oracle_step(synth, wl, shapes):
                 nb = ref.neighbors(l, L.ksize)
                 y = oracle.deconv_fwd(nb, x, w, ref.num(l))
             else:
-                y = oracle.deconv_s2_fwd(ref, l, x, w)
+                y = oracle.deconv_sr_fwd(ref, l, x, w, L.stride)
             saved.append((li, None, x, w, None))
-            n = ref.num(l) if L.stride == 1 else ref.nonempty(l - 1)
+            n = ref.num(l) if L.stride == 1 else ref.nonempty(l - (L.stride.bit_length() - 1))
             flops += 6 * n * L.ksize ** 3 * L.cin * L.cout
             x = y
         elif L.op == "pool":
@@ -751,9 +759,13 @@ def oracle_step(synth, wl, shapes):
             saved.append((li, None, x, sw, None))
             x = y
         elif L.op == "gpool":
-            nb = ref.neighbors(l, L.ksize)
             mode = oracle.POOL_MAX if L.mode == "max" else oracle.POOL_AVG
-            y, sw = oracle.gpool_fwd(nb, x, mode)
+            if L.stride == 1:
+                nb = ref.neighbors(l, L.ksize)
+                y, sw = oracle.gpool_fwd(nb, x, mode)
+            else:
+                nb = None
+                y, sw = oracle.gpool_sr_fwd(ref, l, x, mode, L.stride)
             saved.append((li, nb, x, sw, mode))
             x = y
     g = synth.make_upstream(wl, len(wl.layers) - 1, x.shape[0], x.shape[1])
@@ -771,11 +783,14 @@ def oracle_step(synth, wl, shapes):
             if L.stride == 1:
                 g, _ = oracle.deconv_bwd(ref.neighbors(l, L.ksize), xin, w_or_sw, g)
             else:
-                g, _ = oracle.deconv_s2_bwd(ref, l, xin, w_or_sw, g)
+                g, _ = oracle.deconv_sr_bwd(ref, l, xin, w_or_sw, g, L.stride)
         elif L.op == "unpool":
             g = oracle.unpool_bwd(ref.labels(l - 1), g, w_or_sw)
         elif L.op == "gpool":
-            g = oracle.gpool_bwd(nb, g, w_or_sw, ref.num(l), pre)
+            if L.stride == 1:
+                g = oracle.gpool_bwd(nb, g, w_or_sw, ref.num(l), pre)
+            else:
+                g = oracle.gpool_sr_bwd(ref, l, g, w_or_sw, ref.num(l), pre, L.stride)
         else:
             g = oracle.pool_bwd(ref.labels(l - 1), g, w_or_sw, ref.num(l))
     return flops, time.perf_counter() - t0
@@ -1052,7 +1067,8 @@ WORKLOAD_TEXT = {
     "wide_d7": "16 shapes, 100k points each, depth 7; conv5 64->64 and stride-2 conv3 "
                "64->128, bf16 inputs with fp32 accumulation",
     "gpool_d6": "32 shapes, depth 6; conv3+ReLU 3->16 @d6, stride-1 3x3x3 max-pool and 5x5x5 "
-                "average-pool @d6 (the convolution's neighbourhood), 2x2x2 max-pool d6->d5; fp32 "
+                "average-pool @d6 (the convolution's neighbourhood), 2x2x2 max-pool d6->d5, "
+                "3x3x3 max-pool stride 2 d5->d4, 3x3x3 average-pool stride 4 d4->d2; fp32 "
                 "forward and backward",
     "s4_d6": "32 shapes, depth 6; conv3+ReLU 3->16 @d6, stride-4 conv3+ReLU 16->64 d6->d4, "
              "conv3 64->128 @d4; fp32 forward and backward",

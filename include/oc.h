@@ -349,32 +349,40 @@ oc_status oc_unpool_fwd(const oc_octree* tree, int32_t depth, const float* x, co
 oc_status oc_unpool_bwd(const oc_octree* tree, int32_t depth, const float* dy, const uint8_t* sw,
                         int32_t c, float* dx, hipStream_t stream);
 
-/* General pooling, stride 1 (Sec. 3.2, last paragraph of "Pooling": pooling
- * with other kernel sizes finds the neighbouring octants as the convolution
- * does and applies the pooling operation to them).  For every octant i of
- * depth l and channel c, over the K^3 taps k of its neighbourhood (index as
- * the convolution's weights), where a neighbour that is not in the octree
- * reads as 0:
- *   OC_POOL_MAX  y[i][c] = the maximum; sw[i][c] = the tap of its first
- *                occurrence in tap order, or 255 when that is an absent
- *                neighbour (whose zero then gets no gradient);
- *   OC_POOL_AVG  y[i][c] = the sum over the K^3 taps / K^3 (sw unused).
- *   depth  1..depth of the tree.  ksize 3 or 5.
- *   x  dev f32 [N_l][c];  y dev f32 [N_l][c];  sw dev u8 [N_l][c] (max) or NULL. */
+/* General pooling (Sec. 3.2, last paragraph of "Pooling": pooling with other
+ * kernel or stride sizes finds the neighbouring octants as the convolution
+ * does and applies the pooling operation to them).  Over the K^3 taps k of
+ * the convolution's neighbourhood (index as the convolution's weights), where
+ * a neighbour that is not in the octree reads as 0, for every channel c:
+ *   OC_POOL_MAX  y = the maximum; sw = the tap of its first occurrence in tap
+ *                order, or 255 when that is an absent neighbour (whose zero
+ *                then gets no gradient);
+ *   OC_POOL_AVG  y = the sum over the K^3 taps / K^3 (sw unused).
+ *   depth   l, the input depth (1..depth of the tree).
+ *   ksize   3 or 5 (stride 1); 3 (stride 2^r).
+ *   stride  1: y, sw [N_l][c], one output per octant of depth l.
+ *           2^r, r = 1 .. l: y, sw [N_{l-r}][c]: evaluated where the
+ *             stride-2^r convolution is (the first depth-l position below
+ *             every non-empty depth-(l-r) octant, written to its row); rows
+ *             of empty depth-(l-r) octants get y = 0 and sw = 255.
+ *   x  dev f32 [N_l][c];  y dev f32;  sw dev u8 (max) or NULL (average). */
 #define OC_POOL_MAX 0
 #define OC_POOL_AVG 1
-oc_status oc_gpool_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t mode,
-                       const float* x, int32_t c, float* y, uint8_t* sw, hipStream_t stream);
+oc_status oc_gpool_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                       int32_t mode, const float* x, int32_t c, float* y, uint8_t* sw,
+                       hipStream_t stream);
 
-/* Gradient of oc_gpool_fwd: dx[n][c] = the sum, in tap order, over the octants
- * i whose tap k reaches n of dy[i][c] if sw[i][c] == k (max), or, for the
- * average, the sum of dy over n's own neighbourhood divided by K^3 (the same
- * octants: i reaches n at offset d exactly when n reaches i at -d; it is
- * the forward applied to dy).  A gather (no atomics): deterministic.
- *   dy dev f32 [N_l][c];  sw as produced by oc_gpool_fwd (max) or NULL;
+/* Gradient of oc_gpool_fwd: dx[n][c] = the sum over the outputs i whose tap k
+ * reaches n of dy[i][c] if sw[i][c] == k (max), or of dy[i][c] / K^3
+ * (average).  Stride 1: a gather in tap order (the average is the forward
+ * applied to dy: i reaches n at offset d exactly when n reaches i at -d).
+ * Stride 2: a gather per input row over its at most eight readers.  Stride
+ * 2^r, r >= 2: every input row has at most one reader, which writes it; the
+ * others are 0.  No atomics: deterministic.
+ *   dy dev f32, shaped as y;  sw as produced by oc_gpool_fwd (max) or NULL;
  *   dx dev f32 [N_l][c]. */
-oc_status oc_gpool_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t mode,
-                       const float* dy, const uint8_t* sw, int32_t c, float* dx,
+oc_status oc_gpool_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                       int32_t mode, const float* dy, const uint8_t* sw, int32_t c, float* dx,
                        hipStream_t stream);
 
 /* Profiling: the next launch, on the calling thread, of the kernel that does

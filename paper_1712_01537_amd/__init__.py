@@ -159,8 +159,8 @@ def load():
         "oc_deconv_bwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
         "oc_deconv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, sz, i32, p],
                           C.c_int),
-        "oc_gpool_fwd": ([p, i32, i32, i32, p, i32, p, p, p], C.c_int),
-        "oc_gpool_bwd": ([p, i32, i32, i32, p, p, i32, p, p], C.c_int),
+        "oc_gpool_fwd": ([p, i32, i32, i32, i32, p, i32, p, p, p], C.c_int),
+        "oc_gpool_bwd": ([p, i32, i32, i32, i32, p, p, i32, p, p], C.c_int),
         "oc_pool_fwd": ([p, i32, p, i32, p, p, p], C.c_int),
         "oc_pool_bwd": ([p, i32, p, p, i32, p, p, p], C.c_int),
         "oc_unpool_fwd": ([p, i32, p, p, i32, p, p], C.c_int),
@@ -570,26 +570,29 @@ def oc_unpool_bwd(tree: Octree, depth: int, dy: torch.Tensor, sw: torch.Tensor) 
     return dx
 
 
-def oc_gpool_fwd(tree: Octree, depth: int, ksize: int, mode: int, x: torch.Tensor):
-    """General stride-1 pooling over the K^3 neighbourhood (Sec. 3.2):
+def oc_gpool_fwd(tree: Octree, depth: int, ksize: int, mode: int, x: torch.Tensor,
+                 stride: int = 1):
+    """General pooling over the K^3 neighbourhood (Sec. 3.2), stride 1 or 2^r:
     (y, sw) for OC_POOL_MAX, (y, None) for OC_POOL_AVG."""
-    n = tree.num(depth)
+    r = int(stride).bit_length() - 1
+    n_in, n = tree.num(depth), tree.num(depth - r)
     c = x.shape[1]
     y = torch.empty((n, c), dtype=torch.float32, device=x.device)
     sw = (torch.empty((n, c), dtype=torch.uint8, device=x.device) if mode == OC_POOL_MAX
           else None)
-    _check(load().oc_gpool_fwd(tree.handle, depth, ksize, mode,
-                               _dev(x, "x", torch.float32, (n, c)), c, _dev(y, "y"),
+    _check(load().oc_gpool_fwd(tree.handle, depth, ksize, stride, mode,
+                               _dev(x, "x", torch.float32, (n_in, c)), c, _dev(y, "y"),
                                _dev(sw, "sw") if sw is not None else None, _stream()))
     return y, sw
 
 
 def oc_gpool_bwd(tree: Octree, depth: int, ksize: int, mode: int, dy: torch.Tensor,
-                 sw: torch.Tensor | None) -> torch.Tensor:
-    n = tree.num(depth)
+                 sw: torch.Tensor | None, stride: int = 1) -> torch.Tensor:
+    r = int(stride).bit_length() - 1
+    n_in, n = tree.num(depth), tree.num(depth - r)
     c = dy.shape[1]
-    dx = torch.empty((n, c), dtype=torch.float32, device=dy.device)
-    _check(load().oc_gpool_bwd(tree.handle, depth, ksize, mode,
+    dx = torch.empty((n_in, c), dtype=torch.float32, device=dy.device)
+    _check(load().oc_gpool_bwd(tree.handle, depth, ksize, stride, mode,
                                _dev(dy, "dy", torch.float32, (n, c)),
                                _dev(sw, "sw", torch.uint8, (n, c)) if sw is not None else None,
                                c, _dev(dx, "dx"), _stream()))

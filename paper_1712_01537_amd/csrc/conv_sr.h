@@ -6,6 +6,41 @@
 
 namespace oc {
 
+// Labels of the depths l-r+1 .. l-1 (lab[j] = depth l-r+1+j), the depths a
+// stride-2^r neighbourhood descends through.
+struct SrLabels {
+  const int32_t* lab[OC_MAX_DEPTH];
+};
+
+// First-child row (depth l) of the depth-(l-1) octant Q_o = 2^(r-1) P + a
+// (P: the coordinates of output p, a non-empty depth-(l-r) octant; a in
+// {-1, 0}^3, o = 4 [ax = 0] + 2 [ay = 0] + [az = 0]), or -1 when Q_o is not
+// in the octree or empty.  nbr: the group table of depth l-r+1 (the group of
+// p's children).  The 27 taps of the stride-2^r neighbourhood read children
+// of these eight octants (tap k: o = sr_tap_o(k), child sr_tap_c(k)).
+__device__ __forceinline__ int32_t sr_first_child(const int32_t* __restrict__ nbr,
+                                                  const SrLabels& L, int64_t p, int o, int r) {
+  const int ax = (o >> 2) & 1, ay = (o >> 1) & 1, az = o & 1;  // 1: offset 0, 0: offset -1
+  int32_t f = nbr[27 * p + ax * 9 + ay * 3 + az];  // first child (depth l-r+1) of p's neighbour
+  const int32_t cb = 4 * (1 - ax) + 2 * (1 - ay) + (1 - az);  // child 1 where a = -1
+  for (int j = 0; j < r - 1 && f >= 0; ++j) {
+    const int32_t lb = L.lab[j][f + cb];
+    f = lb > 0 ? 8 * (lb - 1) : -1;
+  }
+  return f;
+}
+__host__ __device__ constexpr int sr_tap_o(int k) {
+  return 4 * (k / 9 >= 1) + 2 * ((k / 3) % 3 >= 1) + (k % 3 >= 1);
+}
+__host__ __device__ constexpr int sr_tap_c(int k) {
+  return 4 * (k / 9 != 1) + 2 * ((k / 3) % 3 != 1) + (k % 3 != 1);
+}
+inline SrLabels sr_labels(const oc_octree* t, int l, int r) {
+  SrLabels L{};
+  for (int j = 0; j < r - 1; ++j) L.lab[j] = t->labels[l - r + 1 + j];
+  return L;
+}
+
 // Workspace bytes of the forward, and of the backward for the requested
 // gradients, at input depth l and stride 2^r (0 when nothing is needed).
 size_t conv_s2_fwd_ws(const oc_octree* t, int l, int r, int cin, int cout, bool bf16);

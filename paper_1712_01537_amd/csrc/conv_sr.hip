@@ -93,12 +93,8 @@ __device__ __forceinline__ v4f mma(v4u a, v4u b, v4f c, uint16_t) {
 
 // Tap k = 9 (dx+1) + 3 (dy+1) + (dz+1): the depth-(l-1) octant index o and
 // the child it reads (see the file comment).
-__host__ __device__ constexpr int tap_o(int k) {
-  return 4 * (k / 9 >= 1) + 2 * ((k / 3) % 3 >= 1) + (k % 3 >= 1);
-}
-__host__ __device__ constexpr int tap_c(int k) {
-  return 4 * (k / 9 != 1) + 2 * ((k / 3) % 3 != 1) + (k % 3 != 1);
-}
+__host__ __device__ constexpr int tap_o(int k) { return oc::sr_tap_o(k); }
+__host__ __device__ constexpr int tap_c(int k) { return oc::sr_tap_c(k); }
 
 // r = 1 input gradient: the j-th subset o of child class c (bits of j
 // deposited on the set bits of c), the tap c - 2o and the group-table column
@@ -124,26 +120,12 @@ __host__ __device__ constexpr int up_col(int o) {  // nbr column of parent offse
 }
 
 // ---------------------------------------------------------------------------
-// The table tab[p][o] (see the file comment).  lab[j] = labels of depth
-// l-r+1+j, j < r-1 (the depths between p's and the leaf depth l).
-struct Labels {
-  const int32_t* lab[OC_MAX_DEPTH];
-};
-
+// The table tab[p][o] (see the file comment).
 __global__ __launch_bounds__(TB) void k_sr_table(const int32_t* __restrict__ nbr, int64_t G, int r,
-                                                 Labels L, int32_t* __restrict__ tab) {
+                                                 oc::SrLabels L, int32_t* __restrict__ tab) {
   const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
   if (e >= G * 8) return;
-  const int64_t p = e >> 3;
-  const int o = (int)(e & 7);
-  const int ax = (o >> 2) & 1, ay = (o >> 1) & 1, az = o & 1;  // 1: offset 0, 0: offset -1
-  int32_t f = nbr[27 * p + ax * 9 + ay * 3 + az];  // first child (depth l-r+1) of N_a
-  const int32_t cb = 4 * (1 - ax) + 2 * (1 - ay) + (1 - az);  // child 1 where a = -1
-  for (int j = 0; j < r - 1 && f >= 0; ++j) {
-    const int32_t lb = L.lab[j][f + cb];
-    f = lb > 0 ? 8 * (lb - 1) : -1;
-  }
-  tab[e] = f;
+  tab[e] = oc::sr_first_child(nbr, L, e >> 3, (int)(e & 7), r);
 }
 
 // ---------------------------------------------------------------------------
@@ -632,11 +614,9 @@ Shape shape_of(const oc_octree* t, int l, int r) { return {t->M[l - r], t->N[l],
 size_t tab_bytes(const Shape& h) { return oc::align256((size_t)h.G * 8 * 4); }
 
 void build_table(const oc_octree* t, int l, int r, int32_t* tab, hipStream_t s) {
-  Labels L{};
-  for (int j = 0; j < r - 1; ++j) L.lab[j] = t->labels[l - r + 1 + j];
   const int64_t G = t->M[l - r];
   oc::launch(k_sr_table, dim3(grid_for(G * 8)), dim3(TB), 0, s, (const int32_t*)t->nbr[l - r + 1],
-             G, r, L, tab);
+             G, r, oc::sr_labels(t, l, r), tab);
 }
 
 // Ranges of the weight gradient's outputs: enough work items to fill the GPU

@@ -1,6 +1,7 @@
 // 2x2x2 max-pooling and max-unpooling across depths through the label
 // buffer (Sec. 3.2 "Pooling" and "Unpooling", Fig. 5 of O-CNN), and general
-// stride-1 pooling over the convolution's neighbourhood (k_gpool_*, below).
+// pooling over the convolution's neighbourhood, stride 1 (k_gpool_*) and
+// stride 2^r (k_gpool_sr_*), below.
 //
 // The eight children of the non-empty octant with label p occupy rows
 // 8(p-1)..8(p-1)+7 of the finer depth, so pooling is a max over 8 contiguous
@@ -10,6 +11,7 @@
 // row; a wavefront therefore streams whole rows (coalesced), and the eight
 // child rows it reads are one contiguous 8*C*4-byte span.
 #include "common.h"
+#include "conv_sr.h"
 
 namespace {
 
@@ -276,6 +278,150 @@ __global__ __launch_bounds__(TB) void k_gpool_bwd(const int32_t* __restrict__ nb
   reinterpret_cast<F*>(dx)[t] = acc;
 }
 
+// Strided general pooling (stride 2^r, K = 3): the neighbourhood of the
+// stride-2^r convolution (the first depth-l position below every non-empty
+// depth-(l-r) octant, its 27 taps reading children of the eight depth-(l-1)
+// octants of sr_first_child), absent neighbours as zeros.  Forward: one
+// thread per (depth-(l-r) row, VEC channels); rows of empty octants get 0
+// and switch 255.
+template <bool AVG, int VEC>
+__global__ __launch_bounds__(TB) void k_gpool_sr_fwd(const int32_t* __restrict__ nbr,
+                                                     oc::SrLabels L, int r,
+                                                     const int32_t* __restrict__ labels,
+                                                     int64_t n_out, const float* __restrict__ x,
+                                                     int cv, float* __restrict__ y,
+                                                     uint8_t* __restrict__ sw) {
+  using F = typename Vec<VEC>::f;
+  using U = typename Vec<VEC>::u8;
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= n_out * cv) return;
+  const int64_t i = t / cv;
+  const int q = (int)(t - i * cv);
+  const F* xv = reinterpret_cast<const F*>(x);
+  F acc;
+  U arg;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) set(acc, e, 0.f), set(arg, e, (uint8_t)255);
+  const int32_t lab = labels[i];
+  if (lab > 0) {
+    int32_t fc[8];
+#pragma unroll
+    for (int o = 0; o < 8; ++o) fc[o] = oc::sr_first_child(nbr, L, lab - 1, o, r);
+    F v[27];
+#pragma unroll
+    for (int k = 0; k < 27; ++k) {
+      const int32_t f = fc[oc::sr_tap_o(k)];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) set(v[k], e, 0.f);
+      if (f >= 0) v[k] = xv[((int64_t)f + oc::sr_tap_c(k)) * cv + q];
+    }
+#pragma unroll
+    for (int k = 0; k < 27; ++k) {
+      const bool present = fc[oc::sr_tap_o(k)] >= 0;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float a = comp(v[k], e);
+        if constexpr (AVG) {
+          set(acc, e, comp(acc, e) + a);
+        } else if (k == 0 || a > comp(acc, e)) {
+          set(acc, e, a);
+          set(arg, e, present ? (uint8_t)k : (uint8_t)255);
+        }
+      }
+    }
+    if constexpr (AVG) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) set(acc, e, comp(acc, e) / 27.f);
+    }
+  }
+  if constexpr (!AVG) reinterpret_cast<U*>(sw)[t] = arg;
+  reinterpret_cast<F*>(y)[t] = acc;
+}
+
+// Backward, r = 1, as a gather: depth-l row 8h + c (child c of group h) is
+// read by the outputs at parent offsets o in {0,1}^3 from h's parent with
+// o_a <= c_a, through tap c - 2o (the strided convolution's input-gradient
+// rule); their contributions are added in increasing o.
+template <bool AVG, int VEC>
+__global__ __launch_bounds__(TB) void k_gpool_s2_bwd(const int32_t* __restrict__ nbr, int64_t n_in,
+                                                     const int32_t* __restrict__ rows,
+                                                     const float* __restrict__ dy,
+                                                     const uint8_t* __restrict__ sw, int cv,
+                                                     float* __restrict__ dx) {
+  using F = typename Vec<VEC>::f;
+  using U = typename Vec<VEC>::u8;
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= n_in * cv) return;
+  const int64_t n = t / cv;
+  const int q = (int)(t - n * cv);
+  const int c = (int)(n & 7);
+  const int64_t h = n >> 3;
+  const F* gv = reinterpret_cast<const F*>(dy);
+  const U* sv = reinterpret_cast<const U*>(sw);
+  F acc;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) set(acc, e, 0.f);
+#pragma unroll
+  for (int o = 0; o < 8; ++o) {
+    if ((o & ~c) != 0) continue;
+    const int32_t f = nbr[27 * h + ((o >> 2) + 1) * 9 + (((o >> 1) & 1) + 1) * 3 + ((o & 1) + 1)];
+    if (f < 0) continue;
+    int k = 0;
+#pragma unroll
+    for (int a = 2; a >= 0; --a) k = 3 * k + (((c >> a) & 1) - 2 * ((o >> a) & 1) + 1);
+    const int64_t row = rows[f >> 3];
+    const F g = gv[row * cv + q];
+    if constexpr (AVG) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) set(acc, e, comp(acc, e) + comp(g, e) / 27.f);
+    } else {
+      const U sgl = sv[row * cv + q];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e)
+        if (comp(sgl, e) == k) set(acc, e, comp(acc, e) + comp(g, e));
+    }
+  }
+  reinterpret_cast<F*>(dx)[t] = acc;
+}
+
+// Backward, r >= 2: every depth-l row is read by at most one (output, tap),
+// so each output scatters its taps' shares over a zeroed dx.
+template <bool AVG, int VEC>
+__global__ __launch_bounds__(TB) void k_gpool_sr_bwd(const int32_t* __restrict__ nbr,
+                                                     oc::SrLabels L, int r, int64_t G,
+                                                     const int32_t* __restrict__ rows,
+                                                     const float* __restrict__ dy,
+                                                     const uint8_t* __restrict__ sw, int cv,
+                                                     float* __restrict__ dx) {
+  using F = typename Vec<VEC>::f;
+  using U = typename Vec<VEC>::u8;
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= G * cv) return;
+  const int64_t p = t / cv;
+  const int q = (int)(t - p * cv);
+  const int64_t row = rows[p];
+  const F g = reinterpret_cast<const F*>(dy)[row * cv + q];
+  U sgl;
+  if constexpr (!AVG) sgl = reinterpret_cast<const U*>(sw)[row * cv + q];
+  int32_t fc[8];
+#pragma unroll
+  for (int o = 0; o < 8; ++o) fc[o] = oc::sr_first_child(nbr, L, p, o, r);
+#pragma unroll
+  for (int k = 0; k < 27; ++k) {
+    const int32_t f = fc[oc::sr_tap_o(k)];
+    if (f < 0) continue;
+    F v;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      if constexpr (AVG)
+        set(v, e, comp(g, e) / 27.f);
+      else
+        set(v, e, comp(sgl, e) == k ? comp(g, e) : 0.f);
+    }
+    reinterpret_cast<F*>(dx)[((int64_t)f + oc::sr_tap_c(k)) * cv + q] = v;
+  }
+}
+
 oc_status check_common(const oc_octree* t, int32_t l, int32_t c, const void* a, const void* b,
                        const void* s, const char* who) {
   oc_status st = oc::check_tree_level(t, l, 1);
@@ -290,19 +436,61 @@ bool vec4_ok(int c, const void* a, const void* b, const void* s) {
          ((uintptr_t)s % 4 == 0);
 }
 
+// Strided general pooling: forward over the depth-(l-r) rows; backward by
+// the r = 1 gather or the r >= 2 scatter.
 template <bool BWD>
-oc_status gpool(const oc_octree* t, int32_t l, int32_t K, int32_t mode, const float* in,
-                const uint8_t* swin, uint8_t* swout, int32_t c, float* out, hipStream_t s,
-                const char* who) {
+oc_status gpool_sr(const oc_octree* t, int32_t l, int32_t r, bool avg, const float* in,
+                   const uint8_t* swin, uint8_t* swout, int32_t c, float* out, hipStream_t s) {
+  const int64_t n_in = t->N[l], n_out = t->N[l - r], G = t->M[l - r];
+  const uint8_t* swp = BWD ? swin : swout;
+  const bool v4 = c % 4 == 0 && (uintptr_t)in % 16 == 0 && (uintptr_t)out % 16 == 0 &&
+                  (avg || (uintptr_t)swp % 4 == 0);
+  const int cv = v4 ? c / 4 : c;
+  const int32_t* nbr = (const int32_t*)t->nbr[l - r + 1];
+  const oc::SrLabels L = oc::sr_labels(t, l, r);
+#define OC_GPS(AVG_, V_)                                                                        \
+  if (avg == AVG_ && (v4 ? 4 : 1) == V_) {                                                      \
+    if constexpr (!BWD) {                                                                       \
+      if (n_out > 0)                                                                            \
+        oc::launch_main(k_gpool_sr_fwd<AVG_, V_>, dim3(grid_for(n_out * cv)), dim3(TB), s, nbr, \
+                        L, r, (const int32_t*)t->labels[l - r], n_out, in, cv, out, swout);     \
+    } else if (r == 1) {                                                                        \
+      if (n_in > 0)                                                                             \
+        oc::launch_main(k_gpool_s2_bwd<AVG_, V_>, dim3(grid_for(n_in * cv)), dim3(TB), s,       \
+                        (const int32_t*)t->nbr[l], n_in, (const int32_t*)t->rows[l - 1], in,    \
+                        swin, cv, out);                                                         \
+    } else {                                                                                    \
+      if (n_in > 0) oc::fill_u32(out, 0u, n_in * c, s);                                         \
+      if (G > 0)                                                                                \
+        oc::launch_main(k_gpool_sr_bwd<AVG_, V_>, dim3(grid_for(G * cv)), dim3(TB), s, nbr, L,  \
+                        r, G, (const int32_t*)t->rows[l - r], in, swin, cv, out);               \
+    }                                                                                           \
+  }
+  OC_GPS(false, 4) OC_GPS(false, 1) OC_GPS(true, 4) OC_GPS(true, 1)
+#undef OC_GPS
+  OC_LAUNCH_CHECK();
+  return OC_OK;
+}
+
+template <bool BWD>
+oc_status gpool(const oc_octree* t, int32_t l, int32_t K, int32_t stride, int32_t mode,
+                const float* in, const uint8_t* swin, uint8_t* swout, int32_t c, float* out,
+                hipStream_t s, const char* who) {
   oc_status st = oc::check_tree_level(t, l, 1);
   if (st != OC_OK) return st;
   if (K != 3 && K != 5) return oc::fail(OC_ERR_UNSUPPORTED, "%s: kernel size %d not 3 or 5", who, K);
+  if (stride < 1 || (stride & (stride - 1)) != 0 || stride > (1 << l))
+    return oc::fail(OC_ERR_ARG, "%s: stride %d not a power of two up to 2^depth", who, stride);
+  if (stride > 1 && K != 3)
+    return oc::fail(OC_ERR_UNSUPPORTED, "%s: stride %d supports kernel size 3 only", who, stride);
   if (mode != OC_POOL_MAX && mode != OC_POOL_AVG)
     return oc::fail(OC_ERR_ARG, "%s: mode %d not OC_POOL_MAX or OC_POOL_AVG", who, mode);
   if (c < 1 || c > 65536) return oc::fail(OC_ERR_ARG, "%s: channels %d out of range", who, c);
   const bool avg = mode == OC_POOL_AVG;
   const uint8_t* swp = BWD ? swin : swout;
   if (!in || !out || (!avg && !swp)) return oc::fail(OC_ERR_ARG, "%s: NULL buffer", who);
+  if (stride > 1)
+    return gpool_sr<BWD>(t, l, __builtin_ctz((unsigned)stride), avg, in, swin, swout, c, out, s);
   const int64_t n = t->N[l];
   if (n == 0) return OC_OK;
   const bool v4 = c % 4 == 0 && (uintptr_t)in % 16 == 0 && (uintptr_t)out % 16 == 0 &&
@@ -404,14 +592,16 @@ oc_status oc_unpool_bwd(const oc_octree* t, int32_t l, const float* dy, const ui
   return OC_OK;
 }
 
-oc_status oc_gpool_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t mode, const float* x,
+oc_status oc_gpool_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, int32_t mode,
+                       const float* x,
                        int32_t c, float* y, uint8_t* sw, hipStream_t s) {
-  return gpool<false>(t, l, K, mode, x, nullptr, sw, c, y, s, "oc_gpool_fwd");
+  return gpool<false>(t, l, K, stride, mode, x, nullptr, sw, c, y, s, "oc_gpool_fwd");
 }
 
-oc_status oc_gpool_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t mode, const float* dy,
+oc_status oc_gpool_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, int32_t mode,
+                       const float* dy,
                        const uint8_t* sw, int32_t c, float* dx, hipStream_t s) {
-  return gpool<true>(t, l, K, mode, dy, sw, nullptr, c, dx, s, "oc_gpool_bwd");
+  return gpool<true>(t, l, K, stride, mode, dy, sw, nullptr, c, dx, s, "oc_gpool_bwd");
 }
 
 }  // extern "C"

@@ -23,7 +23,8 @@ wide_d7     7      16     100k      conv5 64->64 @7 (bf16 and fp32), stride-2 co
 seg_d6      6      32     20k       conv3+ReLU+pool 3->16 @6, 16->32 @5; stride-2 deconv3 32->16
                                     d4->d5; unpool d5->d6; deconv3 16->16 @6
 gpool_d6    6      32     20k       conv3+ReLU 3->16 @6; 3x3x3 max-pool and 5x5x5 average-pool,
-                                    stride 1, @6; 2x2x2 max-pool d6->d5
+                                    stride 1, @6; 2x2x2 max-pool d6->d5; 3x3x3 max-pool
+                                    stride 2 d5->d4; 3x3x3 average-pool stride 4 d4->d2
 s4_d6       6      32     20k       conv3+ReLU 3->16 @6; stride-4 conv3+ReLU 16->64 d6->d4;
                                     conv3 64->128 @4
 ==========  =====  =====  ========  ===============================================
@@ -139,6 +140,8 @@ WORKLOADS = {
             Layer("gpool", 6, 16, 16, ksize=3, mode="max"),
             Layer("gpool", 6, 16, 16, ksize=5, mode="avg"),
             Layer("pool", 6, 16, 16),
+            Layer("gpool", 5, 16, 16, ksize=3, stride=2, mode="max"),
+            Layer("gpool", 4, 16, 16, ksize=3, stride=4, mode="avg"),
         ),
     ),
     "s4_d6": Workload(

@@ -54,8 +54,8 @@ def test_argument_errors_without_device():
     assert L.oc_deconv_bwd(None, 1, 3, 1, 0, None, 4, None, 3, None, None, None, None, 0, 0,
                            None) == 1
     assert L.oc_deconv_fwd_workspace(None, 1, 3, 1, 0, 4, 3) == 0
-    assert L.oc_gpool_fwd(None, 1, 3, 0, None, 4, None, None, None) == 1
-    assert L.oc_gpool_bwd(None, 1, 3, 1, None, None, 4, None, None) == 1
+    assert L.oc_gpool_fwd(None, 1, 3, 1, 0, None, 4, None, None, None) == 1
+    assert L.oc_gpool_bwd(None, 1, 3, 1, 1, None, None, 4, None, None) == 1
     assert L.oc_octree_signal(None) is None
     assert L.oc_status_str(2) == b"point outside the unit cube"
     L.oc_octree_free(None)

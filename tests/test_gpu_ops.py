@@ -303,44 +303,57 @@ def test_conv_bf16_matrix_core(seed, B, n, depth, K, cin, cout, relu):
     assert torch.equal(dx, dx2) and torch.equal(dw, dw2)
 
 
-GPOOL_SMALL = [  # seed, B, n, depth, K, c, relu (inputs through a ReLU: exact zeros, ties)
-    (91, 2, 400, 4, 3, 16, False),
-    (92, 3, 300, 4, 5, 5, False),
-    (93, 1, 800, 5, 3, 7, True),
-    (94, 2, 500, 4, 5, 32, True),
+GPOOL_SMALL = [  # seed, B, n, depth, K, stride, c, relu (inputs through a ReLU: exact zeros, ties)
+    (91, 2, 400, 4, 3, 1, 16, False),
+    (92, 3, 300, 4, 5, 1, 5, False),
+    (93, 1, 800, 5, 3, 1, 7, True),
+    (94, 2, 500, 4, 5, 1, 32, True),
+    (95, 2, 600, 5, 3, 2, 16, False),
+    (96, 3, 500, 4, 3, 2, 7, True),
+    (97, 2, 700, 5, 3, 4, 12, True),
+    (98, 2, 700, 5, 3, 8, 5, False),
+    (99, 1, 400, 4, 3, 16, 8, True),  # depth 4 -> the roots
 ]
 
 
-@pytest.mark.parametrize("seed,B,n,depth,K,c,relu", GPOOL_SMALL)
-def test_gpool_small(seed, B, n, depth, K, c, relu):
+@pytest.mark.parametrize("seed,B,n,depth,K,stride,c,relu", GPOOL_SMALL)
+def test_gpool_small(seed, B, n, depth, K, stride, c, relu):
     oc = _oc()
-    print(f"[gpool] seed={seed} B={B} d={depth} K={K} c={c} relu={relu}", flush=True)
+    print(f"[gpool] seed={seed} B={B} d={depth} K={K} s={stride} c={c} relu={relu}", flush=True)
     pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
     ref, tree = _trees(pts, nrm, offs, depth)
     l = depth
+    r = stride.bit_length() - 1
     rng = np.random.default_rng(seed)
     x = rng.standard_normal((ref.num(l), c)).astype(np.float32)
     if relu:
         x = np.maximum(x, 0)
-    dy = rng.standard_normal((ref.num(l), c)).astype(np.float32)
-    nb = ref.neighbors(l, K)
+    dy = rng.standard_normal((ref.num(l - r), c)).astype(np.float32)
+    if stride == 1:
+        nb = ref.neighbors(l, K)
+        fwd = lambda a, m: oracle.gpool_fwd(nb, a, m)  # noqa: E731
+        bwd = lambda g, s_, m: oracle.gpool_bwd(nb, g, s_, ref.num(l), m)  # noqa: E731
+    else:
+        fwd = lambda a, m: oracle.gpool_sr_fwd(ref, l, a, m, stride)  # noqa: E731
+        bwd = lambda g, s_, m: oracle.gpool_sr_bwd(ref, l, g, s_, ref.num(l), m, stride)  # noqa: E731
     # max: values and switches bit-exact, the gradient within the fp32 rule
-    y, sw = oc.oc_gpool_fwd(tree, l, K, oc.OC_POOL_MAX, _cuda(x))
-    yr, swr = oracle.gpool_fwd(nb, x, oracle.POOL_MAX)
+    y, sw = oc.oc_gpool_fwd(tree, l, K, oc.OC_POOL_MAX, _cuda(x), stride=stride)
+    yr, swr = fwd(x, oracle.POOL_MAX)
     np.testing.assert_array_equal(y.cpu().numpy(), yr)
     np.testing.assert_array_equal(sw.cpu().numpy(), swr)
-    dx = oc.oc_gpool_bwd(tree, l, K, oc.OC_POOL_MAX, _cuda(dy), sw)
-    assert_f32_close(dx.cpu().numpy(), oracle.gpool_bwd(nb, dy, swr, ref.num(l), oracle.POOL_MAX),
-                     "max dx")
+    dx = oc.oc_gpool_bwd(tree, l, K, oc.OC_POOL_MAX, _cuda(dy), sw, stride=stride)
+    assert_f32_close(dx.cpu().numpy(), bwd(dy, swr, oracle.POOL_MAX), "max dx")
     # average
-    ya, _ = oc.oc_gpool_fwd(tree, l, K, oc.OC_POOL_AVG, _cuda(x))
-    assert_f32_close(ya.cpu().numpy(), oracle.gpool_fwd(nb, x, oracle.POOL_AVG)[0], "avg y")
-    dxa = oc.oc_gpool_bwd(tree, l, K, oc.OC_POOL_AVG, _cuda(dy), None)
-    assert_f32_close(dxa.cpu().numpy(), oracle.gpool_bwd(nb, dy, None, ref.num(l), oracle.POOL_AVG),
-                     "avg dx")
+    ya, _ = oc.oc_gpool_fwd(tree, l, K, oc.OC_POOL_AVG, _cuda(x), stride=stride)
+    assert_f32_close(ya.cpu().numpy(), fwd(x, oracle.POOL_AVG)[0], "avg y")
+    dxa = oc.oc_gpool_bwd(tree, l, K, oc.OC_POOL_AVG, _cuda(dy), None, stride=stride)
+    assert_f32_close(dxa.cpu().numpy(), bwd(dy, None, oracle.POOL_AVG), "avg dx")
     # deterministic
-    dx2 = oc.oc_gpool_bwd(tree, l, K, oc.OC_POOL_MAX, _cuda(dy), sw)
+    dx2 = oc.oc_gpool_bwd(tree, l, K, oc.OC_POOL_MAX, _cuda(dy), sw, stride=stride)
     assert torch.equal(dx.view(torch.int32), dx2.view(torch.int32))
+    if stride > 1:
+        with pytest.raises(oc.OcError):  # strided pooling takes K = 3 only
+            oc.oc_gpool_fwd(tree, l, 5, oc.OC_POOL_MAX, _cuda(x), stride=stride)
 
 
 @pytest.mark.parametrize("seed,B,n,depth,c", [(31, 2, 500, 4, 8), (32, 3, 300, 5, 3), (33, 1, 100, 3, 32)])
@@ -605,15 +618,20 @@ def test_workload_full_size(name):
             _check_deconv_full(ref, tree, l, L.ksize, L.stride, x, w, dy, f"{name}/{li}")
         elif L.op == "gpool":
             x = np.maximum(synth.make_features([w_.seed_id, 3000 + li], ref.num(l), L.cin), 0)
-            nb = ref.neighbors(l, L.ksize)
-            print(f"[{name}/{li}] gpool {L.mode} K{L.ksize} d{l} C{L.cin}", flush=True)
+            r = L.stride.bit_length() - 1
+            print(f"[{name}/{li}] gpool {L.mode} K{L.ksize} s{L.stride} d{l} C{L.cin}", flush=True)
             mode = oc.OC_POOL_MAX if L.mode == "max" else oc.OC_POOL_AVG
             rmode = oracle.POOL_MAX if L.mode == "max" else oracle.POOL_AVG
-            y, sw = oc.oc_gpool_fwd(tree, l, L.ksize, mode, _cuda(x))
-            yr, swr = oracle.gpool_fwd(nb, x, rmode)
-            dy = synth.make_upstream(w_, li, ref.num(l), L.cin)
-            dx = oc.oc_gpool_bwd(tree, l, L.ksize, mode, _cuda(dy), sw)
-            dxr = oracle.gpool_bwd(nb, dy, swr, ref.num(l), rmode)
+            y, sw = oc.oc_gpool_fwd(tree, l, L.ksize, mode, _cuda(x), stride=L.stride)
+            dy = synth.make_upstream(w_, li, ref.num(l - r), L.cin)
+            dx = oc.oc_gpool_bwd(tree, l, L.ksize, mode, _cuda(dy), sw, stride=L.stride)
+            if r == 0:
+                nb = ref.neighbors(l, L.ksize)
+                yr, swr = oracle.gpool_fwd(nb, x, rmode)
+                dxr = oracle.gpool_bwd(nb, dy, swr, ref.num(l), rmode)
+            else:
+                yr, swr = oracle.gpool_sr_fwd(ref, l, x, rmode, L.stride)
+                dxr = oracle.gpool_sr_bwd(ref, l, dy, swr, ref.num(l), rmode, L.stride)
             if L.mode == "max":
                 np.testing.assert_array_equal(y.cpu().numpy(), yr)
                 np.testing.assert_array_equal(sw.cpu().numpy(), swr)
