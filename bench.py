@@ -91,6 +91,13 @@ BOUND = {
     "unpool_bwd": "hbm",
     "gpool_fwd": "hbm",
     "gpool_bwd": "hbm",
+    "bn_fwd": "hbm",
+    "bn_bwd": "hbm",
+    "fc_fwd": "hbm",
+    "fc_bwd": "hbm",
+    "dropout": "hbm",
+    "softmax": "hbm",
+    "sgd": "hbm",
     "build": "hbm",
     "build_emit": "hbm",
 }
@@ -414,6 +421,8 @@ class Accounting:
                     + 16 * N[d] + sum(108 * M[k - 1] for k in range(1, d + 1)))
         if tag.startswith(("conv", "deconv")):
             return 2 * self._n_conv(L) * L.ksize ** 3 * L.cin * L.cout
+        if L is None:  # the head and the update: small, counted as their bytes
+            return self.head_bytes(tag)
         l, c = L.depth, L.cin
         if tag == "pool_fwd":
             return N[l] * c * 4 + N[l - 1] * 4 + N[l - 1] * c * 4 + M[l - 1] * c
@@ -423,6 +432,10 @@ class Accounting:
             return M[l - 1] * c * 5 + M[l - 1] * 4 + N[l] * c * 4
         if tag == "unpool_bwd":  # the routed child of each (parent, channel) in, parent rows out
             return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l - 1] * c * 4
+        if tag == "bn_fwd":  # two statistics passes over z, then z in and y out
+            return N[l] * L.cout * 4 * 4
+        if tag == "bn_bwd":  # z and dy in for the sums, then z, dy in and dx out
+            return N[l] * L.cout * 4 * 5
         if tag in ("gpool_fwd", "gpool_bwd"):
             r = L.stride.bit_length() - 1
             if r == 0:  # rows in and out, switches (max), 27 ints per group
@@ -433,6 +446,23 @@ class Accounting:
                     + N[l - r] * 4 + M[l - r] * 32)
         return 0
 
+
+    def head_bytes(self, tag):
+        """Bytes per launch of the classification head's ops and of the SGD
+        update (a rough count for ops of a few microseconds)."""
+        wl = self.wl
+        if not getattr(wl, "train", False):
+            return 0
+        B, c2 = wl.batch, wl.layers[-1].cout
+        if tag == "sgd":  # w, g, v in; w, v out: all parameters over the two launches / 2
+            n = sum(27 * L.cin * L.cout + 2 * L.cout for L in wl.layers)
+            n += 8 * c2 * 128 + 128 + 128 * wl.classes + wl.classes
+            return 5 * 4 * n // 2
+        if tag in ("fc_fwd", "fc_bwd"):
+            return 4 * (B * 8 * c2 + 8 * c2 * 128 + B * 128) // 2
+        if tag == "dropout":
+            return 9 * B * (8 * c2 + 128) // 2
+        return 4 * B * wl.classes * 2  # softmax
 
     def op_class(self, tag):
         """Op class of a tag: the build's two halves are one class."""
@@ -519,6 +549,8 @@ class Step(Accounting):
         k = self.key(tag, li)
         if self.calls is not None and not tag.startswith("build"):
             # every kernel of the call, each bracketed by its own events
+            if len(self.calls) == len(self.call_pool):
+                self.call_pool.append(self.oc.CallProfile(32))
             prof = self.call_pool[len(self.calls)]
             prof.arm()
             try:
@@ -711,6 +743,111 @@ class Step(Accounting):
         return out
 
 
+class TrainStep(Step):
+    """One O-CNN(d) classification training iteration (Sec. 4 "Network
+    structure", Sec. 5 "Training details") on the octree built during the
+    previous step: units U_d .. U_2 (conv, batch normalisation with the ReLU
+    fused, 2x2x2 max-pool), the depth-1 features of each shape (8 C_2 values)
+    through dropout, FC(128), dropout, FC(classes), softmax cross-entropy on
+    synthetic labels; the backward of all of it; one SGD step with momentum
+    0.9, weight decay 5e-4 (convolution and FC weights) and learning rate 0.1.
+    The parameters live in two flat buffers (with and without weight decay),
+    as do their gradients and velocities, so the update is two launches."""
+
+    P_DROP, LR, MOMENTUM, DECAY = 0.5, 0.1, 0.9, 5e-4
+
+    def __init__(self, oc, torch, synth, wl):
+        super().__init__(oc, torch, synth, wl)
+        d = synth.make_train_inputs(wl)
+        dev = "cuda"
+
+        def T(a):
+            return torch.as_tensor(a).to(dev)
+
+        self.labels, self.keep1, self.keep2 = T(d["labels"]), T(d["keep1"]), T(d["keep2"])
+        # flat buffers: decayed = conv weights, fc1_w, fc2_w; plain = gammas, betas, biases
+        dec = [self.weights[li] for li in range(len(wl.layers))] + [T(d["fc1_w"]), T(d["fc2_w"])]
+        pla = [T(a) for g_b in d["bn"] for a in g_b] + [T(d["fc1_b"]), T(d["fc2_b"])]
+        self.flat = {}
+        views = {}
+        for key, lst in (("dec", dec), ("pla", pla)):
+            n = sum(t.numel() for t in lst)
+            buf = {k: torch.zeros(n, dtype=torch.float32, device=dev) for k in ("w", "g", "v")}
+            off, vs = 0, []
+            for t in lst:
+                sl = slice(off, off + t.numel())
+                buf["w"][sl].copy_(t.reshape(-1))
+                vs.append({k: buf[k][sl].view(t.shape) for k in ("w", "g", "v")})
+                off += t.numel()
+            self.flat[key] = buf
+            views[key] = vs
+        nl = len(wl.layers)
+        self.conv_p = views["dec"][:nl]
+        self.fc1_w, self.fc2_w = views["dec"][nl], views["dec"][nl + 1]
+        self.gamma = [views["pla"][2 * i] for i in range(nl)]
+        self.beta = [views["pla"][2 * i + 1] for i in range(nl)]
+        self.fc1_b, self.fc2_b = views["pla"][2 * nl], views["pla"][2 * nl + 1]
+        for li in range(nl):
+            self.weights[li] = self.conv_p[li]["w"]
+        self.loss = None
+
+    def network(self, tree):
+        oc, wl, torch, P = self.oc, self.wl, self.torch, self.P_DROP
+        rec = self.record
+        x = tree.signal()
+        units = []
+        for li, L in enumerate(wl.layers):
+            w = self.conv_p[li]["w"]
+            z = self._run("conv_fwd", li, lambda: oc.oc_conv_fwd(tree, L.depth, 3, 1, x, w))
+            a, mean, invstd = self._run("bn_fwd", li, lambda: oc.oc_bn_fwd(
+                z, self.gamma[li]["w"], self.beta[li]["w"], relu=True))
+            p, sw = self._run("pool_fwd", li, lambda: oc.oc_pool_fwd(tree, L.depth, a))
+            units.append((li, x, z, a, mean, invstd, p, sw))
+            x = p
+        feat = x.view(wl.batch, -1)
+        h0 = self._run("dropout", None, lambda: oc.oc_dropout(feat, self.keep1, P))
+        h1 = self._run("fc_fwd", None, lambda: oc.oc_fc_fwd(h0, self.fc1_w["w"], self.fc1_b["w"]))
+        h2 = self._run("dropout", None, lambda: oc.oc_dropout(h1, self.keep2, P))
+        zl = self._run("fc_fwd", None, lambda: oc.oc_fc_fwd(h2, self.fc2_w["w"], self.fc2_b["w"]))
+        loss, dz = self._run("softmax", None, lambda: oc.oc_softmax_ce(zl, self.labels))
+        dh2, _, _ = self._run("fc_bwd", None, lambda: oc.oc_fc_bwd(
+            h2, self.fc2_w["w"], dz, dw=self.fc2_w["g"], db=self.fc2_b["g"]))
+        dh1 = self._run("dropout", None, lambda: oc.oc_dropout(dh2, self.keep2, P))
+        dh0, _, _ = self._run("fc_bwd", None, lambda: oc.oc_fc_bwd(
+            h0, self.fc1_w["w"], dh1, dw=self.fc1_w["g"], db=self.fc1_b["g"]))
+        g = self._run("dropout", None, lambda: oc.oc_dropout(dh0, self.keep1, P)).view(x.shape)
+        if rec is not None:
+            rec.update(units=units, feat=feat, h0=h0, h1=h1, h2=h2, logits=zl, loss=loss,
+                       dlogits=dz, dh1=dh1, dfeat=g, bwd={})
+        for li, xin, z, a, mean, invstd, p, sw in reversed(units):
+            L = wl.layers[li]
+            w = self.conv_p[li]["w"]
+            g_in = g
+            # the ReLU's backward rides on the routing (the pooled output)
+            da = self._run("pool_bwd", li, lambda: oc.oc_pool_bwd(tree, L.depth, g, sw, y=p))
+            dz_, _, _ = self._run("bn_bwd", li, lambda: oc.oc_bn_bwd(
+                z, da, self.gamma[li]["w"], mean, invstd, dgamma=self.gamma[li]["g"],
+                dbeta=self.beta[li]["g"]))
+            dx = None
+            if li > 0:  # the signal needs no gradient
+                dx, _ = self._run("conv_bwd_data", li, lambda: oc.oc_conv_bwd(
+                    tree, L.depth, 3, 1, xin, w, dz_, need_dx=True, need_dw=False))
+            self._run("conv_bwd_weight", li, lambda: oc.oc_conv_bwd(
+                tree, L.depth, 3, 1, xin, w, dz_, need_dx=False, need_dw=True,
+                dw_out=self.conv_p[li]["g"]))
+            if rec is not None:
+                rec["bwd"][li] = (g_in, da, dz_, dx)
+            g = dx
+        if rec is not None:  # parameters and velocities before the update
+            rec["before"] = {k: {q: b[q].clone() for q in ("w", "v")} for k, b in self.flat.items()}
+        for key, dec in (("dec", self.DECAY), ("pla", 0.0)):
+            b = self.flat[key]
+            self._run("sgd", None, lambda: oc.oc_sgd(b["w"], b["g"], b["v"], self.LR,
+                                                     self.MOMENTUM, dec))
+        self.loss = loss
+        return loss
+
+
 def oracle_step(synth, wl, shapes):
     """The oracle on the first `shapes` shapes of the batch: build, neighbour
     search and the network's forward and backward.  Returns (algorithmic conv
@@ -796,6 +933,30 @@ def oracle_step(synth, wl, shapes):
     return flops, time.perf_counter() - t0
 
 
+def oracle_train_step(synth, wl, shapes):
+    """The oracle's O-CNN(d) training iteration (oracle/train.py) on the first
+    `shapes` shapes: build, forward, backward, SGD.  (conv flops, seconds)."""
+    import numpy as np
+
+    import oracle
+    from oracle import train as T
+
+    pts, nrm, offs = synth.make_points(wl, batch=shapes)
+    d = synth.make_train_inputs(wl, batch=shapes)
+    params = []
+    for li, L in enumerate(wl.layers):
+        params += [synth.make_weights(wl, li, 3, L.cin, L.cout), d["bn"][li][0], d["bn"][li][1]]
+    params += [d["fc1_w"], d["fc1_b"], d["fc2_w"], d["fc2_b"]]
+    params = [np.asarray(q, np.float64) for q in params]
+    vel = [np.zeros_like(q) for q in params]
+    t0 = time.perf_counter()
+    ref = oracle.Octree(pts, nrm, offs, wl.depth, wl.full_depth)
+    T.ocnn_step(ref, params, vel, d["labels"], d["keep1"], d["keep2"])
+    flops = sum((6 if li > 0 else 4) * ref.num(L.depth) * 27 * L.cin * L.cout
+                for li, L in enumerate(wl.layers))
+    return flops, time.perf_counter() - t0
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as fh:
@@ -816,7 +977,8 @@ def cpu_baseline(synth, wl, max_shapes, budget_s=4.0):
     import oracle
 
     threads = oracle.num_threads()
-    f1, t1 = oracle_step(synth, wl, 1)  # warm-up (page faults, thread start)
+    run = oracle_train_step if wl.train else oracle_step
+    f1, t1 = run(synth, wl, 1)  # warm-up (page faults, thread start)
 
     def leg(nthr):
         oracle.set_num_threads(nthr)
@@ -824,7 +986,7 @@ def cpu_baseline(synth, wl, max_shapes, budget_s=4.0):
         if per_shape > 30.0 and nthr == 1:
             return None
         s = max(1, min(max_shapes, int(budget_s / max(per_shape, 1e-3))))
-        runs = sorted(oracle_step(synth, wl, s) for _ in range(3))
+        runs = sorted(run(synth, wl, s) for _ in range(3))
         flops, dt = runs[1]
         return {"value": round(flops / dt / 1e9, 4), "shapes": s, "seconds": round(dt, 3),
                 "gflop": round(flops / 1e9, 3)}
@@ -837,7 +999,8 @@ def cpu_baseline(synth, wl, max_shapes, budget_s=4.0):
     return {"value": full["value"], "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
             "value_all": full["value"], "value_1t": one["value"] if one else None,
             "cpu_model": cpu_model(),
-            "sample": f"one step (build, neighbour search, forward and backward, float64) of the "
+            "sample": f"one step (build, neighbour search, forward and backward"
+                      f"{', SGD update' if wl.train else ''}, float64) of the "
                       f"first {full['shapes']} of {wl.batch} shapes at {threads} threads "
                       f"({full['gflop']} GFLOP, median of 3: {full['seconds']} s)"
                       + (f", and of the first {one['shapes']} shapes at 1 thread "
@@ -872,7 +1035,7 @@ def main():
     torch.cuda.set_device(0)
     wl = synth.WORKLOADS[args.workload]
     print(f"[bench] workload {wl.name}: generating inputs", file=sys.stderr, flush=True)
-    step = Step(oc, torch, synth, wl)
+    step = (TrainStep if wl.train else Step)(oc, torch, synth, wl)
     if args.streams == 2:
         step.side = torch.cuda.Stream()  # default priority, like the main stream
     flops, octants = step.conv_flops()
@@ -1070,6 +1233,11 @@ WORKLOAD_TEXT = {
                 "average-pool @d6 (the convolution's neighbourhood), 2x2x2 max-pool d6->d5, "
                 "3x3x3 max-pool stride 2 d5->d4, 3x3x3 average-pool stride 4 d4->d2; fp32 "
                 "forward and backward",
+    "ocnn_d6": "O-CNN(6) classification training iteration on 32 shapes (20k surface points "
+               "each), octree built on the GPU each step: U_6 .. U_2 (conv3 + batch norm + ReLU "
+               "+ 2x2x2 max-pool; 3->8, 8->16, 16->32, 32->64, 64->128), dropout 0.5, FC(128), "
+               "dropout, FC(40), softmax cross-entropy on synthetic labels, backward, SGD "
+               "(momentum 0.9, weight decay 5e-4); fp32",
     "s4_d6": "32 shapes, depth 6; conv3+ReLU 3->16 @d6, stride-4 conv3+ReLU 16->64 d6->d4, "
              "conv3 64->128 @d4; fp32 forward and backward",
     "seg_d6": "32 shapes, depth 6; encoder conv3+ReLU+maxpool 3->16 @d6, 16->32 @d5; decoder "

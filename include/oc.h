@@ -385,6 +385,58 @@ oc_status oc_gpool_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int3
                        int32_t mode, const float* dy, const uint8_t* sw, int32_t c, float* dx,
                        hipStream_t stream);
 
+/* ---- The rest of the O-CNN(d) training iteration (Sec. 4 "Network
+ * structure": units of convolution + batch normalisation + ReLU + pooling,
+ * then dropout, fully connected layers and softmax; Sec. 5 "Training
+ * details": SGD with momentum and weight decay).  Plain device buffers, fp32,
+ * enqueued on `stream`; no floating-point atomics (reproducible bit for bit).
+ *
+ * Batch normalisation in training mode over the n rows of x [n][c] (all
+ * octants of a depth, empty children included): per channel mean and biased
+ * variance (double-precision sums in a fixed order), y = (x - mean) invstd
+ * gamma + beta, invstd = 1 / sqrt(var + eps); flags OC_FUSE_RELU applies
+ * max(0, .) to y.  mean, invstd: dev f32 [c], written for the backward.
+ * ws: dev, at least oc_bn_workspace(n, c) bytes. */
+size_t oc_bn_workspace(int64_t n, int32_t c);
+oc_status oc_bn_fwd(int64_t n, int32_t c, const float* x, const float* gamma, const float* beta,
+                    float eps, int32_t flags, float* y, float* mean, float* invstd, void* ws,
+                    size_t ws_bytes, hipStream_t stream);
+
+/* Gradients of oc_bn_fwd (without the ReLU: dy is the gradient w.r.t. the
+ * normalised output): dbeta = sum dy, dgamma = sum dy x_hat, dx = gamma
+ * invstd (dy - dbeta / n - x_hat dgamma / n); dev f32, dx [n][c], dgamma and
+ * dbeta [c]. */
+oc_status oc_bn_bwd(int64_t n, int32_t c, const float* x, const float* dy, const float* gamma,
+                    const float* mean, const float* invstd, float* dx, float* dgamma,
+                    float* dbeta, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Fully connected layer: y [B][cout] = x [B][cin] w [cin][cout] + bias [cout]
+ * (bias may be NULL).  Backward: dx = dy w^T, dw = x^T dy, dbias = sum of dy
+ * over the batch; dx and dbias may be NULL. */
+oc_status oc_fc_fwd(int32_t batch, int32_t cin, int32_t cout, const float* x, const float* w,
+                    const float* bias, float* y, hipStream_t stream);
+oc_status oc_fc_bwd(int32_t batch, int32_t cin, int32_t cout, const float* x, const float* w,
+                    const float* dy, float* dx, float* dw, float* dbias, hipStream_t stream);
+
+/* Dropout with ratio p in [0, 1): y = keep ? x / (1 - p) : 0, keep dev u8 [n]
+ * (the mask is an input: the caller draws it).  The backward is the same call
+ * on dy. */
+oc_status oc_dropout(int64_t n, const float* x, const uint8_t* keep, float p, float* y,
+                     hipStream_t stream);
+
+/* Softmax cross-entropy over the batch: loss (dev f32 scalar) = mean over
+ * the rows b of -log softmax(z[b])[labels[b]], dz [B][nc] = (softmax(z) -
+ * onehot(labels)) / B.  z dev f32 [B][nc], labels dev i32 [B] in 0..nc-1.
+ * ws: dev, at least oc_softmax_ce_workspace(B) bytes. */
+size_t oc_softmax_ce_workspace(int32_t batch);
+oc_status oc_softmax_ce(int32_t batch, int32_t nc, const float* z, const int32_t* labels,
+                        float* loss, float* dz, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* SGD step with momentum and weight decay, in place over n parameters:
+ * v = momentum v + lr (g + decay w), w = w - v. */
+oc_status oc_sgd(int64_t n, float* w, const float* g, float* v, float lr, float momentum,
+                 float decay, hipStream_t stream);
+
 /* Profiling: the next launch, on the calling thread, of the kernel that does
  * the main work of an entry point (the kernel oc_conv_kernel names for a
  * convolution pass; the pooling, routing or unpooling kernel of oc_pool_* /

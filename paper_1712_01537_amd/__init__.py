@@ -42,6 +42,13 @@ __all__ = [
     "OC_FUSE_RELU",
     "OC_POOL_MAX",
     "OC_POOL_AVG",
+    "oc_bn_fwd",
+    "oc_bn_bwd",
+    "oc_fc_fwd",
+    "oc_fc_bwd",
+    "oc_dropout",
+    "oc_softmax_ce",
+    "oc_sgd",
     "EXPORTS",
 ]
 
@@ -60,6 +67,8 @@ EXPORTS = (
     "oc_unpool_fwd", "oc_unpool_bwd", "oc_status_str", "oc_last_error", "oc_profile_next",
     "oc_deconv_fwd", "oc_deconv_fwd_workspace", "oc_deconv_bwd", "oc_deconv_bwd_workspace",
     "oc_gpool_fwd", "oc_gpool_bwd", "oc_profile_calls", "oc_conv_fwd_noalloc",
+    "oc_bn_workspace", "oc_bn_fwd", "oc_bn_bwd", "oc_fc_fwd", "oc_fc_bwd", "oc_dropout",
+    "oc_softmax_ce_workspace", "oc_softmax_ce", "oc_sgd",
 )
 
 
@@ -169,6 +178,15 @@ def load():
         "oc_last_error": ([], C.c_char_p),
         "oc_profile_next": ([p, p], C.c_int),
         "oc_profile_calls": ([p, p, i32, p], C.c_int),
+        "oc_bn_workspace": ([i64, i32], sz),
+        "oc_bn_fwd": ([i64, i32, p, p, p, C.c_float, i32, p, p, p, p, sz, p], C.c_int),
+        "oc_bn_bwd": ([i64, i32, p, p, p, p, p, p, p, p, p, sz, p], C.c_int),
+        "oc_fc_fwd": ([i32, i32, i32, p, p, p, p, p], C.c_int),
+        "oc_fc_bwd": ([i32, i32, i32, p, p, p, p, p, p, p], C.c_int),
+        "oc_dropout": ([i64, p, p, C.c_float, p, p], C.c_int),
+        "oc_softmax_ce_workspace": ([i32], sz),
+        "oc_softmax_ce": ([i32, i32, p, p, p, p, p, sz, p], C.c_int),
+        "oc_sgd": ([i64, p, p, p, C.c_float, C.c_float, C.c_float, p], C.c_int),
     }
     for name, (args, res) in sigs.items():
         f = getattr(L, name)
@@ -448,14 +466,19 @@ def oc_conv_fwd_noalloc(tree: Octree, depth: int, ksize: int, stride: int, x: to
 
 def oc_conv_bwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tensor,
                 w: torch.Tensor, dy: torch.Tensor, y: torch.Tensor | None = None,
-                relu: bool = False, need_dx: bool = True, need_dw: bool = True):
+                relu: bool = False, need_dx: bool = True, need_dw: bool = True,
+                dw_out: torch.Tensor | None = None):
+    """(dx or None, dw or None); dw_out: a caller tensor to write dw into."""
     K3, cin, cout, n_in, n_out = _conv_dims(tree, depth, stride, x, w)
     if K3 != ksize ** 3:
         raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
     dt = _dtype_code(w)
     L = load()
     dx = torch.empty((n_in, cin), dtype=torch.float32, device=w.device) if need_dx else None
-    dw = torch.empty((K3, cin, cout), dtype=torch.float32, device=w.device) if need_dw else None
+    dw = None
+    if need_dw:
+        dw = (dw_out.view(K3, cin, cout) if dw_out is not None else
+              torch.empty((K3, cin, cout), dtype=torch.float32, device=w.device))
     ws_bytes = L.oc_conv_bwd_workspace(tree.handle, depth, ksize, stride, dt, cin, cout)
     ws = torch.empty(max(int(ws_bytes), 1), dtype=torch.uint8, device=w.device)
     yp = _dev(y, "y", torch.float32, (n_out, cout)) if relu else None
@@ -597,3 +620,96 @@ def oc_gpool_bwd(tree: Octree, depth: int, ksize: int, mode: int, dy: torch.Tens
                                _dev(sw, "sw", torch.uint8, (n, c)) if sw is not None else None,
                                c, _dev(dx, "dx"), _stream()))
     return dx
+
+
+# --- the rest of the O-CNN(d) training iteration --------------------------
+
+
+def _opt(t, name, **kw):
+    return _dev(t, name, **kw) if t is not None else None
+
+
+def oc_bn_fwd(x: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor, eps: float = 1e-5,
+              relu: bool = False):
+    """Batch normalisation over the rows of x [n][c] (training mode):
+    (y, mean, invstd)."""
+    n, c = x.shape
+    y = torch.empty_like(x)
+    mean = torch.empty(c, dtype=torch.float32, device=x.device)
+    invstd = torch.empty(c, dtype=torch.float32, device=x.device)
+    L = load()
+    ws = torch.empty(max(int(L.oc_bn_workspace(n, c)), 1), dtype=torch.uint8, device=x.device)
+    _check(L.oc_bn_fwd(n, c, _dev(x, "x", torch.float32), _dev(gamma, "gamma", torch.float32),
+                       _dev(beta, "beta", torch.float32), eps, OC_FUSE_RELU if relu else 0,
+                       _dev(y, "y"), _dev(mean, "mean"), _dev(invstd, "invstd"), _dev(ws, "ws"),
+                       ws.numel(), _stream()))
+    return y, mean, invstd
+
+
+def oc_bn_bwd(x, dy, gamma, mean, invstd, dgamma=None, dbeta=None):
+    """(dx, dgamma, dbeta) of oc_bn_fwd (without its ReLU); dgamma, dbeta:
+    optional caller tensors to write into."""
+    n, c = x.shape
+    dx = torch.empty_like(x)
+    dg = dgamma if dgamma is not None else torch.empty(c, dtype=torch.float32, device=x.device)
+    db = dbeta if dbeta is not None else torch.empty(c, dtype=torch.float32, device=x.device)
+    L = load()
+    ws = torch.empty(max(int(L.oc_bn_workspace(n, c)), 1), dtype=torch.uint8, device=x.device)
+    _check(L.oc_bn_bwd(n, c, _dev(x, "x", torch.float32), _dev(dy, "dy", torch.float32, (n, c)),
+                       _dev(gamma, "gamma", torch.float32), _dev(mean, "mean"),
+                       _dev(invstd, "invstd"), _dev(dx, "dx"), _dev(dg, "dgamma"),
+                       _dev(db, "dbeta"), _dev(ws, "ws"), ws.numel(), _stream()))
+    return dx, dg, db
+
+
+def oc_fc_fwd(x, w, b=None):
+    B, cin = x.shape
+    cout = w.shape[1]
+    y = torch.empty((B, cout), dtype=torch.float32, device=x.device)
+    _check(load().oc_fc_fwd(B, cin, cout, _dev(x, "x", torch.float32),
+                            _dev(w, "w", torch.float32, (cin, cout)), _opt(b, "b"), _dev(y, "y"),
+                            _stream()))
+    return y
+
+
+def oc_fc_bwd(x, w, dy, need_dx=True, dw=None, db=None):
+    """(dx or None, dw, db); dw, db: optional caller tensors to write into."""
+    B, cin = x.shape
+    cout = w.shape[1]
+    dx = torch.empty_like(x) if need_dx else None
+    dw = dw if dw is not None else torch.empty_like(w)
+    db = db if db is not None else torch.empty(cout, dtype=torch.float32, device=x.device)
+    _check(load().oc_fc_bwd(B, cin, cout, _dev(x, "x", torch.float32), _dev(w, "w"),
+                            _dev(dy, "dy", torch.float32, (B, cout)), _opt(dx, "dx"),
+                            _dev(dw, "dw"), _dev(db, "db"), _stream()))
+    return dx, dw, db
+
+
+def oc_dropout(x, keep, p):
+    y = torch.empty_like(x)
+    _check(load().oc_dropout(x.numel(), _dev(x, "x", torch.float32),
+                             _dev(keep, "keep", torch.uint8, tuple(x.shape)), p, _dev(y, "y"),
+                             _stream()))
+    return y
+
+
+def oc_softmax_ce(z, labels):
+    """(loss as a 0-d device tensor, dz)."""
+    B, nc = z.shape
+    loss = torch.empty((), dtype=torch.float32, device=z.device)
+    dz = torch.empty_like(z)
+    L = load()
+    ws = torch.empty(max(int(L.oc_softmax_ce_workspace(B)), 1), dtype=torch.uint8,
+                     device=z.device)
+    _check(L.oc_softmax_ce(B, nc, _dev(z, "z", torch.float32),
+                           _dev(labels, "labels", torch.int32, (B,)), _dev(loss, "loss"),
+                           _dev(dz, "dz"), _dev(ws, "ws"), ws.numel(), _stream()))
+    return loss, dz
+
+
+def oc_sgd(w, g, v, lr, momentum, decay):
+    """In place: v = momentum v + lr (g + decay w), w -= v."""
+    _check(load().oc_sgd(w.numel(), _dev(w, "w", torch.float32),
+                         _dev(g, "g", torch.float32, tuple(w.shape)),
+                         _dev(v, "v", torch.float32, tuple(w.shape)), lr, momentum, decay,
+                         _stream()))

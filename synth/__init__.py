@@ -25,6 +25,9 @@ seg_d6      6      32     20k       conv3+ReLU+pool 3->16 @6, 16->32 @5; stride-
 gpool_d6    6      32     20k       conv3+ReLU 3->16 @6; 3x3x3 max-pool and 5x5x5 average-pool,
                                     stride 1, @6; 2x2x2 max-pool d6->d5; 3x3x3 max-pool
                                     stride 2 d5->d4; 3x3x3 average-pool stride 4 d4->d2
+ocnn_d6     6      32     20k       O-CNN(6) training iteration: U_6 .. U_2 (conv3 + BN + ReLU +
+                                    pool; 3->8, 8->16, 16->32, 32->64, 64->128), dropout,
+                                    FC(128), dropout, FC(40), softmax loss, SGD (synthetic labels)
 s4_d6       6      32     20k       conv3+ReLU 3->16 @6; stride-4 conv3+ReLU 16->64 d6->d4;
                                     conv3 64->128 @4
 ==========  =====  =====  ========  ===============================================
@@ -51,6 +54,7 @@ __all__ = [
     "make_points",
     "make_weights",
     "make_features",
+    "make_train_inputs",
     "make_upstream",
     "random_cloud",
 ]
@@ -83,6 +87,8 @@ class Workload:
     weight_sigma: float | None = None  # None: He-normal sqrt(2/(K^3 Cin))
     signal_input: bool = True  # first conv reads the averaged-normal signal
     full_depth: int = 2
+    train: bool = False  # the O-CNN(d) classification training iteration around the convs
+    classes: int = 40
 
 
 WORKLOADS = {
@@ -143,6 +149,16 @@ WORKLOADS = {
             Layer("gpool", 5, 16, 16, ksize=3, stride=2, mode="max"),
             Layer("gpool", 4, 16, 16, ksize=3, stride=4, mode="avg"),
         ),
+    ),
+    # O-CNN(6) (units U_6 .. U_2: conv + BN + ReLU + pool, C_l = 2^max(1, 9-l)),
+    # dropout, FC(128), dropout, FC(40), softmax loss, SGD: one training iteration
+    "ocnn_d6": Workload(
+        "ocnn_d6", 9, 6, 32, 20_000, "union",
+        (
+            Layer("conv", 6, 3, 8), Layer("conv", 5, 8, 16), Layer("conv", 4, 16, 32),
+            Layer("conv", 3, 32, 64), Layer("conv", 2, 64, 128),
+        ),
+        train=True,
     ),
     "s4_d6": Workload(
         "s4_d6", 8, 6, 32, 20_000, "union",
@@ -298,6 +314,30 @@ def make_weights(w: Workload | str, layer: int, ksize: int, cin: int, cout: int)
     rng = np.random.default_rng([w.seed_id, 1000 + layer])
     sigma = w.weight_sigma if w.weight_sigma is not None else math.sqrt(2.0 / (ksize ** 3 * cin))
     return (sigma * rng.standard_normal((ksize ** 3, cin, cout))).astype(np.float32)
+
+
+def make_train_inputs(w: Workload | str, batch: int | None = None, p_drop: float = 0.5):
+    """Draws of a training iteration (the random numbers the method uses):
+    class labels i32 [B] in [0, classes), the two dropout keep masks u8
+    [B][8 C_2] and [B][128] (keep with probability 1 - p_drop), and the head's
+    initial parameters: BN gamma = 1, beta = 0 per conv layer, FC weights
+    N(0, 1/fan_in), FC biases 0."""
+    if isinstance(w, str):
+        w = WORKLOADS[w]
+    B = w.batch if batch is None else batch
+    rng = np.random.default_rng([w.seed_id, 5000])
+    c2 = w.layers[-1].cout
+    out = {
+        "labels": rng.integers(0, w.classes, B).astype(np.int32),
+        "keep1": (rng.random((B, 8 * c2)) >= p_drop).astype(np.uint8),
+        "keep2": (rng.random((B, 128)) >= p_drop).astype(np.uint8),
+        "bn": [(np.ones(L.cout, np.float32), np.zeros(L.cout, np.float32)) for L in w.layers],
+        "fc1_w": (rng.standard_normal((8 * c2, 128)) / math.sqrt(8 * c2)).astype(np.float32),
+        "fc1_b": np.zeros(128, np.float32),
+        "fc2_w": (rng.standard_normal((128, w.classes)) / math.sqrt(128)).astype(np.float32),
+        "fc2_b": np.zeros(w.classes, np.float32),
+    }
+    return out
 
 
 def make_features(seed, rows: int, channels: int):
