@@ -269,16 +269,17 @@ def op_rate(cls, work, us, bf16):
 
 # Kernel classes of a rocprofv3 trace of this script, by kernel name: the
 # build's kernels, the pooling/unpooling kernels, the convolutions' main
-# kernels (the MFMA contraction: hand-written kernels and, for stride 2, the
-# ROCm GEMM library's) and their helpers (split sums, ReLU masks, operand
-# conversion and gathers).  Anything else (the bench's own torch casts) is
-# "other".
+# kernels (the MFMA contractions, the pooled forwards among them) and their
+# helpers (split sums, the pooled split sum included, ReLU masks, operand
+# conversion, gathers and tables).  Anything else (the bench's own torch
+# casts) is "other".
 TRACE_CLASSES = (
     ("build", ("k_quant", "k_mark", "k_reduce", "k_scan_a", "k_scan_c", "k_leaf_mean", "k_emit",
                "__amd_rocclr_copyBuffer")),
     ("pool", ("k_pool_fwd", "k_route_down", "k_route_up", "k_gpool_")),
-    ("conv_main", ("k_conv_", "k_cin_", "Cijk_", "k_s2_fwd<")),
-    ("conv_helper", ("k_sum_", "k_relu_mask", "k_bf_", "k_bf16_to_f32", "k_s2_", "k_fill_u32")),
+    ("conv_main", ("k_conv_", "k_cin_", "k_sr_mm<", "k_sr_dw<")),
+    ("conv_helper", ("k_sum_", "k_relu_mask", "k_bf_", "k_bf16_to_f32", "k_sr_", "k_dc_",
+                     "k_fill_u32")),
 )
 
 
@@ -531,13 +532,23 @@ class Step(Accounting):
             if L.op == "conv":
                 dt = torch.bfloat16 if L.dtype == "bf16" else torch.float32
                 for ps, tag in enumerate(("conv_fwd", "conv_bwd_data", "conv_bwd_weight")):
+                    # the forward of a conv + pool pair: the pooled kernel
+                    pp = 3 if (ps == 0 and self.pooled(li)) else ps
                     self.kname[(li, tag)] = oc.oc_conv_kernel(tree, L.depth, L.ksize, L.stride,
-                                                              L.cin, L.cout, ps, dt)
+                                                              L.cin, L.cout, pp, dt)
             elif L.op == "deconv":  # the transposed convolution's passes, swapped
                 for ps, tag in ((1, "deconv_fwd"), (0, "deconv_bwd_data"), (2, "deconv_bwd_weight")):
                     self.kname[(li, tag)] = oc.oc_conv_kernel(tree, L.depth, L.ksize, L.stride,
                                                               L.cout, L.cin, ps)
         tree.free()
+
+    def pooled(self, li):
+        """True when conv layer li and the 2x2x2 max-pool after it run as one
+        conv + pool call (stride 1, fp32)."""
+        ls = self.wl.layers
+        L = ls[li]
+        return (L.op == "conv" and L.stride == 1 and L.dtype == "f32" and li + 1 < len(ls)
+                and ls[li + 1].op == "pool" and ls[li + 1].depth == L.depth)
 
     # --- one step ----------------------------------------------------------
     def key(self, tag, li):
@@ -625,8 +636,21 @@ class Step(Accounting):
         x = tree.signal() if wl.signal_input else self.x0
         saved = []
         sws = {}  # switches of the pooling at each depth, for the unpooling
+        done = -1  # a pool layer already run with the conv below it
         for li, L in enumerate(wl.layers):
-            if L.op == "conv":
+            if li == done:
+                continue
+            if L.op == "conv" and self.pooled(li):
+                # conv + ReLU + pool in one call: the depth-l output is not kept
+                w = self.weights[li]
+                p, sw = self._run("conv_fwd", li, lambda: oc.oc_conv_pool_fwd(
+                    tree, L.depth, L.ksize, x, w, relu=L.relu))
+                saved.append((li, x, None, None))
+                saved.append((li + 1, None, p, sw))
+                sws[L.depth] = sw
+                done = li + 1
+                x = p
+            elif L.op == "conv":
                 w = self.weights[li]
                 if x.dtype != w.dtype:  # a bf16 layer after an fp32 output
                     x = x.to(w.dtype)

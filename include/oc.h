@@ -207,6 +207,31 @@ oc_status oc_conv_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32
                       oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
                       float* y, void* ws, size_t ws_bytes, int32_t flags, hipStream_t stream);
 
+/* Convolution, ReLU and 2x2x2 max-pooling forward in one call (the unit of
+ * Sec. 4's network structure without its normalisation; operations of
+ * Sec. 3.2): the stride-1 convolution at depth l, max(0, .) when flags has
+ * OC_FUSE_RELU, then oc_pool_fwd's pooling to depth l-1.  Where the kernel
+ * pools in its epilogue (fp32; K = 3 with cin 3 or 4 and cout a multiple of
+ * 16, or cin and cout multiples of 4 with cin >= 16) the depth-l output is
+ * never written to memory.
+ *   depth   l, 1 .. tree depth; ksize 3 or 5; dt, x, cin, w, cout, flags
+ *           as oc_conv_fwd with stride 1.
+ *   y       dev f32 [N_{l-1}][cout], 16-byte aligned: the pooled features;
+ *           rows of empty octants are zero.
+ *   sw      dev u8 [M_{l-1}][cout], 4-byte aligned: the switches, as
+ *           oc_pool_fwd (the first maximum over children 0..7).
+ *   ws      dev workspace of oc_conv_pool_fwd_workspace() bytes (may be NULL
+ *           when that is 0).
+ * y and sw equal, bit for bit, oc_conv_fwd followed by oc_pool_fwd.  The
+ * backward is oc_pool_bwd with y (which applies the ReLU's backward), then
+ * oc_conv_bwd without OC_FUSE_RELU. */
+size_t oc_conv_pool_fwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize,
+                                  oc_dtype dt, int32_t cin, int32_t cout);
+oc_status oc_conv_pool_fwd(const oc_octree* tree, int32_t depth, int32_t ksize, oc_dtype dt,
+                           const void* x, int32_t cin, const void* w, int32_t cout, float* y,
+                           uint8_t* sw, void* ws, size_t ws_bytes, int32_t flags,
+                           hipStream_t stream);
+
 /* oc_conv_fwd without a workspace argument, for callers that cannot allocate
  * device memory (code under HIP graph capture, tight serving loops, harnesses
  * that forbid allocation): the workspace is a static device array of the
@@ -224,7 +249,8 @@ oc_status oc_conv_fwd_noalloc(const oc_octree* tree, int32_t depth, int32_t ksiz
 /* Name, template arguments included (as profilers such as rocprofv3 print
  * it), of the kernel that does the arithmetic of one pass of a convolution
  * call with these arguments: pass 0 = oc_conv_fwd, 1 = the input gradient and
- * 2 = the weight gradient of oc_conv_bwd.  Lets a caller attribute measured
+ * 2 = the weight gradient of oc_conv_bwd, 3 = the convolution kernel of
+ * oc_conv_pool_fwd (stride 1 only).  Lets a caller attribute measured
  * kernel time to the operation it belongs to.  The string lives in
  * thread-local storage until the next call on the thread; "" (and
  * oc_last_error set) for invalid arguments. */

@@ -27,6 +27,7 @@ __all__ = [
     "BuildJob",
     "oc_conv_fwd",
     "oc_conv_fwd_noalloc",
+    "oc_conv_pool_fwd",
     "oc_conv_kernel",
     "oc_profile_next",
     "CallProfile",
@@ -68,7 +69,8 @@ EXPORTS = (
     "oc_deconv_fwd", "oc_deconv_fwd_workspace", "oc_deconv_bwd", "oc_deconv_bwd_workspace",
     "oc_gpool_fwd", "oc_gpool_bwd", "oc_profile_calls", "oc_conv_fwd_noalloc",
     "oc_bn_workspace", "oc_bn_fwd", "oc_bn_bwd", "oc_fc_fwd", "oc_fc_bwd", "oc_dropout",
-    "oc_softmax_ce_workspace", "oc_softmax_ce", "oc_sgd",
+    "oc_softmax_ce_workspace", "oc_softmax_ce", "oc_sgd", "oc_conv_pool_fwd",
+    "oc_conv_pool_fwd_workspace",
 )
 
 
@@ -156,6 +158,9 @@ def load():
         "oc_octree_free": ([p], None),
         "oc_conv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, sz, i32, p], C.c_int),
         "oc_conv_fwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
+        "oc_conv_pool_fwd_workspace": ([p, i32, i32, C.c_int, i32, i32], sz),
+        "oc_conv_pool_fwd": ([p, i32, i32, C.c_int, p, i32, p, i32, p, p, p, sz, i32, p],
+                             C.c_int),
         "oc_conv_fwd_noalloc": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, i32, p],
                                 C.c_int),
         "oc_conv_kernel": ([p, i32, i32, i32, C.c_int, i32, i32, i32], C.c_char_p),
@@ -445,6 +450,29 @@ def oc_conv_fwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tens
                          _dev(ws, "ws") if ws is not None else None, ws_bytes,
                          OC_FUSE_RELU if relu else 0, _stream()))
     return y
+
+
+def oc_conv_pool_fwd(tree: Octree, depth: int, ksize: int, x: torch.Tensor, w: torch.Tensor,
+                     relu: bool = True):
+    """Stride-1 convolution at depth, optional ReLU and the 2x2x2 max-pool to
+    depth - 1 in one call: (pooled [N_{l-1}][cout], switches [M_{l-1}][cout])."""
+    K3, cin, cout, n_in, n_out = _conv_dims(tree, depth, 1, x, w)
+    if K3 != ksize ** 3:
+        raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
+    dt = _dtype_code(x)
+    if w.dtype != x.dtype:
+        raise OcError(1, "x and w must share a dtype")
+    n_p, m = tree.num(depth - 1), tree.nonempty(depth - 1)
+    y = torch.empty((n_p, cout), dtype=torch.float32, device=x.device)
+    sw = torch.empty((m, cout), dtype=torch.uint8, device=x.device)
+    L = load()
+    ws_bytes = int(L.oc_conv_pool_fwd_workspace(tree.handle, depth, ksize, dt, cin, cout))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device) if ws_bytes else None
+    _check(L.oc_conv_pool_fwd(tree.handle, depth, ksize, dt, _dev(x, "x"), cin, _dev(w, "w"),
+                              cout, _dev(y, "y"), _dev(sw, "sw"),
+                              _dev(ws, "ws") if ws is not None else None, ws_bytes,
+                              OC_FUSE_RELU if relu else 0, _stream()))
+    return y, sw
 
 
 def oc_conv_fwd_noalloc(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tensor,

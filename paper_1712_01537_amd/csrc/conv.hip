@@ -141,6 +141,22 @@ size_t fwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype
   return dt == OC_F32 ? tile : x32_bytes(sh, cin) + w32_bytes(sh, cin, cout) + tile;
 }
 
+// Workspace of the conv + pool forward: the fused kernels' split partials,
+// or the depth-l output followed by the plain forward's workspace.
+size_t yl_bytes(const ConvShape& sh, int cout) {
+  return oc::align256((size_t)sh.n_in * cout * sizeof(float));
+}
+bool pool_fused(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,
+                int cout) {
+  return dt == OC_F32 && sh.n_in > 0 && oc::conv_s1_pool_fused(t, l, sh.K, cin, cout);
+}
+size_t pool_fwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,
+                         int cout) {
+  if (sh.n_in == 0) return 0;
+  if (pool_fused(t, l, sh, dt, cin, cout)) return oc::conv_s1_tile_ws(t, l, sh.K, cin, cout);
+  return yl_bytes(sh, cout) + fwd_ws_bytes(t, l, sh, dt, cin, cout);
+}
+
 // The matrix-core path applies the ReLU backward once, into the workspace,
 // ahead of both gradients.
 size_t mask_ws_bytes(const ConvShape& sh, int cout) {
@@ -179,11 +195,12 @@ const char* oc_conv_kernel(const oc_octree* t, int32_t l, int32_t K, int32_t str
   static thread_local char name[128];
   name[0] = 0;
   ConvShape sh;
-  if (pass < 0 || pass > 2) {
-    oc::fail(OC_ERR_ARG, "oc_conv_kernel: pass %d not 0, 1 or 2", pass);
+  if (pass < 0 || pass > 3 || (pass == 3 && stride != 1)) {
+    oc::fail(OC_ERR_ARG, "oc_conv_kernel: pass %d not 0, 1, 2 or (stride 1) 3", pass);
     return name;
   }
   if (check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_kernel") != OC_OK) return name;
+  if (pass == 3 && !pool_fused(t, l, sh, dt, cin, cout)) pass = 0;  // conv, then the pooling
   if (bf16_native(sh, dt, cin, cout)) {
     oc::conv_bf16_kernel_name(K, cin, cout, pass, name, sizeof(name));
   } else if (stride == 1) {  // other bf16 shapes run the fp32 kernels on widened operands
@@ -237,6 +254,50 @@ oc_status oc_conv_fwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
   if (st != OC_OK) return st;
   OC_LAUNCH_CHECK();
   return OC_OK;
+}
+
+size_t oc_conv_pool_fwd_workspace(const oc_octree* t, int32_t l, int32_t K, oc_dtype dt,
+                                  int32_t cin, int32_t cout) {
+  ConvShape sh;
+  if (check_conv(t, l, K, 1, dt, cin, cout, &sh, "oc_conv_pool_fwd_workspace") != OC_OK) return 0;
+  return pool_fwd_ws_bytes(t, l, sh, dt, cin, cout);
+}
+
+oc_status oc_conv_pool_fwd(const oc_octree* t, int32_t l, int32_t K, oc_dtype dt, const void* x,
+                           int32_t cin, const void* w, int32_t cout, float* y, uint8_t* sw,
+                           void* ws, size_t ws_bytes, int32_t flags, hipStream_t s) {
+  ConvShape sh;
+  oc_status st = check_conv(t, l, K, 1, dt, cin, cout, &sh, "oc_conv_pool_fwd");
+  if (st != OC_OK) return st;
+  if (t->N[l - 1] == 0) return OC_OK;
+  // (x and sw are empty, and may be NULL, when depth l has no octant)
+  if ((sh.n_in > 0 && (!x || !sw)) || !w || !y)
+    return oc::fail(OC_ERR_ARG, "oc_conv_pool_fwd: NULL buffer");
+  if ((uintptr_t)y % 16 != 0 || (uintptr_t)sw % 4 != 0)
+    return oc::fail(OC_ERR_ARG, "oc_conv_pool_fwd: y not 16-byte or sw not 4-byte aligned");
+  const size_t need = pool_fwd_ws_bytes(t, l, sh, dt, cin, cout);
+  if (need && (!ws || ws_bytes < need))
+    return oc::fail(OC_ERR_ARG, "oc_conv_pool_fwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0,
+                    need);
+  const int relu = (flags & OC_FUSE_RELU) ? 1 : 0;
+  if (sh.n_in == 0) {  // no depth-l octant: every pooled row is zero
+    oc::fill_u32(y, 0u, t->N[l - 1] * (int64_t)cout, s);
+    OC_LAUNCH_CHECK();
+    return OC_OK;
+  }
+  if (pool_fused(t, l, sh, dt, cin, cout)) {
+    oc::conv_s1_pool_fwd_f32(t, l, K, (const float*)x, cin, (const float*)w, cout, y, sw, relu,
+                             (float*)ws, s);
+    OC_LAUNCH_CHECK();
+    return OC_OK;
+  }
+  // other shapes: the depth-l output into the workspace, then the pooling
+  float* yl = (float*)ws;
+  const size_t head = yl_bytes(sh, cout);
+  st = oc_conv_fwd(t, l, K, 1, dt, x, cin, w, cout, yl, (char*)ws + head, ws_bytes - head, flags,
+                   s);
+  if (st != OC_OK) return st;
+  return oc_pool_fwd(t, l, yl, cout, y, sw, s);
 }
 
 size_t oc_conv_bwd_workspace(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,

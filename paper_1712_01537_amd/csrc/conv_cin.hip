@@ -18,6 +18,7 @@
 // waits are compile-time counts of younger operations (vector-memory
 // operations complete in issue order).
 #include "conv_cin.h"
+#include "pool_fuse.h"
 
 #include <algorithm>
 
@@ -60,8 +61,20 @@ __device__ __forceinline__ void lds_load4(const void* src, uint32_t lds) {
                : "memory", "m0");
 }
 // 16-byte store from inline assembly (counted like the loads by the waits).
+// A store of more than 8 bytes may read its data registers after the next
+// instruction has issued, and the compiler's hazard check does not look
+// into inline assembly: without the wait states, a VALU write of those
+// registers right after the store (which the compiler is free to place
+// there) changes the stored data.
 __device__ __forceinline__ void gstore16(void* dst, v4f v) {
-  asm volatile("global_store_dwordx4 %0, %1, off" ::"v"(dst), "v"(v) : "memory");
+  asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 1" ::"v"(dst), "v"(v) : "memory");
+}
+// 4-byte and 1-byte stores, the same way.
+__device__ __forceinline__ void gstore4(void* dst, uint32_t v) {
+  asm volatile("global_store_dword %0, %1, off" ::"v"(dst), "v"(v) : "memory");
+}
+__device__ __forceinline__ void gstore1(void* dst, uint32_t v) {
+  asm volatile("global_store_byte %0, %1, off" ::"v"(dst), "v"(v) : "memory");
 }
 // Wait until at most N vector-memory operations of this wave are outstanding.
 template <int N>
@@ -119,11 +132,16 @@ __device__ __forceinline__ void tile_dma(const float* __restrict__ x, const int3
 }
 
 // The neighbour entries of tile tl (groups 2 tl, 2 tl + 1): 54 entries into
-// nbs, one instruction; entries of groups past the last read -1.
+// nbs, one instruction; entries of groups past the last read -1.  With prow
+// (the pooled forward), lanes 54 and 55 bring the two groups' output rows of
+// depth l-1 in the same instruction.
 __device__ __forceinline__ void nb_dma(const int32_t* __restrict__ nbr, int64_t ngroups,
-                                       int64_t tl, int32_t* nbs, int lane) {
-  const int64_t g = 2 * tl + lane / 27;
-  const int32_t* src = lane < 54 && g < ngroups ? nbr + 27 * (2 * tl) + lane : &g_cin_absent;
+                                       int64_t tl, int32_t* nbs, int lane,
+                                       const int32_t* __restrict__ prow = nullptr) {
+  const int64_t g = 2 * tl + (lane < 54 ? lane / 27 : lane - 54);
+  const int32_t* src = lane < 54 && g < ngroups            ? nbr + 27 * (2 * tl) + lane
+                       : prow && lane < 56 && g < ngroups ? prow + g
+                                                          : &g_cin_absent;
   lds_load4(src, lds_addr(nbs));
 }
 
@@ -145,13 +163,24 @@ __device__ __forceinline__ void wave_range(int64_t ntiles, int wave, int64_t& t0
 // tiles), y = blocks of 16 output channels.  The MFMA computes y^T: A = W^T
 // (16 output channels x 4 pairs k), B = the gathered rows (4 pairs x 16
 // octants).
-template <int CIN>
+// POOL: the 2x2x2 max-pool follows in the epilogue; y is then the pooled
+// map [npar][cout] of depth l-1 (row prow[g] for group g, brought with the
+// neighbour entries), psw the switches [ngroups][cout]; a tile then issues
+// two stores (values, switches), which the counted waits include; the waves
+// of column block 0 zero an equal share of the rows of empty depth-(l-1)
+// octants after their last wait.
+template <int CIN, bool POOL>
 __global__ __launch_bounds__(TB) void k_cin_fwd(const int32_t* __restrict__ nbr, int64_t ngroups,
                                                 const float* __restrict__ x,
                                                 const float* __restrict__ w, int cout,
-                                                float* __restrict__ y, int relu) {
+                                                float* __restrict__ y, int relu,
+                                                const int32_t* __restrict__ prow,
+                                                const int32_t* __restrict__ plab, int64_t npar,
+                                                uint8_t* __restrict__ psw) {
   constexpr int KF = 27 * CIN, NS = (KF + 3) / 4;
   constexpr int TF = 2 * 64 * 4;  // floats of a tile buffer
+  constexpr int S = POOL ? 2 : 1;  // stores per tile
+  constexpr int WE = 3 + S;        // operations younger than a tile's entries at their wait
   __shared__ __attribute__((aligned(16))) float tiles[NWAVE][NBUF][TF];
   __shared__ __attribute__((aligned(16))) int32_t nbs[NWAVE][2][64];
   const int lane = threadIdx.x & 63;
@@ -160,10 +189,30 @@ __global__ __launch_bounds__(TB) void k_cin_fwd(const int32_t* __restrict__ nbr,
   const int n0 = blockIdx.y * 16;
   int64_t t0, t1;
   wave_range((ngroups + 1) / 2, wave, t0, t1);
-  if (t0 >= t1) return;  // wave-uniform; nothing issued yet
+  // rows of empty depth-(l-1) octants (pooled forward): a share per wave
+  auto zero_share = [&]() {
+    if constexpr (POOL) {
+      if (blockIdx.y != 0) return;
+      const int64_t per = gridDim.x / 8;
+      const int64_t lw = ((int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8) * NWAVE + wave;
+      const int64_t nwv = (int64_t)gridDim.x * NWAVE;
+      const int64_t r0 = npar * lw / nwv, r1 = npar * (lw + 1) / nwv;
+      const int c4 = cout / 4, cnt = (int)(r1 - r0) * c4;
+      for (int e = lane; e < cnt; e += 64) {
+        const int64_t i = r0 + e / c4;
+        if (plab[i] == 0)
+          *reinterpret_cast<v4f*>(y + i * cout + 4 * (e % c4)) = v4f{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  };
+  if (t0 >= t1) {  // wave-uniform; nothing issued yet
+    zero_share();
+    return;
+  }
   float* tw = &tiles[wave][0][0];
   int32_t* nw = &nbs[wave][0][0];
-  nb_dma(nbr, ngroups, t0, nw, lane);  // its latency overlaps the weight loads
+  const int32_t* pr = POOL ? prow : nullptr;
+  nb_dma(nbr, ngroups, t0, nw, lane, pr);  // its latency overlaps the weight loads
 
   // lane (li, q): weight W[k][n0 + li] and row li's tile offset of pair
   // k = 4 s + q (pairs past KF: weight 0, any finite position)
@@ -187,24 +236,36 @@ __global__ __launch_bounds__(TB) void k_cin_fwd(const int32_t* __restrict__ nbr,
   // prologue runs the first D of those steps with dummy stores, so that
   // every wait counts the same younger operations: 4 for entries (tile,
   // store, entries), 4 D for a tile.
+  // pooled forward: the output row of this lane's group for tiles t .. t+D
+  // (read from the entries while they are valid, then shifted along)
+  int32_t pq[D + 1];
+#pragma unroll
+  for (int j = 0; j <= D; ++j) pq[j] = -1;
 #pragma unroll
   for (int j = 0; j < D; ++j) {
-    nb_dma(nbr, ngroups, t0 + j + 1, nw + 64 * ((j + 1) & 1), lane);
+    nb_dma(nbr, ngroups, t0 + j + 1, nw + 64 * ((j + 1) & 1), lane, pr);
     if (j == 0)
       vm_wait_n<1>();
     else
-      vm_wait_n<4>();
+      vm_wait_n<WE>();
+    if constexpr (POOL) pq[j] = nw[64 * (j & 1) + 54 + ((lane >> 4) & 1)];
     tile_dma<CIN>(x, nw + 64 * (j & 1), tw + j * TF, lane);
-    gstore16(g_cin_dummy + 4 * lane, v4f{0.f, 0.f, 0.f, 0.f});
+    if constexpr (POOL) {
+      gstore4(g_cin_dummy + lane, 0u);
+      gstore1(reinterpret_cast<uint8_t*>(g_cin_dummy) + lane, 0u);
+    } else {
+      gstore16(g_cin_dummy + 4 * lane, v4f{0.f, 0.f, 0.f, 0.f});
+    }
   }
   int cur = 0;  // buffer of tile t
   for (int64_t t = t0; t < t1; ++t) {
     const int ahead = (cur + D) % NBUF;  // buffer of tile t+D
     const int e = (int)((t - t0) & 1);   // entry slot of tile t (tile u: slot (u - t0) & 1)
-    nb_dma(nbr, ngroups, t + D + 1, nw + 64 * ((e + D + 1) & 1), lane);
-    vm_wait_n<4>();  // entries of tile t+D
+    nb_dma(nbr, ngroups, t + D + 1, nw + 64 * ((e + D + 1) & 1), lane, pr);
+    vm_wait_n<WE>();  // entries of tile t+D
+    if constexpr (POOL) pq[D] = nw[64 * ((e + D) & 1) + 54 + ((lane >> 4) & 1)];
     tile_dma<CIN>(x, nw + 64 * ((e + D) & 1), tw + ahead * TF, lane);
-    vm_wait_n<4 * D>();  // tile t
+    vm_wait_n<WE * D>();  // tile t
     v4f acc = {0.f, 0.f, 0.f, 0.f};
     const float* bb = tw + cur * TF;
     float xv[NS];  // every read issued before the MFMAs
@@ -212,18 +273,42 @@ __global__ __launch_bounds__(TB) void k_cin_fwd(const int32_t* __restrict__ nbr,
     for (int s = 0; s < NS; ++s) xv[s] = lds_at(bb, xo[s]);
 #pragma unroll
     for (int s = 0; s < NS; ++s) acc = mfma4(wr[s], xv[s], acc);
-    // lane l: row l / 4 of the tile, channels n0 + 4 (l % 4) ..
-    acc = store_order(acc, lane);
     if (relu) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[j] = fmaxf(acc[j], 0.f);
     }
-    const int64_t row = 16 * t + (lane >> 2);
-    float* dst = row < 8 * ngroups ? y + row * cout + n0 + 4 * (lane & 3) : g_cin_dummy + 4 * lane;
-    gstore16(dst, acc);
+    if constexpr (POOL) {
+      // through LDS (tile t's buffer: its MFMA operands have been read, and
+      // tile t+NBUF is loaded into it only in the next iteration): lane o
+      // pools group 2t + (o/16)%2 in channel n0 + o%16; lanes 32-63 repeat
+      // lanes 0-31 (same address, same data: no lane goes to the dummy row,
+      // which every wave of the grid would hit)
+      float* ps = tw + cur * TF;
+      oc::pool_put(ps, acc, lane);
+      uint32_t sw;
+      const float m = oc::pool_scan(ps, lane, sw);
+      const int64_t g = 2 * t + ((lane >> 4) & 1);
+      const bool st = g < ngroups && pq[0] >= 0;
+      const int c = n0 + (lane & 15);
+      gstore4(st ? (void*)(y + (int64_t)pq[0] * cout + c) : (void*)(g_cin_dummy + lane),
+              __float_as_uint(m));
+      gstore1(st ? (void*)(psw + g * cout + c)
+                 : (void*)(reinterpret_cast<uint8_t*>(g_cin_dummy) + lane),
+              sw);
+#pragma unroll
+      for (int j = 0; j < D; ++j) pq[j] = pq[j + 1];
+    } else {
+      // lane l: row l / 4 of the tile, channels n0 + 4 (l % 4) ..
+      acc = store_order(acc, lane);
+      const int64_t row = 16 * t + (lane >> 2);
+      float* dst =
+          row < 8 * ngroups ? y + row * cout + n0 + 4 * (lane & 3) : g_cin_dummy + 4 * lane;
+      gstore16(dst, acc);
+    }
     cur = cur + 1 == NBUF ? 0 : cur + 1;
   }
   vm_wait0();  // no DMA into LDS outlives the workgroup
+  zero_share();
 }
 
 // Weight gradient: part[blockIdx.x][k][n0 + j] = sum over the workgroup's
@@ -390,22 +475,35 @@ bool conv_cin_supported(int K, int cin, int cout) {
   return K == 3 && (cin == 3 || cin == 4) && cout % 16 == 0 && cout > 0;
 }
 
+template <int CIN, bool POOL>
+void launch_cin_fwd(const oc_octree* t, int l, const float* x, const float* w, int cout, float* y,
+                    int relu, uint8_t* sw, hipStream_t s) {
+  const int64_t G = t->M[l - 1];
+  const int ncb = cout / 16;
+  static const int occ = occupancy(k_cin_fwd<CIN, POOL>);
+  const dim3 grid((unsigned)workgroups(G, occ, ncb), (unsigned)ncb);
+  launch_main(k_cin_fwd<CIN, POOL>, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, w, cout,
+              y, relu, POOL ? (const int32_t*)t->rows[l - 1] : nullptr,
+              POOL ? (const int32_t*)t->labels[l - 1] : nullptr, POOL ? t->N[l - 1] : 0, sw);
+}
+
 void conv_cin_fwd(const oc_octree* t, int l, const float* x, int cin, const float* w, int cout,
                   float* y, int relu, hipStream_t s) {
-  const int64_t G = t->M[l - 1];
-  if (G <= 0) return;
-  const int ncb = cout / 16;
-  if (cin == 3) {
-    static const int occ = occupancy(k_cin_fwd<3>);
-    const dim3 grid((unsigned)workgroups(G, occ, ncb), (unsigned)ncb);
-    launch_main(k_cin_fwd<3>, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, w, cout, y,
-                relu);
-  } else {
-    static const int occ = occupancy(k_cin_fwd<4>);
-    const dim3 grid((unsigned)workgroups(G, occ, ncb), (unsigned)ncb);
-    launch_main(k_cin_fwd<4>, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, w, cout, y,
-                relu);
-  }
+  if (t->M[l - 1] <= 0) return;
+  if (cin == 3)
+    launch_cin_fwd<3, false>(t, l, x, w, cout, y, relu, nullptr, s);
+  else
+    launch_cin_fwd<4, false>(t, l, x, w, cout, y, relu, nullptr, s);
+}
+
+void conv_cin_pool_fwd(const oc_octree* t, int l, const float* x, int cin, const float* w,
+                       int cout, float* yp, uint8_t* sw, int relu, hipStream_t s) {
+  if (t->N[l - 1] <= 0) return;
+  // with no non-empty depth-(l-1) octant the kernel still zeroes every row
+  if (cin == 3)
+    launch_cin_fwd<3, true>(t, l, x, w, cout, yp, relu, sw, s);
+  else
+    launch_cin_fwd<4, true>(t, l, x, w, cout, yp, relu, sw, s);
 }
 
 size_t conv_cin_dw_parts(const oc_octree* t, int l, int cin, int cout) {
@@ -427,7 +525,10 @@ void conv_cin_dw(const oc_octree* t, int l, const float* x, int cin, const float
 }
 
 void conv_cin_kernel_name(int cin, int pass, char* buf, size_t n) {
-  snprintf(buf, n, pass == 0 ? "k_cin_fwd<%d>" : "k_cin_dw<%d>", cin);
+  if (pass == 2)
+    snprintf(buf, n, "k_cin_dw<%d>", cin);
+  else
+    snprintf(buf, n, "k_cin_fwd<%d, %s>", cin, pass == 3 ? "true" : "false");
 }
 
 }  // namespace oc

@@ -6,7 +6,8 @@
 namespace oc {
 
 // Name (with template arguments) of the main kernel of pass 0 (forward),
-// 1 (input gradient) or 2 (weight gradient) of a stride-1 convolution.
+// 1 (input gradient), 2 (weight gradient) or 3 (conv + pool forward) of a
+// stride-1 convolution.
 void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, int pass, char* buf,
                          size_t n);
 
@@ -19,6 +20,20 @@ size_t conv_s1_tile_ws(const oc_octree* t, int l, int K, int kk, int nn);
 // bytes.
 void conv_s1_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin, const float* w,
                      int cout, float* y, int relu, float* ws, hipStream_t s);
+
+// True when the forward kernel of this stride-1 fp32 shape pools in its
+// epilogue (or through its split sum): conv_s1_pool_fwd_f32 then needs
+// conv_s1_tile_ws(t, l, K, cin, cout) bytes of workspace and writes no
+// depth-l output.
+bool conv_s1_pool_fused(const oc_octree* t, int l, int K, int cin, int cout);
+
+// yp [N_{l-1}][cout], sw [M_{l-1}][cout] = 2x2x2 max-pool (first maximum
+// over children 0..7) of the stride-1 convolution of x, ReLU'd when relu;
+// rows of empty octants zero.  Only for shapes conv_s1_pool_fused takes; yp
+// 16-byte and sw 4-byte aligned.
+void conv_s1_pool_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin,
+                          const float* w, int cout, float* yp, uint8_t* sw, int relu, float* ws,
+                          hipStream_t s);
 
 // dx [N_l][cin] = input gradient of a stride-1 convolution for upstream
 // gradient dy [N_l][cout].  ws: conv_s1_tile_ws(t, l, K, cout, cin) bytes.

@@ -29,6 +29,7 @@
 // of one row.  Chunks write partial sums that a second kernel adds in a fixed
 // order, so results do not depend on scheduling.
 #include "conv_mfma.h"
+#include "pool_fuse.h"
 
 #include "conv_cin.h"
 
@@ -426,18 +427,28 @@ __global__ __launch_bounds__(TB) void k_conv_tile(const int32_t* __restrict__ nb
 // lanes from 32 banks or 16 lanes from 64.  Each x-slab of a group (16
 // positions x 4 quads) is one wave's load instruction.
 // FLIP: input gradient, W'[k][c][n] = W[26-k][n][c].
-template <int WN, int GPB, bool FLIP>
+// POOL (forward only, one reduction chunk): the 2x2x2 max-pool follows the
+// (ReLU'd) output in the epilogue, through a small LDS area per wave; out
+// is then the pooled map [npar][nn] of depth l-1 (row prow[g] for group g,
+// loaded a tile ahead), psw the switches [ngroups][nn], and the workgroups
+// of column block 0 zero an equal share of the rows of empty depth-(l-1)
+// octants (plab[i] == 0).
+template <int WN, int GPB, bool FLIP, bool POOL>
 __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_conv_tile3(const int32_t* __restrict__ nbr,
                                                    int64_t ngroups, const float* __restrict__ x,
                                                    int kk, const float* __restrict__ w, int nn,
                                                    float* __restrict__ out, int relu,
-                                                   float* __restrict__ part) {
+                                                   float* __restrict__ part,
+                                                   const int32_t* __restrict__ prow,
+                                                   const int32_t* __restrict__ plab, int64_t npar,
+                                                   uint8_t* __restrict__ psw) {
   constexpr int K3 = 27, BN = 16 * WN, WM = WAVES / WN;
   constexpr int RB = GPB / 2 / WM;  // row blocks per wave
   static_assert(RB >= 1 && RB * WM * 2 == GPB, "every row block has one wave");
   constexpr int GSTR = 280, XSTR = 68, BUFC = GPB * GSTR;  // in 16-byte chunks
   __shared__ __attribute__((aligned(16))) v4f X0[BUFC];
   __shared__ __attribute__((aligned(16))) v4f X1[BUFC];
+  __shared__ __attribute__((aligned(16))) float PS[WAVES][POOL ? oc::kPoolLdsFloats : 4];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -448,7 +459,30 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const int lb = nx >= 8 ? (bx % 8) * (nx / 8) + bx / 8 : bx;  // XCD-contiguous ranges
   const int64_t g0 = ngroups * lb / nx, g1 = ngroups * (lb + 1) / nx;  // groups [g0, g1)
   const int T = (int)((g1 - g0 + GPB - 1) / GPB);
+  if constexpr (POOL) {
+    if (blockIdx.y == 0) {  // rows of empty depth-(l-1) octants
+      const int64_t r0 = npar * lb / nx, r1 = npar * (lb + 1) / nx;
+      const int c4 = nn / 4, cnt = (int)(r1 - r0) * c4;
+      for (int e = tid; e < cnt; e += TB) {
+        const int64_t i = r0 + e / c4;
+        if (plab[i] == 0)
+          *reinterpret_cast<v4f*>(out + i * nn + 4 * (e % c4)) = v4f{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  }
   if (T <= 0) return;  // uniform over the workgroup
+  // pooled forward: the depth-(l-1) output row of this lane's group in each
+  // of its row blocks, loaded a tile ahead of the epilogue that stores it
+  int32_t prq[RB];
+  auto load_pr = [&](int t) {
+    if constexpr (POOL) {
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        const int64_t g = g0 + (int64_t)t * GPB + 2 * (wm * RB + r) + ((lane >> 4) & 1);
+        prq[r] = g < g1 ? prow[g] : -1;
+      }
+    }
+  };
 
   // loads: wave w fills x-slab w of every group; lane -> chunk (slot 4y + z,
   // stored quad), holding channel quad (stored ^ ((y + 2z) & 3))
@@ -564,7 +598,28 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
   // accumulator j of lane l: output channel 4(l/16) + j, row l % 16; stored
   // after store_order: lane l writes row l/4, channels 4(l%4)..
   const int64_t rowe = 8 * g1;  // rows past the range are not stored
-  auto store_rb = [&](int t, int rb, const v4f& acc) {
+  // pr: the pooled forward's output row of this lane's group
+  auto store_rb = [&](int t, int rb, const v4f& acc, int32_t pr) {
+    if constexpr (POOL) {
+      // through the wave's LDS area: lane o < 32 pools group o/16 of the
+      // row block in channel n0 + o%16
+      v4f v = acc;
+      if (relu) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = fmaxf(v[j], 0.f);
+      }
+      float* ps = &PS[wave][0];
+      oc::pool_put(ps, v, lane);
+      uint32_t sw;
+      const float m = oc::pool_scan(ps, lane, sw);
+      const int c = n0 + (lane & 15);
+      const int64_t g = g0 + (int64_t)t * GPB + 2 * rb + ((lane >> 4) & 1);
+      if (lane < 32 && c < nn && g < g1) {
+        out[(int64_t)pr * nn + c] = m;
+        psw[g * nn + c] = (uint8_t)sw;
+      }
+      return;
+    }
     const int n = n0 + 4 * (lane & 3);
     const int64_t row = 8 * (g0 + (int64_t)t * GPB) + 16 * rb + (lane >> 2);
     const v4f sv = store_order(acc, lane);
@@ -580,7 +635,7 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
   auto epilogue = [&](int t, v4f (&acc)[RB]) {
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
-      store_rb(t, wm * RB + r, acc[r]);
+      store_rb(t, wm * RB + r, acc[r], POOL ? prq[r] : 0);
       acc[r] = v4f{0.f, 0.f, 0.f, 0.f};
     }
   };
@@ -591,6 +646,7 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
     vm_wait0();  // this wave's loads into cur have landed
     __syncthreads();
     if (t > 0) epilogue(t - 1, accp);
+    load_pr(t);  // lands during tile t's MFMAs
 #pragma unroll
     for (int i = 0; i < GPB; ++i) nbc[i] = nbn[i];
     okc = okn;
@@ -631,9 +687,14 @@ __global__ __launch_bounds__(TB) __attribute__((amdgpu_waves_per_eu(2))) void k_
   // live row blocks of the last tile, rb = wm + WM i
   const int rbl = (int)((g1 - g0 - (int64_t)(T - 1) * GPB + 1) / 2);
   for (int rb = wm; rb < rbl; rb += WM) {
+    int32_t pr = 0;
+    if constexpr (POOL) {
+      const int64_t g = g0 + (int64_t)(T - 1) * GPB + 2 * rb + ((lane >> 4) & 1);
+      pr = g < g1 ? prow[g] : -1;
+    }
     v4f a = v4f{0.f, 0.f, 0.f, 0.f};
     compute1(last0 ? X0 : X1, rb, a);
-    store_rb(T - 1, rb, a);
+    store_rb(T - 1, rb, a, pr);
   }
 }
 
@@ -764,6 +825,59 @@ __global__ __launch_bounds__(TB) void k_sum_split(const float* __restrict__ part
     for (int z = 0; z < splits; ++z) s += part[(int64_t)z * n + i];
     out[i] = relu ? fmaxf(s, 0.f) : s;
   }
+}
+
+// k_sum_split followed by the 2x2x2 max-pool (the conv + pool forward with a
+// split reduction): one thread per (depth-(l-1) octant i, channel quad);
+// each of the eight children's sums is formed in k_sum_split's order, ReLU'd
+// when relu, and the first maximum over children 0..7 wins (strict '>').
+// Empty octants get a zero row.  nn a multiple of 4; part, y 16-byte and sw
+// 4-byte aligned.
+__global__ __launch_bounds__(TB) void k_sum_split_pool(const float* __restrict__ part, int splits,
+                                                       int64_t n, const int32_t* __restrict__ labels,
+                                                       int64_t npar, int cv, int relu,
+                                                       float* __restrict__ y,
+                                                       uint8_t* __restrict__ sw) {
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= npar * cv) return;
+  const int64_t i = t / cv;
+  const int cc = (int)(t - i * cv);
+  const int32_t L = labels[i];
+  if (L == 0) {
+    reinterpret_cast<v4f*>(y)[t] = v4f{0.f, 0.f, 0.f, 0.f};
+    return;
+  }
+  const int64_t g = L - 1, n4 = n / 4;
+  const v4f* p = reinterpret_cast<const v4f*>(part) + 8 * g * cv + cc;
+  v4f sk[8];  // the eight children's sums, their loads of one split in flight together
+#pragma unroll
+  for (int k = 0; k < 8; ++k) sk[k] = v4f{0.f, 0.f, 0.f, 0.f};
+  for (int z = 0; z < splits; ++z) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) sk[k] += p[z * n4 + (int64_t)k * cv];
+  }
+  v4f best = {0.f, 0.f, 0.f, 0.f};
+  uint32_t arg = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    v4f s = sk[k];
+    if (relu) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) s[j] = fmaxf(s[j], 0.f);
+    }
+    if (k == 0) {
+      best = s;
+      continue;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (s[j] > best[j]) {
+        best[j] = s[j];
+        arg = (arg & ~(0xffu << (8 * j))) | ((uint32_t)k << (8 * j));
+      }
+  }
+  reinterpret_cast<v4f*>(y)[t] = best;
+  reinterpret_cast<uint32_t*>(sw)[g * cv + cc] = arg;
 }
 
 // Launch of k_sum_split over n entries.
@@ -1385,13 +1499,24 @@ void launch_tile(const oc_octree* t, int l, const TileCfg& c, const float* x, in
   }
 }
 
+// Destination of a pooled forward (conv + ReLU + 2x2x2 max-pool): the
+// pooled rows of depth l-1 and the switches.
+struct PoolOut {
+  float* y;
+  uint8_t* sw;
+};
+
 template <int NR, int GPB, bool FLIP>
 void launch_tile2(const oc_octree* t, int l, const TileCfg& c, const float* x, int kk,
-                  const float* w, int nn, float* out, int relu, float* part, hipStream_t s) {
-  const auto kernel = k_conv_tile3<NR, GPB, FLIP>;
+                  const float* w, int nn, float* out, int relu, float* part, hipStream_t s,
+                  const PoolOut* po = nullptr) {
+  const auto plain = k_conv_tile3<NR, GPB, FLIP, false>;
+  const auto pooled = k_conv_tile3<NR, GPB, FLIP, true>;
+  const bool fuse = !FLIP && po && c.splits == 1;
+  const auto kernel = fuse ? pooled : plain;
   static const int occ = [&] {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, TB, 0) != hipSuccess || n < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, plain, TB, 0) != hipSuccess || n < 1)
       n = 1;
     return n;
   }();
@@ -1401,10 +1526,25 @@ void launch_tile2(const oc_octree* t, int l, const TileCfg& c, const float* x, i
   int64_t px = std::min<int64_t>(G, std::max<int64_t>(1, (int64_t)oc::cu_count() * occ / gyz));
   if (px >= 8) px -= px % 8;
   dim3 grid((unsigned)px, (unsigned)gy, (unsigned)c.splits);
+  if (fuse) {
+    oc::launch_main(kernel, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, kk, w, nn, po->y,
+                    relu, part, (const int32_t*)t->rows[l - 1], (const int32_t*)t->labels[l - 1],
+                    t->N[l - 1], po->sw);
+    return;
+  }
   oc::launch_main(kernel, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, kk, w, nn, out,
-                  relu, part);
+                  relu, part, (const int32_t*)nullptr, (const int32_t*)nullptr, (int64_t)0,
+                  (uint8_t*)nullptr);
   if (c.splits > 1) {
-    sum_split(part, c.splits, t->N[l] * (int64_t)nn, out, relu, s);
+    if (po) {
+      const int cv = nn / 4;
+      const int64_t npar = t->N[l - 1];
+      oc::launch(k_sum_split_pool, dim3((unsigned)oc::cdiv(npar * cv, TB)), dim3(TB), 0, s,
+                 (const float*)part, c.splits, t->N[l] * (int64_t)nn,
+                 (const int32_t*)t->labels[l - 1], npar, cv, relu, po->y, po->sw);
+    } else {
+      sum_split(part, c.splits, t->N[l] * (int64_t)nn, out, relu, s);
+    }
   }
 }
 
@@ -1591,8 +1731,10 @@ namespace oc {
 
 void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, int pass, char* buf,
                          size_t n) {
+  const bool pooled = pass == 3;  // the conv + pool forward (its convolution kernel)
+  if (pooled) pass = 0;
   if (pass != 1 && conv_cin_supported(K, cin, cout)) {
-    conv_cin_kernel_name(cin, pass, buf, n);
+    conv_cin_kernel_name(cin, pooled ? 3 : pass, buf, n);
     return;
   }
   if (pass == 2) {
@@ -1613,7 +1755,8 @@ void conv_s1_kernel_name(const oc_octree* t, int l, int K, int cin, int cout, in
   const int kk = pass == 0 ? cin : cout, nn = pass == 0 ? cout : cin;
   const TileCfg c = pick_tile(K, t->M[l - 1], kk, nn);
   if (c.v2) {
-    snprintf(buf, n, "k_conv_tile3<%d, %d, %s>", c.NR, c.gpb, pass == 0 ? "false" : "true");
+    snprintf(buf, n, "k_conv_tile3<%d, %d, %s, %s>", c.NR, c.gpb, pass == 0 ? "false" : "true",
+             pooled && c.splits == 1 ? "true" : "false");
     return;
   }
   snprintf(buf, n, "k_conv_tile<%d, %d, %d, %d, %d, %s, %s>", K, c.V, c.MR, c.NR, c.WM,
@@ -1643,6 +1786,31 @@ void conv_s1_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin, 
     return;
   }
   dispatch_tile<false>(t, l, K, x, cin, w, cout, y, relu, ws, s);
+}
+
+bool conv_s1_pool_fused(const oc_octree* t, int l, int K, int cin, int cout) {
+  if (conv_cin_supported(K, cin, cout)) return true;
+  if (use_cin_kernel(K, cin, cout)) return false;
+  return pick_tile(K, t->M[l - 1], cin, cout).v2;
+}
+
+void conv_s1_pool_fwd_f32(const oc_octree* t, int l, int K, const float* x, int cin,
+                          const float* w, int cout, float* yp, uint8_t* sw, int relu, float* ws,
+                          hipStream_t s) {
+  if (conv_cin_supported(K, cin, cout)) {
+    conv_cin_pool_fwd(t, l, x, cin, w, cout, yp, sw, relu, s);
+    return;
+  }
+  const TileCfg c = pick_tile(K, t->M[l - 1], cin, cout);
+  const PoolOut po{yp, sw};
+#define OC_T3(NR_, GPB_)                                                              \
+  if (c.NR == NR_ && c.gpb == GPB_) {                                                 \
+    launch_tile2<NR_, GPB_, false>(t, l, c, x, cin, w, cout, nullptr, relu, ws, s, &po); \
+    return;                                                                           \
+  }
+  OC_T3(1, 8) OC_T3(2, 8) OC_T3(2, 4) OC_T3(4, 8) OC_T3(4, 4) OC_T3(4, 2)
+#undef OC_T3
+  oc::set_error("no pooled kernel for cin=%d cout=%d", cin, cout);
 }
 
 void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, int cout,

@@ -38,10 +38,11 @@ def test_trace_classes():
     assert bench.trace_class("k_leaf_mean") == "build"
     assert bench.trace_class("k_route_down<4>") == "pool"
     assert bench.trace_class("k_conv_dwt<false, 16, 2, 4, true, 2>") == "conv_main"
-    assert bench.trace_class("k_cin_fwd<3>") == "conv_main"
-    assert bench.trace_class("Cijk_Ailk_Bljk_BSS_BH") == "conv_main"
+    assert bench.trace_class("k_cin_fwd<3, true>") == "conv_main"
+    assert bench.trace_class("k_conv_tile3<2, 8, false, true>") == "conv_main"
     assert bench.trace_class("k_sum_parts<16, 4>") == "conv_helper"
-    assert bench.trace_class("k_s2_col<unsigned short>") == "conv_helper"
+    assert bench.trace_class("k_sum_split_pool") == "conv_helper"
+    assert bench.trace_class("k_sr_table") == "conv_helper"
     assert bench.trace_class("at::native::vectorized_elementwise_kernel") == "other"
 
 
@@ -131,6 +132,7 @@ def test_accounting_of_deconvolution_gpool_and_stride4():
     assert acc.work("gpool_bwd", gm) == N[4] * 8 * 8 + N[4] * 8 + M[3] * 108
     assert bench.BOUND["gpool_fwd"] == "hbm" and bench.BOUND["deconv_fwd"] == "mfma"
     assert bench.trace_class("k_gpool_fwd<2, true, 4>") == "pool"
-    assert bench.trace_class("k_s2_fwd<4, 4>") == "conv_main"
-    assert bench.trace_class("k_s2_col<float>") == "conv_helper"
+    assert bench.trace_class("k_sr_mm<float, 0, 2, 2, 2, 2>") == "conv_main"
+    assert bench.trace_class("k_sr_dw<unsigned short, 2, 2, 2, 1>") == "conv_main"
+    assert bench.trace_class("k_sr_dyg<float>") == "conv_helper"
     assert bench.op_rate("deconv_fwd", 2e9, 1000.0, False)["unit"] == "TFLOP/s"

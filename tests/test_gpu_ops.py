@@ -388,6 +388,74 @@ def test_pool_unpool_small(seed, B, n, depth, c):
                                   oracle.unpool_bwd(ref.labels(l - 1), g, swr))
 
 
+def _check_conv_pool(ref, tree, l, K, x, w, relu, tag, dtype=torch.float32, yref=None):
+    """oc_conv_pool_fwd against oc_conv_fwd + oc_pool_fwd (bit for bit), the
+    oracle's pooling of the GPU's own depth-l output (bit for bit: the same
+    fp32 values decide) and, when yref (the oracle's float64 convolution) is
+    given, the oracle's conv + ReLU + pooling within the fp32 tolerance."""
+    oc = _oc()
+    xg, wg = _cuda(x, dtype), _cuda(w, dtype)
+    y, sw = oc.oc_conv_pool_fwd(tree, l, K, xg, wg, relu=relu)
+    yl = oc.oc_conv_fwd(tree, l, K, 1, xg, wg, relu=relu)
+    yu, swu = oc.oc_pool_fwd(tree, l, yl)
+    assert torch.equal(y.view(torch.int32), yu.view(torch.int32)), f"{tag}: fused y != unfused"
+    assert torch.equal(sw, swu), f"{tag}: fused switches != unfused"
+    yo, swo = oracle.pool_fwd(ref.labels(l - 1), yl.cpu().numpy())
+    np.testing.assert_array_equal(y.cpu().numpy(), yo)
+    np.testing.assert_array_equal(sw.cpu().numpy(), swo)
+    if yref is not None:
+        yr = oracle.relu_fwd(yref) if relu else yref
+        assert_f32_close(y.cpu().numpy(), oracle.pool_fwd(ref.labels(l - 1), yr)[0], f"{tag} y")
+    # a second call gives the same bits (fixed-order sums, no atomics)
+    y2, sw2 = oc.oc_conv_pool_fwd(tree, l, K, xg, wg, relu=relu)
+    assert torch.equal(y.view(torch.int32), y2.view(torch.int32)) and torch.equal(sw, sw2)
+
+
+CONV_POOL_SMALL = [  # seed, B, n, depth, K, cin, cout, relu, bf16
+    (121, 2, 500, 4, 3, 3, 16, True, False),    # first-layer kernel, pooled epilogue
+    (122, 3, 300, 5, 3, 4, 32, True, False),    # two column blocks
+    (123, 1, 700, 5, 3, 3, 48, False, False),   # no ReLU
+    (124, 2, 600, 5, 3, 16, 32, True, False),   # group-tile kernel, pooled epilogue
+    (125, 3, 400, 4, 3, 16, 16, False, False),
+    (126, 2, 900, 5, 3, 32, 64, True, False),   # split reduction: pooled split sum
+    (127, 2, 500, 4, 3, 64, 128, True, False),
+    (128, 2, 400, 4, 3, 5, 7, True, False),     # other shapes: conv, then pooling
+    (129, 1, 500, 4, 5, 8, 8, True, False),
+    (130, 2, 500, 4, 3, 16, 32, True, True),
+]
+
+
+@pytest.mark.parametrize("seed,B,n,depth,K,cin,cout,relu,bf16", CONV_POOL_SMALL)
+def test_conv_pool_small(seed, B, n, depth, K, cin, cout, relu, bf16):
+    """Convolution + ReLU + 2x2x2 max-pool in one call (Sec. 3.2, Sec. 4)."""
+    print(f"[conv_pool] seed={seed} B={B} d={depth} K={K} {cin}->{cout} relu={relu} bf16={bf16}",
+          flush=True)
+    pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
+    ref, tree = _trees(pts, nrm, offs, depth)
+    l = depth
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((ref.num(l), cin)).astype(np.float32)
+    w = (rng.standard_normal((K ** 3, cin, cout)) / np.sqrt(K ** 3 * cin)).astype(np.float32)
+    if bf16:
+        x, w = bf16_round(x), bf16_round(w)
+    yref = oracle.conv_fwd(ref.neighbors(l, K), x, w)
+    _check_conv_pool(ref, tree, l, K, x, w, relu, f"conv_pool {seed}",
+                     torch.bfloat16 if bf16 else torch.float32, yref)
+
+
+def test_conv_pool_one_point_tree():
+    """A one-point tree (one sibling group per depth) down to depth 1."""
+    pts = np.array([[0.3, 0.6, 0.9]], np.float32)
+    ref, tree = _trees(pts, np.ones((1, 3), np.float32), [0, 1], 3, 0)
+    rng = np.random.default_rng(17)
+    for l in (1, 2, 3):
+        for cin, cout in ((3, 16), (16, 16), (32, 32)):
+            x = rng.standard_normal((ref.num(l), cin)).astype(np.float32)
+            w = rng.standard_normal((27, cin, cout)).astype(np.float32)
+            _check_conv_pool(ref, tree, l, 3, x, w, True, f"one point l={l} {cin}->{cout}",
+                             yref=oracle.conv_fwd(ref.neighbors(l, 3), x, w))
+
+
 def test_conv_edge_cases():
     oc = _oc()
     # a single shape with one point, full depth 0: depth-1 has 8 octants, one group
@@ -607,6 +675,11 @@ def test_workload_full_size(name):
             n_out = ref.num(l - (L.stride.bit_length() - 1))
             dy = synth.make_upstream(w_, li, n_out, L.cout)
             _check_conv_full(ref, tree, l, K, L.stride, x, w, L.relu, dy, f"{name}/{li}")
+            nxt = w_.layers[li + 1] if li + 1 < len(w_.layers) else None
+            if nxt is not None and nxt.op == "pool" and L.stride == 1 and L.dtype != "bf16":
+                # the network runs this pair as one conv + pool call
+                print(f"[{name}/{li}] conv + pool d{l}", flush=True)
+                _check_conv_pool(ref, tree, l, K, x, w, L.relu, f"{name}/{li}+pool")
             if L.dtype == "bf16":
                 _check_conv_full(ref, tree, l, K, L.stride, x, w, L.relu, dy, f"{name}/{li}/bf16",
                                  dtype=torch.bfloat16)

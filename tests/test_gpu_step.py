@@ -1,5 +1,6 @@
 """The timed step of the bench, end to end at full size: the call sequence
-bench.py runs (fused ReLU in the forward, the ReLU's backward inside the
+bench.py runs (fused ReLU in the forward, conv + ReLU + pool in one call
+where a pooling follows a convolution, the ReLU's backward inside the
 pooling's routing, no input gradient for the first layer, separate input-
 and weight-gradient calls) on the octree the GPU builds, every tensor of the
 step against the oracle.
@@ -45,11 +46,22 @@ def test_bench_step_end_to_end(name):
     torch.cuda.synchronize()
     fwd, bwd = step.record["fwd"], step.record["bwd"]
     print(f"[step] {name}: forward", flush=True)
+    unpooled = {}  # depth-l outputs of conv + pool calls, recomputed unpooled
     for li, L in enumerate(wl.layers):
         x, y, sw = (_np(t) for t in fwd[li])
         l = L.depth
         if li == 0 and wl.signal_input:
             assert_f32_close(x, ref.signal, "signal", rtol=1e-6, atol=1e-7)
+        if L.op == "conv" and y is None:
+            # run with the pooling above it in one call: its output here is
+            # the same kernel's unpooled forward on the same inputs (the two
+            # agree bit for bit, a test of the operations)
+            assert step.pooled(li)
+            y = _np(oc.oc_conv_fwd(tree, l, L.ksize, L.stride, fwd[li][0], step.weights[li],
+                                   relu=L.relu))
+            unpooled[li + 1] = y
+        elif L.op == "pool" and x is None:
+            x = unpooled[li]
         if L.op == "conv":
             nb = ref.neighbors(l, L.ksize, stride=L.stride)
             pre = oracle.conv_fwd(nb, x, _np(step.weights[li]))
@@ -76,6 +88,8 @@ def test_bench_step_end_to_end(name):
         l = L.depth
         g_in, g_out, dw = (_np(t) for t in bwd[li])
         x, y, sw = (_np(t) for t in fwd[li])
+        if L.op == "pool" and x is None:
+            x = unpooled[li]
         if L.op == "conv":
             nb = ref.neighbors(l, L.ksize, stride=L.stride)
             w = _np(step.weights[li])
