@@ -114,11 +114,17 @@ def parse():
     ap.add_argument("--layers", action="store_true", help="also print per-layer timings to stderr")
     ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
                     help="2: weight gradients on a second stream beside the rest of the backward")
+    ap.add_argument("--build-inline", action="store_true",
+                    help="run the next batch's build on the network's stream, between "
+                         "steps, instead of on its own stream beside the network")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="after the steps, run an elementwise copy (y = -x) of MIB MiB three "
                          "times: the known-size kernel that calibrates the HBM byte counters")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the HBM counter summary of two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--summarize-mfma", nargs=2, metavar=("PMC_DIR", "PROF_DIR"),
+                    help="print the matrix-core counters of a --pmc run (MFMA_COUNTERS) "
+                         "against a --kernel-trace --stats run, and exit")
     ap.add_argument("--summarize-trace", nargs=2, metavar=("PROF_DIR", "PROF_LOG"),
                     help="print the per-class kernel time of a rocprofv3 --kernel-trace --stats "
                          "run of this script (its output directory and its stdout) and exit")
@@ -254,6 +260,56 @@ def summarize_counters(fetch_dir, write_dir, copy_mib, workload):
     print("\n```json\n" + json.dumps(rec, indent=1) + "\n```")
 
 
+MFMA_COUNTERS = ("MfmaUtil", "SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_INSTS_VALU_MFMA_MOPS_BF16",
+                 "SQ_WAVE_CYCLES", "SQ_WAIT_INST_LDS", "SQ_LDS_BANK_CONFLICT",
+                 "SQ_ACTIVE_INST_LDS")
+
+
+def summarize_mfma(pmc_dir, prof_dir):
+    """Matrix-core use of each kernel from a rocprofv3 --pmc run with
+    MFMA_COUNTERS (MfmaUtil: the share of the run's busy cycles during which
+    the matrix units of all SIMDs were busy, rocprofv3's own derived counter)
+    and the kernel time of a --kernel-trace --stats run of the same command:
+    the MFMA flops the hardware executed (MOPS x 512) per second of kernel
+    time, padding included, against the dense fp32 or bf16 peak; and the
+    share of wave cycles spent waiting on LDS and LDS bank conflicts per LDS
+    instruction."""
+    per = {}
+    for ctr in MFMA_COUNTERS:
+        for k, v in _counter_rows(pmc_dir, ctr):
+            per.setdefault(_short_name(k), {}).setdefault(ctr, []).append(v)
+    avg_us = {}
+    for f in glob.glob(os.path.join(prof_dir, "**", "*kernel_stats.csv"), recursive=True):
+        with open(f, newline="") as fh:
+            for r in csv.DictReader(fh):
+                avg_us[_short_name(r["Name"])] = float(r["AverageNs"]) / 1e3
+
+    def mean(v, c):
+        x = v.get(c)
+        return sum(x) / len(x) if x else 0.0
+
+    print("| kernel | dispatches | avg us | MfmaUtil % | MFMA TFLOP/s (MOPS x 512 / time) | "
+          "share of peak | LDS wait / wave cycles | bank conflicts / LDS instr |")
+    print("|---|---|---|---|---|---|---|---|")
+    rows = []
+    for k, v in per.items():
+        mops32, mops16 = mean(v, "SQ_INSTS_VALU_MFMA_MOPS_F32"), mean(v, "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+        if mops32 + mops16 <= 0 or k not in avg_us:
+            continue
+        t = avg_us[k]
+        bf16 = mops16 > mops32
+        tf = (mops32 + mops16) * 512 / (t * 1e-6) / 1e12
+        peak = PEAK["bf16_TFLOPs" if bf16 else "fp32_TFLOPs"]
+        wc = mean(v, "SQ_WAVE_CYCLES")
+        lds = mean(v, "SQ_ACTIVE_INST_LDS")
+        rows.append((k, len(v.get("MfmaUtil", [])), t, mean(v, "MfmaUtil"), tf, tf / peak,
+                     mean(v, "SQ_WAIT_INST_LDS") / wc if wc else 0.0,
+                     mean(v, "SQ_LDS_BANK_CONFLICT") / lds if lds else 0.0, bf16))
+    for k, n, t, util, tf, frac, lw, bc, bf16 in sorted(rows, key=lambda r: -r[2] * r[1]):
+        print(f"| `{k}` | {n} | {t:.2f} | {util:.1f} | {tf:.1f} ({'bf16' if bf16 else 'fp32'}) | "
+              f"{100 * frac:.1f}% | {100 * lw:.1f}% | {bc:.2f} |")
+
+
 def op_rate(cls, work, us, bf16):
     """Achieved rate of an op class from its algorithmic work (flops of a conv
     class, HBM bytes otherwise) and its time per step, against the peak."""
@@ -288,6 +344,15 @@ def trace_class(name):
         if any(name.startswith(p) for p in prefixes):
             return cls
     return "other"
+
+
+def pooled_pair(wl, li):
+    """True when conv layer li and the 2x2x2 max-pool after it run as one
+    conv + pool call (stride 1, fp32)."""
+    ls = wl.layers
+    L = ls[li]
+    return (L.op == "conv" and L.stride == 1 and L.dtype == "f32" and li + 1 < len(ls)
+            and ls[li + 1].op == "pool" and ls[li + 1].depth == L.depth)
 
 
 def summarize_trace(prof_dir, prof_log):
@@ -335,8 +400,13 @@ def summarize_trace(prof_dir, prof_log):
         names.setdefault(cls, []).append(k)
     bf16 = any(L.op == "conv" and L.dtype == "bf16" for L in wl.layers)
     flops, _ = acc.conv_flops()
-    pool_bytes = sum(acc.work(t, L) for L in wl.layers if L.op in ("pool", "unpool", "gpool")
-                     for t in (L.op + "_fwd", L.op + "_bwd"))
+    # a pooling run inside the convolution below it (conv + pool calls) has no
+    # forward kernel of its own: its bytes are not the pooling kernels' work
+    fused = {i + 1 for i, L in enumerate(wl.layers) if pooled_pair(wl, i)}
+    pool_bytes = sum(acc.work(t, L) for i, L in enumerate(wl.layers)
+                     if L.op in ("pool", "unpool", "gpool")
+                     for t in (L.op + "_fwd", L.op + "_bwd")
+                     if not (t == "pool_fwd" and i in fused))
     rows = []
     if us.get("build"):
         rows.append(("build", "build", acc.work("build", None), us["build"]))
@@ -428,7 +498,14 @@ class Accounting:
         if tag == "pool_fwd":
             return N[l] * c * 4 + N[l - 1] * 4 + N[l - 1] * c * 4 + M[l - 1] * c
         if tag == "pool_bwd":
-            return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l] * c * 4
+            # per non-empty parent: its gradient row, switches, row index and
+            # (a ReLU'd conv below: its pooled output, the ReLU's mask); every
+            # child row out
+            ls = self.wl.layers
+            i = next(k for k, X in enumerate(ls) if X is L)
+            P = ls[i - 1] if i > 0 else None
+            masked = P is not None and P.op == "conv" and P.relu
+            return M[l - 1] * c * (9 if masked else 5) + M[l - 1] * 4 + N[l] * c * 4
         if tag == "unpool_fwd":  # parent rows and switches in, every child row out
             return M[l - 1] * c * 5 + M[l - 1] * 4 + N[l] * c * 4
         if tag == "unpool_bwd":  # the routed child of each (parent, channel) in, parent rows out
@@ -513,6 +590,9 @@ class Step(Accounting):
             if L0.dtype == "bf16":
                 self.x0 = self.x0.to(torch.bfloat16)
         self.side = None  # stream for the weight gradients (None: all on one stream)
+        # stream for the next batch's build (None: on the network's stream)
+        self.bstream = None
+        self.cur_ready = None  # event: the current octree's build is done
         self.events = None  # {key: [(start, end, layer), ...]} when recording
         # when a list: every op of the step (not the build) is run with all of
         # its kernels bracketed (oc_profile_calls), one CallProfile per op
@@ -543,12 +623,8 @@ class Step(Accounting):
         tree.free()
 
     def pooled(self, li):
-        """True when conv layer li and the 2x2x2 max-pool after it run as one
-        conv + pool call (stride 1, fp32)."""
-        ls = self.wl.layers
-        L = ls[li]
-        return (L.op == "conv" and L.stride == 1 and L.dtype == "f32" and li + 1 < len(ls)
-                and ls[li + 1].op == "pool" and ls[li + 1].depth == L.depth)
+        """True when conv layer li and the pooling after it run as one call."""
+        return pooled_pair(self.wl, li)
 
     # --- one step ----------------------------------------------------------
     def key(self, tag, li):
@@ -613,17 +689,38 @@ class Step(Accounting):
         then the rest of the next build.  As in the paper's training (Sec. 3.2,
         last paragraph) the next batch's octree is prepared while the current
         one trains: the host waits for the next build's counts while the device
-        runs the network.  The device work of the build is not run beside the
-        network: the network's persistent kernels hold every CU, and a build
-        kernel queued beside them delays them more than it costs in line."""
+        runs the network.  With a build stream (bstream) the build's kernels
+        run beside the network's (the build is a chain of short,
+        latency-bound kernels); the network waits for the build of its octree
+        through an event, and the octree's arrays are marked as used on the
+        network's stream before it is freed."""
         self.ncall = {}
+        torch = self.torch
+        B = self.bstream
         if getattr(self, "cur", None) is None:
             self.cur = self._finish(self._begin())
-        job = self._begin()
+            self.cur_ready = None
+        A = torch.cuda.current_stream()
+        if B is None:
+            job = self._begin()
+        else:
+            B.wait_stream(A)  # the build's stream follows the previous step
+            with torch.cuda.stream(B):
+                job = self._begin()
         tree = self.cur
+        if self.cur_ready is not None:
+            A.wait_event(self.cur_ready)
         g = self.network(tree)
-        tree.free()
-        self.cur = self._finish(job)
+        if B is None:
+            tree.free()
+            self.cur = self._finish(job)
+        else:
+            tree.record_stream(A)
+            tree.free()
+            with torch.cuda.stream(B):
+                self.cur = self._finish(job)
+                self.cur_ready = torch.cuda.Event()
+                self.cur_ready.record(B)
         self.nstep += 1
         return g
 
@@ -1041,6 +1138,9 @@ def main():
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace)
         return
+    if args.summarize_mfma:
+        summarize_mfma(*args.summarize_mfma)
+        return
     if args.gpus != 1:
         print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
               f"(the path would shard by shape with one dW all-reduce per layer, not built)",
@@ -1062,6 +1162,8 @@ def main():
     step = (TrainStep if wl.train else Step)(oc, torch, synth, wl)
     if args.streams == 2:
         step.side = torch.cuda.Stream()  # default priority, like the main stream
+    if not args.build_inline:
+        step.bstream = torch.cuda.Stream()  # default priority, like the main stream
     flops, octants = step.conv_flops()
     print(f"[bench] N_l = {step.N}, M_l = {step.M}", file=sys.stderr, flush=True)
 

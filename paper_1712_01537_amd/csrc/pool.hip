@@ -94,30 +94,36 @@ __global__ __launch_bounds__(TB) void k_pool_fwd(const float* __restrict__ x,
 // Routing through the switches (pool backward == unpool forward):
 // out[8g + k][c] = (sw[g][c] == k) ? in[rows[g]][c] : 0 for every child row.
 // With ymask, the routed value is also zeroed where ymask[rows[g]][c] <= 0.
+// One thread per (non-empty parent g, VEC channels): it reads the parent's
+// row, mask and switches once and writes all eight child rows (consecutive
+// threads take consecutive channels, so each of the eight stores of a wave
+// covers whole child rows).
 template <int VEC>
 __global__ __launch_bounds__(TB) void k_route_down(const float* __restrict__ in,
                                                    const float* __restrict__ ymask,
                                                    const uint8_t* __restrict__ sw,
-                                                   const int32_t* __restrict__ rows, int64_t n_l,
+                                                   const int32_t* __restrict__ rows, int64_t ngroups,
                                                    int cv, float* __restrict__ out) {
   using F = typename Vec<VEC>::f;
   using U = typename Vec<VEC>::u8;
   const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (t >= n_l * cv) return;
-  const int64_t row = t / cv;
-  const int cc = (int)(t - row * cv);
-  const int64_t g = row >> 3;
-  const uint8_t k = (uint8_t)(row & 7);
-  const U s = reinterpret_cast<const U*>(sw)[g * cv + cc];
+  if (t >= ngroups * cv) return;
+  const int64_t g = t / cv;
+  const int cc = (int)(t - g * cv);
+  const U s = reinterpret_cast<const U*>(sw)[t];
   const int64_t src = (int64_t)rows[g] * cv + cc;
   const F v = reinterpret_cast<const F*>(in)[src];
   F m;
   if (ymask) m = reinterpret_cast<const F*>(ymask)[src];
-  F o;
+  F* dst = reinterpret_cast<F*>(out) + 8 * g * cv + cc;
 #pragma unroll
-  for (int e = 0; e < VEC; ++e)
-    set(o, e, comp(s, e) == k && (!ymask || comp(m, e) > 0.0f) ? comp(v, e) : 0.0f);
-  reinterpret_cast<F*>(out)[t] = o;
+  for (int k = 0; k < 8; ++k) {
+    F o;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e)
+      set(o, e, comp(s, e) == k && (!ymask || comp(m, e) > 0.0f) ? comp(v, e) : 0.0f);
+    dst[(int64_t)k * cv] = o;
+  }
 }
 
 // Unpool backward: dx[i][c] = dy[8g + sw[g][c]][c] for label L = g+1 > 0.
@@ -550,15 +556,15 @@ static oc_status route_down(const oc_octree* t, int32_t l, const float* in, cons
                             const char* who) {
   oc_status st = check_common(t, l, c, in, out, sw, who);
   if (st != OC_OK) return st;
-  const int64_t n = t->N[l];
-  if (n == 0) return OC_OK;
+  const int64_t G = t->M[l - 1];  // the non-empty parents: N_l = 8 G child rows
+  if (G == 0) return OC_OK;
   if (vec4_ok(c, in, out, sw) && (uintptr_t)ymask % 16 == 0) {
     const int cv = c / 4;
-    oc::launch_main(k_route_down<4>, dim3(grid_for(n * cv)), dim3(TB), s, in, ymask, sw,
-                       (const int32_t*)t->rows[l - 1], n, cv, out);
+    oc::launch_main(k_route_down<4>, dim3(grid_for(G * cv)), dim3(TB), s, in, ymask, sw,
+                       (const int32_t*)t->rows[l - 1], G, cv, out);
   } else {
-    oc::launch_main(k_route_down<1>, dim3(grid_for(n * c)), dim3(TB), s, in, ymask, sw,
-                       (const int32_t*)t->rows[l - 1], n, c, out);
+    oc::launch_main(k_route_down<1>, dim3(grid_for(G * c)), dim3(TB), s, in, ymask, sw,
+                       (const int32_t*)t->rows[l - 1], G, c, out);
   }
   OC_LAUNCH_CHECK();
   return OC_OK;

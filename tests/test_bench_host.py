@@ -103,6 +103,24 @@ def test_summarize_trace(tmp_path, capsys):
     assert "`k_conv_tile3<4, 8, false>` | 15 | 40.00 |" in out
 
 
+def test_accounting_of_pool_backward():
+    """The routing's bytes: per non-empty parent its gradient row, switches
+    and row index, plus the pooled output when a ReLU'd convolution lies
+    below (the ReLU's mask); every child row written."""
+    N = [2, 16, 128, 1024]
+    M = [2, 16, 100, 500]
+    wl = synth.Workload("t", 0, 3, 2, 1000, "union", (
+        synth.Layer("conv", 3, 3, 16, relu=True),
+        synth.Layer("pool", 3, 16, 16),
+        synth.Layer("conv", 2, 16, 16),
+        synth.Layer("pool", 2, 16, 16),
+    ), signal_input=False)
+    acc = bench.Accounting(wl, N, M, 2000)
+    _, p3, _, p2 = wl.layers
+    assert acc.work("pool_bwd", p3) == M[2] * 16 * 9 + M[2] * 4 + N[3] * 16 * 4
+    assert acc.work("pool_bwd", p2) == M[1] * 16 * 5 + M[1] * 4 + N[2] * 16 * 4
+
+
 def test_accounting_of_deconvolution_gpool_and_stride4():
     """Flops and bytes of the ops added beside the convolution, computed by
     hand from the per-depth sizes."""
