@@ -206,8 +206,17 @@ def _check(rc: int):
         raise OcError(rc, load().oc_last_error().decode())
 
 
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
 def _stream():
-    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    """The current stream of the current device, as a raw handle (torch's
+    C-level accessor when present: the Python one costs several
+    microseconds per call, which adds up over the dozens of calls a step
+    makes)."""
+    if _raw_stream is not None:
+        return _raw_stream(torch._C._cuda_getDevice())
+    return torch.cuda.current_stream().cuda_stream
 
 
 def _dev(t: torch.Tensor, name: str, dtype=None, shape=None):

@@ -8,11 +8,13 @@
 // and Szegedy 2015): per channel, the mean and biased variance over all n
 // rows of the feature map.  The statistics are reductions over up to millions
 // of rows, done in double precision and in a fixed order: each block sums a
-// contiguous range of rows per channel (threads over channels and rows, then
-// a fixed-order tree through LDS) into a partial, and one thread per channel
-// adds the partials in block order.  The variance is a second pass over
-// (x - mean)^2, as the definition states (no sum-of-squares cancellation).
-// Results are reproducible bit for bit.
+// contiguous range of rows per channel (threads over channels and rows, four
+// rows in flight per thread, then the row lanes in order through LDS) into a
+// partial, and one block per channel adds the partials (strided over its
+// threads, then a fixed tree through LDS).  The block count gives each
+// thread about 16 rows, so neither pass waits on a long chain of loads.  The
+// variance is a second pass over (x - mean)^2, as the definition states (no
+// sum-of-squares cancellation).  Results are reproducible bit for bit.
 //
 // The head works on a batch of B shapes (B x 1024 x 128 multiply-adds for the
 // first FC layer at depth 6): a few microseconds of plain FMA kernels, bound
@@ -24,11 +26,15 @@
 namespace {
 
 constexpr int TB = 256;
-constexpr int BN_MAX_BLOCKS = 512;
+constexpr int BN_MAX_BLOCKS = 1024;
 
 inline unsigned grid_for(int64_t n) { return (unsigned)oc::cdiv(n, TB); }
 
-int bn_blocks(int64_t n) { return (int)std::max<int64_t>(1, std::min<int64_t>(BN_MAX_BLOCKS, oc::cdiv(n, 256))); }
+// Partial blocks of a reduction over n rows of c channels: about 16 rows per
+// thread.
+int bn_blocks(int64_t n, int c) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>(BN_MAX_BLOCKS, oc::cdiv(n * c, TB * 16)));
+}
 
 // Thread layout of the reductions: channel ch = tid % cc of a group of cc
 // channels (cc = min(c, 256)), row lane tid / cc of rl = 256 / cc lanes; the
@@ -55,6 +61,7 @@ __global__ __launch_bounds__(TB) void k_bn_partial(const float* __restrict__ x,
     if (lane_r < rl && ch < c) {
       const double m = mode == 0 ? 0.0 : (double)mean[ch];
       const double is = mode == 2 ? (double)invstd[ch] : 0.0;
+#pragma unroll 4
       for (int64_t r = r0 + lane_r; r < r1; r += rl) {
         const double v = (double)x[r * c + ch];
         if (mode == 0) {
@@ -85,21 +92,35 @@ __global__ __launch_bounds__(TB) void k_bn_partial(const float* __restrict__ x,
   }
 }
 
-// Per channel, the partials added in block order.
+// Per channel (one block each), the nb partials: thread t adds partials
+// t, t + TB, ... in order, then a fixed tree through LDS.
 // mode 0: mean = sum / n.  mode 1: invstd = 1 / sqrt(sum / n + eps).
 // mode 2: dbeta = sum dy, dgamma = sum dy x_hat.
 __global__ __launch_bounds__(TB) void k_bn_final(const double* __restrict__ part, int nb, int c,
                                                  int64_t n, int mode, float eps,
                                                  float* __restrict__ out0,
                                                  float* __restrict__ out1) {
-  const int ch = blockIdx.x * TB + threadIdx.x;
-  if (ch >= c) return;
+  __shared__ double red[2][TB];
+  const int ch = blockIdx.x, tid = threadIdx.x;
   const int outs = mode == 2 ? 2 : 1;
   double a0 = 0.0, a1 = 0.0;
-  for (int b = 0; b < nb; ++b) {
+  for (int b = tid; b < nb; b += TB) {
     a0 += part[((int64_t)b * c + ch) * outs];
     if (outs == 2) a1 += part[((int64_t)b * c + ch) * outs + 1];
   }
+  red[0][tid] = a0;
+  red[1][tid] = a1;
+  __syncthreads();
+  for (int h = TB / 2; h > 0; h >>= 1) {
+    if (tid < h) {
+      red[0][tid] += red[0][tid + h];
+      red[1][tid] += red[1][tid + h];
+    }
+    __syncthreads();
+  }
+  if (tid != 0) return;
+  a0 = red[0][0];
+  a1 = red[1][0];
   if (mode == 0) {
     out0[ch] = (float)(a0 / (double)n);
   } else if (mode == 1) {
@@ -119,7 +140,7 @@ __global__ __launch_bounds__(TB) void k_bn_apply(const float* __restrict__ x, in
                                                  float* __restrict__ y) {
   const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
   if (e >= n * c) return;
-  const int ch = (int)(e % c);
+  const int ch = n * c <= 0xffffffffll ? (int)((uint32_t)e % (uint32_t)c) : (int)(e % c);
   float v = (x[e] - mean[ch]) * invstd[ch] * gamma[ch] + beta[ch];
   y[e] = relu ? fmaxf(v, 0.f) : v;
 }
@@ -135,7 +156,7 @@ __global__ __launch_bounds__(TB) void k_bn_bwd_apply(const float* __restrict__ x
                                                      float* __restrict__ dx) {
   const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
   if (e >= n * c) return;
-  const int ch = (int)(e % c);
+  const int ch = n * c <= 0xffffffffll ? (int)((uint32_t)e % (uint32_t)c) : (int)(e % c);
   const float inv_n = 1.f / (float)n;
   const float xh = (x[e] - mean[ch]) * invstd[ch];
   dx[e] = gamma[ch] * invstd[ch] * (dy[e] - dbeta[ch] * inv_n - xh * dgamma[ch] * inv_n);
@@ -247,7 +268,7 @@ extern "C" {
 
 size_t oc_bn_workspace(int64_t n, int32_t c) {
   if (n < 1 || c < 1) return 0;
-  return oc::align256((size_t)bn_blocks(n) * c * 2 * sizeof(double));
+  return oc::align256((size_t)bn_blocks(n, c) * c * 2 * sizeof(double));
 }
 
 oc_status oc_bn_fwd(int64_t n, int32_t c, const float* x, const float* gamma, const float* beta,
@@ -260,9 +281,9 @@ oc_status oc_bn_fwd(int64_t n, int32_t c, const float* x, const float* gamma, co
   if (!ws || ws_bytes < oc_bn_workspace(n, c))
     return oc::fail(OC_ERR_ARG, "oc_bn_fwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0,
                     oc_bn_workspace(n, c));
-  const int nb = bn_blocks(n);
+  const int nb = bn_blocks(n, c);
   double* part = (double*)ws;
-  const unsigned gc = (unsigned)oc::cdiv(c, TB);
+  const unsigned gc = (unsigned)c;
   oc::launch(k_bn_partial, dim3(nb), dim3(TB), 0, s, x, (const float*)nullptr, n, (int)c, 0,
              (const float*)nullptr, (const float*)nullptr, part);
   oc::launch(k_bn_final, dim3(gc), dim3(TB), 0, s, (const double*)part, nb, (int)c, n, 0, eps,
@@ -287,10 +308,10 @@ oc_status oc_bn_bwd(int64_t n, int32_t c, const float* x, const float* dy, const
   if (!ws || ws_bytes < oc_bn_workspace(n, c))
     return oc::fail(OC_ERR_ARG, "oc_bn_bwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0,
                     oc_bn_workspace(n, c));
-  const int nb = bn_blocks(n);
+  const int nb = bn_blocks(n, c);
   double* part = (double*)ws;
   oc::launch(k_bn_partial, dim3(nb), dim3(TB), 0, s, x, dy, n, (int)c, 2, mean, invstd, part);
-  oc::launch(k_bn_final, dim3((unsigned)oc::cdiv(c, TB)), dim3(TB), 0, s, (const double*)part, nb,
+  oc::launch(k_bn_final, dim3((unsigned)c), dim3(TB), 0, s, (const double*)part, nb,
              (int)c, n, 2, 0.f, dbeta, dgamma);
   oc::launch_main(k_bn_bwd_apply, dim3(grid_for(n * c)), dim3(TB), s, x, dy, n, (int)c, mean,
                   invstd, gamma, (const float*)dgamma, (const float*)dbeta, dx);
