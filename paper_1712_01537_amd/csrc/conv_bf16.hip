@@ -89,6 +89,11 @@ __device__ __forceinline__ void vm_wait0() { __builtin_amdgcn_s_waitcnt(0x0F70);
 __device__ __forceinline__ void gload16(v4u& r, const void* src) {
   asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(src) : "memory");
 }
+// The same with a wave-uniform 64-bit base in scalar registers and a 32-bit
+// per-lane byte offset (one vector register per address instead of two).
+__device__ __forceinline__ void gload16s(v4u& r, uint32_t voff, const void* sbase) {
+  asm volatile("global_load_dwordx4 %0, %1, %2" : "=v"(r) : "v"(voff), "s"(sbase) : "memory");
+}
 // Wait until at most N vector memory operations of this wave are outstanding
 // (they complete in issue order), then hand the registers w over as written.
 template <int N>
@@ -399,6 +404,271 @@ __global__ __launch_bounds__(512) void k_conv_bf(const int32_t* __restrict__ nbr
 }
 
 // ---------------------------------------------------------------------------
+// The same forward / input gradient over tiles of 16 sibling groups (128 rows,
+// k_conv_bfw): every weight read from L2 then feeds 8 row blocks instead of 4,
+// which halves the weight traffic per row (the whole W is read once per
+// tile).  To fit 16 groups' union blocks, a slab holds one 32-channel half
+// of one x-slab (16 groups x S^2 positions x 4 pieces); the phases are
+// (half h, x-offset dx), h outer, and phase (h, dx) reads slabs h S + dx and
+// h S + dx + 1.  A ring of four slab buffers keeps two slabs in flight
+// beside the two being read (the first phase of a half needs two new ones).
+// Piece o of position (px, py, pz) sits at o ^ (2 (px & 1) + (py & 1)), and
+// positions are 64 bytes apart, so the eight children of a group read eight
+// distinct 16-byte bank groups.  A phase has K^2 steps (taps); each wave takes
+// NFULL whole steps (all 8 row blocks: 8 LDS reads feed 32 MFMAs) and one
+// row block of the leftover step.  Waits are compile-time counts of younger
+// loads from a replay of the fixed issue order (BfwShape::younger).  The eight waves'
+// partial tiles are added in wave order through LDS, 32 rows per round.
+template <int K, int HC>
+struct BfwShape {
+  static constexpr int R = (K - 1) / 2, S = K + 1, S2 = S * S, K2 = K * K, K3 = K2 * K;
+  static constexpr int GT = 16, NW = 8, NRB = GT / 2;
+  static constexpr int SLAB = GT * S2 * 4;  // 16-byte pieces of one slab buffer
+  static constexpr int NB = 4;              // slab buffers
+  static constexpr int NSL = HC * S;        // slabs of a tile
+  static constexpr int NPH = HC * K;        // phases
+  static constexpr int NFULL = K2 / NW, LEFT = K2 % NW;
+  static_assert(LEFT * NRB == NW, "the leftover step's row blocks are one per wave");
+  static constexpr int MI = NFULL + 1;      // items per phase and wave
+  static constexpr int NI = NPH * MI;       // items of the tile
+  static constexpr int RW = 3;              // weight register sets
+  static constexpr int NDMA = GT * S2 * 4 / 64;   // DMA instructions of a slab
+  static constexpr int DC = (NDMA + NW - 1) / NW;  // ... per wave
+  static constexpr int RS = 68;                    // floats per row of a reduction slot
+  static constexpr int RED = NW * 32 * RS;         // floats of one reduction round
+  static constexpr int NV = (NB * SLAB * 16 > RED * 4 ? NB * SLAB * 16 : RED * 4) / 16;
+  static constexpr int slab_of_phase(int ph) { return (ph / K) * S + ph % K; }
+  static constexpr int last_slab(int ph) {  // slabs issued by the start of phase ph
+    return slab_of_phase(ph) + 3 < NSL - 1 ? slab_of_phase(ph) + 3 : NSL - 1;
+  }
+  static constexpr int NPRE = NSL < 3 ? NSL : 3;  // slabs issued before phase 0
+  // Replay of a wave's issue order: stages (DC loads each) and weight sets
+  // (4 loads each).  what = 0: loads issued after stage `idx` when phase
+  // `at` starts (before its own stages); what = 1: loads issued after W(idx)
+  // when item idx starts.
+  static constexpr int younger(int what, int idx, int at) {
+    int stage_end[2 * 6] = {};
+    int w_end[2 * 5 * 4] = {};
+    int ops = 0, issued = -1;
+    for (int s = 0; s < NPRE; ++s) {
+      ops += DC;
+      stage_end[s] = ops;
+      issued = s;
+    }
+    for (int j = 0; j <= RW - 2; ++j)
+      if (j < NI) {
+        ops += 4;
+        w_end[j] = ops;
+      }
+    for (int ph = 0; ph < NPH; ++ph) {
+      if (what == 0 && at == ph) return ops - stage_end[idx];
+      for (int i = 0; i < MI; ++i) {
+        const int n = ph * MI + i;
+        if (what == 1 && idx == n) return ops - w_end[n];
+        if (n + RW - 1 < NI) {
+          ops += 4;
+          w_end[n + RW - 1] = ops;
+        }
+        if (i == 0) {  // the phase's stages, after its first item
+          for (int s = issued + 1; s <= last_slab(ph); ++s) {
+            ops += DC;
+            stage_end[s] = ops;
+            issued = s;
+          }
+        }
+      }
+    }
+    return 0;
+  }
+};
+
+template <int K, int HC, bool FLIP>
+__global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nbr, int64_t ngroups,
+                                                   const uint16_t* __restrict__ x, int kk,
+                                                   const uint16_t* __restrict__ wp, int nn,
+                                                   int chunk, float* __restrict__ out, int acc_in,
+                                                   int relu) {
+  using B = BfwShape<K, HC>;
+  constexpr int R = B::R, S = B::S, S2 = B::S2, K2 = B::K2, K3 = B::K3;
+  constexpr int GT = B::GT, NW = B::NW, NRB = B::NRB, SLAB = B::SLAB, NB = B::NB;
+  constexpr int NFULL = B::NFULL, MI = B::MI, NI = B::NI, RW = B::RW, DC = B::DC;
+  constexpr int NDMA = B::NDMA, RS = B::RS;
+  static_assert(B::NSL <= 12 && NI <= 40, "replay arrays");
+  __shared__ __attribute__((aligned(16))) v4u lds[B::NV];
+  __shared__ __attribute__((aligned(16))) v4u trash[64];  // destination of padding loads
+  __shared__ int32_t nbs[GT * 27];  // neighbour rows of the tile's groups
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int li = lane & 15, q = lane >> 4;
+  const int64_t g0 = (int64_t)blockIdx.x * GT;
+  const int n0 = blockIdx.y * 64;
+  const int KO = kk >> 3;  // channel octets of the reduction
+  const int ob = 8 * chunk;
+  if (tid < GT * 27) nbs[tid] = g0 + tid / 27 < ngroups ? nbr[27 * g0 + tid] : -1;
+  __syncthreads();
+
+  // slab sl (half h = sl / S, x-position j = sl % S) into buffer sl % NB;
+  // DMA instruction i covers 16 positions x 4 pieces
+  auto stage = [&](int sl) {
+    const int h = sl / S, j = sl - h * S;
+    v4u* buf = lds + (sl % NB) * SLAB;
+    // an opaque copy of the lane index: the position arithmetic below is the
+    // same for every slab, and hoisting it out of the unrolled item sequence
+    // would hold its values in registers through the whole tile
+    int ln;
+    asm volatile("" : "=v"(ln) : "0"(lane));
+#pragma unroll
+    for (int k = 0; k < DC; ++k) {
+      const int i = wave + NW * k;
+      const int s = i * 64 + ln;
+      const int pos = s >> 2, g = pos / S2, p = pos - g * S2;
+      const int py = p / S, pz = p - py * S;
+      const int o = ob + 4 * h + ((s & 3) ^ (2 * (j & 1) + (py & 1)));
+      const int32_t row = i < NDMA && o < KO ? tile_row<R>(nbs + 27 * g, j, py, pz) : -1;
+      const void* src = row >= 0 ? (const void*)(x + (int64_t)row * kk + 8 * o)
+                                 : (const void*)g_zero_rows[(s + 64 * (int)blockIdx.x) & (ZROWS - 1)];
+      lds_load16(src, lds_addr(i < NDMA ? buf + i * 64 : trash));
+    }
+  };
+
+  // lane (li, q) of row block b supplies row li: child li & 7 of group
+  // 2b + (li >> 3), channels 8q..8q+7 of the phase's half
+  const int cc = li & 7, cx = cc >> 2, cy = (cc >> 1) & 1, cz = cc & 1, gl = li >> 3;
+  // weights of item n: wp[(o K3 + t) nn + nc][8] for octet o = ob + 4h + q,
+  // column nc = n0 + 16 nf + li: a uniform base per (item, nf) and one lane
+  // offset (the launcher guarantees every lane's octet and column exist)
+  const uint32_t wlane = (uint32_t)(((int64_t)q * K3 * nn + li) * 16);
+  auto load_w = [&](v4u (&wv)[4], int n) {  // item n of the tile
+    const int ph = n / MI, i = n % MI;
+    const int h = ph / K, dx = ph - h * K;
+    const int e = i < NFULL ? wave + NW * i : NFULL * NW;
+    const int t = dx * K2 + e;
+    const uint16_t* wb = wp + ((int64_t)((ob + 4 * h) * K3 + t) * nn + n0) * 8;
+#pragma unroll
+    for (int nf = 0; nf < 4; ++nf) gload16s(wv[nf], wlane, wb + 16 * nf * 8);
+  };
+  v4f acc[NRB][4];
+#pragma unroll
+  for (int b = 0; b < NRB; ++b)
+#pragma unroll
+    for (int nf = 0; nf < 4; ++nf) acc[b][nf] = v4f{0.f, 0.f, 0.f, 0.f};
+  // LDS byte offsets of this lane's operand piece in a phase, for taps of
+  // even and odd y-offset (the piece swizzle depends on the y parity); set at
+  // the start of every phase, so that each item only adds constants
+  uint32_t pb[2];
+  auto phase_bases = [&](int ph) {
+    const int h = ph / K, dx = ph - h * K;
+    const int px = dx + cx;
+    const uint32_t lb = (uint32_t)(((h * S + px) % NB) * SLAB + (gl * S2 + cy * S + cz) * 4) * 16;
+#pragma unroll
+    for (int d = 0; d < 2; ++d) pb[d] = lb + (uint32_t)(q ^ (2 * (px & 1) + ((d + cy) & 1))) * 16;
+  };
+  const char* lbase = reinterpret_cast<const char*>(lds);
+  auto opnd = [&](int dyi, int dzi, int b) {
+    return *reinterpret_cast<const v4u*>(lbase + pb[dyi & 1] + ((dyi * S + dzi) * 4 + 2 * b * S2 * 4) * 16);
+  };
+  auto compute = [&](const v4u (&wv)[4], int n) {
+    const int i = n % MI;
+    const int e = i < NFULL ? wave + NW * i : NFULL * NW;
+    const int dyi = e / K, dzi = e - dyi * K;
+    if (i < NFULL) {
+      // row blocks in pairs; the next pair's operands are read before the
+      // current pair's MFMAs are issued, so the LDS latency hides behind them
+      constexpr int AB = 2, NP = NRB / AB;
+      v4u a[2][AB];
+#pragma unroll
+      for (int b = 0; b < AB; ++b) a[0][b] = opnd(dyi, dzi, b);
+#pragma unroll
+      for (int bh = 0; bh < NP; ++bh) {
+        if (bh + 1 < NP) {
+#pragma unroll
+          for (int b = 0; b < AB; ++b) a[(bh + 1) & 1][b] = opnd(dyi, dzi, (bh + 1) * AB + b);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int b = 0; b < AB; ++b)
+#pragma unroll
+          for (int nf = 0; nf < 4; ++nf)
+            acc[bh * AB + b][nf] = mfma_bf(a[bh & 1][b], wv[nf], acc[bh * AB + b][nf]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      const int only = wave % NRB;
+#pragma unroll
+      for (int b = 0; b < NRB; ++b) {
+        if (b == only) {
+          const v4u a = opnd(dyi, dzi, b);
+#pragma unroll
+          for (int nf = 0; nf < 4; ++nf) acc[b][nf] = mfma_bf(a, wv[nf], acc[b][nf]);
+        }
+      }
+    }
+  };
+
+  v4u W[RW][4];
+#pragma unroll
+  for (int sl = 0; sl < B::NPRE; ++sl) stage(sl);
+#pragma unroll
+  for (int j = 0; j <= RW - 2; ++j)
+    if (j < NI) load_w(W[j], j);
+  static_for<NI>([&](auto nc) {
+    constexpr int n = decltype(nc)::value;
+    constexpr int ph = n / MI;
+    if constexpr (n % MI == 0) {
+      constexpr int need = B::slab_of_phase(ph) + 1;
+      vm_wait_n<B::younger(0, need, ph)>();  // this phase's two slabs have landed
+      lds_barrier();                          // ... everywhere; the previous phase is done
+      phase_bases(ph);
+    }
+    vm_wait_for<B::younger(1, n, 0)>(W[n % RW]);
+    compute(W[n % RW], n);
+    if constexpr (n + RW - 1 < NI) load_w(W[(n + RW - 1) % RW], n + RW - 1);
+    if constexpr (n % MI == 0) {
+      // the slabs whose buffers the previous phase freed, issued once this
+      // phase's first MFMAs are under way (their address lookups then
+      // overlap the matrix work)
+      constexpr int from = ph == 0 ? B::NPRE : B::last_slab(ph - 1) + 1;
+      static_for<B::last_slab(ph) + 1 - from>([&](auto k) { stage(from + decltype(k)::value); });
+    }
+  });
+  vm_wait0();
+
+  // add the waves' tiles in wave order, 32 rows per round (and to out for
+  // a later chunk)
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(lds);
+  const int64_t nrows = 8 * ngroups;
+#pragma unroll
+  for (int rd = 0; rd < NRB / 2; ++rd) {
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int nf = 0; nf < 4; ++nf)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          red[(wave * 32 + bb * 16 + 4 * q + j) * RS + 16 * nf + li] = acc[2 * rd + bb][nf][j];
+    __syncthreads();
+    const int r = tid >> 4, cq = (tid & 15) * 4;
+    const int64_t row = 8 * g0 + 32 * rd + r;
+    const int n = n0 + cq;
+    v4f sum = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < NW; ++w) sum += *reinterpret_cast<const v4f*>(&red[(w * 32 + r) * RS + cq]);
+    if (row < nrows && n < nn) {
+      v4f* dst = reinterpret_cast<v4f*>(out + row * nn + n);
+      if (acc_in) sum = *dst + sum;
+      if (relu) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sum[j] = fmaxf(sum[j], 0.f);
+      }
+      *dst = sum;
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Weight gradient.  x [8 ngroups][cin] bf16, dy [8 ngroups][cout] bf16
 // (cin, cout % 16 == 0).  A unit is a box of tap offsets, x-offsets
 // [x0, x1] by y-offsets [y0, y1] by every z-offset, whose taps read a box of
@@ -621,12 +891,22 @@ void wprep(const uint16_t* w, int K, int kk, int nn, int flip, uint16_t* wp, hip
                      kk, nn, flip, wp);
 }
 
+// Tiles of 16 groups (k_conv_bfw) for K = 5: half the weight reads per row
+// of the 8-group kernel.  Its weight loads have no per-lane masks, so every
+// chunk must hold whole 32-channel halves and the columns whole blocks of 64;
+// K = 3 keeps the 8-group kernel.
+bool wide_tiles(int K, int kk, int nn) { return K == 5 && kk % 32 == 0 && nn % 64 == 0; }
+
 template <int K, int HC, bool FLIP>
 void launch_chunk(const oc_octree* t, int l, const uint16_t* x, int kk, const uint16_t* wp, int nn,
                   int chunk, float* out, int acc_in, int relu, bool main, hipStream_t s) {
   const int64_t G = t->M[l - 1];
-  const dim3 grid(blocks(G, 8), blocks(nn, 64));
-  const auto kern = k_conv_bf<K, HC, FLIP>;
+  const bool wide = wide_tiles(K, kk, nn);
+  const dim3 grid(blocks(G, wide ? 16 : 8), blocks(nn, 64));
+  auto kern = k_conv_bf<K, HC, FLIP>;
+  if constexpr (K == 5) {
+    if (wide) kern = k_conv_bfw<K, HC, FLIP>;
+  }
   if (main)
     oc::launch_main(kern, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, kk, wp, nn, chunk,
                     out, acc_in, relu);
@@ -671,7 +951,8 @@ void conv_bf16_kernel_name(int K, int cin, int cout, int pass, char* buf, size_t
   if (pass == 2)
     snprintf(buf, n, "k_conv_bf_dw<%d, 5>", K);
   else
-    snprintf(buf, n, "k_conv_bf<%d, %d, %s>", K, kk > 32 ? 2 : 1, pass == 1 ? "true" : "false");
+    snprintf(buf, n, "%s<%d, %d, %s>", wide_tiles(K, kk, pass == 1 ? cin : cout) ? "k_conv_bfw" : "k_conv_bf", K,
+             kk > 32 ? 2 : 1, pass == 1 ? "true" : "false");
 }
 
 size_t conv_bf16_fwd_ws(int K, int cin, int cout) { return wp_bytes(K, cin, cout); }

@@ -99,28 +99,40 @@ __device__ __forceinline__ v4f store_order(v4f d, int lane) {
   return r;
 }
 
+// Slot of position (px, py, pz) in {0..3}^3 (relative to the first child of
+// group gg minus one) in the group's 64-slot tile: 16 px + 4 py + pz, or with
+// SWZ the z bits XOR-ed with (2 gg + (px & 1)).  The forward's reads take one
+// channel of one tap for the 16 octants of two groups at a time; unswizzled,
+// the two x-values of the eight children and the two groups fall on the same
+// banks (4-way conflicts), swizzled on different ones (2-way).
+template <bool SWZ>
+__device__ __forceinline__ int tile_slot(int gg, int px, int py, int pz) {
+  return 16 * px + 4 * py + (SWZ ? pz ^ (2 * gg + (px & 1)) : pz);
+}
+
 // Byte offset, in a tile buffer of two groups x 64 positions x 16 bytes, of
 // channel c of the tap (dx, dy, dz) in {0,1,2}^3 (offsets -1..1) of child
-// ch (4x + 2y + z) of group gg.  Position (px, py, pz) in {0..3}^3 relative
-// to the group's first child minus one sits at slot 16 px + 4 py + pz.
+// ch (4x + 2y + z) of group gg.
+template <bool SWZ>
 __device__ __forceinline__ int tap_offset(int gg, int ch, int tap, int c) {
   const int px = ((ch >> 2) & 1) + tap / 9, py = ((ch >> 1) & 1) + (tap / 3) % 3,
             pz = (ch & 1) + tap % 3;
-  return ((gg * 64 + 16 * px + 4 * py + pz) * 16) + 4 * c;
+  return ((gg * 64 + tile_slot<SWZ>(gg, px, py, pz)) * 16) + 4 * c;
 }
 
 // One tile: the two groups' 64 positions each (DMA, one instruction per
-// group) from the neighbour entries in nbs (54 entries, LDS).  Lane p takes
-// position p of each group.
-template <int CIN>
+// group) from the neighbour entries in nbs (54 entries, LDS).  Lane i fills
+// slot i of each group: the position tile_slot<SWZ> puts there.
+template <int CIN, bool SWZ>
 __device__ __forceinline__ void tile_dma(const float* __restrict__ x, const int32_t* nbs,
                                          float* buf, int lane) {
-  const int px = lane >> 4, py = (lane >> 2) & 3, pz = lane & 3;
-  const int ux = px - 1, uy = py - 1, uz = pz - 1;
-  const int slot = ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1);
-  const int coff = 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
+  const int px = lane >> 4, py = (lane >> 2) & 3;
 #pragma unroll
   for (int gg = 0; gg < 2; ++gg) {
+    const int pz = SWZ ? (lane & 3) ^ (2 * gg + (px & 1)) : lane & 3;  // tile_slot inverted
+    const int ux = px - 1, uy = py - 1, uz = pz - 1;
+    const int slot = ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1);
+    const int coff = 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1);
     const int32_t b = nbs[27 * gg + slot];
     const float* src = b >= 0 ? x + (int64_t)(b + coff) * CIN : g_cin_zero;
     const uint32_t a = lds_addr(buf + gg * 64 * 4);
@@ -223,7 +235,7 @@ __global__ __launch_bounds__(TB) void k_cin_fwd(const int32_t* __restrict__ nbr,
     const int k = 4 * s + q;
     const bool on = k < KF;
     wr[s] = on ? w[(int64_t)k * cout + n0 + li] : 0.f;
-    xo[s] = tap_offset(li >> 3, li & 7, on ? k / CIN : 0, on ? k % CIN : 0);
+    xo[s] = tap_offset<true>(li >> 3, li & 7, on ? k / CIN : 0, on ? k % CIN : 0);
   }
   // the weights are in registers here (the compiler waits for their loads,
   // and for the entries above), so the counted waits below see only the
@@ -249,7 +261,7 @@ __global__ __launch_bounds__(TB) void k_cin_fwd(const int32_t* __restrict__ nbr,
     else
       vm_wait_n<WE>();
     if constexpr (POOL) pq[j] = nw[64 * (j & 1) + 54 + ((lane >> 4) & 1)];
-    tile_dma<CIN>(x, nw + 64 * (j & 1), tw + j * TF, lane);
+    tile_dma<CIN, true>(x, nw + 64 * (j & 1), tw + j * TF, lane);
     if constexpr (POOL) {
       gstore4(g_cin_dummy + lane, 0u);
       gstore1(reinterpret_cast<uint8_t*>(g_cin_dummy) + lane, 0u);
@@ -264,7 +276,7 @@ __global__ __launch_bounds__(TB) void k_cin_fwd(const int32_t* __restrict__ nbr,
     nb_dma(nbr, ngroups, t + D + 1, nw + 64 * ((e + D + 1) & 1), lane, pr);
     vm_wait_n<WE>();  // entries of tile t+D
     if constexpr (POOL) pq[D] = nw[64 * ((e + D) & 1) + 54 + ((lane >> 4) & 1)];
-    tile_dma<CIN>(x, nw + 64 * ((e + D) & 1), tw + ahead * TF, lane);
+    tile_dma<CIN, true>(x, nw + 64 * ((e + D) & 1), tw + ahead * TF, lane);
     vm_wait_n<WE * D>();  // tile t
     v4f acc = {0.f, 0.f, 0.f, 0.f};
     const float* bb = tw + cur * TF;
@@ -344,7 +356,7 @@ __global__ __launch_bounds__(TB) void k_cin_dw(const int32_t* __restrict__ nbr, 
     const bool on = k < KF;
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      xo[b][u] = tap_offset(u >> 1, 4 * (u & 1) + q, on ? k / CIN : 0, on ? k % CIN : 0);
+      xo[b][u] = tap_offset<false>(u >> 1, 4 * (u & 1) + q, on ? k / CIN : 0, on ? k % CIN : 0);
   }
 #pragma unroll
   for (int b = 0; b < NMB; ++b)
@@ -379,7 +391,7 @@ __global__ __launch_bounds__(TB) void k_cin_dw(const int32_t* __restrict__ nbr, 
         vm_wait_n<1>();
       else
         vm_wait_n<4>();
-      tile_dma<CIN>(x, nw + 64 * (j & 1), tw + j * BF, lane);
+      tile_dma<CIN, false>(x, nw + 64 * (j & 1), tw + j * BF, lane);
       dy_dma(t0 + j, tw + j * BF + TF);
     }
     int cur = 0;  // buffer of tile t
@@ -388,7 +400,7 @@ __global__ __launch_bounds__(TB) void k_cin_dw(const int32_t* __restrict__ nbr, 
       const int e = (int)((t - t0) & 1);   // entry slot of tile t (tile u: slot (u - t0) & 1)
       nb_dma(nbr, ngroups, t + D + 1, nw + 64 * ((e + D + 1) & 1), lane);
       vm_wait_n<4>();  // entries of tile t+D
-      tile_dma<CIN>(x, nw + 64 * ((e + D) & 1), tw + ahead * BF, lane);
+      tile_dma<CIN, false>(x, nw + 64 * ((e + D) & 1), tw + ahead * BF, lane);
       dy_dma(t + D, tw + ahead * BF + TF);
       vm_wait_n<4 * D>();  // tile t
       const float* bb = tw + cur * BF;

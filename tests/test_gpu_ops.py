@@ -271,6 +271,10 @@ BF16_NATIVE = [  # seed, B, n, depth, K, cin, cout, relu: tiles with ragged tail
     (43, 1, 900, 5, 5, 80, 32, True),
     (44, 2, 300, 4, 3, 128, 96, False),
     (45, 1, 200, 3, 5, 32, 16, False),
+    # 16-group tiles (K = 5, whole 32-channel halves, 64-column blocks): two
+    # chunks of 64, two column blocks, a 64 + 32 split
+    (46, 2, 500, 4, 5, 128, 64, True),
+    (47, 1, 600, 5, 5, 96, 128, False),
 ]
 
 
