@@ -510,8 +510,10 @@ class Accounting:
             return M[l - 1] * c * 5 + M[l - 1] * 4 + N[l] * c * 4
         if tag == "unpool_bwd":  # the routed child of each (parent, channel) in, parent rows out
             return M[l - 1] * c * 5 + N[l - 1] * 4 + N[l - 1] * c * 4
-        if tag == "bn_fwd":  # two statistics passes over z, then z in and y out
-            return N[l] * L.cout * 4 * 4
+        if tag == "bn_fwd":  # (with the pooling) one statistics pass over z, then z in,
+            # the pooled rows, switches and labels out / in
+            c = L.cout
+            return N[l] * c * 8 + N[l - 1] * c * 4 + M[l - 1] * c + N[l - 1] * 4
         if tag == "bn_bwd":  # z and dy in for the sums, then z, dy in and dx out
             return N[l] * L.cout * 4 * 5
         if tag in ("gpool_fwd", "gpool_bwd"):
@@ -867,8 +869,8 @@ class Step(Accounting):
 class TrainStep(Step):
     """One O-CNN(d) classification training iteration (Sec. 4 "Network
     structure", Sec. 5 "Training details") on the octree built during the
-    previous step: units U_d .. U_2 (conv, batch normalisation with the ReLU
-    fused, 2x2x2 max-pool), the depth-1 features of each shape (8 C_2 values)
+    previous step: units U_d .. U_2 (conv, then batch normalisation, ReLU and
+    the 2x2x2 max-pool in one call), the depth-1 features of each shape (8 C_2 values)
     through dropout, FC(128), dropout, FC(classes), softmax cross-entropy on
     synthetic labels; the backward of all of it; one SGD step with momentum
     0.9, weight decay 5e-4 (convolution and FC weights) and learning rate 0.1.
@@ -920,10 +922,12 @@ class TrainStep(Step):
         for li, L in enumerate(wl.layers):
             w = self.conv_p[li]["w"]
             z = self._run("conv_fwd", li, lambda: oc.oc_conv_fwd(tree, L.depth, 3, 1, x, w))
-            a, mean, invstd = self._run("bn_fwd", li, lambda: oc.oc_bn_fwd(
-                z, self.gamma[li]["w"], self.beta[li]["w"], relu=True))
-            p, sw = self._run("pool_fwd", li, lambda: oc.oc_pool_fwd(tree, L.depth, a))
-            units.append((li, x, z, a, mean, invstd, p, sw))
+            # normalisation, ReLU and pooling in one call (the depth-l
+            # activations are not kept: the backward needs z and the pooled
+            # output only)
+            p, sw, mean, invstd = self._run("bn_fwd", li, lambda: oc.oc_bn_pool_fwd(
+                tree, L.depth, z, self.gamma[li]["w"], self.beta[li]["w"], relu=True))
+            units.append((li, x, z, None, mean, invstd, p, sw))
             x = p
         feat = x.view(wl.batch, -1)
         h0 = self._run("dropout", None, lambda: oc.oc_dropout(feat, self.keep1, P))

@@ -419,7 +419,8 @@ oc_status oc_gpool_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int3
  *
  * Batch normalisation in training mode over the n rows of x [n][c] (all
  * octants of a depth, empty children included): per channel mean and biased
- * variance (double-precision sums in a fixed order), y = (x - mean) invstd
+ * variance (double precision, one pass: per-block counts, means and sums of
+ * squared deviations merged pairwise in a fixed order), y = (x - mean) invstd
  * gamma + beta, invstd = 1 / sqrt(var + eps); flags OC_FUSE_RELU applies
  * max(0, .) to y.  mean, invstd: dev f32 [c], written for the backward.
  * ws: dev, at least oc_bn_workspace(n, c) bytes. */
@@ -427,6 +428,24 @@ size_t oc_bn_workspace(int64_t n, int32_t c);
 oc_status oc_bn_fwd(int64_t n, int32_t c, const float* x, const float* gamma, const float* beta,
                     float eps, int32_t flags, float* y, float* mean, float* invstd, void* ws,
                     size_t ws_bytes, hipStream_t stream);
+
+/* Batch normalisation, optional ReLU and 2x2x2 max-pooling forward in one
+ * call (the unit of Sec. 4 after its convolution): the statistics of
+ * oc_bn_fwd over the N_l rows of z; the normalised values (ReLU'd with
+ * OC_FUSE_RELU) are pooled to depth l-1 as oc_pool_fwd does, and never
+ * written at depth l.  The backward is oc_pool_bwd with y (which applies the
+ * ReLU's backward), then oc_bn_bwd on z.
+ *   depth   l, 1 .. tree depth, with N_l > 0.
+ *   z       dev f32 [N_l][c].  gamma, beta dev f32 [c].  eps > 0.
+ *   y       dev f32 [N_{l-1}][c]: pooled features, empty octants' rows zero.
+ *   sw      dev u8 [M_{l-1}][c]: switches, as oc_pool_fwd.
+ *   mean, invstd  dev f32 [c], written for the backward.
+ *   ws      dev, at least oc_bn_workspace(N_l, c) bytes.
+ * y and sw equal oc_bn_fwd followed by oc_pool_fwd bit for bit. */
+oc_status oc_bn_pool_fwd(const oc_octree* tree, int32_t depth, int32_t c, const float* z,
+                         const float* gamma, const float* beta, float eps, int32_t flags, float* y,
+                         uint8_t* sw, float* mean, float* invstd, void* ws, size_t ws_bytes,
+                         hipStream_t stream);
 
 /* Gradients of oc_bn_fwd (without the ReLU: dy is the gradient w.r.t. the
  * normalised output): dbeta = sum dy, dgamma = sum dy x_hat, dx = gamma

@@ -44,6 +44,7 @@ __all__ = [
     "OC_POOL_MAX",
     "OC_POOL_AVG",
     "oc_bn_fwd",
+    "oc_bn_pool_fwd",
     "oc_bn_bwd",
     "oc_fc_fwd",
     "oc_fc_bwd",
@@ -70,7 +71,7 @@ EXPORTS = (
     "oc_gpool_fwd", "oc_gpool_bwd", "oc_profile_calls", "oc_conv_fwd_noalloc",
     "oc_bn_workspace", "oc_bn_fwd", "oc_bn_bwd", "oc_fc_fwd", "oc_fc_bwd", "oc_dropout",
     "oc_softmax_ce_workspace", "oc_softmax_ce", "oc_sgd", "oc_conv_pool_fwd",
-    "oc_conv_pool_fwd_workspace",
+    "oc_conv_pool_fwd_workspace", "oc_bn_pool_fwd",
 )
 
 
@@ -186,6 +187,7 @@ def load():
         "oc_bn_workspace": ([i64, i32], sz),
         "oc_bn_fwd": ([i64, i32, p, p, p, C.c_float, i32, p, p, p, p, sz, p], C.c_int),
         "oc_bn_bwd": ([i64, i32, p, p, p, p, p, p, p, p, p, sz, p], C.c_int),
+        "oc_bn_pool_fwd": ([p, i32, i32, p, p, p, C.c_float, i32, p, p, p, p, p, sz, p], C.c_int),
         "oc_fc_fwd": ([i32, i32, i32, p, p, p, p, p], C.c_int),
         "oc_fc_bwd": ([i32, i32, i32, p, p, p, p, p, p, p], C.c_int),
         "oc_dropout": ([i64, p, p, C.c_float, p, p], C.c_int),
@@ -681,6 +683,29 @@ def oc_bn_fwd(x: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor, eps: flo
                        _dev(y, "y"), _dev(mean, "mean"), _dev(invstd, "invstd"), _dev(ws, "ws"),
                        ws.numel(), _stream()))
     return y, mean, invstd
+
+
+def oc_bn_pool_fwd(tree: Octree, depth: int, z: torch.Tensor, gamma: torch.Tensor,
+                   beta: torch.Tensor, eps: float = 1e-5, relu: bool = True):
+    """Batch normalisation of z [N_l][c] (training mode), optional ReLU and
+    the 2x2x2 max-pool to depth - 1 in one call: (pooled, switches, mean,
+    invstd)."""
+    n, c = z.shape
+    if n != tree.num(depth):
+        raise OcError(1, f"z has {n} rows, depth {depth} has {tree.num(depth)}")
+    n_p, m = tree.num(depth - 1), tree.nonempty(depth - 1)
+    y = torch.empty((n_p, c), dtype=torch.float32, device=z.device)
+    sw = torch.empty((m, c), dtype=torch.uint8, device=z.device)
+    mean = torch.empty(c, dtype=torch.float32, device=z.device)
+    invstd = torch.empty(c, dtype=torch.float32, device=z.device)
+    L = load()
+    ws = torch.empty(max(int(L.oc_bn_workspace(n, c)), 1), dtype=torch.uint8, device=z.device)
+    _check(L.oc_bn_pool_fwd(tree.handle, depth, c, _dev(z, "z", torch.float32),
+                            _dev(gamma, "gamma", torch.float32), _dev(beta, "beta", torch.float32),
+                            eps, OC_FUSE_RELU if relu else 0, _dev(y, "y"), _dev(sw, "sw"),
+                            _dev(mean, "mean"), _dev(invstd, "invstd"), _dev(ws, "ws"),
+                            ws.numel(), _stream()))
+    return y, sw, mean, invstd
 
 
 def oc_bn_bwd(x, dy, gamma, mean, invstd, dgamma=None, dbeta=None):

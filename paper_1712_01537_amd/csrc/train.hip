@@ -7,14 +7,17 @@
 // Batch normalisation in training mode (the method the paper cites, Ioffe
 // and Szegedy 2015): per channel, the mean and biased variance over all n
 // rows of the feature map.  The statistics are reductions over up to millions
-// of rows, done in double precision and in a fixed order: each block sums a
-// contiguous range of rows per channel (threads over channels and rows, four
-// rows in flight per thread, then the row lanes in order through LDS) into a
-// partial, and one block per channel adds the partials (strided over its
-// threads, then a fixed tree through LDS).  The block count gives each
-// thread about 16 rows, so neither pass waits on a long chain of loads.  The
-// variance is a second pass over (x - mean)^2, as the definition states (no
-// sum-of-squares cancellation).  Results are reproducible bit for bit.
+// of rows, done in double precision and in a fixed order: each block reduces
+// a contiguous range of rows per channel (threads over channels and rows,
+// four rows in flight per thread, then the row lanes in order through LDS)
+// into a partial, and one block per channel combines the partials (strided
+// over its threads, then a fixed tree through LDS).  The block count gives
+// each thread about 16 rows, so no pass waits on a long chain of loads.  The
+// forward takes the mean and the variance in one pass: count, mean and sum
+// of squared deviations per partial (Welford's update), combined pairwise
+// (Chan et al.), so the variance never subtracts two large sums.  The
+// backward's two sums (dy and dy x_hat) are plain sums.  Results are
+// reproducible bit for bit.
 //
 // The head works on a batch of B shapes (B x 1024 x 128 multiply-adds for the
 // first FC layer at depth 6): a few microseconds of plain FMA kernels, bound
@@ -40,12 +43,11 @@ int bn_blocks(int64_t n, int c) {
 // channels (cc = min(c, 256)), row lane tid / cc of rl = 256 / cc lanes; the
 // channel groups are taken in turn.
 //
-// mode 0: part[b][ch] = sum x over the block's rows
-// mode 1: part[b][ch] = sum (x - mean)^2
-// mode 2: part[b][2 ch] = sum dy, part[b][2 ch + 1] = sum dy (x - mean) invstd
+// Backward sums: part[b][2 ch] = sum dy, part[b][2 ch + 1] = sum dy (x - mean)
+// invstd over the block's rows.
 __global__ __launch_bounds__(TB) void k_bn_partial(const float* __restrict__ x,
                                                    const float* __restrict__ dy, int64_t n, int c,
-                                                   int mode, const float* __restrict__ mean,
+                                                   const float* __restrict__ mean,
                                                    const float* __restrict__ invstd,
                                                    double* __restrict__ part) {
   __shared__ double red[2][TB];
@@ -54,25 +56,17 @@ __global__ __launch_bounds__(TB) void k_bn_partial(const float* __restrict__ x,
   const int64_t r0 = n * b / nb, r1 = n * (b + 1) / nb;
   const int cc = c < TB ? c : TB, rl = TB / cc;
   const int lane_c = tid % cc, lane_r = tid / cc;
-  const int outs = mode == 2 ? 2 : 1;
   for (int c0 = 0; c0 < c; c0 += cc) {
     const int ch = c0 + lane_c;
     double s0 = 0.0, s1 = 0.0;
     if (lane_r < rl && ch < c) {
-      const double m = mode == 0 ? 0.0 : (double)mean[ch];
-      const double is = mode == 2 ? (double)invstd[ch] : 0.0;
+      const double m = (double)mean[ch], is = (double)invstd[ch];
 #pragma unroll 4
       for (int64_t r = r0 + lane_r; r < r1; r += rl) {
         const double v = (double)x[r * c + ch];
-        if (mode == 0) {
-          s0 += v;
-        } else if (mode == 1) {
-          s0 += (v - m) * (v - m);
-        } else {
-          const double g = (double)dy[r * c + ch];
-          s0 += g;
-          s1 += g * (v - m) * is;
-        }
+        const double g = (double)dy[r * c + ch];
+        s0 += g;
+        s1 += g * (v - m) * is;
       }
     }
     red[0][tid] = s0;
@@ -85,28 +79,112 @@ __global__ __launch_bounds__(TB) void k_bn_partial(const float* __restrict__ x,
         a0 += red[0][lane_c + cc * j];
         a1 += red[1][lane_c + cc * j];
       }
-      part[((int64_t)b * c + ch) * outs] = a0;
-      if (outs == 2) part[((int64_t)b * c + ch) * outs + 1] = a1;
+      part[((int64_t)b * c + ch) * 2] = a0;
+      part[((int64_t)b * c + ch) * 2 + 1] = a1;
     }
     __syncthreads();
   }
 }
 
-// Per channel (one block each), the nb partials: thread t adds partials
-// t, t + TB, ... in order, then a fixed tree through LDS.
-// mode 0: mean = sum / n.  mode 1: invstd = 1 / sqrt(sum / n + eps).
-// mode 2: dbeta = sum dy, dgamma = sum dy x_hat.
+// Forward statistics in one pass: per (block, channel) the count, mean and
+// sum of squared deviations of the block's rows (Welford's update per thread,
+// then the row lanes merged in order with Chan et al.'s pairwise formula),
+// part[b][ch] = {n, mean, M2}.  The final kernel merges the blocks the same
+// way (a fixed order), so the variance never subtracts two large sums.
+struct Moments {
+  double n, mean, m2;
+};
+__device__ __forceinline__ Moments merge(const Moments& a, const Moments& b) {
+  const double n = a.n + b.n;
+  if (n == 0.0) return a;
+  const double d = b.mean - a.mean, f = b.n / n;
+  return Moments{n, a.mean + d * f, a.m2 + b.m2 + d * d * a.n * f};
+}
+
+__global__ __launch_bounds__(TB) void k_bn_stats(const float* __restrict__ x, int64_t n, int c,
+                                                 double* __restrict__ part) {
+  __shared__ double red[3][TB];
+  const int tid = threadIdx.x;
+  const int nb = gridDim.x, b = blockIdx.x;
+  const int64_t r0 = n * b / nb, r1 = n * (b + 1) / nb;
+  const int cc = c < TB ? c : TB, rl = TB / cc;
+  const int lane_c = tid % cc, lane_r = tid / cc;
+  for (int c0 = 0; c0 < c; c0 += cc) {
+    const int ch = c0 + lane_c;
+    Moments m{0.0, 0.0, 0.0};
+    if (lane_r < rl && ch < c) {
+#pragma unroll 4
+      for (int64_t r = r0 + lane_r; r < r1; r += rl) {
+        const double v = (double)x[r * c + ch];
+        m.n += 1.0;
+        const double d = v - m.mean;
+        m.mean += d / m.n;
+        m.m2 += d * (v - m.mean);
+      }
+    }
+    red[0][tid] = m.n;
+    red[1][tid] = m.mean;
+    red[2][tid] = m.m2;
+    __syncthreads();
+    if (lane_r == 0 && ch < c) {
+      Moments a{0.0, 0.0, 0.0};
+      for (int j = 0; j < rl; ++j) {
+        const int k = lane_c + cc * j;
+        a = merge(a, Moments{red[0][k], red[1][k], red[2][k]});
+      }
+      double* o = part + ((int64_t)b * c + ch) * 3;
+      o[0] = a.n;
+      o[1] = a.mean;
+      o[2] = a.m2;
+    }
+    __syncthreads();
+  }
+}
+
+// Per channel (one block each): mean and invstd = 1 / sqrt(M2 / n + eps)
+// from the nb partials of k_bn_stats (thread t merges partials t, t + TB,
+// ... in order, then a fixed tree through LDS).
+__global__ __launch_bounds__(TB) void k_bn_stats_final(const double* __restrict__ part, int nb,
+                                                       int c, float eps, float* __restrict__ mean,
+                                                       float* __restrict__ invstd) {
+  __shared__ double red[3][TB];
+  const int ch = blockIdx.x, tid = threadIdx.x;
+  Moments a{0.0, 0.0, 0.0};
+  for (int b = tid; b < nb; b += TB) {
+    const double* p = part + ((int64_t)b * c + ch) * 3;
+    a = merge(a, Moments{p[0], p[1], p[2]});
+  }
+  red[0][tid] = a.n;
+  red[1][tid] = a.mean;
+  red[2][tid] = a.m2;
+  __syncthreads();
+  for (int h = TB / 2; h > 0; h >>= 1) {
+    if (tid < h) {
+      const Moments m = merge(Moments{red[0][tid], red[1][tid], red[2][tid]},
+                              Moments{red[0][tid + h], red[1][tid + h], red[2][tid + h]});
+      red[0][tid] = m.n;
+      red[1][tid] = m.mean;
+      red[2][tid] = m.m2;
+    }
+    __syncthreads();
+  }
+  if (tid != 0) return;
+  mean[ch] = (float)red[1][0];
+  invstd[ch] = (float)(1.0 / sqrt(red[2][0] / red[0][0] + (double)eps));
+}
+
+// Per channel (one block each), the nb backward partials: thread t adds
+// partials t, t + TB, ... in order, then a fixed tree through LDS; dbeta =
+// sum dy, dgamma = sum dy x_hat.
 __global__ __launch_bounds__(TB) void k_bn_final(const double* __restrict__ part, int nb, int c,
-                                                 int64_t n, int mode, float eps,
-                                                 float* __restrict__ out0,
-                                                 float* __restrict__ out1) {
+                                                 float* __restrict__ dbeta,
+                                                 float* __restrict__ dgamma) {
   __shared__ double red[2][TB];
   const int ch = blockIdx.x, tid = threadIdx.x;
-  const int outs = mode == 2 ? 2 : 1;
   double a0 = 0.0, a1 = 0.0;
   for (int b = tid; b < nb; b += TB) {
-    a0 += part[((int64_t)b * c + ch) * outs];
-    if (outs == 2) a1 += part[((int64_t)b * c + ch) * outs + 1];
+    a0 += part[((int64_t)b * c + ch) * 2];
+    a1 += part[((int64_t)b * c + ch) * 2 + 1];
   }
   red[0][tid] = a0;
   red[1][tid] = a1;
@@ -119,16 +197,55 @@ __global__ __launch_bounds__(TB) void k_bn_final(const double* __restrict__ part
     __syncthreads();
   }
   if (tid != 0) return;
-  a0 = red[0][0];
-  a1 = red[1][0];
-  if (mode == 0) {
-    out0[ch] = (float)(a0 / (double)n);
-  } else if (mode == 1) {
-    out0[ch] = (float)(1.0 / sqrt(a0 / (double)n + (double)eps));
-  } else {
-    out0[ch] = (float)a0;  // dbeta
-    out1[ch] = (float)a1;  // dgamma
+  dbeta[ch] = (float)red[0][0];
+  dgamma[ch] = (float)red[1][0];
+}
+
+// The normalised value of x in channel ch (ReLU'd when relu): one
+// definition for the plain and the pooled forward.
+__device__ __forceinline__ float bn_value(float x, int ch, const float* __restrict__ mean,
+                                          const float* __restrict__ invstd,
+                                          const float* __restrict__ gamma,
+                                          const float* __restrict__ beta, int relu) {
+  const float v = (x - mean[ch]) * invstd[ch] * gamma[ch] + beta[ch];
+  return relu ? fmaxf(v, 0.f) : v;
+}
+
+// Normalisation (and ReLU) with the 2x2x2 max-pool: one thread per
+// (depth-(l-1) row i, channel); the children of label L = g + 1 are rows
+// 8g .. 8g + 7 of x, the first maximum in child order wins (strict '>'),
+// empty parents get 0 and no switch.  The normalised depth-l values are not
+// stored.
+__global__ __launch_bounds__(TB) void k_bn_pool(const float* __restrict__ x,
+                                                const int32_t* __restrict__ labels, int64_t npar,
+                                                int c, const float* __restrict__ mean,
+                                                const float* __restrict__ invstd,
+                                                const float* __restrict__ gamma,
+                                                const float* __restrict__ beta, int relu,
+                                                float* __restrict__ y, uint8_t* __restrict__ sw) {
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= npar * c) return;
+  const int64_t i = t / c;
+  const int ch = (int)(t - i * c);
+  const int32_t L = labels[i];
+  if (L == 0) {
+    y[t] = 0.f;
+    return;
   }
+  const int64_t g = L - 1;
+  const float* src = x + 8 * g * c + ch;
+  float best = bn_value(src[0], ch, mean, invstd, gamma, beta, relu);
+  uint8_t arg = 0;
+#pragma unroll
+  for (int k = 1; k < 8; ++k) {
+    const float v = bn_value(src[(int64_t)k * c], ch, mean, invstd, gamma, beta, relu);
+    if (v > best) {
+      best = v;
+      arg = (uint8_t)k;
+    }
+  }
+  y[t] = best;
+  sw[g * c + ch] = arg;
 }
 
 // y = (x - mean) invstd gamma + beta, ReLU applied when relu.
@@ -141,8 +258,7 @@ __global__ __launch_bounds__(TB) void k_bn_apply(const float* __restrict__ x, in
   const int64_t e = (int64_t)blockIdx.x * TB + threadIdx.x;
   if (e >= n * c) return;
   const int ch = n * c <= 0xffffffffll ? (int)((uint32_t)e % (uint32_t)c) : (int)(e % c);
-  float v = (x[e] - mean[ch]) * invstd[ch] * gamma[ch] + beta[ch];
-  y[e] = relu ? fmaxf(v, 0.f) : v;
+  y[e] = bn_value(x[e], ch, mean, invstd, gamma, beta, relu);
 }
 
 // dx = gamma invstd (dy - dbeta / n - x_hat dgamma / n).
@@ -262,13 +378,22 @@ __global__ __launch_bounds__(TB) void k_sgd(float* __restrict__ w, const float* 
   w[e] -= vn;
 }
 
+// Mean and invstd of x [n][c] (two launches).
+void bn_stats(int64_t n, int c, const float* x, float eps, float* mean, float* invstd,
+              double* part, hipStream_t s) {
+  const int nb = bn_blocks(n, c);
+  oc::launch(k_bn_stats, dim3(nb), dim3(TB), 0, s, x, n, c, part);
+  oc::launch(k_bn_stats_final, dim3((unsigned)c), dim3(TB), 0, s, (const double*)part, nb, c, eps,
+             mean, invstd);
+}
+
 }  // namespace
 
 extern "C" {
 
 size_t oc_bn_workspace(int64_t n, int32_t c) {
   if (n < 1 || c < 1) return 0;
-  return oc::align256((size_t)bn_blocks(n, c) * c * 2 * sizeof(double));
+  return oc::align256((size_t)bn_blocks(n, c) * c * 3 * sizeof(double));
 }
 
 oc_status oc_bn_fwd(int64_t n, int32_t c, const float* x, const float* gamma, const float* beta,
@@ -281,20 +406,34 @@ oc_status oc_bn_fwd(int64_t n, int32_t c, const float* x, const float* gamma, co
   if (!ws || ws_bytes < oc_bn_workspace(n, c))
     return oc::fail(OC_ERR_ARG, "oc_bn_fwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0,
                     oc_bn_workspace(n, c));
-  const int nb = bn_blocks(n, c);
-  double* part = (double*)ws;
-  const unsigned gc = (unsigned)c;
-  oc::launch(k_bn_partial, dim3(nb), dim3(TB), 0, s, x, (const float*)nullptr, n, (int)c, 0,
-             (const float*)nullptr, (const float*)nullptr, part);
-  oc::launch(k_bn_final, dim3(gc), dim3(TB), 0, s, (const double*)part, nb, (int)c, n, 0, eps,
-             mean, (float*)nullptr);
-  oc::launch(k_bn_partial, dim3(nb), dim3(TB), 0, s, x, (const float*)nullptr, n, (int)c, 1,
-             (const float*)mean, (const float*)nullptr, part);
-  oc::launch(k_bn_final, dim3(gc), dim3(TB), 0, s, (const double*)part, nb, (int)c, n, 1, eps,
-             invstd, (float*)nullptr);
+  bn_stats(n, c, x, eps, mean, invstd, (double*)ws, s);
   oc::launch_main(k_bn_apply, dim3(grid_for(n * c)), dim3(TB), s, x, n, (int)c,
                   (const float*)mean, (const float*)invstd, gamma, beta,
                   (flags & OC_FUSE_RELU) ? 1 : 0, y);
+  OC_LAUNCH_CHECK();
+  return OC_OK;
+}
+
+oc_status oc_bn_pool_fwd(const oc_octree* t, int32_t l, int32_t c, const float* z,
+                         const float* gamma, const float* beta, float eps, int32_t flags, float* y,
+                         uint8_t* sw, float* mean, float* invstd, void* ws, size_t ws_bytes,
+                         hipStream_t s) {
+  oc_status st = oc::check_tree_level(t, l, 1);
+  if (st != OC_OK) return st;
+  if (c < 1 || c > 65536) return oc::fail(OC_ERR_ARG, "oc_bn_pool_fwd: %d channels", c);
+  const int64_t n = t->N[l], np = t->N[l - 1];
+  if (np == 0) return OC_OK;
+  if (!y || !gamma || !beta || !mean || !invstd || (n > 0 && (!z || !sw)))
+    return oc::fail(OC_ERR_ARG, "oc_bn_pool_fwd: NULL buffer");
+  if (!(eps > 0.f)) return oc::fail(OC_ERR_ARG, "oc_bn_pool_fwd: eps must be positive");
+  if (n == 0) return oc::fail(OC_ERR_ARG, "oc_bn_pool_fwd: depth %d has no octant", l);
+  if (!ws || ws_bytes < oc_bn_workspace(n, c))
+    return oc::fail(OC_ERR_ARG, "oc_bn_pool_fwd: workspace %zu bytes < %zu", ws ? ws_bytes : 0,
+                    oc_bn_workspace(n, c));
+  bn_stats(n, c, z, eps, mean, invstd, (double*)ws, s);
+  oc::launch_main(k_bn_pool, dim3(grid_for(np * c)), dim3(TB), s, z,
+                  (const int32_t*)t->labels[l - 1], np, (int)c, (const float*)mean,
+                  (const float*)invstd, gamma, beta, (flags & OC_FUSE_RELU) ? 1 : 0, y, sw);
   OC_LAUNCH_CHECK();
   return OC_OK;
 }
@@ -310,9 +449,9 @@ oc_status oc_bn_bwd(int64_t n, int32_t c, const float* x, const float* dy, const
                     oc_bn_workspace(n, c));
   const int nb = bn_blocks(n, c);
   double* part = (double*)ws;
-  oc::launch(k_bn_partial, dim3(nb), dim3(TB), 0, s, x, dy, n, (int)c, 2, mean, invstd, part);
-  oc::launch(k_bn_final, dim3((unsigned)c), dim3(TB), 0, s, (const double*)part, nb,
-             (int)c, n, 2, 0.f, dbeta, dgamma);
+  oc::launch(k_bn_partial, dim3(nb), dim3(TB), 0, s, x, dy, n, (int)c, mean, invstd, part);
+  oc::launch(k_bn_final, dim3((unsigned)c), dim3(TB), 0, s, (const double*)part, nb, (int)c, dbeta,
+             dgamma);
   oc::launch_main(k_bn_bwd_apply, dim3(grid_for(n * c)), dim3(TB), s, x, dy, n, (int)c, mean,
                   invstd, gamma, (const float*)dgamma, (const float*)dbeta, dx);
   OC_LAUNCH_CHECK();

@@ -81,6 +81,37 @@ def test_head_ops_small():
     assert_f32_close(_np(vt), vr, "sgd v")
 
 
+@pytest.mark.parametrize("seed,B,n,depth,c,relu", [(61, 2, 500, 4, 8, True),
+                                                    (62, 3, 300, 5, 16, False),
+                                                    (63, 1, 200, 3, 3, True)])
+def test_bn_pool_fused(seed, B, n, depth, c, relu):
+    """Normalisation + ReLU + 2x2x2 max-pool in one call: bit-identical to the
+    two calls, and the oracle's normalisation and pooling."""
+    import paper_1712_01537_amd as oc
+    pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
+    ref = oracle.Octree(pts, nrm, offs, depth, 2)
+    tree = oc.oc_build(torch.as_tensor(pts).cuda(), torch.as_tensor(nrm).cuda(), offs, depth, 2)
+    l = depth
+    rng = np.random.default_rng(seed)
+    z = (2 * rng.standard_normal((ref.num(l), c)) + 0.3).astype(np.float32)
+    g = rng.uniform(0.5, 1.5, c).astype(np.float32)
+    b = rng.standard_normal(c).astype(np.float32)
+    y, sw, mean, invstd = oc.oc_bn_pool_fwd(tree, l, _cuda(z), _cuda(g), _cuda(b), relu=relu)
+    a, mean2, invstd2 = oc.oc_bn_fwd(_cuda(z), _cuda(g), _cuda(b), relu=relu)
+    yu, swu = oc.oc_pool_fwd(tree, l, a)
+    assert torch.equal(y.view(torch.int32), yu.view(torch.int32)) and torch.equal(sw, swu)
+    assert torch.equal(mean, mean2) and torch.equal(invstd, invstd2)
+    bn, mr, ir = T.bn_fwd(z, g, b)
+    assert_f32_close(_np(mean), mr, "mean", rtol=1e-6, atol=1e-7)
+    assert_f32_close(_np(invstd), ir, "invstd", rtol=1e-6, atol=1e-7)
+    yr, _ = oracle.pool_fwd(ref.labels(l - 1), np.maximum(bn, 0) if relu else bn)
+    assert_f32_close(_np(y), yr, "pooled")
+    po, swo = oracle.pool_fwd(ref.labels(l - 1), _np(a))  # the GPU's own values: exact
+    np.testing.assert_array_equal(_np(y), po)
+    np.testing.assert_array_equal(_np(sw), swo)
+    tree.free()
+
+
 def test_training_step_full_size():
     import bench
     import paper_1712_01537_amd as oc
@@ -97,9 +128,18 @@ def test_training_step_full_size():
     rec = step.record
     d = synth.make_train_inputs(wl)
     print("[train] forward", flush=True)
+    acts = {}  # the depth-l activations the fused call does not keep, recomputed
     for li, xin, z, a, mean, invstd, p, sw in rec["units"]:
         L = wl.layers[li]
         l = L.depth
+        if a is None:
+            # the same normalisation on the GPU, unpooled (bit-identical to
+            # what the fused call pools: a test of the operations), with the
+            # parameters before the update
+            gb = d["bn"][li]
+            a, mean2, invstd2 = oc.oc_bn_fwd(z, _cuda(gb[0]), _cuda(gb[1]), relu=True)
+            assert torch.equal(mean2, mean) and torch.equal(invstd2, invstd)
+        acts[li] = a
         x_, z_, a_ = _np(xin), _np(z), _np(a)
         w = _np(rec["before"]["dec"]["w"])  # conv weights are at the head of the buffer
         off = sum(27 * M.cin * M.cout for M in wl.layers[:li])
@@ -129,7 +169,7 @@ def test_training_step_full_size():
         L = wl.layers[li]
         l = L.depth
         g_in, da, dz_, dx = (_np(t) for t in rec["bwd"][li])
-        da_r = oracle.relu_bwd(_np(a), oracle.pool_bwd(ref.labels(l - 1), g_in, _np(sw),
+        da_r = oracle.relu_bwd(_np(acts[li]), oracle.pool_bwd(ref.labels(l - 1), g_in, _np(sw),
                                                       ref.num(l)))
         np.testing.assert_array_equal(da, da_r)
         g, b = d["bn"][li]
