@@ -681,8 +681,13 @@ __global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nb
 // blocks of 64 output channels, z = blocks of 64 input channels; 512
 // threads (two waves per SIMD, so that one wave's LDS waits overlap the
 // other's MFMAs).  Per step of eight groups the workgroup stages the unit's
-// positions and the 64 dY rows; x piece o of box position (ix, iy, iz) sits
-// at o ^ 2((iz + 2 iy) & 3), dY piece o of row r at o ^ 2(r & 3).
+// positions and the 64 dY rows; x piece o of box position (ix, iy, iz) of
+// the step's group g sits at o ^ 2(((iz + 2 iy) & 3) ^ (g & 1)), dY piece o
+// of row r at o ^ 2((r & 3) ^ ((r >> 3) & 1)).  A transposing load of a
+// 16-lane group reads four children of one group in four distinct 32-byte
+// slots; the group-parity term moves the next 16-lane group (the next
+// group, at the same positions) onto the other four slots of each 256-byte
+// bank row, so 32 lanes read 256 distinct bytes.
 // part [nranges][K^3][cin][cout].
 template <int K, int MAXC>
 __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ nbr,
@@ -702,7 +707,8 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   constexpr int NBP = NW * 64;               // dwords of a neighbour-row slot (8 groups use 216)
   constexpr int DC = (MAXPOS + GS + NW - 1) / NW;  // DMA instructions of a stage per wave
   __shared__ __attribute__((aligned(16))) v4u lds[NB * BUF];
-  __shared__ __attribute__((aligned(16))) int32_t nbs[3][NBP];  // neighbour rows of a step's groups
+  constexpr int NSLOT = 4;                   // neighbour-row slots
+  __shared__ __attribute__((aligned(16))) int32_t nbs[NSLOT][NBP];  // neighbour rows of a step's groups
   __shared__ __attribute__((aligned(16))) v4u trash[64];        // destination of padding loads
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -727,40 +733,72 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   const int64_t gbeg = ngroups * range / nr, gend = ngroups * (range + 1) / nr;
   const int nsteps = (int)((gend - gbeg + GS - 1) / GS);
 
-  // stage st: x positions (npos instructions of 64 pieces), then the 64 dY
-  // rows (GS instructions); every wave issues DC DMA instructions (padding
-  // loads of zeros into the trash slot)
-  auto stage = [&](int st, v4u* buf) {
+  // Stage st: the unit's x positions (npos DMA instructions of 64 pieces),
+  // then the 64 dY rows (GS instructions); every wave issues DC
+  // instructions, those past the stage load zeros into the trash slot.
+  // What a lane loads depends on the step only through the neighbour rows
+  // and the step's first group, so the rest is worked out once: for an x
+  // instruction k, ta = the lane's neighbour entry (27 g + parent cell) and
+  // tb = its element offset in the row block (child offset * cin + channel;
+  // -1 past cin); for a dY instruction, ta = the lane's group of the step and
+  // tb = row * cout + column (-1 past cout).
+  int ta[DC], tb[DC];
+#pragma unroll
+  for (int k = 0; k < DC; ++k) {
+    const int i = wave + NW * k;
+    ta[k] = 0;
+    tb[k] = -1;
+    if (i < npos) {
+      const int s = i * 64 + lane;
+      const int pos = s >> 3, g = pos / npos, p = pos - g * npos;
+      const int ix = p / (NY * S), rem = p - ix * (NY * S), iy = rem / S, iz = rem - iy * S;
+      const int ux = x0 + ix - R, uy = y0 + iy - R, uz = iz - R;
+      const int o = (s & 7) ^ (2 * (((iz + 2 * iy) & 3) ^ (g & 1)));
+      const int ch = c0 + 8 * o;
+      ta[k] = 27 * g + ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1);
+      if (ch < cin) tb[k] = (4 * (ux & 1) + 2 * (uy & 1) + (uz & 1)) * cin + ch;
+    } else if (i < npos + GS) {
+      const int s = (i - npos) * 64 + lane;
+      const int rl = s >> 3;
+      const int o = (s & 7) ^ (2 * ((rl & 3) ^ ((rl >> 3) & 1)));
+      const int co = n0 + 8 * o;
+      ta[k] = rl >> 3;
+      if (co < cout) tb[k] = rl * cout + co;
+    }
+  }
+  // Source addresses of stage st's instructions, from the neighbour rows in
+  // slot st % NSLOT (read in one batch, one LDS round trip); formed while the
+  // matrix work of an earlier step runs and kept in registers until
+  // stage_issue.
+  auto stage_src = [&](int st, const void* (&src)[DC]) {
     const int64_t gs = gbeg + GS * (int64_t)st;
-    const int nxi = npos;
-    const int32_t* nb = nbs[st % 3];
+    const int64_t left = gend - gs;  // groups of the step inside the range
+    const uint16_t* dys = dy + 8 * gs * cout;
+    const int32_t* nb = nbs[st % NSLOT];
+    int32_t e[DC];
+#pragma unroll
+    for (int k = 0; k < DC; ++k) e[k] = nb[ta[k]];
 #pragma unroll
     for (int k = 0; k < DC; ++k) {
       const int i = wave + NW * k;
-      const void* src = g_zero_rows[(lane + 64 * k + 512 * (int)blockIdx.x) & (ZROWS - 1)];
-      v4u* dst = trash;
-      if (i < nxi) {
-        const int s = i * 64 + lane;
-        const int pos = s >> 3, g = pos / npos, p = pos - g * npos;
-        const int ix = p / (NY * S), rem = p - ix * (NY * S), iy = rem / S, iz = rem - iy * S;
-        const int o = (s & 7) ^ (2 * ((iz + 2 * iy) & 3));
-        const int ch = c0 + 8 * o;
-        const int32_t row = ch < cin ? tile_row<R>(nb + 27 * g, x0 + ix, y0 + iy, iz) : -1;
-        if (row >= 0) src = x + (int64_t)row * cin + ch;
-        dst = buf + i * 64;
-      } else if (i < nxi + GS) {
-        const int s = (i - nxi) * 64 + lane;
-        const int rl = s >> 3;
-        const int o = (s & 7) ^ (2 * (rl & 3));
-        const int co = n0 + 8 * o;
-        const int64_t gg = gs + (rl >> 3);
-        if (gg < gend && co < cout) src = dy + (8 * gg + (rl & 7)) * cout + co;
-        dst = buf + XP + (i - nxi) * 64;
+      const void* a = g_zero_rows[(lane + 64 * k + 512 * (int)blockIdx.x) & (ZROWS - 1)];
+      if (i < npos) {
+        if (e[k] >= 0 && tb[k] >= 0) a = x + (int64_t)e[k] * cin + tb[k];
+      } else if (i < npos + GS) {
+        if (ta[k] < left && tb[k] >= 0) a = dys + tb[k];
       }
-      lds_load16(src, lds_addr(dst));
+      src[k] = a;
     }
   };
-  // neighbour rows of step st's groups into slot st % 3: one dword DMA
+  auto stage_issue = [&](v4u* buf, const void* const (&src)[DC]) {
+#pragma unroll
+    for (int k = 0; k < DC; ++k) {
+      const int i = wave + NW * k;
+      const v4u* dst = i < npos ? buf + i * 64 : i < npos + GS ? buf + XP + (i - npos) * 64 : trash;
+      lds_load16(src[k], lds_addr(dst));
+    }
+  };
+  // neighbour rows of step st's groups into slot st % NSLOT: one dword DMA
   // instruction per wave (entries past the range read -1 from the zero rows'
   // neighbour, see below)
   auto nb_dma = [&](int st) {
@@ -768,7 +806,7 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
     const int64_t g = gbeg + GS * (int64_t)st + e / 27;
     const void* src = e < GS * 27 && g < gend ? (const void*)(nbr + 27 * g + e % 27)
                                              : (const void*)&g_minus1;
-    lds_load4(src, lds_addr(&nbs[st % 3][wave * 64]));
+    lds_load4(src, lds_addr(&nbs[st % NSLOT][wave * 64]));
   };
 
   v4f acc[MAXC][4];
@@ -783,8 +821,7 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   const int r4 = li >> 2, tq = li & 3;
   // Each wave multiplies MAXC (tap, 16-channel block) pairs: combo m = wave +
   // NW mi of the unit's ncombo; pairs past ncombo read pair 0's operands and
-  // their sums are dropped, so that the loop has no branches.  Each pair's A loads are issued before the MFMAs
-  // of the pair before it.
+  // their sums are dropped, so that the loop has no branches.
   auto a_off = [&](int m, int gq, int hh) {  // byte offset of pair m's A load hh
     const int mm = m < ncombo ? m : 0;
     const int it = mm / CB, cb = mm - it * CB;
@@ -792,56 +829,67 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
     const int iy = dyl + (r4 >> 1), iz = dzi + (r4 & 1);  // child 4 hh + r4 of group gq
     const int p = ((dxl + hh) * NY + iy) * S + iz;
     const int o = 2 * cb + (tq >> 1);
-    return ((gq * npos + p) * 8 + (o ^ (2 * ((iz + 2 * iy) & 3)))) * 16 + (tq & 1) * 8;
+    return ((gq * npos + p) * 8 + (o ^ (2 * (((iz + 2 * iy) & 3) ^ (gq & 1))))) * 16 + (tq & 1) * 8;
   };
   auto b_off = [&](int nb, int gq, int hh) {  // byte offset of dY fragment nb, load hh
     const int rl = 8 * gq + 4 * hh + r4;
     const int o = 2 * nb + (tq >> 1);
-    return (XP + rl * 8 + (o ^ (2 * (rl & 3)))) * 16 + (tq & 1) * 8;
+    return (XP + rl * 8 + (o ^ (2 * ((rl & 3) ^ ((rl >> 3) & 1))))) * 16 + (tq & 1) * 8;
   };
-  auto compute = [&](const v4u* buf, auto ncc) {
-    constexpr int NC = decltype(ncc)::value;
-    constexpr int SUBS = GS / 4;
-#pragma unroll
-    for (int sub = 0; sub < SUBS; ++sub) {
-      const int gq = 4 * sub + q;
-      v4u bfr[4];
+  // The step's MFMAs in the fixed order (sub-step, pair): the A operand of
+  // the pair two ahead and the dY fragments of the next sub-step are read
+  // before the current pair's MFMAs are issued (scheduling barriers keep the
+  // order), so the LDS latency hides behind matrix work.  mid() runs after
+  // the first sub-step's MFMAs.
+  auto compute = [&](const v4u* buf, auto&& mid) {
+    constexpr int SUBS = GS / 4, NIT = SUBS * MAXC, AD = 2;
+    auto ld_b = [&](v4u (&b)[4], int sb) {
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb)
-        bfr[nb] = join(lds_tr16(buf, b_off(nb, gq, 0)), lds_tr16(buf, b_off(nb, gq, 1)));
-      v4u a[2];
-      a[0] = join(lds_tr16(buf, a_off(wave, gq, 0)), lds_tr16(buf, a_off(wave, gq, 1)));
+        b[nb] = join(lds_tr16(buf, b_off(nb, 4 * sb + q, 0)), lds_tr16(buf, b_off(nb, 4 * sb + q, 1)));
+    };
+    auto ld_a = [&](int it) {
+      const int sb = it / MAXC, m = wave + NW * (it % MAXC);
+      return join(lds_tr16(buf, a_off(m, 4 * sb + q, 0)), lds_tr16(buf, a_off(m, 4 * sb + q, 1)));
+    };
+    v4u bq[2][4], a[AD + 1];
+    ld_b(bq[0], 0);
 #pragma unroll
-      for (int mi = 0; mi < NC; ++mi) {
-        if (mi + 1 < NC) {
-          const int m1 = wave + NW * (mi + 1);
-          a[(mi + 1) & 1] = join(lds_tr16(buf, a_off(m1, gq, 0)), lds_tr16(buf, a_off(m1, gq, 1)));
-        }
+    for (int it = 0; it < AD; ++it) a[it] = ld_a(it);
+    static_for<NIT>([&](auto itc) {
+      constexpr int it = decltype(itc)::value, sb = it / MAXC, mi = it % MAXC;
+      if constexpr (it + AD < NIT) a[(it + AD) % (AD + 1)] = ld_a(it + AD);
+      if constexpr (mi == 1 && sb + 1 < SUBS) ld_b(bq[(sb + 1) & 1], sb + 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-          acc[mi][nb] = mfma_bf(a[mi & 1], bfr[nb], acc[mi][nb]);
-      }
-    }
+      for (int nb = 0; nb < 4; ++nb) acc[mi][nb] = mfma_bf(a[it % (AD + 1)], bq[sb & 1][nb], acc[mi][nb]);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (it == MAXC - 1) mid();
+    });
   };
 
-  // Load order of a wave: nb(0), nb(1) (waited for); stage(0), nb(2),
-  // stage(1), nb(3); at step st, after the barrier: stage(st+2), nb(st+4).
-  // When step st starts, the loads younger than stage(st) and nb(st+2) are
-  // those of step st-1: DC + 1.
-  nb_dma(0);
-  nb_dma(1);
+  // Load order of a wave: nb(0..3) (waited for); stage(0), stage(1).  At
+  // step st, after the barrier: nb(st+4), stage(st+2).  When step st starts,
+  // the loads younger than stage(st) and nb(st+3) are stage(st+1)'s: DC.
+  // The addresses of stage(st+3) are formed during step st from slot
+  // (st+3) % NSLOT; slot st % NSLOT is refilled at step st, after every wave
+  // has formed stage(st)'s addresses (at step st-3, or before the loop).
+  const void* src[DC];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) nb_dma(k);
   vm_wait0();
   lds_barrier();
-  stage(0, lds);
-  nb_dma(2);
-  stage(1, lds + BUF);
-  nb_dma(3);
+  stage_src(0, src);
+  stage_issue(lds, src);
+  stage_src(1, src);
+  stage_issue(lds + BUF, src);
+  stage_src(2, src);
   for (int st = 0; st < nsteps; ++st) {
-    vm_wait_n<DC + 1>();  // stage st and the neighbour rows of step st+2 have landed
-    lds_barrier();        // ... everywhere; step st-1 is no longer read
-    stage(st + 2, lds + ((st + 2) % NB) * BUF);
+    vm_wait_n<DC>();  // stage st and the neighbour rows of step st+3 have landed
+    lds_barrier();    // ... everywhere; step st-1 is no longer read
     nb_dma(st + 4);
-    compute(lds + (st % NB) * BUF, std::integral_constant<int, MAXC>{});
+    stage_issue(lds + ((st + 2) % NB) * BUF, src);
+    compute(lds + (st % NB) * BUF, [&] { stage_src(st + 3, src); });
   }
   vm_wait0();
 
