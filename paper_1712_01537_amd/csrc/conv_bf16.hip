@@ -435,7 +435,7 @@ struct BfwShape {
   static constexpr int NDMA = GT * S2 * 4 / 64;   // DMA instructions of a slab
   static constexpr int DC = (NDMA + NW - 1) / NW;  // ... per wave
   static constexpr int RS = 68;                    // floats per row of a reduction slot
-  static constexpr int RED = NW * 32 * RS;         // floats of one reduction round
+  static constexpr int RED = NRB * 16 * RS;        // floats of the tile's sum
   static constexpr int NV = (NB * SLAB * 16 > RED * 4 ? NB * SLAB * 16 : RED * 4) / 16;
   static constexpr int slab_of_phase(int ph) { return (ph / K) * S + ph % K; }
   static constexpr int last_slab(int ph) {  // slabs issued by the start of phase ph
@@ -565,8 +565,11 @@ __global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nb
     for (int d = 0; d < 2; ++d) pb[d] = lb + (uint32_t)(q ^ (2 * (px & 1) + ((d + cy) & 1))) * 16;
   };
   const char* lbase = reinterpret_cast<const char*>(lds);
+  // accumulator set b of wave w holds row block (b + w) % 8, so that the
+  // leftover step's row block (w) is set 0 in every wave
   auto opnd = [&](int dyi, int dzi, int b) {
-    return *reinterpret_cast<const v4u*>(lbase + pb[dyi & 1] + ((dyi * S + dzi) * 4 + 2 * b * S2 * 4) * 16);
+    const uint32_t rb = (uint32_t)(((b + wave) & (NRB - 1)) * 2 * S2 * 4 * 16);
+    return *reinterpret_cast<const v4u*>(lbase + pb[dyi & 1] + rb + ((dyi * S + dzi) * 4) * 16);
   };
   auto compute = [&](const v4u (&wv)[4], int n) {
     const int i = n % MI;
@@ -594,15 +597,10 @@ __global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nb
         __builtin_amdgcn_sched_barrier(0);
       }
     } else {
-      const int only = wave % NRB;
+      // the leftover step: this wave's own row block (set 0)
+      const v4u a = opnd(dyi, dzi, 0);
 #pragma unroll
-      for (int b = 0; b < NRB; ++b) {
-        if (b == only) {
-          const v4u a = opnd(dyi, dzi, b);
-#pragma unroll
-          for (int nf = 0; nf < 4; ++nf) acc[b][nf] = mfma_bf(a, wv[nf], acc[b][nf]);
-        }
-      }
+      for (int nf = 0; nf < 4; ++nf) acc[0][nf] = mfma_bf(a, wv[nf], acc[0][nf]);
     }
   };
 
@@ -634,27 +632,32 @@ __global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nb
   });
   vm_wait0();
 
-  // add the waves' tiles in wave order, 32 rows per round (and to out for
-  // a later chunk)
+  // add the waves' tiles through one 128 x 64 sum in LDS: in round r wave w
+  // adds its set r, row block (w + r) % 8, so the eight waves work on eight
+  // distinct blocks; block c gets its terms from waves c, c-1, .., c-7
+  // (mod 8), a fixed order.  Then the sum goes to out (added to it for a
+  // later chunk).
   __syncthreads();
   float* red = reinterpret_cast<float*>(lds);
+#pragma unroll
+  for (int r = 0; r < NRB; ++r) {
+    const int blk = (wave + r) & (NRB - 1);
+#pragma unroll
+    for (int nf = 0; nf < 4; ++nf)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float* d = &red[(16 * blk + 4 * q + j) * RS + 16 * nf + li];
+        *d = r == 0 ? acc[r][nf][j] : *d + acc[r][nf][j];
+      }
+    __syncthreads();
+  }
   const int64_t nrows = 8 * ngroups;
 #pragma unroll
   for (int rd = 0; rd < NRB / 2; ++rd) {
-#pragma unroll
-    for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-      for (int nf = 0; nf < 4; ++nf)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          red[(wave * 32 + bb * 16 + 4 * q + j) * RS + 16 * nf + li] = acc[2 * rd + bb][nf][j];
-    __syncthreads();
-    const int r = tid >> 4, cq = (tid & 15) * 4;
-    const int64_t row = 8 * g0 + 32 * rd + r;
+    const int r = 32 * rd + (tid >> 4), cq = (tid & 15) * 4;
+    const int64_t row = 8 * g0 + r;
     const int n = n0 + cq;
-    v4f sum = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int w = 0; w < NW; ++w) sum += *reinterpret_cast<const v4f*>(&red[(w * 32 + r) * RS + cq]);
+    v4f sum = *reinterpret_cast<const v4f*>(&red[r * RS + cq]);
     if (row < nrows && n < nn) {
       v4f* dst = reinterpret_cast<v4f*>(out + row * nn + n);
       if (acc_in) sum = *dst + sum;
@@ -664,7 +667,6 @@ __global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nb
       }
       *dst = sum;
     }
-    __syncthreads();
   }
 }
 
