@@ -332,7 +332,7 @@ def op_rate(cls, work, us, bf16):
 TRACE_CLASSES = (
     ("build", ("k_quant", "k_mark", "k_reduce", "k_scan_a", "k_scan_c", "k_leaf_mean", "k_emit",
                "__amd_rocclr_copyBuffer")),
-    ("pool", ("k_pool_fwd", "k_route_down", "k_route_up", "k_gpool_")),
+    ("pool", ("k_pool_fwd", "k_route_down", "k_route_up", "k_gpool_", "k_route_parts")),
     ("conv_main", ("k_conv_", "k_cin_", "k_sr_mm<", "k_sr_dw<")),
     ("conv_helper", ("k_sum_", "k_relu_mask", "k_bf_", "k_bf16_to_f32", "k_sr_", "k_dc_",
                      "k_fill_u32")),
@@ -628,6 +628,23 @@ class Step(Accounting):
         """True when conv layer li and the pooling after it run as one call."""
         return pooled_pair(self.wl, li)
 
+    def routed_pool(self, li):
+        """The 2x2x2 max-pool layer right below conv layer li (which made its
+        input) when the conv's input gradient is routed through it in the
+        same call (stride 1, fp32), else None."""
+        ls = self.wl.layers
+        L = ls[li]
+        if (li >= 1 and L.op == "conv" and L.stride == 1 and L.dtype == "f32"
+                and ls[li - 1].op == "pool" and ls[li - 1].depth == L.depth + 1):
+            return li - 1
+        return None
+
+    def pool_mask(self, li):
+        """True when pool layer li sits on a ReLU'd conv: its backward applies
+        that ReLU's backward (the pooled values mask the routed gradient)."""
+        P = self.wl.layers[li - 1] if li > 0 else None
+        return P is not None and P.op == "conv" and P.relu
+
     # --- one step ----------------------------------------------------------
     def key(self, tag, li):
         """Kernel name of a conv pass; the op class for the other ops."""
@@ -785,13 +802,30 @@ class Step(Accounting):
         if rec is not None:  # the tensors of this step, for a parity test
             rec["fwd"] = {li: (xin, yout, sw) for li, xin, yout, sw in saved}
             rec["bwd"] = {}
+        saved_sw = {li: sw for li, xin, yout, sw in saved}
+        routed = set()  # pool layers whose backward ran with the conv above them
         for li, xin, yout, sw in reversed(saved):
             L = wl.layers[li]
             g_in, dw = g, None
+            if li in routed:
+                continue
             if L.op == "conv":
                 w = self.weights[li]
                 relu = L.relu and not masked
-                if li > 0:  # the first layer's input, the signal, needs no gradient
+                below = self.routed_pool(li)
+                if below is not None:
+                    # the input gradient goes straight on through the pooling
+                    # that made x (and the ReLU under it): one call, no
+                    # depth-l gradient
+                    psw, mask = saved_sw[below], self.pool_mask(below)
+                    dxf = self._run("conv_bwd_data", li, lambda: oc.oc_conv_bwd_pool(
+                        tree, L.depth, L.ksize, w, g, psw, xp=xin if mask else None, y=yout,
+                        relu=relu))
+                    routed.add(below)
+                    if rec is not None:
+                        rec["bwd"][below] = (None, dxf, None)
+                    dx = None
+                elif li > 0:  # the first layer's input, the signal, needs no gradient
                     dx, _ = self._run("conv_bwd_data", li, lambda: oc.oc_conv_bwd(
                         tree, L.depth, L.ksize, L.stride, xin, w, g, y=yout, relu=relu,
                         need_dx=True, need_dw=False))
@@ -815,7 +849,10 @@ class Step(Accounting):
                         if t is not None:
                             t.record_stream(self.side)
                     tree.record_stream(self.side)
-                g, masked = dx, False
+                if below is not None:
+                    g, masked = dxf, self.pool_mask(below)
+                else:
+                    g, masked = dx, False
             elif L.op == "deconv":
                 w = self.weights[li]
                 dx, _ = self._run("deconv_bwd_data", li, lambda: oc.oc_deconv_bwd(
@@ -830,15 +867,14 @@ class Step(Accounting):
                 masked = False
             elif L.op == "pool":
                 # a ReLU right below the pooling: its backward goes into the routing
-                P = wl.layers[li - 1] if li > 0 else None
-                masked = P is not None and P.op == "conv" and P.relu
+                masked = self.pool_mask(li)
                 ym = yout if masked else None
                 g = self._run("pool_bwd", li, lambda: oc.oc_pool_bwd(tree, L.depth, g, sw, y=ym))
             elif L.op == "unpool":
                 g = self._run("unpool_bwd", li, lambda: oc.oc_unpool_bwd(tree, L.depth, g, sw))
                 masked = False
-            if rec is not None:
-                rec["bwd"][li] = (g_in, g, dw)
+            if rec is not None:  # a routed input gradient is the pooling's record
+                rec["bwd"][li] = (g_in, None if li - 1 in routed and L.op == "conv" else g, dw)
         if self.side is not None:
             self.torch.cuda.current_stream().wait_stream(self.side)
         return g

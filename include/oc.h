@@ -286,6 +286,34 @@ oc_status oc_conv_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32
                       const float* y, const float* dy, float* dx, float* dw, void* ws,
                       size_t ws_bytes, int32_t flags, hipStream_t stream);
 
+/* The input gradient of a stride-1 fp32 convolution whose input x is the
+ * output of a 2x2x2 max-pooling from depth l+1, carried on through that
+ * pooling's backward (Sec. 3.2 "Pooling" and the transposed products of the
+ * convolution): oc_conv_bwd's input gradient followed by oc_pool_bwd, in one
+ * call that never stores the depth-l gradient (the partial sums of its
+ * split reduction go straight into the routing).
+ *   depth   l, the convolution's depth (depth l+1 must exist).
+ *   w, cin, cout, y, dy, flags   as oc_conv_bwd (OC_FUSE_RELU masks dy with
+ *           [y > 0], the convolution's own ReLU).
+ *   xp      dev f32 [N_l][cin] or NULL: the pooled values (x itself); the
+ *           routed gradient is kept only where xp > 0, the backward of a
+ *           ReLU below the pooling, as oc_pool_bwd's y.
+ *   sw      dev u8 [M_l][cin], the pooling's switches (oc_pool_fwd or
+ *           oc_conv_pool_fwd at depth l+1).
+ *   dxf     dev f32 [N_{l+1}][cin]: overwritten with the gradient w.r.t. the
+ *           pooling's input (the pre-activation of the layer below when xp
+ *           is given).
+ *   ws      dev workspace of oc_conv_bwd_pool_workspace() bytes.
+ * dxf equals, bit for bit, oc_conv_bwd (dx only, same flags) followed by
+ * oc_pool_bwd(depth + 1, dx, sw, xp).  The weight gradient is a separate
+ * oc_conv_bwd call (dx NULL). */
+size_t oc_conv_bwd_pool_workspace(const oc_octree* tree, int32_t depth, int32_t ksize,
+                                  int32_t cin, int32_t cout);
+oc_status oc_conv_bwd_pool(const oc_octree* tree, int32_t depth, int32_t ksize, const float* w,
+                           int32_t cin, int32_t cout, const float* y, const float* dy,
+                           const float* xp, const uint8_t* sw, float* dxf, void* ws,
+                           size_t ws_bytes, int32_t flags, hipStream_t stream);
+
 /* Octree deconvolution, also called transposed convolution (Sec. 3.2
  * "Deconvolution"): the transpose of the convolution cout -> cin with the
  * same weight tensor, obtained as the paper does by swapping that

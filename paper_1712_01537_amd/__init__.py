@@ -32,6 +32,7 @@ __all__ = [
     "oc_profile_next",
     "CallProfile",
     "oc_conv_bwd",
+    "oc_conv_bwd_pool",
     "oc_deconv_fwd",
     "oc_deconv_bwd",
     "oc_pool_fwd",
@@ -71,7 +72,8 @@ EXPORTS = (
     "oc_gpool_fwd", "oc_gpool_bwd", "oc_profile_calls", "oc_conv_fwd_noalloc",
     "oc_bn_workspace", "oc_bn_fwd", "oc_bn_bwd", "oc_fc_fwd", "oc_fc_bwd", "oc_dropout",
     "oc_softmax_ce_workspace", "oc_softmax_ce", "oc_sgd", "oc_conv_pool_fwd",
-    "oc_conv_pool_fwd_workspace", "oc_bn_pool_fwd",
+    "oc_conv_pool_fwd_workspace", "oc_bn_pool_fwd", "oc_conv_bwd_pool_workspace",
+    "oc_conv_bwd_pool",
 )
 
 
@@ -168,6 +170,8 @@ def load():
         "oc_conv_bwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
         "oc_conv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, p, sz, i32, p],
                         C.c_int),
+        "oc_conv_bwd_pool_workspace": ([p, i32, i32, i32, i32], sz),
+        "oc_conv_bwd_pool": ([p, i32, i32, p, i32, i32, p, p, p, p, p, p, sz, i32, p], C.c_int),
         "oc_deconv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, sz, i32, p],
                           C.c_int),
         "oc_deconv_fwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
@@ -528,6 +532,33 @@ def oc_conv_bwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tens
                          _dev(dw, "dw") if dw is not None else None,
                          _dev(ws, "ws"), ws.numel(), OC_FUSE_RELU if relu else 0, _stream()))
     return dx, dw
+
+
+def oc_conv_bwd_pool(tree: Octree, depth: int, ksize: int, w: torch.Tensor, dy: torch.Tensor,
+                     sw: torch.Tensor, xp: torch.Tensor | None = None,
+                     y: torch.Tensor | None = None, relu: bool = False) -> torch.Tensor:
+    """Input gradient of the stride-1 fp32 convolution at depth (input: the
+    2x2x2 max-pool of depth + 1 with switches sw), routed on through that
+    pooling: [N_{depth+1}][cin].  xp: the pooled values (the convolution's
+    input), masking the gradient as oc_pool_bwd's y; relu with y: the
+    convolution's own ReLU applied to dy first."""
+    K3, cin, cout = w.shape
+    if K3 != ksize ** 3:
+        raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
+    if not 1 <= depth < tree.depth:
+        raise OcError(1, f"depth {depth} not in 1..{tree.depth - 1}")
+    n_l, n_f, m = tree.num(depth), tree.num(depth + 1), tree.nonempty(depth)
+    L = load()
+    dxf = torch.empty((n_f, cin), dtype=torch.float32, device=w.device)
+    ws_bytes = int(L.oc_conv_bwd_pool_workspace(tree.handle, depth, ksize, cin, cout))
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=w.device)
+    _check(L.oc_conv_bwd_pool(tree.handle, depth, ksize, _dev(w, "w", torch.float32), cin, cout,
+                              _dev(y, "y", torch.float32, (n_l, cout)) if relu else None,
+                              _dev(dy, "dy", torch.float32, (n_l, cout)),
+                              _dev(xp, "xp", torch.float32, (n_l, cin)) if xp is not None else None,
+                              _dev(sw, "sw", torch.uint8, (m, cin)), _dev(dxf, "dxf"),
+                              _dev(ws, "ws"), ws.numel(), OC_FUSE_RELU if relu else 0, _stream()))
+    return dxf
 
 
 def _deconv_dims(tree: Octree, depth: int, stride: int, x, w):

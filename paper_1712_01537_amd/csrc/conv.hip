@@ -163,6 +163,14 @@ size_t mask_ws_bytes(const ConvShape& sh, int cout) {
   return oc::align256((size_t)sh.n_out * cout * sizeof(float));
 }
 
+// oc_conv_bwd_pool: the depth-l input gradient (stored only when the
+// reduction is not split, or for the unfused shapes), the ReLU-masked
+// upstream gradient, the input gradient's partial sums.
+size_t bwd_pool_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, int cin, int cout) {
+  if (sh.n_in == 0) return 0;
+  return x32_bytes(sh, cin) + mask_ws_bytes(sh, cout) + oc::conv_s1_tile_ws(t, l, sh.K, cout, cin);
+}
+
 size_t bwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,
                     int cout) {
   if (sh.units == 0) return 0;
@@ -305,6 +313,52 @@ size_t oc_conv_bwd_workspace(const oc_octree* t, int32_t l, int32_t K, int32_t s
   ConvShape sh;
   if (check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_bwd_workspace") != OC_OK) return 0;
   return bwd_ws_bytes(t, l, sh, dt, cin, cout);
+}
+
+size_t oc_conv_bwd_pool_workspace(const oc_octree* t, int32_t l, int32_t K, int32_t cin,
+                                  int32_t cout) {
+  ConvShape sh;
+  if (check_conv(t, l, K, 1, OC_F32, cin, cout, &sh, "oc_conv_bwd_pool_workspace") != OC_OK) return 0;
+  return bwd_pool_ws_bytes(t, l, sh, cin, cout);
+}
+
+oc_status oc_conv_bwd_pool(const oc_octree* t, int32_t l, int32_t K, const float* w, int32_t cin,
+                           int32_t cout, const float* y, const float* dy, const float* xp,
+                           const uint8_t* sw, float* dxf, void* ws, size_t ws_bytes,
+                           int32_t flags, hipStream_t s) {
+  ConvShape sh;
+  oc_status st = check_conv(t, l, K, 1, OC_F32, cin, cout, &sh, "oc_conv_bwd_pool");
+  if (st != OC_OK) return st;
+  st = oc::check_tree_level(t, l + 1, 1);
+  if (st != OC_OK) return st;
+  if (sh.n_in == 0) return OC_OK;  // no depth-l octant: no depth-(l+1) octant either
+  if (!w || !dy || !sw || !dxf) return oc::fail(OC_ERR_ARG, "oc_conv_bwd_pool: NULL buffer");
+  if ((flags & OC_FUSE_RELU) && !y)
+    return oc::fail(OC_ERR_ARG, "oc_conv_bwd_pool: OC_FUSE_RELU needs y");
+  const size_t need = bwd_pool_ws_bytes(t, l, sh, cin, cout);
+  if (!ws || ws_bytes < need)
+    return oc::fail(OC_ERR_ARG, "oc_conv_bwd_pool: workspace %zu bytes < %zu", ws ? ws_bytes : 0,
+                    need);
+  float* dxl = (float*)ws;
+  float* wsf = (float*)((char*)ws + x32_bytes(sh, cin));
+  if (flags & OC_FUSE_RELU) {  // dy masked with [y > 0]
+    const int64_t n = sh.n_out * (int64_t)cout;
+    const int vec = (uintptr_t)y % 16 == 0 && (uintptr_t)dy % 16 == 0;
+    oc::launch(k_relu_mask, dim3((unsigned)oc::cdiv(n, 4 * TB)), dim3(TB), 0, s, y, dy, n, vec, 0,
+               wsf);
+    dy = wsf;
+  }
+  wsf = (float*)((char*)wsf + mask_ws_bytes(sh, cout));
+  if (cin % 4 == 0 && (uintptr_t)dxf % 16 == 0 && (uintptr_t)sw % 4 == 0 &&
+      (!xp || (uintptr_t)xp % 16 == 0)) {
+    oc::conv_s1_bwd_data_pool_f32(t, l, K, dy, cout, w, cin, dxl, xp, sw, dxf, wsf, s);
+    OC_LAUNCH_CHECK();
+    return OC_OK;
+  }
+  // other shapes: the depth-l input gradient, then the pool backward
+  oc::conv_s1_bwd_data_f32(t, l, K, dy, cout, w, cin, dxl, wsf, s);
+  OC_LAUNCH_CHECK();
+  return oc_pool_bwd(t, l + 1, dxl, sw, cin, xp, dxf, s);
 }
 
 oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, oc_dtype dt,

@@ -40,6 +40,17 @@ void conv_s1_pool_fwd_f32(const oc_octree* t, int l, int K, const float* x, int 
 void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, int cout,
                           const float* w, int cin, float* dx, float* ws, hipStream_t s);
 
+// The same input gradient routed through the 2x2x2 max-pool from depth l+1
+// that produced x: dxf [N_{l+1}][cin] = the pool backward of it (switches sw
+// [M_l][cin], the gradient kept where the pooled value mask [N_l][cin] is
+// > 0; mask NULL: everywhere).  cin % 4 == 0, dxf 16-byte and sw 4-byte
+// aligned.  dx [N_l][cin] is scratch (written only when the reduction is not
+// split), ws as conv_s1_bwd_data_f32.  Equal, bit for bit, to
+// conv_s1_bwd_data_f32 followed by the pool backward.
+void conv_s1_bwd_data_pool_f32(const oc_octree* t, int l, int K, const float* dy, int cout,
+                               const float* w, int cin, float* dx, const float* mask,
+                               const uint8_t* sw, float* dxf, float* ws, hipStream_t s);
+
 // Number of [K^3][cin][cout] fp32 partial sums conv_s1_bwd_weight_f32 needs.
 size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout);
 

@@ -887,6 +887,65 @@ void sum_split(const float* part, int splits, int64_t n, float* out, int relu, h
                      n, out, relu, vec);
 }
 
+// Max-pool backward (Sec. 3.2 "Pooling") of an input gradient that is still
+// held as the split partial sums of its reduction: thread (g, quad) forms the
+// gradient of group g's parent row rows[g] (depth l) in channels 4 quad ..
+// 4 quad + 3 (splits > 1: the sum over part[z] in k_sum_split's order; 1: the
+// gradient itself) and writes the eight child rows 8g .. 8g+7 (depth l+1):
+// the gradient in the child the switch names where the pooled value mask is
+// > 0 (no mask: NULL), zero elsewhere.  The depth-l gradient is never
+// stored; the result equals k_sum_split followed by the pool backward.
+// pn: floats per split (N_l * cin); cv = cin / 4.
+__global__ __launch_bounds__(TB) void k_route_parts(const float* __restrict__ part, int splits,
+                                                    int64_t pn, const float* __restrict__ mask,
+                                                    const uint8_t* __restrict__ sw,
+                                                    const int32_t* __restrict__ rows,
+                                                    int64_t ngroups, int cv,
+                                                    float* __restrict__ out) {
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= ngroups * cv) return;
+  const int64_t g = t / cv;
+  const int cc = (int)(t - g * cv);
+  const uint32_t sv = reinterpret_cast<const uint32_t*>(sw)[t];
+  const int64_t src = (int64_t)rows[g] * cv + cc;
+  const v4f* p = reinterpret_cast<const v4f*>(part) + src;
+  v4f v;
+  if (splits == 1) {
+    v = p[0];
+  } else {
+    const int64_t n4 = pn / 4;
+    v = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int z = 0; z < splits; ++z) v += p[z * n4];
+  }
+  v4f m = {1.f, 1.f, 1.f, 1.f};
+  if (mask) m = reinterpret_cast<const v4f*>(mask)[src];
+  v4f* dst = reinterpret_cast<v4f*>(out) + 8 * g * cv + cc;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    v4f o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = ((sv >> (8 * e)) & 0xffu) == (uint32_t)k && m[e] > 0.f ? v[e] : 0.f;
+    dst[(int64_t)k * cv] = o;
+  }
+}
+
+// Routing of a depth-l input gradient through the 2x2x2 max-pool from depth
+// l+1 (see k_route_parts).
+struct RouteOut {
+  const float* mask;  // pooled values [N_l][cin], or NULL
+  const uint8_t* sw;  // switches [M_l][cin]
+  float* out;         // [N_{l+1}][cin]
+};
+
+void route_parts(const oc_octree* t, int l, const float* part, int splits, int cin,
+                 const RouteOut& ro, hipStream_t s) {
+  const int64_t G = t->M[l];
+  const int cv = cin / 4;
+  if (G == 0) return;
+  oc::launch(k_route_parts, dim3((unsigned)oc::cdiv(G * cv, TB)), dim3(TB), 0, s, part, splits,
+             t->N[l] * (int64_t)cin, ro.mask, ro.sw, (const int32_t*)t->rows[l], G, cv, ro.out);
+}
+
 // ---------------------------------------------------------------------------
 // Weight gradient partial sums, stride 1:
 //   dW[k][c][n] = sum over octants i of x[nb(i,k)][c] * dY[i][n], an M x N =
@@ -1476,7 +1535,8 @@ TileCfg pick_tile(int K, int64_t G, int kk, int nn) {
 
 template <int K, int V, int MR, int NR, int WM, bool FLIP, bool VEC>
 void launch_tile(const oc_octree* t, int l, const TileCfg& c, const float* x, int kk,
-                 const float* w, int nn, float* out, int relu, float* part, hipStream_t s) {
+                 const float* w, int nn, float* out, int relu, float* part, hipStream_t s,
+                 const RouteOut* ro = nullptr) {
   const auto kernel = k_conv_tile<K, V, MR, NR, WM, FLIP, VEC>;
   static const int occ = [&] {
     int n = 0;
@@ -1494,7 +1554,9 @@ void launch_tile(const oc_octree* t, int l, const TileCfg& c, const float* x, in
   dim3 grid((unsigned)px, (unsigned)oc::cdiv(nn, BN), (unsigned)c.splits);
   oc::launch_main(kernel, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, kk, w, nn, out, relu,
                   c.cps, part);
-  if (c.splits > 1) {
+  if (ro) {  // input gradient routed on (relu is 0)
+    route_parts(t, l, c.splits > 1 ? part : out, c.splits, nn, *ro, s);
+  } else if (c.splits > 1) {
     sum_split(part, c.splits, t->N[l] * (int64_t)nn, out, relu, s);
   }
 }
@@ -1509,7 +1571,7 @@ struct PoolOut {
 template <int NR, int GPB, bool FLIP>
 void launch_tile2(const oc_octree* t, int l, const TileCfg& c, const float* x, int kk,
                   const float* w, int nn, float* out, int relu, float* part, hipStream_t s,
-                  const PoolOut* po = nullptr) {
+                  const PoolOut* po = nullptr, const RouteOut* ro = nullptr) {
   const auto plain = k_conv_tile3<NR, GPB, FLIP, false>;
   const auto pooled = k_conv_tile3<NR, GPB, FLIP, true>;
   const bool fuse = !FLIP && po && c.splits == 1;
@@ -1535,6 +1597,10 @@ void launch_tile2(const oc_octree* t, int l, const TileCfg& c, const float* x, i
   oc::launch_main(kernel, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, kk, w, nn, out,
                   relu, part, (const int32_t*)nullptr, (const int32_t*)nullptr, (int64_t)0,
                   (uint8_t*)nullptr);
+  if (ro) {  // input gradient routed on (relu is 0)
+    route_parts(t, l, c.splits > 1 ? part : out, c.splits, nn, *ro, s);
+    return;
+  }
   if (c.splits > 1) {
     if (po) {
       const int cv = nn / 4;
@@ -1550,22 +1616,23 @@ void launch_tile2(const oc_octree* t, int l, const TileCfg& c, const float* x, i
 
 template <bool FLIP>
 void dispatch_tile(const oc_octree* t, int l, int K, const float* x, int kk, const float* w,
-                   int nn, float* out, int relu, float* part, hipStream_t s) {
+                   int nn, float* out, int relu, float* part, hipStream_t s,
+                   const RouteOut* ro = nullptr) {
   const TileCfg c = pick_tile(K, t->M[l - 1], kk, nn);
   if (c.v2) {
-#define OC_T3(NR_, GPB_)                                                       \
-  if (c.NR == NR_ && c.gpb == GPB_) {                                          \
-    launch_tile2<NR_, GPB_, FLIP>(t, l, c, x, kk, w, nn, out, relu, part, s);  \
-    return;                                                                    \
+#define OC_T3(NR_, GPB_)                                                                 \
+  if (c.NR == NR_ && c.gpb == GPB_) {                                                    \
+    launch_tile2<NR_, GPB_, FLIP>(t, l, c, x, kk, w, nn, out, relu, part, s, nullptr, ro); \
+    return;                                                                              \
   }
     OC_T3(1, 8) OC_T3(2, 8) OC_T3(2, 4) OC_T3(4, 8) OC_T3(4, 4) OC_T3(4, 2)
 #undef OC_T3
     return;
   }
-#define OC_TILE(K_, V_, MR_, NR_, WM_, VEC_)                                                \
-  if (K == K_ && c.V == V_ && c.MR == MR_ && c.NR == NR_ && c.WM == WM_ && c.VEC == VEC_) { \
-    launch_tile<K_, V_, MR_, NR_, WM_, FLIP, VEC_>(t, l, c, x, kk, w, nn, out, relu, part, s); \
-    return;                                                                                 \
+#define OC_TILE(K_, V_, MR_, NR_, WM_, VEC_)                                                    \
+  if (K == K_ && c.V == V_ && c.MR == MR_ && c.NR == NR_ && c.WM == WM_ && c.VEC == VEC_) {     \
+    launch_tile<K_, V_, MR_, NR_, WM_, FLIP, VEC_>(t, l, c, x, kk, w, nn, out, relu, part, s, ro); \
+    return;                                                                                     \
   }
   OC_TILE(3, 4, 1, 1, 4, true) OC_TILE(3, 4, 1, 2, 4, true)
   OC_TILE(3, 1, 2, 1, 4, true) OC_TILE(3, 1, 2, 1, 4, false)
@@ -1816,6 +1883,13 @@ void conv_s1_pool_fwd_f32(const oc_octree* t, int l, int K, const float* x, int 
 void conv_s1_bwd_data_f32(const oc_octree* t, int l, int K, const float* dy, int cout,
                           const float* w, int cin, float* dx, float* ws, hipStream_t s) {
   dispatch_tile<true>(t, l, K, dy, cout, w, cin, dx, 0, ws, s);
+}
+
+void conv_s1_bwd_data_pool_f32(const oc_octree* t, int l, int K, const float* dy, int cout,
+                               const float* w, int cin, float* dx, const float* mask,
+                               const uint8_t* sw, float* dxf, float* ws, hipStream_t s) {
+  const RouteOut ro{mask, sw, dxf};
+  dispatch_tile<true>(t, l, K, dy, cout, w, cin, dx, 0, ws, s, &ro);
 }
 
 size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout) {

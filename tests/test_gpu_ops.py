@@ -447,6 +447,57 @@ def test_conv_pool_small(seed, B, n, depth, K, cin, cout, relu, bf16):
                      torch.bfloat16 if bf16 else torch.float32, yref)
 
 
+CONV_BWD_POOL_SMALL = [  # seed, B, n, fine depth, K, cin, cout, conv ReLU, pooled-value mask
+    (141, 2, 500, 5, 3, 16, 16, False, True),   # one reduction chunk: no split
+    (142, 2, 600, 5, 3, 16, 32, True, True),    # two splits, the convolution's own ReLU
+    (143, 3, 400, 4, 3, 32, 64, False, True),   # four splits
+    (144, 2, 500, 4, 3, 64, 128, True, True),   # eight splits
+    (145, 2, 400, 4, 3, 6, 8, False, True),     # cin % 4 != 0: gradient, then routing
+    (146, 1, 500, 4, 5, 8, 8, False, True),     # K = 5 group-tile kernel
+    (147, 2, 300, 4, 3, 4, 16, True, False),    # no mask
+]
+
+
+@pytest.mark.parametrize("seed,B,n,depth,K,cin,cout,relu,masked", CONV_BWD_POOL_SMALL)
+def test_conv_bwd_pool_small(seed, B, n, depth, K, cin, cout, relu, masked):
+    """Input gradient of a convolution routed on through the max-pool that
+    produced its input (Sec. 3.2 "Pooling"): bit for bit oc_conv_bwd's input
+    gradient followed by oc_pool_bwd, and the oracle's gradient within the
+    fp32 tolerance."""
+    print(f"[conv_bwd_pool] seed={seed} B={B} d={depth} K={K} {cin}->{cout} relu={relu} "
+          f"masked={masked}", flush=True)
+    oc = _oc()
+    pts, nrm, offs = synth.random_cloud(seed, B, n, "union")
+    ref, tree = _trees(pts, nrm, offs, depth)
+    lf, l = depth, depth - 1
+    rng = np.random.default_rng(seed)
+    # the layer below: ReLU'd activations at depth lf, pooled to depth l
+    z = rng.standard_normal((ref.num(lf), cin)).astype(np.float32)
+    z[1::7] = 0.0
+    a = np.maximum(z, 0.0)
+    p, sw = oc.oc_pool_fwd(tree, lf, _cuda(a))
+    _, swr = oracle.pool_fwd(ref.labels(l), a)
+    w = (rng.standard_normal((K ** 3, cin, cout)) / np.sqrt(K ** 3 * cin)).astype(np.float32)
+    dy = rng.standard_normal((ref.num(l), cout)).astype(np.float32)
+    y = rng.standard_normal((ref.num(l), cout)).astype(np.float32)
+    y[::3] = 0.0
+    wg, dyg, yg = _cuda(w), _cuda(dy), _cuda(y)
+    xp = p if masked else None
+    dxf = oc.oc_conv_bwd_pool(tree, l, K, wg, dyg, sw, xp=xp, y=yg, relu=relu)
+    dx, _ = oc.oc_conv_bwd(tree, l, K, 1, p, wg, dyg, y=yg, relu=relu, need_dx=True,
+                           need_dw=False)
+    dxu = oc.oc_pool_bwd(tree, lf, dx, sw, y=xp)
+    assert torch.equal(dxf.view(torch.int32), dxu.view(torch.int32)), "fused != unfused"
+    g = oracle.relu_bwd(y, dy) if relu else dy
+    dxo = oracle.conv_bwd_data(ref.neighbors(l, K), g, w, ref.num(l))
+    ro = oracle.pool_bwd(ref.labels(l), dxo, swr, ref.num(lf))
+    if masked:
+        ro = oracle.relu_bwd(z, ro)
+    assert_f32_close(dxf.cpu().numpy(), ro, f"conv_bwd_pool {seed}")
+    dxf2 = oc.oc_conv_bwd_pool(tree, l, K, wg, dyg, sw, xp=xp, y=yg, relu=relu)
+    assert torch.equal(dxf.view(torch.int32), dxf2.view(torch.int32)), "not reproducible"
+
+
 def test_conv_pool_one_point_tree():
     """A one-point tree (one sibling group per depth) down to depth 1."""
     pts = np.array([[0.3, 0.6, 0.9]], np.float32)

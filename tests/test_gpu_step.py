@@ -1,8 +1,9 @@
 """The timed step of the bench, end to end at full size: the call sequence
 bench.py runs (fused ReLU in the forward, conv + ReLU + pool in one call
 where a pooling follows a convolution, the ReLU's backward inside the
-pooling's routing, no input gradient for the first layer, separate input-
-and weight-gradient calls) on the octree the GPU builds, every tensor of the
+pooling's routing, a convolution's input gradient routed through the
+pooling below it in one call, no input gradient for the first layer,
+separate input- and weight-gradient calls) on the octree the GPU builds, every tensor of the
 step against the oracle.
 
 Each op is checked on the GPU's own inputs to that op, so errors do not
@@ -106,6 +107,19 @@ def test_bench_step_end_to_end(name):
             print(f"[step] {name}/{li} dw rule: {rule}", flush=True)
             if li == 0:
                 assert g_out is None  # the signal needs no gradient
+            elif g_out is None:
+                # the input gradient went on through the pooling below in the
+                # same call: check the routed gradient the pooling recorded
+                assert step.routed_pool(li) == li - 1
+                _, routed_gpu, _ = (_np(t) for t in bwd[li - 1])
+                px, _, psw = (_np(t) for t in fwd[li - 1])
+                if px is None:
+                    px = unpooled[li - 1]
+                routed = oracle.pool_bwd(ref.labels(l), oracle.conv_bwd_data(nb, ge, w, x.shape[0]),
+                                         psw, ref.num(l + 1))
+                if step.pool_mask(li - 1):
+                    routed = oracle.relu_bwd(px, routed)  # the ReLU below, on the GPU's values
+                assert_f32_close(routed_gpu, routed, f"{name}/{li} dx routed")
             else:
                 assert_f32_close(g_out, oracle.conv_bwd_data(nb, ge, w, x.shape[0]),
                                  f"{name}/{li} dx")
@@ -117,6 +131,8 @@ def test_bench_step_end_to_end(name):
                 dxr, dwr = oracle.deconv_s2_bwd(ref, l, x, w, g_in)
             assert_f32_close(g_out, dxr, f"{name}/{li} dx")
             assert_dw_close(dw, dwr, f"{name}/{li} dw")
+        elif L.op == "pool" and g_in is None:
+            continue  # routed with the input gradient of the conv above (checked there)
         elif L.op == "pool":
             routed = oracle.pool_bwd(ref.labels(l - 1), g_in, sw, ref.num(l))
             below = wl.layers[li - 1] if li > 0 else None
