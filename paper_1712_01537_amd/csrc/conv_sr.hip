@@ -142,6 +142,8 @@ __global__ __launch_bounds__(TB) void k_sr_table(const int32_t* __restrict__ nbr
 //   tap's last chunk), skipped when absent.
 // A workgroup is WGM x WGN waves; a wave owns WR x WC blocks of 16 rows x 16
 // columns, so one LDS read of A feeds WC MFMA groups and one of B feeds WR.
+// A stage is KS consecutive (slot, chunk) steps: its global loads are issued
+// a stage ahead, and one barrier per stage separates the LDS buffers.
 enum { MODE_FWD = 0, MODE_DX1 = 1, MODE_DXS = 2 };
 
 struct MmArgs {
@@ -156,15 +158,15 @@ struct MmArgs {
   int C, N, relu, vec;  // vec: C * sizeof(T) % 16 == 0 and aligned buffers (16-byte pieces)
 };
 
-template <typename T, int MODE, int WGM, int WGN, int WR, int WC>
+template <typename T, int MODE, int WGM, int WGN, int WR, int WC, int KS>
 __global__ __launch_bounds__(TB) void k_sr_mm(MmArgs g) {
   static_assert(WGM * WGN * 64 == TB, "waves");
   constexpr int BM = 16 * WR * WGM, BN = 16 * WC * WGN;
   constexpr int ES = sizeof(T), EPP = 16 / ES, KC = 64 / ES;  // elements per piece, per chunk
   constexpr int APT = BM * 4 / TB, BPT = (BN * 4 + TB - 1) / TB;  // pieces per thread
   static_assert(BM * 4 % TB == 0, "A pieces");
-  __shared__ __attribute__((aligned(16))) char lA[2][BM * LROW];
-  __shared__ __attribute__((aligned(16))) char lB[2][BN * LROW];
+  __shared__ __attribute__((aligned(16))) char lA[2][KS][BM * LROW];
+  __shared__ __attribute__((aligned(16))) char lB[2][KS][BN * LROW];
   __shared__ int32_t ltab[BM][8];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -211,15 +213,16 @@ __global__ __launch_bounds__(TB) void k_sr_mm(MmArgs g) {
   };
   auto btap = [&](int j) -> int { return MODE == MODE_DX1 ? dx1_tap(cls, subset(cls, j)) : j; };
 
-  v4u pa[APT], pb[BPT];
-  // global loads of step t into pa, pb
-  auto load = [&](int t) {
-    const int j = t / nch, c0 = (t - j * nch) * KC;
+  v4u pa[KS][APT], pb[KS][BPT];
+  // global loads of step t into pa, pb (zeros past the last step)
+  auto load = [&](int t, v4u (&pa)[APT], v4u (&pb)[BPT]) {
+    const bool live = t < nsteps;
+    const int j = live ? t / nch : 0, c0 = (t - j * nch) * KC;
 #pragma unroll
     for (int u = 0; u < APT; ++u) {
       const int e = tid + TB * u, mm = e >> 2, part = e & 3;
       const int c = c0 + part * EPP;
-      const int64_t row = arow(mm, j);
+      const int64_t row = live ? arow(mm, j) : -1;
       if (g.vec) {
         const uint32_t off = row >= 0 && c < C ? (uint32_t)((row * C + c) * ES) : OOB;
         pa[u] = bload16(ra, off);
@@ -242,7 +245,7 @@ __global__ __launch_bounds__(TB) void k_sr_mm(MmArgs g) {
     for (int u = 0; u < BPT; ++u) {
       const int e = tid + TB * u, nn = e >> 2, part = e & 3;
       const int c = c0 + part * EPP, n = n0 + nn;
-      const bool ok = e < BN * 4 && n < N;
+      const bool ok = live && e < BN * 4 && n < N;
       if (g.vec) {
         const uint32_t off = ok && c < C ? (uint32_t)(((bbase + n) * C + c) * ES) : OOB;
         pb[u] = bload16(rb, off);
@@ -262,16 +265,24 @@ __global__ __launch_bounds__(TB) void k_sr_mm(MmArgs g) {
       }
     }
   };
+  auto load_stage = [&](int st) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) load(st * KS + ks, pa[ks], pb[ks]);
+  };
   auto stash = [&](int buf) {
 #pragma unroll
-    for (int u = 0; u < APT; ++u) {
-      const int e = tid + TB * u;
-      *reinterpret_cast<v4u*>(&lA[buf][(e >> 2) * LROW + (e & 3) * 16]) = pa[u];
-    }
+    for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-    for (int u = 0; u < BPT; ++u) {
-      const int e = tid + TB * u;
-      if (e < BN * 4) *reinterpret_cast<v4u*>(&lB[buf][(e >> 2) * LROW + (e & 3) * 16]) = pb[u];
+      for (int u = 0; u < APT; ++u) {
+        const int e = tid + TB * u;
+        *reinterpret_cast<v4u*>(&lA[buf][ks][(e >> 2) * LROW + (e & 3) * 16]) = pa[ks][u];
+      }
+#pragma unroll
+      for (int u = 0; u < BPT; ++u) {
+        const int e = tid + TB * u;
+        if (e < BN * 4)
+          *reinterpret_cast<v4u*>(&lB[buf][ks][(e >> 2) * LROW + (e & 3) * 16]) = pb[ks][u];
+      }
     }
   };
 
@@ -319,31 +330,40 @@ __global__ __launch_bounds__(TB) void k_sr_mm(MmArgs g) {
     }
   };
 
-  load(0);
+  const int nstages = (nsteps + KS - 1) / KS;
+  load_stage(0);
   stash(0);
   __syncthreads();
-  for (int t = 0; t < nsteps; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < nsteps) load(t + 1);
-    v4u av[WC], bv[WR];
+  for (int st = 0; st < nstages; ++st) {
+    const int buf = st & 1;
+    if (st + 1 < nstages) load_stage(st + 1);
 #pragma unroll
-    for (int k = 0; k < WC; ++k)
-      av[k] = *reinterpret_cast<const v4u*>(&lB[buf][((wn * WC + k) * 16 + li) * LROW + q * 16]);
+    for (int ks = 0; ks < KS; ++ks) {
+      const int t = st * KS + ks;
+      if (t < nsteps) {  // uniform
+        v4u av[WC], bv[WR];
 #pragma unroll
-    for (int i = 0; i < WR; ++i)
-      bv[i] = *reinterpret_cast<const v4u*>(&lA[buf][((wm * WR + i) * 16 + li) * LROW + q * 16]);
+        for (int k = 0; k < WC; ++k)
+          av[k] = *reinterpret_cast<const v4u*>(
+              &lB[buf][ks][((wn * WC + k) * 16 + li) * LROW + q * 16]);
 #pragma unroll
-    for (int i = 0; i < WR; ++i)
+        for (int i = 0; i < WR; ++i)
+          bv[i] = *reinterpret_cast<const v4u*>(
+              &lA[buf][ks][((wm * WR + i) * 16 + li) * LROW + q * 16]);
 #pragma unroll
-      for (int k = 0; k < WC; ++k) acc[i][k] = mma(av[k], bv[i], acc[i][k], T{});
-    if (MODE == MODE_DXS && (t + 1) % nch == 0) {
-      store(t / nch);
+        for (int i = 0; i < WR; ++i)
 #pragma unroll
-      for (int i = 0; i < WR; ++i)
+          for (int k = 0; k < WC; ++k) acc[i][k] = mma(av[k], bv[i], acc[i][k], T{});
+        if (MODE == MODE_DXS && (t + 1) % nch == 0) {
+          store(t / nch);
 #pragma unroll
-        for (int k = 0; k < WC; ++k) acc[i][k] = v4f{0.f, 0.f, 0.f, 0.f};
+          for (int i = 0; i < WR; ++i)
+#pragma unroll
+            for (int k = 0; k < WC; ++k) acc[i][k] = v4f{0.f, 0.f, 0.f, 0.f};
+        }
+      }
     }
-    if (t + 1 < nsteps) stash(buf ^ 1);
+    if (st + 1 < nstages) stash(buf ^ 1);
     __syncthreads();
   }
   if (MODE != MODE_DXS) store(0);
@@ -644,11 +664,13 @@ void launch_mm(const MmArgs& a, int classes, bool main_kernel, hipStream_t s) {
       oc::launch(kern, grid, blk, 0, s, a);
   };
   if (a.N <= 16)
-    go(k_sr_mm<T, MODE, 4, 1, 1, 1>, 64, 16);
+    go(k_sr_mm<T, MODE, 4, 1, 1, 1, 4>, 64, 16);
   else if (a.N <= 32)
-    go(k_sr_mm<T, MODE, 4, 1, 1, 2>, 64, 32);
+    go(k_sr_mm<T, MODE, 4, 1, 1, 2, 4>, 64, 32);
+  else if (a.N <= 64)
+    go(k_sr_mm<T, MODE, 2, 2, 2, 2, 1>, 64, 64);
   else
-    go(k_sr_mm<T, MODE, 2, 2, 2, 2>, 64, 64);
+    go(k_sr_mm<T, MODE, 2, 2, 4, 4, 1>, 128, 128);
 }
 
 template <typename T>
@@ -687,7 +709,10 @@ const char* conv_sr_kernel_name(int pass, int r, bool bf16, int cin, int cout) {
   } else {
     const int n = pass == 0 ? cout : cin;
     const int mode = pass == 0 ? MODE_FWD : r == 1 ? MODE_DX1 : MODE_DXS;
-    const char* cfg = n <= 16 ? "4, 1, 1, 1" : n <= 32 ? "4, 1, 1, 2" : "2, 2, 2, 2";
+    const char* cfg = n <= 16   ? "4, 1, 1, 1, 4"
+                      : n <= 32 ? "4, 1, 1, 2, 4"
+                      : n <= 64 ? "2, 2, 2, 2, 1"
+                                : "2, 2, 4, 4, 1";
     snprintf(buf, sizeof(buf), "k_sr_mm<%s, %d, %s>", T, mode, cfg);
   }
   return buf;
