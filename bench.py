@@ -980,25 +980,32 @@ class TrainStep(Step):
         if rec is not None:
             rec.update(units=units, feat=feat, h0=h0, h1=h1, h2=h2, logits=zl, loss=loss,
                        dlogits=dz, dh1=dh1, dfeat=g, bwd={})
+        da_up = None  # the unit above routed its input gradient into this unit's pooling
         for li, xin, z, a, mean, invstd, p, sw in reversed(units):
             L = wl.layers[li]
             w = self.conv_p[li]["w"]
             g_in = g
-            # the ReLU's backward rides on the routing (the pooled output)
-            da = self._run("pool_bwd", li, lambda: oc.oc_pool_bwd(tree, L.depth, g, sw, y=p))
+            if da_up is None:
+                # the ReLU's backward rides on the routing (the pooled output)
+                da = self._run("pool_bwd", li, lambda: oc.oc_pool_bwd(tree, L.depth, g, sw, y=p))
+            else:
+                da = da_up
             dz_, _, _ = self._run("bn_bwd", li, lambda: oc.oc_bn_bwd(
                 z, da, self.gamma[li]["w"], mean, invstd, dgamma=self.gamma[li]["g"],
                 dbeta=self.beta[li]["g"]))
-            dx = None
+            da_up = None
             if li > 0:  # the signal needs no gradient
-                dx, _ = self._run("conv_bwd_data", li, lambda: oc.oc_conv_bwd(
-                    tree, L.depth, 3, 1, xin, w, dz_, need_dx=True, need_dw=False))
+                # the input gradient goes on through the pooling (and ReLU) of
+                # the unit below in the same call: that unit's da
+                _, _, _, _, _, _, p_below, sw_below = units[li - 1]
+                da_up = self._run("conv_bwd_data", li, lambda: oc.oc_conv_bwd_pool(
+                    tree, L.depth, 3, w, dz_, sw_below, xp=p_below))
             self._run("conv_bwd_weight", li, lambda: oc.oc_conv_bwd(
                 tree, L.depth, 3, 1, xin, w, dz_, need_dx=False, need_dw=True,
                 dw_out=self.conv_p[li]["g"]))
             if rec is not None:
-                rec["bwd"][li] = (g_in, da, dz_, dx)
-            g = dx
+                rec["bwd"][li] = (g_in, da, dz_, None)
+            g = None
         if rec is not None:  # parameters and velocities before the update
             rec["before"] = {k: {q: b[q].clone() for q in ("w", "v")} for k, b in self.flat.items()}
         for key, dec in (("dec", self.DECAY), ("pla", 0.0)):
