@@ -818,9 +818,13 @@ class Step(Accounting):
                     # that made x (and the ReLU under it): one call, no
                     # depth-l gradient
                     psw, mask = saved_sw[below], self.pool_mask(below)
+                    # the ReLU's backward once: the masked dy serves the weight gradient too
+                    dym = self.torch.empty_like(g) if relu else None
                     dxf = self._run("conv_bwd_data", li, lambda: oc.oc_conv_bwd_pool(
                         tree, L.depth, L.ksize, w, g, psw, xp=xin if mask else None, y=yout,
-                        relu=relu))
+                        relu=relu, dym=dym))
+                    if dym is not None:
+                        g, relu = dym, False
                     routed.add(below)
                     if rec is not None:
                         rec["bwd"][below] = (None, dxf, None)

@@ -303,6 +303,9 @@ oc_status oc_conv_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32
  *   dxf     dev f32 [N_{l+1}][cin]: overwritten with the gradient w.r.t. the
  *           pooling's input (the pre-activation of the layer below when xp
  *           is given).
+ *   dym     dev f32 [N_l][cout] or NULL: with OC_FUSE_RELU, receives dy
+ *           masked with [y > 0] (the operand the weight gradient needs: a
+ *           following oc_conv_bwd for dw can take it without OC_FUSE_RELU).
  *   ws      dev workspace of oc_conv_bwd_pool_workspace() bytes.
  * dxf equals, bit for bit, oc_conv_bwd (dx only, same flags) followed by
  * oc_pool_bwd(depth + 1, dx, sw, xp).  The weight gradient is a separate
@@ -311,7 +314,7 @@ size_t oc_conv_bwd_pool_workspace(const oc_octree* tree, int32_t depth, int32_t 
                                   int32_t cin, int32_t cout);
 oc_status oc_conv_bwd_pool(const oc_octree* tree, int32_t depth, int32_t ksize, const float* w,
                            int32_t cin, int32_t cout, const float* y, const float* dy,
-                           const float* xp, const uint8_t* sw, float* dxf, void* ws,
+                           const float* xp, const uint8_t* sw, float* dxf, float* dym, void* ws,
                            size_t ws_bytes, int32_t flags, hipStream_t stream);
 
 /* Octree deconvolution, also called transposed convolution (Sec. 3.2

@@ -171,7 +171,8 @@ def load():
         "oc_conv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, p, sz, i32, p],
                         C.c_int),
         "oc_conv_bwd_pool_workspace": ([p, i32, i32, i32, i32], sz),
-        "oc_conv_bwd_pool": ([p, i32, i32, p, i32, i32, p, p, p, p, p, p, sz, i32, p], C.c_int),
+        "oc_conv_bwd_pool": ([p, i32, i32, p, i32, i32, p, p, p, p, p, p, p, sz, i32, p],
+                             C.c_int),
         "oc_deconv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, sz, i32, p],
                           C.c_int),
         "oc_deconv_fwd_workspace": ([p, i32, i32, i32, C.c_int, i32, i32], sz),
@@ -536,12 +537,14 @@ def oc_conv_bwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tens
 
 def oc_conv_bwd_pool(tree: Octree, depth: int, ksize: int, w: torch.Tensor, dy: torch.Tensor,
                      sw: torch.Tensor, xp: torch.Tensor | None = None,
-                     y: torch.Tensor | None = None, relu: bool = False) -> torch.Tensor:
+                     y: torch.Tensor | None = None, relu: bool = False,
+                     dym: torch.Tensor | None = None) -> torch.Tensor:
     """Input gradient of the stride-1 fp32 convolution at depth (input: the
     2x2x2 max-pool of depth + 1 with switches sw), routed on through that
     pooling: [N_{depth+1}][cin].  xp: the pooled values (the convolution's
     input), masking the gradient as oc_pool_bwd's y; relu with y: the
-    convolution's own ReLU applied to dy first."""
+    convolution's own ReLU applied to dy first, the masked dy also written
+    to dym when given."""
     K3, cin, cout = w.shape
     if K3 != ksize ** 3:
         raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
@@ -557,6 +560,8 @@ def oc_conv_bwd_pool(tree: Octree, depth: int, ksize: int, w: torch.Tensor, dy: 
                               _dev(dy, "dy", torch.float32, (n_l, cout)),
                               _dev(xp, "xp", torch.float32, (n_l, cin)) if xp is not None else None,
                               _dev(sw, "sw", torch.uint8, (m, cin)), _dev(dxf, "dxf"),
+                              _dev(dym, "dym", torch.float32, (n_l, cout))
+                              if dym is not None and relu else None,
                               _dev(ws, "ws"), ws.numel(), OC_FUSE_RELU if relu else 0, _stream()))
     return dxf
 

@@ -324,7 +324,7 @@ size_t oc_conv_bwd_pool_workspace(const oc_octree* t, int32_t l, int32_t K, int3
 
 oc_status oc_conv_bwd_pool(const oc_octree* t, int32_t l, int32_t K, const float* w, int32_t cin,
                            int32_t cout, const float* y, const float* dy, const float* xp,
-                           const uint8_t* sw, float* dxf, void* ws, size_t ws_bytes,
+                           const uint8_t* sw, float* dxf, float* dym, void* ws, size_t ws_bytes,
                            int32_t flags, hipStream_t s) {
   ConvShape sh;
   oc_status st = check_conv(t, l, K, 1, OC_F32, cin, cout, &sh, "oc_conv_bwd_pool");
@@ -341,12 +341,13 @@ oc_status oc_conv_bwd_pool(const oc_octree* t, int32_t l, int32_t K, const float
                     need);
   float* dxl = (float*)ws;
   float* wsf = (float*)((char*)ws + x32_bytes(sh, cin));
-  if (flags & OC_FUSE_RELU) {  // dy masked with [y > 0]
+  if (flags & OC_FUSE_RELU) {  // dy masked with [y > 0] (into dym when given)
+    float* m = dym ? dym : wsf;
     const int64_t n = sh.n_out * (int64_t)cout;
-    const int vec = (uintptr_t)y % 16 == 0 && (uintptr_t)dy % 16 == 0;
+    const int vec = (uintptr_t)y % 16 == 0 && (uintptr_t)dy % 16 == 0 && (uintptr_t)m % 16 == 0;
     oc::launch(k_relu_mask, dim3((unsigned)oc::cdiv(n, 4 * TB)), dim3(TB), 0, s, y, dy, n, vec, 0,
-               wsf);
-    dy = wsf;
+               m);
+    dy = m;
   }
   wsf = (float*)((char*)wsf + mask_ws_bytes(sh, cout));
   if (cin % 4 == 0 && (uintptr_t)dxf % 16 == 0 && (uintptr_t)sw % 4 == 0 &&

@@ -483,7 +483,10 @@ def test_conv_bwd_pool_small(seed, B, n, depth, K, cin, cout, relu, masked):
     y[::3] = 0.0
     wg, dyg, yg = _cuda(w), _cuda(dy), _cuda(y)
     xp = p if masked else None
-    dxf = oc.oc_conv_bwd_pool(tree, l, K, wg, dyg, sw, xp=xp, y=yg, relu=relu)
+    dym = torch.full_like(dyg, float("nan")) if relu else None
+    dxf = oc.oc_conv_bwd_pool(tree, l, K, wg, dyg, sw, xp=xp, y=yg, relu=relu, dym=dym)
+    if relu:  # the masked upstream gradient handed out for the weight gradient
+        np.testing.assert_array_equal(dym.cpu().numpy(), np.where(y > 0, dy, np.float32(0)))
     dx, _ = oc.oc_conv_bwd(tree, l, K, 1, p, wg, dyg, y=yg, relu=relu, need_dx=True,
                            need_dw=False)
     dxu = oc.oc_pool_bwd(tree, lf, dx, sw, y=xp)
