@@ -584,22 +584,41 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
 }
 
 // dyg[g] = dy[rows[g]], zero where ym[rows[g]] <= 0 (ym null: no mask); T =
-// bf16 rounds to nearest even.  One element per thread.
-template <typename T>
+// bf16 rounds to nearest even.  V elements per thread (V = 4: cout % 4 == 0
+// and 16-byte aligned dy, ym, dyg).
+template <typename T, int V>
 __global__ __launch_bounds__(TB) void k_sr_dyg(const int32_t* __restrict__ rows, int64_t ng,
                                                const float* __restrict__ dy,
                                                const float* __restrict__ ym, int cout,
                                                T* __restrict__ dyg) {
+  const int cv = cout / V;
   const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
-  if (t >= ng * cout) return;
-  const int64_t g = t / cout;
-  const int c = (int)(t - g * cout);
+  if (t >= ng * cv) return;
+  const int64_t g = t / cv;
+  const int c = (int)(t - g * cv) * V;
   const int64_t src = (int64_t)rows[g] * cout + c;
-  const float v = (ym && !(ym[src] > 0.f)) ? 0.f : dy[src];
-  if constexpr (sizeof(T) == 2)
-    dyg[t] = bf16_rne(v);
-  else
-    dyg[t] = v;
+  float v[V];
+  if constexpr (V == 4) {
+    const v4f a = *reinterpret_cast<const v4f*>(dy + src);
+    v4f m = {1.f, 1.f, 1.f, 1.f};
+    if (ym) m = *reinterpret_cast<const v4f*>(ym + src);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = m[e] > 0.f ? a[e] : 0.f;
+  } else {
+    v[0] = (ym && !(ym[src] > 0.f)) ? 0.f : dy[src];
+  }
+  T* o = dyg + g * cout + c;
+  if constexpr (sizeof(T) == 2 && V == 4) {
+    *reinterpret_cast<uint2*>(o) =
+        uint2{bf16_rne(v[0]) | ((uint32_t)bf16_rne(v[1]) << 16),
+              bf16_rne(v[2]) | ((uint32_t)bf16_rne(v[3]) << 16)};
+  } else if constexpr (sizeof(T) == 2) {
+    o[0] = bf16_rne(v[0]);
+  } else if constexpr (V == 4) {
+    *reinterpret_cast<v4f*>(o) = v4f{v[0], v[1], v[2], v[3]};
+  } else {
+    o[0] = v[0];
+  }
 }
 
 // wt[k][n][c] = w[k][c][n] (27 taps).
@@ -620,6 +639,13 @@ __global__ __launch_bounds__(TB) void k_sr_zero_empty(const int32_t* __restrict_
   const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
   if (t >= n * c) return;
   if (labels[t / c] == 0) y[t] = 0.f;
+}
+// The same four channels per thread (c % 4 == 0, y 16-byte aligned).
+__global__ __launch_bounds__(TB) void k_sr_zero_empty4(const int32_t* __restrict__ labels,
+                                                       int64_t n, int cv, float* __restrict__ y) {
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= n * cv) return;
+  if (labels[t / cv] == 0) reinterpret_cast<v4f*>(y)[t] = v4f{0.f, 0.f, 0.f, 0.f};
 }
 
 inline unsigned grid_for(int64_t n) { return (unsigned)oc::cdiv(n, TB); }
@@ -756,8 +782,12 @@ oc_status conv_s2_fwd(const oc_octree* t, int l, int r, const void* x, int cin, 
   else
     launch(k_sr_wt<float>, dim3(grid_for(nw)), dim3(TB), 0, s, (const float*)w, cin, cout,
            (float*)wt);
-  launch(k_sr_zero_empty, dim3(grid_for(h.n_out * cout)), dim3(TB), 0, s,
-         (const int32_t*)t->labels[l - r], h.n_out, cout, y);
+  if (cout % 4 == 0 && (uintptr_t)y % 16 == 0)
+    launch(k_sr_zero_empty4, dim3(grid_for(h.n_out * (cout / 4))), dim3(TB), 0, s,
+           (const int32_t*)t->labels[l - r], h.n_out, cout / 4, y);
+  else
+    launch(k_sr_zero_empty, dim3(grid_for(h.n_out * cout)), dim3(TB), 0, s,
+           (const int32_t*)t->labels[l - r], h.n_out, cout, y);
   MmArgs a{x, (int64_t)h.n_in * cin * (int64_t)es, wt, nw * (int64_t)es, y, tab,
            t->rows[l - r], h.G, cin, cout, relu,
            (int)(vec_ok(cin, es, x, wt) && (uintptr_t)y % 16 == 0)};
@@ -789,12 +819,19 @@ oc_status conv_s2_bwd(const oc_octree* t, int l, int r, const void* x, int cin, 
   p += align256((size_t)h.G * cout * es);
   float* part = (float*)p;
   const int32_t* prow = t->rows[l - r];
-  if (bf16)
-    launch(k_sr_dyg<uint16_t>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow, h.G, dy, ym,
+  const bool v4 = cout % 4 == 0 && (uintptr_t)dy % 16 == 0 && (!ym || (uintptr_t)ym % 16 == 0);
+  if (bf16 && v4)
+    launch(k_sr_dyg<uint16_t, 4>, dim3(grid_for(h.G * (cout / 4))), dim3(TB), 0, s, prow, h.G, dy,
+           ym, cout, (uint16_t*)dyg);
+  else if (bf16)
+    launch(k_sr_dyg<uint16_t, 1>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow, h.G, dy, ym,
            cout, (uint16_t*)dyg);
+  else if (v4)
+    launch(k_sr_dyg<float, 4>, dim3(grid_for(h.G * (cout / 4))), dim3(TB), 0, s, prow, h.G, dy,
+           ym, cout, (float*)dyg);
   else
-    launch(k_sr_dyg<float>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow, h.G, dy, ym, cout,
-           (float*)dyg);
+    launch(k_sr_dyg<float, 1>, dim3(grid_for(h.G * cout)), dim3(TB), 0, s, prow, h.G, dy, ym,
+           cout, (float*)dyg);
   if (dw || (dx && r > 1)) build_table(t, l, r, tab, s);
   if (dx) {
     // dx = sum of dyg W^T: reduction over the output channels, N = cin
