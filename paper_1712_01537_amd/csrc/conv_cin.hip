@@ -471,11 +471,12 @@ int64_t workgroups(int64_t G, int slots_per_cu, int ncb) {
   return 8 * oc::cdiv(n, 8);
 }
 
-// The weight gradient keeps at most two workgroups per CU: each one writes a
-// partial sum of every entry, so fewer, longer ranges mean less to add.
+// The weight gradient keeps at most three workgroups per CU (as many as its
+// LDS allows): each one writes a partial sum of every entry (27 Cin Cout
+// floats), so more would add little latency hiding for more to add.
 template <int CIN>
 int64_t dw_workgroups(int64_t G, int cout) {
-  static const int occ = std::min(2, occupancy(k_cin_dw<CIN>));
+  static const int occ = std::min(3, occupancy(k_cin_dw<CIN>));
   return workgroups(G, occ, cout / 16);
 }
 
