@@ -236,6 +236,75 @@ __global__ __launch_bounds__(TB) void k_gpool_fwd(const int32_t* __restrict__ nb
   reinterpret_cast<F*>(y)[t] = acc;
 }
 
+// Average pooling, stride 1, as separable box sums over each sibling group's
+// union block: the (2R+1)^3 neighbourhoods of the group's eight children
+// tile the (2R+2)^3 block of positions around the group (Fig. 4), so their
+// sums are the block's window sums along z (per (x, y) line), then along y,
+// then along x, about a third of the additions and a fifth of the row reads
+// of summing each child's neighbourhood.  Absent positions are zero (the
+// zero-padded average, reading 16), and the sum is divided by (2R+1)^3.
+// Thread (group g, channel quad q) writes rows 8g .. 8g+7.  The additions
+// run in a fixed order, so results are reproducible.
+template <int R>
+__global__ __launch_bounds__(TB) void k_gpool_avg_sep(const int32_t* __restrict__ nbr,
+                                                      int64_t ngroups,
+                                                      const float* __restrict__ x, int cv,
+                                                      float* __restrict__ y) {
+  constexpr int K = 2 * R + 1, S = K + 1, K3 = K * K * K;
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= ngroups * cv) return;
+  const int64_t g = t / cv;
+  const int q = (int)(t - g * cv);
+  const float4* xv = reinterpret_cast<const float4*>(x);
+  int32_t nb[27];
+#pragma unroll
+  for (int c = 0; c < 27; ++c) nb[c] = nbr[27 * g + c];
+  auto at = [&](int ix, int iy, int iz) -> float4 {  // block position (ix, iy, iz)
+    const int ux = ix - R, uy = iy - R, uz = iz - R;
+    const int32_t b = nb[((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1)];
+    if (b < 0) return make_float4(0.f, 0.f, 0.f, 0.f);
+    return xv[((int64_t)b + 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1)) * cv + q];
+  };
+  auto add = [](float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); };
+  float4 o[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) o[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 1
+  for (int ix = 0; ix < S; ++ix) {
+    float4 z[S][2];  // window sums along z of each y line, for cz = 0, 1
+#pragma unroll
+    for (int iy = 0; iy < S; ++iy) {
+      float4 b[S];
+#pragma unroll
+      for (int iz = 0; iz < S; ++iz) b[iz] = at(ix, iy, iz);
+      float4 m = b[1];
+#pragma unroll
+      for (int iz = 2; iz < K; ++iz) m = add(m, b[iz]);
+      z[iy][0] = add(b[0], m);
+      z[iy][1] = add(m, b[K]);
+    }
+#pragma unroll
+    for (int cy = 0; cy < 2; ++cy)
+#pragma unroll
+      for (int cz = 0; cz < 2; ++cz) {
+        float4 w = z[cy][cz];
+#pragma unroll
+        for (int dy = 1; dy < K; ++dy) w = add(w, z[cy + dy][cz]);
+        // this x-slab is in the x-window of child cx = 0 when ix < K, of
+        // cx = 1 when ix >= 1
+        if (ix < K) o[2 * cy + cz] = add(o[2 * cy + cz], w);
+        if (ix >= 1) o[4 + 2 * cy + cz] = add(o[4 + 2 * cy + cz], w);
+      }
+  }
+  float4* yv = reinterpret_cast<float4*>(y);
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    const float4 v = o[c];
+    yv[(8 * g + c) * cv + q] = make_float4(v.x / (float)K3, v.y / (float)K3, v.z / (float)K3,
+                                           v.w / (float)K3);
+  }
+}
+
 // Backward of the max as a gather, in tap order: input row n receives, from
 // the octant i whose tap k lands on n (i is n's neighbour at the mirrored
 // offset, tap K^3 - 1 - k), dy[i] where sw[i] == k.  (The average's
@@ -508,6 +577,16 @@ oc_status gpool(const oc_octree* t, int32_t l, int32_t K, int32_t stride, int32_
   // neighbour relation is symmetric (n sees i at offset d iff i sees n at
   // -d), so both are dy summed over n's neighbourhood / K^3.  It runs on the
   // forward kernel, whose taps are batched (the same sum, divided once).
+  if (avg && v4 && (K == 3 || K == 5)) {  // separable sums over each group's union block
+    const int64_t G = t->M[l - 1];
+    const dim3 gg(grid_for(G * cv));
+    if (K == 3)
+      oc::launch_main(k_gpool_avg_sep<1>, gg, dim3(TB), s, nbr, G, in, cv, out);
+    else
+      oc::launch_main(k_gpool_avg_sep<2>, gg, dim3(TB), s, nbr, G, in, cv, out);
+    OC_LAUNCH_CHECK();
+    return OC_OK;
+  }
 #define OC_GP(R_, AVG_, V_)                                                                   \
   if (K == 2 * R_ + 1 && avg == AVG_ && (v4 ? 4 : 1) == V_) {                                 \
     if constexpr (BWD) {                                                                      \
