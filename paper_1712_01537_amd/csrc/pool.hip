@@ -305,6 +305,175 @@ __global__ __launch_bounds__(TB) void k_gpool_avg_sep(const int32_t* __restrict_
   }
 }
 
+// Max pooling, stride 1, the same way: window maxima of each group's union
+// block along z, then y, then x.  Each stage keeps its first candidate and
+// replaces it only by a strictly greater value, so the winner is the first
+// maximum in the order (dx, dy, dz), which is the tap order k = (dx K + dy)
+// K + dz of the one-tap-at-a-time scan: the switch is k, or 255 when the
+// winning position is absent (absent positions take part as zeros).
+// Thread (group g, channel quad q).  For finite inputs (a NaN first in a
+// window would hide the rest of that window).
+template <int R>
+__global__ __launch_bounds__(TB) void k_gpool_max_sep(const int32_t* __restrict__ nbr,
+                                                      int64_t ngroups,
+                                                      const float* __restrict__ x, int cv,
+                                                      float* __restrict__ y,
+                                                      uint8_t* __restrict__ sw) {
+  constexpr int K = 2 * R + 1, S = K + 1;
+  constexpr int ABSENT = 256;  // flag on a candidate's code: the position is absent
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= ngroups * cv) return;
+  const int64_t g = t / cv;
+  const int q = (int)(t - g * cv);
+  const float4* xv = reinterpret_cast<const float4*>(x);
+  int32_t nb[27];
+#pragma unroll
+  for (int c = 0; c < 27; ++c) nb[c] = nbr[27 * g + c];
+  // candidate: four channel values and their codes (partial tap index | ABSENT)
+  struct Cand {
+    float v[4];
+    int k[4];
+  };
+  auto better = [](Cand& m, const Cand& c, int add) {  // strictly greater replaces
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (c.v[e] > m.v[e]) m.v[e] = c.v[e], m.k[e] = c.k[e] + add;
+  };
+  auto shifted = [](const Cand& c, int add) {
+    Cand r = c;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r.k[e] += add;
+    return r;
+  };
+  Cand o[8];
+#pragma unroll 1
+  for (int ix = 0; ix < S; ++ix) {
+    Cand z[S][2];  // per y line: the z-window maxima for cz = 0, 1 (code dz)
+#pragma unroll
+    for (int iy = 0; iy < S; ++iy) {
+      Cand b[S];
+#pragma unroll
+      for (int iz = 0; iz < S; ++iz) {
+        const int ux = ix - R, uy = iy - R, uz = iz - R;
+        const int32_t base = nb[((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1)];
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        int code = ABSENT;
+        if (base >= 0) {
+          v = xv[((int64_t)base + 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1)) * cv + q];
+          code = 0;
+        }
+        b[iz].v[0] = v.x, b[iz].v[1] = v.y, b[iz].v[2] = v.z, b[iz].v[3] = v.w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) b[iz].k[e] = code;
+      }
+#pragma unroll
+      for (int cz = 0; cz < 2; ++cz) {
+        Cand m = b[cz];
+#pragma unroll
+        for (int dz = 1; dz < K; ++dz) better(m, b[cz + dz], dz);
+        z[iy][cz] = m;
+      }
+    }
+#pragma unroll
+    for (int cy = 0; cy < 2; ++cy)
+#pragma unroll
+      for (int cz = 0; cz < 2; ++cz) {
+        Cand m = z[cy][cz];
+#pragma unroll
+        for (int dy = 1; dy < K; ++dy) better(m, z[cy + dy][cz], K * dy);
+        // the x-windows of child cx take this slab at dx = ix - cx
+        const int c0 = 2 * cy + cz, c1 = 4 + 2 * cy + cz;
+        if (ix == 0) o[c0] = m;
+        else if (ix < K) better(o[c0], m, K * K * ix);
+        if (ix == 1) o[c1] = m;
+        else if (ix > 1) better(o[c1], m, K * K * (ix - 1));
+      }
+  }
+  float4* yv = reinterpret_cast<float4*>(y);
+  uint32_t* sv = reinterpret_cast<uint32_t*>(sw);
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    const int64_t r = (8 * g + c) * cv + q;
+    yv[r] = make_float4(o[c].v[0], o[c].v[1], o[c].v[2], o[c].v[3]);
+    uint32_t packed = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t k = o[c].k[e] >= ABSENT ? 255u : (uint32_t)o[c].k[e];
+      packed |= k << (8 * e);
+    }
+    sv[r] = packed;
+  }
+}
+
+// Backward of the max by sibling group: the outputs whose taps can land on
+// a group's eight rows are the positions of its union block (child c takes,
+// for tap k = (dx, dy, dz), the output at block position c + 2R - d), so
+// thread (group g, channel quad q) reads each block position's dy and
+// switches once, an x-slab at a time, and adds to row 8g + c the dy of every
+// position whose switch names the tap that lands on c.  The additions run
+// in a fixed order (x-slab, then child, then tap).
+template <int R>
+__global__ __launch_bounds__(TB) void k_gpool_max_bwd_sep(const int32_t* __restrict__ nbr,
+                                                          int64_t ngroups,
+                                                          const float* __restrict__ dy,
+                                                          const uint8_t* __restrict__ sw, int cv,
+                                                          float* __restrict__ dx) {
+  constexpr int K = 2 * R + 1, S = K + 1;
+  const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
+  if (t >= ngroups * cv) return;
+  const int64_t g = t / cv;
+  const int q = (int)(t - g * cv);
+  const float4* dv = reinterpret_cast<const float4*>(dy);
+  const uint32_t* sv = reinterpret_cast<const uint32_t*>(sw);
+  int32_t nb[27];
+#pragma unroll
+  for (int c = 0; c < 27; ++c) nb[c] = nbr[27 * g + c];
+  float4 acc[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 1
+  for (int ix = 0; ix < S; ++ix) {
+    float4 d[S][S];
+    uint32_t w[S][S];  // switches; 0xffffffff for an absent position (matches no tap)
+#pragma unroll
+    for (int iy = 0; iy < S; ++iy)
+#pragma unroll
+      for (int iz = 0; iz < S; ++iz) {
+        const int ux = ix - R, uy = iy - R, uz = iz - R;
+        const int32_t base = nb[((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1)];
+        d[iy][iz] = make_float4(0.f, 0.f, 0.f, 0.f);
+        w[iy][iz] = 0xffffffffu;
+        if (base >= 0) {
+          const int64_t r = ((int64_t)base + 4 * (ux & 1) + 2 * (uy & 1) + (uz & 1)) * cv + q;
+          d[iy][iz] = dv[r];
+          w[iy][iz] = sv[r];
+        }
+      }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int cx = c >> 2, cy = (c >> 1) & 1, cz = c & 1;
+      const int ddx = cx + 2 * R - ix;  // the tap's x index that lands on c from this slab
+      if (ddx < 0 || ddx >= K) continue;
+#pragma unroll
+      for (int ddy = 0; ddy < K; ++ddy)
+#pragma unroll
+        for (int ddz = 0; ddz < K; ++ddz) {
+          const int py = cy + 2 * R - ddy, pz = cz + 2 * R - ddz;
+          const uint32_t k = (uint32_t)((ddx * K + ddy) * K + ddz);
+          const uint32_t sw4 = w[py][pz];
+          const float4 v = d[py][pz];
+          if ((sw4 & 0xffu) == k) acc[c].x += v.x;
+          if (((sw4 >> 8) & 0xffu) == k) acc[c].y += v.y;
+          if (((sw4 >> 16) & 0xffu) == k) acc[c].z += v.z;
+          if ((sw4 >> 24) == k) acc[c].w += v.w;
+        }
+    }
+  }
+  float4* xv = reinterpret_cast<float4*>(dx);
+#pragma unroll
+  for (int c = 0; c < 8; ++c) xv[(8 * g + c) * cv + q] = acc[c];
+}
+
 // Backward of the max as a gather, in tap order: input row n receives, from
 // the octant i whose tap k lands on n (i is n's neighbour at the mirrored
 // offset, tap K^3 - 1 - k), dy[i] where sw[i] == k.  (The average's
@@ -577,6 +746,23 @@ oc_status gpool(const oc_octree* t, int32_t l, int32_t K, int32_t stride, int32_
   // neighbour relation is symmetric (n sees i at offset d iff i sees n at
   // -d), so both are dy summed over n's neighbourhood / K^3.  It runs on the
   // forward kernel, whose taps are batched (the same sum, divided once).
+  if (BWD && !avg && v4 && K == 3) {  // the max's backward by sibling group
+    const int64_t G = t->M[l - 1];
+    oc::launch_main(k_gpool_max_bwd_sep<1>, dim3(grid_for(G * cv)), dim3(TB), s, nbr, G, in, swin,
+                    cv, out);
+    OC_LAUNCH_CHECK();
+    return OC_OK;
+  }
+  if (!BWD && !avg && v4 && (K == 3 || K == 5)) {  // separable maxima over each group's union block
+    const int64_t G = t->M[l - 1];
+    const dim3 gg(grid_for(G * cv));
+    if (K == 3)
+      oc::launch_main(k_gpool_max_sep<1>, gg, dim3(TB), s, nbr, G, in, cv, out, swout);
+    else
+      oc::launch_main(k_gpool_max_sep<2>, gg, dim3(TB), s, nbr, G, in, cv, out, swout);
+    OC_LAUNCH_CHECK();
+    return OC_OK;
+  }
   if (avg && v4 && (K == 3 || K == 5)) {  // separable sums over each group's union block
     const int64_t G = t->M[l - 1];
     const dim3 gg(grid_for(G * cv));
