@@ -210,7 +210,7 @@ const char* oc_conv_kernel(const oc_octree* t, int32_t l, int32_t K, int32_t str
   if (check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_kernel") != OC_OK) return name;
   if (pass == 3 && !pool_fused(t, l, sh, dt, cin, cout)) pass = 0;  // conv, then the pooling
   if (bf16_native(sh, dt, cin, cout)) {
-    oc::conv_bf16_kernel_name(K, cin, cout, pass, name, sizeof(name));
+    oc::conv_bf16_kernel_name(K, cin, cout, pass, t->N[l], name, sizeof(name));
   } else if (stride == 1) {  // other bf16 shapes run the fp32 kernels on widened operands
     oc::conv_s1_kernel_name(t, l, K, cin, cout, pass, name, sizeof(name));
   } else {

@@ -12,8 +12,10 @@ bool conv_bf16_supported(int K, int cin, int cout);
 
 // Name of the main kernel of pass 0 (forward), 1 (input gradient) or 2
 // (weight gradient); for more than 64 reduction channels the first of the
-// launches, one per 64 channels.
-void conv_bf16_kernel_name(int K, int cin, int cout, int pass, char* buf, size_t n);
+// launches, one per 64 channels.  rows: the octants of the layer's depth
+// (the 16-group forward tiles need its input to span less than 2 GiB).
+void conv_bf16_kernel_name(int K, int cin, int cout, int pass, int64_t rows, char* buf,
+                           size_t n);
 
 // Workspace bytes of a forward call: the weights in MFMA order.
 size_t conv_bf16_fwd_ws(int K, int cin, int cout);

@@ -75,6 +75,26 @@ __device__ __forceinline__ void lds_load16(const void* src, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(src)
                : "memory", "m0");
 }
+// Buffer resource over `bytes` bytes at p (raw: offsets in bytes, no stride);
+// loads at offsets past `bytes` return zeros.
+typedef int32_t sv4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ sv4 buf_rsrc(const void* p, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)p;
+  sv4 r;
+  r[0] = (int32_t)(uint32_t)a;
+  r[1] = (int32_t)((a >> 32) & 0xffffu);
+  r[2] = (int32_t)bytes;
+  r[3] = 0x00020000;
+  return r;
+}
+// The same direct load through a buffer resource: lane i's 16 bytes at byte
+// offset off of the resource land at lds + 16 i; an offset past the end
+// stores zeros.
+__device__ __forceinline__ void lds_bload16(sv4 rsrc, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds), "v"(off),
+               "s"(rsrc)
+               : "memory", "m0");
+}
 // The same for 4 bytes per lane (lane i's dword lands at lds + 4 i).
 __device__ __forceinline__ void lds_load4(const void* src, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(lds), "v"(src)
@@ -496,39 +516,59 @@ __global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nb
   static_assert(B::NSL <= 12 && NI <= 40, "replay arrays");
   __shared__ __attribute__((aligned(16))) v4u lds[B::NV];
   __shared__ __attribute__((aligned(16))) v4u trash[64];  // destination of padding loads
-  __shared__ int32_t nbs[GT * 27];  // neighbour rows of the tile's groups
+  // neighbour rows of the tile's groups, then 27 entries of -1 (the entries
+  // that DMA lanes past a slab look up)
+  __shared__ int32_t nbs[GT * 27 + 27];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int li = lane & 15, q = lane >> 4;
   const int64_t g0 = (int64_t)blockIdx.x * GT;
   const int n0 = blockIdx.y * 64;
-  const int KO = kk >> 3;  // channel octets of the reduction
-  const int ob = 8 * chunk;
-  if (tid < GT * 27) nbs[tid] = g0 + tid / 27 < ngroups ? nbr[27 * g0 + tid] : -1;
+    const int ob = 8 * chunk;
+  if (tid < GT * 27 + 27)
+    nbs[tid] = tid < GT * 27 && g0 + tid / 27 < ngroups ? nbr[27 * g0 + tid] : -1;
+
+  // DMA instruction i of a slab covers 16 positions x 4 pieces.  What a lane
+  // loads depends on the slab (half h, x-position j) only through the x-cell
+  // and x-bit of j, its parity and h, so the rest is worked out once per
+  // tile: nbi[k] = the lane's neighbour entry without the x-cell, eb[k] =
+  // the byte offset in the row block of its child's y, z bits and of its
+  // 16-byte piece before the slab's swizzle.  The piece is
+  // ((s & 3) ^ (py & 1)) ^ 2 (j & 1) of octet block ob + 4h (the launcher
+  // guarantees every such octet exists), and an absent row reads zeros
+  // through an offset past the end of x.
+  const sv4 xr = buf_rsrc(x, (uint32_t)(8 * ngroups * kk * 2));
+  int nbi[DC];
+  uint32_t eb[DC];
+#pragma unroll
+  for (int k = 0; k < DC; ++k) {
+    const int i = wave + NW * k;
+    const int s = i * 64 + lane;
+    const int pos = s >> 2, g = pos / S2, p = pos - g * S2;
+    const int py = p / S, pz = p - py * S;
+    const int uy = py - R, uz = pz - R;
+    nbi[k] = i < NDMA ? 27 * g + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1) : GT * 27;
+    eb[k] = 2u * (uint32_t)((2 * (uy & 1) + (uz & 1)) * kk + 8 * (ob + ((s & 3) ^ (py & 1))));
+  }
   __syncthreads();
 
-  // slab sl (half h = sl / S, x-position j = sl % S) into buffer sl % NB;
-  // DMA instruction i covers 16 positions x 4 pieces
+  // slab sl (half h = sl / S, x-position j = sl % S) into buffer sl % NB
   auto stage = [&](int sl) {
     const int h = sl / S, j = sl - h * S;
+    const int ux = j - R, xcell = (ux >> 1) + 1;
     v4u* buf = lds + (sl % NB) * SLAB;
-    // an opaque copy of the lane index: the position arithmetic below is the
-    // same for every slab, and hoisting it out of the unrolled item sequence
-    // would hold its values in registers through the whole tile
-    int ln;
-    asm volatile("" : "=v"(ln) : "0"(lane));
+    // the slab's constant (the child's x bit and the half) and swizzle term
+    const uint32_t cb = 2u * (uint32_t)(4 * (ux & 1) * kk + 32 * h), xo = 32u * (uint32_t)(j & 1);
+    int32_t b[DC];
+#pragma unroll
+    for (int k = 0; k < DC; ++k) b[k] = nbs[nbi[k] + 9 * xcell];
 #pragma unroll
     for (int k = 0; k < DC; ++k) {
       const int i = wave + NW * k;
-      const int s = i * 64 + ln;
-      const int pos = s >> 2, g = pos / S2, p = pos - g * S2;
-      const int py = p / S, pz = p - py * S;
-      const int o = ob + 4 * h + ((s & 3) ^ (2 * (j & 1) + (py & 1)));
-      const int32_t row = i < NDMA && o < KO ? tile_row<R>(nbs + 27 * g, j, py, pz) : -1;
-      const void* src = row >= 0 ? (const void*)(x + (int64_t)row * kk + 8 * o)
-                                 : (const void*)g_zero_rows[(s + 64 * (int)blockIdx.x) & (ZROWS - 1)];
-      lds_load16(src, lds_addr(i < NDMA ? buf + i * 64 : trash));
+      const uint32_t off =
+          b[k] < 0 ? 0x80000000u : (uint32_t)b[k] * (uint32_t)(2 * kk) + ((eb[k] ^ xo) + cb);
+      lds_bload16(xr, off, lds_addr(i < NDMA ? buf + i * 64 : trash));
     }
   };
 
@@ -945,13 +985,15 @@ void wprep(const uint16_t* w, int K, int kk, int nn, int flip, uint16_t* wp, hip
 // of the 8-group kernel.  Its weight loads have no per-lane masks, so every
 // chunk must hold whole 32-channel halves and the columns whole blocks of 64;
 // K = 3 keeps the 8-group kernel.
-bool wide_tiles(int K, int kk, int nn) { return K == 5 && kk % 32 == 0 && nn % 64 == 0; }
+bool wide_tiles(int K, int kk, int nn, int64_t rows) {
+  return K == 5 && kk % 32 == 0 && nn % 64 == 0 && rows * kk * 2 < ((int64_t)1 << 31);
+}
 
 template <int K, int HC, bool FLIP>
 void launch_chunk(const oc_octree* t, int l, const uint16_t* x, int kk, const uint16_t* wp, int nn,
                   int chunk, float* out, int acc_in, int relu, bool main, hipStream_t s) {
   const int64_t G = t->M[l - 1];
-  const bool wide = wide_tiles(K, kk, nn);
+  const bool wide = wide_tiles(K, kk, nn, 8 * G);
   const dim3 grid(blocks(G, wide ? 16 : 8), blocks(nn, 64));
   auto kern = k_conv_bf<K, HC, FLIP>;
   if constexpr (K == 5) {
@@ -996,12 +1038,14 @@ bool conv_bf16_supported(int K, int cin, int cout) {
   return (K == 3 || K == 5) && cin % 16 == 0 && cout % 16 == 0;
 }
 
-void conv_bf16_kernel_name(int K, int cin, int cout, int pass, char* buf, size_t n) {
+void conv_bf16_kernel_name(int K, int cin, int cout, int pass, int64_t rows, char* buf,
+                           size_t n) {
   const int kk = pass == 1 ? cout : cin;  // reduction channels of the first chunk
   if (pass == 2)
     snprintf(buf, n, "k_conv_bf_dw<%d, 5>", K);
   else
-    snprintf(buf, n, "%s<%d, %d, %s>", wide_tiles(K, kk, pass == 1 ? cin : cout) ? "k_conv_bfw" : "k_conv_bf", K,
+    snprintf(buf, n, "%s<%d, %d, %s>",
+             wide_tiles(K, kk, pass == 1 ? cin : cout, rows) ? "k_conv_bfw" : "k_conv_bf", K,
              kk > 32 ? 2 : 1, pass == 1 ? "true" : "false");
 }
 
