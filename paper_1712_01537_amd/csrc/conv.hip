@@ -128,8 +128,11 @@ size_t w32_bytes(const ConvShape& sh, int cin, int cout) {
 }
 
 // bf16 stride-1 calls whose channel counts the bf16 matrix-core kernels take
+// The bf16 kernels address x and dy through 32-bit byte offsets: layers whose
+// rows span 2 GiB or more run the fp32 kernels on widened operands instead.
 bool bf16_native(const ConvShape& sh, oc_dtype dt, int cin, int cout) {
-  return dt == OC_BF16 && sh.stride == 1 && oc::conv_bf16_supported(sh.K, cin, cout);
+  return dt == OC_BF16 && sh.stride == 1 && oc::conv_bf16_supported(sh.K, cin, cout) &&
+         sh.n_in * std::max(cin, cout) * 2 < ((int64_t)1 << 31);
 }
 
 size_t fwd_ws_bytes(const oc_octree* t, int32_t l, const ConvShape& sh, oc_dtype dt, int cin,

@@ -780,16 +780,22 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   // instructions, those past the stage load zeros into the trash slot.
   // What a lane loads depends on the step only through the neighbour rows
   // and the step's first group, so the rest is worked out once: for an x
-  // instruction k, ta = the lane's neighbour entry (27 g + parent cell) and
-  // tb = its element offset in the row block (child offset * cin + channel;
-  // -1 past cin); for a dY instruction, ta = the lane's group of the step and
-  // tb = row * cout + column (-1 past cout).
-  int ta[DC], tb[DC];
+  // instruction k, ta = the lane's neighbour entry (27 g + parent cell; past
+  // cin an entry that holds -1) and tb = its byte offset in the row block
+  // (child offset * cin + channel); for a dY instruction, ta = the lane's
+  // group of the step (GS past cout and for padding instructions) and tb =
+  // the byte offset of (row, column) in the step's rows.  Loads go through
+  // buffer resources over x and dY, absent rows to an offset past the end
+  // (zeros).
+  const sv4 xr = buf_rsrc(x, (uint32_t)(8 * ngroups * cin * 2));
+  const sv4 dr = buf_rsrc(dy, (uint32_t)(8 * ngroups * cout * 2));
+  int ta[DC];
+  uint32_t tb[DC];
 #pragma unroll
   for (int k = 0; k < DC; ++k) {
     const int i = wave + NW * k;
-    ta[k] = 0;
-    tb[k] = -1;
+    ta[k] = GS;
+    tb[k] = 0;
     if (i < npos) {
       const int s = i * 64 + lane;
       const int pos = s >> 3, g = pos / npos, p = pos - g * npos;
@@ -797,25 +803,27 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
       const int ux = x0 + ix - R, uy = y0 + iy - R, uz = iz - R;
       const int o = (s & 7) ^ (2 * (((iz + 2 * iy) & 3) ^ (g & 1)));
       const int ch = c0 + 8 * o;
-      ta[k] = 27 * g + ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1);
-      if (ch < cin) tb[k] = (4 * (ux & 1) + 2 * (uy & 1) + (uz & 1)) * cin + ch;
+      ta[k] = ch < cin ? 27 * g + ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1)
+                       : GS * 27;
+      tb[k] = 2u * (uint32_t)((4 * (ux & 1) + 2 * (uy & 1) + (uz & 1)) * cin + (ch < cin ? ch : 0));
     } else if (i < npos + GS) {
       const int s = (i - npos) * 64 + lane;
       const int rl = s >> 3;
       const int o = (s & 7) ^ (2 * ((rl & 3) ^ ((rl >> 3) & 1)));
       const int co = n0 + 8 * o;
-      ta[k] = rl >> 3;
-      if (co < cout) tb[k] = rl * cout + co;
+      ta[k] = co < cout ? rl >> 3 : GS;
+      tb[k] = 2u * (uint32_t)(rl * cout + (co < cout ? co : 0));
     }
   }
-  // Source addresses of stage st's instructions, from the neighbour rows in
+  // Source offsets of stage st's instructions, from the neighbour rows in
   // slot st % NSLOT (read in one batch, one LDS round trip); formed while the
   // matrix work of an earlier step runs and kept in registers until
   // stage_issue.
-  auto stage_src = [&](int st, const void* (&src)[DC]) {
+  auto stage_src = [&](int st, uint32_t (&src)[DC]) {
     const int64_t gs = gbeg + GS * (int64_t)st;
-    const int64_t left = gend - gs;  // groups of the step inside the range
-    const uint16_t* dys = dy + 8 * gs * cout;
+    const int64_t lf = gend - gs;  // groups of the step inside the range
+    const int left = lf < 0 ? 0 : lf > GS ? GS : (int)lf;
+    const uint32_t db = (uint32_t)(8 * gs * cout * 2);
     const int32_t* nb = nbs[st % NSLOT];
     int32_t e[DC];
 #pragma unroll
@@ -823,21 +831,22 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
 #pragma unroll
     for (int k = 0; k < DC; ++k) {
       const int i = wave + NW * k;
-      const void* a = g_zero_rows[(lane + 64 * k + 512 * (int)blockIdx.x) & (ZROWS - 1)];
-      if (i < npos) {
-        if (e[k] >= 0 && tb[k] >= 0) a = x + (int64_t)e[k] * cin + tb[k];
-      } else if (i < npos + GS) {
-        if (ta[k] < left && tb[k] >= 0) a = dys + tb[k];
-      }
-      src[k] = a;
+      const uint32_t ox = e[k] >= 0 ? (uint32_t)e[k] * (uint32_t)(2 * cin) + tb[k] : 0x80000000u;
+      const uint32_t od = ta[k] < left ? db + tb[k] : 0x80000000u;
+      src[k] = i < npos ? ox : od;
     }
   };
-  auto stage_issue = [&](v4u* buf, const void* const (&src)[DC]) {
+  // LDS byte addresses: the stage buffers (buffer b at L0 + b BUF 16) and the
+  // padding slot
+  const uint32_t L0 = lds_addr(lds), LT = lds_addr(trash);
+  auto stage_issue = [&](uint32_t bo, const uint32_t (&src)[DC]) {  // bo: the buffer's offset
 #pragma unroll
     for (int k = 0; k < DC; ++k) {
       const int i = wave + NW * k;
-      const v4u* dst = i < npos ? buf + i * 64 : i < npos + GS ? buf + XP + (i - npos) * 64 : trash;
-      lds_load16(src[k], lds_addr(dst));
+      const uint32_t dst = i < npos        ? L0 + bo + (uint32_t)i * 1024
+                           : i < npos + GS ? L0 + bo + (uint32_t)(XP + (i - npos) * 64) * 16
+                                           : LT;
+      lds_bload16(i < npos ? xr : dr, src[k], dst);
     }
   };
   // neighbour rows of step st's groups into slot st % NSLOT: one dword DMA
@@ -878,21 +887,39 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
     const int o = 2 * nb + (tq >> 1);
     return (XP + rl * 8 + (o ^ (2 * ((rl & 3) ^ ((rl >> 3) & 1))))) * 16 + (tq & 1) * 8;
   };
+  // Byte offsets of this lane's transposing loads in a stage buffer for
+  // sub-step 0: pair mi's A loads, and dY fragment nb's first load.  A later
+  // sub-step sb adds 512 npos sb (A) or 4096 sb (dY, whose second load is
+  // 512 bytes on), uniform terms, so each load costs at most one add.
+  uint32_t pa[MAXC][2], pbq[4];
+#pragma unroll
+  for (int mi = 0; mi < MAXC; ++mi)
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) pa[mi][hh] = (uint32_t)a_off(wave + NW * mi, q, hh);
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) pbq[nb] = (uint32_t)b_off(nb, q, 0);
+
   // The step's MFMAs in the fixed order (sub-step, pair): the A operand of
   // the pair two ahead and the dY fragments of the next sub-step are read
   // before the current pair's MFMAs are issued (scheduling barriers keep the
   // order), so the LDS latency hides behind matrix work.  mid() runs after
   // the first sub-step's MFMAs.
-  auto compute = [&](const v4u* buf, auto&& mid) {
+  auto compute = [&](uint32_t bo, auto&& mid) {
     constexpr int SUBS = GS / 4, NIT = SUBS * MAXC, AD = 2;
+    const lds_char* lb = (const lds_char*)(lptr_t)lds + bo;
     auto ld_b = [&](v4u (&b)[4], int sb) {
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb)
-        b[nb] = join(lds_tr16(buf, b_off(nb, 4 * sb + q, 0)), lds_tr16(buf, b_off(nb, 4 * sb + q, 1)));
+      for (int nb = 0; nb < 4; ++nb) {
+        const lds_char* p = lb + pbq[nb] + 4096 * sb;
+        b[nb] = join(__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p),
+                     __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p + 512)));
+      }
     };
     auto ld_a = [&](int it) {
-      const int sb = it / MAXC, m = wave + NW * (it % MAXC);
-      return join(lds_tr16(buf, a_off(m, 4 * sb + q, 0)), lds_tr16(buf, a_off(m, 4 * sb + q, 1)));
+      const int sb = it / MAXC, mi = it % MAXC;
+      const lds_char* p = lb + 512 * npos * sb;
+      return join(__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p + pa[mi][0])),
+                  __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p + pa[mi][1])));
     };
     v4u bq[2][4], a[AD + 1];
     ld_b(bq[0], 0);
@@ -916,22 +943,30 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   // The addresses of stage(st+3) are formed during step st from slot
   // (st+3) % NSLOT; slot st % NSLOT is refilled at step st, after every wave
   // has formed stage(st)'s addresses (at step st-3, or before the loop).
-  const void* src[DC];
+  uint32_t src[DC];
 #pragma unroll
   for (int k = 0; k < 4; ++k) nb_dma(k);
   vm_wait0();
   lds_barrier();
+  constexpr uint32_t BB = BUF * 16;  // bytes of a stage buffer
+  static_assert(NB == 3, "the buffer offsets below cycle through three buffers");
   stage_src(0, src);
-  stage_issue(lds, src);
+  stage_issue(0, src);
   stage_src(1, src);
-  stage_issue(lds + BUF, src);
+  stage_issue(BB, src);
   stage_src(2, src);
+  // offsets of the buffers of steps st and st + 2, advanced by a select (not
+  // a multiple of st % 3, which the compiler would turn into per-address
+  // corrections)
+  uint32_t bo = 0, bo2 = 2 * BB;
   for (int st = 0; st < nsteps; ++st) {
     vm_wait_n<DC>();  // stage st and the neighbour rows of step st+3 have landed
     lds_barrier();    // ... everywhere; step st-1 is no longer read
     nb_dma(st + 4);
-    stage_issue(lds + ((st + 2) % NB) * BUF, src);
-    compute(lds + (st % NB) * BUF, [&] { stage_src(st + 3, src); });
+    stage_issue(bo2, src);
+    compute(bo, [&] { stage_src(st + 3, src); });
+    bo = __builtin_amdgcn_readfirstlane(bo == 2 * BB ? 0u : bo + BB);
+    bo2 = __builtin_amdgcn_readfirstlane(bo2 == 2 * BB ? 0u : bo2 + BB);
   }
   vm_wait0();
 
