@@ -743,7 +743,7 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   constexpr int MAXPOS = 36;                 // staged positions per group, at most
   constexpr int XP = GS * MAXPOS * 8;        // pieces of the staged x
   constexpr int YP = GS * 8 * 8;             // pieces of the staged dY rows
-  constexpr int BUF = XP + YP;
+  constexpr int BUF = XP + YP + 64;         // ... and a padding slot (loads past the stage)
   constexpr int NW = 8;                      // waves
   constexpr int NB = 3;                      // stage buffers (two steps in flight)
   constexpr int NBP = NW * 64;               // dwords of a neighbour-row slot (8 groups use 216)
@@ -751,7 +751,6 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   __shared__ __attribute__((aligned(16))) v4u lds[NB * BUF];
   constexpr int NSLOT = 4;                   // neighbour-row slots
   __shared__ __attribute__((aligned(16))) int32_t nbs[NSLOT][NBP];  // neighbour rows of a step's groups
-  __shared__ __attribute__((aligned(16))) v4u trash[64];        // destination of padding loads
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -775,39 +774,42 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   const int64_t gbeg = ngroups * range / nr, gend = ngroups * (range + 1) / nr;
   const int nsteps = (int)((gend - gbeg + GS - 1) / GS);
 
-  // Stage st: the unit's x positions (npos DMA instructions of 64 pieces),
-  // then the 64 dY rows (GS instructions); every wave issues DC
-  // instructions, those past the stage load zeros into the trash slot.
-  // What a lane loads depends on the step only through the neighbour rows
-  // and the step's first group, so the rest is worked out once: for an x
-  // instruction k, ta = the lane's neighbour entry (27 g + parent cell; past
-  // cin an entry that holds -1) and tb = its byte offset in the row block
-  // (child offset * cin + channel); for a dY instruction, ta = the lane's
-  // group of the step (GS past cout and for padding instructions) and tb =
-  // the byte offset of (row, column) in the step's rows.  Loads go through
-  // buffer resources over x and dY, absent rows to an offset past the end
-  // (zeros).
+  // Stage st: the unit's x positions, MAXPOS per group (MAXPOS DMA
+  // instructions of 64 pieces; positions past npos read zeros), then the 64
+  // dY rows (GS instructions), then the buffer's padding slot: every wave
+  // issues DC instructions, and instruction k of wave w is number i = w +
+  // NW k.  What a lane loads depends on the step only through the neighbour
+  // rows and the step's first group, so the rest is worked out once: for an x
+  // instruction, ta = the lane's neighbour entry (27 g + parent cell) and tb
+  // = its byte offset in the row block (child offset * cin + channel; 2^31,
+  // past any row, for channels past cin and positions past npos); for a dY
+  // instruction, ta = the lane's group of the step (GS past cout and for
+  // padding instructions) and tb = the byte offset of (row, column) in the
+  // step's rows.  Loads go through buffer resources over x and dY, absent
+  // rows to an offset past the end (zeros).
   const sv4 xr = buf_rsrc(x, (uint32_t)(8 * ngroups * cin * 2));
   const sv4 dr = buf_rsrc(dy, (uint32_t)(8 * ngroups * cout * 2));
   int ta[DC];
-  uint32_t tb[DC];
+  uint32_t tb[DC], dk[DC];  // dk: the instruction's byte offset in a stage buffer
 #pragma unroll
   for (int k = 0; k < DC; ++k) {
     const int i = wave + NW * k;
     ta[k] = GS;
     tb[k] = 0;
-    if (i < npos) {
+    dk[k] = i < MAXPOS ? i * 1024 : i < MAXPOS + GS ? (XP + (i - MAXPOS) * 64) * 16 : (XP + YP) * 16;
+    if (i < MAXPOS) {
       const int s = i * 64 + lane;
-      const int pos = s >> 3, g = pos / npos, p = pos - g * npos;
+      const int pos = s >> 3, g = pos / MAXPOS, p = pos - g * MAXPOS;
       const int ix = p / (NY * S), rem = p - ix * (NY * S), iy = rem / S, iz = rem - iy * S;
       const int ux = x0 + ix - R, uy = y0 + iy - R, uz = iz - R;
       const int o = (s & 7) ^ (2 * (((iz + 2 * iy) & 3) ^ (g & 1)));
       const int ch = c0 + 8 * o;
-      ta[k] = ch < cin ? 27 * g + ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1)
-                       : GS * 27;
-      tb[k] = 2u * (uint32_t)((4 * (ux & 1) + 2 * (uy & 1) + (uz & 1)) * cin + (ch < cin ? ch : 0));
-    } else if (i < npos + GS) {
-      const int s = (i - npos) * 64 + lane;
+      ta[k] = p < npos ? 27 * g + ((ux >> 1) + 1) * 9 + ((uy >> 1) + 1) * 3 + ((uz >> 1) + 1) : 0;
+      tb[k] = p < npos && ch < cin
+                  ? 2u * (uint32_t)((4 * (ux & 1) + 2 * (uy & 1) + (uz & 1)) * cin + ch)
+                  : 0x80000000u;
+    } else if (i < MAXPOS + GS) {
+      const int s = (i - MAXPOS) * 64 + lane;
       const int rl = s >> 3;
       const int o = (s & 7) ^ (2 * ((rl & 3) ^ ((rl >> 3) & 1)));
       const int co = n0 + 8 * o;
@@ -815,6 +817,10 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
       tb[k] = 2u * (uint32_t)(rl * cout + (co < cout ? co : 0));
     }
   }
+  // Instruction k of every wave stages x (XK), or of none (DK); otherwise
+  // the kind depends on the wave.
+  auto XK = [](auto kc) { return NW * decltype(kc)::value + NW - 1 < MAXPOS; };
+  auto DK = [](auto kc) { return NW * decltype(kc)::value >= MAXPOS; };
   // Source offsets of stage st's instructions, from the neighbour rows in
   // slot st % NSLOT (read in one batch, one LDS round trip); formed while the
   // matrix work of an earlier step runs and kept in registers until
@@ -826,38 +832,41 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
     const uint32_t db = (uint32_t)(8 * gs * cout * 2);
     const int32_t* nb = nbs[st % NSLOT];
     int32_t e[DC];
-#pragma unroll
-    for (int k = 0; k < DC; ++k) e[k] = nb[ta[k]];
-#pragma unroll
-    for (int k = 0; k < DC; ++k) {
-      const int i = wave + NW * k;
-      const uint32_t ox = e[k] >= 0 ? (uint32_t)e[k] * (uint32_t)(2 * cin) + tb[k] : 0x80000000u;
-      const uint32_t od = ta[k] < left ? db + tb[k] : 0x80000000u;
-      src[k] = i < npos ? ox : od;
-    }
+    static_for<DC>([&](auto kc) {
+      constexpr int k = decltype(kc)::value;
+      if constexpr (!DK(kc)) e[k] = nb[ta[k]];
+    });
+    static_for<DC>([&](auto kc) {
+      constexpr int k = decltype(kc)::value;
+      auto ox = [&] { return e[k] >= 0 ? (uint32_t)e[k] * (uint32_t)(2 * cin) + tb[k] : 0x80000000u; };
+      auto od = [&] { return ta[k] < left ? db + tb[k] : 0x80000000u; };
+      if constexpr (XK(kc))
+        src[k] = ox();
+      else if constexpr (DK(kc))
+        src[k] = od();
+      else
+        src[k] = wave + NW * k < MAXPOS ? ox() : od();
+    });
   };
-  // LDS byte addresses: the stage buffers (buffer b at L0 + b BUF 16) and the
-  // padding slot
-  const uint32_t L0 = lds_addr(lds), LT = lds_addr(trash);
+  // LDS byte address of the stage buffers (buffer b at L0 + b BUF 16)
+  const uint32_t L0 = lds_addr(lds);
   auto stage_issue = [&](uint32_t bo, const uint32_t (&src)[DC]) {  // bo: the buffer's offset
-#pragma unroll
-    for (int k = 0; k < DC; ++k) {
-      const int i = wave + NW * k;
-      const uint32_t dst = i < npos        ? L0 + bo + (uint32_t)i * 1024
-                           : i < npos + GS ? L0 + bo + (uint32_t)(XP + (i - npos) * 64) * 16
-                                           : LT;
-      lds_bload16(i < npos ? xr : dr, src[k], dst);
-    }
+    static_for<DC>([&](auto kc) {
+      constexpr int k = decltype(kc)::value;
+      const sv4 r = XK(kc) ? xr : DK(kc) ? dr : wave + NW * k < MAXPOS ? xr : dr;
+      lds_bload16(r, src[k], L0 + bo + dk[k]);
+    });
   };
   // neighbour rows of step st's groups into slot st % NSLOT: one dword DMA
-  // instruction per wave (entries past the range read -1 from the zero rows'
-  // neighbour, see below)
+  // instruction per wave; entries of groups past the range and past the
+  // step's 8 x 27 read -1
+  const uint32_t NB0 = lds_addr(&nbs[0][0]);
+  const int ne = wave * 64 + lane, neg = ne / 27;  // entry of the slot, its group
   auto nb_dma = [&](int st) {
-    const int e = wave * 64 + lane;  // entry of the slot
-    const int64_t g = gbeg + GS * (int64_t)st + e / 27;
-    const void* src = e < GS * 27 && g < gend ? (const void*)(nbr + 27 * g + e % 27)
-                                             : (const void*)&g_minus1;
-    lds_load4(src, lds_addr(&nbs[st % NSLOT][wave * 64]));
+    const int64_t gs = gbeg + GS * (int64_t)st;
+    const bool ok = ne < GS * 27 && gs + neg < gend;
+    const void* src = ok ? (const void*)(nbr + 27 * gs + ne) : (const void*)&g_minus1;
+    lds_load4(src, NB0 + (uint32_t)(((st % NSLOT) * NBP + wave * 64) * 4));
   };
 
   v4f acc[MAXC][4];
@@ -880,7 +889,7 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
     const int iy = dyl + (r4 >> 1), iz = dzi + (r4 & 1);  // child 4 hh + r4 of group gq
     const int p = ((dxl + hh) * NY + iy) * S + iz;
     const int o = 2 * cb + (tq >> 1);
-    return ((gq * npos + p) * 8 + (o ^ (2 * (((iz + 2 * iy) & 3) ^ (gq & 1))))) * 16 + (tq & 1) * 8;
+    return ((gq * MAXPOS + p) * 8 + (o ^ (2 * (((iz + 2 * iy) & 3) ^ (gq & 1))))) * 16 + (tq & 1) * 8;
   };
   auto b_off = [&](int nb, int gq, int hh) {  // byte offset of dY fragment nb, load hh
     const int rl = 8 * gq + 4 * hh + r4;
@@ -889,8 +898,8 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   };
   // Byte offsets of this lane's transposing loads in a stage buffer for
   // sub-step 0: pair mi's A loads, and dY fragment nb's first load.  A later
-  // sub-step sb adds 512 npos sb (A) or 4096 sb (dY, whose second load is
-  // 512 bytes on), uniform terms, so each load costs at most one add.
+  // sub-step sb adds 512 MAXPOS sb (A) or 4096 sb (dY, whose second load is
+  // 512 bytes on), constants that the loads take as immediate offsets.
   uint32_t pa[MAXC][2], pbq[4];
 #pragma unroll
   for (int mi = 0; mi < MAXC; ++mi)
@@ -917,7 +926,7 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
     };
     auto ld_a = [&](int it) {
       const int sb = it / MAXC, mi = it % MAXC;
-      const lds_char* p = lb + 512 * npos * sb;
+      const lds_char* p = lb + 512 * MAXPOS * sb;
       return join(__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p + pa[mi][0])),
                   __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p + pa[mi][1])));
     };
