@@ -720,34 +720,39 @@ __global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nb
 // x-offset and every y-offset.  Every unit but the last K = 5 one has
 // 10 (K = 5) or 9 (K = 3) taps and at most 36 positions.
 // Grid: x = units x ranges (a range is a contiguous run of groups), y =
-// blocks of 64 output channels, z = blocks of 64 input channels; 512
-// threads (two waves per SIMD, so that one wave's LDS waits overlap the
-// other's MFMAs).  Per step of eight groups the workgroup stages the unit's
-// positions and the 64 dY rows; x piece o of box position (ix, iy, iz) of
-// the step's group g sits at o ^ 2(((iz + 2 iy) & 3) ^ (g & 1)), dY piece o
-// of row r at o ^ 2((r & 3) ^ ((r >> 3) & 1)).  A transposing load of a
+// blocks of 64 output channels, z = blocks of 64 input channels; NW waves
+// of MAXC (tap, 16-channel block) pairs each, two waves per SIMD (one
+// wave's LDS waits overlap the other's MFMAs): K = 5 runs two workgroups of
+// four waves per compute unit on steps of GS = 4 groups (one workgroup's
+// step barrier then leaves the other's waves running), K = 3 one of eight
+// waves on steps of 8 groups.  Per step the workgroup stages the unit's
+// positions of its GS groups and their 8 GS dY rows; x piece o of box
+// position (ix, iy, iz) of the step's group g sits at
+// o ^ 2(((iz + 2 iy) & 3) ^ (g & 1)), dY piece o of row r at
+// o ^ 2((r & 3) ^ ((r >> 3) & 1)).  A transposing load of a
 // 16-lane group reads four children of one group in four distinct 32-byte
 // slots; the group-parity term moves the next 16-lane group (the next
 // group, at the same positions) onto the other four slots of each 256-byte
 // bank row, so 32 lanes read 256 distinct bytes.
 // part [nranges][K^3][cin][cout].
-template <int K, int MAXC>
-__global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ nbr,
+template <int K, int MAXC, int NW, int GS>
+__global__ __launch_bounds__(NW * 64, 8 / NW) void k_conv_bf_dw(const int32_t* __restrict__ nbr,
                                                       int64_t ngroups,
                                                       const uint16_t* __restrict__ x, int cin,
                                                       const uint16_t* __restrict__ dy, int cout,
                                                       int nranges, float* __restrict__ part) {
   constexpr int R = (K - 1) / 2, S = K + 1, K3 = K * K * K;
   constexpr int NU = K == 5 ? 13 : 3;        // units
-  constexpr int GS = 8;                      // groups per step
+  static_assert(GS % 4 == 0 && NW * MAXC >= (K == 5 ? 40 : 36), "tile");
   constexpr int MAXPOS = 36;                 // staged positions per group, at most
   constexpr int XP = GS * MAXPOS * 8;        // pieces of the staged x
   constexpr int YP = GS * 8 * 8;             // pieces of the staged dY rows
-  constexpr int BUF = XP + YP + 64;         // ... and a padding slot (loads past the stage)
-  constexpr int NW = 8;                      // waves
+  constexpr int BUF = XP + YP + 64;          // ... and a padding slot (loads past the stage)
+  constexpr int NXI = GS * MAXPOS / 8, NYI = GS;  // DMA instructions of the x positions, dY rows
   constexpr int NB = 3;                      // stage buffers (two steps in flight)
-  constexpr int NBP = NW * 64;               // dwords of a neighbour-row slot (8 groups use 216)
-  constexpr int DC = (MAXPOS + GS + NW - 1) / NW;  // DMA instructions of a stage per wave
+  constexpr int NBP = NW * 64;               // dwords of a neighbour-row slot (27 GS used)
+  static_assert(NBP >= GS * 27, "neighbour slot");
+  constexpr int DC = (NXI + NYI + NW - 1) / NW;  // DMA instructions of a stage per wave
   __shared__ __attribute__((aligned(16))) v4u lds[NB * BUF];
   constexpr int NSLOT = 4;                   // neighbour-row slots
   __shared__ __attribute__((aligned(16))) int32_t nbs[NSLOT][NBP];  // neighbour rows of a step's groups
@@ -774,9 +779,9 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   const int64_t gbeg = ngroups * range / nr, gend = ngroups * (range + 1) / nr;
   const int nsteps = (int)((gend - gbeg + GS - 1) / GS);
 
-  // Stage st: the unit's x positions, MAXPOS per group (MAXPOS DMA
-  // instructions of 64 pieces; positions past npos read zeros), then the 64
-  // dY rows (GS instructions), then the buffer's padding slot: every wave
+  // Stage st: the unit's x positions, MAXPOS per group (NXI DMA
+  // instructions of 64 pieces; positions past npos read zeros), then the
+  // 8 GS dY rows (NYI instructions), then the buffer's padding slot: every wave
   // issues DC instructions, and instruction k of wave w is number i = w +
   // NW k.  What a lane loads depends on the step only through the neighbour
   // rows and the step's first group, so the rest is worked out once: for an x
@@ -796,8 +801,8 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
     const int i = wave + NW * k;
     ta[k] = GS;
     tb[k] = 0;
-    dk[k] = i < MAXPOS ? i * 1024 : i < MAXPOS + GS ? (XP + (i - MAXPOS) * 64) * 16 : (XP + YP) * 16;
-    if (i < MAXPOS) {
+    dk[k] = i < NXI ? i * 1024 : i < NXI + NYI ? (XP + (i - NXI) * 64) * 16 : (XP + YP) * 16;
+    if (i < NXI) {
       const int s = i * 64 + lane;
       const int pos = s >> 3, g = pos / MAXPOS, p = pos - g * MAXPOS;
       const int ix = p / (NY * S), rem = p - ix * (NY * S), iy = rem / S, iz = rem - iy * S;
@@ -808,8 +813,8 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
       tb[k] = p < npos && ch < cin
                   ? 2u * (uint32_t)((4 * (ux & 1) + 2 * (uy & 1) + (uz & 1)) * cin + ch)
                   : 0x80000000u;
-    } else if (i < MAXPOS + GS) {
-      const int s = (i - MAXPOS) * 64 + lane;
+    } else if (i < NXI + NYI) {
+      const int s = (i - NXI) * 64 + lane;
       const int rl = s >> 3;
       const int o = (s & 7) ^ (2 * ((rl & 3) ^ ((rl >> 3) & 1)));
       const int co = n0 + 8 * o;
@@ -819,8 +824,8 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   }
   // Instruction k of every wave stages x (XK), or of none (DK); otherwise
   // the kind depends on the wave.
-  auto XK = [](auto kc) { return NW * decltype(kc)::value + NW - 1 < MAXPOS; };
-  auto DK = [](auto kc) { return NW * decltype(kc)::value >= MAXPOS; };
+  auto XK = [](auto kc) { return NW * decltype(kc)::value + NW - 1 < NXI; };
+  auto DK = [](auto kc) { return NW * decltype(kc)::value >= NXI; };
   // Source offsets of stage st's instructions, from the neighbour rows in
   // slot st % NSLOT (read in one batch, one LDS round trip); formed while the
   // matrix work of an earlier step runs and kept in registers until
@@ -845,7 +850,7 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
       else if constexpr (DK(kc))
         src[k] = od();
       else
-        src[k] = wave + NW * k < MAXPOS ? ox() : od();
+        src[k] = wave + NW * k < NXI ? ox() : od();
     });
   };
   // LDS byte address of the stage buffers (buffer b at L0 + b BUF 16)
@@ -853,13 +858,13 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
   auto stage_issue = [&](uint32_t bo, const uint32_t (&src)[DC]) {  // bo: the buffer's offset
     static_for<DC>([&](auto kc) {
       constexpr int k = decltype(kc)::value;
-      const sv4 r = XK(kc) ? xr : DK(kc) ? dr : wave + NW * k < MAXPOS ? xr : dr;
+      const sv4 r = XK(kc) ? xr : DK(kc) ? dr : wave + NW * k < NXI ? xr : dr;
       lds_bload16(r, src[k], L0 + bo + dk[k]);
     });
   };
   // neighbour rows of step st's groups into slot st % NSLOT: one dword DMA
   // instruction per wave; entries of groups past the range and past the
-  // step's 8 x 27 read -1
+  // step's GS x 27 read -1
   const uint32_t NB0 = lds_addr(&nbs[0][0]);
   const int ne = wave * 64 + lane, neg = ne / 27;  // entry of the slot, its group
   auto nb_dma = [&](int st) {
@@ -942,7 +947,7 @@ __global__ __launch_bounds__(512) void k_conv_bf_dw(const int32_t* __restrict__ 
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb) acc[mi][nb] = mfma_bf(a[it % (AD + 1)], bq[sb & 1][nb], acc[mi][nb]);
       __builtin_amdgcn_sched_barrier(0);
-      if constexpr (it == MAXC - 1) mid();
+      if constexpr (it == (SUBS > 1 ? MAXC - 1 : MAXC / 2)) mid();
     });
   };
 
@@ -1086,7 +1091,7 @@ void conv_bf16_kernel_name(int K, int cin, int cout, int pass, int64_t rows, cha
                            size_t n) {
   const int kk = pass == 1 ? cout : cin;  // reduction channels of the first chunk
   if (pass == 2)
-    snprintf(buf, n, "k_conv_bf_dw<%d, 5>", K);
+    snprintf(buf, n, K == 5 ? "k_conv_bf_dw<5, 10, 4, 4>" : "k_conv_bf_dw<3, 5, 8, 8>");
   else
     snprintf(buf, n, "%s<%d, %d, %s>",
              wide_tiles(K, kk, pass == 1 ? cin : cout, rows) ? "k_conv_bfw" : "k_conv_bf", K,
@@ -1131,11 +1136,11 @@ void conv_bf16_bwd(const oc_octree* t, int l, int K, const uint16_t* x, int cin,
     const int nr = dw_ranges(t, l, K, cin, cout);
     const dim3 grid((unsigned)dw_items(K, nr), blocks(cout, 64), blocks(cin, 64));
     if (K == 5)
-      launch_main(k_conv_bf_dw<5, 5>, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, cin,
-                  dy16, cout, nr, part);
+      launch_main(k_conv_bf_dw<5, 10, 4, 4>, grid, dim3(256), s, (const int32_t*)t->nbr[l], G, x,
+                  cin, dy16, cout, nr, part);
     else
-      launch_main(k_conv_bf_dw<3, 5>, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, cin,
-                  dy16, cout, nr, part);
+      launch_main(k_conv_bf_dw<3, 5, 8, 8>, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x,
+                  cin, dy16, cout, nr, part);
     const int64_t E = (int64_t)K3 * cin * cout;
     oc::launch(k_bf_sum, dim3(blocks(E, 4 * TB)), dim3(TB), 0, s, part, nr, E, dw);
   }
