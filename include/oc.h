@@ -198,8 +198,10 @@ void oc_octree_free(oc_octree* tree);
  *   ws      dev workspace of at least oc_conv_fwd_workspace() bytes (may be
  *           NULL when that is 0): partial sums of a reduction split across
  *           workgroups, added in a fixed order (results are reproducible);
- *           for OC_BF16 shapes the bf16 matrix-core kernels do not take, x
- *           and w widened to fp32; when strided, each output's eight
+ *           for OC_BF16 shapes the bf16 matrix-core kernels do not take
+ *           (strided; channel counts not multiples of 16; rows of x or of
+ *           the output gradient spanning 2 GiB or more), x and w widened to
+ *           fp32; when strided, each output's eight
  *           source-group rows (32 bytes per output) and w transposed.
  *   flags   0 or OC_FUSE_RELU.
  * cin, cout in 1..1024. */
