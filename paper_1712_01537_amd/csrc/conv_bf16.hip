@@ -525,7 +525,7 @@ __global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nb
   const int li = lane & 15, q = lane >> 4;
   const int64_t g0 = (int64_t)blockIdx.x * GT;
   const int n0 = blockIdx.y * 64;
-    const int ob = 8 * chunk;
+  const int ob = 8 * chunk;
   if (tid < GT * 27 + 27)
     nbs[tid] = tid < GT * 27 && g0 + tid / 27 < ngroups ? nbr[27 * g0 + tid] : -1;
 
@@ -760,7 +760,13 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_conv_bf_dw(const int32_t* _
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int li = lane & 15, q = lane >> 4;
-  const int unit = blockIdx.x % NU, range = blockIdx.x / NU, nr = nranges;
+  // Work item of this workgroup: workgroups are dealt to the eight XCDs
+  // round-robin (x = blockIdx.x % 8), so item = x-th share of the items +
+  // blockIdx.x / 8 puts the units of a range, which stage the same rows, on
+  // one XCD, where its L2 serves the re-reads.  A bijection on 0..gridDim.x-1.
+  const int nitems = (int)gridDim.x, xcd = (int)blockIdx.x & 7, per = nitems >> 3;
+  const int item = xcd * per + (xcd < (nitems & 7) ? xcd : (nitems & 7)) + ((int)blockIdx.x >> 3);
+  const int unit = item % NU, range = item / NU, nr = nranges;
   int x0, x1, y0, y1;  // the unit's box of tap offsets (indices 0..K-1)
   if (K == 3) {
     x0 = x1 = unit, y0 = 0, y1 = 2;
