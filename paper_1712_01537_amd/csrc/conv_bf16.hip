@@ -523,7 +523,13 @@ __global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nb
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int li = lane & 15, q = lane >> 4;
-  const int64_t g0 = (int64_t)blockIdx.x * GT;
+  // tile of this workgroup: workgroups are dealt to the eight XCDs
+  // round-robin, so tile = x-th share of the tiles + blockIdx.x / 8 (x =
+  // blockIdx.x % 8) keeps neighbouring tiles, which share union rows, in one
+  // XCD's L2.  A bijection on 0..gridDim.x-1.
+  const int ntiles = (int)gridDim.x, xcd = (int)blockIdx.x & 7, tper = ntiles >> 3;
+  const int tile = xcd * tper + (xcd < (ntiles & 7) ? xcd : (ntiles & 7)) + ((int)blockIdx.x >> 3);
+  const int64_t g0 = (int64_t)tile * GT;
   const int n0 = blockIdx.y * 64;
   const int ob = 8 * chunk;
   if (tid < GT * 27 + 27)
