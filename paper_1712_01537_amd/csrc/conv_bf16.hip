@@ -439,10 +439,11 @@ __global__ __launch_bounds__(512) void k_conv_bf(const int32_t* __restrict__ nbr
 // row block of the leftover step.  Waits are compile-time counts of younger
 // loads from a replay of the fixed issue order (BfwShape::younger).  The eight waves'
 // partial tiles are added in wave order through LDS, 32 rows per round.
-template <int K, int HC>
+template <int K, int HC, int GT_, int NW_>
 struct BfwShape {
   static constexpr int R = (K - 1) / 2, S = K + 1, S2 = S * S, K2 = K * K, K3 = K2 * K;
-  static constexpr int GT = 16, NW = 8, NRB = GT / 2;
+  static constexpr int GT = GT_, NW = NW_, NRB = GT / 2;
+  static_assert(NW == NRB, "the reduction rounds give every row block one term per wave");
   static constexpr int SLAB = GT * S2 * 4;  // 16-byte pieces of one slab buffer
   static constexpr int NB = 4;              // slab buffers
   static constexpr int NSL = HC * S;        // slabs of a tile
@@ -468,7 +469,7 @@ struct BfwShape {
   // when item idx starts.
   static constexpr int younger(int what, int idx, int at) {
     int stage_end[2 * 6] = {};
-    int w_end[2 * 5 * 4] = {};
+    int w_end[96] = {};
     int ops = 0, issued = -1;
     for (int s = 0; s < NPRE; ++s) {
       ops += DC;
@@ -502,18 +503,19 @@ struct BfwShape {
   }
 };
 
-template <int K, int HC, bool FLIP>
-__global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nbr, int64_t ngroups,
+template <int K, int HC, bool FLIP, int GT_, int NW_>
+__global__ __launch_bounds__(NW_ * 64, 8 / NW_) void k_conv_bfw(const int32_t* __restrict__ nbr, int64_t ngroups,
                                                    const uint16_t* __restrict__ x, int kk,
                                                    const uint16_t* __restrict__ wp, int nn,
                                                    int chunk, float* __restrict__ out, int acc_in,
                                                    int relu) {
-  using B = BfwShape<K, HC>;
+  using B = BfwShape<K, HC, GT_, NW_>;
   constexpr int R = B::R, S = B::S, S2 = B::S2, K2 = B::K2, K3 = B::K3;
   constexpr int GT = B::GT, NW = B::NW, NRB = B::NRB, SLAB = B::SLAB, NB = B::NB;
   constexpr int NFULL = B::NFULL, MI = B::MI, NI = B::NI, RW = B::RW, DC = B::DC;
   constexpr int NDMA = B::NDMA, RS = B::RS;
-  static_assert(B::NSL <= 12 && NI <= 40, "replay arrays");
+  static_assert(B::NSL <= 12 && NI <= 96, "replay arrays");
+  static_assert(GT * 27 + 27 <= NW * 64, "one neighbour entry per thread");
   __shared__ __attribute__((aligned(16))) v4u lds[B::NV];
   __shared__ __attribute__((aligned(16))) v4u trash[64];  // destination of padding loads
   // neighbour rows of the tile's groups, then 27 entries of -1 (the entries
@@ -698,9 +700,10 @@ __global__ __launch_bounds__(512) void k_conv_bfw(const int32_t* __restrict__ nb
     __syncthreads();
   }
   const int64_t nrows = 8 * ngroups;
+  constexpr int RPR = NW * 64 / 16;  // rows per round, 16 threads a row
 #pragma unroll
-  for (int rd = 0; rd < NRB / 2; ++rd) {
-    const int r = 32 * rd + (tid >> 4), cq = (tid & 15) * 4;
+  for (int rd = 0; rd < 16 * NRB / RPR; ++rd) {
+    const int r = RPR * rd + (tid >> 4), cq = (tid & 15) * 4;
     const int64_t row = 8 * g0 + r;
     const int n = n0 + cq;
     v4f sum = *reinterpret_cast<const v4f*>(&red[r * RS + cq]);
@@ -1046,6 +1049,12 @@ void wprep(const uint16_t* w, int K, int kk, int nn, int flip, uint16_t* wp, hip
 // of the 8-group kernel.  Its weight loads have no per-lane masks, so every
 // chunk must hold whole 32-channel halves and the columns whole blocks of 64;
 // K = 3 keeps the 8-group kernel.
+// Tile groups and waves of the K = 5 forward (k_conv_bfw): 8-group tiles of
+// four waves, two workgroups per compute unit, so that one workgroup's
+// epilogue (its waves' partial tiles added through LDS) runs beside the
+// other's MFMAs.
+constexpr int BFW_GT = 8, BFW_NW = 4;
+
 bool wide_tiles(int K, int kk, int nn, int64_t rows) {
   return K == 5 && kk % 32 == 0 && nn % 64 == 0 && rows * kk * 2 < ((int64_t)1 << 31);
 }
@@ -1055,17 +1064,18 @@ void launch_chunk(const oc_octree* t, int l, const uint16_t* x, int kk, const ui
                   int chunk, float* out, int acc_in, int relu, bool main, hipStream_t s) {
   const int64_t G = t->M[l - 1];
   const bool wide = wide_tiles(K, kk, nn, 8 * G);
-  const dim3 grid(blocks(G, wide ? 16 : 8), blocks(nn, 64));
+  const dim3 grid(blocks(G, wide ? BFW_GT : 8), blocks(nn, 64));
+  const dim3 block(wide ? BFW_NW * 64 : 512);
   auto kern = k_conv_bf<K, HC, FLIP>;
   if constexpr (K == 5) {
-    if (wide) kern = k_conv_bfw<K, HC, FLIP>;
+    if (wide) kern = k_conv_bfw<K, HC, FLIP, BFW_GT, BFW_NW>;
   }
   if (main)
-    oc::launch_main(kern, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x, kk, wp, nn, chunk,
-                    out, acc_in, relu);
+    oc::launch_main(kern, grid, block, s, (const int32_t*)t->nbr[l], G, x, kk, wp, nn, chunk, out,
+                    acc_in, relu);
   else
-    oc::launch(kern, grid, dim3(512), 0, s, (const int32_t*)t->nbr[l], G, x, kk, wp, nn,
-                       chunk, out, acc_in, relu);
+    oc::launch(kern, grid, block, 0, s, (const int32_t*)t->nbr[l], G, x, kk, wp, nn, chunk, out,
+               acc_in, relu);
 }
 
 // out = conv over kk reduction channels, in chunks of 64 added in order; the
@@ -1104,10 +1114,11 @@ void conv_bf16_kernel_name(int K, int cin, int cout, int pass, int64_t rows, cha
   const int kk = pass == 1 ? cout : cin;  // reduction channels of the first chunk
   if (pass == 2)
     snprintf(buf, n, K == 5 ? "k_conv_bf_dw<5, 10, 4, 4>" : "k_conv_bf_dw<3, 5, 8, 8>");
+  else if (wide_tiles(K, kk, pass == 1 ? cin : cout, rows))
+    snprintf(buf, n, "k_conv_bfw<%d, %d, %s, %d, %d>", K, kk > 32 ? 2 : 1,
+             pass == 1 ? "true" : "false", BFW_GT, BFW_NW);
   else
-    snprintf(buf, n, "%s<%d, %d, %s>",
-             wide_tiles(K, kk, pass == 1 ? cin : cout, rows) ? "k_conv_bfw" : "k_conv_bf", K,
-             kk > 32 ? 2 : 1, pass == 1 ? "true" : "false");
+    snprintf(buf, n, "k_conv_bf<%d, %d, %s>", K, kk > 32 ? 2 : 1, pass == 1 ? "true" : "false");
 }
 
 size_t conv_bf16_fwd_ws(int K, int cin, int cout) { return wp_bytes(K, cin, cout); }
