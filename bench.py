@@ -484,7 +484,7 @@ class Accounting:
     def work(self, tag, L):
         """Algorithmic flops (MFMA-bound classes) or HBM bytes of one launch."""
         N, M = self.N, self.M
-        if tag == "build_emit":  # counted with the first half
+        if tag in ("build_emit", "dw_sum"):  # counted with the first half; no flops
             return 0
         if tag == "build":
             d = self.wl.depth
@@ -804,6 +804,8 @@ class Step(Accounting):
             rec["bwd"] = {}
         saved_sw = {li: sw for li, xin, yout, sw in saved}
         routed = set()  # pool layers whose backward ran with the conv above them
+        # the weight gradients' partial sums, added by one launch at the end
+        pending = []
         for li, xin, yout, sw in reversed(saved):
             L = wl.layers[li]
             g_in, dw = g, None
@@ -837,7 +839,7 @@ class Step(Accounting):
                     dx = None
                 dwf = (lambda: oc.oc_conv_bwd(
                     tree, L.depth, L.ksize, L.stride, xin, w, g, y=yout, relu=relu,
-                    need_dx=False, need_dw=True))
+                    need_dx=False, need_dw=True, defer=pending))
                 if self.side is None:
                     _, dw = self._run("conv_bwd_weight", li, dwf)
                 else:
@@ -879,6 +881,12 @@ class Step(Accounting):
                 masked = False
             if rec is not None:  # a routed input gradient is the pooling's record
                 rec["bwd"][li] = (g_in, None if li - 1 in routed and L.op == "conv" else g, dw)
+        if pending:  # on the stream of the weight gradients
+            if self.side is None:
+                self._run("dw_sum", None, lambda: oc.oc_sum_partials(pending))
+            else:
+                with self.torch.cuda.stream(self.side):
+                    self._run("dw_sum", None, lambda: oc.oc_sum_partials(pending))
         if self.side is not None:
             self.torch.cuda.current_stream().wait_stream(self.side)
         return g
@@ -985,6 +993,7 @@ class TrainStep(Step):
             rec.update(units=units, feat=feat, h0=h0, h1=h1, h2=h2, logits=zl, loss=loss,
                        dlogits=dz, dh1=dh1, dfeat=g, bwd={})
         da_up = None  # the unit above routed its input gradient into this unit's pooling
+        pending = []  # the weight gradients' partial sums, added by one launch
         for li, xin, z, a, mean, invstd, p, sw in reversed(units):
             L = wl.layers[li]
             w = self.conv_p[li]["w"]
@@ -1006,10 +1015,12 @@ class TrainStep(Step):
                     tree, L.depth, 3, w, dz_, sw_below, xp=p_below))
             self._run("conv_bwd_weight", li, lambda: oc.oc_conv_bwd(
                 tree, L.depth, 3, 1, xin, w, dz_, need_dx=False, need_dw=True,
-                dw_out=self.conv_p[li]["g"]))
+                dw_out=self.conv_p[li]["g"], defer=pending))
             if rec is not None:
                 rec["bwd"][li] = (g_in, da, dz_, None)
             g = None
+        if pending:
+            self._run("dw_sum", None, lambda: oc.oc_sum_partials(pending))
         if rec is not None:  # parameters and velocities before the update
             rec["before"] = {k: {q: b[q].clone() for q in ("w", "v")} for k, b in self.flat.items()}
         for key, dec in (("dec", self.DECAY), ("pla", 0.0)):
@@ -1334,6 +1345,10 @@ def main():
                        "frac": r["frac"]})
         tot_us += t
         tot_work += work
+    # the weight gradients' partial sums of all layers, one launch per step
+    a = allk.get((None, "dw_sum"))
+    if a and a[1]:
+        tot_us += a[0] * 1e3 / a[1]
     if tot_us > 0:
         ops_out["conv_fwd_bwd_all"] = op_rate("conv", tot_work, tot_us, bf16)
 

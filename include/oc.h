@@ -61,6 +61,14 @@ typedef enum { OC_F32 = 0, OC_BF16 = 1 } oc_dtype;
  * masks dy with [y > 0] (Sec. 4, ReLU after each convolution). */
 #define OC_FUSE_RELU 1
 
+/* oc_conv_bwd flag: leave the weight gradient as its partial sums in the
+ * workspace instead of adding them into dw, so that one oc_sum_partials
+ * launch can add those of several layers (dw is then written by that call;
+ * the workspace must stay untouched until it has run).  Layers whose weight
+ * gradient has no deferred form still write dw; oc_conv_dw_partials tells
+ * which, and where the partial sums are. */
+#define OC_DEFER_DW 2
+
 /* Device memory provider for the octree's arrays and oc_build's temporaries.
  * alloc returns device memory usable in stream order on `stream` (NULL on
  * failure); free releases it in stream order.  Pass NULL to oc_build to use
@@ -279,6 +287,7 @@ size_t oc_conv_bwd_workspace(const oc_octree* tree, int32_t depth, int32_t ksize
  *   dx   dev f32 [N_l][cin] or NULL: gradient w.r.t. x (overwritten).
  *   dw   dev f32 [K^3][cin][cout] or NULL: gradient w.r.t. w (overwritten).
  *   ws   dev workspace of at least oc_conv_bwd_workspace() bytes.
+ *   flags   0, OC_FUSE_RELU, OC_DEFER_DW or both.
  * Deterministic: no floating-point atomics; repeated calls give identical
  * bits.  The strided workspace holds each output's eight source-group rows,
  * the upstream gradient gathered at the evaluated outputs and the weight
@@ -287,6 +296,28 @@ oc_status oc_conv_bwd(const oc_octree* tree, int32_t depth, int32_t ksize, int32
                       oc_dtype dt, const void* x, int32_t cin, const void* w, int32_t cout,
                       const float* y, const float* dy, float* dx, float* dw, void* ws,
                       size_t ws_bytes, int32_t flags, hipStream_t stream);
+
+/* Where oc_conv_bwd with OC_DEFER_DW leaves the weight gradient of these
+ * arguments (the same as oc_conv_bwd's): *nparts partial sums of *count =
+ * K^3 cin cout floats each, one after another at byte *offset of its
+ * workspace (256-byte aligned); dw = their sum in index order, which
+ * oc_sum_partials forms.  *nparts = 0: the layer writes dw itself (strided,
+ * bf16 on the bf16 kernels, or no octants).  The first layer's and the
+ * matrix-core kernels' reductions over ranges of groups (the transposed
+ * products of Sec. 3.2) are what is deferred. */
+oc_status oc_conv_dw_partials(const oc_octree* tree, int32_t depth, int32_t ksize, int32_t stride,
+                              oc_dtype dt, int32_t cin, int32_t cout, size_t* offset,
+                              int32_t* nparts, int64_t* count);
+
+/* outs[i][e] = sum over p < nparts[i] of parts[i][p counts[i] + e], for every
+ * set i < n, in one launch per eight sets whose buffers are 16-byte aligned
+ * and whose counts are multiples of 4 (others alone).  Each entry gets its
+ * terms in the same fixed order as inside oc_conv_bwd, so the bits equal a
+ * call without OC_DEFER_DW.  Host arrays of device pointers; outs may not
+ * overlap parts.  OC_ERR_ARG for n < 0, NULL arrays, nparts < 1 or
+ * counts < 0. */
+oc_status oc_sum_partials(int32_t n, const float* const* parts, const int32_t* nparts,
+                          const int64_t* counts, float* const* outs, hipStream_t stream);
 
 /* The input gradient of a stride-1 fp32 convolution whose input x is the
  * output of a 2x2x2 max-pooling from depth l+1, carried on through that

@@ -32,6 +32,7 @@ __all__ = [
     "oc_profile_next",
     "CallProfile",
     "oc_conv_bwd",
+    "oc_sum_partials",
     "oc_conv_bwd_pool",
     "oc_deconv_fwd",
     "oc_deconv_bwd",
@@ -42,6 +43,7 @@ __all__ = [
     "oc_gpool_fwd",
     "oc_gpool_bwd",
     "OC_FUSE_RELU",
+    "OC_DEFER_DW",
     "OC_POOL_MAX",
     "OC_POOL_AVG",
     "oc_bn_fwd",
@@ -57,6 +59,7 @@ __all__ = [
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 OC_FUSE_RELU = 1
+OC_DEFER_DW = 2
 OC_POOL_MAX, OC_POOL_AVG = 0, 1
 OC_F32, OC_BF16 = 0, 1
 STATUS = {0: "OC_OK", 1: "OC_ERR_ARG", 2: "OC_ERR_RANGE", 3: "OC_ERR_NOMEM", 4: "OC_ERR_DEVICE",
@@ -73,7 +76,7 @@ EXPORTS = (
     "oc_bn_workspace", "oc_bn_fwd", "oc_bn_bwd", "oc_fc_fwd", "oc_fc_bwd", "oc_dropout",
     "oc_softmax_ce_workspace", "oc_softmax_ce", "oc_sgd", "oc_conv_pool_fwd",
     "oc_conv_pool_fwd_workspace", "oc_bn_pool_fwd", "oc_conv_bwd_pool_workspace",
-    "oc_conv_bwd_pool",
+    "oc_conv_bwd_pool", "oc_conv_dw_partials", "oc_sum_partials",
 )
 
 
@@ -171,6 +174,8 @@ def load():
         "oc_conv_bwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, p, p, p, sz, i32, p],
                         C.c_int),
         "oc_conv_bwd_pool_workspace": ([p, i32, i32, i32, i32], sz),
+        "oc_conv_dw_partials": ([p, i32, i32, i32, C.c_int, i32, i32, p, p, p], C.c_int),
+        "oc_sum_partials": ([i32, p, p, p, p, p], C.c_int),
         "oc_conv_bwd_pool": ([p, i32, i32, p, i32, i32, p, p, p, p, p, p, p, sz, i32, p],
                              C.c_int),
         "oc_deconv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, sz, i32, p],
@@ -511,8 +516,11 @@ def oc_conv_fwd_noalloc(tree: Octree, depth: int, ksize: int, stride: int, x: to
 def oc_conv_bwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tensor,
                 w: torch.Tensor, dy: torch.Tensor, y: torch.Tensor | None = None,
                 relu: bool = False, need_dx: bool = True, need_dw: bool = True,
-                dw_out: torch.Tensor | None = None):
-    """(dx or None, dw or None); dw_out: a caller tensor to write dw into."""
+                dw_out: torch.Tensor | None = None, defer: list | None = None):
+    """(dx or None, dw or None); dw_out: a caller tensor to write dw into.
+    defer: a list; when the layer's weight gradient has a deferred form
+    (oc_conv_dw_partials), its partial sums stay in this call's workspace, a
+    record is appended to the list, and dw is written by oc_sum_partials(defer)."""
     K3, cin, cout, n_in, n_out = _conv_dims(tree, depth, stride, x, w)
     if K3 != ksize ** 3:
         raise OcError(1, f"w has {K3} taps, expected {ksize ** 3}")
@@ -526,13 +534,39 @@ def oc_conv_bwd(tree: Octree, depth: int, ksize: int, stride: int, x: torch.Tens
     ws_bytes = L.oc_conv_bwd_workspace(tree.handle, depth, ksize, stride, dt, cin, cout)
     ws = torch.empty(max(int(ws_bytes), 1), dtype=torch.uint8, device=w.device)
     yp = _dev(y, "y", torch.float32, (n_out, cout)) if relu else None
+    flags = OC_FUSE_RELU if relu else 0
+    rec = None
+    if defer is not None and need_dw:
+        off, npart, cnt = C.c_size_t(0), C.c_int32(0), C.c_int64(0)
+        _check(L.oc_conv_dw_partials(tree.handle, depth, ksize, stride, dt, cin, cout,
+                                     C.byref(off), C.byref(npart), C.byref(cnt)))
+        if npart.value > 0:
+            flags |= OC_DEFER_DW
+            rec = (ws, off.value, npart.value, cnt.value, dw)
     _check(L.oc_conv_bwd(tree.handle, depth, ksize, stride, dt, _dev(x, "x") if x is not None else None,
                          cin, _dev(w, "w"), cout, yp,
                          _dev(dy, "dy", torch.float32, (n_out, cout)),
                          _dev(dx, "dx") if dx is not None else None,
                          _dev(dw, "dw") if dw is not None else None,
-                         _dev(ws, "ws"), ws.numel(), OC_FUSE_RELU if relu else 0, _stream()))
+                         _dev(ws, "ws"), ws.numel(), flags, _stream()))
+    if rec is not None:
+        defer.append(rec)
     return dx, dw
+
+
+def oc_sum_partials(defer: list) -> None:
+    """Write the weight gradients of the oc_conv_bwd calls recorded in defer
+    (their partial sums, one launch per eight layers) and empty the list."""
+    if not defer:
+        return
+    L = load()
+    n = len(defer)
+    parts = (C.c_void_p * n)(*[r[0].data_ptr() + r[1] for r in defer])
+    nparts = (C.c_int32 * n)(*[r[2] for r in defer])
+    counts = (C.c_int64 * n)(*[r[3] for r in defer])
+    outs = (C.c_void_p * n)(*[_dev(r[4], "dw") for r in defer])
+    _check(L.oc_sum_partials(n, parts, nparts, counts, outs, _stream()))
+    defer.clear()
 
 
 def oc_conv_bwd_pool(tree: Octree, depth: int, ksize: int, w: torch.Tensor, dy: torch.Tensor,

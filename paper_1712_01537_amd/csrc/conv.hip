@@ -425,8 +425,47 @@ oc_status oc_conv_bwd(const oc_octree* t, int32_t l, int32_t K, int32_t stride, 
     if (sh.units == 0)
       oc::fill_u32(dw, 0u, (int64_t)sh.K3 * cin * cout, s);
     else
-      oc::conv_s1_bwd_weight_f32(t, l, K, (const float*)x, cin, dy, cout, dw, wsf, s);
+      oc::conv_s1_bwd_weight_f32(t, l, K, (const float*)x, cin, dy, cout, dw, wsf, s,
+                                 (flags & OC_DEFER_DW) != 0);
   }
+  OC_LAUNCH_CHECK();
+  return OC_OK;
+}
+
+oc_status oc_conv_dw_partials(const oc_octree* t, int32_t l, int32_t K, int32_t stride,
+                              oc_dtype dt, int32_t cin, int32_t cout, size_t* offset,
+                              int32_t* nparts, int64_t* count) {
+  ConvShape sh;
+  oc_status st = check_conv(t, l, K, stride, dt, cin, cout, &sh, "oc_conv_dw_partials");
+  if (st != OC_OK) return st;
+  if (!offset || !nparts || !count)
+    return oc::fail(OC_ERR_ARG, "oc_conv_dw_partials: NULL output pointer");
+  *count = (int64_t)sh.K3 * cin * cout;
+  *offset = 0;
+  *nparts = 0;
+  // strided and native-bf16 layers, and layers without groups, write dw directly
+  if (stride > 1 || bf16_native(sh, dt, cin, cout) || sh.units == 0) return OC_OK;
+  // oc_conv_bwd's stride-1 workspace: (bf16: widened w and x,) the masked dy,
+  // then the weight gradient's partial sums
+  size_t off = mask_ws_bytes(sh, cout);
+  if (dt == OC_BF16) off += w32_bytes(sh, cin, cout) + x32_bytes(sh, cin);
+  *offset = off;
+  *nparts = (int32_t)oc::conv_s1_dw_parts(t, l, K, cin, cout);
+  return OC_OK;
+}
+
+oc_status oc_sum_partials(int32_t n, const float* const* parts, const int32_t* nparts,
+                          const int64_t* counts, float* const* outs, hipStream_t s) {
+  if (n < 0) return oc::fail(OC_ERR_ARG, "oc_sum_partials: n = %d < 0", (int)n);
+  if (n == 0) return OC_OK;
+  if (!parts || !nparts || !counts || !outs)
+    return oc::fail(OC_ERR_ARG, "oc_sum_partials: NULL array");
+  for (int i = 0; i < n; ++i) {
+    if (nparts[i] < 1 || counts[i] < 0 || (counts[i] > 0 && (!parts[i] || !outs[i])))
+      return oc::fail(OC_ERR_ARG, "oc_sum_partials: set %d: %d partials of %lld entries", i,
+                      (int)nparts[i], (long long)counts[i]);
+  }
+  oc::sum_partials_multi(n, parts, (const int*)nparts, counts, outs, s);
   OC_LAUNCH_CHECK();
   return OC_OK;
 }

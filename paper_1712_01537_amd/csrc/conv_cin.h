@@ -25,9 +25,10 @@ void conv_cin_pool_fwd(const oc_octree* t, int l, const float* x, int cin, const
 size_t conv_cin_dw_parts(const oc_octree* t, int l, int cin, int cout);
 
 // dw [27][cin][cout] = weight gradient for upstream gradient dy [N_l][cout];
-// part holds conv_cin_dw_parts() partial sums.
+// part holds conv_cin_dw_parts() partial sums.  defer: leave the partial
+// sums in part (dw not written).
 void conv_cin_dw(const oc_octree* t, int l, const float* x, int cin, const float* dy, int cout,
-                 float* dw, float* part, hipStream_t s);
+                 float* dw, float* part, hipStream_t s, bool defer = false);
 
 // Name of the kernel of pass 0 (forward), 2 (weight gradient) or 3 (the
 // pooled forward).

@@ -525,7 +525,7 @@ size_t conv_cin_dw_parts(const oc_octree* t, int l, int cin, int cout) {
 }
 
 void conv_cin_dw(const oc_octree* t, int l, const float* x, int cin, const float* dy, int cout,
-                 float* dw, float* part, hipStream_t s) {
+                 float* dw, float* part, hipStream_t s, bool defer) {
   const int64_t G = t->M[l - 1];
   const int64_t entries = (int64_t)27 * cin * cout;
   const int64_t np = (int64_t)conv_cin_dw_parts(t, l, cin, cout);
@@ -534,7 +534,7 @@ void conv_cin_dw(const oc_octree* t, int l, const float* x, int cin, const float
     launch_main(k_cin_dw<3>, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, dy, cout, part);
   else
     launch_main(k_cin_dw<4>, grid, dim3(TB), s, (const int32_t*)t->nbr[l], G, x, dy, cout, part);
-  sum_partials(part, (int)np, entries, dw, s);
+  if (!defer) sum_partials(part, (int)np, entries, dw, s);
 }
 
 void conv_cin_kernel_name(int cin, int pass, char* buf, size_t n) {

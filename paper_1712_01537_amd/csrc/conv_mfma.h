@@ -55,8 +55,17 @@ void conv_s1_bwd_data_pool_f32(const oc_octree* t, int l, int K, const float* dy
 size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout);
 
 // dw [K^3][cin][cout] = weight gradient of a stride-1 convolution; part holds
-// conv_s1_dw_parts() partial sums.
+// conv_s1_dw_parts() partial sums.  defer: leave the partial sums in part
+// (dw not written), for a later sum_partials_multi.
 void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, int cin,
-                            const float* dy, int cout, float* dw, float* part, hipStream_t s);
+                            const float* dy, int cout, float* dw, float* part, hipStream_t s,
+                            bool defer = false);
+
+// outs[i] = fixed-order sum of nparts[i] partials of counts[i] fp32 entries at
+// parts[i], for i < n, in as few launches as possible (one per eight sets
+// with 16-byte aligned buffers and counts a multiple of 4; other sets alone);
+// the same bits as sum_partials of each set.
+void sum_partials_multi(int n, const float* const* parts, const int* nparts,
+                        const int64_t* counts, float* const* outs, hipStream_t s);
 
 }  // namespace oc

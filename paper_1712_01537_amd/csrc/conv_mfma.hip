@@ -1460,11 +1460,62 @@ __global__ __launch_bounds__(TB) void k_sum_parts(const float* __restrict__ part
   }
 }
 
+// Sub-sums per slot of k_sum_parts for nv entry slots: 16 when that gives two
+// workgroups per CU, else 64.
+int sum_sub(int64_t nv) { return oc::cdiv(nv, TB / 16) >= 2 * (int64_t)oc::cu_count() ? 16 : 64; }
+
+// Several k_sum_parts in one launch: workgroups [first[i], first[i + 1]) add
+// set i with its own sub-sum count, so every entry gets the same terms in the
+// same order (and bits) as a k_sum_parts of that set alone.  Four entries per
+// slot (every set's count a multiple of 4, 16-byte aligned buffers).
+struct PartSet {
+  const float* part;
+  float* out;
+  int64_t n;
+  int np, sub, first;
+};
+constexpr int MAX_SETS = 8;
+struct PartSets {
+  PartSet s[MAX_SETS];
+  int n;
+};
+
+__global__ __launch_bounds__(TB) void k_sum_parts_multi(PartSets sets) {
+  __shared__ v4f r[TB];
+  int i = 0;
+  while (i + 1 < sets.n && (int)blockIdx.x >= sets.s[i + 1].first) ++i;
+  const PartSet& d = sets.s[i];
+  const int SUB = d.sub, SLOTS = TB / SUB;
+  const int el = threadIdx.x % SLOTS, sg = threadIdx.x / SLOTS;
+  const int64_t nv = d.n / 4, e = (int64_t)((int)blockIdx.x - d.first) * SLOTS + el;
+  const v4f* pv = reinterpret_cast<const v4f*>(d.part);
+  const int np = d.np;
+  v4f acc = {};
+  if (e < nv) {
+    int p = sg;
+    for (; p + 3 * SUB < np; p += 4 * SUB) {  // four independent loads in flight
+      const v4f a = pv[(int64_t)p * nv + e], b = pv[(int64_t)(p + SUB) * nv + e];
+      const v4f c = pv[(int64_t)(p + 2 * SUB) * nv + e], f = pv[(int64_t)(p + 3 * SUB) * nv + e];
+      acc += a;
+      acc += b;
+      acc += c;
+      acc += f;
+    }
+    for (; p < np; p += SUB) acc += pv[(int64_t)p * nv + e];
+  }
+  r[sg * SLOTS + el] = acc;
+  __syncthreads();
+  if (sg == 0 && e < nv) {
+    v4f t = r[el];
+    for (int k = 1; k < SUB; ++k) t += r[k * SLOTS + el];
+    reinterpret_cast<v4f*>(d.out)[e] = t;
+  }
+}
+
 void sum_parts(const float* part, int np, int64_t n, float* out, hipStream_t s) {
   const bool v4 = n % 4 == 0 && (uintptr_t)part % 16 == 0 && (uintptr_t)out % 16 == 0;
   const int64_t nv = v4 ? n / 4 : n;
-  // 16 sub-sums per slot when that gives two workgroups per CU, else 64
-  const bool wide = oc::cdiv(nv, TB / 16) >= 2 * (int64_t)oc::cu_count();
+  const bool wide = sum_sub(nv) == 16;
   const unsigned grid = (unsigned)oc::cdiv(nv, TB / (wide ? 16 : 64));
   if (v4 && wide)
     oc::launch((k_sum_parts<16, 4>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
@@ -1906,16 +1957,16 @@ size_t conv_s1_dw_parts(const oc_octree* t, int l, int K, int cin, int cout) {
 
 void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, int cin,
                             const float* dy, int cout, float* dw, float* part,
-                            hipStream_t s) {
+                            hipStream_t s, bool defer) {
   const int64_t entries = (int64_t)K * K * K * cin * cout;
   if (conv_cin_supported(K, cin, cout)) {
-    conv_cin_dw(t, l, x, cin, dy, cout, dw, part, s);
+    conv_cin_dw(t, l, x, cin, dy, cout, dw, part, s, defer);
     return;
   }
   DwtCfg d;
   if (pick_dwt(K, t->M[l - 1], cin, cout, &d)) {
     if (dispatch_dwt(t, l, d, x, cin, dy, cout, part, s)) {
-      sum_parts(part, (int)d.nchunks, entries, dw, s);
+      if (!defer) sum_parts(part, (int)d.nchunks, entries, dw, s);
     } else {
       oc::set_error("no weight-gradient kernel for cin=%d cout=%d", cin, cout);
     }
@@ -1944,11 +1995,35 @@ void conv_s1_bwd_weight_f32(const oc_octree* t, int l, int K, const float* x, in
     oc::set_error("no weight-gradient kernel for K=%d cin=%d cout=%d", K, cin, cout);
   }
 #undef OC_DW
-  sum_parts(part, (int)c.nchunks, entries, dw, s);
+  if (!defer) sum_parts(part, (int)c.nchunks, entries, dw, s);
 }
 
 void sum_partials(const float* part, int np, int64_t n, float* out, hipStream_t s) {
   sum_parts(part, np, n, out, s);
+}
+
+void sum_partials_multi(int n, const float* const* parts, const int* nparts,
+                        const int64_t* counts, float* const* outs, hipStream_t s) {
+  PartSets sets{};
+  int blocks = 0;
+  for (int i = 0; i < n; ++i) {
+    const bool v4 = counts[i] % 4 == 0 && (uintptr_t)parts[i] % 16 == 0 &&
+                    (uintptr_t)outs[i] % 16 == 0;
+    if (!v4 || nparts[i] < 1 || counts[i] == 0) {  // not for the batch: alone
+      if (counts[i] > 0) sum_parts(parts[i], nparts[i], counts[i], outs[i], s);
+      continue;
+    }
+    if (sets.n == MAX_SETS) {  // a full batch goes now
+      oc::launch(k_sum_parts_multi, dim3((unsigned)blocks), dim3(TB), 0, s, sets);
+      sets.n = 0;
+      blocks = 0;
+    }
+    const int64_t nv = counts[i] / 4;
+    const int sub = sum_sub(nv);
+    sets.s[sets.n++] = PartSet{parts[i], outs[i], counts[i], nparts[i], sub, blocks};
+    blocks += (int)oc::cdiv(nv, TB / sub);
+  }
+  if (sets.n > 0) oc::launch(k_sum_parts_multi, dim3((unsigned)blocks), dim3(TB), 0, s, sets);
 }
 
 }  // namespace oc

@@ -56,6 +56,14 @@ def test_argument_errors_without_device():
     assert L.oc_deconv_fwd_workspace(None, 1, 3, 1, 0, 4, 3) == 0
     assert L.oc_gpool_fwd(None, 1, 3, 1, 0, None, 4, None, None, None) == 1
     assert L.oc_gpool_bwd(None, 1, 3, 1, 1, None, None, 4, None, None) == 1
+    off, npart, cnt = C.c_size_t(), C.c_int32(), C.c_int64()
+    assert L.oc_conv_dw_partials(None, 1, 3, 1, 0, 4, 4, C.byref(off), C.byref(npart),
+                                 C.byref(cnt)) == 1
+    assert L.oc_sum_partials(-1, None, None, None, None, None) == 1
+    assert L.oc_sum_partials(0, None, None, None, None, None) == 0
+    one = (C.c_void_p * 1)(None)
+    assert L.oc_sum_partials(1, one, (C.c_int32 * 1)(0), (C.c_int64 * 1)(4), one, None) == 1
+    assert L.oc_sum_partials(1, None, (C.c_int32 * 1)(2), (C.c_int64 * 1)(4), one, None) == 1
     assert L.oc_octree_signal(None) is None
     assert L.oc_status_str(2) == b"point outside the unit cube"
     L.oc_octree_free(None)

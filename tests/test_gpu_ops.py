@@ -264,6 +264,52 @@ def test_conv_small_bf16(K, stride):
     assert_dw_close(dw.cpu().numpy(), dwr, "dw bf16 inputs")
 
 
+DEFER_LAYERS = [  # K, stride, dtype, cin, cout: every weight-gradient path, and layers
+    # without a deferred form (strided; bf16 on the bf16 kernels)
+    (3, 1, torch.float32, 3, 16),     # first layer (Cin 3)
+    (3, 1, torch.float32, 4, 32),     # first layer (Cin 4)
+    (3, 1, torch.float32, 16, 32),    # matrix-core weight gradient, K = 3
+    (3, 1, torch.float32, 5, 7),      # ragged channels
+    (5, 1, torch.float32, 8, 16),     # K = 5
+    (3, 1, torch.bfloat16, 8, 24),    # bf16 widened to fp32
+    (3, 2, torch.float32, 16, 16),    # strided: dw written by the call
+    (3, 1, torch.bfloat16, 16, 32),   # bf16 kernels: dw written by the call
+    (3, 1, torch.float32, 32, 64),
+    (3, 1, torch.float32, 64, 128),
+    (3, 1, torch.float32, 16, 16),    # a ninth deferred set: a second launch
+]
+
+
+def test_conv_bwd_deferred_dw():
+    """oc_conv_bwd with OC_DEFER_DW leaves the weight gradient's partial sums
+    in its workspace; one oc_sum_partials over all layers gives the same bits
+    as the calls without it."""
+    oc = _oc()
+    pts, nrm, offs = synth.random_cloud(151, 2, 600, "union")
+    ref, tree = _trees(pts, nrm, offs, 5)
+    rng = np.random.default_rng(151)
+    pending, direct, deferred, nparts = [], [], [], []
+    for K, stride, dt, cin, cout in DEFER_LAYERS:
+        l = 5
+        n_out = ref.num(l) if stride == 1 else ref.num(l - 1)
+        x = _cuda(rng.standard_normal((ref.num(l), cin)).astype(np.float32), dt)
+        w = _cuda((rng.standard_normal((K ** 3, cin, cout)) / np.sqrt(K ** 3 * cin)).astype(np.float32), dt)
+        dy = _cuda(rng.standard_normal((n_out, cout)).astype(np.float32))
+        _, dw = oc.oc_conv_bwd(tree, l, K, stride, x, w, dy, need_dx=False)
+        before = len(pending)
+        _, dwd = oc.oc_conv_bwd(tree, l, K, stride, x, w, dy, need_dx=False, defer=pending)
+        nparts.append(len(pending) - before)
+        print(f"[defer] K{K} s{stride} {dt} {cin}->{cout}: deferred {nparts[-1]}", flush=True)
+        direct.append(dw)
+        deferred.append(dwd)
+    # every stride-1 layer off the bf16 kernels has a deferred form
+    assert nparts == [1, 1, 1, 1, 1, 1, 0, 0, 1, 1, 1]
+    oc.oc_sum_partials(pending)
+    assert pending == []
+    for (K, stride, dt, cin, cout), a, b in zip(DEFER_LAYERS, direct, deferred):
+        assert torch.equal(a, b), (K, stride, dt, cin, cout)
+
+
 BF16_NATIVE = [  # seed, B, n, depth, K, cin, cout, relu: tiles with ragged tails, one or two
     # 64-channel chunks of the reduction, one or two 64-column output blocks
     (41, 2, 700, 5, 5, 64, 64, False),
