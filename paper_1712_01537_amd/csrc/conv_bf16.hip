@@ -27,7 +27,8 @@
 // per lane; the transposing LDS load ds_read_b64_tr_b16 gives exactly that
 // from row-major tiles (lane i of a 16-lane group receives element i % 4 of
 // the 8-byte rows read by lanes 4r + i / 4, r = 0..3), so the staged x
-// positions and dY rows keep the layout of HBM.  A workgroup owns the taps
+// positions keep the layout of HBM, and dY is rounded to bf16 into a
+// sibling-group layout whose 16-byte pieces are eight children of a column.  A workgroup owns the taps
 // of one x-offset and up to two (K = 5) or three (K = 3) y-offsets for every
 // input channel block, the waves split those (tap, channel block) pairs and
 // keep their dW blocks in registers, and the workgroup streams a range of
@@ -207,6 +208,65 @@ __global__ __launch_bounds__(TB) void k_bf_cvt(const float* __restrict__ in,
   } else {
     for (int64_t i = e; i < n && i < e + 4; ++i)
       out[i] = (uint16_t)f2bf(ym && !(ym[i] > 0.f) ? 0.f : in[i]);
+  }
+}
+
+// The same conversion into the sibling-group layout of the weight gradient:
+// outg[g][c][j] = bf16(masked in[8g + j][c]) (the eight children of a group
+// contiguous per column, so that eight consecutive octants of one column are
+// one 16-byte piece), and the row-major copy outr[8g + j][c] when outr is
+// not NULL.  A workgroup converts 8 groups (64 rows) x 64 columns: 16-byte
+// loads of the rows, the bf16 values written transposed into LDS, then
+// 16-byte pieces read back and stored contiguously.  C % 4 == 0 and
+// 16-byte aligned rows (vec), else element loads.
+__global__ __launch_bounds__(TB) void k_bf_cvt_g(const float* __restrict__ in,
+                                                 const float* __restrict__ ym, int64_t ngroups,
+                                                 int C, int vec, uint16_t* __restrict__ outg,
+                                                 uint16_t* __restrict__ outr) {
+  constexpr int TP = 64 + 8;  // LDS row (one column of the tile) in bf16, padded
+  __shared__ __attribute__((aligned(16))) uint16_t tt[64 * TP];
+  const int64_t g0 = (int64_t)blockIdx.x * 8, nrows = 8 * ngroups;
+  const int c0 = blockIdx.y * 64;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int idx = threadIdx.x + TB * k, r = idx >> 4, cq = (idx & 15) * 4;
+    const int64_t row = 8 * g0 + r;
+    const int c = c0 + cq;
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (row < nrows && c < C) {
+      const int64_t e = row * C + c;
+      if (vec) {
+        const float4 a = *reinterpret_cast<const float4*>(in + e);
+        v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w;
+        if (ym) {
+          const float4 y = *reinterpret_cast<const float4*>(ym + e);
+          v[0] = y.x > 0.f ? v[0] : 0.f, v[1] = y.y > 0.f ? v[1] : 0.f;
+          v[2] = y.z > 0.f ? v[2] : 0.f, v[3] = y.w > 0.f ? v[3] : 0.f;
+        }
+      } else {
+        for (int i = 0; i < 4 && c + i < C; ++i) v[i] = ym && !(ym[e + i] > 0.f) ? 0.f : in[e + i];
+      }
+      uint32_t h[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) h[i] = f2bf(v[i]);
+      if (outr) {
+        if (vec)
+          *reinterpret_cast<uint2*>(outr + e) = uint2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+        else
+          for (int i = 0; i < 4 && c + i < C; ++i) outr[e + i] = (uint16_t)h[i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) tt[(cq + i) * TP + r] = (uint16_t)h[i];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int idx = threadIdx.x + TB * k, gl = idx >> 6, cl = idx & 63;
+    const int64_t g = g0 + gl;
+    if (g < ngroups && c0 + cl < C)
+      reinterpret_cast<v4u*>(outg)[g * C + c0 + cl] =
+          *reinterpret_cast<const v4u*>(&tt[cl * TP + 8 * gl]);
   }
 }
 
@@ -737,18 +797,20 @@ __global__ __launch_bounds__(NW_ * 64, 8 / NW_) void k_conv_bfw(const int32_t* _
 // waves on steps of 8 groups.  Per step the workgroup stages the unit's
 // positions of its GS groups and their 8 GS dY rows; x piece o of box
 // position (ix, iy, iz) of the step's group g sits at
-// o ^ 2(((iz + 2 iy) & 3) ^ (g & 1)), dY piece o of row r at
-// o ^ 2((r & 3) ^ ((r >> 3) & 1)).  A transposing load of a
+// o ^ 2(((iz + 2 iy) & 3) ^ (g & 1)).  dY comes in the sibling-group layout
+// dyg[g][c][8] (the eight children of a group contiguous per column), staged
+// as [group][64 columns][8]: the B operand of an MFMA (eight consecutive
+// octants of one column per lane) is then one 16-byte LDS read.  A transposing load of a
 // 16-lane group reads four children of one group in four distinct 32-byte
 // slots; the group-parity term moves the next 16-lane group (the next
 // group, at the same positions) onto the other four slots of each 256-byte
 // bank row, so 32 lanes read 256 distinct bytes.
-// part [nranges][K^3][cin][cout].
+// dyg [ngroups][cout][8] bf16; part [nranges][K^3][cin][cout].
 template <int K, int MAXC, int NW, int GS>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void k_conv_bf_dw(const int32_t* __restrict__ nbr,
                                                       int64_t ngroups,
                                                       const uint16_t* __restrict__ x, int cin,
-                                                      const uint16_t* __restrict__ dy, int cout,
+                                                      const uint16_t* __restrict__ dyg, int cout,
                                                       int nranges, float* __restrict__ part) {
   constexpr int R = (K - 1) / 2, S = K + 1, K3 = K * K * K;
   constexpr int NU = K == 5 ? 13 : 3;        // units
@@ -803,12 +865,13 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_conv_bf_dw(const int32_t* _
   // instruction, ta = the lane's neighbour entry (27 g + parent cell) and tb
   // = its byte offset in the row block (child offset * cin + channel; 2^31,
   // past any row, for channels past cin and positions past npos); for a dY
-  // instruction, ta = the lane's group of the step (GS past cout and for
-  // padding instructions) and tb = the byte offset of (row, column) in the
-  // step's rows.  Loads go through buffer resources over x and dY, absent
-  // rows to an offset past the end (zeros).
+  // instruction (one group of the step, its 64 columns of the workgroup's
+  // block, 16 bytes each), ta = that group (GS past cout and for padding
+  // instructions) and tb = the byte offset of (group, column) in the step's
+  // groups.  Loads go through buffer resources over x and dY, absent rows to
+  // an offset past the end (zeros).
   const sv4 xr = buf_rsrc(x, (uint32_t)(8 * ngroups * cin * 2));
-  const sv4 dr = buf_rsrc(dy, (uint32_t)(8 * ngroups * cout * 2));
+  const sv4 dr = buf_rsrc(dyg, (uint32_t)(8 * ngroups * cout * 2));
   int ta[DC];
   uint32_t tb[DC], dk[DC];  // dk: the instruction's byte offset in a stage buffer
 #pragma unroll
@@ -829,12 +892,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_conv_bf_dw(const int32_t* _
                   ? 2u * (uint32_t)((4 * (ux & 1) + 2 * (uy & 1) + (uz & 1)) * cin + ch)
                   : 0x80000000u;
     } else if (i < NXI + NYI) {
-      const int s = (i - NXI) * 64 + lane;
-      const int rl = s >> 3;
-      const int o = (s & 7) ^ (2 * ((rl & 3) ^ ((rl >> 3) & 1)));
-      const int co = n0 + 8 * o;
-      ta[k] = co < cout ? rl >> 3 : GS;
-      tb[k] = 2u * (uint32_t)(rl * cout + (co < cout ? co : 0));
+      const int gq = i - NXI, co = n0 + lane;
+      ta[k] = co < cout ? gq : GS;
+      tb[k] = 16u * (uint32_t)(gq * cout + (co < cout ? co : 0));
     }
   }
   // Instruction k of every wave stages x (XK), or of none (DK); otherwise
@@ -911,22 +971,18 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_conv_bf_dw(const int32_t* _
     const int o = 2 * cb + (tq >> 1);
     return ((gq * MAXPOS + p) * 8 + (o ^ (2 * (((iz + 2 * iy) & 3) ^ (gq & 1))))) * 16 + (tq & 1) * 8;
   };
-  auto b_off = [&](int nb, int gq, int hh) {  // byte offset of dY fragment nb, load hh
-    const int rl = 8 * gq + 4 * hh + r4;
-    const int o = 2 * nb + (tq >> 1);
-    return (XP + rl * 8 + (o ^ (2 * ((rl & 3) ^ ((rl >> 3) & 1))))) * 16 + (tq & 1) * 8;
-  };
-  // Byte offsets of this lane's transposing loads in a stage buffer for
-  // sub-step 0: pair mi's A loads, and dY fragment nb's first load.  A later
-  // sub-step sb adds 512 MAXPOS sb (A) or 4096 sb (dY, whose second load is
-  // 512 bytes on), constants that the loads take as immediate offsets.
+  // Byte offsets of this lane's loads in a stage buffer for sub-step 0: pair
+  // mi's transposing A loads, and dY fragment nb (group q's eight children
+  // of column n0 + 16 nb + li, one 16-byte piece).  A later sub-step sb adds
+  // 512 MAXPOS sb (A) or 4096 sb (dY), constants that the loads take as
+  // immediate offsets.
   uint32_t pa[MAXC][2], pbq[4];
 #pragma unroll
   for (int mi = 0; mi < MAXC; ++mi)
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) pa[mi][hh] = (uint32_t)a_off(wave + NW * mi, q, hh);
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) pbq[nb] = (uint32_t)b_off(nb, q, 0);
+  for (int nb = 0; nb < 4; ++nb) pbq[nb] = (uint32_t)((XP + q * 64 + 16 * nb + li) * 16);
 
   // The step's MFMAs in the fixed order (sub-step, pair): the A operand of
   // the pair two ahead and the dY fragments of the next sub-step are read
@@ -938,11 +994,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void k_conv_bf_dw(const int32_t* _
     const lds_char* lb = (const lds_char*)(lptr_t)lds + bo;
     auto ld_b = [&](v4u (&b)[4], int sb) {
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        const lds_char* p = lb + pbq[nb] + 4096 * sb;
-        b[nb] = join(__builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p),
-                     __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p + 512)));
-      }
+      for (int nb = 0; nb < 4; ++nb)
+        b[nb] = *reinterpret_cast<const __attribute__((address_space(3))) v4u*>(lb + pbq[nb] + 4096 * sb);
     };
     auto ld_a = [&](int it) {
       const int sb = it / MAXC, mi = it % MAXC;
@@ -1127,7 +1180,7 @@ size_t conv_bf16_bwd_ws(const oc_octree* t, int l, int K, int cin, int cout) {
   const size_t dy16 = align256((size_t)t->N[l] * cout * 2);
   const size_t part =
       align256((size_t)dw_ranges(t, l, K, cin, cout) * K * K * K * cin * cout * sizeof(float));
-  return dy16 + wp_bytes(K, cout, cin) + part;
+  return 2 * dy16 + wp_bytes(K, cout, cin) + part;  // dy rounded to bf16: row-major, by group
 }
 
 void conv_bf16_fwd(const oc_octree* t, int l, int K, const uint16_t* x, int cin,
@@ -1142,14 +1195,20 @@ void conv_bf16_bwd(const oc_octree* t, int l, int K, const uint16_t* x, int cin,
                    float* dw, void* ws, hipStream_t s) {
   const int64_t N = t->N[l], G = t->M[l - 1];
   char* p = (char*)ws;
-  uint16_t* dy16 = (uint16_t*)p;
+  uint16_t* dy16 = (uint16_t*)p;  // dy rounded to bf16, row-major (input gradient)
+  p += align256((size_t)N * cout * 2);
+  uint16_t* dyg = (uint16_t*)p;   // ... in the sibling-group layout (weight gradient)
   p += align256((size_t)N * cout * 2);
   uint16_t* wpf = (uint16_t*)p;
   p += wp_bytes(K, cout, cin);
   float* part = (float*)p;
   const int64_t n = N * cout;
   const int vec = (uintptr_t)dy % 16 == 0 && (!ym || (uintptr_t)ym % 16 == 0);
-  oc::launch(k_bf_cvt, dim3(blocks(n, 4 * TB)), dim3(TB), 0, s, dy, ym, n, vec, dy16);
+  if (dw)
+    oc::launch(k_bf_cvt_g, dim3(blocks(G, 8), blocks(cout, 64)), dim3(TB), 0, s, dy, ym, G, cout,
+               vec && cout % 4 == 0, dyg, dx ? dy16 : nullptr);
+  else
+    oc::launch(k_bf_cvt, dim3(blocks(n, 4 * TB)), dim3(TB), 0, s, dy, ym, n, vec, dy16);
   if (dx) {
     wprep(w, K, cout, cin, 1, wpf, s);
     launch_conv<true>(t, l, K, dy16, cout, wpf, cin, dx, 0, s);
@@ -1160,10 +1219,10 @@ void conv_bf16_bwd(const oc_octree* t, int l, int K, const uint16_t* x, int cin,
     const dim3 grid((unsigned)dw_items(K, nr), blocks(cout, 64), blocks(cin, 64));
     if (K == 5)
       launch_main(k_conv_bf_dw<5, 10, 4, 4>, grid, dim3(256), s, (const int32_t*)t->nbr[l], G, x,
-                  cin, dy16, cout, nr, part);
+                  cin, dyg, cout, nr, part);
     else
       launch_main(k_conv_bf_dw<3, 5, 8, 8>, grid, dim3(512), s, (const int32_t*)t->nbr[l], G, x,
-                  cin, dy16, cout, nr, part);
+                  cin, dyg, cout, nr, part);
     const int64_t E = (int64_t)K3 * cin * cout;
     oc::launch(k_bf_sum, dim3(blocks(E, 4 * TB)), dim3(TB), 0, s, part, nr, E, dw);
   }
