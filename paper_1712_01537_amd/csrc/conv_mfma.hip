@@ -1423,11 +1423,12 @@ __global__ __launch_bounds__(TB * HV) void k_conv_dwt(const int32_t* __restrict_
   }
 }
 
-// Fixed-order sum of np partials of n entries in one pass: a workgroup takes
-// TB / SUB entry slots (four consecutive entries each when V = 4: n a multiple
-// of 4, 16-byte aligned buffers), and thread (slot, k) adds partials k,
-// k + SUB, k + 2 SUB, ... in order, four loads in flight; the SUB sub-sums of
-// a slot are then added in k order.  SUB = 64 gives small n enough threads.
+// Fixed-order sum of np partials of n entries in one pass, for buffers that
+// k_sum_parts_multi cannot take (not 16-byte aligned, or n not a multiple of
+// 4): a workgroup takes TB / SUB entry slots (four consecutive entries each
+// when V = 4), and thread (slot, k) adds partials k, k + SUB, k + 2 SUB, ...
+// in order, four loads in flight; the SUB sub-sums of a slot are then added
+// in k order.  SUB = 64 gives small n enough threads.
 template <int SUB, int V>
 __global__ __launch_bounds__(TB) void k_sum_parts(const float* __restrict__ part, int np,
                                                   int64_t n, float* __restrict__ out) {
@@ -1460,14 +1461,22 @@ __global__ __launch_bounds__(TB) void k_sum_parts(const float* __restrict__ part
   }
 }
 
-// Sub-sums per slot of k_sum_parts for nv entry slots: 16 when that gives two
-// workgroups per CU, else 64.
-int sum_sub(int64_t nv) { return oc::cdiv(nv, TB / 16) >= 2 * (int64_t)oc::cu_count() ? 16 : 64; }
+// Sub-sums per entry slot of k_sum_parts_multi for np partials: the power of
+// two nearest below np / 8 (about eight loads per thread), 1 to 64.
+int sum_sub(int np) {
+  int sub = 1;
+  while (sub < 64 && 16 * sub <= np) sub *= 2;
+  return sub;
+}
 
-// Several k_sum_parts in one launch: workgroups [first[i], first[i + 1]) add
-// set i with its own sub-sum count, so every entry gets the same terms in the
-// same order (and bits) as a k_sum_parts of that set alone.  Four entries per
-// slot (every set's count a multiple of 4, 16-byte aligned buffers).
+// Fixed-order sums of several sets of partials in one launch: workgroups
+// [first[i], first[i + 1]) add set i.  A workgroup takes TB / SUB entry
+// slots of four consecutive entries; thread (slot, k) adds partials k,
+// k + SUB, k + 2 SUB, ... in order, four loads in flight, and the SUB
+// sub-sums of a slot are then added pairwise in LDS (k + SUB/2 into k, then
+// k + SUB/4, ...).  The order depends only on the set's partial count, so
+// every entry's bits are the same in any batch.  Every set's count a
+// multiple of 4, 16-byte aligned buffers.
 struct PartSet {
   const float* part;
   float* out;
@@ -1486,7 +1495,7 @@ __global__ __launch_bounds__(TB) void k_sum_parts_multi(PartSets sets) {
   while (i + 1 < sets.n && (int)blockIdx.x >= sets.s[i + 1].first) ++i;
   const PartSet& d = sets.s[i];
   const int SUB = d.sub, SLOTS = TB / SUB;
-  const int el = threadIdx.x % SLOTS, sg = threadIdx.x / SLOTS;
+  const int el = threadIdx.x % SLOTS, sg = threadIdx.x / SLOTS;  // slot, sub-sum
   const int64_t nv = d.n / 4, e = (int64_t)((int)blockIdx.x - d.first) * SLOTS + el;
   const v4f* pv = reinterpret_cast<const v4f*>(d.part);
   const int np = d.np;
@@ -1504,24 +1513,23 @@ __global__ __launch_bounds__(TB) void k_sum_parts_multi(PartSets sets) {
     for (; p < np; p += SUB) acc += pv[(int64_t)p * nv + e];
   }
   r[sg * SLOTS + el] = acc;
-  __syncthreads();
-  if (sg == 0 && e < nv) {
-    v4f t = r[el];
-    for (int k = 1; k < SUB; ++k) t += r[k * SLOTS + el];
-    reinterpret_cast<v4f*>(d.out)[e] = t;
+  for (int h = SUB / 2; h >= 1; h /= 2) {
+    __syncthreads();
+    if (sg < h) r[sg * SLOTS + el] += r[(sg + h) * SLOTS + el];
   }
+  if (sg == 0 && e < nv) reinterpret_cast<v4f*>(d.out)[e] = r[el];
 }
 
 void sum_parts(const float* part, int np, int64_t n, float* out, hipStream_t s) {
   const bool v4 = n % 4 == 0 && (uintptr_t)part % 16 == 0 && (uintptr_t)out % 16 == 0;
-  const int64_t nv = v4 ? n / 4 : n;
-  const bool wide = sum_sub(nv) == 16;
-  const unsigned grid = (unsigned)oc::cdiv(nv, TB / (wide ? 16 : 64));
-  if (v4 && wide)
-    oc::launch((k_sum_parts<16, 4>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
-  else if (v4)
-    oc::launch((k_sum_parts<64, 4>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
-  else if (wide)
+  if (v4) {  // the batched kernel with one set: the same bits as in a batch
+    oc::sum_partials_multi(1, &part, &np, &n, &out, s);
+    return;
+  }
+  // unaligned or ragged: one entry per slot
+  const bool wide = oc::cdiv(n, TB / 16) >= 2 * (int64_t)oc::cu_count();
+  const unsigned grid = (unsigned)oc::cdiv(n, TB / (wide ? 16 : 64));
+  if (wide)
     oc::launch((k_sum_parts<16, 1>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
   else
     oc::launch((k_sum_parts<64, 1>), dim3(grid), dim3(TB), 0, s, part, np, n, out);
@@ -2010,7 +2018,7 @@ void sum_partials_multi(int n, const float* const* parts, const int* nparts,
     const bool v4 = counts[i] % 4 == 0 && (uintptr_t)parts[i] % 16 == 0 &&
                     (uintptr_t)outs[i] % 16 == 0;
     if (!v4 || nparts[i] < 1 || counts[i] == 0) {  // not for the batch: alone
-      if (counts[i] > 0) sum_parts(parts[i], nparts[i], counts[i], outs[i], s);
+      if (counts[i] > 0 && nparts[i] >= 1) sum_parts(parts[i], nparts[i], counts[i], outs[i], s);
       continue;
     }
     if (sets.n == MAX_SETS) {  // a full batch goes now
@@ -2019,7 +2027,7 @@ void sum_partials_multi(int n, const float* const* parts, const int* nparts,
       blocks = 0;
     }
     const int64_t nv = counts[i] / 4;
-    const int sub = sum_sub(nv);
+    const int sub = sum_sub(nparts[i]);
     sets.s[sets.n++] = PartSet{parts[i], outs[i], counts[i], nparts[i], sub, blocks};
     blocks += (int)oc::cdiv(nv, TB / sub);
   }
