@@ -828,26 +828,27 @@ __global__ __launch_bounds__(TB) void k_sum_split(const float* __restrict__ part
 }
 
 // k_sum_split followed by the 2x2x2 max-pool (the conv + pool forward with a
-// split reduction): one thread per (depth-(l-1) octant i, channel quad);
-// each of the eight children's sums is formed in k_sum_split's order, ReLU'd
-// when relu, and the first maximum over children 0..7 wins (strict '>').
-// Empty octants get a zero row.  nn a multiple of 4; part, y 16-byte and sw
-// 4-byte aligned.
+// split reduction).  Thread (i, channel quad) has two independent jobs, so
+// that no load waits for another: as depth-(l-1) octant i, it writes a zero
+// row when i is empty (labels[i] == 0); as sibling group i (i < ngroups), it
+// forms the eight children's sums in k_sum_split's order, ReLU'd when relu,
+// and writes their maximum (the first over children 0..7 wins, strict '>')
+// to the row of group i's parent, rows[i], with its switches.  nn a
+// multiple of 4; part, y 16-byte and sw 4-byte aligned.
 __global__ __launch_bounds__(TB) void k_sum_split_pool(const float* __restrict__ part, int splits,
                                                        int64_t n, const int32_t* __restrict__ labels,
-                                                       int64_t npar, int cv, int relu,
-                                                       float* __restrict__ y,
+                                                       const int32_t* __restrict__ rows,
+                                                       int64_t npar, int64_t ngroups, int cv,
+                                                       int relu, float* __restrict__ y,
                                                        uint8_t* __restrict__ sw) {
   const int64_t t = (int64_t)blockIdx.x * TB + threadIdx.x;
   if (t >= npar * cv) return;
   const int64_t i = t / cv;
   const int cc = (int)(t - i * cv);
-  const int32_t L = labels[i];
-  if (L == 0) {
-    reinterpret_cast<v4f*>(y)[t] = v4f{0.f, 0.f, 0.f, 0.f};
-    return;
-  }
-  const int64_t g = L - 1, n4 = n / 4;
+  if (labels[i] == 0) reinterpret_cast<v4f*>(y)[t] = v4f{0.f, 0.f, 0.f, 0.f};
+  if (i >= ngroups) return;
+  const int64_t g = i, n4 = n / 4;
+  const int64_t prow = rows[g];
   const v4f* p = reinterpret_cast<const v4f*>(part) + 8 * g * cv + cc;
   v4f sk[8];  // the eight children's sums, their loads of one split in flight together
 #pragma unroll
@@ -876,7 +877,7 @@ __global__ __launch_bounds__(TB) void k_sum_split_pool(const float* __restrict__
         arg = (arg & ~(0xffu << (8 * j))) | ((uint32_t)k << (8 * j));
       }
   }
-  reinterpret_cast<v4f*>(y)[t] = best;
+  reinterpret_cast<v4f*>(y)[prow * cv + cc] = best;
   reinterpret_cast<uint32_t*>(sw)[g * cv + cc] = arg;
 }
 
@@ -1666,7 +1667,8 @@ void launch_tile2(const oc_octree* t, int l, const TileCfg& c, const float* x, i
       const int64_t npar = t->N[l - 1];
       oc::launch(k_sum_split_pool, dim3((unsigned)oc::cdiv(npar * cv, TB)), dim3(TB), 0, s,
                  (const float*)part, c.splits, t->N[l] * (int64_t)nn,
-                 (const int32_t*)t->labels[l - 1], npar, cv, relu, po->y, po->sw);
+                 (const int32_t*)t->labels[l - 1], (const int32_t*)t->rows[l - 1], npar,
+                 t->M[l - 1], cv, relu, po->y, po->sw);
     } else {
       sum_split(part, c.splits, t->N[l] * (int64_t)nn, out, relu, s);
     }
