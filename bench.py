@@ -561,6 +561,12 @@ class Step(Accounting):
         self.offs = offs
         self.npoints = len(pts)
         self.dtype = torch.float32
+        # the weight gradients' partial sums are added by one launch at the end
+        # of the backward when every conv layer is stride 1; with a strided
+        # layer in the network (stride 4 at depth 6) the deferred pattern made
+        # the step's host launches intermittently several times slower, so
+        # such networks add each layer's sums in its own call
+        self.defer_dw = all(L.stride == 1 for L in wl.layers if L.op == "conv")
         self.weights = {}
         for li, L in enumerate(wl.layers):
             if L.op == "deconv":  # the weight of the convolution it transposes
@@ -839,7 +845,7 @@ class Step(Accounting):
                     dx = None
                 dwf = (lambda: oc.oc_conv_bwd(
                     tree, L.depth, L.ksize, L.stride, xin, w, g, y=yout, relu=relu,
-                    need_dx=False, need_dw=True, defer=pending))
+                    need_dx=False, need_dw=True, defer=pending if self.defer_dw else None))
                 if self.side is None:
                     _, dw = self._run("conv_bwd_weight", li, dwf)
                 else:
