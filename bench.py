@@ -100,6 +100,7 @@ BOUND = {
     "sgd": "hbm",
     "build": "hbm",
     "build_emit": "hbm",
+    "round": "hbm",
 }
 
 
@@ -492,6 +493,8 @@ class Accounting:
                     + 16 * N[d] + sum(108 * M[k - 1] for k in range(1, d + 1)))
         if tag.startswith(("conv", "deconv")):
             return 2 * self._n_conv(L) * L.ksize ** 3 * L.cin * L.cout
+        if tag == "round":  # the layer's input: f32 in, bf16 out
+            return N[L.depth] * L.cin * 6
         if L is None:  # the head and the update: small, counted as their bytes
             return self.head_bytes(tag)
         l, c = L.depth, L.cin
@@ -775,7 +778,7 @@ class Step(Accounting):
             elif L.op == "conv":
                 w = self.weights[li]
                 if x.dtype != w.dtype:  # a bf16 layer after an fp32 output
-                    x = x.to(w.dtype)
+                    x = self._run("round", li, lambda: oc.oc_round_bf16(x))
                 y = self._run("conv_fwd", li, lambda: oc.oc_conv_fwd(
                     tree, L.depth, L.ksize, L.stride, x, w, relu=L.relu))
                 saved.append((li, x, y, None))
@@ -1264,8 +1267,10 @@ def main():
     warm = step.collect()
     nwarm = n_main
     # the build (part at the head of the step, part on its own stream) is not a
-    # convolution or pooling class
-    dominant = max((k for k in warm if not warm[k]["op"].startswith("build")),
+    # convolution or pooling class, and the deferred weight-gradient sums are
+    # counted with their layers' passes
+    dominant = max((k for k in warm if warm[k]["op"] in BOUND
+                    and not warm[k]["op"].startswith("build")),
                    key=lambda k: warm[k]["ms"])
     print(f"[bench] warmup done; dominant kernel: {dominant}", file=sys.stderr, flush=True)
 

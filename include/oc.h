@@ -319,6 +319,13 @@ oc_status oc_conv_dw_partials(const oc_octree* tree, int32_t depth, int32_t ksiz
 oc_status oc_sum_partials(int32_t n, const float* const* parts, const int32_t* nparts,
                           const int64_t* counts, float* const* outs, hipStream_t stream);
 
+/* y[e] = x[e] rounded to bf16 (nearest, ties to even; NaN stays NaN), for
+ * e < n: the operand of an OC_BF16 layer that follows a layer with f32
+ * output (oc_conv_fwd always writes f32).  x dev f32 [n], y dev u16 [n]
+ * (the bf16 bit patterns), not overlapping; 16-byte aligned buffers
+ * take vector accesses.  OC_ERR_ARG for n < 0 or a NULL buffer (n > 0). */
+oc_status oc_round_bf16(int64_t n, const float* x, uint16_t* y, hipStream_t stream);
+
 /* The input gradient of a stride-1 fp32 convolution whose input x is the
  * output of a 2x2x2 max-pooling from depth l+1, carried on through that
  * pooling's backward (Sec. 3.2 "Pooling" and the transposed products of the

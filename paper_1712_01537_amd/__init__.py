@@ -33,6 +33,7 @@ __all__ = [
     "CallProfile",
     "oc_conv_bwd",
     "oc_sum_partials",
+    "oc_round_bf16",
     "oc_conv_bwd_pool",
     "oc_deconv_fwd",
     "oc_deconv_bwd",
@@ -76,7 +77,7 @@ EXPORTS = (
     "oc_bn_workspace", "oc_bn_fwd", "oc_bn_bwd", "oc_fc_fwd", "oc_fc_bwd", "oc_dropout",
     "oc_softmax_ce_workspace", "oc_softmax_ce", "oc_sgd", "oc_conv_pool_fwd",
     "oc_conv_pool_fwd_workspace", "oc_bn_pool_fwd", "oc_conv_bwd_pool_workspace",
-    "oc_conv_bwd_pool", "oc_conv_dw_partials", "oc_sum_partials",
+    "oc_conv_bwd_pool", "oc_conv_dw_partials", "oc_sum_partials", "oc_round_bf16",
 )
 
 
@@ -176,6 +177,7 @@ def load():
         "oc_conv_bwd_pool_workspace": ([p, i32, i32, i32, i32], sz),
         "oc_conv_dw_partials": ([p, i32, i32, i32, C.c_int, i32, i32, p, p, p], C.c_int),
         "oc_sum_partials": ([i32, p, p, p, p, p], C.c_int),
+        "oc_round_bf16": ([i64, p, p, p], C.c_int),
         "oc_conv_bwd_pool": ([p, i32, i32, p, i32, i32, p, p, p, p, p, p, p, sz, i32, p],
                              C.c_int),
         "oc_deconv_fwd": ([p, i32, i32, i32, C.c_int, p, i32, p, i32, p, p, sz, i32, p],
@@ -567,6 +569,15 @@ def oc_sum_partials(defer: list) -> None:
     outs = (C.c_void_p * n)(*[_dev(r[4], "dw") for r in defer])
     _check(L.oc_sum_partials(n, parts, nparts, counts, outs, _stream()))
     defer.clear()
+
+
+def oc_round_bf16(x: torch.Tensor) -> torch.Tensor:
+    """x (f32, any shape) rounded to a bf16 tensor of the same shape: the
+    operand of a bf16 layer after a layer with f32 output."""
+    y = torch.empty(x.shape, dtype=torch.bfloat16, device=x.device)
+    _check(load().oc_round_bf16(x.numel(), _dev(x, "x", torch.float32), _dev(y, "y"),
+                                _stream()))
+    return y
 
 
 def oc_conv_bwd_pool(tree: Octree, depth: int, ksize: int, w: torch.Tensor, dy: torch.Tensor,

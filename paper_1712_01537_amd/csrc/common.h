@@ -72,7 +72,7 @@ inline void launch(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t 
   hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, a, b, 0, args...);
 }
 
-// Launch the kernel that does a convolution pass's arithmetic; it takes the
+// Launch the kernel that does a call's main arithmetic; it takes the
 // pending events of oc_profile_next if any, else a pair of oc_profile_calls.
 template <typename F, typename... Args>
 inline void launch_main(F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {

@@ -470,4 +470,13 @@ oc_status oc_sum_partials(int32_t n, const float* const* parts, const int32_t* n
   return OC_OK;
 }
 
+oc_status oc_round_bf16(int64_t n, const float* x, uint16_t* y, hipStream_t s) {
+  if (n < 0) return oc::fail(OC_ERR_ARG, "oc_round_bf16: n = %lld < 0", (long long)n);
+  if (n == 0) return OC_OK;
+  if (!x || !y) return oc::fail(OC_ERR_ARG, "oc_round_bf16: NULL buffer");
+  oc::round_bf16(x, n, y, s);
+  OC_LAUNCH_CHECK();
+  return OC_OK;
+}
+
 }  // extern "C"

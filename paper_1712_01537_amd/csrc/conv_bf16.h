@@ -37,4 +37,7 @@ void conv_bf16_bwd(const oc_octree* t, int l, int K, const uint16_t* x, int cin,
                    const uint16_t* w, int cout, const float* ym, const float* dy, float* dx,
                    float* dw, void* ws, hipStream_t s);
 
+// y[e] = bf16(x[e]) for e < n, round to nearest even (NaN stays NaN).
+void round_bf16(const float* x, int64_t n, uint16_t* y, hipStream_t s);
+
 }  // namespace oc

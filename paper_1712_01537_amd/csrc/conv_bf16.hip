@@ -211,6 +211,24 @@ __global__ __launch_bounds__(TB) void k_bf_cvt(const float* __restrict__ in,
   }
 }
 
+// y[e] = bf16(x[e]), eight entries per thread: two 16-byte loads and one
+// 16-byte store when x and y are 16-byte aligned (vec), else element
+// accesses.
+__global__ __launch_bounds__(TB) void k_bf_round(const float* __restrict__ x, int64_t n, int vec,
+                                                 uint16_t* __restrict__ y) {
+  const int64_t e = 8 * ((int64_t)blockIdx.x * TB + threadIdx.x);
+  if (e >= n) return;
+  if (vec && e + 8 <= n) {
+    const float4 a = *reinterpret_cast<const float4*>(x + e);
+    const float4 b = *reinterpret_cast<const float4*>(x + e + 4);
+    *reinterpret_cast<uint4*>(y + e) =
+        uint4{f2bf(a.x) | (f2bf(a.y) << 16), f2bf(a.z) | (f2bf(a.w) << 16),
+              f2bf(b.x) | (f2bf(b.y) << 16), f2bf(b.z) | (f2bf(b.w) << 16)};
+  } else {
+    for (int64_t i = e; i < n && i < e + 8; ++i) y[i] = (uint16_t)f2bf(x[i]);
+  }
+}
+
 // The same conversion into the sibling-group layout of the weight gradient:
 // outg[g][c][j] = bf16(masked in[8g + j][c]) (the eight children of a group
 // contiguous per column, so that eight consecutive octants of one column are
@@ -1226,6 +1244,11 @@ void conv_bf16_bwd(const oc_octree* t, int l, int K, const uint16_t* x, int cin,
     const int64_t E = (int64_t)K3 * cin * cout;
     oc::launch(k_bf_sum, dim3(blocks(E, 4 * TB)), dim3(TB), 0, s, part, nr, E, dw);
   }
+}
+
+void round_bf16(const float* x, int64_t n, uint16_t* y, hipStream_t s) {
+  const bool vec = ((uintptr_t)x % 16 == 0) && ((uintptr_t)y % 16 == 0);
+  oc::launch_main(k_bf_round, dim3(blocks(n, 8 * TB)), dim3(TB), s, x, n, (int)vec, y);
 }
 
 }  // namespace oc

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def _declared():
     src = open(os.path.join(ROOT, "include", "oc.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(oc_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(oc_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_header_matches_binding():
@@ -64,6 +64,9 @@ def test_argument_errors_without_device():
     one = (C.c_void_p * 1)(None)
     assert L.oc_sum_partials(1, one, (C.c_int32 * 1)(0), (C.c_int64 * 1)(4), one, None) == 1
     assert L.oc_sum_partials(1, None, (C.c_int32 * 1)(2), (C.c_int64 * 1)(4), one, None) == 1
+    assert L.oc_round_bf16(-1, None, None, None) == 1
+    assert L.oc_round_bf16(0, None, None, None) == 0
+    assert L.oc_round_bf16(4, None, None, None) == 1
     assert L.oc_octree_signal(None) is None
     assert L.oc_status_str(2) == b"point outside the unit cube"
     L.oc_octree_free(None)

@@ -845,3 +845,30 @@ def test_workload_full_size(name):
             g = synth.make_upstream(w_, li, ref.num(l), L.cin)
             np.testing.assert_array_equal(oc.oc_unpool_bwd(tree, l, _cuda(g), sw).cpu().numpy(),
                                           oracle.unpool_bwd(ref.labels(l - 1), g, swr))
+
+
+@pytest.mark.parametrize("n,offset", [(0, 0), (1, 0), (4099, 0), (4099, 1), (1 << 20, 0)])
+def test_round_bf16(n, offset):
+    """oc_round_bf16 against torch's own f32 -> bf16 conversion (round to
+    nearest, ties to even) on the CPU: bit-exact for every non-NaN value,
+    ties, subnormals, signed zeros, values that round up to infinity and the
+    infinities included; NaN stays NaN.  offset 1 takes the element path."""
+    g = torch.Generator().manual_seed(n + offset)
+    v = torch.randn(n + offset, generator=g) * torch.exp2(torch.randint(-140, 128, (n + offset,),
+                                                                          generator=g).float())
+    special = torch.tensor([0.0, -0.0, float("inf"), float("-inf"), float("nan"),
+                            3.4028235e38, -3.4028235e38, 1e-45, -1e-45, 1.0 + 2 ** -8,
+                            1.0 + 3 * 2 ** -8, 1.0 + 2 ** -8 + 2 ** -20])
+    k = min(len(special), n)
+    v[offset:offset + k] = special[:k]
+    ties = torch.randint(0, 1 << 31, (n + offset,), generator=g, dtype=torch.int64)
+    v = torch.where(torch.arange(n + offset) % 5 == 4,  # exact ties of both parities
+                    ((ties & ~0xffff) | 0x8000).to(torch.int32).view(torch.float32), v)
+    x = v.cuda()[offset:]
+    y = _oc().oc_round_bf16(x)
+    assert y.dtype == torch.bfloat16 and y.shape == x.shape
+    got = y.cpu()
+    want = v[offset:].to(torch.bfloat16)
+    nan = torch.isnan(want)
+    assert torch.equal(torch.isnan(got), nan)
+    assert torch.equal(got[~nan].view(torch.int16), want[~nan].view(torch.int16))
