@@ -71,6 +71,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+# Networks whose next build starts after the forward of this layer instead
+# of at the head of the step: wide_d7's first layer is a pair of persistent
+# matrix-core kernels that hold every compute unit, and the build's kernels
+# beside them stretch both; after its forward the build runs beside the
+# stride-2 layer, which leaves the matrix cores mostly idle.
+BUILD_AFTER = {"wide_d7": 0}
+
 PEAK = {  # MI355X published peaks
     "hbm_GBps": 8000.0,
     "fp32_TFLOPs": 157.3,
@@ -603,6 +610,10 @@ class Step(Accounting):
         self.side = None  # stream for the weight gradients (None: all on one stream)
         # stream for the next batch's build (None: on the network's stream)
         self.bstream = None
+        # with a build stream: the layer after whose forward the next build
+        # starts (None: at the head of the step)
+        self.build_after = BUILD_AFTER.get(wl.name)
+        self._job, self._in_step = None, False
         self.cur_ready = None  # event: the current octree's build is done
         self.events = None  # {key: [(start, end, layer), ...]} when recording
         # when a list: every op of the step (not the build) is run with all of
@@ -729,16 +740,21 @@ class Step(Accounting):
             self.cur = self._finish(self._begin())
             self.cur_ready = None
         A = torch.cuda.current_stream()
+        self._job = None
         if B is None:
             job = self._begin()
-        else:
-            B.wait_stream(A)  # the build's stream follows the previous step
-            with torch.cuda.stream(B):
-                job = self._begin()
+        elif self.build_after is None:
+            job = self._start_build()
         tree = self.cur
         if self.cur_ready is not None:
             A.wait_event(self.cur_ready)
-        g = self.network(tree)
+        self._in_step = B is not None and self.build_after is not None
+        try:
+            g = self.network(tree)
+        finally:
+            self._in_step = False
+        if B is not None and self.build_after is not None:
+            job = self._job if self._job is not None else self._start_build()
         if B is None:
             tree.free()
             self.cur = self._finish(job)
@@ -752,6 +768,21 @@ class Step(Accounting):
         self.nstep += 1
         return g
 
+    def _start_build(self):
+        """Queue the first half of the next build on the build stream, after
+        everything queued so far on the network's stream (the previous step,
+        and with build_after that layer's forward)."""
+        torch, B = self.torch, self.bstream
+        B.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(B):
+            return self._begin()
+
+    def _layer_done(self, li):
+        """Called after the forward of layer li: start the next build there
+        when it is build_after's layer."""
+        if self._in_step and li == self.build_after and self._job is None:
+            self._job = self._start_build()
+
     def drain(self):
         """Nothing of a step is left on the host once it returns."""
         return None
@@ -763,6 +794,8 @@ class Step(Accounting):
         sws = {}  # switches of the pooling at each depth, for the unpooling
         done = -1  # a pool layer already run with the conv below it
         for li, L in enumerate(wl.layers):
+            if li > 0:
+                self._layer_done(li - 1)
             if li == done:
                 continue
             if L.op == "conv" and self.pooled(li):
