@@ -143,3 +143,56 @@ def test_bench_step_end_to_end(name):
             np.testing.assert_array_equal(g_out, oracle.unpool_bwd(ref.labels(l - 1), g_in, sw))
     tree.free()
     print(f"[step] {name}: every tensor of the step matches", flush=True)
+
+
+def _same_tensors(got, want, where):
+    if isinstance(got, dict):
+        assert got.keys() == want.keys(), where
+        for k in got:
+            _same_tensors(got[k], want[k], f"{where}/{k}")
+    elif isinstance(got, (tuple, list)):
+        assert len(got) == len(want), where
+        for i, (a, b) in enumerate(zip(got, want)):
+            _same_tensors(a, b, f"{where}/{i}")
+    elif got is None or want is None:
+        assert got is None and want is None, where
+    else:
+        assert torch.equal(got, want), where
+
+
+@pytest.mark.parametrize("name", ["net_d6", "wide_d7"])
+def test_bench_step_build_stream(name):
+    """The timed step with the next batch's build on its own stream, started
+    after the forward of the layer the bench names for this network: after
+    several steps, every tensor of the network (outputs, switches, input and
+    weight gradients) equals bit for bit that of the same network on an
+    octree built alone, and the octree built for the next step equals a
+    direct build at every depth.  The kernels are deterministic, so any
+    difference is an ordering fault between the two streams."""
+    import bench
+    import paper_1712_01537_amd as oc
+
+    wl = synth.WORKLOADS[name]
+    print(f"[step] {name}: two-stream steps", flush=True)
+    step = bench.Step(oc, torch, synth, wl)
+    assert step.build_after == bench.BUILD_AFTER[name]
+    step.bstream = torch.cuda.Stream()
+    for _ in range(3):
+        step()
+    step.record = {}
+    step()
+    torch.cuda.synchronize()
+    got = step.record
+    _, _, offs = synth.make_points(wl)
+    tree = oc.oc_build(step.pts, step.nrm, offs, wl.depth, wl.full_depth)
+    for l in range(wl.depth + 1):
+        assert torch.equal(step.cur.labels(l), tree.labels(l)), l
+    print(f"[step] {name}: one-stream reference", flush=True)
+    step.record = {}
+    step.network(tree)
+    torch.cuda.synchronize()
+    want = step.record
+    # the first layer's input may be the freed octree's signal: left out
+    got["fwd"][0] = got["fwd"][0][1:]
+    want["fwd"][0] = want["fwd"][0][1:]
+    _same_tensors(got, want, name)
